@@ -1,0 +1,219 @@
+#!/usr/bin/env python3
+"""Bench: keys scanned/s and achieved HBM GB/s of the Fathom decode-step scan.
+
+Workload: one Qwen3-8B-shaped layer of one sequence -- 8 KV heads, 4 query
+heads each, head_dim 128, n = 2^20 cached tokens per head, a 48-bit budget,
+k = 2048 -- on synthetic keys with log-normal channel scales and 4 outlier
+channels (seeded; see paper_2609_17652_amd/synth.py).
+
+Before timing, the store is packed (the prefill) into R distinct copies so
+consecutive steps read different buffers and the working set exceeds the
+256 MB last-level cache.  One timed step = depth allocation + fused scan/top-k
++ sparse attention over the winners, on store copy (step mod R).
+`value` is the metric's scan + top-k throughput (keys/s, summed over the 8
+KV heads); the full step's rate is reported beside it.  The roofline object
+covers the scan kernel, timed per launch with HIP events on the stream it
+runs on; algorithmic bytes per launch = sum over heads of n * sum_j t_j / 8.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+import torch
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import paper_2609_17652_amd as F  # noqa: E402
+from paper_2609_17652_amd import synth  # noqa: E402
+
+METRIC = "keys scanned/s and achieved HBM GB/s (scan+top-k), n=1M, 48-bit budget"
+HBM_PEAK_GBPS = 8000.0
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=30)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--budget", type=int, default=48)
+    ap.add_argument("--mode", choices=["waterfill", "r16", "r32"], default="waterfill")
+    ap.add_argument("--copies", type=int, default=8, help="distinct store copies rotated across steps")
+    ap.add_argument("--scan-reps", type=int, default=32, help="extra scan-only launches timed for the roofline")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-units", type=int, default=4, help="units in the oracle's CPU-baseline sample")
+    return ap.parse_args()
+
+
+def cpu_baseline(planes, scales, q, var, n, mode, B, k, units):
+    """The oracle as it stands (depth allocation + fp32 score replica + top-k per
+    head), one thread per sampled unit; ctypes calls release the GIL."""
+    import concurrent.futures as cf
+
+    import oracle
+
+    P = planes[:units].cpu().numpy().view(np.uint64)
+    S = scales[:units].cpu().numpy().view(np.uint16)
+    qh = q[:units].cpu().numpy().astype(np.float32)
+    vh = var[:units].cpu().numpy()
+    nh = n[:units].cpu().numpy()
+
+    def one(u):
+        if mode == F.FATHOM_WATERFILL:
+            d, _, _ = oracle.alloc_waterfill(qh[u], vh[u], B)
+        else:
+            d, _, _ = oracle.alloc_topr(qh[u], B)
+        s = oracle.scores_f32(P[u], S[u], int(nh[u]), qh[u], d)
+        for h in range(qh.shape[1]):
+            oracle.topk(s[h], k)
+        return int(nh[u])
+
+    oracle.build() if not os.path.exists(oracle.lib_path()) else None
+    t0 = time.perf_counter()
+    with cf.ThreadPoolExecutor(max_workers=units) as ex:
+        keys = sum(ex.map(one, range(units)))
+    dt = time.perf_counter() - t0
+    return {"value": keys / dt, "unit": "keys/s", "cores": units, "kind": "oracle",
+            "sample": f"{units} of 8 KV heads at the full n = {int(nh[0])}, all {qh.shape[1]} query heads: "
+                      f"oracle depth allocation + fp32 score replica + top-{k}, one thread per head "
+                      f"({dt:.1f} s wall)"}
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus > 1 or world > 1:
+        print(json.dumps({"error": "this build runs on one GPU only: --gpus must be 1 "
+                                   "(the path shards by KV head or session; see DESIGN.md)"}))
+        sys.exit(2)
+    torch.cuda.set_device(0)
+    dev = "cuda:0"
+    cfg = synth.CONFIGS[2]
+    mode = {"waterfill": F.FATHOM_WATERFILL, "r16": F.FATHOM_UNIFORM_TOPR, "r32": F.FATHOM_UNIFORM_TOPR}[args.mode]
+    B = {"waterfill": args.budget, "r16": 16, "r32": 32}[args.mode]
+    k = cfg.k
+    log(f"[bench] generating config 2 inputs: 8 KV heads x n=2^20, G=4, mode={args.mode} B/r={B}, k={k}")
+    data = synth.device_units(cfg, with_values=True)
+    K, V, q, var, n = data["K"], data["V"], data["q"], data["var"], data["n"]
+    U, N, D = K.shape
+    G = q.shape[1]
+    nb_cap = (N + 63) // 64
+    stream = torch.cuda.current_stream()
+
+    # ---- prefill: pack R store copies (timed for the report, not part of a step)
+    R = max(1, args.copies)
+    planes = [torch.empty((U, D, 4, nb_cap), dtype=torch.int64, device=dev) for _ in range(R)]
+    scales = [torch.empty((U, D, nb_cap), dtype=torch.int16, device=dev) for _ in range(R)]
+    st = F.new_status(dev)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    F.fathom_pack(K, n, nb_cap, planes[0], scales[0], st)
+    e0.record(stream)
+    for r in range(R):
+        F.fathom_pack(K, n, nb_cap, planes[r], scales[r], st)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    pack_ms = e0.elapsed_time(e1) / R
+    pack_bytes = U * N * D * 4 + U * nb_cap * D * (4 * 8 + 2)
+    K16 = K.half()
+    del K, data
+    torch.cuda.empty_cache()
+    log(f"[bench] packed {R} store copies, {pack_ms:.3f} ms each")
+
+    d = torch.empty((U, D), dtype=torch.uint8, device=dev)
+    theta = torch.empty((U,), dtype=torch.float32, device=dev)
+    idx = torch.empty((U, G, k), dtype=torch.int32, device=dev)
+    val = torch.empty((U, G, k), dtype=torch.float32, device=dev)
+    out = torch.empty((U, G, D), dtype=torch.float32, device=dev)
+    ws = torch.empty((F.fathom_scan_topk_workspace_size(U, G, 64 * nb_cap, k),), dtype=torch.uint8, device=dev)
+
+    nev = 4
+    def step(i, evs=None):
+        c = i % R
+        if evs is not None:
+            evs[0].record(stream)
+        F.fathom_alloc_depths(q, var, mode, B, d, theta, st)
+        F.fathom_scan_topk(planes[c], scales[c], n, q, d, k, 0, 0, idx, val, ws, st)
+        if evs is not None:
+            evs[1].record(stream)
+        F.fathom_sparse_attn(q, K16, V, n, idx, 0, 0, None, out, st)
+        if evs is not None:
+            evs[2].record(stream)
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    log(f"[bench] warmup {args.warmup} steps done; timing {args.steps}")
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(nev)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(args.warmup + i, evs[i])
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ms_per_step = (t1 - t0) * 1e3 / args.steps
+    scan_topk_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
+    attn_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
+    status = int(st.item()) & 0xFFFFFFFF
+
+    # ---- scan kernel alone, per launch, for the roofline
+    dn = d.cpu().numpy().astype(np.int64)
+    nh = n.cpu().numpy()
+    alg_bytes = float(sum(int(nh[u]) * int(dn[u].sum()) for u in range(U)) / 8)
+    active = float(np.mean((dn > 0).sum(1)))
+    scores = ws[: U * G * 64 * nb_cap * 4].view(torch.float32).view(U, G, 64 * nb_cap)
+    reps = max(1, args.scan_reps)
+    sev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+    for r in range(reps):
+        sev[r][0].record(stream)
+        F.fathom_scan(planes[r % R], scales[r % R], n, q, d, scores, 64 * nb_cap, st)
+        sev[r][1].record(stream)
+    torch.cuda.synchronize()
+    scan_ms = float(np.mean([a.elapsed_time(b) for a, b in sev]))
+    scan_gbps = alg_bytes / (scan_ms * 1e-3) / 1e9
+
+    keys = float(nh.sum())
+    res = {
+        "metric": METRIC,
+        "value": keys / (scan_topk_ms * 1e-3),
+        "unit": "keys/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic (seeded; log-normal channel scales + 4 outlier channels, fp16 queries)",
+        "config": {"workload": "one Qwen3-8B layer of one sequence: 8 KV heads x n=2^20 tokens, 4 query heads "
+                               f"each, head_dim 128, {args.mode} B/r={B}, k={k}",
+                   "kv_heads": U, "n": N, "G": G, "D": D, "mode": args.mode, "budget_or_r": B, "k": k,
+                   "store_copies": R},
+        "hbm_gbps": alg_bytes / (scan_topk_ms * 1e-3) / 1e9,
+        "hbm_frac": alg_bytes / (scan_topk_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS,
+        "step_keys_per_s": keys / (ms_per_step * 1e-3),
+        "stages_ms": {"alloc+scan_topk": scan_topk_ms, "sparse_attn": attn_ms, "scan_kernel": scan_ms,
+                      "prefill_pack_per_store": pack_ms},
+        "prefill_pack_gbps": pack_bytes / (pack_ms * 1e-3) / 1e9,
+        "active_channels_mean": active,
+        "plane_bits_per_key_mean": float(dn.sum(1).mean()),
+        "device_status": status,
+        "roofline": {"bound": "hbm", "kernel": "scan_kernel", "achieved": scan_gbps, "peak": HBM_PEAK_GBPS,
+                     "unit": "GB/s", "frac": scan_gbps / HBM_PEAK_GBPS, "traffic": None,
+                     "alg_bytes_per_launch": alg_bytes, "avg_launch_ms": scan_ms},
+    }
+    if not args.no_cpu_baseline:
+        log(f"[bench] cpu baseline: oracle on {args.cpu_units} units")
+        res["cpu_baseline"] = cpu_baseline(planes[0], scales[0], q, var, n, mode, B, k, args.cpu_units)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

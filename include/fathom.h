@@ -1,0 +1,200 @@
+/*
+ * fathom.h -- C ABI of libfathom, an MI355X (gfx950) implementation of the
+ * per-query variable-depth key scan of "Fathom: Per-Query Read Depth for Sparse
+ * Decoding over Offloaded KV Caches" (arXiv 2609.17652).
+ *
+ * Terms (Sec. 3.1 cost model, Sec. 3.2 store, Sec. 3.3 read depth):
+ *   unit u   one (sequence, layer, KV head); U units per call, independent.
+ *   n[u]     tokens cached for unit u.  nb_cap >= ceil(max_u n[u] / 64) is the
+ *            common block stride of the store; blocks are 64 tokens.
+ *   D        head dimension (channels).  This version supports D == 128.
+ *   G        query heads per KV head (grouped-query attention), 1..8.  Query
+ *            head h of unit u is row h of that unit's [G][D] query block.
+ *
+ * Conventions shared by every entry point:
+ *   - All pointers to array data are DEVICE pointers unless stated otherwise.
+ *     The caller allocates and owns every buffer; the library never allocates
+ *     device memory and keeps no state between calls.
+ *   - Every call is asynchronous on `stream` (a hipStream_t; NULL = the null
+ *     stream) and never synchronises the host.
+ *   - Argument errors detectable on the host return an error status before
+ *     anything is launched.  FATHOM_ERR_HIP reports a launch/runtime error.
+ *   - Conditions found on the device are OR-ed into *dev_status (a device
+ *     word; may be NULL).  The caller zeroes it and reads it after its own
+ *     synchronisation.  Outputs whose inputs raised a device condition are
+ *     defined as documented per bit below, not checked further.
+ *   - Integer and index results (planes, scales, depths, top-k indices) are
+ *     deterministic; floating-point results are computed in the fixed order
+ *     stated per entry point, so repeated calls are bit-identical.
+ */
+#ifndef FATHOM_H
+#define FATHOM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  FATHOM_OK = 0,
+  FATHOM_ERR_INVALID = -1,     /* null pointer, negative size, bad stride or alignment */
+  FATHOM_ERR_UNSUPPORTED = -2, /* D != 128, G outside 1..8, k above FATHOM_MAX_K, unknown dtype */
+  FATHOM_ERR_RANGE = -3,       /* budget outside [0, 4D] or r outside [0, D] */
+  FATHOM_ERR_HIP = -4,         /* HIP launch or runtime error */
+  FATHOM_ERR_WORKSPACE = -5    /* workspace missing or smaller than the *_workspace_size() */
+} fathom_status;
+
+typedef enum { FATHOM_F32 = 0, FATHOM_F16 = 1 } fathom_dtype;
+
+typedef enum {
+  FATHOM_WATERFILL = 0,   /* Sec. 3.3 Eq. (wf): graded depths under a bit budget B */
+  FATHOM_UNIFORM_TOPR = 1 /* Sec. 2 (SparQ grouped rule): r channels at all 4 planes */
+} fathom_mode;
+
+#define FATHOM_MAX_K 8192 /* largest k accepted by the top-k entry points */
+
+/* device status bits */
+#define FATHOM_DEV_SCALE_OVERFLOW 1u /* a block absmax rounds to fp16 infinity; that block's codes are 8 */
+#define FATHOM_DEV_NONFINITE 2u      /* NaN/Inf in K, q, var, g or scores (NaN keys take code 8; NaN scores rank last) */
+#define FATHOM_DEV_TOPK_FALLBACK 4u  /* the fused filter under-collected and the exact unfiltered path ran */
+#define FATHOM_DEV_TOPK_SHORT 8u     /* fewer than k eligible keys: trailing slots hold index -1, value NaN */
+#define FATHOM_DEV_BAD_N 16u         /* n[u] < 0 or > 64 * nb_cap: that unit is treated as empty */
+
+/*
+ * fathom_pack -- Sec. 3.2, Eq. (2): per-channel 4-bit quantisation with one
+ * fp16 scale per 64-token block, stored channel-major as bit planes.
+ *
+ * For unit u, block b (tokens 64b .. 64b+63 below n[u]) and channel j:
+ *   a16 = fp16_rne(max |K| over the block's valid tokens), s = a16 / 8,
+ *   c   = clip(floor(k / s), -8, 7) + 8 in [0, 16)  (exact real floor; c = 8
+ *         when a16 == 0 or the key is NaN),
+ *   planes[u][j][p][b] bit i = bit (3 - p) of c of token 64b + i  (p = 0 is
+ *         the sign/most significant plane; bit i is token 64b + i),
+ *   scales[u][j][b] = bit pattern of a16.
+ * Pad bits (tokens >= n[u]) and blocks b >= ceil(n[u]/64) are written as 0,
+ * so the first t planes of a channel are its exact t-bit quantiser.
+ *
+ *   K        [U][n][D] keys, element (u, i, c) at K[u*ld_unit + i*ld_tok + c];
+ *            kdt FATHOM_F32 or FATHOM_F16 (converted to fp32 exactly).
+ *            16-byte aligned; ld_tok >= D; ld_tok and ld_unit multiples of 16 bytes.
+ *   n        [U] int64 (device): valid tokens per unit.
+ *   planes   [U][D][4][nb_cap] uint64 (device, written).
+ *   scales   [U][D][nb_cap] uint16 fp16 bits (device, written).
+ * Device status: SCALE_OVERFLOW, NONFINITE, BAD_N.
+ */
+fathom_status fathom_pack(const void* K, fathom_dtype kdt, int64_t ld_tok, int64_t ld_unit,
+                          const int64_t* n, int U, int D, int64_t nb_cap, uint64_t* planes,
+                          uint16_t* scales, uint32_t* dev_status, void* stream);
+
+/*
+ * fathom_alloc_depths -- Sec. 3.3, Eq. (g) and Eq. (wf): the per-query read
+ * depth of every channel, shared by the G query heads of a unit.
+ *
+ * FATHOM_WATERFILL, budget B in [0, 4D] code bits per key:
+ *   g_j = fl32(fl32(sum_h fl32(q_hj^2)) * var_j)   (heads ascending, no FMA)
+ *   candidates c_{j,m} = g_j * 2^-(2m-1), m = 1..4, exact in fp64;
+ *   theta* = the (B+1)-th largest candidate (0 when B >= 4D);
+ *   depths[u][j] = #{m : c_{j,m} > theta*}.
+ *   This is Eq. (wf) with round-half-up, clip to [0, 4], evaluated at any
+ *   water line in (theta*, next candidate]: the smallest water line at which
+ *   sum_j t_j <= B.  theta[u] = fp32(theta*).
+ * FATHOM_UNIFORM_TOPR, r in [0, D]:
+ *   w_j = fl32(sum_h |q_hj|) (heads ascending); the r channels first in
+ *   (w desc, j asc) order get depth 4, all others 0; theta[u] = w of the r-th.
+ *
+ *   q        [U][G][D] queries, qdt FATHOM_F32 or FATHOM_F16, contiguous.
+ *   var      [U][D] fp32 channel variances (calibration statistic), >= 0.
+ *   depths   [U][D] uint8 (written).   theta  [U] fp32 (written) or NULL.
+ * Device status: NONFINITE (non-finite or negative g / w).
+ */
+fathom_status fathom_alloc_depths(const void* q, fathom_dtype qdt, int U, int G, int D,
+                                  const float* var, fathom_mode mode, int budget_or_r,
+                                  uint8_t* depths, float* theta, uint32_t* dev_status,
+                                  void* stream);
+
+/*
+ * fathom_scan -- Sec. 3.2-3.3: approximate scores from the first t_j planes
+ * of every active channel (t_j = depths[u][j] > 0), for all G heads:
+ *   s_h(i) = sum_{j: t_j > 0} q_hj * khat_ij,
+ *   khat_ij = (c^(t) + 1/2 - 2^(t-1)) * a16 * 2^(1-t),  c^(t) = first t bits of c.
+ * Raw q.khat, no 1/sqrt(D) (App. A).  Floating-point order, per (h, i),
+ * channels ascending:  x = fl32(fl32(q_hj * a16) * 2^(1-t_j)),
+ * y = c^(t) + 1/2 - 2^(t-1) (exact),  acc = fmaf(x, y, acc) from acc = +0.
+ *
+ *   planes, scales  the store written by fathom_pack.
+ *   q        [U][G][D] (qdt), depths [U][D] (values above 4 are read as 4).
+ *   scores   [U][G][ld_s] fp32 (written for i < min(n[u], ld_s) only).
+ * Device status: BAD_N.
+ */
+fathom_status fathom_scan(const uint64_t* planes, const uint16_t* scales, const int64_t* n, int U,
+                          int D, int64_t nb_cap, const void* q, fathom_dtype qdt, int G,
+                          const uint8_t* depths, float* scores, int64_t ld_s,
+                          uint32_t* dev_status, void* stream);
+
+/*
+ * fathom_topk -- Sec. 2 (top-k decoding): per query head, the k indices with
+ * the largest scores among the eligible positions [lo, n[u] - tail), ordered
+ * by (score desc, index asc); -0.0 ranks equal to +0.0 and NaN below every
+ * number.  The paper's protocol keeps the first 4 and last 32 tokens
+ * unconditionally (lo = 4, tail = 32) and selects the remaining k - 36.
+ *
+ *   scores   [U][G][ld_s] fp32.     idx [U][G][k] int32 (written).
+ *   val      [U][G][k] fp32 (written: the selected scores) or NULL.
+ *   ws       device workspace of at least fathom_topk_workspace_size(U, G, max_n, k) bytes.
+ * Device status: NONFINITE, TOPK_SHORT, BAD_N.
+ */
+fathom_status fathom_topk(const float* scores, int64_t ld_s, const int64_t* n, int U, int G,
+                          int k, int64_t lo, int64_t tail, int32_t* idx, float* val, void* ws,
+                          size_t ws_bytes, uint32_t* dev_status, void* stream);
+size_t fathom_topk_workspace_size(int U, int G, int64_t max_n, int k);
+
+/*
+ * fathom_scan_topk -- fathom_scan followed by fathom_topk in one call, with
+ * the same outputs bit for bit (same scores, same order rules), without the
+ * score array as an output.  This is the decode-step scan.
+ *   ws       device workspace of at least
+ *            fathom_scan_topk_workspace_size(U, G, max_n, k) bytes.
+ * Device status: NONFINITE, TOPK_SHORT, TOPK_FALLBACK, BAD_N.
+ */
+fathom_status fathom_scan_topk(const uint64_t* planes, const uint16_t* scales, const int64_t* n,
+                               int U, int D, int64_t nb_cap, const void* q, fathom_dtype qdt,
+                               int G, const uint8_t* depths, int k, int64_t lo, int64_t tail,
+                               int32_t* idx, float* val, void* ws, size_t ws_bytes,
+                               uint32_t* dev_status, void* stream);
+size_t fathom_scan_topk_workspace_size(int U, int G, int64_t max_n, int k);
+
+/*
+ * fathom_sparse_attn -- Sec. 2 (top-k decoding) and Sec. 4 (fidelity metric):
+ * exact attention of each query head over its selected set
+ *   S_h = sink [0, ns) U local [l0, n) U {idx[u][h][r] in [ns, l0)},
+ *   ns = min(n_sink, n[u]),  l0 = max(ns, n[u] - n_local);
+ * index entries outside [ns, l0) (including -1) are skipped, so S_h has no
+ * duplicates when idx does not.
+ *   out_h = sum_{i in S_h} softmax_i(sm_scale * q_h . K_i) V_i,  fp32 arithmetic.
+ *
+ *   q        [U][G][D] (qdt).
+ *   Krows, Vrows  [U][n][D] fp16 rows, element (u, i, c) at [u*ld_unit + i*ld_tok + c];
+ *            4-byte aligned; ld_tok >= D; ld_tok, ld_unit even.
+ *   idx      [U][G][k] int32 (k may be 0; idx may then be NULL).
+ *   out      [U][G][D] fp32 (written; 0 for an empty set).
+ * Device status: BAD_N (nb_cap is not known here: only n[u] < 0 is flagged).
+ */
+fathom_status fathom_sparse_attn(const void* q, fathom_dtype qdt, const uint16_t* Krows,
+                                 const uint16_t* Vrows, int64_t ld_tok, int64_t ld_unit,
+                                 const int64_t* n, int U, int G, int D, const int32_t* idx, int k,
+                                 int n_sink, int n_local, float sm_scale, float* out,
+                                 uint32_t* dev_status, void* stream);
+
+/* Human-readable name of a status code (static storage). */
+const char* fathom_status_string(fathom_status s);
+
+/* Library version string, e.g. "fathom-mi355x 0.1 gfx950" (static storage). */
+const char* fathom_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FATHOM_H */

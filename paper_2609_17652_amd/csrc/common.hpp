@@ -1,0 +1,73 @@
+// Internal helpers of libfathom (gfx950, wave64).  Not part of the C ABI.
+#pragma once
+
+#include <hip/hip_fp16.h>
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/fathom.h"
+
+namespace fathom {
+
+constexpr int kWave = 64;
+constexpr int kBlockTokens = 64;  // tokens per quantisation block (Sec. 3.2)
+constexpr int kPlanes = 4;        // 4-bit codes
+constexpr int kD = 128;           // supported head dimension
+
+#define FATHOM_LAUNCH_CHECK()                                   \
+  do {                                                          \
+    hipError_t e_ = hipGetLastError();                          \
+    if (e_ != hipSuccess) return FATHOM_ERR_HIP;                \
+  } while (0)
+
+__device__ __forceinline__ void set_status(uint32_t* st, uint32_t bits) {
+  if (st && bits) atomicOr(st, bits);
+}
+
+// n[u] clamped to [0, cap]; raises BAD_N and returns 0 for out-of-range values.
+__device__ __forceinline__ int64_t unit_tokens(const int64_t* n, int u, int64_t cap, uint32_t* st) {
+  int64_t v = n[u];
+  if (v < 0 || v > cap) {
+    set_status(st, FATHOM_DEV_BAD_N);
+    return 0;
+  }
+  return v;
+}
+
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) v = fmaxf(v, __shfl_xor(v, m, kWave));
+  return v;
+}
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) v = __fadd_rn(v, __shfl_xor(v, m, kWave));
+  return v;
+}
+
+__device__ __forceinline__ int wave_sum_int(int v) {
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m, kWave);
+  return v;
+}
+
+__device__ __forceinline__ float half_bits_to_float(uint16_t h) {
+  return __half2float(__ushort_as_half(h));
+}
+
+__device__ __forceinline__ float load_q(const void* q, fathom_dtype qdt, int64_t i) {
+  if (qdt == FATHOM_F16) return __half2float(reinterpret_cast<const __half*>(q)[i]);
+  return reinterpret_cast<const float*>(q)[i];
+}
+
+// Order-preserving map fp32 -> uint32: larger score -> larger key; -0 == +0;
+// NaN -> 0, below every number (-inf maps to 0x007FFFFF).
+__device__ __forceinline__ uint32_t score_key(float s) {
+  if (s != s) return 0u;
+  if (s == 0.0f) s = 0.0f;
+  uint32_t b = __float_as_uint(s);
+  return (b & 0x80000000u) ? ~b : (b | 0x80000000u);
+}
+
+}  // namespace fathom

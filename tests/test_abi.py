@@ -1,0 +1,135 @@
+"""CPU checks of the C ABI: the library loads, exports every symbol declared in
+include/fathom.h, and rejects bad arguments on the host before any launch.
+No call here reaches a kernel (all of them fail validation or are no-ops)."""
+import ctypes as C
+import os
+import re
+
+import numpy as np
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def fl():
+    import paper_2609_17652_amd as F
+    if not os.path.exists(F.LIB_PATH):
+        from paper_2609_17652_amd import build
+        build.build()
+    return F
+
+
+def declared_symbols():
+    src = open(os.path.join(ROOT, "include", "fathom.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(fathom_[a-z_]+)\s*\(", src)))
+
+
+def test_header_declares_the_five_steps():
+    syms = declared_symbols()
+    for s in ("fathom_pack", "fathom_alloc_depths", "fathom_scan", "fathom_topk", "fathom_sparse_attn"):
+        assert s in syms
+
+
+def test_library_exports_every_declared_symbol(fl):
+    L = fl.lib()
+    for s in declared_symbols():
+        assert hasattr(L, s), s
+    assert sorted(fl.EXPORTED) == declared_symbols()
+
+
+def test_status_strings_and_version(fl):
+    assert fl.fathom_status_string(0) == "FATHOM_OK"
+    assert fl.fathom_status_string(-5) == "FATHOM_ERR_WORKSPACE"
+    assert "gfx950" in fl.fathom_version()
+
+
+def test_constants_match_header(fl):
+    src = open(os.path.join(ROOT, "include", "fathom.h")).read()
+    for name in ("FATHOM_DEV_SCALE_OVERFLOW", "FATHOM_DEV_NONFINITE", "FATHOM_DEV_TOPK_FALLBACK",
+                 "FATHOM_DEV_TOPK_SHORT", "FATHOM_DEV_BAD_N", "FATHOM_MAX_K"):
+        m = re.search(rf"#define {name} (\d+)u?", src)
+        assert m and int(m.group(1)) == getattr(fl, name), name
+    for name, val in (("FATHOM_ERR_INVALID", -1), ("FATHOM_ERR_UNSUPPORTED", -2), ("FATHOM_ERR_RANGE", -3),
+                      ("FATHOM_ERR_HIP", -4), ("FATHOM_ERR_WORKSPACE", -5)):
+        assert re.search(rf"{name} = {val}", src) and getattr(fl, name) == val
+
+
+def test_workspace_sizes(fl):
+    a = fl.fathom_topk_workspace_size(8, 4, 1 << 20, 2048)
+    b = fl.fathom_topk_workspace_size(8, 4, 1 << 20, 4096)
+    assert 0 < a < b
+    s = fl.fathom_scan_topk_workspace_size(8, 4, 1 << 20, 2048)
+    assert s >= 8 * 4 * (1 << 20) * 4 + a
+    assert fl.fathom_topk_workspace_size(0, 4, 10, 10) == 0
+
+
+NULL = None
+S = C.c_void_p(0)
+FAKE = C.c_void_p(0x1000)  # never dereferenced: every call below fails host validation
+
+
+def test_host_validation(fl):
+    L = fl.lib()
+    # pack: D != 128, bad dtype, negative U, null pointers, misaligned K, bad ld_tok
+    assert L.fathom_pack(FAKE, 0, 128, 0, FAKE, 1, 64, 1, FAKE, FAKE, NULL, S) == fl.FATHOM_ERR_UNSUPPORTED
+    assert L.fathom_pack(FAKE, 7, 128, 0, FAKE, 1, 128, 1, FAKE, FAKE, NULL, S) == fl.FATHOM_ERR_UNSUPPORTED
+    assert L.fathom_pack(FAKE, 0, 128, 0, FAKE, -1, 128, 1, FAKE, FAKE, NULL, S) == fl.FATHOM_ERR_INVALID
+    assert L.fathom_pack(NULL, 0, 128, 0, FAKE, 1, 128, 1, FAKE, FAKE, NULL, S) == fl.FATHOM_ERR_INVALID
+    assert L.fathom_pack(C.c_void_p(0x1004), 0, 128, 0, FAKE, 1, 128, 1, FAKE, FAKE, NULL, S) == fl.FATHOM_ERR_INVALID
+    assert L.fathom_pack(FAKE, 0, 100, 0, FAKE, 1, 128, 1, FAKE, FAKE, NULL, S) == fl.FATHOM_ERR_INVALID
+    assert L.fathom_pack(FAKE, 0, 130, 0, FAKE, 1, 128, 1, FAKE, FAKE, NULL, S) == fl.FATHOM_ERR_INVALID
+    assert L.fathom_pack(NULL, 0, 128, 0, NULL, 0, 128, 1, NULL, NULL, NULL, S) == fl.FATHOM_OK  # U = 0: no-op
+    # alloc: budget / r range, G range, mode
+    assert L.fathom_alloc_depths(FAKE, 0, 1, 4, 128, FAKE, 0, 513, FAKE, NULL, NULL, S) == fl.FATHOM_ERR_RANGE
+    assert L.fathom_alloc_depths(FAKE, 0, 1, 4, 128, FAKE, 0, -1, FAKE, NULL, NULL, S) == fl.FATHOM_ERR_RANGE
+    assert L.fathom_alloc_depths(FAKE, 0, 1, 4, 128, FAKE, 1, 129, FAKE, NULL, NULL, S) == fl.FATHOM_ERR_RANGE
+    assert L.fathom_alloc_depths(FAKE, 0, 1, 9, 128, FAKE, 0, 48, FAKE, NULL, NULL, S) == fl.FATHOM_ERR_UNSUPPORTED
+    assert L.fathom_alloc_depths(FAKE, 0, 1, 4, 128, FAKE, 5, 48, FAKE, NULL, NULL, S) == fl.FATHOM_ERR_UNSUPPORTED
+    assert L.fathom_alloc_depths(FAKE, 0, 1, 4, 128, NULL, 0, 48, FAKE, NULL, NULL, S) == fl.FATHOM_ERR_INVALID
+    # scan: G = 0, D = 64, null depths, ld_s < 1
+    assert L.fathom_scan(FAKE, FAKE, FAKE, 1, 128, 4, FAKE, 0, 0, FAKE, FAKE, 256, NULL, S) == fl.FATHOM_ERR_UNSUPPORTED
+    assert L.fathom_scan(FAKE, FAKE, FAKE, 1, 64, 4, FAKE, 0, 4, FAKE, FAKE, 256, NULL, S) == fl.FATHOM_ERR_UNSUPPORTED
+    assert L.fathom_scan(FAKE, FAKE, FAKE, 1, 128, 4, FAKE, 0, 4, NULL, FAKE, 256, NULL, S) == fl.FATHOM_ERR_INVALID
+    assert L.fathom_scan(FAKE, FAKE, FAKE, 1, 128, 4, FAKE, 0, 4, FAKE, FAKE, 0, NULL, S) == fl.FATHOM_ERR_INVALID
+    # top-k: k too large, k < 1, small workspace, misaligned workspace
+    ws = fl.fathom_topk_workspace_size(1, 4, 4096, 64)
+    assert L.fathom_topk(FAKE, 4096, FAKE, 1, 4, 9000, 0, 0, FAKE, NULL, FAKE, ws, NULL, S) == fl.FATHOM_ERR_UNSUPPORTED
+    assert L.fathom_topk(FAKE, 4096, FAKE, 1, 4, 0, 0, 0, FAKE, NULL, FAKE, ws, NULL, S) == fl.FATHOM_ERR_INVALID
+    assert L.fathom_topk(FAKE, 4096, FAKE, 1, 4, 64, 0, 0, FAKE, NULL, FAKE, ws - 1, NULL, S) == fl.FATHOM_ERR_WORKSPACE
+    assert L.fathom_topk(FAKE, 4096, FAKE, 1, 4, 64, -1, 0, FAKE, NULL, FAKE, ws, NULL, S) == fl.FATHOM_ERR_INVALID
+    assert L.fathom_topk(FAKE, 4096, FAKE, 1, 4, 64, 0, 0, FAKE, NULL, C.c_void_p(0x1010), ws, NULL, S) == \
+        fl.FATHOM_ERR_INVALID
+    ws2 = fl.fathom_scan_topk_workspace_size(1, 4, 4096, 64)
+    assert L.fathom_scan_topk(FAKE, FAKE, FAKE, 1, 128, 64, FAKE, 1, 4, FAKE, 64, 0, 0, FAKE, NULL, FAKE, ws2 - 1,
+                              NULL, S) == fl.FATHOM_ERR_WORKSPACE
+    # sparse attention: sink + local too large, odd ld_tok, null out
+    assert L.fathom_sparse_attn(FAKE, 0, FAKE, FAKE, 128, 0, FAKE, 1, 4, 128, FAKE, 8, 1000, 100, C.c_float(1.0),
+                                FAKE, NULL, S) == fl.FATHOM_ERR_UNSUPPORTED
+    assert L.fathom_sparse_attn(FAKE, 0, FAKE, FAKE, 129, 0, FAKE, 1, 4, 128, FAKE, 8, 4, 32, C.c_float(1.0),
+                                FAKE, NULL, S) == fl.FATHOM_ERR_INVALID
+    assert L.fathom_sparse_attn(FAKE, 0, FAKE, FAKE, 128, 0, FAKE, 1, 4, 128, FAKE, 8, 4, 32, C.c_float(1.0),
+                                NULL, NULL, S) == fl.FATHOM_ERR_INVALID
+
+
+def test_synth_is_deterministic_and_shaped():
+    from paper_2609_17652_amd import synth
+    cfg = synth.CONFIGS[0]
+    a = synth.host_units(cfg)
+    b = synth.host_units(cfg)
+    assert np.array_equal(a.K, b.K) and np.array_equal(a.q, b.q) and np.array_equal(a.var, b.var)
+    assert a.K.shape == (1, 4096, 128) and a.q.shape == (1, 1, 128) and a.q.dtype == np.float32
+    c1 = synth.CONFIGS[1]
+    h = synth.host_units(c1, units=[0, 1], n_override=256)
+    assert h.q.dtype == np.float16 and h.q.shape == (2, 4, 128)
+    assert not np.array_equal(h.K[0], h.K[1])
+    n3 = synth.unit_lengths(synth.CONFIGS[3])
+    assert n3.shape == (128,) and n3.min() >= 65536 and n3.max() <= 524288
+    assert (n3.reshape(16, 8) == n3.reshape(16, 8)[:, :1]).all()  # one length per session
+    # 4 outlier channels at 8x
+    rng = synth.unit_rng(0, 0, 0, 0)
+    z = np.exp(rng.standard_normal(128))
+    rng = synth.unit_rng(0, 0, 0, 0)
+    s = synth.channel_sigma(rng)
+    assert np.isclose(s / z, 8.0).sum() == 4 and np.isclose(s / z, 1.0).sum() == 124

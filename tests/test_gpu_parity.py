@@ -1,0 +1,448 @@
+"""GPU parity: every step of the HIP path against the CPU oracle, element by
+element, on the same seeded inputs (all calls go through the C ABI via the
+ctypes binding).
+
+Bars: planes, scales, depths, top-k indices bit-exact; scores bit-exact to the
+oracle's fp32 replica and within 1e-5 * sum_j |q_hj khat_ij| of its fp64
+reference; attention within 1e-5 * (sum_i p_i |V_i|) / (sum_i p_i) of the fp64
+oracle (p = softmax weights).
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2609_17652_amd as F
+from paper_2609_17652_amd import synth
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda"
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    F.lib()
+
+
+def u64(t):
+    return t.cpu().numpy().view(np.uint64)
+
+
+def u16(t):
+    return t.cpu().numpy().view(np.uint16)
+
+
+def status(st):
+    torch.cuda.synchronize()
+    return int(st.item()) & 0xFFFFFFFF
+
+
+def special_keys(rng, n, dtype=np.float32):
+    """Keys with log-normal channel scales plus edge cases: an all-zero channel,
+    -0.0, exact cell boundaries, a block whose absmax is exactly 1."""
+    sig = np.exp(rng.standard_normal(128))
+    K = (rng.standard_normal((n, 128)) * sig).astype(np.float32)
+    K[:, 5] = 0.0
+    K[: min(n, 7), 9] = -0.0
+    if n >= 16:
+        K[:16, 11] = (np.arange(-8, 8) * 0.125).astype(np.float32)  # exact multiples of s = 1/8
+        K[0, 11] = -1.0
+    return K.astype(dtype)
+
+
+# ---------------------------------------------------------------------- pack
+@pytest.mark.parametrize("kdt", [np.float32, np.float16])
+def test_pack_ragged_units(kdt):
+    rng = np.random.default_rng(11)
+    ns = [1, 63, 64, 65, 1000, 4096, 0]
+    nmax = max(ns)
+    nb_cap = (nmax + 63) // 64 + 1
+    K = np.zeros((len(ns), nmax, 128), kdt)
+    for u, n in enumerate(ns):
+        K[u, :n] = special_keys(rng, n, kdt)
+    Kt = torch.from_numpy(K).to(DEV)
+    nt = torch.tensor(ns, dtype=torch.int64, device=DEV)
+    st = F.new_status()
+    planes, scales = F.fathom_pack(Kt, nt, nb_cap=nb_cap, dev_status=st)
+    assert status(st) == 0
+    P, Sc = u64(planes), u16(scales)
+    for u, n in enumerate(ns):
+        op, os_, ost = oracle.pack(K[u, :n].astype(np.float32), nb_cap=nb_cap)
+        assert ost == 0
+        assert np.array_equal(P[u], op), f"planes unit {u} n={n}"
+        assert np.array_equal(Sc[u], os_), f"scales unit {u} n={n}"
+
+
+def test_pack_flags_overflow_nan():
+    K = np.random.default_rng(3).standard_normal((2, 200, 128)).astype(np.float32)
+    K[0, 70, 3] = 70000.0  # block 1 of channel 3 overflows fp16
+    K[1, 5, 8] = np.nan
+    K[1, 130, 9] = np.inf
+    nt = torch.tensor([200, 200], dtype=torch.int64, device=DEV)
+    st = F.new_status()
+    planes, scales = F.fathom_pack(torch.from_numpy(K).to(DEV), nt, dev_status=st)
+    s = status(st)
+    assert s & F.FATHOM_DEV_SCALE_OVERFLOW and s & F.FATHOM_DEV_NONFINITE
+    for u in range(2):
+        op, os_, ost = oracle.pack(K[u], nb_cap=planes.shape[-1])
+        assert np.array_equal(u64(planes)[u], op) and np.array_equal(u16(scales)[u], os_)
+
+
+def test_pack_bad_n_flag():
+    K = torch.zeros((2, 128, 128), dtype=torch.float32, device=DEV)
+    nt = torch.tensor([128, 1000], dtype=torch.int64, device=DEV)
+    st = F.new_status()
+    planes, scales = F.fathom_pack(K, nt, nb_cap=2, dev_status=st)
+    assert status(st) & F.FATHOM_DEV_BAD_N
+    assert (u64(planes)[1] == 0).all()
+
+
+# ---------------------------------------------------------------------- depths
+@pytest.mark.parametrize("G,qdt", [(1, np.float32), (4, np.float16), (4, np.float32), (8, np.float16)])
+def test_alloc_waterfill(G, qdt):
+    rng = np.random.default_rng(G)
+    U = 12
+    sig = np.exp(rng.standard_normal((U, 128)))
+    sig[:, :4] *= 8
+    var = (sig ** 2).astype(np.float32)
+    q = rng.standard_normal((U, G, 128)).astype(qdt)
+    q[0, :, 3] = 0
+    var[1, 10] = 0.0
+    q[2] = 1.0  # ties in g across channels with equal variance
+    var[2, :] = 2.0
+    qt, vt = torch.from_numpy(q).to(DEV), torch.from_numpy(var).to(DEV)
+    for B in [0, 1, 7, 40, 48, 80, 200, 511, 512]:
+        st = F.new_status()
+        d, th = F.fathom_alloc_depths(qt, vt, F.FATHOM_WATERFILL, B, dev_status=st)
+        assert status(st) == 0
+        d, th = d.cpu().numpy(), th.cpu().numpy()
+        for u in range(U):
+            od, oth, ost = oracle.alloc_waterfill(q[u].astype(np.float32), var[u], B)
+            assert np.array_equal(d[u], od), (B, u)
+            assert th[u] == oth, (B, u)
+
+
+@pytest.mark.parametrize("G", [1, 4])
+def test_alloc_topr(G):
+    rng = np.random.default_rng(5)
+    U = 6
+    q = rng.integers(-3, 4, (U, G, 128)).astype(np.float16)  # heavy ties in sum |q|
+    qt = torch.from_numpy(q).to(DEV)
+    for r in [0, 1, 16, 32, 127, 128]:
+        d, th = F.fathom_alloc_depths(qt, None, F.FATHOM_UNIFORM_TOPR, r)
+        d, th = d.cpu().numpy(), th.cpu().numpy()
+        for u in range(U):
+            od, oth, _ = oracle.alloc_topr(q[u].astype(np.float32), r)
+            assert np.array_equal(d[u], od) and th[u] == oth, (r, u)
+
+
+# ---------------------------------------------------------------------- scan
+def _store(ns, seed, kdt=np.float32):
+    rng = np.random.default_rng(seed)
+    nmax = max(ns)
+    nb_cap = (nmax + 63) // 64
+    K = np.zeros((len(ns), nmax, 128), np.float32)
+    for u, n in enumerate(ns):
+        K[u, :n] = special_keys(rng, n)
+    nt = torch.tensor(ns, dtype=torch.int64, device=DEV)
+    planes, scales = F.fathom_pack(torch.from_numpy(K).to(DEV), nt, nb_cap=nb_cap)
+    return K, nt, planes, scales
+
+
+def _depth_modes(rng, U, G, q):
+    var = np.exp(2 * rng.standard_normal((U, 128))).astype(np.float32)
+    modes = {}
+    qt, vt = torch.from_numpy(q).to(DEV), torch.from_numpy(var).to(DEV)
+    modes["wf48"] = F.fathom_alloc_depths(qt, vt, F.FATHOM_WATERFILL, 48)[0]
+    modes["wf80"] = F.fathom_alloc_depths(qt, vt, F.FATHOM_WATERFILL, 80)[0]
+    modes["r16"] = F.fathom_alloc_depths(qt, vt, F.FATHOM_UNIFORM_TOPR, 16)[0]
+    modes["all4"] = torch.full((U, 128), 4, dtype=torch.uint8, device=DEV)
+    modes["all1"] = torch.full((U, 128), 1, dtype=torch.uint8, device=DEV)
+    modes["none"] = torch.zeros((U, 128), dtype=torch.uint8, device=DEV)
+    mixed = rng.integers(0, 5, (U, 128)).astype(np.uint8)
+    modes["mixed"] = torch.from_numpy(mixed).to(DEV)
+    return modes
+
+
+@pytest.mark.parametrize("G,qdt", [(1, np.float32), (4, np.float16), (3, np.float32)])
+def test_scan_bit_exact(G, qdt):
+    ns = [4096, 1000, 65, 1]
+    K, nt, planes, scales = _store(ns, 21)
+    rng = np.random.default_rng(22)
+    q = rng.standard_normal((len(ns), G, 128)).astype(qdt)
+    P, Sc = u64(planes), u16(scales)
+    for name, d in _depth_modes(rng, len(ns), G, q).items():
+        s = F.fathom_scan(planes, scales, nt, torch.from_numpy(q).to(DEV), d).cpu().numpy()
+        dn = d.cpu().numpy()
+        for u, n in enumerate(ns):
+            q32 = q[u].astype(np.float32)
+            ref32 = oracle.scores_f32(P[u], Sc[u], n, q32, dn[u])
+            assert np.array_equal(s[u, :, :n].view(np.uint32), ref32.view(np.uint32)), (name, u)
+            ref64, ab = oracle.scores_f64(P[u], Sc[u], n, q32, dn[u], with_abs=True)
+            assert (np.abs(s[u, :, :n] - ref64) <= 1e-5 * ab + 1e-30).all(), (name, u)
+
+
+# ---------------------------------------------------------------------- top-k
+def _rows(rng, U, G, ld, kind):
+    if kind == "ties":
+        s = rng.integers(-20, 20, (U, G, ld)).astype(np.float32)
+        s[rng.random(s.shape) < 0.1] = -0.0
+        s[rng.random(s.shape) < 0.05] = 0.0
+    elif kind == "nan":
+        s = rng.standard_normal((U, G, ld)).astype(np.float32)
+        s[rng.random(s.shape) < 0.01] = np.nan
+        s[rng.random(s.shape) < 0.01] = -np.inf
+        s[rng.random(s.shape) < 0.01] = np.inf
+    else:
+        s = rng.standard_normal((U, G, ld)).astype(np.float32)
+    return s
+
+
+@pytest.mark.parametrize("kind", ["gauss", "ties", "nan"])
+@pytest.mark.parametrize("k,lo,tail", [(1, 0, 0), (64, 0, 0), (1000, 4, 32), (2048, 0, 0)])
+def test_topk_bit_exact(kind, k, lo, tail):
+    rng = np.random.default_rng(k + lo)
+    ns = [70000, 5000, 1000, 3, 0]
+    U, G, ld = len(ns), 4, 70000
+    s = _rows(rng, U, G, ld, kind)
+    st = F.new_status()
+    idx, val = F.fathom_topk(torch.from_numpy(s).to(DEV), torch.tensor(ns, dtype=torch.int64, device=DEV), k, lo,
+                             tail, dev_status=st)
+    flags = status(st)
+    idx, val = idx.cpu().numpy(), val.cpu().numpy()
+    want_flags = 0
+    for u, n in enumerate(ns):
+        for h in range(G):
+            oi, ov, ost = oracle.topk(s[u, h, :n], k, lo, tail)
+            want_flags |= ost
+            assert np.array_equal(idx[u, h], oi), (u, h)
+            assert np.array_equal(np.isnan(val[u, h]), np.isnan(ov))
+            m = ~np.isnan(ov)
+            assert np.array_equal(val[u, h][m], ov[m])
+    assert flags == want_flags
+
+
+def test_scan_topk_equals_oracle_and_unfused():
+    ns = [20000, 4096, 300]
+    K, nt, planes, scales = _store(ns, 31)
+    rng = np.random.default_rng(32)
+    G = 4
+    q = rng.standard_normal((len(ns), G, 128)).astype(np.float16)
+    qt = torch.from_numpy(q).to(DEV)
+    var = torch.from_numpy(np.exp(rng.standard_normal((len(ns), 128))).astype(np.float32)).to(DEV)
+    d, _ = F.fathom_alloc_depths(qt, var, F.FATHOM_WATERFILL, 48)
+    for k, lo, tail in [(256, 0, 0), (100, 4, 32)]:
+        st = F.new_status()
+        idx, val = F.fathom_scan_topk(planes, scales, nt, qt, d, k, lo, tail, dev_status=st)
+        s = F.fathom_scan(planes, scales, nt, qt, d)
+        idx2, val2 = F.fathom_topk(s, nt, k, lo, tail)
+        assert torch.equal(idx, idx2) and torch.equal(val.view(torch.int32), val2.view(torch.int32))
+        P, Sc, dn = u64(planes), u16(scales), d.cpu().numpy()
+        idx = idx.cpu().numpy()
+        for u, n in enumerate(ns):
+            ref = oracle.scores_f32(P[u], Sc[u], n, q[u].astype(np.float32), dn[u])
+            for h in range(G):
+                oi, _, _ = oracle.topk(ref[h], k, lo, tail)
+                assert np.array_equal(idx[u, h], oi), (k, u, h)
+
+
+# ---------------------------------------------------------------------- attention
+def _attn_tol(q, K16, V16, idx, ns_, nl, sm):
+    """1e-5 * (sum p |V|) / (sum p) per (head, channel), weights from fp64 logits."""
+    n = K16.shape[0]
+    ns = min(ns_, n)
+    l0 = max(ns, n - nl)
+    tol = np.zeros((q.shape[0], 128))
+    for h in range(q.shape[0]):
+        rows = list(range(ns)) + list(range(l0, n)) + [i for i in idx[h] if ns <= i < l0]
+        if not rows:
+            continue
+        z = (K16[rows].astype(np.float64) @ q[h].astype(np.float64)) * float(sm)
+        p = np.exp(z - z.max())
+        tol[h] = 1e-5 * (p @ np.abs(V16[rows].astype(np.float64))) / p.sum()
+    return tol + 1e-7
+
+
+@pytest.mark.parametrize("qdt", [np.float32, np.float16])
+def test_sparse_attn(qdt):
+    rng = np.random.default_rng(41)
+    ns = [5000, 600, 30, 0]
+    U, G, k = len(ns), 4, 512
+    nmax = max(ns)
+    K16 = rng.standard_normal((U, nmax, 128)).astype(np.float16)
+    V16 = rng.standard_normal((U, nmax, 128)).astype(np.float16)
+    q = (2 * rng.standard_normal((U, G, 128))).astype(qdt)
+    idx = np.full((U, G, k), -1, np.int32)
+    for u, n in enumerate(ns):
+        for h in range(G):
+            c = rng.permutation(max(n, 1))[: min(k, n)]
+            idx[u, h, : len(c)] = c
+    sm = np.float32(1 / np.sqrt(128))
+    for (nsk, nl) in [(4, 32), (0, 0)]:
+        out = F.fathom_sparse_attn(torch.from_numpy(q).to(DEV), torch.from_numpy(K16).to(DEV),
+                                   torch.from_numpy(V16).to(DEV), torch.tensor(ns, dtype=torch.int64, device=DEV),
+                                   torch.from_numpy(idx).to(DEV), nsk, nl, float(sm)).cpu().numpy()
+        for u, n in enumerate(ns):
+            ref = oracle.sparse_attn(q[u].astype(np.float32), K16[u, :n], V16[u, :n], idx[u], nsk, nl, sm)
+            tol = _attn_tol(q[u].astype(np.float32), K16[u, :n], V16[u, :n], idx[u], nsk, nl, sm)
+            assert (np.abs(out[u] - ref) <= tol).all(), (u, nsk, float(np.abs(out[u] - ref).max()))
+
+
+# ---------------------------------------------------------------------- configurations
+def _pipeline(K, nt, q, var, B, k, lo=0, tail=0, mode=F.FATHOM_WATERFILL):
+    st = F.new_status()
+    planes, scales = F.fathom_pack(K, nt, dev_status=st)
+    d, th = F.fathom_alloc_depths(q, var, mode, B, dev_status=st)
+    idx, val = F.fathom_scan_topk(planes, scales, nt, q, d, k, lo, tail, dev_status=st)
+    return planes, scales, d, th, idx, val, st
+
+
+def test_config0_end_to_end():
+    """Single KV head, n = 4096, fp32 query, B = 48, k = 64: every stage bit-exact."""
+    cfg = synth.CONFIGS[0]
+    h = synth.host_units(cfg)
+    K, q, var = torch.from_numpy(h.K).to(DEV), torch.from_numpy(h.q).to(DEV), torch.from_numpy(h.var).to(DEV)
+    nt = torch.from_numpy(h.n).to(DEV)
+    planes, scales, d, th, idx, val, st = _pipeline(K, nt, q, var, 48, cfg.k)
+    V = torch.from_numpy(h.V).to(DEV)
+    out = F.fathom_sparse_attn(q, K.half(), V, nt, idx)
+    assert status(st) == 0
+    op, os_, _ = oracle.pack(h.K[0])
+    assert np.array_equal(u64(planes)[0], op) and np.array_equal(u16(scales)[0], os_)
+    od, oth, _ = oracle.alloc_waterfill(h.q[0], h.var[0], 48)
+    assert np.array_equal(d.cpu().numpy()[0], od) and th.item() == oth
+    assert od.sum() <= 48
+    ref = oracle.scores_f32(op, os_, 4096, h.q[0], od)
+    oi, ov, _ = oracle.topk(ref[0], cfg.k)
+    assert np.array_equal(idx.cpu().numpy()[0, 0], oi) and np.array_equal(val.cpu().numpy()[0, 0], ov)
+    K16 = h.K[0].astype(np.float16)
+    oo = oracle.sparse_attn(h.q[0], K16, h.V[0], oi[None], 0, 0, 1 / np.sqrt(128))
+    tol = _attn_tol(h.q[0], K16, h.V[0], oi[None], 0, 0, np.float32(1 / np.sqrt(128)))
+    assert (np.abs(out.cpu().numpy()[0] - oo) <= tol).all()
+
+
+@pytest.mark.parametrize("cfg_id", [1, 2])
+def test_config_full_size_sampled(cfg_id):
+    """Configs 1 (n = 131072) and 2 (n = 2^20): all 8 KV heads in one launch, as
+    timed by the bench; oracle on sampled units / blocks, every budget and mode."""
+    cfg = synth.CONFIGS[cfg_id]
+    data = synth.device_units(cfg, with_values=True)
+    K, q, var, nt = data["K"], data["q"], data["var"], data["n"]
+    n = int(data["n_host"][0])
+    planes, scales = F.fathom_pack(K, nt)
+    P_u = [0, 7]
+    for u in P_u:  # sampled block ranges of the store
+        for b0 in [0, n // 64 // 2, n // 64 - 3]:
+            kk = K[u, 64 * b0: 64 * (b0 + 3)].cpu().numpy()
+            op, os_, _ = oracle.pack(kk)
+            assert np.array_equal(u64(planes[u, :, :, b0:b0 + 3]), op), (u, b0)
+            assert np.array_equal(u16(scales[u, :, b0:b0 + 3]), os_), (u, b0)
+    qh, vh = q.cpu().numpy().astype(np.float32), var.cpu().numpy()
+    modes = [(F.FATHOM_WATERFILL, B) for B in cfg.budgets] + [(F.FATHOM_UNIFORM_TOPR, r) for r in cfg.uniform_r]
+    su = 3
+    Psu, Ssu = u64(planes[su]), u16(scales[su])
+    for mode, B in modes:
+        st = F.new_status()
+        d, th = F.fathom_alloc_depths(q, var, mode, B, dev_status=st)
+        idx, val = F.fathom_scan_topk(planes, scales, nt, q, d, cfg.k, dev_status=st)
+        assert status(st) == 0
+        dn = d.cpu().numpy()
+        for u in range(8):
+            od = (oracle.alloc_waterfill(qh[u], vh[u], B) if mode == F.FATHOM_WATERFILL else
+                  oracle.alloc_topr(qh[u], B))[0]
+            assert np.array_equal(dn[u], od), (mode, B, u)
+        ref = oracle.scores_f32(Psu, Ssu, n, qh[su], dn[su])
+        ix = idx[su].cpu().numpy()
+        for h in range(cfg.G):
+            oi, _, _ = oracle.topk(ref[h], cfg.k)
+            assert np.array_equal(ix[h], oi), (mode, B, h)
+        # attention over the selected rows of the sampled unit
+        K16 = K[su].half()
+        out = F.fathom_sparse_attn(q[su:su + 1], K16[None], data["V"][su:su + 1], nt[su:su + 1], idx[su:su + 1])
+        rows = np.unique(ix.ravel())
+        Kh = np.zeros((n, 128), np.float16)
+        Vh = np.zeros((n, 128), np.float16)
+        Kh[rows] = K16[torch.from_numpy(rows).to(DEV)].cpu().numpy()
+        Vh[rows] = data["V"][su][torch.from_numpy(rows).to(DEV)].cpu().numpy()
+        oo = oracle.sparse_attn(qh[su], Kh, Vh, ix, 0, 0, 1 / np.sqrt(128))
+        tol = _attn_tol(qh[su], Kh, Vh, ix, 0, 0, np.float32(1 / np.sqrt(128)))
+        assert (np.abs(out.cpu().numpy()[0] - oo) <= tol).all()
+        if cfg_id == 2:
+            break  # the full-size run checks one budget end to end; depths for all modes above
+    del data, K, planes, scales
+    torch.cuda.empty_cache()
+
+
+def test_config3_ragged_sessions():
+    """16 sessions with ragged n in [65536, 524288], 8 KV heads each, B = 40, k = 1024,
+    one batched launch over all 128 units; oracle on the shortest and longest units."""
+    cfg = synth.CONFIGS[3]
+    data = synth.device_units(cfg, with_values=False)
+    K, q, var, nt, nh = data["K"], data["q"], data["var"], data["n"], data["n_host"]
+    st = F.new_status()
+    planes, scales = F.fathom_pack(K, nt, dev_status=st)
+    d, _ = F.fathom_alloc_depths(q, var, F.FATHOM_WATERFILL, 40, dev_status=st)
+    idx, _ = F.fathom_scan_topk(planes, scales, nt, q, d, cfg.k, dev_status=st)
+    assert status(st) == 0
+    for u in [int(np.argmin(nh)), int(np.argmax(nh))]:
+        n = int(nh[u])
+        op, os_, _ = oracle.pack(K[u, :n].cpu().numpy(), nb_cap=planes.shape[-1])
+        assert np.array_equal(u64(planes[u]), op) and np.array_equal(u16(scales[u]), os_)
+        qu = q[u].cpu().numpy().astype(np.float32)
+        od, _, _ = oracle.alloc_waterfill(qu, var[u].cpu().numpy(), 40)
+        assert np.array_equal(d[u].cpu().numpy(), od)
+        ref = oracle.scores_f32(op, os_, n, qu, od)
+        for h in range(cfg.G):
+            oi, _, _ = oracle.topk(ref[h], cfg.k)
+            assert np.array_equal(idx[u, h].cpu().numpy(), oi), (u, h)
+    del data, K, planes, scales
+    torch.cuda.empty_cache()
+
+
+def test_config4_layer_protocol():
+    """One layer of the full decode step: 4 sessions x 8 KV heads at n = 2^20, B = 48,
+    sink 4 + local 32 + top-(2048 - 36); oracle on one sampled unit."""
+    cfg = synth.CONFIGS[4]
+    units = [s * cfg.layers * cfg.kv_heads + h for s in range(cfg.sessions) for h in range(cfg.kv_heads)]
+    data = synth.device_units(cfg, units=units, with_values=True)
+    K, q, var, nt = data["K"], data["q"], data["var"], data["n"]
+    n = int(data["n_host"][0])
+    ktop = cfg.k - cfg.n_sink - cfg.n_local
+    planes, scales, d, _, idx, _, st = _pipeline(K, nt, q, var, 48, ktop, cfg.n_sink, cfg.n_local)
+    out = F.fathom_sparse_attn(q, K.half(), data["V"], nt, idx, cfg.n_sink, cfg.n_local)
+    assert status(st) == 0
+    su = 13
+    qu = q[su].cpu().numpy().astype(np.float32)
+    od, _, _ = oracle.alloc_waterfill(qu, var[su].cpu().numpy(), 48)
+    assert np.array_equal(d[su].cpu().numpy(), od)
+    ref = oracle.scores_f32(u64(planes[su]), u16(scales[su]), n, qu, od)
+    ix = idx[su].cpu().numpy()
+    for h in range(cfg.G):
+        oi, _, _ = oracle.topk(ref[h], ktop, cfg.n_sink, cfg.n_local)
+        assert np.array_equal(ix[h], oi), h
+    rows = np.unique(np.concatenate([ix.ravel(), np.arange(4), np.arange(n - 32, n)]))
+    Kh = np.zeros((n, 128), np.float16)
+    Vh = np.zeros((n, 128), np.float16)
+    rt = torch.from_numpy(rows).to(DEV)
+    Kh[rows] = K[su][rt].half().cpu().numpy()
+    Vh[rows] = data["V"][su][rt].cpu().numpy()
+    oo = oracle.sparse_attn(qu, Kh, Vh, ix, cfg.n_sink, cfg.n_local, 1 / np.sqrt(128))
+    tol = _attn_tol(qu, Kh, Vh, ix, cfg.n_sink, cfg.n_local, np.float32(1 / np.sqrt(128)))
+    assert (np.abs(out[su].cpu().numpy() - oo) <= tol).all()
+    del data, K, planes, scales
+    torch.cuda.empty_cache()
+
+
+def test_repeatable_bit_identical():
+    ns = [50000, 7000]
+    K, nt, planes, scales = _store(ns, 51)
+    rng = np.random.default_rng(52)
+    q = torch.from_numpy(rng.standard_normal((2, 4, 128)).astype(np.float16)).to(DEV)
+    var = torch.from_numpy(np.exp(rng.standard_normal((2, 128))).astype(np.float32)).to(DEV)
+    d, _ = F.fathom_alloc_depths(q, var, F.FATHOM_WATERFILL, 48)
+    a = F.fathom_scan_topk(planes, scales, nt, q, d, 512)
+    b = F.fathom_scan_topk(planes, scales, nt, q, d, 512)
+    assert torch.equal(a[0], b[0]) and torch.equal(a[1].view(torch.int32), b[1].view(torch.int32))
