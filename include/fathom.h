@@ -120,8 +120,8 @@ fathom_status fathom_alloc_depths(const void* q, fathom_dtype qdt, int U, int G,
  *   s_h(i) = sum_{j: t_j > 0} q_hj * khat_ij,
  *   khat_ij = (c^(t) + 1/2 - 2^(t-1)) * a16 * 2^(1-t),  c^(t) = first t bits of c.
  * Raw q.khat, no 1/sqrt(D) (App. A).  Floating-point order, per (h, i),
- * channels ascending:  x = fl32(fl32(q_hj * a16) * 2^(1-t_j)),
- * y = c^(t) + 1/2 - 2^(t-1) (exact),  acc = fmaf(x, y, acc) from acc = +0.
+ * channels ascending: khat is exact in fp32 (<= 16 significant bits) and
+ * acc = fmaf(q_hj, khat, acc) from acc = +0 (q_hj converted to fp32 exactly).
  *
  *   planes, scales  the store written by fathom_pack.
  *   q        [U][G][D] (qdt), depths [U][D] (values above 4 are read as 4).

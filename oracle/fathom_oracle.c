@@ -280,9 +280,8 @@ void orc_scores_f64(const uint64_t* planes, const uint16_t* scales, int64_t n, i
 /* ------------------------------------------------------------------------- */
 /* fp32 score replica (the reading of the paper's silence on score precision  */
 /* and order listed in the design doc): per head and key, channels ascending,      */
-/*   x   = fl32( fl32(q_hj * a16) * 2^(1-t_j) )                               */
-/*   y   = c^(t) + 1/2 - 2^(t-1)            (exact)                           */
-/*   acc = fmaf(x, y, acc),  acc starting at +0.                              */
+/*   khat = (c^(t) + 1/2 - 2^(t-1)) * a16 * 2^(1-t)   (exact in fp32)         */
+/*   acc  = fmaf(q_hj, khat, acc),  acc starting at +0.                       */
 /* ------------------------------------------------------------------------- */
 void orc_scores_f32(const uint64_t* planes, const uint16_t* scales, int64_t n, int64_t nb_cap,
                     int D, const float* q, int G, const uint8_t* depths, float* out) {
@@ -292,11 +291,8 @@ void orc_scores_f32(const uint64_t* planes, const uint16_t* scales, int64_t n, i
       for (int j = 0; j < D; ++j) {
         int t = depths[j];
         if (t == 0) continue;
-        float a16 = (float)orc_f16_to_f64(scales[(int64_t)j * nb_cap + i / 64]);
-        float x = q[h * D + j] * a16;
-        x = x * ldexpf(1.0f, 1 - t);
-        float y = (float)((double)prefix_code(planes, nb_cap, j, t, i) + 0.5 - ldexp(1.0, t - 1));
-        acc = fmaf(x, y, acc);
+        float khat = (float)orc_dequant(planes, scales, nb_cap, j, t, i); /* exact */
+        acc = fmaf(q[h * D + j], khat, acc);
       }
       out[(int64_t)h * n + i] = acc;
     }

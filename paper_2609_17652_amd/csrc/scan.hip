@@ -5,10 +5,11 @@
 // One wave per 64-key block, lane i = key 64b + i.  The unit's active
 // channels (t_j > 0) are compacted into LDS once per workgroup; per active
 // channel the wave reads the block's fp16 scale and the first t plane words
-// as wave-uniform (scalar) loads, each lane extracts its t code bits, and
-// every head accumulates one fused multiply-add in the documented order:
-//   x = fl32(fl32(q_hj * a16) * 2^(1-t)),  y = c^(t) + 1/2 - 2^(t-1),
-//   acc_h = fmaf(x, y, acc_h),  channels ascending, acc from +0.
+// as wave-uniform (scalar) loads, each lane extracts its t code bits and
+// dequantises its key exactly, and every head accumulates one fused
+// multiply-add in the documented order:
+//   khat = (c^(t) + 1/2 - 2^(t-1)) * a16 * 2^(1-t)   (exact in fp32),
+//   acc_h = fmaf(q_hj, khat, acc_h),  channels ascending, acc from +0.
 #include "common.hpp"
 
 namespace fathom {
@@ -68,11 +69,9 @@ __global__ __launch_bounds__(kScanThreads) void scan_kernel(const uint64_t* __re
     for (int p = 0; p < t; ++p) c = 2u * c + (uint32_t)((Pj[(int64_t)p * nb_cap] >> lane) & 1ull);
     const float y = (float)c + (0.5f - (float)(1 << (t - 1)));  // exact half-integer
     const float sc = __uint_as_float((uint32_t)(128 - t) << 23);  // 2^(1-t)
+    const float khat = __fmul_rn(y, __fmul_rn(af, sc));            // exact: <= 16 significant bits
 #pragma unroll
-    for (int h = 0; h < G; ++h) {
-      const float x = __fmul_rn(__fmul_rn(qs[h][j], af), sc);
-      acc[h] = __fmaf_rn(x, y, acc[h]);
-    }
+    for (int h = 0; h < G; ++h) acc[h] = __fmaf_rn(qs[h][j], khat, acc[h]);
   }
   const int64_t i = b * kBlockTokens + lane;
   if (i < nu && i < ld_s) {
