@@ -15,6 +15,10 @@ fathom_status launch_sparse_attn(const void*, fathom_dtype, const uint16_t*, con
                                  const int64_t*, int, int, const int32_t*, int, int, int, float, float*, uint32_t*,
                                  hipStream_t);
 size_t topk_ws_bytes(int R, int64_t max_n, int k);
+size_t fused_ws_bytes(int R, int64_t nb_cap, int k);
+fathom_status launch_scan_topk_fused(const uint64_t*, const uint16_t*, const int64_t*, int, int64_t, const void*,
+                                     fathom_dtype, int, const uint8_t*, int, int64_t, int64_t, int32_t*, float*, void*,
+                                     uint32_t*, hipStream_t);
 int attn_max_sink_local();
 }  // namespace fathom
 
@@ -43,8 +47,8 @@ fathom_status check_store(const uint64_t* planes, const uint16_t* scales, const 
 }
 
 size_t scan_topk_ws(int U, int G, int64_t max_n, int k) {
-  const int64_t ld = ((max_n + 63) / 64) * 64;
-  return round256((size_t)U * G * (size_t)(ld > 0 ? ld : 1) * 4) + topk_ws_bytes(U * G, ld, k);
+  const int64_t nb = (max_n + 63) / 64;
+  return fused_ws_bytes(U * G, nb > 0 ? nb : 1, k);
 }
 
 }  // namespace
@@ -142,14 +146,9 @@ fathom_status fathom_scan_topk(const uint64_t* planes, const uint16_t* scales, c
   if (k > FATHOM_MAX_K) return FATHOM_ERR_UNSUPPORTED;
   if (U == 0) return FATHOM_OK;
   if (!idx || !ws || !aligned(idx, 4) || (val && !aligned(val, 4)) || !aligned(ws, 256)) return FATHOM_ERR_INVALID;
-  const int64_t ld = nb_cap * 64 > 0 ? nb_cap * 64 : 64;
-  if (ws_bytes < scan_topk_ws(U, G, ld, k)) return FATHOM_ERR_WORKSPACE;
-  float* scores = reinterpret_cast<float*>(ws);
-  void* tws = reinterpret_cast<char*>(ws) + round256((size_t)U * G * (size_t)ld * 4);
-  hipStream_t s = as_stream(stream);
-  e = launch_scan(planes, scales, n, U, nb_cap, q, qdt, G, depths, scores, ld, dev_status, s);
-  if (e != FATHOM_OK) return e;
-  return launch_topk(scores, ld, n, U, G, k, lo, tail, idx, val, tws, dev_status, s);
+  if (ws_bytes < scan_topk_ws(U, G, nb_cap * 64, k)) return FATHOM_ERR_WORKSPACE;
+  return launch_scan_topk_fused(planes, scales, n, U, nb_cap, q, qdt, G, depths, k, lo, tail, idx, val, ws,
+                                dev_status, as_stream(stream));
 }
 
 fathom_status fathom_sparse_attn(const void* q, fathom_dtype qdt, const uint16_t* Krows, const uint16_t* Vrows,

@@ -70,4 +70,52 @@ __device__ __forceinline__ uint32_t score_key(float s) {
   return (b & 0x80000000u) ? ~b : (b | 0x80000000u);
 }
 
+// Block-wide search over a digit histogram hist[0..nb): the largest digit d
+// with (number of items in digits >= d) >= need; *above = items in digits > d.
+// If the total is below need, d = 0 and *above = total - hist[0].  All threads
+// of the block must call it; part[] needs blockDim.x / 64 entries.
+__device__ inline void find_crossing(const uint32_t* hist, int nb, uint32_t need, uint32_t* part, int* s_digit,
+                                     uint32_t* s_above) {
+  const int tid = threadIdx.x, nt = blockDim.x, lane = tid & 63, wave = tid >> 6, nw = nt >> 6;
+  const int per = (nb + nt - 1) / nt;
+  // thread t owns digits nb-1-t*per down to nb-(t+1)*per (top-down order)
+  uint32_t mine = 0;
+  for (int x = 0; x < per; ++x) {
+    const int d = nb - 1 - tid * per - x;
+    if (d >= 0) mine += hist[d];
+  }
+  uint32_t inc = mine;  // inclusive scan within the wave
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const uint32_t v = __shfl_up(inc, o, kWave);
+    if (lane >= o) inc += v;
+  }
+  if (lane == 63) part[wave] = inc;
+  __syncthreads();
+  uint32_t before = 0, total = 0;
+  for (int w = 0; w < nw; ++w) {
+    if (w < wave) before += part[w];
+    total += part[w];
+  }
+  const uint32_t cum = before + inc, prev = cum - mine;
+  if (prev < need && cum >= need) {
+    uint32_t above = prev;
+    for (int x = 0; x < per; ++x) {
+      const int d = nb - 1 - tid * per - x;
+      if (d < 0) break;
+      if (above + hist[d] >= need) {
+        *s_digit = d;
+        *s_above = above;
+        break;
+      }
+      above += hist[d];
+    }
+  }
+  if (tid == 0 && total < need) {
+    *s_digit = 0;
+    *s_above = total - hist[0];
+  }
+  __syncthreads();
+}
+
 }  // namespace fathom

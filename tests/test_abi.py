@@ -61,7 +61,8 @@ def test_workspace_sizes(fl):
     b = fl.fathom_topk_workspace_size(8, 4, 1 << 20, 4096)
     assert 0 < a < b
     s = fl.fathom_scan_topk_workspace_size(8, 4, 1 << 20, 2048)
-    assert s >= 8 * 4 * (1 << 20) * 4 + a
+    # the fused scan + top-k keeps no score array: far below 8 x 4 x 2^20 fp32 scores
+    assert 0 < s < 8 * 4 * (1 << 20) * 4 // 16
     assert fl.fathom_topk_workspace_size(0, 4, 10, 10) == 0
 
 

@@ -446,3 +446,42 @@ def test_repeatable_bit_identical():
     a = F.fathom_scan_topk(planes, scales, nt, q, d, 512)
     b = F.fathom_scan_topk(planes, scales, nt, q, d, 512)
     assert torch.equal(a[0], b[0]) and torch.equal(a[1].view(torch.int32), b[1].view(torch.int32))
+
+
+@pytest.mark.parametrize("scale", [50.0, 0.01])
+def test_scan_topk_fallback_is_exact(scale):
+    """Force the fused path's fallback from the data: the threshold is estimated
+    from every 8th block; scaling exactly those blocks' keys up (threshold too
+    high -> too few survivors) or down (threshold too low -> survivor buffer
+    overflow) must still give the oracle's top-k, with TOPK_FALLBACK raised."""
+    n, G, k = 65536, 4, 256
+    rng = np.random.default_rng(61)
+    K = special_keys(rng, n)[None].copy()
+    for b in range(0, n // 64, 8):
+        K[0, 64 * b:64 * b + 64] *= np.float32(scale)
+    nt = torch.tensor([n], dtype=torch.int64, device=DEV)
+    planes, scales = F.fathom_pack(torch.from_numpy(K).to(DEV), nt)
+    q = rng.standard_normal((1, G, 128)).astype(np.float16)
+    var = np.exp(rng.standard_normal((1, 128))).astype(np.float32)
+    qt = torch.from_numpy(q).to(DEV)
+    d, _ = F.fathom_alloc_depths(qt, torch.from_numpy(var).to(DEV), F.FATHOM_WATERFILL, 48)
+    st = F.new_status()
+    idx, val = F.fathom_scan_topk(planes, scales, nt, qt, d, k, dev_status=st)
+    assert status(st) & F.FATHOM_DEV_TOPK_FALLBACK
+    ref = oracle.scores_f32(u64(planes)[0], u16(scales)[0], n, q[0].astype(np.float32), d.cpu().numpy()[0])
+    for h in range(G):
+        oi, ov, _ = oracle.topk(ref[h], k)
+        assert np.array_equal(idx[0, h].cpu().numpy(), oi), h
+        assert np.array_equal(val[0, h].cpu().numpy(), ov), h
+
+
+def test_scan_topk_no_fallback_on_config_data():
+    """On the synthetic workloads the sampled threshold never needs the fallback."""
+    cfg = synth.CONFIGS[1]
+    data = synth.device_units(cfg, with_values=False)
+    st = F.new_status()
+    planes, scales = F.fathom_pack(data["K"], data["n"], dev_status=st)
+    for B in cfg.budgets:
+        d, _ = F.fathom_alloc_depths(data["q"], data["var"], F.FATHOM_WATERFILL, B, dev_status=st)
+        F.fathom_scan_topk(planes, scales, data["n"], data["q"], d, cfg.k, dev_status=st)
+    assert status(st) == 0
