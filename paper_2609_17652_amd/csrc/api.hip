@@ -15,7 +15,7 @@ fathom_status launch_sparse_attn(const void*, fathom_dtype, const uint16_t*, con
                                  const int64_t*, int, int, const int32_t*, int, int, int, float, float*, uint32_t*,
                                  hipStream_t);
 size_t topk_ws_bytes(int R, int64_t max_n, int k);
-size_t fused_ws_bytes(int R, int64_t nb_cap, int k);
+size_t fused_ws_bytes(int R, int U, int64_t nb_cap, int k);
 fathom_status launch_scan_topk_fused(const uint64_t*, const uint16_t*, const int64_t*, int, int64_t, const void*,
                                      fathom_dtype, int, const uint8_t*, int, int64_t, int64_t, int32_t*, float*, void*,
                                      uint32_t*, hipStream_t);
@@ -48,7 +48,7 @@ fathom_status check_store(const uint64_t* planes, const uint16_t* scales, const 
 
 size_t scan_topk_ws(int U, int G, int64_t max_n, int k) {
   const int64_t nb = (max_n + 63) / 64;
-  return fused_ws_bytes(U * G, nb > 0 ? nb : 1, k);
+  return fused_ws_bytes(U * G, U, nb > 0 ? nb : 1, k);
 }
 
 }  // namespace
@@ -144,6 +144,7 @@ fathom_status fathom_scan_topk(const uint64_t* planes, const uint16_t* scales, c
   if (e != FATHOM_OK) return e;
   if (lo < 0 || tail < 0 || k < 1) return FATHOM_ERR_INVALID;
   if (k > FATHOM_MAX_K) return FATHOM_ERR_UNSUPPORTED;
+  if (nb_cap >= ((int64_t)1 << 20)) return FATHOM_ERR_UNSUPPORTED;  // plane-row offsets are 32-bit
   if (U == 0) return FATHOM_OK;
   if (!idx || !ws || !aligned(idx, 4) || (val && !aligned(val, 4)) || !aligned(ws, 256)) return FATHOM_ERR_INVALID;
   if (ws_bytes < scan_topk_ws(U, G, nb_cap * 64, k)) return FATHOM_ERR_WORKSPACE;

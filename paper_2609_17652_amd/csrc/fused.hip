@@ -27,24 +27,37 @@ namespace fathom {
 
 constexpr int kFT = 256;          // threads per workgroup (4 waves)
 constexpr int kFW = kFT / kWave;
-constexpr int kSub = 16;          // blocks per weight-setup sub-tile (4 per wave)
-constexpr int kRange = 64;        // blocks per workgroup in the full pass
+constexpr int kGrp = 8;           // consecutive blocks per wave step: one 64-byte line per plane row
+constexpr int kSub = kFW * kGrp;  // 32 blocks per weight-setup sub-tile
+constexpr int kRange = 4 * kSub;  // 128 blocks per workgroup in the full pass
 constexpr int kFlush = 256;       // re-score when this many survivors are queued
 constexpr int kQueue = kFlush + kSub * kBlockTokens;
 constexpr int kMaxDw = kD / 4;    // z' dwords for 128 active channels
-constexpr int kSampleBlocks = 512;  // at most this many sampled blocks per row
+constexpr int kMaxCells = kD * kPlanes;
+constexpr int kSampleGroups = 64; // at most this many sampled groups (512 blocks) per row
 constexpr int kSelThreads = 1024;
 constexpr int kSelCap = 16384;    // LDS composites in the select kernel
 constexpr float kNegInf = -__builtin_huge_valf();
+
+// Per-unit read plan, built once per call: byte offsets (from the unit's plane
+// base) of the plane rows the proxy reads, in active-channel order.
+struct Plan {
+  uint32_t off[kD][4];       // rows of planes 0..3 of active channel a; planes >= t repeat plane t-1
+  uint32_t cell[kMaxCells];  // rows of every plane read (p < t), for the L2 prefetch
+  uint32_t tpack[kMaxDw];    // depth of channel 4d+k in byte k
+  uint32_t zinit[kMaxDw];    // 2^(4-t) in byte k: the constant part of z'
+  int32_t A, ncells, pad[62];
+};
 
 struct FusedWs {
   float* tau;       // [R] threshold on exact scores (-inf: every eligible key is kept)
   uint32_t* cnt;    // [R] survivors appended
   uint64_t* cand;   // [R][cap] composites (score_key << 32 | ~index)
-  float* sample;    // [R][s_cap] proxies of sampled keys
+  float* sample;    // [R][s_groups * 512] proxies of sampled keys
+  Plan* plan;       // [U]
   int cap;
-  int64_t s_stride; // sample every s_stride-th block
-  int64_t s_blocks; // sampled blocks per row
+  int64_t s_gstride;  // sample every s_gstride-th group of 8 blocks
+  int64_t s_groups;   // sampled groups per row
 };
 
 static inline size_t a256(size_t x) { return (x + 255) & ~(size_t)255; }
@@ -54,29 +67,32 @@ static inline int fused_cap(int k) {
   return c < kSelCap ? c : kSelCap;
 }
 
-static inline void fused_geometry(int64_t nb_cap, int64_t* stride, int64_t* sblocks) {
-  int64_t s = (nb_cap + kSampleBlocks - 1) / kSampleBlocks;
-  if (s < 8) s = 8;
-  *stride = s;
-  *sblocks = (nb_cap + s - 1) / s;
+static inline void fused_geometry(int64_t nb_cap, int64_t* gstride, int64_t* sgroups) {
+  const int64_t ng = (nb_cap + kGrp - 1) / kGrp;
+  int64_t s = (ng + kSampleGroups - 1) / kSampleGroups;
+  if (s < 2) s = 2;
+  *gstride = s;
+  *sgroups = (ng + s - 1) / s;
 }
 
-size_t fused_ws_bytes(int R, int64_t nb_cap, int k) {
-  int64_t s, sb;
-  fused_geometry(nb_cap > 0 ? nb_cap : 1, &s, &sb);
+size_t fused_ws_bytes(int R, int U, int64_t nb_cap, int k) {
+  int64_t s, sg;
+  fused_geometry(nb_cap > 0 ? nb_cap : 1, &s, &sg);
   return a256((size_t)R * 4) + a256((size_t)R * 4) + a256((size_t)R * fused_cap(k) * 8) +
-         a256((size_t)R * sb * kBlockTokens * 4);
+         a256((size_t)R * sg * kGrp * kBlockTokens * 4) + a256((size_t)U * sizeof(Plan));
 }
 
-static FusedWs fused_carve(void* ws, int R, int64_t nb_cap, int k) {
+static FusedWs fused_carve(void* ws, int R, int U, int64_t nb_cap, int k) {
   FusedWs w;
-  fused_geometry(nb_cap > 0 ? nb_cap : 1, &w.s_stride, &w.s_blocks);
+  fused_geometry(nb_cap > 0 ? nb_cap : 1, &w.s_gstride, &w.s_groups);
   w.cap = fused_cap(k);
   char* p = reinterpret_cast<char*>(ws);
   w.tau = reinterpret_cast<float*>(p); p += a256((size_t)R * 4);
   w.cnt = reinterpret_cast<uint32_t*>(p); p += a256((size_t)R * 4);
   w.cand = reinterpret_cast<uint64_t*>(p); p += a256((size_t)R * w.cap * 8);
-  w.sample = reinterpret_cast<float*>(p);
+  w.sample = reinterpret_cast<float*>(p); p += a256((size_t)R * w.s_groups * kGrp * kBlockTokens * 4);
+  w.plan = reinterpret_cast<Plan*>(p);
+  (void)U;
   return w;
 }
 
@@ -98,7 +114,6 @@ template <int G>
 struct FusedSmem {
   int act[kD];                      // j | (t << 8), active channels ascending
   float qa[kD][G];                  // fp32 query of active channel a, head h
-  uint32_t zinit[kMaxDw];           // constant bits of z' per dword
   uint32_t w8[kSub][kMaxDw][G];     // packed int8 weights
   float hdelta[kSub][G];            // delta / 2
   float ebound[kSub][G];            // error bound (inf: no bound, every key survives)
@@ -110,76 +125,171 @@ struct FusedSmem {
 
 __device__ __forceinline__ uint64_t lanemask_lt(int lane) { return lane == 0 ? 0ull : (~0ull >> (64 - lane)); }
 
-// Wave-uniform read of a plane word through the constant address space, so it
-// is a scalar (SMEM) load straight into SGPRs.  The store is never written
-// while a scan runs.
+// Wave-uniform reads through the constant address space are scalar (SMEM)
+// loads straight into SGPRs.  Neither the store nor the plan is written while
+// a scan runs.
+struct Words8 {
+  uint64_t w[kGrp];
+};
 typedef __attribute__((address_space(4))) const uint64_t cu64;
-__device__ __forceinline__ uint64_t sload(const uint64_t* p) { return *(cu64*)(p); }
-
-// z' bits of one channel (byte K of the dword) from its t plane words: one
-// EXEC-masked OR per plane, EXEC saved and restored inside the statement.
-template <int K>
-__device__ __forceinline__ uint32_t gather_channel(uint32_t z, int t, const uint64_t* __restrict__ Pj,
-                                                   int64_t pstride) {
-  uint64_t sv;
-  const uint64_t w0 = sload(Pj);
-  if (t == 1) {
-    asm volatile(
-        "s_mov_b64 %1, exec\n\t"
-        "s_andn2_b64 exec, %1, %2\n\t"
-        "v_or_b32 %0, %3, %0\n\t"
-        "s_mov_b64 exec, %1"
-        : "+v"(z), "=&s"(sv)
-        : "s"(w0), "i"(0xF0u << (8 * K)));
-    return z;
+typedef __attribute__((address_space(4))) const uint32_t cu32;
+typedef __attribute__((ext_vector_type(4))) unsigned int v4u;
+typedef __attribute__((address_space(4))) const v4u cu4;
+typedef __attribute__((ext_vector_type(16))) unsigned int v16u;
+typedef __attribute__((address_space(4))) const v16u cv16;
+__device__ __forceinline__ uint64_t sload64(const void* p) { return *(cu64*)(p); }
+__device__ __forceinline__ uint32_t sload32(const void* p) { return *(cu32*)(p); }
+__device__ __forceinline__ v4u sload128(const void* p) { return *(cu4*)(p); }
+__device__ __forceinline__ const char* uniform_ptr(const char* p) {
+  const uint64_t v = reinterpret_cast<uint64_t>(p);
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
+  return reinterpret_cast<const char*>(((uint64_t)hi << 32) | lo);
+}
+// The plane words of the 8 blocks of a group from one row; a group that runs
+// past nb_cap (the last one, when nb_cap % 8 != 0) reads only words inside it.
+template <bool FULL>
+__device__ __forceinline__ Words8 sload_words(const char* row, int64_t nleft) {
+  row = uniform_ptr(row);
+  Words8 w;
+  if constexpr (FULL) {
+    const v16u v = *(cv16*)(row);
+#pragma unroll
+    for (int g = 0; g < kGrp; ++g) w.w[g] = ((uint64_t)v[2 * g + 1] << 32) | v[2 * g];
+  } else {
+#pragma unroll
+    for (int g = 0; g < kGrp; ++g) {
+      w.w[g] = 0ull;
+      if (g < nleft) w.w[g] = sload64(row + 8 * g);
+    }
   }
-  const uint64_t w1 = sload(Pj + pstride);
-  if (t == 2) {
-    asm volatile(
-        "s_mov_b64 %1, exec\n\t"
-        "s_andn2_b64 exec, %1, %2\n\t"
-        "v_or_b32 %0, %4, %0\n\t"
-        "s_and_b64 exec, %1, %3\n\t"
-        "v_or_b32 %0, %5, %0\n\t"
-        "s_mov_b64 exec, %1"
-        : "+v"(z), "=&s"(sv)
-        : "s"(w0), "s"(w1), "i"(0xF0u << (8 * K)), "i"(8u << (8 * K)));
-    return z;
-  }
-  const uint64_t w2 = sload(Pj + 2 * pstride);
-  if (t == 3) {
-    asm volatile(
-        "s_mov_b64 %1, exec\n\t"
-        "s_andn2_b64 exec, %1, %2\n\t"
-        "v_or_b32 %0, %5, %0\n\t"
-        "s_and_b64 exec, %1, %3\n\t"
-        "v_or_b32 %0, %6, %0\n\t"
-        "s_and_b64 exec, %1, %4\n\t"
-        "v_or_b32 %0, %7, %0\n\t"
-        "s_mov_b64 exec, %1"
-        : "+v"(z), "=&s"(sv)
-        : "s"(w0), "s"(w1), "s"(w2), "i"(0xF0u << (8 * K)), "i"(8u << (8 * K)), "i"(4u << (8 * K)));
-    return z;
-  }
-  const uint64_t w3 = sload(Pj + 3 * pstride);
-  asm volatile(
-      "s_mov_b64 %1, exec\n\t"
-      "s_andn2_b64 exec, %1, %2\n\t"
-      "v_or_b32 %0, %6, %0\n\t"
-      "s_and_b64 exec, %1, %3\n\t"
-      "v_or_b32 %0, %7, %0\n\t"
-      "s_and_b64 exec, %1, %4\n\t"
-      "v_or_b32 %0, %8, %0\n\t"
-      "s_and_b64 exec, %1, %5\n\t"
-      "v_or_b32 %0, %9, %0\n\t"
-      "s_mov_b64 exec, %1"
-      : "+v"(z), "=&s"(sv)
-      : "s"(w0), "s"(w1), "s"(w2), "s"(w3), "i"(0xF0u << (8 * K)), "i"(8u << (8 * K)), "i"(4u << (8 * K)),
-        "i"(2u << (8 * K)));
-  return z;
+  return w;
 }
 
-// Unit-level setup: active channels, fp32 queries per active channel, z' constants.
+// One plane of one channel (byte K of the z' dword) for the 8 blocks of a
+// group: lanes whose key has the bit set (the plane word is the lane mask)
+// OR in the plane's value; the sign plane ORs 0xF0 where the bit is clear.
+// EXEC is saved and restored inside the statement; SCC is clobbered (the
+// compiler must not keep a carry or compare result live across it).
+template <int K, int P>
+__device__ __forceinline__ void or_plane(uint32_t (&z)[kGrp], const Words8& w) {
+  uint64_t sv;
+  constexpr uint32_t c = P == 0 ? (0xF0u << (8 * K)) : ((8u >> (P > 0 ? P - 1 : 0)) << (8 * K));
+  if (P == 0) {
+    asm volatile(
+        "s_mov_b64 %8, exec\n\t"
+        "s_andn2_b64 exec, %8, %9\n\tv_or_b32 %0, %17, %0\n\t"
+        "s_andn2_b64 exec, %8, %10\n\tv_or_b32 %1, %17, %1\n\t"
+        "s_andn2_b64 exec, %8, %11\n\tv_or_b32 %2, %17, %2\n\t"
+        "s_andn2_b64 exec, %8, %12\n\tv_or_b32 %3, %17, %3\n\t"
+        "s_andn2_b64 exec, %8, %13\n\tv_or_b32 %4, %17, %4\n\t"
+        "s_andn2_b64 exec, %8, %14\n\tv_or_b32 %5, %17, %5\n\t"
+        "s_andn2_b64 exec, %8, %15\n\tv_or_b32 %6, %17, %6\n\t"
+        "s_andn2_b64 exec, %8, %16\n\tv_or_b32 %7, %17, %7\n\t"
+        "s_mov_b64 exec, %8"
+        : "+v"(z[0]), "+v"(z[1]), "+v"(z[2]), "+v"(z[3]), "+v"(z[4]), "+v"(z[5]), "+v"(z[6]), "+v"(z[7]),
+          "=&s"(sv)
+        : "s"(w.w[0]), "s"(w.w[1]), "s"(w.w[2]), "s"(w.w[3]), "s"(w.w[4]), "s"(w.w[5]), "s"(w.w[6]), "s"(w.w[7]),
+          "i"(c)
+        : "scc");
+  } else {
+    asm volatile(
+        "s_mov_b64 %8, exec\n\t"
+        "s_and_b64 exec, %8, %9\n\tv_or_b32 %0, %17, %0\n\t"
+        "s_and_b64 exec, %8, %10\n\tv_or_b32 %1, %17, %1\n\t"
+        "s_and_b64 exec, %8, %11\n\tv_or_b32 %2, %17, %2\n\t"
+        "s_and_b64 exec, %8, %12\n\tv_or_b32 %3, %17, %3\n\t"
+        "s_and_b64 exec, %8, %13\n\tv_or_b32 %4, %17, %4\n\t"
+        "s_and_b64 exec, %8, %14\n\tv_or_b32 %5, %17, %5\n\t"
+        "s_and_b64 exec, %8, %15\n\tv_or_b32 %6, %17, %6\n\t"
+        "s_and_b64 exec, %8, %16\n\tv_or_b32 %7, %17, %7\n\t"
+        "s_mov_b64 exec, %8"
+        : "+v"(z[0]), "+v"(z[1]), "+v"(z[2]), "+v"(z[3]), "+v"(z[4]), "+v"(z[5]), "+v"(z[6]), "+v"(z[7]),
+          "=&s"(sv)
+        : "s"(w.w[0]), "s"(w.w[1]), "s"(w.w[2]), "s"(w.w[3]), "s"(w.w[4]), "s"(w.w[5]), "s"(w.w[6]), "s"(w.w[7]),
+          "i"(c)
+        : "scc");
+  }
+}
+
+// z' byte K of one channel for a group: its t plane rows (the plan repeats row
+// t-1 for planes >= t, so the four loads are unconditional and hit one line).
+template <int K, bool FULL>
+__device__ __forceinline__ void gather_channel(uint32_t (&z)[kGrp], int t, const char* base, const Plan* plan,
+                                               int a, int64_t nleft) {
+  const v4u o = sload128(&plan->off[a][0]);
+  {
+    const Words8 w0 = sload_words<FULL>(base + o.x, nleft);
+    const Words8 w1 = sload_words<FULL>(base + o.y, nleft);  // row of plane 0 again when t == 1
+    or_plane<K, 0>(z, w0);
+    if (t > 1) or_plane<K, 1>(z, w1);
+  }
+  if (t > 2) {
+    const Words8 w2 = sload_words<FULL>(base + o.z, nleft);
+    const Words8 w3 = sload_words<FULL>(base + o.w, nleft);
+    or_plane<K, 2>(z, w2);
+    if (t > 3) or_plane<K, 3>(z, w3);
+  }
+}
+
+// ---------------------------------------------------------------- plan
+// One workgroup of 128 threads per unit.
+__global__ __launch_bounds__(kD) void fused_plan_kernel(FusedArgs a) {
+  __shared__ int act[kD];
+  __shared__ int wc[2];
+  __shared__ int cstart[kD + 1];
+  const int u = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  Plan* pl = a.ws.plan + u;
+  int t = a.depths[(int64_t)u * kD + tid];
+  t = t > kPlanes ? kPlanes : t;
+  const bool on = t > 0;
+  const uint64_t m = __ballot(on);
+  if (lane == 0) wc[wave] = __popcll(m);
+  __syncthreads();
+  if (on) act[(wave == 1 ? wc[0] : 0) + __popcll(m & lanemask_lt(lane))] = tid | (t << 8);
+  const int A = wc[0] + wc[1];
+  __syncthreads();
+  const uint32_t rowb = (uint32_t)(a.nb_cap * 8);  // bytes per plane row
+  if (tid < A) {
+    const int j = act[tid] & 0xFF, tt = act[tid] >> 8;
+#pragma unroll
+    for (int p = 0; p < 4; ++p) pl->off[tid][p] = (uint32_t)(j * kPlanes + (p < tt ? p : tt - 1)) * rowb;
+  } else {
+#pragma unroll
+    for (int p = 0; p < 4; ++p) pl->off[tid][p] = 0u;  // row 0 of the unit: valid, never ORed
+  }
+  // prefix of depths for the cell list
+  if (tid == 0) {
+    int c = 0;
+    for (int x = 0; x < A; ++x) {
+      cstart[x] = c;
+      c += act[x] >> 8;
+    }
+    cstart[A] = c;
+    pl->A = A;
+    pl->ncells = c;
+  }
+  __syncthreads();
+  if (tid < A) {
+    const int j = act[tid] & 0xFF, tt = act[tid] >> 8;
+    for (int p = 0; p < tt; ++p) pl->cell[cstart[tid] + p] = (uint32_t)(j * kPlanes + p) * rowb;
+  }
+  if (tid < kMaxDw) {
+    uint32_t tp = 0u, zi = 0u;
+    for (int k2 = 0; k2 < 4; ++k2) {
+      const int x = 4 * tid + k2;
+      if (x < A) {
+        const int tt = act[x] >> 8;
+        tp |= (uint32_t)tt << (8 * k2);
+        zi |= (8u >> (tt - 1)) << (8 * k2);
+      }
+    }
+    pl->tpack[tid] = tp;
+    pl->zinit[tid] = zi;
+  }
+}
+
+// Unit-level LDS setup: active channels and fp32 queries per active channel.
 template <int G>
 __device__ void unit_setup(FusedSmem<G>& sm, const FusedArgs& a, int u) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -205,34 +315,26 @@ __device__ void unit_setup(FusedSmem<G>& sm, const FusedArgs& a, int u) {
     const int j = sm.act[ai] & 0xFF;
     sm.qa[ai][h] = load_q(a.q, a.qdt, ((int64_t)u * G + h) * kD + j);
   }
-  for (int d = tid; d < kMaxDw; d += kFT) {
-    uint32_t z = 0;
-    for (int k = 0; k < 4; ++k) {
-      const int ai = 4 * d + k;
-      if (ai < A) z |= (8u >> ((sm.act[ai] >> 8) - 1)) << (8 * k);  // 2^(4-t)
-    }
-    sm.zinit[d] = z;
-  }
   __syncthreads();
 }
 
-// Weights of up to kSub blocks (block indices from blk_of): 16 threads per
-// block, each owning whole dwords of 4 channels.
+// Weights of the kSub blocks of a sub-tile (block indices from blk_of; -1 or
+// >= nbu: unused): 8 threads per block, each owning whole dwords of 4 channels.
 template <int G, typename BlkOf>
 __device__ void weight_setup(FusedSmem<G>& sm, const FusedArgs& a, int u, int64_t nbu, BlkOf blk_of) {
+  constexpr int TPB = kFT / kSub;  // threads per block
   const int tid = threadIdx.x;
-  const int blk = tid >> 4, sl = tid & 15;
+  const int blk = tid / TPB, sl = tid % TPB;
   const int A = sm.nact, AD = (A + 3) >> 2;
   const int64_t b = blk_of(blk);
   const bool valid = b >= 0 && b < nbu;
   const uint16_t* Su = a.scales + (int64_t)u * kD * a.nb_cap;
-  // pass 1: max |w| per head over the block's active channels
   float mx[G];
 #pragma unroll
   for (int h = 0; h < G; ++h) mx[h] = 0.0f;
   bool finite = true;
   if (valid) {
-    for (int d = sl; d < AD; d += 16) {
+    for (int d = sl; d < AD; d += TPB) {
       for (int k = 0; k < 4; ++k) {
         const int ai = 4 * d + k;
         if (ai >= A) break;
@@ -250,29 +352,26 @@ __device__ void weight_setup(FusedSmem<G>& sm, const FusedArgs& a, int u, int64_
 #pragma unroll
   for (int h = 0; h < G; ++h)
 #pragma unroll
-    for (int o = 8; o >= 1; o >>= 1) mx[h] = fmaxf(mx[h], __shfl_xor(mx[h], o, 16));
-  // __any over the 16 lanes of the block
+    for (int o = TPB / 2; o >= 1; o >>= 1) mx[h] = fmaxf(mx[h], __shfl_xor(mx[h], o, TPB));
   int fin = finite ? 1 : 0;
 #pragma unroll
-  for (int o = 8; o >= 1; o >>= 1) fin &= __shfl_xor(fin, o, 16);
+  for (int o = TPB / 2; o >= 1; o >>= 1) fin &= __shfl_xor(fin, o, TPB);
   float delta[G], inv[G];
   bool ok[G];
 #pragma unroll
   for (int h = 0; h < G; ++h) {
     int e;
     (void)frexpf(mx[h], &e);  // mx in [2^(e-1), 2^e)
-    ok[h] = fin && mx[h] >= 0x1p-100f;
-    if (mx[h] == 0.0f) ok[h] = fin;
+    ok[h] = fin && (mx[h] >= 0x1p-100f || mx[h] == 0.0f);
     const int ee = e < -100 ? -100 : e;
     delta[h] = ldexpf(1.0f, ee - 7);  // |w| / delta < 128
     inv[h] = ldexpf(1.0f, 7 - ee);
   }
-  // pass 2: quantise, pack, error bound
   float eb[G];
 #pragma unroll
   for (int h = 0; h < G; ++h) eb[h] = 0.0f;
   if (valid) {
-    for (int d = sl; d < AD; d += 16) {
+    for (int d = sl; d < AD; d += TPB) {
       uint32_t pk[G];
 #pragma unroll
       for (int h = 0; h < G; ++h) pk[h] = 0u;
@@ -299,7 +398,7 @@ __device__ void weight_setup(FusedSmem<G>& sm, const FusedArgs& a, int u, int64_
 #pragma unroll
   for (int h = 0; h < G; ++h)
 #pragma unroll
-    for (int o = 8; o >= 1; o >>= 1) eb[h] = __fadd_rn(eb[h], __shfl_xor(eb[h], o, 16));
+    for (int o = TPB / 2; o >= 1; o >>= 1) eb[h] = __fadd_rn(eb[h], __shfl_xor(eb[h], o, TPB));
   if (sl == 0) {
 #pragma unroll
     for (int h = 0; h < G; ++h) {
@@ -311,37 +410,54 @@ __device__ void weight_setup(FusedSmem<G>& sm, const FusedArgs& a, int u, int64_
   }
 }
 
-// Proxy of the wave's block b for all G heads (lane = key): acc = sum_j w8_j z'_j.
-template <int G>
-__device__ __forceinline__ void proxy_block(const FusedSmem<G>& sm, const FusedArgs& a, int u, int blk, int64_t b,
-                                            int acc[G]) {
-  const int A = sm.nact, AD = (A + 3) >> 2;
-  const uint64_t* Pu = a.planes + (int64_t)u * kD * kPlanes * a.nb_cap + b;
-  const int64_t ps = a.nb_cap;
-#pragma unroll
-  for (int h = 0; h < G; ++h) acc[h] = 0;
-  for (int d = 0; d < AD; ++d) {
-    uint32_t z = sm.zinit[d];
-    const int a0 = 4 * d;
-    {
-      const int e = __builtin_amdgcn_readfirstlane(sm.act[a0]);
-      z = gather_channel<0>(z, e >> 8, Pu + (int64_t)(e & 0xFF) * kPlanes * ps, ps);
-    }
-    if (a0 + 1 < A) {
-      const int e = __builtin_amdgcn_readfirstlane(sm.act[a0 + 1]);
-      z = gather_channel<1>(z, e >> 8, Pu + (int64_t)(e & 0xFF) * kPlanes * ps, ps);
-    }
-    if (a0 + 2 < A) {
-      const int e = __builtin_amdgcn_readfirstlane(sm.act[a0 + 2]);
-      z = gather_channel<2>(z, e >> 8, Pu + (int64_t)(e & 0xFF) * kPlanes * ps, ps);
-    }
-    if (a0 + 3 < A) {
-      const int e = __builtin_amdgcn_readfirstlane(sm.act[a0 + 3]);
-      z = gather_channel<3>(z, e >> 8, Pu + (int64_t)(e & 0xFF) * kPlanes * ps, ps);
-    }
-#pragma unroll
-    for (int h = 0; h < G; ++h) acc[h] = __builtin_amdgcn_sdot4((int)z, (int)sm.w8[blk][d][h], acc[h], false);
+// Touch the plane lines of a group (one 4-byte load per row, 64 rows per
+// instruction) so they are in L2 when the scalar loads ask for them; the
+// returned value only keeps the loads alive.
+__device__ __forceinline__ uint32_t prefetch_group(const char* base, const Plan* plan, int ncells, bool any) {
+  uint32_t acc = 0u;
+  if (any) {
+    const int lane = threadIdx.x & 63;
+    for (int c = lane; c < ncells; c += kWave) acc ^= *reinterpret_cast<const uint32_t*>(base + plan->cell[c]);
   }
+  return acc;
+}
+
+// Proxy sums of the 8 blocks of a group for all G heads (lane = key):
+// acc[g][h] = sum_j w8_j z'_j for block g.
+template <int G, bool FULL>
+__device__ __forceinline__ void proxy_group_impl(const FusedSmem<G>& sm, const Plan* plan, const char* base,
+                                                 int64_t nleft, int blk0, int acc[kGrp][G]) {
+  const int A = sm.nact, AD = (A + 3) >> 2;
+#pragma unroll
+  for (int g = 0; g < kGrp; ++g)
+#pragma unroll
+    for (int h = 0; h < G; ++h) acc[g][h] = 0;
+  for (int d = 0; d < AD; ++d) {
+    const uint32_t tp = sload32(&plan->tpack[d]);
+    const uint32_t zi = sload32(&plan->zinit[d]);
+    uint32_t z[kGrp];
+#pragma unroll
+    for (int g = 0; g < kGrp; ++g) z[g] = zi;
+    gather_channel<0, FULL>(z, (int)(tp & 0xFF), base, plan, 4 * d, nleft);
+    if ((tp >> 8) & 0xFF) gather_channel<1, FULL>(z, (int)((tp >> 8) & 0xFF), base, plan, 4 * d + 1, nleft);
+    if ((tp >> 16) & 0xFF) gather_channel<2, FULL>(z, (int)((tp >> 16) & 0xFF), base, plan, 4 * d + 2, nleft);
+    if (tp >> 24) gather_channel<3, FULL>(z, (int)(tp >> 24), base, plan, 4 * d + 3, nleft);
+#pragma unroll
+    for (int g = 0; g < kGrp; ++g) {
+#pragma unroll
+      for (int h = 0; h < G; ++h)
+        acc[g][h] = __builtin_amdgcn_sdot4((int)z[g], (int)sm.w8[blk0 + g][d][h], acc[g][h], false);
+    }
+  }
+}
+
+template <int G>
+__device__ __forceinline__ void proxy_group(const FusedSmem<G>& sm, const FusedArgs& a, const Plan* plan,
+                                            const char* base, int64_t gb, int blk0, int acc[kGrp][G]) {
+  if (gb + kGrp <= a.nb_cap)
+    proxy_group_impl<G, true>(sm, plan, base, kGrp, blk0, acc);
+  else
+    proxy_group_impl<G, false>(sm, plan, base, a.nb_cap - gb, blk0, acc);
 }
 
 // Exact documented scores of key (block b, bit) for all G heads, read from the store.
@@ -380,6 +496,7 @@ __device__ __forceinline__ void row_window(const FusedArgs& a, int u, int64_t* n
 }
 
 // ---------------------------------------------------------------- pass 1
+// Each workgroup: 4 sampled groups (one per wave) of the unit.
 template <int G>
 __global__ __launch_bounds__(kFT) void fused_sample_kernel(FusedArgs a) {
   __shared__ FusedSmem<G> sm;
@@ -387,34 +504,37 @@ __global__ __launch_bounds__(kFT) void fused_sample_kernel(FusedArgs a) {
   int64_t nu, lo, hi;
   row_window(a, u, &nu, &lo, &hi, false);
   const int64_t nbu = (nu + kBlockTokens - 1) / kBlockTokens;
-  const int64_t sb0 = (int64_t)blockIdx.x * kSub;  // first sampled block index of this workgroup
+  const Plan* plan = a.ws.plan + u;
+  const char* base = reinterpret_cast<const char*>(a.planes + (int64_t)u * kD * kPlanes * a.nb_cap);
+  const int64_t sg = (int64_t)blockIdx.x * kFW + wave;  // sampled group index
+  const int64_t gb = sg * a.ws.s_gstride * kGrp;        // its first block
+  const bool mine = sg < a.ws.s_groups && gb < nbu;
+  const uint32_t pf = prefetch_group(base + gb * 8, plan, sload32(&plan->ncells), mine);
   unit_setup<G>(sm, a, u);
-  weight_setup<G>(sm, a, u, nbu, [&](int blk) { return (sb0 + blk) * a.ws.s_stride; });
+  weight_setup<G>(sm, a, u, nbu, [&](int blk) {
+    const int64_t s2 = (int64_t)blockIdx.x * kFW + blk / kGrp;
+    return s2 < a.ws.s_groups ? s2 * a.ws.s_gstride * kGrp + blk % kGrp : (int64_t)-1;
+  });
   __syncthreads();
-  for (int r = 0; r < kSub / kFW; ++r) {
-    const int blk = wave + kFW * r;
-    const int64_t sb = sb0 + blk;
-    if (sb >= a.ws.s_blocks) break;
-    const int64_t b = sb * a.ws.s_stride;
+  if (sg >= a.ws.s_groups) return;
+  const int blk0 = wave * kGrp;
+  int acc[kGrp][G];
+  if (gb < nbu) proxy_group<G>(sm, a, plan, base + gb * 8, gb, blk0, acc);
+  asm volatile("" ::"v"(pf));
+#pragma unroll
+  for (int g = 0; g < kGrp; ++g) {
+    const int64_t b = gb + g;
     const int64_t i = b * kBlockTokens + lane;
-    float lb[G];
-    if (b < nbu) {
-      int acc[G];
-      proxy_block<G>(sm, a, u, blk, b, acc);
 #pragma unroll
-      for (int h = 0; h < G; ++h) {
-        // the proxy itself (exact in fp32): tau only steers how many keys are
-        // re-scored; the survivor count, not tau, guarantees the result
-        lb[h] = __fmul_rn(sm.hdelta[blk][h], (float)acc[h]);
-        if (!(i >= lo && i < hi) || !(sm.ebound[blk][h] <= 3.402823466e38f)) lb[h] = kNegInf;
-      }
-    } else {
-#pragma unroll
-      for (int h = 0; h < G; ++h) lb[h] = kNegInf;
+    for (int h = 0; h < G; ++h) {
+      // the proxy itself (exact in fp32): tau only steers how many keys are
+      // re-scored; the survivor count, not tau, guarantees the result
+      float v = kNegInf;
+      if (b < nbu && i >= lo && i < hi && sm.ebound[blk0 + g][h] <= 3.402823466e38f)
+        v = __fmul_rn(sm.hdelta[blk0 + g][h], (float)acc[g][h]);
+      a.ws.sample[((int64_t)u * G + h) * a.ws.s_groups * (kGrp * kBlockTokens) + (sg * kGrp + g) * kBlockTokens +
+                  lane] = v;
     }
-#pragma unroll
-    for (int h = 0; h < G; ++h)
-      a.ws.sample[((int64_t)u * G + h) * a.ws.s_blocks * kBlockTokens + sb * kBlockTokens + lane] = lb[h];
   }
 }
 
@@ -422,6 +542,7 @@ __global__ __launch_bounds__(kFT) void fused_sample_kernel(FusedArgs a) {
 // tau = the m-th largest sampled proxy, m ~ 1.25 k * (sampled / eligible) + 16;
 // tau = -inf when the row has no more eligible keys than the survivor buffer holds.
 __global__ __launch_bounds__(kSelThreads) void fused_tau_kernel(FusedArgs a, int G) {
+  extern __shared__ uint32_t keys[];  // the row's sample as order-preserving keys (0 = unusable)
   __shared__ uint32_t hist[2048];
   __shared__ uint32_t s_prefix, s_mask, s_above;
   __shared__ int s_need, s_digit;
@@ -438,13 +559,17 @@ __global__ __launch_bounds__(kSelThreads) void fused_tau_kernel(FusedArgs a, int
     }
     return;
   }
-  const float* smp = a.ws.sample + (int64_t)r * a.ws.s_blocks * kBlockTokens;
-  const int64_t ns = a.ws.s_blocks * kBlockTokens;
-  // count sampled eligible keys with a usable proxy
+  const float* smp = a.ws.sample + (int64_t)r * a.ws.s_groups * (kGrp * kBlockTokens);
+  const int ns = (int)(a.ws.s_groups * kGrp * kBlockTokens);
   if (tid == 0) s_total = 0u;
   __syncthreads();
   uint32_t c = 0;
-  for (int64_t i = tid; i < ns; i += kSelThreads) c += smp[i] > kNegInf;
+  for (int i = tid; i < ns; i += kSelThreads) {
+    const float v = smp[i];
+    const bool use = v > kNegInf;
+    keys[i] = use ? (score_key(v) | 1u) : 0u;  // keep 0 free: NaN proxies do not occur
+    c += use;
+  }
   atomicAdd(&s_total, c);
   __syncthreads();
   const int64_t m_s = s_total;
@@ -467,12 +592,9 @@ __global__ __launch_bounds__(kSelThreads) void fused_tau_kernel(FusedArgs a, int
     for (int b = tid; b < 2048; b += kSelThreads) hist[b] = 0u;
     __syncthreads();
     const uint32_t prefix = s_prefix, mask = s_mask, dm = (1u << bits[pass]) - 1u;
-    for (int64_t i = tid; i < ns; i += kSelThreads) {
-      const float v = smp[i];
-      if (v > kNegInf) {
-        const uint32_t key = score_key(v);
-        if ((key & mask) == prefix) atomicAdd(&hist[(key >> shifts[pass]) & dm], 1u);
-      }
+    for (int i = tid; i < ns; i += kSelThreads) {
+      const uint32_t key = keys[i];
+      if (key && (key & mask) == prefix) atomicAdd(&hist[(key >> shifts[pass]) & dm], 1u);
     }
     __syncthreads();
     find_crossing(hist, (int)dm + 1, (uint32_t)s_need, part, &s_digit, &s_above);
@@ -484,7 +606,7 @@ __global__ __launch_bounds__(kSelThreads) void fused_tau_kernel(FusedArgs a, int
     __syncthreads();
   }
   if (tid == 0) {
-    const uint32_t key = s_prefix;
+    const uint32_t key = s_prefix & ~1u;  // the low bit was forced on: round the key down
     const uint32_t bitsf = (key & 0x80000000u) ? (key & 0x7FFFFFFFu) : ~key;
     a.ws.tau[r] = __uint_as_float(bitsf);
     a.ws.cnt[r] = 0u;
@@ -536,6 +658,11 @@ __global__ __launch_bounds__(kFT) void fused_full_kernel(FusedArgs a) {
   const int64_t nbu = (nu + kBlockTokens - 1) / kBlockTokens;
   const int64_t b0 = (int64_t)blockIdx.x * kRange;
   if (b0 >= nbu || b0 * kBlockTokens >= hi || (b0 + kRange) * kBlockTokens <= lo) return;
+  const Plan* plan = a.ws.plan + u;
+  const char* base = reinterpret_cast<const char*>(a.planes + (int64_t)u * kD * kPlanes * a.nb_cap);
+  const int ncells = (int)sload32(&plan->ncells);
+  // L2 prefetch of this wave's first group
+  uint32_t pf = prefetch_group(base + (b0 + wave * kGrp) * 8, plan, ncells, b0 + wave * kGrp < nbu);
   unit_setup<G>(sm, a, u);
   if (tid < G) sm.tau[tid] = a.ws.tau[u * G + tid];
   for (int s0 = 0; s0 < kRange; s0 += kSub) {
@@ -544,29 +671,36 @@ __global__ __launch_bounds__(kFT) void fused_full_kernel(FusedArgs a) {
     __syncthreads();  // previous sub-tile's weights and queue are consumed
     weight_setup<G>(sm, a, u, nbu, [&](int blk) { return sbase + blk; });
     __syncthreads();
-    for (int r = 0; r < kSub / kFW; ++r) {
-      const int blk = wave + kFW * r;
-      const int64_t b = sbase + blk;
-      if (b >= nbu) break;
-      int acc[G];
-      proxy_block<G>(sm, a, u, blk, b, acc);
-      const int64_t i = b * kBlockTokens + lane;
-      const bool elig = i >= lo && i < hi;
-      int hm = 0;
+    const int64_t gb = sbase + wave * kGrp;
+    if (gb < nbu) {
+      const int blk0 = wave * kGrp;
+      int acc[kGrp][G];
+      proxy_group<G>(sm, a, plan, base + gb * 8, gb, blk0, acc);
+      asm volatile("" ::"v"(pf));
+      const int64_t gnext = gb + kSub;  // prefetch this wave's next group
+      pf = prefetch_group(base + gnext * 8, plan, ncells, s0 + kSub < kRange && gnext < nbu);
 #pragma unroll
-      for (int h = 0; h < G; ++h) {
-        const float p = __fmul_rn(sm.hdelta[blk][h], (float)acc[h]);
-        const float ub = __fadd_rn(p, sm.ebound[blk][h]);
-        if (elig && (ub >= sm.tau[h] || sm.tau[h] == kNegInf || ub != ub)) hm |= 1 << h;
-      }
-      const uint64_t any = __ballot(hm != 0);
-      if (any) {
-        int basep = 0;
-        const int leader = __ffsll((unsigned long long)any) - 1;
-        if (lane == leader) basep = atomicAdd(&sm.qcount, __popcll(any));
-        basep = __shfl(basep, leader, kWave);
-        if (hm) sm.queue[basep + __popcll(any & lanemask_lt(lane))] = (uint32_t)((b - b0) * kBlockTokens + lane) |
-                                                                      ((uint32_t)hm << 16);
+      for (int g = 0; g < kGrp; ++g) {
+        const int64_t b = gb + g;
+        const int64_t i = b * kBlockTokens + lane;
+        const bool elig = b < nbu && i >= lo && i < hi;
+        int hm = 0;
+#pragma unroll
+        for (int h = 0; h < G; ++h) {
+          const float p = __fmul_rn(sm.hdelta[blk0 + g][h], (float)acc[g][h]);
+          const float ub = __fadd_rn(p, sm.ebound[blk0 + g][h]);
+          if (elig && (ub >= sm.tau[h] || sm.tau[h] == kNegInf || ub != ub)) hm |= 1 << h;
+        }
+        const uint64_t any = __ballot(hm != 0);
+        if (any) {
+          int basep = 0;
+          const int leader = __ffsll((unsigned long long)any) - 1;
+          if (lane == leader) basep = atomicAdd(&sm.qcount, __popcll(any));
+          basep = __shfl(basep, leader, kWave);
+          if (hm)
+            sm.queue[basep + __popcll(any & lanemask_lt(lane))] =
+                (uint32_t)((b - b0) * kBlockTokens + lane) | ((uint32_t)hm << 16);
+        }
       }
     }
     __syncthreads();
@@ -577,6 +711,7 @@ __global__ __launch_bounds__(kFT) void fused_full_kernel(FusedArgs a) {
       if (tid == 0) sm.qcount = 0;
     }
   }
+  asm volatile("" ::"v"(pf));
 }
 
 // ---------------------------------------------------------------- pass 4
@@ -726,13 +861,18 @@ static fathom_status launch_fused_g(const FusedArgs& fa, int U, int32_t* idx, fl
   static bool attr = false;
   if (!attr) {
     if (hipFuncSetAttribute(reinterpret_cast<const void*>(&fused_select_kernel<G>),
-                            hipFuncAttributeMaxDynamicSharedMemorySize, kSelCap * 8) != hipSuccess)
+                            hipFuncAttributeMaxDynamicSharedMemorySize, kSelCap * 8) != hipSuccess ||
+        hipFuncSetAttribute(reinterpret_cast<const void*>(&fused_tau_kernel),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, kSampleGroups * kGrp * kBlockTokens * 4) !=
+            hipSuccess)
       return FATHOM_ERR_HIP;
     attr = true;
   }
-  dim3 gs((unsigned)((fa.ws.s_blocks + kSub - 1) / kSub), (unsigned)U);
+  hipLaunchKernelGGL(fused_plan_kernel, dim3(U), dim3(kD), 0, s, fa);
+  dim3 gs((unsigned)((fa.ws.s_groups + kFW - 1) / kFW), (unsigned)U);
   hipLaunchKernelGGL(fused_sample_kernel<G>, gs, dim3(kFT), 0, s, fa);
-  hipLaunchKernelGGL(fused_tau_kernel, dim3(R), dim3(kSelThreads), 0, s, fa, G);
+  const size_t tau_lds = (size_t)fa.ws.s_groups * kGrp * kBlockTokens * 4;
+  hipLaunchKernelGGL(fused_tau_kernel, dim3(R), dim3(kSelThreads), tau_lds, s, fa, G);
   dim3 gf((unsigned)((fa.nb_cap + kRange - 1) / kRange), (unsigned)U);
   hipLaunchKernelGGL(fused_full_kernel<G>, gf, dim3(kFT), 0, s, fa);
   hipLaunchKernelGGL(fused_select_kernel<G>, dim3(R), dim3(kSelThreads), (size_t)kSelCap * 8, s, fa, idx, val);
@@ -761,7 +901,7 @@ fathom_status launch_scan_topk_fused(const uint64_t* planes, const uint16_t* sca
   fa.lo = lo;
   fa.tail = tail;
   fa.k = k;
-  fa.ws = fused_carve(ws, U * G, nb_cap, k);
+  fa.ws = fused_carve(ws, U * G, U, nb_cap, k);
   fa.st = st;
   switch (G) {
     case 1: return launch_fused_g<1>(fa, U, idx, val, s);

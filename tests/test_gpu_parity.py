@@ -450,15 +450,19 @@ def test_repeatable_bit_identical():
 
 @pytest.mark.parametrize("scale", [50.0, 0.01])
 def test_scan_topk_fallback_is_exact(scale):
-    """Force the fused path's fallback from the data: the threshold is estimated
-    from every 8th block; scaling exactly those blocks' keys up (threshold too
-    high -> too few survivors) or down (threshold too low -> survivor buffer
-    overflow) must still give the oracle's top-k, with TOPK_FALLBACK raised."""
+    """Force the fused path's fallback from the data.  The threshold is estimated
+    from every s-th group of 8 blocks (s = max(2, ceil(groups / 64))); scaling
+    exactly the sampled groups' keys up (threshold too high -> too few keys reach
+    it) or down (threshold too low -> survivor buffer overflow) must still give
+    the oracle's top-k, with TOPK_FALLBACK raised."""
     n, G, k = 65536, 4, 256
+    nb = n // 64
+    groups = (nb + 7) // 8
+    stride = max(2, -(-groups // 64))
     rng = np.random.default_rng(61)
     K = special_keys(rng, n)[None].copy()
-    for b in range(0, n // 64, 8):
-        K[0, 64 * b:64 * b + 64] *= np.float32(scale)
+    for g in range(0, groups, stride):
+        K[0, 512 * g:512 * g + 512] *= np.float32(scale)
     nt = torch.tensor([n], dtype=torch.int64, device=DEV)
     planes, scales = F.fathom_pack(torch.from_numpy(K).to(DEV), nt)
     q = rng.standard_normal((1, G, 128)).astype(np.float16)
