@@ -91,15 +91,15 @@ def main():
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus > 1 or world > 1:
         print(json.dumps({"error": "this build runs on one GPU only: --gpus must be 1 "
-                                   "(the path shards by KV head or session; see DESIGN.md)"}))
+                                   "(the path shards by KV head or session, one shard per GPU)"}))
         sys.exit(2)
     torch.cuda.set_device(0)
     dev = "cuda:0"
-    cfg = synth.CONFIGS[2]
+    cfg = synth.WORKLOADS["layer1m"]
     mode = {"waterfill": F.FATHOM_WATERFILL, "r16": F.FATHOM_UNIFORM_TOPR, "r32": F.FATHOM_UNIFORM_TOPR}[args.mode]
     B = {"waterfill": args.budget, "r16": 16, "r32": 32}[args.mode]
     k = cfg.k
-    log(f"[bench] generating config 2 inputs: 8 KV heads x n=2^20, G=4, mode={args.mode} B/r={B}, k={k}")
+    log(f"[bench] generating inputs: 8 KV heads x n=2^20, G=4, mode={args.mode} B/r={B}, k={k}")
     data = synth.device_units(cfg, with_values=True)
     K, V, q, var, n = data["K"], data["V"], data["q"], data["var"], data["n"]
     U, N, D = K.shape

@@ -15,9 +15,10 @@
  *                            attention over the selected set.
  *   App. A                   worked example (the main pin of the oracle).
  *
- * Arithmetic is fp64 unless a step is defined in fp32 by the reading listed in
- * the design doc (importance g in fp32, and the fp32 score replica).  Compile with
- * -O2 -ffp-contract=off so that no multiply-add is fused behind our back.
+ * Arithmetic is fp64 except two steps the paper leaves unspecified and this
+ * oracle fixes in fp32: the importance g (Eq. (g), summed over heads in fp32)
+ * and the fp32 score replica below.  Compile with -O2 -ffp-contract=off so
+ * that no multiply-add is fused behind our back.
  */
 #include <math.h>
 #include <stdint.h>
@@ -278,8 +279,8 @@ void orc_scores_f64(const uint64_t* planes, const uint16_t* scales, int64_t n, i
 }
 
 /* ------------------------------------------------------------------------- */
-/* fp32 score replica (the reading of the paper's silence on score precision  */
-/* and order listed in the design doc): per head and key, channels ascending,      */
+/* fp32 score replica (the paper states no score precision or order; this    */
+/* is the order the GPU path must reproduce): per head and key, channels asc, */
 /*   khat = (c^(t) + 1/2 - 2^(t-1)) * a16 * 2^(1-t)   (exact in fp32)         */
 /*   acc  = fmaf(q_hj, khat, acc),  acc starting at +0.                       */
 /* ------------------------------------------------------------------------- */

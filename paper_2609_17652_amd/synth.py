@@ -5,7 +5,7 @@ values, channel variances and ragged lengths, and is the one source of inputs
 shared by the HIP path and the CPU oracle.
 
 Per unit (one KV head of one sequence and layer), in this draw order from
-``numpy.random.default_rng(SeedSequence(seed, spawn_key=(cfg, session, layer, head)))``:
+``numpy.random.default_rng(SeedSequence(seed, spawn_key=(seed_key, session, layer, head)))``:
   1. sigma_c = exp(z_c), z_c ~ N(0, 1), c < 128   (log-normal channel scales)
   2. 4 outlier channels drawn without replacement; sigma_c *= 8 there
   3. queries q ~ N(0, 1), [G][D], stored fp32 or fp16
@@ -13,7 +13,7 @@ Per unit (one KV head of one sequence and layer), in this draw order from
 var_c = fp32(sigma_c^2) is the population variance of the generator (the
 calibration statistic of Sec. 3.3, given identically to both sides).
 
-Large configurations draw K and V on the GPU with torch's device generator,
+Large workloads draw K and V on the GPU with torch's device generator,
 seeded from the same tuple; the oracle always consumes copies of the device
 values, never a re-draw.
 """
@@ -30,7 +30,7 @@ D = 128
 @dataclasses.dataclass(frozen=True)
 class Config:
     name: str
-    cfg: int
+    seed_key: int            # first element of every seed tuple of this workload
     sessions: int
     layers: int
     kv_heads: int
@@ -49,21 +49,28 @@ class Config:
         return self.sessions * self.layers * self.kv_heads
 
 
-CONFIGS = {
-    0: Config("single head, n=4096", 0, 1, 1, 1, 1, 4096, None, "f32", (48,), (), 64),
-    1: Config("Qwen3-8B layer, n=131072", 1, 1, 1, 8, 4, 131072, None, "f16", (40, 48, 80), (), 1024),
-    2: Config("Qwen3-8B layer, n=1M", 2, 1, 1, 8, 4, 1 << 20, None, "f16", (48, 80), (16, 32), 2048),
-    3: Config("16 ragged sessions", 3, 16, 1, 8, 4, None, (65536, 524288), "f16", (40,), (), 1024),
-    4: Config("full decode step, 4 x 1M", 4, 4, 36, 8, 4, 1 << 20, None, "f16", (48,), (), 2048, 4, 32),
+# The five workloads, by what they are.  The seed key keeps every draw of one
+# workload independent of the others.
+WORKLOADS = {
+    "head4k": Config("single KV head, n=4096, fp32 query, B=48, k=64",
+                     0, 1, 1, 1, 1, 4096, None, "f32", (48,), (), 64),
+    "layer128k": Config("one Qwen3-8B layer, 8 KV heads x 4 query heads, n=131072, k=1024",
+                        1, 1, 1, 8, 4, 131072, None, "f16", (40, 48, 80), (), 1024),
+    "layer1m": Config("one Qwen3-8B layer, 8 KV heads x 4 query heads, n=2^20, k=2048",
+                      2, 1, 1, 8, 4, 1 << 20, None, "f16", (48, 80), (16, 32), 2048),
+    "ragged16": Config("16 resident sessions, ragged n in [65536, 524288], 8 KV heads x 4, B=40, k=1024",
+                       3, 16, 1, 8, 4, None, (65536, 524288), "f16", (40,), (), 1024),
+    "step4x1m": Config("full decode step: 4 sessions x 36 layers x 8 KV heads, n=2^20, B=48, k=2048, "
+                       "4 sink + 32 local", 4, 4, 36, 8, 4, 1 << 20, None, "f16", (48,), (), 2048, 4, 32),
 }
 
 
-def unit_rng(cfg: int, session: int, layer: int, head: int, seed: int = 0) -> np.random.Generator:
-    return np.random.default_rng(np.random.SeedSequence(seed, spawn_key=(cfg, session, layer, head)))
+def unit_rng(seed_key: int, session: int, layer: int, head: int, seed: int = 0) -> np.random.Generator:
+    return np.random.default_rng(np.random.SeedSequence(seed, spawn_key=(seed_key, session, layer, head)))
 
 
-def torch_seed(cfg: int, session: int, layer: int, head: int, stream: str, seed: int = 0) -> int:
-    h = hashlib.sha256(f"{seed}/{cfg}/{session}/{layer}/{head}/{stream}".encode()).digest()
+def torch_seed(seed_key: int, session: int, layer: int, head: int, stream: str, seed: int = 0) -> int:
+    h = hashlib.sha256(f"{seed}/{seed_key}/{session}/{layer}/{head}/{stream}".encode()).digest()
     return int.from_bytes(h[:8], "little") & ((1 << 63) - 1)
 
 
@@ -92,7 +99,7 @@ def values_host(rng: np.random.Generator, n: int) -> np.ndarray:
 
 def ragged_lengths(cfg: Config, seed: int = 0) -> np.ndarray:
     """Per-session lengths uniform in n_range (inclusive), one draw per session."""
-    rng = np.random.default_rng(np.random.SeedSequence(seed, spawn_key=(cfg.cfg, 10 ** 6)))
+    rng = np.random.default_rng(np.random.SeedSequence(seed, spawn_key=(cfg.seed_key, 10 ** 6)))
     lo, hi = cfg.n_range
     return rng.integers(lo, hi + 1, cfg.sessions).astype(np.int64)
 
@@ -132,7 +139,7 @@ def host_units(cfg: Config, units=None, n_override: int | None = None, seed: int
     q = np.zeros((len(sel), cfg.G, D), np.float16 if cfg.q_dtype == "f16" else np.float32)
     var = np.zeros((len(sel), D), np.float32)
     for a, i in enumerate(sel):
-        rng = unit_rng(cfg.cfg, *ids[i], seed=seed)
+        rng = unit_rng(cfg.seed_key, *ids[i], seed=seed)
         sig = channel_sigma(rng)
         var[a] = variance(sig)
         q[a] = queries(rng, cfg.G, cfg.q_dtype)
@@ -160,15 +167,15 @@ def device_units(cfg: Config, units=None, n_override: int | None = None, seed: i
     var = np.zeros((len(sel), D), np.float32)
     g = torch.Generator(device=device)
     for a, i in enumerate(sel):
-        rng = unit_rng(cfg.cfg, *ids[i], seed=seed)
+        rng = unit_rng(cfg.seed_key, *ids[i], seed=seed)
         sig = channel_sigma(rng)
         var[a] = variance(sig)
         q[a] = queries(rng, cfg.G, cfg.q_dtype)
-        g.manual_seed(torch_seed(cfg.cfg, *ids[i], "K", seed))
+        g.manual_seed(torch_seed(cfg.seed_key, *ids[i], "K", seed))
         sig_t = torch.from_numpy(sig.astype(np.float32)).to(device)
         K[a, :ns[a]] = (torch.randn((int(ns[a]), D), generator=g, device=device, dtype=torch.float32) * sig_t).to(kd)
         if with_values:
-            g.manual_seed(torch_seed(cfg.cfg, *ids[i], "V", seed))
+            g.manual_seed(torch_seed(cfg.seed_key, *ids[i], "V", seed))
             V[a, :ns[a]] = torch.randn((int(ns[a]), D), generator=g, device=device, dtype=torch.float32).half()
     return {
         "K": K, "V": V,

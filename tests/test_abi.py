@@ -116,16 +116,16 @@ def test_host_validation(fl):
 
 def test_synth_is_deterministic_and_shaped():
     from paper_2609_17652_amd import synth
-    cfg = synth.CONFIGS[0]
+    cfg = synth.WORKLOADS["head4k"]
     a = synth.host_units(cfg)
     b = synth.host_units(cfg)
     assert np.array_equal(a.K, b.K) and np.array_equal(a.q, b.q) and np.array_equal(a.var, b.var)
     assert a.K.shape == (1, 4096, 128) and a.q.shape == (1, 1, 128) and a.q.dtype == np.float32
-    c1 = synth.CONFIGS[1]
+    c1 = synth.WORKLOADS["layer128k"]
     h = synth.host_units(c1, units=[0, 1], n_override=256)
     assert h.q.dtype == np.float16 and h.q.shape == (2, 4, 128)
     assert not np.array_equal(h.K[0], h.K[1])
-    n3 = synth.unit_lengths(synth.CONFIGS[3])
+    n3 = synth.unit_lengths(synth.WORKLOADS["ragged16"])
     assert n3.shape == (128,) and n3.min() >= 65536 and n3.max() <= 524288
     assert (n3.reshape(16, 8) == n3.reshape(16, 8)[:, :1]).all()  # one length per session
     # 4 outlier channels at 8x

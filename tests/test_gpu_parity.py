@@ -291,7 +291,7 @@ def test_sparse_attn(qdt):
             assert (np.abs(out[u] - ref) <= tol).all(), (u, nsk, float(np.abs(out[u] - ref).max()))
 
 
-# ---------------------------------------------------------------------- configurations
+# ---------------------------------------------------------------------- workloads
 def _pipeline(K, nt, q, var, B, k, lo=0, tail=0, mode=F.FATHOM_WATERFILL):
     st = F.new_status()
     planes, scales = F.fathom_pack(K, nt, dev_status=st)
@@ -300,9 +300,9 @@ def _pipeline(K, nt, q, var, B, k, lo=0, tail=0, mode=F.FATHOM_WATERFILL):
     return planes, scales, d, th, idx, val, st
 
 
-def test_config0_end_to_end():
+def test_head4k_end_to_end():
     """Single KV head, n = 4096, fp32 query, B = 48, k = 64: every stage bit-exact."""
-    cfg = synth.CONFIGS[0]
+    cfg = synth.WORKLOADS["head4k"]
     h = synth.host_units(cfg)
     K, q, var = torch.from_numpy(h.K).to(DEV), torch.from_numpy(h.q).to(DEV), torch.from_numpy(h.var).to(DEV)
     nt = torch.from_numpy(h.n).to(DEV)
@@ -324,11 +324,12 @@ def test_config0_end_to_end():
     assert (np.abs(out.cpu().numpy()[0] - oo) <= tol).all()
 
 
-@pytest.mark.parametrize("cfg_id", [1, 2])
-def test_config_full_size_sampled(cfg_id):
-    """Configs 1 (n = 131072) and 2 (n = 2^20): all 8 KV heads in one launch, as
-    timed by the bench; oracle on sampled units / blocks, every budget and mode."""
-    cfg = synth.CONFIGS[cfg_id]
+@pytest.mark.parametrize("name", ["layer128k", "layer1m"])
+def test_layer_full_size_sampled(name):
+    """One Qwen3-8B layer at n = 131072 and at n = 2^20: all 8 KV heads in one
+    launch, as timed by the bench; oracle on sampled units / blocks, every budget
+    and mode."""
+    cfg = synth.WORKLOADS[name]
     data = synth.device_units(cfg, with_values=True)
     K, q, var, nt = data["K"], data["q"], data["var"], data["n"]
     n = int(data["n_host"][0])
@@ -370,16 +371,16 @@ def test_config_full_size_sampled(cfg_id):
         oo = oracle.sparse_attn(qh[su], Kh, Vh, ix, 0, 0, 1 / np.sqrt(128))
         tol = _attn_tol(qh[su], Kh, Vh, ix, 0, 0, np.float32(1 / np.sqrt(128)))
         assert (np.abs(out.cpu().numpy()[0] - oo) <= tol).all()
-        if cfg_id == 2:
+        if name == "layer1m":
             break  # the full-size run checks one budget end to end; depths for all modes above
     del data, K, planes, scales
     torch.cuda.empty_cache()
 
 
-def test_config3_ragged_sessions():
+def test_ragged_sessions():
     """16 sessions with ragged n in [65536, 524288], 8 KV heads each, B = 40, k = 1024,
     one batched launch over all 128 units; oracle on the shortest and longest units."""
-    cfg = synth.CONFIGS[3]
+    cfg = synth.WORKLOADS["ragged16"]
     data = synth.device_units(cfg, with_values=False)
     K, q, var, nt, nh = data["K"], data["q"], data["var"], data["n"], data["n_host"]
     st = F.new_status()
@@ -402,10 +403,10 @@ def test_config3_ragged_sessions():
     torch.cuda.empty_cache()
 
 
-def test_config4_layer_protocol():
+def test_decode_step_layer_protocol():
     """One layer of the full decode step: 4 sessions x 8 KV heads at n = 2^20, B = 48,
     sink 4 + local 32 + top-(2048 - 36); oracle on one sampled unit."""
-    cfg = synth.CONFIGS[4]
+    cfg = synth.WORKLOADS["step4x1m"]
     units = [s * cfg.layers * cfg.kv_heads + h for s in range(cfg.sessions) for h in range(cfg.kv_heads)]
     data = synth.device_units(cfg, units=units, with_values=True)
     K, q, var, nt = data["K"], data["q"], data["var"], data["n"]
@@ -479,9 +480,9 @@ def test_scan_topk_fallback_is_exact(scale):
         assert np.array_equal(val[0, h].cpu().numpy(), ov), h
 
 
-def test_scan_topk_no_fallback_on_config_data():
+def test_scan_topk_no_fallback_on_workload_data():
     """On the synthetic workloads the sampled threshold never needs the fallback."""
-    cfg = synth.CONFIGS[1]
+    cfg = synth.WORKLOADS["layer128k"]
     data = synth.device_units(cfg, with_values=False)
     st = F.new_status()
     planes, scales = F.fathom_pack(data["K"], data["n"], dev_status=st)
