@@ -144,7 +144,6 @@ fathom_status fathom_scan_topk(const uint64_t* planes, const uint16_t* scales, c
   if (e != FATHOM_OK) return e;
   if (lo < 0 || tail < 0 || k < 1) return FATHOM_ERR_INVALID;
   if (k > FATHOM_MAX_K) return FATHOM_ERR_UNSUPPORTED;
-  if (nb_cap >= ((int64_t)1 << 20)) return FATHOM_ERR_UNSUPPORTED;  // plane-row offsets are 32-bit
   if (U == 0) return FATHOM_OK;
   if (!idx || !ws || !aligned(idx, 4) || (val && !aligned(val, 4)) || !aligned(ws, 256)) return FATHOM_ERR_INVALID;
   if (ws_bytes < scan_topk_ws(U, G, nb_cap * 64, k)) return FATHOM_ERR_WORKSPACE;

@@ -21,7 +21,9 @@ constexpr int kD = 128;           // supported head dimension
   } while (0)
 
 __device__ __forceinline__ void set_status(uint32_t* st, uint32_t bits) {
-  if (st && bits) atomicOr(st, bits);
+  if (st && bits)
+    __hip_atomic_fetch_or((__attribute__((address_space(1))) uint32_t*)st, bits, __ATOMIC_RELAXED,
+                          __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // n[u] clamped to [0, cap]; raises BAD_N and returns 0 for out-of-range values.
@@ -56,9 +58,12 @@ __device__ __forceinline__ float half_bits_to_float(uint16_t h) {
   return __half2float(__ushort_as_half(h));
 }
 
+// Query element i (fp16 converts to fp32 exactly), read through the global
+// address space so it never counts against the LDS wait counter.
 __device__ __forceinline__ float load_q(const void* q, fathom_dtype qdt, int64_t i) {
-  if (qdt == FATHOM_F16) return __half2float(reinterpret_cast<const __half*>(q)[i]);
-  return reinterpret_cast<const float*>(q)[i];
+  if (qdt == FATHOM_F16)
+    return __half2float(__ushort_as_half(((const __attribute__((address_space(1))) uint16_t*)q)[i]));
+  return ((const __attribute__((address_space(1))) float*)q)[i];
 }
 
 // Order-preserving map fp32 -> uint32: larger score -> larger key; -0 == +0;

@@ -4,22 +4,33 @@
 // The exact result is defined by the documented fp32 scores (exact
 // dequantisation, fma(q, khat, acc) over active channels ascending) and the
 // (score desc, index asc) order.  To avoid computing those scores for every
-// key, each key first gets a cheap proxy with a rigorous error bound:
-//   score = sum_j (w_j / 2) z'_j,  w_j = q_hj a16_bj / 8,
-//   z'_j  = 2 (c^(t) - 2^(t-1)) 2^(4-t) + 2^(4-t)   (odd multiple, |z'| <= 15),
-//   proxy = (delta / 2) sum_j w8_j z'_j  with w8_j = rne(w_j / delta) in int8,
-//   delta = a power of two per (block, head), so the proxy is exact in fp32;
-//   |score - proxy| <= E = sum_j |w_j - delta w8_j| max|z'_j| / 2 (+ slack for
-//   the fp32 rounding of the exact scores).
-// Per lane (= key), z' of 4 channels is one dword built from the plane words
-// with one EXEC-masked OR per plane bit (the word is the lane mask), and one
-// v_dot4_i32_i8 per head folds it in.  Keys whose bound reaches the row's
-// threshold tau are re-scored exactly; those with score >= tau are kept.
+// key, each key first gets a cheap integer proxy with a rigorous error bound.
+// With khat = z' a16 / 16, where
+//   z' = 2 (c^(t) - 2^(t-1)) 2^(4-t) + 2^(4-t)   (an odd multiple, |z'| <= 15),
+// the score is sum_j (w_j / 2) z'_j with w_j = q_hj a16_bj / 8.  Per block and
+// head, delta is a power of two with max|w| / delta < 128 and w8_j = rne(w_j /
+// delta) in int8; the proxy is (delta / 2) sum_j w8_j z'_j, exact in fp32, and
+//   |score - proxy| <= E = (sum_j |w_j - delta w8_j| zmax_j / 2
+//                           + A 2^-21 sum_j |w_j|) (1 + 2^-10),
+// the second term covering the fp32 rounding of the documented score.
 //
-// Passes: (1) proxies of a strided sample of blocks; (2) per row, tau = a rank
-// statistic of the sample chosen so that ~1.25 k keys are expected above it; (3) full proxy pass + exact re-scoring of the survivors;
-// (4) per row, the k best survivors in order.  If fewer than k keys reach tau
-// (or the survivor buffer overflows), pass (4) recomputes the row exactly on
+// Bits to proxy digits.  z'_j = U_j + 2^(4-t_j) - 16 with U_j = sum_{p<t}
+// b_p 2^(4-p) built from the plane bits b_p.  A wave holds 64 keys of a block
+// (lane = key).  The plane words of a group of 8 blocks are staged in LDS,
+// each 32-bit half rotated left by the bit position q = 8K + 4 - p its plane
+// takes in the U dword (byte K = channel K of 4).  Lane s then gathers bit s of
+// every row with one v_and_or_b32 against the per-lane mask
+// 1 << ((s + q) mod 32), building U rotated left by s; one v_alignbit_b32
+// rotates it back.  The constant parts go into a per-(block, head) bias, and
+// v_dot4_i32_i8 folds 4 channels per head into an int32 accumulator.
+//
+// Passes: (1) proxies of a strided sample of 8-block groups; (2) per row, tau =
+// a rank statistic of the sample chosen so that ~1.25 k keys are expected
+// above it; (3) the full proxy pass: keys whose proxy + E reaches tau are
+// queued per wave and re-scored exactly (their plane lines are still in L2);
+// those with score >= tau are appended to the row's survivor list; (4) per
+// row, the survivors are sorted and the first k written.  If fewer than k
+// reach tau (or the list overflows), pass (4) recomputes the row exactly on
 // its own (FATHOM_DEV_TOPK_FALLBACK).  The result never depends on tau.
 #include "common.hpp"
 
@@ -27,35 +38,32 @@ namespace fathom {
 
 constexpr int kFT = 256;          // threads per workgroup (4 waves)
 constexpr int kFW = kFT / kWave;
-constexpr int kGrp = 8;           // consecutive blocks per wave step: one 64-byte line per plane row
-constexpr int kSub = kFW * kGrp;  // 32 blocks per weight-setup sub-tile
-constexpr int kRange = 4 * kSub;  // 128 blocks per workgroup in the full pass
-constexpr int kFlush = 256;       // re-score when this many survivors are queued
-constexpr int kQueue = kFlush + kSub * kBlockTokens;
-constexpr int kMaxDw = kD / 4;    // z' dwords for 128 active channels
-constexpr int kMaxCells = kD * kPlanes;
+constexpr int kGrp = 8;           // blocks per group (one wave step)
+constexpr int kChunkRows = 64;    // plane rows staged per chunk (padded)
+constexpr int kStageK = kChunkRows / 8;  // rows loaded per lane per chunk (8 lanes per row)
+constexpr int kChunkDw = 16;      // U dwords per chunk (a full dword has >= 4 rows)
+constexpr int kMaxDw = kD / 4;
+constexpr int kGroupsPerWave = 4; // full pass: groups per wave, interleaved across the workgroup
+constexpr int kGroupsPerWG = kFW * kGroupsPerWave;
+constexpr int kWGQ = 512;        // full pass: candidate keys a workgroup gathers in LDS before writing
+constexpr int kWGCap = 2048;     // candidate keys per full-pass workgroup (more: exact fallback)
+constexpr int kRsT = 256;        // re-scoring threads per workgroup
+constexpr int kSlots = 8;        // survivor sub-lists per row (spreads the append counters)
 constexpr int kSampleGroups = 64; // at most this many sampled groups (512 blocks) per row
 constexpr int kSelThreads = 1024;
 constexpr int kSelCap = 16384;    // LDS composites in the select kernel
 constexpr float kNegInf = -__builtin_huge_valf();
 
-// Per-unit read plan, built once per call: byte offsets (from the unit's plane
-// base) of the plane rows the proxy reads, in active-channel order.
-struct Plan {
-  uint32_t off[kD][4];       // rows of planes 0..3 of active channel a; planes >= t repeat plane t-1
-  uint32_t cell[kMaxCells];  // rows of every plane read (p < t), for the L2 prefetch
-  uint32_t tpack[kMaxDw];    // depth of channel 4d+k in byte k
-  uint32_t zinit[kMaxDw];    // 2^(4-t) in byte k: the constant part of z'
-  int32_t A, ncells, pad[62];
-};
-
 struct FusedWs {
   float* tau;       // [R] threshold on exact scores (-inf: every eligible key is kept)
-  uint32_t* cnt;    // [R] survivors appended
-  uint64_t* cand;   // [R][cap] composites (score_key << 32 | ~index)
+  uint32_t* cnt;    // [R][kSlots] survivors appended to sub-list s
+  uint64_t* cand;   // [R][kSlots][scap] survivors: score_key << 32 | ~index
+  uint32_t* ecnt;   // [U][nwg] candidate keys found by full-pass workgroup w (> kWGCap: overflow)
+  uint32_t* ent;    // [U][nwg][kWGCap] key offset from the workgroup's first block | head mask << 16
+  uint32_t* uovf;   // [U] a workgroup of the unit overflowed its list: exact fallback for the unit
+  int64_t nwg;      // full-pass workgroups per unit
   float* sample;    // [R][s_groups * 512] proxies of sampled keys
-  Plan* plan;       // [U]
-  int cap;
+  int cap, scap;  // survivors per row (select kernel), per sub-list
   int64_t s_gstride;  // sample every s_gstride-th group of 8 blocks
   int64_t s_groups;   // sampled groups per row
 };
@@ -75,24 +83,39 @@ static inline void fused_geometry(int64_t nb_cap, int64_t* gstride, int64_t* sgr
   *sgroups = (ng + s - 1) / s;
 }
 
+static inline int fused_scap(int k) { return fused_cap(k) / 4; }
+
+static inline int64_t fused_nwg(int64_t nb_cap) {
+  const int64_t ng = (nb_cap + kGrp - 1) / kGrp;
+  return (ng + kGroupsPerWG - 1) / kGroupsPerWG;
+}
+
 size_t fused_ws_bytes(int R, int U, int64_t nb_cap, int k) {
   int64_t s, sg;
-  fused_geometry(nb_cap > 0 ? nb_cap : 1, &s, &sg);
-  return a256((size_t)R * 4) + a256((size_t)R * 4) + a256((size_t)R * fused_cap(k) * 8) +
-         a256((size_t)R * sg * kGrp * kBlockTokens * 4) + a256((size_t)U * sizeof(Plan));
+  if (nb_cap < 1) nb_cap = 1;
+  fused_geometry(nb_cap, &s, &sg);
+  const size_t nw = (size_t)U * fused_nwg(nb_cap);
+  return a256((size_t)R * 4) + a256((size_t)R * kSlots * 4) + a256((size_t)R * kSlots * fused_scap(k) * 8) +
+         a256(nw * 4) +
+         a256(nw * kWGCap * 4) + a256((size_t)U * 4) + a256((size_t)R * sg * kGrp * kBlockTokens * 4);
 }
 
 static FusedWs fused_carve(void* ws, int R, int U, int64_t nb_cap, int k) {
   FusedWs w;
-  fused_geometry(nb_cap > 0 ? nb_cap : 1, &w.s_gstride, &w.s_groups);
+  if (nb_cap < 1) nb_cap = 1;
+  fused_geometry(nb_cap, &w.s_gstride, &w.s_groups);
   w.cap = fused_cap(k);
+  w.scap = fused_scap(k);
+  w.nwg = fused_nwg(nb_cap);
+  const size_t nw = (size_t)U * w.nwg;
   char* p = reinterpret_cast<char*>(ws);
   w.tau = reinterpret_cast<float*>(p); p += a256((size_t)R * 4);
-  w.cnt = reinterpret_cast<uint32_t*>(p); p += a256((size_t)R * 4);
-  w.cand = reinterpret_cast<uint64_t*>(p); p += a256((size_t)R * w.cap * 8);
-  w.sample = reinterpret_cast<float*>(p); p += a256((size_t)R * w.s_groups * kGrp * kBlockTokens * 4);
-  w.plan = reinterpret_cast<Plan*>(p);
-  (void)U;
+  w.cnt = reinterpret_cast<uint32_t*>(p); p += a256((size_t)R * kSlots * 4);
+  w.cand = reinterpret_cast<uint64_t*>(p); p += a256((size_t)R * kSlots * w.scap * 8);
+  w.ecnt = reinterpret_cast<uint32_t*>(p); p += a256(nw * 4);
+  w.ent = reinterpret_cast<uint32_t*>(p); p += a256(nw * kWGCap * 4);
+  w.uovf = reinterpret_cast<uint32_t*>(p); p += a256((size_t)U * 4);
+  w.sample = reinterpret_cast<float*>(p);
   return w;
 }
 
@@ -110,381 +133,76 @@ struct FusedArgs {
   uint32_t* st;
 };
 
+// Per-unit plan, shared by the waves of a workgroup.  Proxy channel order:
+// depth descending, channel ascending (the integer proxy does not depend on
+// the order; the exact scores use channel order ascending).  The plane rows of
+// each U dword (4 channels) are listed channel by channel, plane by plane, and
+// padded with zero rows to a multiple of 4.
+constexpr uint32_t kPadRow = 0xFFFFFFFFu;
 template <int G>
-struct FusedSmem {
-  int act[kD];                      // j | (t << 8), active channels ascending
-  float qa[kD][G];                  // fp32 query of active channel a, head h
-  uint32_t w8[kSub][kMaxDw][G];     // packed int8 weights
-  float hdelta[kSub][G];            // delta / 2
-  float ebound[kSub][G];            // error bound (inf: no bound, every key survives)
+struct alignas(16) UnitLds {
+  int act[kD];                    // j | t << 8
+  int pidx[kD];                   // proxy index of the x-th active channel in channel order
+  float qa[kD][G];                // q_hj (fp32) of active channel a
+  float qa8[kD][G];               // q_hj / 8
+  float zmx[kD];                  // 16 - 2^(4-t): the largest |z'| of channel a
+  uint32_t rrow[kD * kPlanes];    // padded row r: plane-row index 4j+p, or kPadRow
+  uint32_t rsh[kD * kPlanes];     // padded row r: (32 - q) mod 32, q = 8K + 4 - p its bit in the U dword
+  uint32_t tpk[kMaxDw];           // depths of channels 4d..4d+3, byte K
+  uint32_t drow[kMaxDw];          // first padded row of dword d, relative to its chunk
+  uint32_t dnq[kMaxDw];           // row quads of dword d
+  int dch[kMaxDw];                // chunk of dword d
+  int chd[kMaxDw + 1];            // chunk c = dwords [chd[c], chd[c+1])
+  int chr[kMaxDw + 1];            // first padded row of chunk c
+  int cnt[2][5];
+  int A, nch;
   float tau[G];
-  uint32_t queue[kQueue];
-  int nact;
-  int qcount;
+};
+
+// Per-wave staging and per-(block, head) state.
+template <int G4>
+struct alignas(16) WaveLds {
+  uint32_t rows[kChunkRows][2][kGrp];  // [row][32-bit half][block], rotated
+  uint16_t scl[kChunkRows][kGrp];      // fp16 scales of the chunk's channels
+  uint32_t w8[kGrp][kChunkDw][G4];     // packed int8 weights
+  float sdel[kGrp][8];                 // delta (0: no usable bound)
+  float sinv[kGrp][8];                 // 1 / delta
+  float seb[kGrp][8];                  // sum |w - delta w8| zmax
+  float ssw[kGrp][8];                  // sum |w|
+  int sbias[kGrp][8];                  // sum w8 (2^(4-t) - 16)
+  int sthr[kGrp][8];                   // full pass: candidate iff acc >= sthr
 };
 
 __device__ __forceinline__ uint64_t lanemask_lt(int lane) { return lane == 0 ? 0ull : (~0ull >> (64 - lane)); }
 
-// Wave-uniform reads through the constant address space are scalar (SMEM)
-// loads straight into SGPRs.  Neither the store nor the plan is written while
-// a scan runs.
-struct Words8 {
-  uint64_t w[kGrp];
-};
-typedef __attribute__((address_space(4))) const uint64_t cu64;
-typedef __attribute__((address_space(4))) const uint32_t cu32;
-typedef __attribute__((ext_vector_type(4))) unsigned int v4u;
-typedef __attribute__((address_space(4))) const v4u cu4;
-typedef __attribute__((ext_vector_type(16))) unsigned int v16u;
-typedef __attribute__((address_space(4))) const v16u cv16;
-__device__ __forceinline__ uint64_t sload64(const void* p) { return *(cu64*)(p); }
-__device__ __forceinline__ uint32_t sload32(const void* p) { return *(cu32*)(p); }
-__device__ __forceinline__ v4u sload128(const void* p) { return *(cu4*)(p); }
-__device__ __forceinline__ const char* uniform_ptr(const char* p) {
-  const uint64_t v = reinterpret_cast<uint64_t>(p);
-  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
-  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
-  return reinterpret_cast<const char*>(((uint64_t)hi << 32) | lo);
+// Orders this wave's LDS writes before its later LDS reads (other lanes).
+__device__ __forceinline__ void wave_lds_sync() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+
+__device__ __forceinline__ int uni(int v) { return __builtin_amdgcn_readfirstlane(v); }
+
+// Global-memory accesses through the global address space: the pointers live
+// in a by-value argument struct, and generic (flat) accesses would also count
+// against the LDS wait counter, making every LDS wait wait for HBM loads.
+template <typename T>
+__device__ __forceinline__ T gload(const T* p) {
+  return *(const __attribute__((address_space(1))) T*)p;
 }
-// The plane words of the 8 blocks of a group from one row; a group that runs
-// past nb_cap (the last one, when nb_cap % 8 != 0) reads only words inside it.
-template <bool FULL>
-__device__ __forceinline__ Words8 sload_words(const char* row, int64_t nleft) {
-  row = uniform_ptr(row);
-  Words8 w;
-  if constexpr (FULL) {
-    const v16u v = *(cv16*)(row);
-#pragma unroll
-    for (int g = 0; g < kGrp; ++g) w.w[g] = ((uint64_t)v[2 * g + 1] << 32) | v[2 * g];
-  } else {
-#pragma unroll
-    for (int g = 0; g < kGrp; ++g) {
-      w.w[g] = 0ull;
-      if (g < nleft) w.w[g] = sload64(row + 8 * g);
-    }
-  }
-  return w;
+template <typename T>
+__device__ __forceinline__ void gstore(T* p, T v) {
+  *(__attribute__((address_space(1))) T*)p = v;
+}
+__device__ __forceinline__ uint32_t gatomic_add(uint32_t* p, uint32_t v) {
+  return __hip_atomic_fetch_add((__attribute__((address_space(1))) uint32_t*)p, v,
+                                __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// One plane of one channel (byte K of the z' dword) for the 8 blocks of a
-// group: lanes whose key has the bit set (the plane word is the lane mask)
-// OR in the plane's value; the sign plane ORs 0xF0 where the bit is clear.
-// EXEC is saved and restored inside the statement; SCC is clobbered (the
-// compiler must not keep a carry or compare result live across it).
-template <int K, int P>
-__device__ __forceinline__ void or_plane(uint32_t (&z)[kGrp], const Words8& w) {
-  uint64_t sv;
-  constexpr uint32_t c = P == 0 ? (0xF0u << (8 * K)) : ((8u >> (P > 0 ? P - 1 : 0)) << (8 * K));
-  if (P == 0) {
-    asm volatile(
-        "s_mov_b64 %8, exec\n\t"
-        "s_andn2_b64 exec, %8, %9\n\tv_or_b32 %0, %17, %0\n\t"
-        "s_andn2_b64 exec, %8, %10\n\tv_or_b32 %1, %17, %1\n\t"
-        "s_andn2_b64 exec, %8, %11\n\tv_or_b32 %2, %17, %2\n\t"
-        "s_andn2_b64 exec, %8, %12\n\tv_or_b32 %3, %17, %3\n\t"
-        "s_andn2_b64 exec, %8, %13\n\tv_or_b32 %4, %17, %4\n\t"
-        "s_andn2_b64 exec, %8, %14\n\tv_or_b32 %5, %17, %5\n\t"
-        "s_andn2_b64 exec, %8, %15\n\tv_or_b32 %6, %17, %6\n\t"
-        "s_andn2_b64 exec, %8, %16\n\tv_or_b32 %7, %17, %7\n\t"
-        "s_mov_b64 exec, %8"
-        : "+v"(z[0]), "+v"(z[1]), "+v"(z[2]), "+v"(z[3]), "+v"(z[4]), "+v"(z[5]), "+v"(z[6]), "+v"(z[7]),
-          "=&s"(sv)
-        : "s"(w.w[0]), "s"(w.w[1]), "s"(w.w[2]), "s"(w.w[3]), "s"(w.w[4]), "s"(w.w[5]), "s"(w.w[6]), "s"(w.w[7]),
-          "i"(c)
-        : "scc");
-  } else {
-    asm volatile(
-        "s_mov_b64 %8, exec\n\t"
-        "s_and_b64 exec, %8, %9\n\tv_or_b32 %0, %17, %0\n\t"
-        "s_and_b64 exec, %8, %10\n\tv_or_b32 %1, %17, %1\n\t"
-        "s_and_b64 exec, %8, %11\n\tv_or_b32 %2, %17, %2\n\t"
-        "s_and_b64 exec, %8, %12\n\tv_or_b32 %3, %17, %3\n\t"
-        "s_and_b64 exec, %8, %13\n\tv_or_b32 %4, %17, %4\n\t"
-        "s_and_b64 exec, %8, %14\n\tv_or_b32 %5, %17, %5\n\t"
-        "s_and_b64 exec, %8, %15\n\tv_or_b32 %6, %17, %6\n\t"
-        "s_and_b64 exec, %8, %16\n\tv_or_b32 %7, %17, %7\n\t"
-        "s_mov_b64 exec, %8"
-        : "+v"(z[0]), "+v"(z[1]), "+v"(z[2]), "+v"(z[3]), "+v"(z[4]), "+v"(z[5]), "+v"(z[6]), "+v"(z[7]),
-          "=&s"(sv)
-        : "s"(w.w[0]), "s"(w.w[1]), "s"(w.w[2]), "s"(w.w[3]), "s"(w.w[4]), "s"(w.w[5]), "s"(w.w[6]), "s"(w.w[7]),
-          "i"(c)
-        : "scc");
-  }
-}
-
-// z' byte K of one channel for a group: its t plane rows (the plan repeats row
-// t-1 for planes >= t, so the four loads are unconditional and hit one line).
-template <int K, bool FULL>
-__device__ __forceinline__ void gather_channel(uint32_t (&z)[kGrp], int t, const char* base, const Plan* plan,
-                                               int a, int64_t nleft) {
-  const v4u o = sload128(&plan->off[a][0]);
-  {
-    const Words8 w0 = sload_words<FULL>(base + o.x, nleft);
-    const Words8 w1 = sload_words<FULL>(base + o.y, nleft);  // row of plane 0 again when t == 1
-    or_plane<K, 0>(z, w0);
-    if (t > 1) or_plane<K, 1>(z, w1);
-  }
-  if (t > 2) {
-    const Words8 w2 = sload_words<FULL>(base + o.z, nleft);
-    const Words8 w3 = sload_words<FULL>(base + o.w, nleft);
-    or_plane<K, 2>(z, w2);
-    if (t > 3) or_plane<K, 3>(z, w3);
-  }
-}
-
-// ---------------------------------------------------------------- plan
-// One workgroup of 128 threads per unit.
-__global__ __launch_bounds__(kD) void fused_plan_kernel(FusedArgs a) {
-  __shared__ int act[kD];
-  __shared__ int wc[2];
-  __shared__ int cstart[kD + 1];
-  const int u = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  Plan* pl = a.ws.plan + u;
-  int t = a.depths[(int64_t)u * kD + tid];
-  t = t > kPlanes ? kPlanes : t;
-  const bool on = t > 0;
-  const uint64_t m = __ballot(on);
-  if (lane == 0) wc[wave] = __popcll(m);
-  __syncthreads();
-  if (on) act[(wave == 1 ? wc[0] : 0) + __popcll(m & lanemask_lt(lane))] = tid | (t << 8);
-  const int A = wc[0] + wc[1];
-  __syncthreads();
-  const uint32_t rowb = (uint32_t)(a.nb_cap * 8);  // bytes per plane row
-  if (tid < A) {
-    const int j = act[tid] & 0xFF, tt = act[tid] >> 8;
-#pragma unroll
-    for (int p = 0; p < 4; ++p) pl->off[tid][p] = (uint32_t)(j * kPlanes + (p < tt ? p : tt - 1)) * rowb;
-  } else {
-#pragma unroll
-    for (int p = 0; p < 4; ++p) pl->off[tid][p] = 0u;  // row 0 of the unit: valid, never ORed
-  }
-  // prefix of depths for the cell list
-  if (tid == 0) {
-    int c = 0;
-    for (int x = 0; x < A; ++x) {
-      cstart[x] = c;
-      c += act[x] >> 8;
-    }
-    cstart[A] = c;
-    pl->A = A;
-    pl->ncells = c;
-  }
-  __syncthreads();
-  if (tid < A) {
-    const int j = act[tid] & 0xFF, tt = act[tid] >> 8;
-    for (int p = 0; p < tt; ++p) pl->cell[cstart[tid] + p] = (uint32_t)(j * kPlanes + p) * rowb;
-  }
-  if (tid < kMaxDw) {
-    uint32_t tp = 0u, zi = 0u;
-    for (int k2 = 0; k2 < 4; ++k2) {
-      const int x = 4 * tid + k2;
-      if (x < A) {
-        const int tt = act[x] >> 8;
-        tp |= (uint32_t)tt << (8 * k2);
-        zi |= (8u >> (tt - 1)) << (8 * k2);
-      }
-    }
-    pl->tpack[tid] = tp;
-    pl->zinit[tid] = zi;
-  }
-}
-
-// Unit-level LDS setup: active channels and fp32 queries per active channel.
-template <int G>
-__device__ void unit_setup(FusedSmem<G>& sm, const FusedArgs& a, int u) {
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  __shared__ int wc[2];
-  int t = 0;
-  if (tid < kD) {
-    t = a.depths[(int64_t)u * kD + tid];
-    t = t > kPlanes ? kPlanes : t;
-  }
-  const bool on = tid < kD && t > 0;
-  const uint64_t m = __ballot(on);
-  if (tid < kD && lane == 0) wc[wave] = __popcll(m);
-  __syncthreads();
-  if (on) sm.act[(wave == 1 ? wc[0] : 0) + __popcll(m & lanemask_lt(lane))] = tid | (t << 8);
-  if (tid == 0) {
-    sm.nact = wc[0] + wc[1];
-    sm.qcount = 0;
-  }
-  __syncthreads();
-  const int A = sm.nact;
-  for (int x = tid; x < A * G; x += kFT) {
-    const int ai = x / G, h = x % G;
-    const int j = sm.act[ai] & 0xFF;
-    sm.qa[ai][h] = load_q(a.q, a.qdt, ((int64_t)u * G + h) * kD + j);
-  }
-  __syncthreads();
-}
-
-// Weights of the kSub blocks of a sub-tile (block indices from blk_of; -1 or
-// >= nbu: unused): 8 threads per block, each owning whole dwords of 4 channels.
-template <int G, typename BlkOf>
-__device__ void weight_setup(FusedSmem<G>& sm, const FusedArgs& a, int u, int64_t nbu, BlkOf blk_of) {
-  constexpr int TPB = kFT / kSub;  // threads per block
-  const int tid = threadIdx.x;
-  const int blk = tid / TPB, sl = tid % TPB;
-  const int A = sm.nact, AD = (A + 3) >> 2;
-  const int64_t b = blk_of(blk);
-  const bool valid = b >= 0 && b < nbu;
-  const uint16_t* Su = a.scales + (int64_t)u * kD * a.nb_cap;
-  float mx[G];
-#pragma unroll
-  for (int h = 0; h < G; ++h) mx[h] = 0.0f;
-  bool finite = true;
-  if (valid) {
-    for (int d = sl; d < AD; d += TPB) {
-      for (int k = 0; k < 4; ++k) {
-        const int ai = 4 * d + k;
-        if (ai >= A) break;
-        const int j = sm.act[ai] & 0xFF;
-        const float af = half_bits_to_float(Su[(int64_t)j * a.nb_cap + b]);
-#pragma unroll
-        for (int h = 0; h < G; ++h) {
-          const float w = __fmul_rn(__fmul_rn(sm.qa[ai][h], af), 0.125f);
-          if (!(fabsf(w) <= 3.402823466e38f)) finite = false;
-          mx[h] = fmaxf(mx[h], fabsf(w));
-        }
-      }
-    }
-  }
-#pragma unroll
-  for (int h = 0; h < G; ++h)
-#pragma unroll
-    for (int o = TPB / 2; o >= 1; o >>= 1) mx[h] = fmaxf(mx[h], __shfl_xor(mx[h], o, TPB));
-  int fin = finite ? 1 : 0;
-#pragma unroll
-  for (int o = TPB / 2; o >= 1; o >>= 1) fin &= __shfl_xor(fin, o, TPB);
-  float delta[G], inv[G];
-  bool ok[G];
-#pragma unroll
-  for (int h = 0; h < G; ++h) {
-    int e;
-    (void)frexpf(mx[h], &e);  // mx in [2^(e-1), 2^e)
-    ok[h] = fin && (mx[h] >= 0x1p-100f || mx[h] == 0.0f);
-    const int ee = e < -100 ? -100 : e;
-    delta[h] = ldexpf(1.0f, ee - 7);  // |w| / delta < 128
-    inv[h] = ldexpf(1.0f, 7 - ee);
-  }
-  float eb[G];
-#pragma unroll
-  for (int h = 0; h < G; ++h) eb[h] = 0.0f;
-  if (valid) {
-    for (int d = sl; d < AD; d += TPB) {
-      uint32_t pk[G];
-#pragma unroll
-      for (int h = 0; h < G; ++h) pk[h] = 0u;
-      for (int k = 0; k < 4; ++k) {
-        const int ai = 4 * d + k;
-        if (ai >= A) break;
-        const int j = sm.act[ai] & 0xFF, t = sm.act[ai] >> 8;
-        const float zmax = t == 4 ? 15.0f : t == 3 ? 14.0f : t == 2 ? 12.0f : 8.0f;
-        const float af = half_bits_to_float(Su[(int64_t)j * a.nb_cap + b]);
-#pragma unroll
-        for (int h = 0; h < G; ++h) {
-          const float w = __fmul_rn(__fmul_rn(sm.qa[ai][h], af), 0.125f);
-          float r = rintf(__fmul_rn(w, inv[h]));
-          r = fminf(fmaxf(r, -127.0f), 127.0f);
-          const float err = fabsf(__fsub_rn(w, __fmul_rn(r, delta[h])));
-          eb[h] = __fmaf_rn(err, zmax, eb[h]);
-          pk[h] |= ((uint32_t)(int)r & 0xFFu) << (8 * k);
-        }
-      }
-#pragma unroll
-      for (int h = 0; h < G; ++h) sm.w8[blk][d][h] = pk[h];
-    }
-  }
-#pragma unroll
-  for (int h = 0; h < G; ++h)
-#pragma unroll
-    for (int o = TPB / 2; o >= 1; o >>= 1) eb[h] = __fadd_rn(eb[h], __shfl_xor(eb[h], o, TPB));
-  if (sl == 0) {
-#pragma unroll
-    for (int h = 0; h < G; ++h) {
-      sm.hdelta[blk][h] = ok[h] ? 0.5f * delta[h] : 0.0f;
-      // half the sum, inflated for the rounding of this sum and of the exact scores
-      sm.ebound[blk][h] = ok[h] ? __fmaf_rn(eb[h], 0.5f * (1.0f + 0x1p-10f), __fmul_rn(delta[h], (float)A * 0x1p-6f))
-                                : __builtin_huge_valf();
-    }
-  }
-}
-
-// Touch the plane lines of a group (one 4-byte load per row, 64 rows per
-// instruction) so they are in L2 when the scalar loads ask for them; the
-// returned value only keeps the loads alive.
-__device__ __forceinline__ uint32_t prefetch_group(const char* base, const Plan* plan, int ncells, bool any) {
-  uint32_t acc = 0u;
-  if (any) {
-    const int lane = threadIdx.x & 63;
-    for (int c = lane; c < ncells; c += kWave) acc ^= *reinterpret_cast<const uint32_t*>(base + plan->cell[c]);
-  }
-  return acc;
-}
-
-// Proxy sums of the 8 blocks of a group for all G heads (lane = key):
-// acc[g][h] = sum_j w8_j z'_j for block g.
-template <int G, bool FULL>
-__device__ __forceinline__ void proxy_group_impl(const FusedSmem<G>& sm, const Plan* plan, const char* base,
-                                                 int64_t nleft, int blk0, int acc[kGrp][G]) {
-  const int A = sm.nact, AD = (A + 3) >> 2;
-#pragma unroll
-  for (int g = 0; g < kGrp; ++g)
-#pragma unroll
-    for (int h = 0; h < G; ++h) acc[g][h] = 0;
-  for (int d = 0; d < AD; ++d) {
-    const uint32_t tp = sload32(&plan->tpack[d]);
-    const uint32_t zi = sload32(&plan->zinit[d]);
-    uint32_t z[kGrp];
-#pragma unroll
-    for (int g = 0; g < kGrp; ++g) z[g] = zi;
-    gather_channel<0, FULL>(z, (int)(tp & 0xFF), base, plan, 4 * d, nleft);
-    if ((tp >> 8) & 0xFF) gather_channel<1, FULL>(z, (int)((tp >> 8) & 0xFF), base, plan, 4 * d + 1, nleft);
-    if ((tp >> 16) & 0xFF) gather_channel<2, FULL>(z, (int)((tp >> 16) & 0xFF), base, plan, 4 * d + 2, nleft);
-    if (tp >> 24) gather_channel<3, FULL>(z, (int)(tp >> 24), base, plan, 4 * d + 3, nleft);
-#pragma unroll
-    for (int g = 0; g < kGrp; ++g) {
-#pragma unroll
-      for (int h = 0; h < G; ++h)
-        acc[g][h] = __builtin_amdgcn_sdot4((int)z[g], (int)sm.w8[blk0 + g][d][h], acc[g][h], false);
-    }
-  }
-}
-
-template <int G>
-__device__ __forceinline__ void proxy_group(const FusedSmem<G>& sm, const FusedArgs& a, const Plan* plan,
-                                            const char* base, int64_t gb, int blk0, int acc[kGrp][G]) {
-  if (gb + kGrp <= a.nb_cap)
-    proxy_group_impl<G, true>(sm, plan, base, kGrp, blk0, acc);
-  else
-    proxy_group_impl<G, false>(sm, plan, base, a.nb_cap - gb, blk0, acc);
-}
-
-// Exact documented scores of key (block b, bit) for all G heads, read from the store.
-template <int G>
-__device__ __forceinline__ void exact_scores(const int* act, int A, const float (*qa)[G], const FusedArgs& a, int u,
-                                             int64_t b, int bit, float acc[G]) {
-  const uint64_t* Pu = a.planes + (int64_t)u * kD * kPlanes * a.nb_cap + b;
-  const uint16_t* Su = a.scales + (int64_t)u * kD * a.nb_cap + b;
-#pragma unroll
-  for (int h = 0; h < G; ++h) acc[h] = 0.0f;
-  for (int ai = 0; ai < A; ++ai) {
-    const int e = act[ai];
-    const int j = e & 0xFF, t = e >> 8;
-    const float af = half_bits_to_float(Su[(int64_t)j * a.nb_cap]);
-    const uint64_t* Pj = Pu + (int64_t)j * kPlanes * a.nb_cap;
-    uint32_t c = 0;
-    for (int p = 0; p < t; ++p) c = 2u * c + (uint32_t)((Pj[(int64_t)p * a.nb_cap] >> bit) & 1ull);
-    const float y = (float)c + (0.5f - (float)(1 << (t - 1)));
-    const float khat = __fmul_rn(y, __fmul_rn(af, __uint_as_float((uint32_t)(128 - t) << 23)));
-#pragma unroll
-    for (int h = 0; h < G; ++h) acc[h] = __fmaf_rn(qa[ai][h], khat, acc[h]);
-  }
+__device__ __forceinline__ uint32_t rotl32(uint32_t x, int q) {
+  return __builtin_amdgcn_alignbit(x, x, (uint32_t)(32 - q) & 31u);
 }
 
 __device__ __forceinline__ void row_window(const FusedArgs& a, int u, int64_t* nu, int64_t* lo, int64_t* hi,
                                            bool flag) {
-  int64_t v = a.n[u];
+  int64_t v = gload(a.n + u);
   if (v < 0 || v > a.nb_cap * kBlockTokens) {
     if (flag) set_status(a.st, FATHOM_DEV_BAD_N);
     v = 0;
@@ -495,52 +213,428 @@ __device__ __forceinline__ void row_window(const FusedArgs& a, int u, int64_t* n
   if (*hi < *lo) *hi = *lo;
 }
 
+// ---------------------------------------------------------------- unit plan
+template <int G>
+__device__ void unit_setup(UnitLds<G>& P, const FusedArgs& a, int u) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  int t = 0;
+  if (tid < kD) {
+    t = gload(a.depths + (int64_t)u * kD + tid);
+    t = t > kPlanes ? kPlanes : t;
+  }
+  uint64_t bal[5];
+#pragma unroll
+  for (int v = 1; v <= 4; ++v) bal[v] = __ballot(tid < kD && t == v);
+  if (tid < kD && lane == 0) {
+#pragma unroll
+    for (int v = 1; v <= 4; ++v) P.cnt[wave][v] = __popcll(bal[v]);
+  }
+  __syncthreads();
+  int first[5];
+  {
+    int pos = 0;
+#pragma unroll
+    for (int v = 4; v >= 1; --v) {
+      first[v] = pos;
+      pos += P.cnt[0][v] + P.cnt[1][v];
+    }
+    if (tid == 0) P.A = pos;
+  }
+  if (tid < kD && t > 0) {
+    const int a_ = first[t] + (wave == 1 ? P.cnt[0][t] : 0) + __popcll(bal[t] & lanemask_lt(lane));
+    P.act[a_] = tid | (t << 8);
+    const uint64_t on = bal[1] | bal[2] | bal[3] | bal[4];
+    const int w0 = P.cnt[0][1] + P.cnt[0][2] + P.cnt[0][3] + P.cnt[0][4];
+    P.pidx[(wave == 1 ? w0 : 0) + __popcll(on & lanemask_lt(lane))] = a_;
+  }
+  __syncthreads();
+  const int A = P.A, AD = (A + 3) >> 2;
+  for (int x = tid; x < A * G; x += kFT) {
+    const int ai = x / G, h = x % G;
+    const float qv = load_q(a.q, a.qdt, ((int64_t)u * G + h) * kD + (P.act[ai] & 0xFF));
+    P.qa[ai][h] = qv;
+    P.qa8[ai][h] = __fmul_rn(qv, 0.125f);
+  }
+  if (tid < A) P.zmx[tid] = (float)(16 - (16 >> (P.act[tid] >> 8)));
+  if (tid < AD) {
+    uint32_t tp = 0u;
+#pragma unroll
+    for (int k2 = 0; k2 < 4; ++k2) {
+      const int x = 4 * tid + k2;
+      if (x < A) tp |= (uint32_t)(P.act[x] >> 8) << (8 * k2);
+    }
+    P.tpk[tid] = tp;
+  }
+  __syncthreads();
+  if (wave == 0) {  // padded row counts per dword; greedy chunks of whole dwords, at most kChunkRows rows each
+    int rd4 = 0;
+    if (lane < AD) {
+      const uint32_t tp = P.tpk[lane];
+      rd4 = ((int)((tp & 0xFF) + ((tp >> 8) & 0xFF) + ((tp >> 16) & 0xFF) + (tp >> 24)) + 3) & ~3;
+    }
+    int c = 0, rows = 0, r0 = 0, my_row = 0, my_ch = 0;
+    for (int d = 0; d < AD; ++d) {
+      const int v = __builtin_amdgcn_readlane(rd4, d);
+      if (rows + v > kChunkRows) {
+        ++c;
+        r0 += rows;
+        rows = 0;
+        if (lane == 0) {
+          P.chd[c] = d;
+          P.chr[c] = r0;
+        }
+      }
+      if (lane == d) {
+        my_row = rows;
+        my_ch = c;
+      }
+      rows += v;
+    }
+    if (lane < AD) {
+      P.drow[lane] = (uint32_t)my_row;
+      P.dnq[lane] = (uint32_t)(rd4 >> 2);
+      P.dch[lane] = my_ch;
+    }
+    if (lane == 0) {
+      const int nch = AD > 0 ? c + 1 : 0;
+      P.chd[0] = 0;
+      P.chr[0] = 0;
+      P.nch = nch;
+      P.chd[nch] = AD;
+      P.chr[nch] = r0 + rows;
+    }
+  }
+  __syncthreads();
+  // rows of channel a: its dword's first padded row (global) + the depths before it in the dword
+  if (tid < A) {
+    const int d = tid >> 2, K = tid & 3, e = P.act[tid], j = e & 0xFF, tt = e >> 8;
+    const uint32_t tp = P.tpk[d];
+    int r0 = P.chr[P.dch[d]] + (int)P.drow[d];
+    for (int k2 = 0; k2 < K; ++k2) r0 += (int)((tp >> (8 * k2)) & 0xFF);
+    for (int p = 0; p < tt; ++p) {
+      P.rrow[r0 + p] = (uint32_t)(4 * j + p);
+      P.rsh[r0 + p] = (uint32_t)(32 - (8 * K + 4 - p)) & 31u;
+    }
+  }
+  if (tid < AD) {  // pad rows of dword tid
+    const int d = tid;
+    const uint32_t tp = P.tpk[d];
+    const int rd = (int)((tp & 0xFF) + ((tp >> 8) & 0xFF) + ((tp >> 16) & 0xFF) + (tp >> 24));
+    const int r0 = P.chr[P.dch[d]] + (int)P.drow[d];
+    for (int r = rd; r < (int)P.dnq[d] * 4; ++r) {
+      P.rrow[r0 + r] = kPadRow;
+      P.rsh[r0 + r] = 0u;
+    }
+  }
+  __syncthreads();
+}
+
+// ---------------------------------------------------------------- one wave's pipeline
+struct Stage {
+  uint64_t rw[kStageK];
+  uint32_t sv[kStageK];
+};
+
+template <int G>
+__device__ __forceinline__ void stage_load(Stage& S, const UnitLds<G>& P, const FusedArgs& a, int u, int64_t gb,
+                                           int c) {
+  const int lane = threadIdx.x & 63, rl = lane >> 3, bl = lane & 7;
+  const int row0 = P.chr[c], rows = P.chr[c + 1] - row0;
+  const int a0 = 4 * P.chd[c];
+  int a1 = 4 * P.chd[c + 1];
+  a1 = a1 < P.A ? a1 : P.A;
+  const int64_t b = gb + bl;
+  const bool bok = b < a.nb_cap;
+  const uint64_t* Pu = a.planes + (int64_t)u * kD * kPlanes * a.nb_cap;
+  const uint16_t* Su = a.scales + (int64_t)u * kD * a.nb_cap;
+#pragma unroll
+  for (int k = 0; k < kStageK; ++k) {
+    const int r = rl + 8 * k;
+    S.rw[k] = 0ull;
+    if (bok && r < rows) {
+      const uint32_t rr = P.rrow[row0 + r];
+      if (rr != kPadRow) S.rw[k] = gload(Pu + (int64_t)rr * a.nb_cap + b);
+    }
+    S.sv[k] = 0u;
+    if (bok && r < a1 - a0) S.sv[k] = gload(Su + (int64_t)(P.act[a0 + r] & 0xFF) * a.nb_cap + b);
+  }
+}
+
+template <int G, int G4>
+__device__ __forceinline__ void stage_store(const Stage& S, const UnitLds<G>& P, WaveLds<G4>& W, int c) {
+  const int lane = threadIdx.x & 63, rl = lane >> 3, bl = lane & 7;
+  const int row0 = P.chr[c], rows = P.chr[c + 1] - row0;
+  const int nchan = (4 * P.chd[c + 1] < P.A ? 4 * P.chd[c + 1] : P.A) - 4 * P.chd[c];
+#pragma unroll
+  for (int k = 0; k < kStageK; ++k) {
+    const int r = rl + 8 * k;
+    if (r < rows) {
+      const uint32_t sh = P.rsh[row0 + r];
+      const uint32_t lo = (uint32_t)S.rw[k], hi = (uint32_t)(S.rw[k] >> 32);
+      W.rows[r][0][bl] = __builtin_amdgcn_alignbit(lo, lo, sh);
+      W.rows[r][1][bl] = __builtin_amdgcn_alignbit(hi, hi, sh);
+    }
+    if (r < nchan) W.scl[r][bl] = (uint16_t)S.sv[k];
+  }
+}
+
+// Weights of chunk c for the 8 blocks of the group.  Lane = (block g, head
+// h, channel phase kk): each lane walks the chunk's channels a = kk, kk + KL,
+// ... and the per-(block, head) sums are reduced over kk.  first: this chunk
+// fixes delta; last: the candidate thresholds.  Blocks >= nbu get no bound
+// (their keys are never eligible).
+template <int G, int G4, bool SAMPLE>
+__device__ void weights(const UnitLds<G>& P, WaveLds<G4>& W, int c, bool first, bool last, int64_t gb, int64_t nbu) {
+  constexpr int Gp = G <= 1 ? 1 : G <= 2 ? 2 : G <= 4 ? 4 : 8;
+  constexpr int KL = 8 / Gp;
+  const int lane = threadIdx.x & 63, g = lane >> 3, sub = lane & 7, h = sub % Gp, kk = sub / Gp;
+  const bool gh = h < G;
+  const bool bv = gh && gb + g < nbu;
+  const int a0 = 4 * P.chd[c];
+  int a1 = 4 * P.chd[c + 1];
+  a1 = a1 < P.A ? a1 : P.A;
+  const int A = P.A;
+  const int hh = gh ? h : 0;
+  float delta, inv;
+  int fin = 1;
+  if (first) {
+    float mx = 0.0f;
+    if (bv) {
+      for (int ai = a0 + kk; ai < a1; ai += KL) {
+        const float w = __fmul_rn(P.qa8[ai][hh], half_bits_to_float(W.scl[ai - a0][g]));
+        if (!(fabsf(w) <= 3.402823466e38f)) fin = 0;
+        mx = fmaxf(mx, fabsf(w));
+      }
+    }
+#pragma unroll
+    for (int m = Gp; m < 8; m <<= 1) {
+      mx = fmaxf(mx, __shfl_xor(mx, m, kWave));
+      fin &= __shfl_xor(fin, m, kWave);
+    }
+    int e;
+    (void)frexpf(mx, &e);  // mx in [2^(e-1), 2^e)
+    const bool ok = fin && (mx >= 0x1p-100f || mx == 0.0f);
+    const int ee = e < -100 ? -100 : e;
+    delta = ok ? ldexpf(1.0f, ee - 7) : 0.0f;  // |w| / delta < 128
+    inv = ok ? ldexpf(1.0f, 7 - ee) : 0.0f;
+  } else {
+    delta = gh ? W.sdel[g][h] : 0.0f;
+    inv = gh ? W.sinv[g][h] : 0.0f;
+  }
+  float eb = 0.0f, sw = 0.0f;
+  int bias = 0;
+  if (bv) {
+    uint8_t* w8b = reinterpret_cast<uint8_t*>(&W.w8[g][0][0]);
+    for (int ai = a0 + kk; ai < a1; ai += KL) {
+      const int al = ai - a0;
+      const float w = __fmul_rn(P.qa8[ai][hh], half_bits_to_float(W.scl[al][g]));
+      if (!(fabsf(w) <= 3.402823466e38f)) fin = 0;
+      const float zm = P.zmx[ai];
+      const float r = fminf(fmaxf(rintf(__fmul_rn(w, inv)), -127.0f), 127.0f);
+      const int ri = (int)r;
+      eb = __fmaf_rn(fabsf(__fmaf_rn(r, delta, -w)), zm, eb);
+      sw = __fadd_rn(sw, fabsf(w));
+      bias -= ri * (int)zm;
+      w8b[((al >> 2) * G4 + h) * 4 + (al & 3)] = (uint8_t)(ri & 0xFF);
+    }
+  }
+#pragma unroll
+  for (int m = Gp; m < 8; m <<= 1) {
+    eb = __fadd_rn(eb, __shfl_xor(eb, m, kWave));
+    sw = __fadd_rn(sw, __shfl_xor(sw, m, kWave));
+    bias += __shfl_xor(bias, m, kWave);
+    fin &= __shfl_xor(fin, m, kWave);
+  }
+  if (gh && kk == 0) {
+    if (!fin) delta = 0.0f;
+    const float ebt = first ? eb : __fadd_rn(W.seb[g][h], eb);
+    const float swt = first ? sw : __fadd_rn(W.ssw[g][h], sw);
+    const int biast = first ? bias : W.sbias[g][h] + bias;
+    W.sdel[g][h] = delta;
+    W.sinv[g][h] = inv;
+    W.seb[g][h] = ebt;
+    W.ssw[g][h] = swt;
+    W.sbias[g][h] = biast;
+    if (last && !SAMPLE) {
+      // candidate iff hdelta (acc + bias) + E >= tau, made conservative on
+      // integers: acc >= floor((tau - E) / hdelta) - bias - 1
+      const float E = __fmul_rn(__fmaf_rn(ebt, 0.5f, __fmul_rn((float)A * 0x1p-21f, swt)), 1.0f + 0x1p-10f);
+      const float tau = P.tau[h];
+      int thr = INT32_MIN;
+      if (delta > 0.0f && tau != kNegInf && E <= 3.402823466e38f) {
+        const double x = ((double)tau - (double)E) / (0.5 * (double)delta);
+        if (x == x) {
+          const double f = floor(x) - (double)biast - 1.0;
+          thr = f <= -2147483648.0 ? INT32_MIN : f >= 2147483647.0 ? INT32_MAX : (int)f;
+        }
+      }
+      if (gb + g >= nbu) thr = INT32_MAX;
+      W.sthr[g][h] = thr;
+    }
+  }
+}
+
+// Integer proxy sums of chunk c for the 8 blocks, added to acc.
+template <int G, int G4>
+__device__ __forceinline__ void chunk_proxy(const UnitLds<G>& P, const WaveLds<G4>& W, int c, uint32_t M0, int s,
+                                            int acc[kGrp][G]) {
+  const int lane = threadIdx.x & 63, half = lane >> 5;
+  const int d0 = uni(P.chd[c]), d1 = uni(P.chd[c + 1]), cr0 = uni(P.chr[c]);
+  for (int d = d0; d < d1; ++d) {
+    const int nq = uni((int)P.dnq[d]);
+    const int rb = uni((int)P.drow[d]);
+    uint32_t zr[kGrp];
+#pragma unroll
+    for (int g = 0; g < kGrp; ++g) zr[g] = 0u;
+    for (int iq = 0; iq < nq; ++iq) {
+      const int r = rb + 4 * iq;
+      const uint4 sh = *reinterpret_cast<const uint4*>(&P.rsh[cr0 + r]);
+      uint4 x[4][2];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const uint4* rp = reinterpret_cast<const uint4*>(&W.rows[r + i][half][0]);
+        x[i][0] = rp[0];
+        x[i][1] = rp[1];
+      }
+      const uint32_t m[4] = {__builtin_amdgcn_alignbit(M0, M0, sh.x), __builtin_amdgcn_alignbit(M0, M0, sh.y),
+                             __builtin_amdgcn_alignbit(M0, M0, sh.z), __builtin_amdgcn_alignbit(M0, M0, sh.w)};
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        zr[0] |= x[i][0].x & m[i];
+        zr[1] |= x[i][0].y & m[i];
+        zr[2] |= x[i][0].z & m[i];
+        zr[3] |= x[i][0].w & m[i];
+        zr[4] |= x[i][1].x & m[i];
+        zr[5] |= x[i][1].y & m[i];
+        zr[6] |= x[i][1].z & m[i];
+        zr[7] |= x[i][1].w & m[i];
+      }
+    }
+    const int dl = d - d0;
+#pragma unroll
+    for (int g = 0; g < kGrp; ++g) {
+      const uint32_t z = __builtin_amdgcn_alignbit(zr[g], zr[g], (uint32_t)s);
+#pragma unroll
+      for (int h = 0; h < G; ++h) acc[g][h] = __builtin_amdgcn_sdot4((int)z, (int)W.w8[g][dl][h], acc[g][h], false);
+    }
+  }
+}
+
+// Runs the proxy over `ngroups` groups of unit u (group index gi -> first
+// block via group_block), chunk by chunk with the next chunk's loads in flight,
+// and hands each finished group to `finish(gb, acc)`.
+template <int G, int G4, bool SAMPLE, typename GroupBlock, typename Finish>
+__device__ void wave_groups(const UnitLds<G>& P, WaveLds<G4>& W, const FusedArgs& a, int u, int ngroups, int64_t nbu,
+                            GroupBlock group_block, Finish finish) {
+  const int lane = threadIdx.x & 63, s = lane & 31;
+  const int nch = uni(P.nch);
+  if (ngroups <= 0 || nch <= 0) {
+    for (int gi = 0; gi < ngroups; ++gi) {  // no active channel: every proxy is 0 with E = 0
+      int acc[kGrp][G];
+#pragma unroll
+      for (int g = 0; g < kGrp; ++g)
+#pragma unroll
+        for (int h = 0; h < G; ++h) acc[g][h] = 0;
+      const int64_t gb = group_block(gi);
+      {
+        const int g = lane >> 3, h = lane & 7;
+        if (h < G) {
+          W.sdel[g][h] = 1.0f;
+          W.sinv[g][h] = 1.0f;
+          W.seb[g][h] = 0.0f;
+          W.ssw[g][h] = 0.0f;
+          W.sbias[g][h] = 0;
+          int thr = INT32_MIN;
+          if (!SAMPLE && P.tau[h] > 0.0f) thr = INT32_MAX;
+          if (gb + g >= nbu) thr = INT32_MAX;
+          W.sthr[g][h] = thr;
+        }
+      }
+      wave_lds_sync();
+      finish(gb, acc);
+      wave_lds_sync();
+    }
+    return;
+  }
+  const uint32_t M0 = 1u << s;
+  const int items = ngroups * nch;
+  Stage S;
+  stage_load<G>(S, P, a, u, group_block(0), 0);
+  int acc[kGrp][G];
+#pragma unroll
+  for (int g = 0; g < kGrp; ++g)
+#pragma unroll
+    for (int h = 0; h < G; ++h) acc[g][h] = 0;
+  for (int it = 0; it < items; ++it) {
+    const int gi = it / nch, c = it - gi * nch;
+    const int64_t gb = group_block(gi);
+    stage_store<G, G4>(S, P, W, c);
+    if (it + 1 < items) {
+      const int gi2 = (it + 1) / nch;
+      stage_load<G>(S, P, a, u, group_block(gi2), it + 1 - gi2 * nch);
+    }
+    wave_lds_sync();
+    weights<G, G4, SAMPLE>(P, W, c, c == 0, c == nch - 1, gb, nbu);
+    wave_lds_sync();
+    chunk_proxy<G, G4>(P, W, c, M0, s, acc);
+    if (c == nch - 1) {
+      finish(gb, acc);
+#pragma unroll
+      for (int g = 0; g < kGrp; ++g)
+#pragma unroll
+        for (int h = 0; h < G; ++h) acc[g][h] = 0;
+    }
+    wave_lds_sync();  // this item's LDS reads are done before the next stage_store
+  }
+}
+
 // ---------------------------------------------------------------- pass 1
 // Each workgroup: 4 sampled groups (one per wave) of the unit.
 template <int G>
 __global__ __launch_bounds__(kFT) void fused_sample_kernel(FusedArgs a) {
-  __shared__ FusedSmem<G> sm;
-  const int u = blockIdx.y, tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  constexpr int G4 = (G + 3) & ~3;
+  __shared__ UnitLds<G> P;
+  __shared__ WaveLds<G4> WL[kFW];
+  const int u = blockIdx.y, lane = threadIdx.x & 63, wave = uni(threadIdx.x >> 6);
   int64_t nu, lo, hi;
   row_window(a, u, &nu, &lo, &hi, false);
   const int64_t nbu = (nu + kBlockTokens - 1) / kBlockTokens;
-  const Plan* plan = a.ws.plan + u;
-  const char* base = reinterpret_cast<const char*>(a.planes + (int64_t)u * kD * kPlanes * a.nb_cap);
+  unit_setup<G>(P, a, u);
   const int64_t sg = (int64_t)blockIdx.x * kFW + wave;  // sampled group index
-  const int64_t gb = sg * a.ws.s_gstride * kGrp;        // its first block
-  const bool mine = sg < a.ws.s_groups && gb < nbu;
-  const uint32_t pf = prefetch_group(base + gb * 8, plan, sload32(&plan->ncells), mine);
-  unit_setup<G>(sm, a, u);
-  weight_setup<G>(sm, a, u, nbu, [&](int blk) {
-    const int64_t s2 = (int64_t)blockIdx.x * kFW + blk / kGrp;
-    return s2 < a.ws.s_groups ? s2 * a.ws.s_gstride * kGrp + blk % kGrp : (int64_t)-1;
-  });
-  __syncthreads();
   if (sg >= a.ws.s_groups) return;
-  const int blk0 = wave * kGrp;
-  int acc[kGrp][G];
-  if (gb < nbu) proxy_group<G>(sm, a, plan, base + gb * 8, gb, blk0, acc);
-  asm volatile("" ::"v"(pf));
+  const int64_t gb = sg * a.ws.s_gstride * kGrp;
+  WaveLds<G4>& W = WL[wave];
+  auto put = [&](int64_t gbb, int (&acc)[kGrp][G]) {
 #pragma unroll
-  for (int g = 0; g < kGrp; ++g) {
-    const int64_t b = gb + g;
-    const int64_t i = b * kBlockTokens + lane;
+    for (int g = 0; g < kGrp; ++g) {
+      const int64_t b = gbb + g;
+      const int64_t i = b * kBlockTokens + lane;
 #pragma unroll
-    for (int h = 0; h < G; ++h) {
-      // the proxy itself (exact in fp32): tau only steers how many keys are
-      // re-scored; the survivor count, not tau, guarantees the result
-      float v = kNegInf;
-      if (b < nbu && i >= lo && i < hi && sm.ebound[blk0 + g][h] <= 3.402823466e38f)
-        v = __fmul_rn(sm.hdelta[blk0 + g][h], (float)acc[g][h]);
-      a.ws.sample[((int64_t)u * G + h) * a.ws.s_groups * (kGrp * kBlockTokens) + (sg * kGrp + g) * kBlockTokens +
-                  lane] = v;
+      for (int h = 0; h < G; ++h) {
+        // the proxy itself (exact in fp32): tau only steers how many keys are
+        // re-scored; the candidate count, not tau, guarantees the result
+        float v = kNegInf;
+        const float del = W.sdel[g][h];
+        if (b < nbu && i >= lo && i < hi && del > 0.0f)
+          v = __fmul_rn(0.5f * del, (float)(acc[g][h] + W.sbias[g][h]));
+        gstore(&a.ws.sample[((int64_t)u * G + h) * a.ws.s_groups * (kGrp * kBlockTokens) +
+                            (sg * kGrp + g) * kBlockTokens + lane], v);
+      }
     }
+  };
+  if (gb < nbu) {
+    wave_groups<G, G4, true>(P, W, a, u, 1, nbu, [&](int) { return gb; }, put);
+  } else {
+    for (int g = 0; g < kGrp; ++g)
+      for (int h = 0; h < G; ++h)
+        a.ws.sample[((int64_t)u * G + h) * a.ws.s_groups * (kGrp * kBlockTokens) + (sg * kGrp + g) * kBlockTokens +
+                    lane] = kNegInf;
   }
 }
 
 // ---------------------------------------------------------------- pass 2
 // tau = the m-th largest sampled proxy, m ~ 1.25 k * (sampled / eligible) + 16;
-// tau = -inf when the row has no more eligible keys than the survivor buffer holds.
+// tau = -inf when the row has no more eligible keys than the candidate list holds.
 __global__ __launch_bounds__(kSelThreads) void fused_tau_kernel(FusedArgs a, int G) {
   extern __shared__ uint32_t keys[];  // the row's sample as order-preserving keys (0 = unusable)
   __shared__ uint32_t hist[2048];
@@ -549,13 +643,14 @@ __global__ __launch_bounds__(kSelThreads) void fused_tau_kernel(FusedArgs a, int
   __shared__ uint32_t s_total;
   __shared__ uint32_t part[kSelThreads / kWave];
   const int r = blockIdx.x, u = r / G, tid = threadIdx.x;
+  if (tid == 0 && r % G == 0) a.ws.uovf[u] = 0u;
   int64_t nu, lo, hi;
   row_window(a, u, &nu, &lo, &hi, false);
   const int64_t m_e = hi - lo;
   if (m_e <= a.ws.cap) {
     if (tid == 0) {
       a.ws.tau[r] = kNegInf;
-      a.ws.cnt[r] = 0u;
+      for (int q2 = 0; q2 < kSlots; ++q2) a.ws.cnt[r * kSlots + q2] = 0u;
     }
     return;
   }
@@ -576,7 +671,7 @@ __global__ __launch_bounds__(kSelThreads) void fused_tau_kernel(FusedArgs a, int
   if (m_s == 0) {
     if (tid == 0) {
       a.ws.tau[r] = kNegInf;
-      a.ws.cnt[r] = 0u;
+      for (int q2 = 0; q2 < kSlots; ++q2) a.ws.cnt[r * kSlots + q2] = 0u;
     }
     return;
   }
@@ -609,109 +704,204 @@ __global__ __launch_bounds__(kSelThreads) void fused_tau_kernel(FusedArgs a, int
     const uint32_t key = s_prefix & ~1u;  // the low bit was forced on: round the key down
     const uint32_t bitsf = (key & 0x80000000u) ? (key & 0x7FFFFFFFu) : ~key;
     a.ws.tau[r] = __uint_as_float(bitsf);
-    a.ws.cnt[r] = 0u;
+    for (int q2 = 0; q2 < kSlots; ++q2) a.ws.cnt[r * kSlots + q2] = 0u;
   }
 }
 
 // ---------------------------------------------------------------- pass 3
 template <int G>
-__device__ void rescore_queue(FusedSmem<G>& sm, const FusedArgs& a, int u, int64_t base_block) {
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int count = sm.qcount;
-  for (int e0 = wave * kWave; e0 < count; e0 += kFT) {
-    const int e = e0 + lane;
-    uint32_t ent = 0u;
-    if (e < count) ent = sm.queue[e];
-    const int off = (int)(ent & 0xFFFFu), hm = (int)(ent >> 16);
-    const int64_t i = base_block * kBlockTokens + off;
-    float s[G];
-#pragma unroll
-    for (int h = 0; h < G; ++h) s[h] = 0.0f;
-    if (hm) exact_scores<G>(sm.act, sm.nact, sm.qa, a, u, i / kBlockTokens, (int)(i % kBlockTokens), s);
-#pragma unroll
-    for (int h = 0; h < G; ++h) {
-      const float tau = sm.tau[h];
-      const bool keep = ((hm >> h) & 1) && (s[h] >= tau || tau == kNegInf);
-      const uint64_t bm = __ballot(keep);
-      if (bm) {
-        const int r = u * G + h;
-        uint32_t basep = 0;
-        if (lane == __ffsll((unsigned long long)bm) - 1) basep = atomicAdd(&a.ws.cnt[r], (uint32_t)__popcll(bm));
-        basep = __shfl(basep, __ffsll((unsigned long long)bm) - 1, kWave);
-        if (keep) {
-          const uint32_t pos = basep + (uint32_t)__popcll(bm & lanemask_lt(lane));
-          if (pos < (uint32_t)a.ws.cap)
-            a.ws.cand[(int64_t)r * a.ws.cap + pos] =
-                ((uint64_t)score_key(s[h]) << 32) | (uint64_t)(~(uint32_t)i);
-        }
-      }
-    }
-  }
-}
-
-template <int G>
 __global__ __launch_bounds__(kFT) void fused_full_kernel(FusedArgs a) {
-  __shared__ FusedSmem<G> sm;
-  const int u = blockIdx.y, tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  constexpr int G4 = (G + 3) & ~3;
+  __shared__ UnitLds<G> P;
+  __shared__ WaveLds<G4> WL[kFW];
+  __shared__ uint32_t wq[kWGQ];  // this workgroup's candidates
+  __shared__ int wqn;
+  const int u = blockIdx.y, tid = threadIdx.x, lane = tid & 63, wave = uni(tid >> 6);
   int64_t nu, lo, hi;
   row_window(a, u, &nu, &lo, &hi, blockIdx.x == 0 && tid == 0);
   const int64_t nbu = (nu + kBlockTokens - 1) / kBlockTokens;
-  const int64_t b0 = (int64_t)blockIdx.x * kRange;
-  if (b0 >= nbu || b0 * kBlockTokens >= hi || (b0 + kRange) * kBlockTokens <= lo) return;
-  const Plan* plan = a.ws.plan + u;
-  const char* base = reinterpret_cast<const char*>(a.planes + (int64_t)u * kD * kPlanes * a.nb_cap);
-  const int ncells = (int)sload32(&plan->ncells);
-  // L2 prefetch of this wave's first group
-  uint32_t pf = prefetch_group(base + (b0 + wave * kGrp) * 8, plan, ncells, b0 + wave * kGrp < nbu);
-  unit_setup<G>(sm, a, u);
-  if (tid < G) sm.tau[tid] = a.ws.tau[u * G + tid];
-  for (int s0 = 0; s0 < kRange; s0 += kSub) {
-    const int64_t sbase = b0 + s0;
-    if (sbase >= nbu) break;
-    __syncthreads();  // previous sub-tile's weights and queue are consumed
-    weight_setup<G>(sm, a, u, nbu, [&](int blk) { return sbase + blk; });
+  const int64_t g0 = (int64_t)blockIdx.x * kGroupsPerWG;  // first group of this workgroup
+  const int64_t b0 = g0 * kGrp, b1 = (g0 + kGroupsPerWG) * kGrp;
+  const int64_t region = (int64_t)u * a.ws.nwg + blockIdx.x;
+  // rows with no more eligible keys than the survivor list holds are
+  // computed exactly by pass 4: no candidates from here
+  if (b0 >= nbu || b0 * kBlockTokens >= hi || b1 * kBlockTokens <= lo || hi - lo <= a.ws.cap) {
+    if (tid == 0) gstore(&a.ws.ecnt[region], 0u);
+    return;
+  }
+  if (tid == 0) wqn = 0;
+  unit_setup<G>(P, a, u);
+  if (tid < G) P.tau[tid] = gload(a.ws.tau + u * G + tid);
+  __syncthreads();
+  // this wave's groups: g0 + wave + kFW * x, those that hold eligible keys
+  int mine[kGroupsPerWave] = {0};
+  int ng = 0;
+#pragma unroll
+  for (int x = 0; x < kGroupsPerWave; ++x) {
+    const int64_t gbx = (g0 + wave + kFW * x) * kGrp;
+    if (gbx < nbu && gbx * kBlockTokens < hi && (gbx + kGrp) * kBlockTokens > lo) mine[ng++] = x;
+  }
+  WaveLds<G4>& W = WL[wave];
+  auto gblock = [&](int gi) {
+    int x = 0;
+#pragma unroll
+    for (int y = 0; y < kGroupsPerWave; ++y)
+      if (y == gi) x = mine[y];
+    return (g0 + wave + kFW * x) * kGrp;
+  };
+  auto put = [&](int64_t gbb, int (&acc)[kGrp][G]) {
+#pragma unroll
+    for (int g = 0; g < kGrp; ++g) {
+      const int64_t b = gbb + g;
+      const int64_t i = b * kBlockTokens + lane;
+      const bool elig = b < nbu && i >= lo && i < hi;
+      int thr[8];
+      *reinterpret_cast<int4*>(&thr[0]) = *reinterpret_cast<const int4*>(&W.sthr[g][0]);
+      if (G > 4) *reinterpret_cast<int4*>(&thr[4]) = *reinterpret_cast<const int4*>(&W.sthr[g][4]);
+      int hm = 0;
+#pragma unroll
+      for (int h = 0; h < G; ++h) hm |= (int)(acc[g][h] >= thr[h]) << h;
+      hm = elig ? hm : 0;
+      const uint64_t any = __ballot(hm != 0);
+      if (any) {
+        int base = 0;
+        if (lane == 0) base = atomicAdd(&wqn, __popcll(any));
+        base = __shfl(base, 0, kWave);
+        const int pos = base + __popcll(any & lanemask_lt(lane));
+        const uint32_t en = (uint32_t)((b - b0) * kBlockTokens + lane) | ((uint32_t)hm << 16);
+        if (hm && pos < kWGQ) wq[pos] = en;
+        else if (hm && pos < kWGCap) gstore(&a.ws.ent[region * kWGCap + pos], en);
+      }
+    }
+  };
+  wave_groups<G, G4, false>(P, W, a, u, ng, nbu, gblock, put);
+  __syncthreads();
+  const int nq = wqn;
+  const int nc = nq < kWGQ ? nq : kWGQ;
+  for (int e = tid; e < nc; e += kFT) gstore(&a.ws.ent[region * kWGCap + e], wq[e]);
+  if (tid == 0) gstore(&a.ws.ecnt[region], (uint32_t)nq);
+}
+
+// ---------------------------------------------------------------- pass 3b
+// The documented fp32 scores (active channels ascending, khat exact, acc =
+// fma(q, khat, acc)) of the candidates of one full-pass workgroup, one key per
+// thread with the loads of 16 channels in flight together; keys with score >=
+// tau for a head in their mask join that row's survivor list.
+constexpr int kRsChunk = 16;
+template <int G>
+__global__ __launch_bounds__(kRsT) void fused_rescore_kernel(FusedArgs a) {
+  __shared__ int act[kD];  // j | t << 8, channels ascending
+  __shared__ float qa[kD][G];
+  __shared__ float tau[G];
+  __shared__ int wc[2];
+  __shared__ uint64_t kept[G][kRsT];  // this pass's survivors per head
+  __shared__ int nk[G];
+  __shared__ uint32_t kbase[G];
+  const int u = blockIdx.y, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int64_t region = (int64_t)u * a.ws.nwg + blockIdx.x;
+  const uint32_t nq = gload(a.ws.ecnt + region);
+  if (nq == 0) return;
+  if (nq > (uint32_t)kWGCap) {
+    if (tid == 0) set_status(a.ws.uovf + u, 1u);
+    return;
+  }
+  int t = 0;
+  if (tid < kD) {
+    t = gload(a.depths + (int64_t)u * kD + tid);
+    t = t > kPlanes ? kPlanes : t;
+  }
+  const uint64_t m = __ballot(tid < kD && t > 0);
+  if (tid < kD && lane == 0) wc[wave] = __popcll(m);
+  __syncthreads();
+  if (tid < kD && t > 0) act[(wave == 1 ? wc[0] : 0) + __popcll(m & lanemask_lt(lane))] = tid | (t << 8);
+  if (tid < G) tau[tid] = gload(a.ws.tau + u * G + tid);
+  __syncthreads();
+  const int A = wc[0] + wc[1];
+  for (int x = tid; x < A * G; x += kRsT) qa[x / G][x % G] = load_q(a.q, a.qdt, ((int64_t)u * G + x % G) * kD + (act[x / G] & 0xFF));
+  __syncthreads();
+  const int64_t b0 = (int64_t)blockIdx.x * kGroupsPerWG * kGrp;
+  const int slot = (int)(blockIdx.x % kSlots);
+  for (uint32_t e0 = 0; e0 < nq; e0 += kRsT) {
+    if (tid < G) nk[tid] = 0;
     __syncthreads();
-    const int64_t gb = sbase + wave * kGrp;
-    if (gb < nbu) {
-      const int blk0 = wave * kGrp;
-      int acc[kGrp][G];
-      proxy_group<G>(sm, a, plan, base + gb * 8, gb, blk0, acc);
-      asm volatile("" ::"v"(pf));
-      const int64_t gnext = gb + kSub;  // prefetch this wave's next group
-      pf = prefetch_group(base + gnext * 8, plan, ncells, s0 + kSub < kRange && gnext < nbu);
+    const uint32_t e = e0 + tid;
+    uint32_t en = 0u;
+    if (e < nq) en = gload(a.ws.ent + region * kWGCap + e);
+    const int hm = (int)(en >> 16);
+    const int64_t i = b0 * kBlockTokens + (int64_t)(en & 0xFFFFu);
+    float acc[G];
 #pragma unroll
-      for (int g = 0; g < kGrp; ++g) {
-        const int64_t b = gb + g;
-        const int64_t i = b * kBlockTokens + lane;
-        const bool elig = b < nbu && i >= lo && i < hi;
-        int hm = 0;
+    for (int h = 0; h < G; ++h) acc[h] = 0.0f;
+    if (hm) {
+      const int64_t b = i >> 6;
+      const int hw = (int)((i >> 5) & 1), sh = (int)(i & 31);
+      const uint64_t* Pu = a.planes + (int64_t)u * kD * kPlanes * a.nb_cap + b;
+      const uint16_t* Su = a.scales + (int64_t)u * kD * a.nb_cap + b;
+      for (int a0 = 0; a0 < A; a0 += kRsChunk) {
+        uint32_t wd[kRsChunk][4];
+        uint16_t sc[kRsChunk];
 #pragma unroll
-        for (int h = 0; h < G; ++h) {
-          const float p = __fmul_rn(sm.hdelta[blk0 + g][h], (float)acc[g][h]);
-          const float ub = __fadd_rn(p, sm.ebound[blk0 + g][h]);
-          if (elig && (ub >= sm.tau[h] || sm.tau[h] == kNegInf || ub != ub)) hm |= 1 << h;
+        for (int K = 0; K < kRsChunk; ++K) {
+          const int x = a0 + K;
+          sc[K] = 0;
+#pragma unroll
+          for (int p = 0; p < 4; ++p) wd[K][p] = 0u;
+          if (x < A) {
+            const int e2 = act[x], j = e2 & 0xFF, tt = e2 >> 8;
+            sc[K] = gload(Su + (int64_t)j * a.nb_cap);
+#pragma unroll
+            for (int p = 0; p < 4; ++p)
+              if (p < tt) wd[K][p] = gload(reinterpret_cast<const uint32_t*>(Pu + (int64_t)(4 * j + p) * a.nb_cap) + hw);
+          }
         }
-        const uint64_t any = __ballot(hm != 0);
-        if (any) {
-          int basep = 0;
-          const int leader = __ffsll((unsigned long long)any) - 1;
-          if (lane == leader) basep = atomicAdd(&sm.qcount, __popcll(any));
-          basep = __shfl(basep, leader, kWave);
-          if (hm)
-            sm.queue[basep + __popcll(any & lanemask_lt(lane))] =
-                (uint32_t)((b - b0) * kBlockTokens + lane) | ((uint32_t)hm << 16);
+#pragma unroll
+        for (int K = 0; K < kRsChunk; ++K) {
+          const int x = a0 + K;
+          if (x < A) {
+            const int tt = act[x] >> 8;
+            uint32_t c = 0;
+#pragma unroll
+            for (int p = 0; p < 4; ++p)
+              if (p < tt) c = 2u * c + ((wd[K][p] >> sh) & 1u);
+            const float y = (float)c + (0.5f - (float)(1 << (tt - 1)));
+            const float khat =
+                __fmul_rn(y, __fmul_rn(half_bits_to_float(sc[K]), __uint_as_float((uint32_t)(128 - tt) << 23)));
+#pragma unroll
+            for (int h = 0; h < G; ++h) acc[h] = __fmaf_rn(qa[x][h], khat, acc[h]);
+          }
         }
       }
     }
-    __syncthreads();
-    const bool last = s0 + kSub >= kRange || sbase + kSub >= nbu;
-    if (sm.qcount >= kFlush || last) {
-      rescore_queue<G>(sm, a, u, b0);
-      __syncthreads();
-      if (tid == 0) sm.qcount = 0;
+    // gather this pass's survivors per head in LDS, then one global append per head
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+      const bool keep = ((hm >> h) & 1) && acc[h] >= tau[h];
+      const uint64_t bm = __ballot(keep);
+      if (bm) {
+        const int leader = __ffsll((unsigned long long)bm) - 1;
+        int basep = 0;
+        if (lane == leader) basep = atomicAdd(&nk[h], __popcll(bm));
+        basep = __shfl(basep, leader, kWave);
+        if (keep)
+          kept[h][basep + __popcll(bm & lanemask_lt(lane))] =
+              ((uint64_t)score_key(acc[h]) << 32) | (uint64_t)(~(uint32_t)i);
+      }
     }
+    __syncthreads();
+    if (tid < G && nk[tid] > 0)
+      kbase[tid] = gatomic_add(&a.ws.cnt[(u * G + tid) * kSlots + slot], (uint32_t)nk[tid]);
+    __syncthreads();
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+      const int nh = nk[h];
+      if (tid < nh) {
+        const uint32_t pos = kbase[h] + (uint32_t)tid;
+        if (pos < (uint32_t)a.ws.scap)
+          gstore(&a.ws.cand[((int64_t)(u * G + h) * kSlots + slot) * a.ws.scap + pos], kept[h][tid]);
+      }
+    }
+    __syncthreads();
   }
-  asm volatile("" ::"v"(pf));
 }
 
 // ---------------------------------------------------------------- pass 4
@@ -740,57 +930,94 @@ __device__ __forceinline__ float key_to_score(uint32_t key) {
   return __uint_as_float((key & 0x80000000u) ? (key & 0x7FFFFFFFu) : ~key);
 }
 
+// Exact documented score of key (block b, bit) for head h of unit u, for
+// the fallback path (channels ascending from the act list).
+__device__ __forceinline__ float exact_score1(const int* act, int A, const float* qh, const FusedArgs& a, int u,
+                                              int64_t b, int bit) {
+  const uint64_t* Pu = a.planes + (int64_t)u * kD * kPlanes * a.nb_cap + b;
+  const uint16_t* Su = a.scales + (int64_t)u * kD * a.nb_cap + b;
+  float acc = 0.0f;
+  for (int ai = 0; ai < A; ++ai) {
+    const int e = act[ai], j = e & 0xFF, t = e >> 8;
+    const float af = half_bits_to_float(Su[(int64_t)j * a.nb_cap]);
+    uint32_t c = 0;
+    for (int p = 0; p < t; ++p) c = 2u * c + (uint32_t)((Pu[(int64_t)(4 * j + p) * a.nb_cap] >> bit) & 1ull);
+    const float y = (float)c + (0.5f - (float)(1 << (t - 1)));
+    const float khat = __fmul_rn(y, __fmul_rn(af, __uint_as_float((uint32_t)(128 - t) << 23)));
+    acc = __fmaf_rn(qh[ai], khat, acc);
+  }
+  return acc;
+}
+
 template <int G>
 __global__ __launch_bounds__(kSelThreads) void fused_select_kernel(FusedArgs a, int32_t* __restrict__ idx,
                                                                    float* __restrict__ val) {
   extern __shared__ uint64_t buf[];
-  __shared__ int act[kD];         // active channels and queries for the exact fallback
-  __shared__ float qa[kD][G];
+  __shared__ int act[kD];          // active channels ascending (fallback)
+  __shared__ float qa[kD];         // q of this row's head per active channel
   __shared__ int nact;
   __shared__ int s_count;
   __shared__ uint64_t s_thr;
+  __shared__ int wc[2];
   const int r = blockIdx.x, u = r / G, h = r % G, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   int64_t nu, lo, hi;
   row_window(a, u, &nu, &lo, &hi, false);
   const int k = a.k;
-  const uint32_t C = a.ws.cnt[r];
-  const float tau = a.ws.tau[r];
-  const bool fallback = C > (uint32_t)a.ws.cap || (C < (uint32_t)k && tau != kNegInf);
+  __shared__ uint32_t s_sub[kSlots];
+  if (tid < kSlots) s_sub[tid] = gload(a.ws.cnt + r * kSlots + tid);
+  __syncthreads();
+  uint32_t C = 0;
+  bool sub_over = false;
+  for (int q2 = 0; q2 < kSlots; ++q2) {
+    C += s_sub[q2];
+    sub_over |= s_sub[q2] > (uint32_t)a.ws.scap;
+  }
+  const float tau = gload(a.ws.tau + r);
+  // direct: few enough eligible keys to score them all; fallback: the filter
+  // under-collected or a list overflowed
+  const bool direct = hi - lo <= a.ws.cap;
+  const bool fallback =
+      !direct && (sub_over || C > (uint32_t)kSelCap || C < (uint32_t)k || gload(a.ws.uovf + u) != 0u || tau == kNegInf);
   int count;
-  if (!fallback) {
+  if (!direct && !fallback) {
     count = (int)C;
-    int P = 1;
-    while (P < count) P <<= 1;
-    for (int i = tid; i < P; i += kSelThreads) buf[i] = i < count ? a.ws.cand[(int64_t)r * a.ws.cap + i] : 0ull;
+    int P2 = 1;
+    while (P2 < count) P2 <<= 1;
+    for (int i = tid; i < P2; i += kSelThreads) {
+      uint64_t v = 0ull;
+      if (i < count) {  // element i of the concatenated sub-lists
+        int q2 = 0;
+        uint32_t off = (uint32_t)i;
+        while (off >= s_sub[q2]) off -= s_sub[q2++];
+        v = gload(a.ws.cand + ((int64_t)r * kSlots + q2) * a.ws.scap + off);
+      }
+      buf[i] = v;
+    }
     __syncthreads();
-    bitonic_desc(buf, P);
+    bitonic_desc(buf, P2);
   } else {
     // exact recomputation of the row: a streaming top-k over all eligible keys
-    if (tid == 0) set_status(a.st, FATHOM_DEV_TOPK_FALLBACK);
-    {
-      __shared__ int wc[2];
-      int t = 0;
-      if (tid < kD) {
-        t = a.depths[(int64_t)u * kD + tid];
-        t = t > kPlanes ? kPlanes : t;
-      }
-      const bool on = tid < kD && t > 0;
-      const uint64_t m = __ballot(on);
-      if (tid < kD && lane == 0) wc[wave] = __popcll(m);
-      __syncthreads();
-      if (on) act[(wave == 1 ? wc[0] : 0) + __popcll(m & lanemask_lt(lane))] = tid | (t << 8);
-      if (tid == 0) nact = wc[0] + wc[1];
-      __syncthreads();
-      for (int x = tid; x < nact * G; x += kSelThreads) {
-        const int ai = x / G, hh = x % G;
-        qa[ai][hh] = load_q(a.q, a.qdt, ((int64_t)u * G + hh) * kD + (act[ai] & 0xFF));
-      }
+    int t = 0;
+    if (tid < kD) {
+      t = a.depths[(int64_t)u * kD + tid];
+      t = t > kPlanes ? kPlanes : t;
     }
+    const bool on = tid < kD && t > 0;
+    const uint64_t m = __ballot(on);
+    if (tid < kD && lane == 0) wc[wave] = __popcll(m);
+    __syncthreads();
+    if (on) act[(wave == 1 ? wc[0] : 0) + __popcll(m & lanemask_lt(lane))] = tid | (t << 8);
     if (tid == 0) {
+      nact = wc[0] + wc[1];
       s_count = 0;
       s_thr = 0ull;
+      if (fallback) set_status(a.st, FATHOM_DEV_TOPK_FALLBACK);
     }
     __syncthreads();
+    for (int x = tid; x < nact; x += kSelThreads)
+      qa[x] = load_q(a.q, a.qdt, ((int64_t)u * G + h) * kD + (act[x] & 0xFF));
+    __syncthreads();
+    const int A = nact;
     const int nwaves = kSelThreads / kWave;
     const int64_t bfirst = lo / kBlockTokens, bend = (hi + kBlockTokens - 1) / kBlockTokens;
     for (int64_t bb = bfirst; bb < bend; bb += nwaves) {
@@ -799,9 +1026,8 @@ __global__ __launch_bounds__(kSelThreads) void fused_select_kernel(FusedArgs a, 
       const bool elig = b < bend && i >= lo && i < hi;
       uint64_t comp = 0ull;
       if (elig) {
-        float s[G];
-        exact_scores<G>(act, nact, qa, a, u, b, lane, s);
-        comp = ((uint64_t)score_key(s[h]) << 32) | (uint64_t)(~(uint32_t)i);
+        const float s = exact_score1(act, A, qa, a, u, b, lane);
+        comp = ((uint64_t)score_key(s) << 32) | (uint64_t)(~(uint32_t)i);
       }
       const uint64_t thr = s_thr;
       const bool add = elig && comp > thr;
@@ -868,13 +1094,14 @@ static fathom_status launch_fused_g(const FusedArgs& fa, int U, int32_t* idx, fl
       return FATHOM_ERR_HIP;
     attr = true;
   }
-  hipLaunchKernelGGL(fused_plan_kernel, dim3(U), dim3(kD), 0, s, fa);
   dim3 gs((unsigned)((fa.ws.s_groups + kFW - 1) / kFW), (unsigned)U);
   hipLaunchKernelGGL(fused_sample_kernel<G>, gs, dim3(kFT), 0, s, fa);
   const size_t tau_lds = (size_t)fa.ws.s_groups * kGrp * kBlockTokens * 4;
   hipLaunchKernelGGL(fused_tau_kernel, dim3(R), dim3(kSelThreads), tau_lds, s, fa, G);
-  dim3 gf((unsigned)((fa.nb_cap + kRange - 1) / kRange), (unsigned)U);
+  const int64_t ngroups = (fa.nb_cap + kGrp - 1) / kGrp;
+  dim3 gf((unsigned)((ngroups + kGroupsPerWG - 1) / kGroupsPerWG), (unsigned)U);
   hipLaunchKernelGGL(fused_full_kernel<G>, gf, dim3(kFT), 0, s, fa);
+  hipLaunchKernelGGL(fused_rescore_kernel<G>, dim3((unsigned)fa.ws.nwg, (unsigned)U), dim3(kRsT), 0, s, fa);
   hipLaunchKernelGGL(fused_select_kernel<G>, dim3(R), dim3(kSelThreads), (size_t)kSelCap * 8, s, fa, idx, val);
   FATHOM_LAUNCH_CHECK();
   return FATHOM_OK;
