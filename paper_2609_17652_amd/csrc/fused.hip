@@ -43,12 +43,12 @@ constexpr int kChunkRows = 64;    // plane rows staged per chunk (padded)
 constexpr int kStageK = kChunkRows / 8;  // rows loaded per lane per chunk (8 lanes per row)
 constexpr int kChunkDw = 16;      // U dwords per chunk (a full dword has >= 4 rows)
 constexpr int kMaxDw = kD / 4;
-constexpr int kGroupsPerWave = 4; // full pass: groups per wave, interleaved across the workgroup
-constexpr int kGroupsPerWG = kFW * kGroupsPerWave;
+constexpr int kResidentWG = 768;  // full-pass workgroups resident at once on MI355X (256 CUs x 3)
+constexpr int kMaxGroupsPerWave = 32;  // keeps a workgroup's key offsets within 16 bits
 constexpr int kWGQ = 512;        // full pass: candidate keys a workgroup gathers in LDS before writing
-constexpr int kWGCap = 2048;     // candidate keys per full-pass workgroup (more: exact fallback)
-constexpr int kRsT = 256;        // re-scoring threads per workgroup
+constexpr int kCapPerGroup = 128;  // candidate keys recorded per group of a full-pass workgroup (more: exact fallback)
 constexpr int kSlots = 8;        // survivor sub-lists per row (spreads the append counters)
+constexpr int kSmp = 64;         // sampled proxies kept per (row, sampled group): 16 lanes x 4
 constexpr int kSampleGroups = 64; // at most this many sampled groups (512 blocks) per row
 constexpr int kSelThreads = 1024;
 constexpr int kSelCap = 16384;    // LDS composites in the select kernel
@@ -58,11 +58,13 @@ struct FusedWs {
   float* tau;       // [R] threshold on exact scores (-inf: every eligible key is kept)
   uint32_t* cnt;    // [R][kSlots] survivors appended to sub-list s
   uint64_t* cand;   // [R][kSlots][scap] survivors: score_key << 32 | ~index
-  uint32_t* ecnt;   // [U][nwg] candidate keys found by full-pass workgroup w (> kWGCap: overflow)
-  uint32_t* ent;    // [U][nwg][kWGCap] key offset from the workgroup's first block | head mask << 16
+  uint32_t* ent;    // [U][nwg][wgcap] key offset from the workgroup's first block | head mask << 16
   uint32_t* uovf;   // [U] a workgroup of the unit overflowed its list: exact fallback for the unit
   int64_t nwg;      // full-pass workgroups per unit
-  float* sample;    // [R][s_groups * 512] proxies of sampled keys
+  int gpw;          // full pass: groups per wave, interleaved across the workgroup
+  int wgcap;        // candidate keys recorded per full-pass workgroup: kCapPerGroup per group
+  float* sample;    // [R][s_groups][128] per sampled group: each lane's two largest proxies
+  uint32_t* bnd;    // [R][8] score keys splitting the survivors into kSlots ranges (select pass)
   int cap, scap;  // survivors per row (select kernel), per sub-list
   int64_t s_gstride;  // sample every s_gstride-th group of 8 blocks
   int64_t s_groups;   // sampled groups per row
@@ -85,19 +87,26 @@ static inline void fused_geometry(int64_t nb_cap, int64_t* gstride, int64_t* sgr
 
 static inline int fused_scap(int k) { return fused_cap(k) / 4; }
 
-static inline int64_t fused_nwg(int64_t nb_cap) {
+// Groups per wave: enough that the full pass over all units fits in one round
+// of resident workgroups.
+static inline int fused_gpw(int U, int64_t nb_cap) {
   const int64_t ng = (nb_cap + kGrp - 1) / kGrp;
-  return (ng + kGroupsPerWG - 1) / kGroupsPerWG;
+  int64_t g = ((int64_t)U * ng + (int64_t)kFW * kResidentWG - 1) / ((int64_t)kFW * kResidentWG);
+  return (int)(g < 1 ? 1 : g > kMaxGroupsPerWave ? kMaxGroupsPerWave : g);
+}
+
+static inline int64_t fused_nwg(int U, int64_t nb_cap) {
+  const int64_t ng = (nb_cap + kGrp - 1) / kGrp, per = (int64_t)kFW * fused_gpw(U, nb_cap);
+  return (ng + per - 1) / per;
 }
 
 size_t fused_ws_bytes(int R, int U, int64_t nb_cap, int k) {
   int64_t s, sg;
   if (nb_cap < 1) nb_cap = 1;
   fused_geometry(nb_cap, &s, &sg);
-  const size_t nw = (size_t)U * fused_nwg(nb_cap);
+  const size_t nw = (size_t)U * fused_nwg(U, nb_cap);
   return a256((size_t)R * 4) + a256((size_t)R * kSlots * 4) + a256((size_t)R * kSlots * fused_scap(k) * 8) +
-         a256(nw * 4) +
-         a256(nw * kWGCap * 4) + a256((size_t)U * 4) + a256((size_t)R * sg * kGrp * kBlockTokens * 4);
+         a256(nw * (size_t)kCapPerGroup * kFW * fused_gpw(U, nb_cap) * 4) + a256((size_t)U * 4) + a256((size_t)R * kSlots * 4) + a256((size_t)R * sg * kSmp * 4);
 }
 
 static FusedWs fused_carve(void* ws, int R, int U, int64_t nb_cap, int k) {
@@ -106,15 +115,17 @@ static FusedWs fused_carve(void* ws, int R, int U, int64_t nb_cap, int k) {
   fused_geometry(nb_cap, &w.s_gstride, &w.s_groups);
   w.cap = fused_cap(k);
   w.scap = fused_scap(k);
-  w.nwg = fused_nwg(nb_cap);
+  w.nwg = fused_nwg(U, nb_cap);
+  w.gpw = fused_gpw(U, nb_cap);
+  w.wgcap = kCapPerGroup * kFW * w.gpw;
   const size_t nw = (size_t)U * w.nwg;
   char* p = reinterpret_cast<char*>(ws);
   w.tau = reinterpret_cast<float*>(p); p += a256((size_t)R * 4);
   w.cnt = reinterpret_cast<uint32_t*>(p); p += a256((size_t)R * kSlots * 4);
   w.cand = reinterpret_cast<uint64_t*>(p); p += a256((size_t)R * kSlots * w.scap * 8);
-  w.ecnt = reinterpret_cast<uint32_t*>(p); p += a256(nw * 4);
-  w.ent = reinterpret_cast<uint32_t*>(p); p += a256(nw * kWGCap * 4);
+  w.ent = reinterpret_cast<uint32_t*>(p); p += a256(nw * (size_t)w.wgcap * 4);
   w.uovf = reinterpret_cast<uint32_t*>(p); p += a256((size_t)U * 4);
+  w.bnd = reinterpret_cast<uint32_t*>(p); p += a256((size_t)R * kSlots * 4);
   w.sample = reinterpret_cast<float*>(p);
   return w;
 }
@@ -164,7 +175,8 @@ template <int G4>
 struct alignas(16) WaveLds {
   uint32_t rows[kChunkRows][2][kGrp];  // [row][32-bit half][block], rotated
   uint16_t scl[kChunkRows][kGrp];      // fp16 scales of the chunk's channels
-  uint32_t w8[kGrp][kChunkDw][G4];     // packed int8 weights
+  uint32_t wB[kGrp][G4][kChunkDw];     // packed int8 weights: [block][head][U dword], 4 channels a dword
+  uint32_t zero16[4];                  // a zero MFMA operand for the lanes that carry no weights
   float sdel[kGrp][8];                 // delta (0: no usable bound)
   float sinv[kGrp][8];                 // 1 / delta
   float seb[kGrp][8];                  // sum |w - delta w8| zmax
@@ -424,7 +436,7 @@ __device__ void weights(const UnitLds<G>& P, WaveLds<G4>& W, int c, bool first, 
   float eb = 0.0f, sw = 0.0f;
   int bias = 0;
   if (bv) {
-    uint8_t* w8b = reinterpret_cast<uint8_t*>(&W.w8[g][0][0]);
+    uint8_t* w8b = reinterpret_cast<uint8_t*>(&W.wB[g][h][0]);
     for (int ai = a0 + kk; ai < a1; ai += KL) {
       const int al = ai - a0;
       const float w = __fmul_rn(P.qa8[ai][hh], half_bits_to_float(W.scl[al][g]));
@@ -435,7 +447,7 @@ __device__ void weights(const UnitLds<G>& P, WaveLds<G4>& W, int c, bool first, 
       eb = __fmaf_rn(fabsf(__fmaf_rn(r, delta, -w)), zm, eb);
       sw = __fadd_rn(sw, fabsf(w));
       bias -= ri * (int)zm;
-      w8b[((al >> 2) * G4 + h) * 4 + (al & 3)] = (uint8_t)(ri & 0xFF);
+      w8b[al] = (uint8_t)(ri & 0xFF);
     }
   }
 #pragma unroll
@@ -474,48 +486,64 @@ __device__ void weights(const UnitLds<G>& P, WaveLds<G4>& W, int c, bool first, 
   }
 }
 
-// Integer proxy sums of chunk c for the 8 blocks, added to acc.
+// Integer proxy sums of chunk c for the 8 blocks, added to acc.  Per 4 U
+// dwords (16 channels) one v_mfma_i32_16x16x64_i8 per block: A = the 16 proxy
+// digits of each lane's key; B is block-diagonal, so lane group g' of A (keys
+// 16g'..16g'+15) meets only the weights in columns 4g'..4g'+3 (heads 0..3):
+// C[i][4g' + h] = sum_j z'_{16g'+i, j} w8_{j, h}.  Lane l then holds heads
+// 4p + l%4 of keys 16((l%16)/4) + 4(l/16) + r, r = 0..3, in acc[g][p][r].
+typedef __attribute__((ext_vector_type(4))) int v4i;
 template <int G, int G4>
 __device__ __forceinline__ void chunk_proxy(const UnitLds<G>& P, const WaveLds<G4>& W, int c, uint32_t M0, int s,
-                                            int acc[kGrp][G]) {
+                                            v4i (&acc)[kGrp][G4 / 4]) {
+  constexpr int NP = G4 / 4;
   const int lane = threadIdx.x & 63, half = lane >> 5;
   const int d0 = uni(P.chd[c]), d1 = uni(P.chd[c + 1]), cr0 = uni(P.chr[c]);
-  for (int d = d0; d < d1; ++d) {
-    const int nq = uni((int)P.dnq[d]);
-    const int rb = uni((int)P.drow[d]);
-    uint32_t zr[kGrp];
+  const bool wlane = (lane >> 4) == ((lane & 15) >> 2);
 #pragma unroll
-    for (int g = 0; g < kGrp; ++g) zr[g] = 0u;
-    for (int iq = 0; iq < nq; ++iq) {
-      const int r = rb + 4 * iq;
-      const uint4 sh = *reinterpret_cast<const uint4*>(&P.rsh[cr0 + r]);
-      uint4 x[4][2];
+  for (int gh = 0; gh < kGrp; gh += 4) {  // blocks gh .. gh+3
+    for (int db = d0; db < d1; db += 4) {
+      uint32_t zq[4][4];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const uint4* rp = reinterpret_cast<const uint4*>(&W.rows[r + i][half][0]);
-        x[i][0] = rp[0];
-        x[i][1] = rp[1];
+      for (int q = 0; q < 4; ++q) {
+        uint32_t zr[4] = {0u, 0u, 0u, 0u};
+        const int d = db + q;
+        if (d < d1) {
+          const int nq = uni((int)P.dnq[d]);
+          const int rb = uni((int)P.drow[d]);
+          for (int iq = 0; iq < nq; ++iq) {
+            const int r = rb + 4 * iq;
+            const uint4 sh = *reinterpret_cast<const uint4*>(&P.rsh[cr0 + r]);
+            uint4 x[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) x[i] = *reinterpret_cast<const uint4*>(&W.rows[r + i][half][gh]);
+            const uint32_t m[4] = {__builtin_amdgcn_alignbit(M0, M0, sh.x), __builtin_amdgcn_alignbit(M0, M0, sh.y),
+                                   __builtin_amdgcn_alignbit(M0, M0, sh.z), __builtin_amdgcn_alignbit(M0, M0, sh.w)};
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              zr[0] |= x[i].x & m[i];
+              zr[1] |= x[i].y & m[i];
+              zr[2] |= x[i].z & m[i];
+              zr[3] |= x[i].w & m[i];
+            }
+          }
+        }
+#pragma unroll
+        for (int g = 0; g < 4; ++g) zq[q][g] = __builtin_amdgcn_alignbit(zr[g], zr[g], (uint32_t)s);
       }
-      const uint32_t m[4] = {__builtin_amdgcn_alignbit(M0, M0, sh.x), __builtin_amdgcn_alignbit(M0, M0, sh.y),
-                             __builtin_amdgcn_alignbit(M0, M0, sh.z), __builtin_amdgcn_alignbit(M0, M0, sh.w)};
+      const int mq = (db - d0) >> 2;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        zr[0] |= x[i][0].x & m[i];
-        zr[1] |= x[i][0].y & m[i];
-        zr[2] |= x[i][0].z & m[i];
-        zr[3] |= x[i][0].w & m[i];
-        zr[4] |= x[i][1].x & m[i];
-        zr[5] |= x[i][1].y & m[i];
-        zr[6] |= x[i][1].z & m[i];
-        zr[7] |= x[i][1].w & m[i];
+      for (int pp = 0; pp < NP; ++pp) {
+        const int hh = 4 * pp + (lane & 3);
+        const bool wl = wlane && hh < G;
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const uint32_t* src = wl ? &W.wB[gh + g][hh < G4 ? hh : 0][4 * mq] : W.zero16;
+          const v4i bv = *reinterpret_cast<const v4i*>(src);
+          const v4i av = {(int)zq[0][g], (int)zq[1][g], (int)zq[2][g], (int)zq[3][g]};
+          acc[gh + g][pp] = __builtin_amdgcn_mfma_i32_16x16x64_i8(av, bv, acc[gh + g][pp], 0, 0, 0);
+        }
       }
-    }
-    const int dl = d - d0;
-#pragma unroll
-    for (int g = 0; g < kGrp; ++g) {
-      const uint32_t z = __builtin_amdgcn_alignbit(zr[g], zr[g], (uint32_t)s);
-#pragma unroll
-      for (int h = 0; h < G; ++h) acc[g][h] = __builtin_amdgcn_sdot4((int)z, (int)W.w8[g][dl][h], acc[g][h], false);
     }
   }
 }
@@ -530,11 +558,11 @@ __device__ void wave_groups(const UnitLds<G>& P, WaveLds<G4>& W, const FusedArgs
   const int nch = uni(P.nch);
   if (ngroups <= 0 || nch <= 0) {
     for (int gi = 0; gi < ngroups; ++gi) {  // no active channel: every proxy is 0 with E = 0
-      int acc[kGrp][G];
+      v4i acc[kGrp][G4 / 4];
 #pragma unroll
       for (int g = 0; g < kGrp; ++g)
 #pragma unroll
-        for (int h = 0; h < G; ++h) acc[g][h] = 0;
+        for (int pp = 0; pp < G4 / 4; ++pp) acc[g][pp] = v4i{0, 0, 0, 0};
       const int64_t gb = group_block(gi);
       {
         const int g = lane >> 3, h = lane & 7;
@@ -560,11 +588,12 @@ __device__ void wave_groups(const UnitLds<G>& P, WaveLds<G4>& W, const FusedArgs
   const int items = ngroups * nch;
   Stage S;
   stage_load<G>(S, P, a, u, group_block(0), 0);
-  int acc[kGrp][G];
+  if (lane < 4) W.zero16[lane] = 0u;
+  v4i acc[kGrp][G4 / 4];
 #pragma unroll
   for (int g = 0; g < kGrp; ++g)
 #pragma unroll
-    for (int h = 0; h < G; ++h) acc[g][h] = 0;
+    for (int pp = 0; pp < G4 / 4; ++pp) acc[g][pp] = v4i{0, 0, 0, 0};
   for (int it = 0; it < items; ++it) {
     const int gi = it / nch, c = it - gi * nch;
     const int64_t gb = group_block(gi);
@@ -582,7 +611,7 @@ __device__ void wave_groups(const UnitLds<G>& P, WaveLds<G4>& W, const FusedArgs
 #pragma unroll
       for (int g = 0; g < kGrp; ++g)
 #pragma unroll
-        for (int h = 0; h < G; ++h) acc[g][h] = 0;
+        for (int pp = 0; pp < G4 / 4; ++pp) acc[g][pp] = v4i{0, 0, 0, 0};
     }
     wave_lds_sync();  // this item's LDS reads are done before the next stage_store
   }
@@ -591,7 +620,7 @@ __device__ void wave_groups(const UnitLds<G>& P, WaveLds<G4>& W, const FusedArgs
 // ---------------------------------------------------------------- pass 1
 // Each workgroup: 4 sampled groups (one per wave) of the unit.
 template <int G>
-__global__ __launch_bounds__(kFT) void fused_sample_kernel(FusedArgs a) {
+__global__ __launch_bounds__(kFT, 3) void fused_sample_kernel(FusedArgs a) {
   constexpr int G4 = (G + 3) & ~3;
   __shared__ UnitLds<G> P;
   __shared__ WaveLds<G4> WL[kFW];
@@ -604,113 +633,215 @@ __global__ __launch_bounds__(kFT) void fused_sample_kernel(FusedArgs a) {
   if (sg >= a.ws.s_groups) return;
   const int64_t gb = sg * a.ws.s_gstride * kGrp;
   WaveLds<G4>& W = WL[wave];
-  auto put = [&](int64_t gbb, int (&acc)[kGrp][G]) {
+  // lane l holds heads 4p + l%4 of 4 keys per block; it keeps the four largest
+  // of its 32 proxies per head: the m-th largest of what the 16 lanes of a
+  // head keep is at most the m-th largest sampled proxy
+  const int kl = 16 * ((lane & 15) >> 2) + 4 * (lane >> 4);
+  auto put = [&](int64_t gbb, v4i (&acc)[kGrp][G4 / 4]) {
 #pragma unroll
-    for (int g = 0; g < kGrp; ++g) {
-      const int64_t b = gbb + g;
-      const int64_t i = b * kBlockTokens + lane;
+    for (int pp = 0; pp < G4 / 4; ++pp) {
+      const int hh = 4 * pp + (lane & 3);
+      const int hc = hh < G ? hh : 0;
+      float t[4] = {kNegInf, kNegInf, kNegInf, kNegInf};
 #pragma unroll
-      for (int h = 0; h < G; ++h) {
-        // the proxy itself (exact in fp32): tau only steers how many keys are
-        // re-scored; the candidate count, not tau, guarantees the result
-        float v = kNegInf;
-        const float del = W.sdel[g][h];
-        if (b < nbu && i >= lo && i < hi && del > 0.0f)
-          v = __fmul_rn(0.5f * del, (float)(acc[g][h] + W.sbias[g][h]));
-        gstore(&a.ws.sample[((int64_t)u * G + h) * a.ws.s_groups * (kGrp * kBlockTokens) +
-                            (sg * kGrp + g) * kBlockTokens + lane], v);
+      for (int g = 0; g < kGrp; ++g) {
+        const int64_t b = gbb + g;
+        const float del = W.sdel[g][hc];
+        const int bias = W.sbias[g][hc];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int64_t i = b * kBlockTokens + kl + q;
+          // the proxy itself (exact in fp32): tau only steers how many keys are
+          // re-scored; the survivor count, not tau, guarantees the result
+          float v = kNegInf;
+          if (b < nbu && i >= lo && i < hi && del > 0.0f) v = __fmul_rn(0.5f * del, (float)(acc[g][pp][q] + bias));
+#pragma unroll
+          for (int z = 0; z < 4; ++z) {  // insert into the descending t[0..3]
+            const float hi2 = fmaxf(t[z], v);
+            v = fminf(t[z], v);
+            t[z] = hi2;
+          }
+        }
+      }
+      if (hh < G) {
+        float* dst = a.ws.sample + (((int64_t)u * G + hh) * a.ws.s_groups + sg) * kSmp + (lane >> 2) * 4;
+#pragma unroll
+        for (int z = 0; z < 4; ++z) gstore(dst + z, t[z]);
       }
     }
   };
   if (gb < nbu) {
     wave_groups<G, G4, true>(P, W, a, u, 1, nbu, [&](int) { return gb; }, put);
   } else {
-    for (int g = 0; g < kGrp; ++g)
-      for (int h = 0; h < G; ++h)
-        a.ws.sample[((int64_t)u * G + h) * a.ws.s_groups * (kGrp * kBlockTokens) + (sg * kGrp + g) * kBlockTokens +
-                    lane] = kNegInf;
+    for (int pp = 0; pp < G4 / 4; ++pp) {
+      const int hh = 4 * pp + (lane & 3);
+      if (hh < G) {
+        float* dst = a.ws.sample + (((int64_t)u * G + hh) * a.ws.s_groups + sg) * kSmp + (lane >> 2) * 4;
+        for (int z = 0; z < 4; ++z) gstore(dst + z, kNegInf);
+      }
+    }
   }
 }
 
 // ---------------------------------------------------------------- pass 2
-// tau = the m-th largest sampled proxy, m ~ 1.25 k * (sampled / eligible) + 16;
-// tau = -inf when the row has no more eligible keys than the candidate list holds.
+// tau = the m-th largest kept sample proxy, m ~ 1.25 k * (sampled / eligible)
+// + 16; tau = -inf when the row has no more eligible keys than the survivor
+// list holds.  The kept proxies stay in registers as order-preserving keys (0
+// = unusable); the m-th largest is found bit by bit from the top with
+// block-wide counts.  The kept proxies above tau, ranked, also give kSlots - 1
+// boundaries that split the expected survivors into ranges of similar size.
+constexpr int kTauPer = kSampleGroups * kSmp / kSelThreads;  // kept proxies per thread
 __global__ __launch_bounds__(kSelThreads) void fused_tau_kernel(FusedArgs a, int G) {
-  extern __shared__ uint32_t keys[];  // the row's sample as order-preserving keys (0 = unusable)
-  __shared__ uint32_t hist[2048];
-  __shared__ uint32_t s_prefix, s_mask, s_above;
-  __shared__ int s_need, s_digit;
-  __shared__ uint32_t s_total;
-  __shared__ uint32_t part[kSelThreads / kWave];
-  const int r = blockIdx.x, u = r / G, tid = threadIdx.x;
+  __shared__ uint32_t part[2 * (kSelThreads / kWave)];
+  __shared__ uint32_t top[kSelThreads];
+  __shared__ uint32_t srt[kSelThreads];
+  __shared__ int ntop;
+  const int r = blockIdx.x, u = r / G, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   if (tid == 0 && r % G == 0) a.ws.uovf[u] = 0u;
+  if (tid < kSlots) a.ws.cnt[r * kSlots + tid] = 0u;
   int64_t nu, lo, hi;
   row_window(a, u, &nu, &lo, &hi, false);
   const int64_t m_e = hi - lo;
   if (m_e <= a.ws.cap) {
-    if (tid == 0) {
-      a.ws.tau[r] = kNegInf;
-      for (int q2 = 0; q2 < kSlots; ++q2) a.ws.cnt[r * kSlots + q2] = 0u;
-    }
+    if (tid == 0) a.ws.tau[r] = kNegInf;
     return;
   }
-  const float* smp = a.ws.sample + (int64_t)r * a.ws.s_groups * (kGrp * kBlockTokens);
-  const int ns = (int)(a.ws.s_groups * kGrp * kBlockTokens);
-  if (tid == 0) s_total = 0u;
-  __syncthreads();
-  uint32_t c = 0;
-  for (int i = tid; i < ns; i += kSelThreads) {
-    const float v = smp[i];
-    const bool use = v > kNegInf;
-    keys[i] = use ? (score_key(v) | 1u) : 0u;  // keep 0 free: NaN proxies do not occur
-    c += use;
-  }
-  atomicAdd(&s_total, c);
-  __syncthreads();
-  const int64_t m_s = s_total;
-  if (m_s == 0) {
-    if (tid == 0) {
-      a.ws.tau[r] = kNegInf;
-      for (int q2 = 0; q2 < kSlots; ++q2) a.ws.cnt[r * kSlots + q2] = 0u;
+  const float* smp = a.ws.sample + (int64_t)r * a.ws.s_groups * kSmp;
+  const int ns = (int)(a.ws.s_groups * kSmp);
+  uint32_t key[kTauPer];
+#pragma unroll
+  for (int x = 0; x < kTauPer; ++x) {
+    const int i = tid + x * kSelThreads;
+    key[x] = 0u;
+    if (i < ns) {
+      const float v = gload(smp + i);
+      if (v > kNegInf) key[x] = score_key(v) | 1u;  // keep 0 free: proxies are never NaN
     }
+  }
+  // eligible keys of the sampled groups
+  uint32_t msg = 0;
+  if (tid < a.ws.s_groups) {
+    const int64_t k0 = (int64_t)tid * a.ws.s_gstride * kGrp * kBlockTokens, k1 = k0 + kGrp * kBlockTokens;
+    const int64_t x0 = k0 > lo ? k0 : lo, x1 = k1 < hi ? k1 : hi;
+    msg = x1 > x0 ? (uint32_t)(x1 - x0) : 0u;
+  }
+  int ph = 0;  // partial sums double-buffered: one barrier per count
+  auto block_sum = [&](uint32_t v) {  // v: this wave's total (wave-uniform)
+    if (lane == 0) part[ph * (kSelThreads / kWave) + wave] = v;
+    __syncthreads();
+    uint32_t t = 0;
+#pragma unroll
+    for (int w = 0; w < kSelThreads / kWave; ++w) t += part[ph * (kSelThreads / kWave) + w];
+    ph ^= 1;
+    return t;
+  };
+  uint32_t cw = 0, uw = 0;
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) msg += __shfl_xor(msg, o, kWave);
+  cw = msg;
+#pragma unroll
+  for (int x = 0; x < kTauPer; ++x) uw += (uint32_t)__popcll(__ballot(key[x] != 0u));
+  const int64_t m_s = block_sum(cw);
+  const int64_t usable = block_sum(uw);
+  if (m_s == 0 || usable == 0) {
+    if (tid == 0) a.ws.tau[r] = kNegInf;
     return;
   }
   int64_t m = (5 * (int64_t)a.k * m_s + 4 * m_e - 1) / (4 * m_e) + 16;
-  if (m > m_s) m = m_s;
-  if (tid == 0) {
-    s_prefix = 0u;
-    s_mask = 0u;
-    s_need = (int)m;
+  if (m > usable) m = usable;
+  uint32_t prefix = 0u;
+  for (int bit = 31; bit >= 0; --bit) {
+    const uint32_t cand = prefix | (1u << bit);
+    uint32_t cnt = 0;  // wave total from ballots (scalar)
+#pragma unroll
+    for (int x = 0; x < kTauPer; ++x) cnt += (uint32_t)__popcll(__ballot(key[x] >= cand));
+    if ((int64_t)block_sum(cnt) >= m) prefix = cand;
   }
-  const int shifts[3] = {21, 10, 0}, bits[3] = {11, 11, 10};
-  for (int pass = 0; pass < 3; ++pass) {
-    for (int b = tid; b < 2048; b += kSelThreads) hist[b] = 0u;
-    __syncthreads();
-    const uint32_t prefix = s_prefix, mask = s_mask, dm = (1u << bits[pass]) - 1u;
-    for (int i = tid; i < ns; i += kSelThreads) {
-      const uint32_t key = keys[i];
-      if (key && (key & mask) == prefix) atomicAdd(&hist[(key >> shifts[pass]) & dm], 1u);
+  // rank the kept proxies >= tau (at most kSelThreads of them) for the range boundaries
+  if (tid == 0) ntop = 0;
+  __syncthreads();
+#pragma unroll
+  for (int x = 0; x < kTauPer; ++x) {
+    if (key[x] >= prefix && key[x] != 0u) {
+      const int p2 = atomicAdd(&ntop, 1);
+      if (p2 < kSelThreads) top[p2] = key[x];
     }
-    __syncthreads();
-    find_crossing(hist, (int)dm + 1, (uint32_t)s_need, part, &s_digit, &s_above);
-    if (tid == 0) {
-      s_prefix = prefix | ((uint32_t)s_digit << shifts[pass]);
-      s_mask = mask | (dm << shifts[pass]);
-      s_need = s_need - (int)s_above;
-    }
-    __syncthreads();
   }
+  __syncthreads();
+  const int nt = ntop < kSelThreads ? ntop : kSelThreads;
+  if (tid < nt) {
+    const uint32_t v = top[tid];
+    int rk = 0;
+    for (int x = 0; x < nt; ++x) {
+      const uint32_t w = top[x];
+      rk += (w > v) || (w == v && x < tid);
+    }
+    srt[rk] = v;
+  }
+  __syncthreads();
   if (tid == 0) {
-    const uint32_t key = s_prefix & ~1u;  // the low bit was forced on: round the key down
-    const uint32_t bitsf = (key & 0x80000000u) ? (key & 0x7FFFFFFFu) : ~key;
+    const uint32_t key0 = prefix & ~1u;  // the low bit was forced on: round the key down
+    const uint32_t bitsf = (key0 & 0x80000000u) ? (key0 & 0x7FFFFFFFu) : ~key0;
     a.ws.tau[r] = __uint_as_float(bitsf);
-    for (int q2 = 0; q2 < kSlots; ++q2) a.ws.cnt[r * kSlots + q2] = 0u;
   }
+  if (tid >= 1 && tid < kSlots) {
+    // boundary b: survivors with key > bnd[b] go to ranges < b
+    const int at = (int)(((int64_t)tid * nt) / kSlots);
+    a.ws.bnd[r * kSlots + tid] = nt > 0 ? (srt[at < nt ? at : nt - 1] & ~1u) : 0u;
+  }
+  if (tid == 0) a.ws.bnd[r * kSlots] = 0xFFFFFFFFu;
 }
 
 // ---------------------------------------------------------------- pass 3
+// The documented fp32 scores of key i for all G heads: active channels
+// ascending, khat exact, acc = fma(q, khat, acc); the loads of 8 channels are
+// issued together.
+constexpr int kRsChunk = 8;
 template <int G>
-__global__ __launch_bounds__(kFT) void fused_full_kernel(FusedArgs a) {
+__device__ __forceinline__ void exact_scores(const UnitLds<G>& P, const FusedArgs& a, int u, int64_t i,
+                                             float (&acc)[G]) {
+  const int64_t b = i >> 6;
+  const int hw = (int)((i >> 5) & 1), sh = (int)(i & 31), A = P.A;
+  const uint64_t* Pu = a.planes + (int64_t)u * kD * kPlanes * a.nb_cap + b;
+  const uint16_t* Su = a.scales + (int64_t)u * kD * a.nb_cap + b;
+  for (int a0 = 0; a0 < A; a0 += kRsChunk) {
+    uint32_t wd[kRsChunk][4];
+    uint16_t sc[kRsChunk];
+#pragma unroll
+    for (int K = 0; K < kRsChunk; ++K) {
+      const int x = a0 + K;
+      sc[K] = 0;
+#pragma unroll
+      for (int p = 0; p < 4; ++p) wd[K][p] = 0u;
+      if (x < A) {
+        const int e2 = P.act[P.pidx[x]], j = e2 & 0xFF, tt = e2 >> 8;
+        sc[K] = gload(Su + (int64_t)j * a.nb_cap);
+#pragma unroll
+        for (int p = 0; p < 4; ++p)
+          if (p < tt) wd[K][p] = gload(reinterpret_cast<const uint32_t*>(Pu + (int64_t)(4 * j + p) * a.nb_cap) + hw);
+      }
+    }
+#pragma unroll
+    for (int K = 0; K < kRsChunk; ++K) {
+      const int x = a0 + K;
+      if (x < A) {
+        const int pi = P.pidx[x], tt = P.act[pi] >> 8;
+        uint32_t c = 0;
+#pragma unroll
+        for (int p = 0; p < 4; ++p)
+          if (p < tt) c = 2u * c + ((wd[K][p] >> sh) & 1u);
+        const float y = (float)c + (0.5f - (float)(1 << (tt - 1)));
+        const float khat =
+            __fmul_rn(y, __fmul_rn(half_bits_to_float(sc[K]), __uint_as_float((uint32_t)(128 - tt) << 23)));
+#pragma unroll
+        for (int h = 0; h < G; ++h) acc[h] = __fmaf_rn(P.qa[pi][h], khat, acc[h]);
+      }
+    }
+  }
+}
+
+template <int G>
+__global__ __launch_bounds__(kFT, 3) void fused_full_kernel(FusedArgs a) {
   constexpr int G4 = (G + 3) & ~3;
   __shared__ UnitLds<G> P;
   __shared__ WaveLds<G4> WL[kFW];
@@ -720,162 +851,94 @@ __global__ __launch_bounds__(kFT) void fused_full_kernel(FusedArgs a) {
   int64_t nu, lo, hi;
   row_window(a, u, &nu, &lo, &hi, blockIdx.x == 0 && tid == 0);
   const int64_t nbu = (nu + kBlockTokens - 1) / kBlockTokens;
-  const int64_t g0 = (int64_t)blockIdx.x * kGroupsPerWG;  // first group of this workgroup
-  const int64_t b0 = g0 * kGrp, b1 = (g0 + kGroupsPerWG) * kGrp;
+  const int gpw = a.ws.gpw;
+  const int64_t g0 = (int64_t)blockIdx.x * kFW * gpw;  // first group of this workgroup
+  const int64_t b0 = g0 * kGrp, b1 = (g0 + (int64_t)kFW * gpw) * kGrp;
   const int64_t region = (int64_t)u * a.ws.nwg + blockIdx.x;
   // rows with no more eligible keys than the survivor list holds are
   // computed exactly by pass 4: no candidates from here
-  if (b0 >= nbu || b0 * kBlockTokens >= hi || b1 * kBlockTokens <= lo || hi - lo <= a.ws.cap) {
-    if (tid == 0) gstore(&a.ws.ecnt[region], 0u);
-    return;
-  }
+  if (b0 >= nbu || b0 * kBlockTokens >= hi || b1 * kBlockTokens <= lo || hi - lo <= a.ws.cap) return;
   if (tid == 0) wqn = 0;
   unit_setup<G>(P, a, u);
   if (tid < G) P.tau[tid] = gload(a.ws.tau + u * G + tid);
   __syncthreads();
   // this wave's groups: g0 + wave + kFW * x, those that hold eligible keys
-  int mine[kGroupsPerWave] = {0};
-  int ng = 0;
-#pragma unroll
-  for (int x = 0; x < kGroupsPerWave; ++x) {
+  // this wave's groups g0 + wave + kFW x that hold eligible keys: a contiguous range of x
+  int x_lo = gpw, x_hi = 0;
+  for (int x = 0; x < gpw; ++x) {
     const int64_t gbx = (g0 + wave + kFW * x) * kGrp;
-    if (gbx < nbu && gbx * kBlockTokens < hi && (gbx + kGrp) * kBlockTokens > lo) mine[ng++] = x;
+    if (gbx < nbu && gbx * kBlockTokens < hi && (gbx + kGrp) * kBlockTokens > lo) {
+      x_lo = x < x_lo ? x : x_lo;
+      x_hi = x + 1;
+    }
   }
+  const int ng = x_hi > x_lo ? x_hi - x_lo : 0;
   WaveLds<G4>& W = WL[wave];
-  auto gblock = [&](int gi) {
-    int x = 0;
+  auto gblock = [&](int gi) { return (g0 + wave + kFW * (int64_t)(x_lo + gi)) * kGrp; };
+  // lane l holds heads 4p + l%4 of keys 16((l%16)/4) + 4(l/16) + q of each block
+  const int kl = 16 * ((lane & 15) >> 2) + 4 * (lane >> 4);
+  auto put = [&](int64_t gbb, v4i (&acc)[kGrp][G4 / 4]) {
+    // eligibility relative to the group's first key (32-bit)
+    const int64_t key0 = gbb * kBlockTokens;
+    const int64_t lr = lo - key0, hr = hi - key0, br = nbu - gbb;
+    const int lo_r = lr < -1 ? -1 : lr > 1024 ? 1024 : (int)lr;
+    const int hi_r = hr < -1 ? -1 : hr > 1024 ? 1024 : (int)hr;
+    const int nb_r = br < 0 ? 0 : br > kGrp ? kGrp : (int)br;
 #pragma unroll
-    for (int y = 0; y < kGroupsPerWave; ++y)
-      if (y == gi) x = mine[y];
-    return (g0 + wave + kFW * x) * kGrp;
-  };
-  auto put = [&](int64_t gbb, int (&acc)[kGrp][G]) {
+    for (int pp = 0; pp < G4 / 4; ++pp) {
+      const int hh = 4 * pp + (lane & 3);
+      int thr[kGrp];
 #pragma unroll
-    for (int g = 0; g < kGrp; ++g) {
-      const int64_t b = gbb + g;
-      const int64_t i = b * kBlockTokens + lane;
-      const bool elig = b < nbu && i >= lo && i < hi;
-      int thr[8];
-      *reinterpret_cast<int4*>(&thr[0]) = *reinterpret_cast<const int4*>(&W.sthr[g][0]);
-      if (G > 4) *reinterpret_cast<int4*>(&thr[4]) = *reinterpret_cast<const int4*>(&W.sthr[g][4]);
-      int hm = 0;
+      for (int g = 0; g < kGrp; ++g) thr[g] = hh < G ? W.sthr[g][hh] : INT32_MAX;
+      uint32_t bits = 0u;  // bit 4g + q: key q of block g reaches its threshold
 #pragma unroll
-      for (int h = 0; h < G; ++h) hm |= (int)(acc[g][h] >= thr[h]) << h;
-      hm = elig ? hm : 0;
-      const uint64_t any = __ballot(hm != 0);
-      if (any) {
-        int base = 0;
-        if (lane == 0) base = atomicAdd(&wqn, __popcll(any));
-        base = __shfl(base, 0, kWave);
-        const int pos = base + __popcll(any & lanemask_lt(lane));
-        const uint32_t en = (uint32_t)((b - b0) * kBlockTokens + lane) | ((uint32_t)hm << 16);
-        if (hm && pos < kWGQ) wq[pos] = en;
-        else if (hm && pos < kWGCap) gstore(&a.ws.ent[region * kWGCap + pos], en);
+      for (int g = 0; g < kGrp; ++g)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) bits |= (uint32_t)(acc[g][pp][q] >= thr[g]) << (4 * g + q);
+      if (__ballot(bits != 0u)) {
+        while (bits) {
+          const int bi = __ffs((int)bits) - 1;
+          bits &= bits - 1u;
+          const int g = bi >> 2, rel = g * kBlockTokens + kl + (bi & 3);
+          if (rel >= lo_r && rel < hi_r && g < nb_r) {
+            const int pos = atomicAdd(&wqn, 1);
+            const uint32_t en = (uint32_t)((gbb - b0) * kBlockTokens + rel) | (1u << (16 + hh));
+            if (pos < kWGQ) wq[pos] = en;
+            else if (pos < a.ws.wgcap) gstore(&a.ws.ent[region * a.ws.wgcap + pos], en);
+          }
+        }
       }
     }
   };
   wave_groups<G, G4, false>(P, W, a, u, ng, nbu, gblock, put);
   __syncthreads();
+  // exact documented scores of this workgroup's candidates (their plane lines
+  // are still in L2); survivors go to the rows' lists through LDS, one append
+  // per pass and head
   const int nq = wqn;
-  const int nc = nq < kWGQ ? nq : kWGQ;
-  for (int e = tid; e < nc; e += kFT) gstore(&a.ws.ent[region * kWGCap + e], wq[e]);
-  if (tid == 0) gstore(&a.ws.ecnt[region], (uint32_t)nq);
-}
-
-// ---------------------------------------------------------------- pass 3b
-// The documented fp32 scores (active channels ascending, khat exact, acc =
-// fma(q, khat, acc)) of the candidates of one full-pass workgroup, one key per
-// thread with the loads of 16 channels in flight together; keys with score >=
-// tau for a head in their mask join that row's survivor list.
-constexpr int kRsChunk = 16;
-template <int G>
-__global__ __launch_bounds__(kRsT) void fused_rescore_kernel(FusedArgs a) {
-  __shared__ int act[kD];  // j | t << 8, channels ascending
-  __shared__ float qa[kD][G];
-  __shared__ float tau[G];
-  __shared__ int wc[2];
-  __shared__ uint64_t kept[G][kRsT];  // this pass's survivors per head
-  __shared__ int nk[G];
-  __shared__ uint32_t kbase[G];
-  const int u = blockIdx.y, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int64_t region = (int64_t)u * a.ws.nwg + blockIdx.x;
-  const uint32_t nq = gload(a.ws.ecnt + region);
-  if (nq == 0) return;
-  if (nq > (uint32_t)kWGCap) {
+  if (nq > a.ws.wgcap) {
     if (tid == 0) set_status(a.ws.uovf + u, 1u);
     return;
   }
-  int t = 0;
-  if (tid < kD) {
-    t = gload(a.depths + (int64_t)u * kD + tid);
-    t = t > kPlanes ? kPlanes : t;
-  }
-  const uint64_t m = __ballot(tid < kD && t > 0);
-  if (tid < kD && lane == 0) wc[wave] = __popcll(m);
-  __syncthreads();
-  if (tid < kD && t > 0) act[(wave == 1 ? wc[0] : 0) + __popcll(m & lanemask_lt(lane))] = tid | (t << 8);
-  if (tid < G) tau[tid] = gload(a.ws.tau + u * G + tid);
-  __syncthreads();
-  const int A = wc[0] + wc[1];
-  for (int x = tid; x < A * G; x += kRsT) qa[x / G][x % G] = load_q(a.q, a.qdt, ((int64_t)u * G + x % G) * kD + (act[x / G] & 0xFF));
-  __syncthreads();
-  const int64_t b0 = (int64_t)blockIdx.x * kGroupsPerWG * kGrp;
-  const int slot = (int)(blockIdx.x % kSlots);
-  for (uint32_t e0 = 0; e0 < nq; e0 += kRsT) {
+  uint64_t(*kept)[kFT] = reinterpret_cast<uint64_t(*)[kFT]>(&WL[0]);  // the staging area is free now
+  __shared__ int nk[G];
+  __shared__ uint32_t kbase[G];
+  for (int e0 = 0; e0 < nq; e0 += kFT) {
+    const int slot = (int)((blockIdx.x + e0 / kFT) % kSlots);  // spread the appends over the sub-lists
     if (tid < G) nk[tid] = 0;
     __syncthreads();
-    const uint32_t e = e0 + tid;
+    const int e = e0 + tid;
     uint32_t en = 0u;
-    if (e < nq) en = gload(a.ws.ent + region * kWGCap + e);
+    if (e < nq) en = e < kWGQ ? wq[e] : gload(a.ws.ent + region * a.ws.wgcap + e);
     const int hm = (int)(en >> 16);
     const int64_t i = b0 * kBlockTokens + (int64_t)(en & 0xFFFFu);
     float acc[G];
 #pragma unroll
     for (int h = 0; h < G; ++h) acc[h] = 0.0f;
-    if (hm) {
-      const int64_t b = i >> 6;
-      const int hw = (int)((i >> 5) & 1), sh = (int)(i & 31);
-      const uint64_t* Pu = a.planes + (int64_t)u * kD * kPlanes * a.nb_cap + b;
-      const uint16_t* Su = a.scales + (int64_t)u * kD * a.nb_cap + b;
-      for (int a0 = 0; a0 < A; a0 += kRsChunk) {
-        uint32_t wd[kRsChunk][4];
-        uint16_t sc[kRsChunk];
-#pragma unroll
-        for (int K = 0; K < kRsChunk; ++K) {
-          const int x = a0 + K;
-          sc[K] = 0;
-#pragma unroll
-          for (int p = 0; p < 4; ++p) wd[K][p] = 0u;
-          if (x < A) {
-            const int e2 = act[x], j = e2 & 0xFF, tt = e2 >> 8;
-            sc[K] = gload(Su + (int64_t)j * a.nb_cap);
-#pragma unroll
-            for (int p = 0; p < 4; ++p)
-              if (p < tt) wd[K][p] = gload(reinterpret_cast<const uint32_t*>(Pu + (int64_t)(4 * j + p) * a.nb_cap) + hw);
-          }
-        }
-#pragma unroll
-        for (int K = 0; K < kRsChunk; ++K) {
-          const int x = a0 + K;
-          if (x < A) {
-            const int tt = act[x] >> 8;
-            uint32_t c = 0;
-#pragma unroll
-            for (int p = 0; p < 4; ++p)
-              if (p < tt) c = 2u * c + ((wd[K][p] >> sh) & 1u);
-            const float y = (float)c + (0.5f - (float)(1 << (tt - 1)));
-            const float khat =
-                __fmul_rn(y, __fmul_rn(half_bits_to_float(sc[K]), __uint_as_float((uint32_t)(128 - tt) << 23)));
-#pragma unroll
-            for (int h = 0; h < G; ++h) acc[h] = __fmaf_rn(qa[x][h], khat, acc[h]);
-          }
-        }
-      }
-    }
-    // gather this pass's survivors per head in LDS, then one global append per head
+    if (hm) exact_scores<G>(P, a, u, i, acc);
 #pragma unroll
     for (int h = 0; h < G; ++h) {
-      const bool keep = ((hm >> h) & 1) && acc[h] >= tau[h];
+      const bool keep = ((hm >> h) & 1) && acc[h] >= P.tau[h];
       const uint64_t bm = __ballot(keep);
       if (bm) {
         const int leader = __ffsll((unsigned long long)bm) - 1;
@@ -893,8 +956,7 @@ __global__ __launch_bounds__(kRsT) void fused_rescore_kernel(FusedArgs a) {
     __syncthreads();
 #pragma unroll
     for (int h = 0; h < G; ++h) {
-      const int nh = nk[h];
-      if (tid < nh) {
+      if (tid < nk[h]) {
         const uint32_t pos = kbase[h] + (uint32_t)tid;
         if (pos < (uint32_t)a.ws.scap)
           gstore(&a.ws.cand[((int64_t)(u * G + h) * kSlots + slot) * a.ws.scap + pos], kept[h][tid]);
@@ -905,22 +967,44 @@ __global__ __launch_bounds__(kRsT) void fused_rescore_kernel(FusedArgs a) {
 }
 
 // ---------------------------------------------------------------- pass 4
+// Bitonic sort of buf[0..P) (P a power of two) into descending order; every
+// thread owns whole compare-exchange pairs, all loads of a stage issued first.
 __device__ void bitonic_desc(uint64_t* buf, int P) {
-  const int tid = threadIdx.x, nt = blockDim.x;
+  const int tid = threadIdx.x, nt = blockDim.x, npairs = P >> 1;
   for (int size = 2; size <= P; size <<= 1) {
     for (int stride = size >> 1; stride > 0; stride >>= 1) {
-      for (int i = tid; i < P; i += nt) {
-        const int j = i ^ stride;
-        if (j > i) {
-          const bool desc = (i & size) == 0;
-          const uint64_t x = buf[i], y = buf[j];
-          if (desc ? (x < y) : (x > y)) {
-            buf[i] = y;
-            buf[j] = x;
+      for (int p0 = 0; p0 < npairs; p0 += 2 * nt) {
+        int ii[2];
+        uint64_t x[2], y[2];
+#pragma unroll
+        for (int q2 = 0; q2 < 2; ++q2) {
+          const int pid = p0 + tid + q2 * nt;
+          ii[q2] = ((pid & ~(stride - 1)) << 1) | (pid & (stride - 1));
+          if (pid < npairs) {
+            x[q2] = buf[ii[q2]];
+            y[q2] = buf[ii[q2] + stride];
+          }
+        }
+#pragma unroll
+        for (int q2 = 0; q2 < 2; ++q2) {
+          const int pid = p0 + tid + q2 * nt;
+          if (pid < npairs) {
+            const bool desc = (ii[q2] & size) == 0;
+            if (desc ? (x[q2] < y[q2]) : (x[q2] > y[q2])) {
+              buf[ii[q2]] = y[q2];
+              buf[ii[q2] + stride] = x[q2];
+            }
           }
         }
       }
-      __syncthreads();
+      // pairs of strides <= 64 stay inside one wave's elements from one stage
+      // to the next (thread t owns pairs t and t + nt): a wave-level LDS wait
+      // suffices unless the next stride is larger
+      const int next = stride > 1 ? stride >> 1 : size;  // the next stage's stride
+      if (next <= 64 && stride <= 64 && nt % kWave == 0)
+        wave_lds_sync();
+      else
+        __syncthreads();
     }
   }
 }
@@ -949,22 +1033,34 @@ __device__ __forceinline__ float exact_score1(const int* act, int A, const float
   return acc;
 }
 
+// Pass 4, one workgroup per (score range, row).  Normally the survivors of a
+// row are split by the boundaries from pass 2: workgroup b sorts the survivors
+// of range b and writes them after the ones of the ranges above.  A row with
+// no more eligible keys than the survivor list holds is scored directly, and a
+// row whose filter under-collected (or whose lists overflowed) is recomputed
+// exactly; both by the range-0 workgroup with a streaming top-k.
 template <int G>
 __global__ __launch_bounds__(kSelThreads) void fused_select_kernel(FusedArgs a, int32_t* __restrict__ idx,
                                                                    float* __restrict__ val) {
   extern __shared__ uint64_t buf[];
-  __shared__ int act[kD];          // active channels ascending (fallback)
+  __shared__ int act[kD];          // active channels ascending (streaming path)
   __shared__ float qa[kD];         // q of this row's head per active channel
   __shared__ int nact;
-  __shared__ int s_count;
+  __shared__ int s_count, s_above;
   __shared__ uint64_t s_thr;
   __shared__ int wc[2];
-  const int r = blockIdx.x, u = r / G, h = r % G, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  __shared__ uint32_t s_sub[kSlots];
+  const int part = blockIdx.x, r = blockIdx.y, u = r / G, h = r % G, tid = threadIdx.x, lane = tid & 63,
+            wave = tid >> 6;
   int64_t nu, lo, hi;
   row_window(a, u, &nu, &lo, &hi, false);
   const int k = a.k;
-  __shared__ uint32_t s_sub[kSlots];
   if (tid < kSlots) s_sub[tid] = gload(a.ws.cnt + r * kSlots + tid);
+  if (tid == 0) {
+    s_count = 0;
+    s_above = 0;
+    s_thr = 0ull;
+  }
   __syncthreads();
   uint32_t C = 0;
   bool sub_over = false;
@@ -973,33 +1069,47 @@ __global__ __launch_bounds__(kSelThreads) void fused_select_kernel(FusedArgs a, 
     sub_over |= s_sub[q2] > (uint32_t)a.ws.scap;
   }
   const float tau = gload(a.ws.tau + r);
-  // direct: few enough eligible keys to score them all; fallback: the filter
-  // under-collected or a list overflowed
   const bool direct = hi - lo <= a.ws.cap;
   const bool fallback =
       !direct && (sub_over || C > (uint32_t)kSelCap || C < (uint32_t)k || gload(a.ws.uovf + u) != 0u || tau == kNegInf);
-  int count;
   if (!direct && !fallback) {
-    count = (int)C;
-    int P2 = 1;
-    while (P2 < count) P2 <<= 1;
-    for (int i = tid; i < P2; i += kSelThreads) {
-      uint64_t v = 0ull;
-      if (i < count) {  // element i of the concatenated sub-lists
-        int q2 = 0;
-        uint32_t off = (uint32_t)i;
-        while (off >= s_sub[q2]) off -= s_sub[q2++];
-        v = gload(a.ws.cand + ((int64_t)r * kSlots + q2) * a.ws.scap + off);
+    const uint32_t ub = gload(a.ws.bnd + r * kSlots + part);
+    const uint32_t lb = part + 1 < kSlots ? gload(a.ws.bnd + r * kSlots + part + 1) : 0u;
+    int above = 0;
+    for (uint32_t i = tid; i < C; i += kSelThreads) {  // element i of the concatenated sub-lists
+      int q2 = 0;
+      uint32_t off = i;
+      while (off >= s_sub[q2]) off -= s_sub[q2++];
+      const uint64_t v = gload(a.ws.cand + ((int64_t)r * kSlots + q2) * a.ws.scap + off);
+      const uint32_t key = (uint32_t)(v >> 32);
+      if (key > ub) {
+        ++above;
+      } else if (key > lb) {
+        buf[atomicAdd(&s_count, 1)] = v;
       }
-      buf[i] = v;
     }
+    if (above) atomicAdd(&s_above, above);
+    __syncthreads();
+    const int off0 = s_above, cnt = s_count;
+    if (off0 >= k || cnt == 0) return;
+    int P2 = 1;
+    while (P2 < cnt) P2 <<= 1;
+    for (int i = cnt + tid; i < P2; i += kSelThreads) buf[i] = 0ull;
     __syncthreads();
     bitonic_desc(buf, P2);
-  } else {
-    // exact recomputation of the row: a streaming top-k over all eligible keys
+    for (int x = tid; x < cnt && off0 + x < k; x += kSelThreads) {
+      const uint64_t c = buf[x];
+      idx[(int64_t)r * k + off0 + x] = (int32_t)(~(uint32_t)(c & 0xFFFFFFFFull));
+      if (val) val[(int64_t)r * k + off0 + x] = key_to_score((uint32_t)(c >> 32));
+    }
+    return;
+  }
+  if (part != 0) return;
+  // streaming top-k over all eligible keys with exact scores
+  {
     int t = 0;
     if (tid < kD) {
-      t = a.depths[(int64_t)u * kD + tid];
+      t = gload(a.depths + (int64_t)u * kD + tid);
       t = t > kPlanes ? kPlanes : t;
     }
     const bool on = tid < kD && t > 0;
@@ -1009,52 +1119,54 @@ __global__ __launch_bounds__(kSelThreads) void fused_select_kernel(FusedArgs a, 
     if (on) act[(wave == 1 ? wc[0] : 0) + __popcll(m & lanemask_lt(lane))] = tid | (t << 8);
     if (tid == 0) {
       nact = wc[0] + wc[1];
-      s_count = 0;
-      s_thr = 0ull;
       if (fallback) set_status(a.st, FATHOM_DEV_TOPK_FALLBACK);
     }
     __syncthreads();
     for (int x = tid; x < nact; x += kSelThreads)
       qa[x] = load_q(a.q, a.qdt, ((int64_t)u * G + h) * kD + (act[x] & 0xFF));
     __syncthreads();
-    const int A = nact;
-    const int nwaves = kSelThreads / kWave;
-    const int64_t bfirst = lo / kBlockTokens, bend = (hi + kBlockTokens - 1) / kBlockTokens;
-    for (int64_t bb = bfirst; bb < bend; bb += nwaves) {
-      const int64_t b = bb + wave;
-      const int64_t i = b * kBlockTokens + lane;
-      const bool elig = b < bend && i >= lo && i < hi;
-      uint64_t comp = 0ull;
-      if (elig) {
-        const float s = exact_score1(act, A, qa, a, u, b, lane);
-        comp = ((uint64_t)score_key(s) << 32) | (uint64_t)(~(uint32_t)i);
-      }
-      const uint64_t thr = s_thr;
-      const bool add = elig && comp > thr;
-      const uint64_t bm = __ballot(add);
-      if (bm) {
-        int basep = 0;
-        const int leader = __ffsll((unsigned long long)bm) - 1;
-        if (lane == leader) basep = atomicAdd(&s_count, __popcll(bm));
-        basep = __shfl(basep, leader, kWave);
-        if (add) buf[basep + __popcll(bm & lanemask_lt(lane))] = comp;
-      }
-      __syncthreads();
-      if (s_count > kSelCap - kSelThreads) {  // room for one more round
-        bitonic_desc(buf, kSelCap);
-        if (tid == 0) {
-          s_count = k;
-          s_thr = buf[k - 1];
-        }
-        for (int x = k + tid; x < kSelCap; x += kSelThreads) buf[x] = 0ull;
-        __syncthreads();
-      }
-    }
-    count = s_count;
-    for (int x = count + tid; x < kSelCap; x += kSelThreads) buf[x] = 0ull;
-    __syncthreads();
-    bitonic_desc(buf, kSelCap);
   }
+  const int A = nact;
+  const int nwaves = kSelThreads / kWave;
+  const int64_t bfirst = lo / kBlockTokens, bend = (hi + kBlockTokens - 1) / kBlockTokens;
+  for (int64_t bb = bfirst; bb < bend; bb += nwaves) {
+    const int64_t b = bb + wave;
+    const int64_t i = b * kBlockTokens + lane;
+    const bool elig = b < bend && i >= lo && i < hi;
+    uint64_t comp = 0ull;
+    if (elig) {
+      const float s = exact_score1(act, A, qa, a, u, b, lane);
+      comp = ((uint64_t)score_key(s) << 32) | (uint64_t)(~(uint32_t)i);
+    }
+    const uint64_t thr = s_thr;
+    const bool add = elig && comp > thr;
+    const uint64_t bm = __ballot(add);
+    if (bm) {
+      int basep = 0;
+      const int leader = __ffsll((unsigned long long)bm) - 1;
+      if (lane == leader) basep = atomicAdd(&s_count, __popcll(bm));
+      basep = __shfl(basep, leader, kWave);
+      if (add) buf[basep + __popcll(bm & lanemask_lt(lane))] = comp;
+    }
+    __syncthreads();
+    if (s_count > kSelCap - kSelThreads) {  // room for one more round
+      for (int x = s_count + tid; x < kSelCap; x += kSelThreads) buf[x] = 0ull;
+      __syncthreads();
+      bitonic_desc(buf, kSelCap);
+      if (tid == 0) {
+        s_count = k;
+        s_thr = buf[k - 1];
+      }
+      for (int x = k + tid; x < kSelCap; x += kSelThreads) buf[x] = 0ull;
+      __syncthreads();
+    }
+  }
+  const int count = s_count;
+  int P2 = 1;
+  while (P2 < count) P2 <<= 1;
+  for (int x = count + tid; x < P2; x += kSelThreads) buf[x] = 0ull;
+  __syncthreads();
+  bitonic_desc(buf, P2 > 1 ? P2 : 2);
   bool shortfall = false;
   for (int x = tid; x < k; x += kSelThreads) {
     const uint64_t c = x < count ? buf[x] : 0ull;
@@ -1087,22 +1199,16 @@ static fathom_status launch_fused_g(const FusedArgs& fa, int U, int32_t* idx, fl
   static bool attr = false;
   if (!attr) {
     if (hipFuncSetAttribute(reinterpret_cast<const void*>(&fused_select_kernel<G>),
-                            hipFuncAttributeMaxDynamicSharedMemorySize, kSelCap * 8) != hipSuccess ||
-        hipFuncSetAttribute(reinterpret_cast<const void*>(&fused_tau_kernel),
-                            hipFuncAttributeMaxDynamicSharedMemorySize, kSampleGroups * kGrp * kBlockTokens * 4) !=
-            hipSuccess)
+                            hipFuncAttributeMaxDynamicSharedMemorySize, kSelCap * 8) != hipSuccess)
       return FATHOM_ERR_HIP;
     attr = true;
   }
   dim3 gs((unsigned)((fa.ws.s_groups + kFW - 1) / kFW), (unsigned)U);
   hipLaunchKernelGGL(fused_sample_kernel<G>, gs, dim3(kFT), 0, s, fa);
-  const size_t tau_lds = (size_t)fa.ws.s_groups * kGrp * kBlockTokens * 4;
-  hipLaunchKernelGGL(fused_tau_kernel, dim3(R), dim3(kSelThreads), tau_lds, s, fa, G);
-  const int64_t ngroups = (fa.nb_cap + kGrp - 1) / kGrp;
-  dim3 gf((unsigned)((ngroups + kGroupsPerWG - 1) / kGroupsPerWG), (unsigned)U);
+  hipLaunchKernelGGL(fused_tau_kernel, dim3(R), dim3(kSelThreads), 0, s, fa, G);
+  dim3 gf((unsigned)fa.ws.nwg, (unsigned)U);
   hipLaunchKernelGGL(fused_full_kernel<G>, gf, dim3(kFT), 0, s, fa);
-  hipLaunchKernelGGL(fused_rescore_kernel<G>, dim3((unsigned)fa.ws.nwg, (unsigned)U), dim3(kRsT), 0, s, fa);
-  hipLaunchKernelGGL(fused_select_kernel<G>, dim3(R), dim3(kSelThreads), (size_t)kSelCap * 8, s, fa, idx, val);
+  hipLaunchKernelGGL(fused_select_kernel<G>, dim3(kSlots, R), dim3(kSelThreads), (size_t)kSelCap * 8, s, fa, idx, val);
   FATHOM_LAUNCH_CHECK();
   return FATHOM_OK;
 }

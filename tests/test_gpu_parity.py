@@ -490,3 +490,24 @@ def test_scan_topk_no_fallback_on_workload_data():
         d, _ = F.fathom_alloc_depths(data["q"], data["var"], F.FATHOM_WATERFILL, B, dev_status=st)
         F.fathom_scan_topk(planes, scales, data["n"], data["q"], d, cfg.k, dev_status=st)
     assert status(st) == 0
+
+
+def test_scan_topk_direct_rows_large_k():
+    """Rows with no more eligible keys than the survivor list holds are scored
+    directly; with k = 8192 and 16000 keys the streaming top-k compacts its
+    buffer once on the way (the unused tail must not leak into the result)."""
+    n, G, k = 16000, 2, 8192
+    K, nt, planes, scales = _store([n, 9000], 71)
+    rng = np.random.default_rng(72)
+    q = rng.standard_normal((2, G, 128)).astype(np.float32)
+    qt = torch.from_numpy(q).to(DEV)
+    d = torch.from_numpy(rng.integers(0, 5, (2, 128)).astype(np.uint8)).to(DEV)
+    st = F.new_status()
+    idx, val = F.fathom_scan_topk(planes, scales, nt, qt, d, k, dev_status=st)
+    assert status(st) & ~F.FATHOM_DEV_TOPK_SHORT == 0
+    for u, nu in enumerate([n, 9000]):
+        ref = oracle.scores_f32(u64(planes)[u], u16(scales)[u], nu, q[u], d.cpu().numpy()[u])
+        for h in range(G):
+            oi, ov, _ = oracle.topk(ref[h], k)
+            assert np.array_equal(idx[u, h].cpu().numpy(), oi), (u, h)
+            assert np.array_equal(val[u, h].cpu().numpy().view(np.uint32), ov.view(np.uint32)), (u, h)
