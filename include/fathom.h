@@ -172,20 +172,24 @@ size_t fathom_scan_topk_workspace_size(int U, int G, int64_t max_n, int k);
  *   ns = min(n_sink, n[u]),  l0 = max(ns, n[u] - n_local);
  * index entries outside [ns, l0) (including -1) are skipped, so S_h has no
  * duplicates when idx does not.
- *   out_h = sum_{i in S_h} softmax_i(sm_scale * q_h . K_i) V_i,  fp32 arithmetic.
+ *   out_h = sum_{i in S_h} softmax_i(sm_scale * q_h . K_i) V_i,  fp32 arithmetic
+ *   (the set is processed in chunks whose softmax partials are combined).
  *
  *   q        [U][G][D] (qdt).
  *   Krows, Vrows  [U][n][D] fp16 rows, element (u, i, c) at [u*ld_unit + i*ld_tok + c];
  *            4-byte aligned; ld_tok >= D; ld_tok, ld_unit even.
  *   idx      [U][G][k] int32 (k may be 0; idx may then be NULL).
  *   out      [U][G][D] fp32 (written; 0 for an empty set).
+ *   ws       device workspace of at least
+ *            fathom_sparse_attn_workspace_size(U, G, k, n_sink, n_local) bytes, 256-byte aligned.
  * Device status: BAD_N (nb_cap is not known here: only n[u] < 0 is flagged).
  */
 fathom_status fathom_sparse_attn(const void* q, fathom_dtype qdt, const uint16_t* Krows,
                                  const uint16_t* Vrows, int64_t ld_tok, int64_t ld_unit,
                                  const int64_t* n, int U, int G, int D, const int32_t* idx, int k,
-                                 int n_sink, int n_local, float sm_scale, float* out,
-                                 uint32_t* dev_status, void* stream);
+                                 int n_sink, int n_local, float sm_scale, float* out, void* ws,
+                                 size_t ws_bytes, uint32_t* dev_status, void* stream);
+size_t fathom_sparse_attn_workspace_size(int U, int G, int k, int n_sink, int n_local);
 
 /* Human-readable name of a status code (static storage). */
 const char* fathom_status_string(fathom_status s);

@@ -37,8 +37,8 @@ FATHOM_DEV_BAD_N = 16
 
 EXPORTED = (
     "fathom_pack", "fathom_alloc_depths", "fathom_scan", "fathom_topk", "fathom_topk_workspace_size",
-    "fathom_scan_topk", "fathom_scan_topk_workspace_size", "fathom_sparse_attn", "fathom_status_string",
-    "fathom_version",
+    "fathom_scan_topk", "fathom_scan_topk_workspace_size", "fathom_sparse_attn",
+    "fathom_sparse_attn_workspace_size", "fathom_status_string", "fathom_version",
 )
 
 
@@ -67,7 +67,8 @@ def lib() -> C.CDLL:
             "fathom_scan": [P, P, P, i32, i32, i64, P, i32, i32, P, P, i64, P, P],
             "fathom_topk": [P, i64, P, i32, i32, i32, i64, i64, P, P, P, C.c_size_t, P, P],
             "fathom_scan_topk": [P, P, P, i32, i32, i64, P, i32, i32, P, i32, i64, i64, P, P, P, C.c_size_t, P, P],
-            "fathom_sparse_attn": [P, i32, P, P, i64, i64, P, i32, i32, i32, P, i32, i32, i32, C.c_float, P, P, P],
+            "fathom_sparse_attn": [P, i32, P, P, i64, i64, P, i32, i32, i32, P, i32, i32, i32, C.c_float, P, P,
+                                   C.c_size_t, P, P],
         }
         for name, args in sig.items():
             f = getattr(L, name)
@@ -77,6 +78,8 @@ def lib() -> C.CDLL:
             f = getattr(L, name)
             f.argtypes = [i32, i32, i64, i32]
             f.restype = C.c_size_t
+        L.fathom_sparse_attn_workspace_size.argtypes = [i32, i32, i32, i32, i32]
+        L.fathom_sparse_attn_workspace_size.restype = C.c_size_t
         L.fathom_status_string.argtypes = [st]
         L.fathom_status_string.restype = C.c_char_p
         L.fathom_version.argtypes = []
@@ -219,8 +222,12 @@ def fathom_scan_topk(planes, scales, n, q, depths, k, lo=0, tail=0, idx=None, va
     return idx, val
 
 
+def fathom_sparse_attn_workspace_size(U, G, k, n_sink=0, n_local=0) -> int:
+    return int(lib().fathom_sparse_attn_workspace_size(int(U), int(G), int(k), int(n_sink), int(n_local)))
+
+
 def fathom_sparse_attn(q, Krows, Vrows, n, idx, n_sink=0, n_local=0, sm_scale=None, out=None, dev_status=None,
-                       stream=None):
+                       stream=None, ws=None):
     """Sec. 2: exact attention over sink + local + idx rows; Krows/Vrows [U][n][D] fp16 -> out [U][G][D] fp32."""
     _dev(q, Krows, Vrows, n, idx)
     U, G, D = q.shape
@@ -233,7 +240,9 @@ def fathom_sparse_attn(q, Krows, Vrows, n, idx, n_sink=0, n_local=0, sm_scale=No
         sm_scale = 1.0 / (D ** 0.5)
     if out is None:
         out = torch.empty((U, G, D), dtype=torch.float32, device=q.device)
+    wsb = fathom_sparse_attn_workspace_size(U, G, k, n_sink, n_local)
+    ws = _ws(wsb, ws, q.device)
     _check(lib().fathom_sparse_attn(_p(q), _dt(q), _p(Krows), _p(Vrows), Krows.stride(1), Krows.stride(0), _p(n),
                                     U, G, D, _p(idx), k, int(n_sink), int(n_local), C.c_float(sm_scale), _p(out),
-                                    _p(dev_status), _stream(stream)), "fathom_sparse_attn")
+                                    _p(ws), ws.numel(), _p(dev_status), _stream(stream)), "fathom_sparse_attn")
     return out

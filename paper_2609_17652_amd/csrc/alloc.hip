@@ -4,7 +4,7 @@
 // One wave per unit; lane l owns channels l and l + 64.  The water line is
 // found exactly: the 4D candidates g_j * 2^-(2m-1) are non-negative doubles,
 // so their IEEE bit patterns order like their values, and a 64-step bitwise
-// search over the pattern (each step a wave-wide count) yields the (B+1)-th
+// search over the pattern (each step a wave-wide count from ballots) yields the (B+1)-th
 // largest candidate with no log, exp or rounding -- a bisection on log(theta)
 // carried to the last bit.
 #include "common.hpp"
@@ -40,12 +40,12 @@ __global__ __launch_bounds__(kWave) void alloc_waterfill_kernel(const void* __re
   if (B < 4 * kD) {
     for (int bit = 63; bit >= 0; --bit) {
       const uint64_t cand = T | (1ull << bit);
-      int c = 0;
+      int c = 0;  // wave-wide count from ballots: no cross-lane data movement
 #pragma unroll
       for (int r = 0; r < 2; ++r)
 #pragma unroll
-        for (int m = 0; m < 4; ++m) c += key[r][m] >= cand;
-      if (wave_sum_int(c) >= B + 1) T = cand;
+        for (int m = 0; m < 4; ++m) c += __popcll(__ballot(key[r][m] >= cand));
+      if (c >= B + 1) T = cand;
     }
   }
 #pragma unroll

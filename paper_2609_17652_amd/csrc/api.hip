@@ -12,8 +12,9 @@ fathom_status launch_scan(const uint64_t*, const uint16_t*, const int64_t*, int,
 fathom_status launch_topk(const float*, int64_t, const int64_t*, int, int, int, int64_t, int64_t, int32_t*, float*,
                           void*, uint32_t*, hipStream_t);
 fathom_status launch_sparse_attn(const void*, fathom_dtype, const uint16_t*, const uint16_t*, int64_t, int64_t,
-                                 const int64_t*, int, int, const int32_t*, int, int, int, float, float*, uint32_t*,
-                                 hipStream_t);
+                                 const int64_t*, int, int, const int32_t*, int, int, int, float, float*, void*,
+                                 uint32_t*, hipStream_t);
+size_t attn_ws_bytes(int U, int G, int k, int n_sink, int n_local);
 size_t topk_ws_bytes(int R, int64_t max_n, int k);
 size_t fused_ws_bytes(int R, int U, int64_t nb_cap, int k);
 fathom_status launch_scan_topk_fused(const uint64_t*, const uint16_t*, const int64_t*, int, int64_t, const void*,
@@ -151,10 +152,15 @@ fathom_status fathom_scan_topk(const uint64_t* planes, const uint16_t* scales, c
                                 dev_status, as_stream(stream));
 }
 
+size_t fathom_sparse_attn_workspace_size(int U, int G, int k, int n_sink, int n_local) {
+  if (U <= 0 || G <= 0 || k < 0 || n_sink < 0 || n_local < 0) return 0;
+  return attn_ws_bytes(U, G, k, n_sink, n_local);
+}
+
 fathom_status fathom_sparse_attn(const void* q, fathom_dtype qdt, const uint16_t* Krows, const uint16_t* Vrows,
                                  int64_t ld_tok, int64_t ld_unit, const int64_t* n, int U, int G, int D,
                                  const int32_t* idx, int k, int n_sink, int n_local, float sm_scale, float* out,
-                                 uint32_t* dev_status, void* stream) {
+                                 void* ws, size_t ws_bytes, uint32_t* dev_status, void* stream) {
   if (U < 0 || k < 0 || n_sink < 0 || n_local < 0) return FATHOM_ERR_INVALID;
   if (D != kD) return FATHOM_ERR_UNSUPPORTED;
   if (G < 1 || G > 8 || !dtype_ok(qdt)) return FATHOM_ERR_UNSUPPORTED;
@@ -165,8 +171,10 @@ fathom_status fathom_sparse_attn(const void* q, fathom_dtype qdt, const uint16_t
   if (!aligned(Krows, 4) || !aligned(Vrows, 4) || !aligned(q, dtype_size(qdt)) || !aligned(out, 4) ||
       !aligned(n, 8) || (idx && !aligned(idx, 4)))
     return FATHOM_ERR_INVALID;
+  if (!ws || !aligned(ws, 256)) return FATHOM_ERR_INVALID;
+  if (ws_bytes < attn_ws_bytes(U, G, k, n_sink, n_local)) return FATHOM_ERR_WORKSPACE;
   return launch_sparse_attn(q, qdt, Krows, Vrows, ld_tok, ld_unit, n, U, G, idx, k, n_sink, n_local, sm_scale, out,
-                            dev_status, as_stream(stream));
+                            ws, dev_status, as_stream(stream));
 }
 
 }  // extern "C"

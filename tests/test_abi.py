@@ -106,12 +106,16 @@ def test_host_validation(fl):
     assert L.fathom_scan_topk(FAKE, FAKE, FAKE, 1, 128, 64, FAKE, 1, 4, FAKE, 64, 0, 0, FAKE, NULL, FAKE, ws2 - 1,
                               NULL, S) == fl.FATHOM_ERR_WORKSPACE
     # sparse attention: sink + local too large, odd ld_tok, null out
+    wsa = fl.fathom_sparse_attn_workspace_size(1, 4, 8, 4, 32)
+    assert wsa > 0
     assert L.fathom_sparse_attn(FAKE, 0, FAKE, FAKE, 128, 0, FAKE, 1, 4, 128, FAKE, 8, 1000, 100, C.c_float(1.0),
-                                FAKE, NULL, S) == fl.FATHOM_ERR_UNSUPPORTED
+                                FAKE, FAKE, wsa, NULL, S) == fl.FATHOM_ERR_UNSUPPORTED
     assert L.fathom_sparse_attn(FAKE, 0, FAKE, FAKE, 129, 0, FAKE, 1, 4, 128, FAKE, 8, 4, 32, C.c_float(1.0),
-                                FAKE, NULL, S) == fl.FATHOM_ERR_INVALID
+                                FAKE, FAKE, wsa, NULL, S) == fl.FATHOM_ERR_INVALID
     assert L.fathom_sparse_attn(FAKE, 0, FAKE, FAKE, 128, 0, FAKE, 1, 4, 128, FAKE, 8, 4, 32, C.c_float(1.0),
-                                NULL, NULL, S) == fl.FATHOM_ERR_INVALID
+                                NULL, FAKE, wsa, NULL, S) == fl.FATHOM_ERR_INVALID
+    assert L.fathom_sparse_attn(FAKE, 0, FAKE, FAKE, 128, 0, FAKE, 1, 4, 128, FAKE, 8, 4, 32, C.c_float(1.0),
+                                FAKE, FAKE, wsa - 1, NULL, S) == fl.FATHOM_ERR_WORKSPACE
 
 
 def test_synth_is_deterministic_and_shaped():
