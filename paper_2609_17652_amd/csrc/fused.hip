@@ -7,22 +7,32 @@
 // key, each key first gets a cheap integer proxy with a rigorous error bound.
 // With khat = z' a16 / 16, where
 //   z' = 2 (c^(t) - 2^(t-1)) 2^(4-t) + 2^(4-t)   (an odd multiple, |z'| <= 15),
-// the score is sum_j (w_j / 2) z'_j with w_j = q_hj a16_bj / 8.  Per block and
-// head, delta is a power of two with max|w| / delta < 128 and w8_j = rne(w_j /
-// delta) in int8; the proxy is (delta / 2) sum_j w8_j z'_j, exact in fp32, and
-//   |score - proxy| <= E = (sum_j |w_j - delta w8_j| zmax_j / 2
-//                           + A 2^-21 sum_j |w_j|) (1 + 2^-10),
-// the second term covering the fp32 rounding of the documented score.
+// the score is sum_j w_j z'_j / 16 with w_j = q_hj a16_bj.  Per block and
+// head, delta is a power of two with max|w| / delta < 1024 and W_j = rne(w_j /
+// delta) clamped to [-1020, 1019]; the proxy is (delta / 16) sum_j W_j z'_j,
+// exact in fp32, and
+//   |score - proxy| <= E = (sum_j |w_j - delta W_j| zmax_j / 16
+//                           + (A + 1) 2^-24 sum_j |w_j| + A 2^-120) (1 + 2^-10),
+// where the second term covers the rounding of w and the A roundings of the
+// documented fma chain (each term |q khat| <= 15/16 |w|), the third any
+// subnormal rounding, and the factor the rounding of E's own sums.
 //
-// Bits to proxy digits.  z'_j = U_j + 2^(4-t_j) - 16 with U_j = sum_{p<t}
-// b_p 2^(4-p) built from the plane bits b_p.  A wave holds 64 keys of a block
-// (lane = key).  The plane words of a group of 8 blocks are staged in LDS,
-// each 32-bit half rotated left by the bit position q = 8K + 4 - p its plane
-// takes in the U dword (byte K = channel K of 4).  Lane s then gathers bit s of
-// every row with one v_and_or_b32 against the per-lane mask
-// 1 << ((s + q) mod 32), building U rotated left by s; one v_alignbit_b32
-// rotates it back.  The constant parts go into a per-(block, head) bias, and
-// v_dot4_i32_i8 folds 4 channels per head into an int32 accumulator.
+// W_j has 11 bits, more than an int8 MFMA operand: W = 8 Wh + Wl with Wh in
+// [-127, 127] and Wl in [-4, 3].  The digits enter as u_j = U_j / 2 in [0, 15]
+// (U_j = sum_{p<t} b_p 2^(4-p), so z'_j = 2 u_j - zmax_j), and the MFMA
+// accumulates sum_j (8 u_j) Wh_j + sum_j u_j Wl_j = sum_j u_j W_j into one
+// int32: 8 u_j <= 120 still fits the signed byte.  The proxy is then
+// (delta / 16) (2 acc + bias) with bias = -sum_j W_j zmax_j per (block, head).
+//
+// Bits to proxy digits.  A wave holds 64 keys of a block (lane = key).  Four
+// channels form a U dword (byte K = u of channel K of 4, plane p at bit
+// 8K + 3 - p).  A row group is one plane p of the 4 channels of a U dword;
+// staging byte-transposes its 4 plane rows of a block (v_perm_b32) into 8
+// words, word m holding keys 8m..8m+7 of the 4 channels (byte K), rotated left
+// by 3 - p.  Lane 8m + s then gathers its 4 bits of the row group with one
+// v_and_or_b32 against the mask 0x01010101 << ((s + 3 - p) mod 8), building
+// the U dword rotated left by s; one v_alignbit_b32 per U dword rotates it
+// back.
 //
 // Passes: (1) proxies of a strided sample of 8-block groups; (2) per row, tau =
 // a rank statistic of the sample chosen so that ~1.25 k keys are expected
@@ -39,9 +49,12 @@ namespace fathom {
 constexpr int kFT = 256;          // threads per workgroup (4 waves)
 constexpr int kFW = kFT / kWave;
 constexpr int kGrp = 8;           // blocks per group (one wave step)
-constexpr int kChunkRows = 64;    // plane rows staged per chunk (padded)
-constexpr int kStageK = kChunkRows / 8;  // rows loaded per lane per chunk (8 lanes per row)
-constexpr int kChunkDw = 16;      // U dwords per chunk (a full dword has >= 4 rows)
+constexpr int kChunkRG = 16;      // row groups staged per chunk (a row group: one plane of a U dword's 4 channels)
+constexpr int kStageItems = kChunkRG * kGrp / kWave;  // (row group, block) items staged per lane
+constexpr int kRgStride = 36;     // LDS dwords per (row group, 4-block half): 8 words x 4 blocks, padded
+constexpr int kChunkDw = 8;       // U dwords per chunk
+constexpr int kChunkCh = 4 * kChunkDw;  // channels per chunk
+constexpr int kScaleK = kD / 8;         // scale loads per lane, first chunk of a group (8 lanes per channel)
 constexpr int kMaxDw = kD / 4;
 constexpr int kResidentWG = 768;  // full-pass workgroups resident at once on MI355X (256 CUs x 3)
 constexpr int kMaxGroupsPerWave = 32;  // keeps a workgroup's key offsets within 16 bits
@@ -146,25 +159,25 @@ struct FusedArgs {
 
 // Per-unit plan, shared by the waves of a workgroup.  Proxy channel order:
 // depth descending, channel ascending (the integer proxy does not depend on
-// the order; the exact scores use channel order ascending).  The plane rows of
-// each U dword (4 channels) are listed channel by channel, plane by plane, and
-// padded with zero rows to a multiple of 4.
+// the order; the exact scores use channel order ascending).  A U dword has as
+// many row groups as its first (deepest) channel has planes; a row group lists
+// the plane row of each of its 4 channels, kPadRow where the channel is absent
+// or shallower.
 constexpr uint32_t kPadRow = 0xFFFFFFFFu;
 template <int G>
 struct alignas(16) UnitLds {
+  uint4 rgrow[kD];                // row group g: plane-row index 4j+p of its 4 channels, or kPadRow
   int act[kD];                    // j | t << 8
   int pidx[kD];                   // proxy index of the x-th active channel in channel order
   float qa[kD][G];                // q_hj (fp32) of active channel a
-  float qa8[kD][G];               // q_hj / 8
   float zmx[kD];                  // 16 - 2^(4-t): the largest |z'| of channel a
-  uint32_t rrow[kD * kPlanes];    // padded row r: plane-row index 4j+p, or kPadRow
-  uint32_t rsh[kD * kPlanes];     // padded row r: (32 - q) mod 32, q = 8K + 4 - p its bit in the U dword
+  uint32_t rgp[kD];               // row group g: its plane p
   uint32_t tpk[kMaxDw];           // depths of channels 4d..4d+3, byte K
-  uint32_t drow[kMaxDw];          // first padded row of dword d, relative to its chunk
-  uint32_t dnq[kMaxDw];           // row quads of dword d
+  uint32_t drg[kMaxDw];           // first row group of dword d, relative to its chunk
+  uint32_t dnr[kMaxDw];           // row groups of dword d
   int dch[kMaxDw];                // chunk of dword d
   int chd[kMaxDw + 1];            // chunk c = dwords [chd[c], chd[c+1])
-  int chr[kMaxDw + 1];            // first padded row of chunk c
+  int chr[kMaxDw + 1];            // first row group of chunk c
   int cnt[2][5];
   int A, nch;
   float tau[G];
@@ -173,15 +186,16 @@ struct alignas(16) UnitLds {
 // Per-wave staging and per-(block, head) state.
 template <int G4>
 struct alignas(16) WaveLds {
-  uint32_t rows[kChunkRows][2][kGrp];  // [row][32-bit half][block], rotated
-  uint16_t scl[kChunkRows][kGrp];      // fp16 scales of the chunk's channels
-  uint32_t wB[kGrp][G4][kChunkDw];     // packed int8 weights: [block][head][U dword], 4 channels a dword
+  uint32_t rows[kChunkRG][2][kRgStride];  // [row group][blocks 0-3 | 4-7][4 word m + block], transposed, rotated
+  uint16_t scl[kD][kGrp];                 // fp16 scales of the group's active channels (proxy order)
+  uint32_t wB[kGrp][G4][kChunkDw];     // int8 Wh: [block][head][U dword], 4 channels a dword
+  uint32_t wBl[kGrp][G4][kChunkDw];    // int8 Wl, same layout
   uint32_t zero16[4];                  // a zero MFMA operand for the lanes that carry no weights
   float sdel[kGrp][8];                 // delta (0: no usable bound)
   float sinv[kGrp][8];                 // 1 / delta
-  float seb[kGrp][8];                  // sum |w - delta w8| zmax
+  float seb[kGrp][8];                  // sum |w - delta W| zmax
   float ssw[kGrp][8];                  // sum |w|
-  int sbias[kGrp][8];                  // sum w8 (2^(4-t) - 16)
+  int sbias[kGrp][8];                  // bias = -sum W zmax
   int sthr[kGrp][8];                   // full pass: candidate iff acc >= sthr
 };
 
@@ -265,7 +279,6 @@ __device__ void unit_setup(UnitLds<G>& P, const FusedArgs& a, int u) {
     const int ai = x / G, h = x % G;
     const float qv = load_q(a.q, a.qdt, ((int64_t)u * G + h) * kD + (P.act[ai] & 0xFF));
     P.qa[ai][h] = qv;
-    P.qa8[ai][h] = __fmul_rn(qv, 0.125f);
   }
   if (tid < A) P.zmx[tid] = (float)(16 - (16 >> (P.act[tid] >> 8)));
   if (tid < AD) {
@@ -278,19 +291,18 @@ __device__ void unit_setup(UnitLds<G>& P, const FusedArgs& a, int u) {
     P.tpk[tid] = tp;
   }
   __syncthreads();
-  if (wave == 0) {  // padded row counts per dword; greedy chunks of whole dwords, at most kChunkRows rows each
-    int rd4 = 0;
-    if (lane < AD) {
-      const uint32_t tp = P.tpk[lane];
-      rd4 = ((int)((tp & 0xFF) + ((tp >> 8) & 0xFF) + ((tp >> 16) & 0xFF) + (tp >> 24)) + 3) & ~3;
-    }
-    int c = 0, rows = 0, r0 = 0, my_row = 0, my_ch = 0;
+  if (wave == 0) {  // row groups per dword; greedy chunks of whole dwords, at most kChunkRG row groups
+                    // and kChunkDw dwords each
+    int nr = 0;
+    if (lane < AD) nr = (int)(P.tpk[lane] & 0xFF);  // the first channel of a dword is its deepest
+    int c = 0, rows = 0, r0 = 0, ndw = 0, my_row = 0, my_ch = 0;
     for (int d = 0; d < AD; ++d) {
-      const int v = __builtin_amdgcn_readlane(rd4, d);
-      if (rows + v > kChunkRows) {
+      const int v = __builtin_amdgcn_readlane(nr, d);
+      if (rows + v > kChunkRG || ndw == kChunkDw) {
         ++c;
         r0 += rows;
         rows = 0;
+        ndw = 0;
         if (lane == 0) {
           P.chd[c] = d;
           P.chr[c] = r0;
@@ -301,10 +313,11 @@ __device__ void unit_setup(UnitLds<G>& P, const FusedArgs& a, int u) {
         my_ch = c;
       }
       rows += v;
+      ++ndw;
     }
     if (lane < AD) {
-      P.drow[lane] = (uint32_t)my_row;
-      P.dnq[lane] = (uint32_t)(rd4 >> 2);
+      P.drg[lane] = (uint32_t)my_row;
+      P.dnr[lane] = (uint32_t)nr;
       P.dch[lane] = my_ch;
     }
     if (lane == 0) {
@@ -317,25 +330,20 @@ __device__ void unit_setup(UnitLds<G>& P, const FusedArgs& a, int u) {
     }
   }
   __syncthreads();
-  // rows of channel a: its dword's first padded row (global) + the depths before it in the dword
-  if (tid < A) {
-    const int d = tid >> 2, K = tid & 3, e = P.act[tid], j = e & 0xFF, tt = e >> 8;
-    const uint32_t tp = P.tpk[d];
-    int r0 = P.chr[P.dch[d]] + (int)P.drow[d];
-    for (int k2 = 0; k2 < K; ++k2) r0 += (int)((tp >> (8 * k2)) & 0xFF);
-    for (int p = 0; p < tt; ++p) {
-      P.rrow[r0 + p] = (uint32_t)(4 * j + p);
-      P.rsh[r0 + p] = (uint32_t)(32 - (8 * K + 4 - p)) & 31u;
-    }
-  }
-  if (tid < AD) {  // pad rows of dword tid
+  // row groups of dword d: plane p of its 4 channels
+  if (tid < AD) {
     const int d = tid;
     const uint32_t tp = P.tpk[d];
-    const int rd = (int)((tp & 0xFF) + ((tp >> 8) & 0xFF) + ((tp >> 16) & 0xFF) + (tp >> 24));
-    const int r0 = P.chr[P.dch[d]] + (int)P.drow[d];
-    for (int r = rd; r < (int)P.dnq[d] * 4; ++r) {
-      P.rrow[r0 + r] = kPadRow;
-      P.rsh[r0 + r] = 0u;
+    const int g0 = P.chr[P.dch[d]] + (int)P.drg[d], nr = (int)P.dnr[d];
+    for (int p = 0; p < nr; ++p) {
+      uint32_t rr[4];
+#pragma unroll
+      for (int K = 0; K < 4; ++K) {
+        const int x = 4 * d + K;
+        rr[K] = (x < A && (int)((tp >> (8 * K)) & 0xFF) > p) ? (uint32_t)(4 * (P.act[x] & 0xFF) + p) : kPadRow;
+      }
+      P.rgrow[g0 + p] = make_uint4(rr[0], rr[1], rr[2], rr[3]);
+      P.rgp[g0 + p] = (uint32_t)p;
     }
   }
   __syncthreads();
@@ -343,58 +351,89 @@ __device__ void unit_setup(UnitLds<G>& P, const FusedArgs& a, int u) {
 
 // ---------------------------------------------------------------- one wave's pipeline
 struct Stage {
-  uint64_t rw[kStageK];
-  uint32_t sv[kStageK];
+  uint64_t rw[kStageItems][4];
+  uint32_t sv[kScaleK];
 };
 
+// Lane (i, b): row groups i and i + 8 of chunk c for block gb + b and, with
+// the first chunk, the scales of active channels i, i + 8, ... (all chunks:
+// delta is fixed over every channel of the block).
 template <int G>
 __device__ __forceinline__ void stage_load(Stage& S, const UnitLds<G>& P, const FusedArgs& a, int u, int64_t gb,
                                            int c) {
-  const int lane = threadIdx.x & 63, rl = lane >> 3, bl = lane & 7;
-  const int row0 = P.chr[c], rows = P.chr[c + 1] - row0;
-  const int a0 = 4 * P.chd[c];
-  int a1 = 4 * P.chd[c + 1];
-  a1 = a1 < P.A ? a1 : P.A;
+  const int lane = threadIdx.x & 63, il = lane >> 3, bl = lane & 7;
+  const int rg0 = P.chr[c], nrg = P.chr[c + 1] - rg0;
+  const int nsc = c == 0 ? P.A : 0;
   const int64_t b = gb + bl;
   const bool bok = b < a.nb_cap;
   const uint64_t* Pu = a.planes + (int64_t)u * kD * kPlanes * a.nb_cap;
   const uint16_t* Su = a.scales + (int64_t)u * kD * a.nb_cap;
 #pragma unroll
-  for (int k = 0; k < kStageK; ++k) {
-    const int r = rl + 8 * k;
-    S.rw[k] = 0ull;
-    if (bok && r < rows) {
-      const uint32_t rr = P.rrow[row0 + r];
-      if (rr != kPadRow) S.rw[k] = gload(Pu + (int64_t)rr * a.nb_cap + b);
+  for (int k = 0; k < kStageItems; ++k) {
+    const int g = il + 8 * k;
+#pragma unroll
+    for (int K = 0; K < 4; ++K) S.rw[k][K] = 0ull;
+    if (bok && g < nrg) {
+      const uint4 rr = P.rgrow[rg0 + g];
+      const uint32_t r4[4] = {rr.x, rr.y, rr.z, rr.w};
+#pragma unroll
+      for (int K = 0; K < 4; ++K)
+        if (r4[K] != kPadRow) S.rw[k][K] = gload(Pu + (int64_t)r4[K] * a.nb_cap + b);
     }
+  }
+#pragma unroll
+  for (int k = 0; k < kScaleK; ++k) {
+    const int r = il + 8 * k;
     S.sv[k] = 0u;
-    if (bok && r < a1 - a0) S.sv[k] = gload(Su + (int64_t)(P.act[a0 + r] & 0xFF) * a.nb_cap + b);
+    if (bok && r < nsc) S.sv[k] = gload(Su + (int64_t)(P.act[r] & 0xFF) * a.nb_cap + b);
   }
 }
 
+// Byte transpose of a row group's 4 rows (one block): word m = byte m of rows
+// 0..3 in bytes 0..3, i.e. keys 8m..8m+7 of the 4 channels; then rotated left
+// by 3 - p.  v_perm_b32 picks bytes 0-3 from its second operand, 4-7 from its first.
 template <int G, int G4>
 __device__ __forceinline__ void stage_store(const Stage& S, const UnitLds<G>& P, WaveLds<G4>& W, int c) {
-  const int lane = threadIdx.x & 63, rl = lane >> 3, bl = lane & 7;
-  const int row0 = P.chr[c], rows = P.chr[c + 1] - row0;
-  const int nchan = (4 * P.chd[c + 1] < P.A ? 4 * P.chd[c + 1] : P.A) - 4 * P.chd[c];
+  const int lane = threadIdx.x & 63, il = lane >> 3, bl = lane & 7;
+  const int rg0 = P.chr[c], nrg = P.chr[c + 1] - rg0;
+  const int nsc = c == 0 ? P.A : 0;
 #pragma unroll
-  for (int k = 0; k < kStageK; ++k) {
-    const int r = rl + 8 * k;
-    if (r < rows) {
-      const uint32_t sh = P.rsh[row0 + r];
-      const uint32_t lo = (uint32_t)S.rw[k], hi = (uint32_t)(S.rw[k] >> 32);
-      W.rows[r][0][bl] = __builtin_amdgcn_alignbit(lo, lo, sh);
-      W.rows[r][1][bl] = __builtin_amdgcn_alignbit(hi, hi, sh);
+  for (int k = 0; k < kStageItems; ++k) {
+    const int g = il + 8 * k;
+    if (g < nrg) {
+      const uint32_t rot = (29u + P.rgp[rg0 + g]) & 31u;  // rotate right by 29 + p = left by 3 - p
+      uint32_t w[8];
+#pragma unroll
+      for (int hw = 0; hw < 2; ++hw) {
+        const uint32_t r0 = (uint32_t)(S.rw[k][0] >> (32 * hw)), r1 = (uint32_t)(S.rw[k][1] >> (32 * hw));
+        const uint32_t r2 = (uint32_t)(S.rw[k][2] >> (32 * hw)), r3 = (uint32_t)(S.rw[k][3] >> (32 * hw));
+        const uint32_t t01l = __builtin_amdgcn_perm(r1, r0, 0x05010400u);  // r0.b0 r1.b0 r0.b1 r1.b1
+        const uint32_t t01h = __builtin_amdgcn_perm(r1, r0, 0x07030602u);  // r0.b2 r1.b2 r0.b3 r1.b3
+        const uint32_t t23l = __builtin_amdgcn_perm(r3, r2, 0x05010400u);
+        const uint32_t t23h = __builtin_amdgcn_perm(r3, r2, 0x07030602u);
+        w[4 * hw + 0] = __builtin_amdgcn_perm(t23l, t01l, 0x05040100u);
+        w[4 * hw + 1] = __builtin_amdgcn_perm(t23l, t01l, 0x07060302u);
+        w[4 * hw + 2] = __builtin_amdgcn_perm(t23h, t01h, 0x05040100u);
+        w[4 * hw + 3] = __builtin_amdgcn_perm(t23h, t01h, 0x07060302u);
+      }
+      uint32_t* dst = &W.rows[g][bl >> 2][bl & 3];
+#pragma unroll
+      for (int m = 0; m < 8; ++m) dst[4 * m] = __builtin_amdgcn_alignbit(w[m], w[m], rot);
     }
-    if (r < nchan) W.scl[r][bl] = (uint16_t)S.sv[k];
+  }
+#pragma unroll
+  for (int k = 0; k < kScaleK; ++k) {
+    const int r = il + 8 * k;
+    if (r < nsc) W.scl[r][bl] = (uint16_t)S.sv[k];
   }
 }
 
 // Weights of chunk c for the 8 blocks of the group.  Lane = (block g, head
 // h, channel phase kk): each lane walks the chunk's channels a = kk, kk + KL,
-// ... and the per-(block, head) sums are reduced over kk.  first: this chunk
-// fixes delta; last: the candidate thresholds.  Blocks >= nbu get no bound
-// (their keys are never eligible).
+// ... and the per-(block, head) sums are reduced over kk.  first: delta is
+// fixed from every active channel; last: the candidate thresholds.  Blocks >= nbu get no bound
+// (their keys are never eligible).  A non-finite w leaves delta = 0 (first
+// chunk) or a non-finite E: no bound, every key of the block is a candidate.
 template <int G, int G4, bool SAMPLE>
 __device__ void weights(const UnitLds<G>& P, WaveLds<G4>& W, int c, bool first, bool last, int64_t gb, int64_t nbu) {
   constexpr int Gp = G <= 1 ? 1 : G <= 2 ? 2 : G <= 4 ? 4 : 8;
@@ -408,75 +447,68 @@ __device__ void weights(const UnitLds<G>& P, WaveLds<G4>& W, int c, bool first, 
   const int A = P.A;
   const int hh = gh ? h : 0;
   float delta, inv;
-  int fin = 1;
   if (first) {
-    float mx = 0.0f;
-    if (bv) {
-      for (int ai = a0 + kk; ai < a1; ai += KL) {
-        const float w = __fmul_rn(P.qa8[ai][hh], half_bits_to_float(W.scl[ai - a0][g]));
-        if (!(fabsf(w) <= 3.402823466e38f)) fin = 0;
-        mx = fmaxf(mx, fabsf(w));
-      }
+    float mx = 0.0f;  // fmaxf skips NaN; an infinite w makes mx infinite
+    if (bv) {  // over every active channel, not only this chunk's
+      for (int ai = kk; ai < A; ai += KL)
+        mx = fmaxf(mx, fabsf(__fmul_rn(P.qa[ai][hh], half_bits_to_float(W.scl[ai][g]))));
     }
 #pragma unroll
-    for (int m = Gp; m < 8; m <<= 1) {
-      mx = fmaxf(mx, __shfl_xor(mx, m, kWave));
-      fin &= __shfl_xor(fin, m, kWave);
-    }
+    for (int m = Gp; m < 8; m <<= 1) mx = fmaxf(mx, __shfl_xor(mx, m, kWave));
     int e;
     (void)frexpf(mx, &e);  // mx in [2^(e-1), 2^e)
-    const bool ok = fin && (mx >= 0x1p-100f || mx == 0.0f);
+    const bool ok = mx <= 3.402823466e38f && (mx >= 0x1p-100f || mx == 0.0f);
     const int ee = e < -100 ? -100 : e;
-    delta = ok ? ldexpf(1.0f, ee - 7) : 0.0f;  // |w| / delta < 128
-    inv = ok ? ldexpf(1.0f, 7 - ee) : 0.0f;
+    delta = ok ? ldexpf(1.0f, ee - 10) : 0.0f;  // |w| / delta < 1024
+    inv = ok ? ldexpf(1.0f, 10 - ee) : 0.0f;
   } else {
     delta = gh ? W.sdel[g][h] : 0.0f;
     inv = gh ? W.sinv[g][h] : 0.0f;
   }
-  float eb = 0.0f, sw = 0.0f;
-  int bias = 0;
+  float eb = 0.0f, sw = 0.0f, bs = 0.0f;  // bs: sum W zmax, an integer below 2^24
   if (bv) {
-    uint8_t* w8b = reinterpret_cast<uint8_t*>(&W.wB[g][h][0]);
+    uint8_t* whb = reinterpret_cast<uint8_t*>(&W.wB[g][h][0]);
+    uint8_t* wlb = reinterpret_cast<uint8_t*>(&W.wBl[g][h][0]);
     for (int ai = a0 + kk; ai < a1; ai += KL) {
       const int al = ai - a0;
-      const float w = __fmul_rn(P.qa8[ai][hh], half_bits_to_float(W.scl[al][g]));
-      if (!(fabsf(w) <= 3.402823466e38f)) fin = 0;
+      const float w = __fmul_rn(P.qa[ai][hh], half_bits_to_float(W.scl[ai][g]));
       const float zm = P.zmx[ai];
-      const float r = fminf(fmaxf(rintf(__fmul_rn(w, inv)), -127.0f), 127.0f);
-      const int ri = (int)r;
-      eb = __fmaf_rn(fabsf(__fmaf_rn(r, delta, -w)), zm, eb);
+      const float Wf = fminf(fmaxf(rintf(__fmul_rn(w, inv)), -1020.0f), 1019.0f);
+      eb = __fmaf_rn(fabsf(__fmaf_rn(Wf, delta, -w)), zm, eb);
       sw = __fadd_rn(sw, fabsf(w));
-      bias -= ri * (int)zm;
-      w8b[al] = (uint8_t)(ri & 0xFF);
+      bs = __fmaf_rn(Wf, zm, bs);
+      const int Wi = (int)Wf, wh = (Wi + 4) >> 3;
+      whb[al] = (uint8_t)(wh & 0xFF);
+      wlb[al] = (uint8_t)((Wi - 8 * wh) & 0xFF);
     }
   }
 #pragma unroll
   for (int m = Gp; m < 8; m <<= 1) {
     eb = __fadd_rn(eb, __shfl_xor(eb, m, kWave));
     sw = __fadd_rn(sw, __shfl_xor(sw, m, kWave));
-    bias += __shfl_xor(bias, m, kWave);
-    fin &= __shfl_xor(fin, m, kWave);
+    bs = __fadd_rn(bs, __shfl_xor(bs, m, kWave));
   }
   if (gh && kk == 0) {
-    if (!fin) delta = 0.0f;
     const float ebt = first ? eb : __fadd_rn(W.seb[g][h], eb);
     const float swt = first ? sw : __fadd_rn(W.ssw[g][h], sw);
-    const int biast = first ? bias : W.sbias[g][h] + bias;
+    const int biast = (first ? 0 : W.sbias[g][h]) - (int)bs;
     W.sdel[g][h] = delta;
     W.sinv[g][h] = inv;
     W.seb[g][h] = ebt;
     W.ssw[g][h] = swt;
     W.sbias[g][h] = biast;
     if (last && !SAMPLE) {
-      // candidate iff hdelta (acc + bias) + E >= tau, made conservative on
-      // integers: acc >= floor((tau - E) / hdelta) - bias - 1
-      const float E = __fmul_rn(__fmaf_rn(ebt, 0.5f, __fmul_rn((float)A * 0x1p-21f, swt)), 1.0f + 0x1p-10f);
+      // candidate iff (delta / 16) (2 acc + bias) + E >= tau, made conservative
+      // on integers: 2 acc >= floor((tau - E) 16 / delta) - bias - 1
+      const float E = __fmul_rn(
+          __fmaf_rn(ebt, 0.0625f, __fmaf_rn((float)(A + 1) * 0x1p-24f, swt, (float)A * 0x1p-120f)), 1.0f + 0x1p-10f);
       const float tau = P.tau[h];
       int thr = INT32_MIN;
       if (delta > 0.0f && tau != kNegInf && E <= 3.402823466e38f) {
-        const double x = ((double)tau - (double)E) / (0.5 * (double)delta);
+        const double x = ((double)tau - (double)E) * 16.0 / (double)delta;
         if (x == x) {
-          const double f = floor(x) - (double)biast - 1.0;
+          const double X = floor(x) - (double)biast - 1.0;
+          const double f = floor((X + 1.0) * 0.5);  // acc >= ceil(X / 2)
           thr = f <= -2147483648.0 ? INT32_MIN : f >= 2147483647.0 ? INT32_MAX : (int)f;
         }
       }
@@ -487,19 +519,22 @@ __device__ void weights(const UnitLds<G>& P, WaveLds<G4>& W, int c, bool first, 
 }
 
 // Integer proxy sums of chunk c for the 8 blocks, added to acc.  Per 4 U
-// dwords (16 channels) one v_mfma_i32_16x16x64_i8 per block: A = the 16 proxy
-// digits of each lane's key; B is block-diagonal, so lane group g' of A (keys
-// 16g'..16g'+15) meets only the weights in columns 4g'..4g'+3 (heads 0..3):
-// C[i][4g' + h] = sum_j z'_{16g'+i, j} w8_{j, h}.  Lane l then holds heads
+// dwords (16 channels) two v_mfma_i32_16x16x64_i8 per block: A = the 16
+// digits u (then 8 u) of each lane's key; B = Wl (then Wh), block-diagonal, so
+// lane group g' of A (keys 16g'..16g'+15) meets only the weights in columns
+// 4g'..4g'+3 (heads 0..3): C[i][4g' + h] = sum_j u_{16g'+i, j} W_{j, h}.  Lane l then holds heads
 // 4p + l%4 of keys 16((l%16)/4) + 4(l/16) + r, r = 0..3, in acc[g][p][r].
 typedef __attribute__((ext_vector_type(4))) int v4i;
 template <int G, int G4>
-__device__ __forceinline__ void chunk_proxy(const UnitLds<G>& P, const WaveLds<G4>& W, int c, uint32_t M0, int s,
+__device__ __forceinline__ void chunk_proxy(const UnitLds<G>& P, const WaveLds<G4>& W, int c,
                                             v4i (&acc)[kGrp][G4 / 4]) {
   constexpr int NP = G4 / 4;
-  const int lane = threadIdx.x & 63, half = lane >> 5;
-  const int d0 = uni(P.chd[c]), d1 = uni(P.chd[c + 1]), cr0 = uni(P.chr[c]);
+  const int lane = threadIdx.x & 63, sk = lane & 7, m4 = 4 * (lane >> 3);
+  const int d0 = uni(P.chd[c]), d1 = uni(P.chd[c + 1]);
   const bool wlane = (lane >> 4) == ((lane & 15) >> 2);
+  uint32_t mk[4];  // plane p: this lane's bits of a transposed, rotated word
+#pragma unroll
+  for (int p = 0; p < 4; ++p) mk[p] = 0x01010101u << ((sk + 3 - p) & 7);
 #pragma unroll
   for (int gh = 0; gh < kGrp; gh += 4) {  // blocks gh .. gh+3
     for (int db = d0; db < d1; db += 4) {
@@ -509,27 +544,21 @@ __device__ __forceinline__ void chunk_proxy(const UnitLds<G>& P, const WaveLds<G
         uint32_t zr[4] = {0u, 0u, 0u, 0u};
         const int d = db + q;
         if (d < d1) {
-          const int nq = uni((int)P.dnq[d]);
-          const int rb = uni((int)P.drow[d]);
-          for (int iq = 0; iq < nq; ++iq) {
-            const int r = rb + 4 * iq;
-            const uint4 sh = *reinterpret_cast<const uint4*>(&P.rsh[cr0 + r]);
-            uint4 x[4];
+          const int nr = uni((int)P.dnr[d]);
+          const int rb = uni((int)P.drg[d]);
 #pragma unroll
-            for (int i = 0; i < 4; ++i) x[i] = *reinterpret_cast<const uint4*>(&W.rows[r + i][half][gh]);
-            const uint32_t m[4] = {__builtin_amdgcn_alignbit(M0, M0, sh.x), __builtin_amdgcn_alignbit(M0, M0, sh.y),
-                                   __builtin_amdgcn_alignbit(M0, M0, sh.z), __builtin_amdgcn_alignbit(M0, M0, sh.w)};
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-              zr[0] |= x[i].x & m[i];
-              zr[1] |= x[i].y & m[i];
-              zr[2] |= x[i].z & m[i];
-              zr[3] |= x[i].w & m[i];
+          for (int p = 0; p < 4; ++p) {
+            if (p < nr) {
+              const uint4 x = *reinterpret_cast<const uint4*>(&W.rows[rb + p][gh >> 2][m4]);
+              zr[0] |= x.x & mk[p];
+              zr[1] |= x.y & mk[p];
+              zr[2] |= x.z & mk[p];
+              zr[3] |= x.w & mk[p];
             }
           }
         }
 #pragma unroll
-        for (int g = 0; g < 4; ++g) zq[q][g] = __builtin_amdgcn_alignbit(zr[g], zr[g], (uint32_t)s);
+        for (int g = 0; g < 4; ++g) zq[q][g] = __builtin_amdgcn_alignbit(zr[g], zr[g], (uint32_t)sk);
       }
       const int mq = (db - d0) >> 2;
 #pragma unroll
@@ -538,10 +567,13 @@ __device__ __forceinline__ void chunk_proxy(const UnitLds<G>& P, const WaveLds<G
         const bool wl = wlane && hh < G;
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
-          const uint32_t* src = wl ? &W.wB[gh + g][hh < G4 ? hh : 0][4 * mq] : W.zero16;
-          const v4i bv = *reinterpret_cast<const v4i*>(src);
-          const v4i av = {(int)zq[0][g], (int)zq[1][g], (int)zq[2][g], (int)zq[3][g]};
-          acc[gh + g][pp] = __builtin_amdgcn_mfma_i32_16x16x64_i8(av, bv, acc[gh + g][pp], 0, 0, 0);
+          const int hc = hh < G4 ? hh : 0;
+          const v4i bl = *reinterpret_cast<const v4i*>(wl ? &W.wBl[gh + g][hc][4 * mq] : W.zero16);
+          const v4i bh = *reinterpret_cast<const v4i*>(wl ? &W.wB[gh + g][hc][4 * mq] : W.zero16);
+          const v4i al = {(int)zq[0][g], (int)zq[1][g], (int)zq[2][g], (int)zq[3][g]};
+          const v4i ah = {(int)(zq[0][g] << 3), (int)(zq[1][g] << 3), (int)(zq[2][g] << 3), (int)(zq[3][g] << 3)};
+          acc[gh + g][pp] = __builtin_amdgcn_mfma_i32_16x16x64_i8(al, bl, acc[gh + g][pp], 0, 0, 0);
+          acc[gh + g][pp] = __builtin_amdgcn_mfma_i32_16x16x64_i8(ah, bh, acc[gh + g][pp], 0, 0, 0);
         }
       }
     }
@@ -554,7 +586,7 @@ __device__ __forceinline__ void chunk_proxy(const UnitLds<G>& P, const WaveLds<G
 template <int G, int G4, bool SAMPLE, typename GroupBlock, typename Finish>
 __device__ void wave_groups(const UnitLds<G>& P, WaveLds<G4>& W, const FusedArgs& a, int u, int ngroups, int64_t nbu,
                             GroupBlock group_block, Finish finish) {
-  const int lane = threadIdx.x & 63, s = lane & 31;
+  const int lane = threadIdx.x & 63;
   const int nch = uni(P.nch);
   if (ngroups <= 0 || nch <= 0) {
     for (int gi = 0; gi < ngroups; ++gi) {  // no active channel: every proxy is 0 with E = 0
@@ -584,7 +616,6 @@ __device__ void wave_groups(const UnitLds<G>& P, WaveLds<G4>& W, const FusedArgs
     }
     return;
   }
-  const uint32_t M0 = 1u << s;
   const int items = ngroups * nch;
   Stage S;
   stage_load<G>(S, P, a, u, group_block(0), 0);
@@ -605,7 +636,7 @@ __device__ void wave_groups(const UnitLds<G>& P, WaveLds<G4>& W, const FusedArgs
     wave_lds_sync();
     weights<G, G4, SAMPLE>(P, W, c, c == 0, c == nch - 1, gb, nbu);
     wave_lds_sync();
-    chunk_proxy<G, G4>(P, W, c, M0, s, acc);
+    chunk_proxy<G, G4>(P, W, c, acc);
     if (c == nch - 1) {
       finish(gb, acc);
 #pragma unroll
@@ -654,7 +685,7 @@ __global__ __launch_bounds__(kFT, 3) void fused_sample_kernel(FusedArgs a) {
           // the proxy itself (exact in fp32): tau only steers how many keys are
           // re-scored; the survivor count, not tau, guarantees the result
           float v = kNegInf;
-          if (b < nbu && i >= lo && i < hi && del > 0.0f) v = __fmul_rn(0.5f * del, (float)(acc[g][pp][q] + bias));
+          if (b < nbu && i >= lo && i < hi && del > 0.0f) v = __fmul_rn(0.0625f * del, (float)(2 * acc[g][pp][q] + bias));
 #pragma unroll
           for (int z = 0; z < 4; ++z) {  // insert into the descending t[0..3]
             const float hi2 = fmaxf(t[z], v);

@@ -511,3 +511,43 @@ def test_scan_topk_direct_rows_large_k():
             oi, ov, _ = oracle.topk(ref[h], k)
             assert np.array_equal(idx[u, h].cpu().numpy(), oi), (u, h)
             assert np.array_equal(val[u, h].cpu().numpy().view(np.uint32), ov.view(np.uint32)), (u, h)
+
+
+@pytest.mark.parametrize("case", ["waterfill48", "waterfill200", "random_depths"])
+def test_scan_topk_filter_misses_no_survivor(case):
+    """White-box check of the fused filter's bound (Sec. 3.2 scores, proxy
+    error bound): every eligible key whose documented score reaches the row's
+    threshold tau must be kept, so the survivor count the full pass leaves per
+    row equals the oracle's count of scores >= tau.  Reads tau and the
+    per-sub-list counts from the workspace (tau: the first U*G floats; counts:
+    the next 256-byte aligned region, 8 per row)."""
+    rng = np.random.default_rng(81)
+    ns = [131072, 100000, 77777, 131000]
+    K, nt, planes, scales = _store(ns, 82)
+    U, G, k = len(ns), 4, 1024
+    q = rng.standard_normal((U, G, 128)).astype(np.float16)
+    qt = torch.from_numpy(q).to(DEV)
+    var = torch.from_numpy(np.exp(rng.standard_normal((U, 128))).astype(np.float32)).to(DEV)
+    if case == "random_depths":
+        d = torch.from_numpy(rng.integers(0, 5, (U, 128)).astype(np.uint8)).to(DEV)
+    else:
+        d, _ = F.fathom_alloc_depths(qt, var, F.FATHOM_WATERFILL, 48 if case == "waterfill48" else 200)
+    nb = planes.shape[-1]
+    wsb = F.fathom_scan_topk_workspace_size(U, G, 64 * nb, k)
+    ws = torch.zeros((wsb,), dtype=torch.uint8, device=DEV)
+    st = F.new_status()
+    idx, val = F.fathom_scan_topk(planes, scales, nt, qt, d, k, ws=ws, dev_status=st)
+    assert status(st) == 0
+    R = U * G
+    tau = ws[:4 * R].view(torch.float32).cpu().numpy()
+    off = (4 * R + 255) // 256 * 256
+    cnt = ws[off:off + 32 * R].view(torch.int32).view(R, 8).sum(1).cpu().numpy()
+    dd = d.cpu().numpy()
+    for u, nu in enumerate(ns):
+        ref = oracle.scores_f32(u64(planes)[u], u16(scales)[u], nu, q[u].astype(np.float32), dd[u])
+        for h in range(G):
+            r = u * G + h
+            assert np.isfinite(tau[r]), r
+            assert int(cnt[r]) == int(np.count_nonzero(ref[h] >= tau[r])), (case, u, h)
+            oi, ov, _ = oracle.topk(ref[h], k)
+            assert np.array_equal(idx[u, h].cpu().numpy(), oi), (case, u, h)
