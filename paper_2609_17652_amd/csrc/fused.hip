@@ -57,7 +57,7 @@ constexpr int kMaxRg = kD;         // row groups: at most 4 planes x 32 dwords
 constexpr int kStP = 65;           // LDS dwords per staged row group (64 lanes + pad)
 constexpr int kRing = 3;           // superquads of scales kept for re-scoring
 constexpr int kQCap = 64;          // queued candidates per wave at most
-constexpr int kSlots = 8;          // survivor sub-lists per row (spreads the append counters)
+constexpr int kSlots = 8;          // survivor value buckets per row
 constexpr int kSmpW = 8;           // sample proxies kept per (sampled wave, head)
 constexpr int kSampleQuads = 64;   // at most this many sampled quads per unit
 constexpr int kSmpRow = kSampleQuads * kSmpW;
@@ -71,12 +71,12 @@ constexpr float kNegInf = -__builtin_huge_valf();
 
 struct FusedWs {
   float* tau;       // [R] threshold on exact scores (-inf: the row is computed exactly by pass 4)
-  uint32_t* cnt;    // [R][kSlots] survivors appended to sub-list s
-  uint64_t* cand;   // [R][kSlots][scap] survivors: score_key << 32 | ~index
+  uint32_t* cnt;    // [R][kSlots] survivors appended to value bucket z
+  uint64_t* cand;   // [R][kSlots][scap] survivors by bucket: score_key << 32 | ~index
+  uint32_t* bnd;    // [R][kSlots] score keys splitting a row's survivors into kSlots value buckets
   uint32_t* uovf;   // [U] from pass 2: (slices of the unit's filter) << 1, 0 = no filter; bit 0 unused
-  uint32_t* bnd;    // [R][kSlots] score keys splitting the survivors into kSlots ranges
   float* samp;      // [R][kSmpRow] sampled proxies
-  int cap, scap;    // survivors per row (select kernel), per sub-list
+  int cap, scap;    // rows with at most cap eligible keys are scored directly; bucket capacity
   int64_t s_stride; // sample every s_stride-th quad
   int s_quads;      // sampled quads per unit
   int qpw;          // full pass: quads per wave (a multiple of 4)
@@ -202,6 +202,7 @@ struct alignas(16) Plan {
   int rgslot[kMaxRg];          // row group g: staging slot 4 * (d mod 4) + p within its slice
   int slmask[kMaxSl];          // slice s: bit 4 dd + p set iff dword 4s + dd has plane p
   float tau[4];
+  uint32_t bnd[4][kSlots];     // head h: score keys splitting its survivors into value buckets
 };
 
 __device__ void plan_setup(Plan& P, const FusedArgs& a, int u) {
@@ -568,7 +569,7 @@ __device__ __forceinline__ void task_stage(const uint64_t (&w)[4], const Plan& P
 // digits and the scales kept in the ring, and their appends to the survivor
 // lists.
 template <int SQB, class WL>
-__device__ __forceinline__ void rescore_batch(const Plan& P, WL& W, const FusedArgs& a, int u, int nq, int slot) {
+__device__ __forceinline__ void rescore_batch(const Plan& P, WL& W, const FusedArgs& a, int u, int nq) {
   const int lane = threadIdx.x & 63, G = a.G;
   wave_lds_sync();
   const bool on = lane < nq;
@@ -603,32 +604,43 @@ __device__ __forceinline__ void rescore_batch(const Plan& P, WL& W, const FusedA
       }
     }
   }
+  // value buckets: boundaries bnd[h][1..] descend and bucket z holds keys in
+  // (bnd[h][z+1], bnd[h][z]].  Lane 8 h + z counts head h's survivors in
+  // bucket z, so one atomic instruction reserves every list's slots.
+  uint32_t key[4], pre[4] = {0u, 0u, 0u, 0u}, cl = 0u;
+  int bk[4] = {0, 0, 0, 0};
+  bool keep[4];
+  bool any = false;
 #pragma unroll
   for (int h = 0; h < 4; ++h) {
-    if (h >= G) break;
-    const bool keep = on && ((hm >> h) & 1) && s[h] >= P.tau[h];
-    const uint64_t bm = __ballot(keep);
-    if (bm) {
-      const int r = u * G + h;
-      const int leader = __ffsll((unsigned long long)bm) - 1;
-      uint32_t base = 0;
-      if (lane == leader) base = gatomic_add(&a.ws.cnt[r * kSlots + slot], (uint32_t)__popcll(bm));
-      base = __shfl(base, leader, kWave);
-      if (keep) {
-        const uint32_t pos = base + (uint32_t)__popcll(bm & lanemask_lt(lane));
-        if (pos < (uint32_t)a.ws.scap)
-          gstore(&a.ws.cand[((int64_t)r * kSlots + slot) * a.ws.scap + pos],
-                 ((uint64_t)score_key(s[h]) << 32) | (uint64_t)(~i));
-      }
+    keep[h] = h < G && on && ((hm >> h) & 1) && s[h] >= P.tau[h];
+    key[h] = score_key(s[h]);
+    if (__ballot(keep[h]) == 0ull) continue;
+    any = true;
+#pragma unroll
+    for (int z = 1; z < kSlots; ++z) bk[h] += key[h] <= P.bnd[h][z];
+#pragma unroll
+    for (int z = 0; z < kSlots; ++z) {
+      const bool mine = keep[h] && bk[h] == z;
+      const uint64_t bm = __ballot(mine);
+      if (lane == kSlots * h + z) cl = (uint32_t)__popcll(bm);
+      if (mine) pre[h] = (uint32_t)__popcll(bm & lanemask_lt(lane));
+    }
+  }
+  if (any) {
+    uint32_t base = 0u;
+    if (cl) base = gatomic_add(&a.ws.cnt[u * G * kSlots + lane], cl);
+#pragma unroll
+    for (int h = 0; h < 4; ++h) {
+      const uint32_t pos = __shfl(base, kSlots * h + bk[h], kWave) + pre[h];
+      if (keep[h] && pos < (uint32_t)a.ws.scap)
+        gstore(&a.ws.cand[((int64_t)(u * G + h) * kSlots + bk[h]) * a.ws.scap + pos],
+               ((uint64_t)key[h] << 32) | (uint64_t)(~i));
     }
   }
   wave_lds_sync();
 }
 
-template <int SQB, class WL>
-__device__ __noinline__ void rescore_batch_call(const Plan& P, WL& W, const FusedArgs& a, int u, int nq, int slot) {
-  rescore_batch<SQB>(P, W, a, u, nq, slot);
-}
 
 // Runs superquads of SQB blocks over blocks [b0, b1) (b0 a multiple of 4) of
 // unit u.  The next quad's plane words (one register set per slice) and the
@@ -639,7 +651,7 @@ __device__ __noinline__ void rescore_batch_call(const Plan& P, WL& W, const Fuse
 // SAMPLE: one quad; the 8 largest proxies per head go to sample slot `sidx`.
 template <bool QF16, bool SAMPLE, int NSLM, int SQB, int RQ, int QCAP>
 __device__ void wave_run(const Plan& P, WaveLdsT<NSLM, SQB, RQ, QCAP>& W, const FusedArgs& a, int u, int64_t b0,
-                         int64_t b1, int64_t nbu, int64_t lo, int64_t hi, int64_t sidx, int slot0) {
+                         int64_t b1, int64_t nbu, int64_t lo, int64_t hi, int64_t sidx) {
   constexpr int NCH = NSLM > 4 ? 2 : 1;
   constexpr int kFlushAt = QCAP * 3 / 4;
   const int lane = threadIdx.x & 63;
@@ -648,7 +660,7 @@ __device__ void wave_run(const Plan& P, WaveLdsT<NSLM, SQB, RQ, QCAP>& W, const 
   const int lb = lane >> 4;                              // block of the quad
   const bool wl = ((lane & 15) >> 2) == lb;              // carries weights in the A operand
   const int wh = lane & 3;
-  int pending = 0, batches = 0, oldest = 0;
+  int pending = 0, oldest = 0;
   SclRegs<NCH, SQB> sr;
   scl_issue(sr, P, a, u, b0);
   uint64_t ring[NSLM][4];
@@ -659,7 +671,7 @@ __device__ void wave_run(const Plan& P, WaveLdsT<NSLM, SQB, RQ, QCAP>& W, const 
   for (int64_t sb0 = b0; sb0 < b1; sb0 += SQB, ++sqi) {
     const int rslot = sqi % RQ;
     if (!SAMPLE && pending > 0 && oldest <= sqi - RQ) {  // its scales are about to be overwritten
-      rescore_batch<SQB>(P, W, a, u, pending, (slot0 + batches++) % kSlots);
+      rescore_batch<SQB>(P, W, a, u, pending);
       pending = 0;
     }
     const SqInfo si = scl_commit<QF16, NCH, SQB>(sr, P, W, rslot);
@@ -668,7 +680,7 @@ __device__ void wave_run(const Plan& P, WaveLdsT<NSLM, SQB, RQ, QCAP>& W, const 
     const int64_t sb1 = sb0 + SQB < b1 ? sb0 + SQB : b1;
     for (int64_t qb0 = sb0; qb0 < sb1; qb0 += kQB) {
       if (!SAMPLE && pending >= kFlushAt) {
-        rescore_batch<SQB>(P, W, a, u, pending, (slot0 + batches++) % kSlots);
+        rescore_batch<SQB>(P, W, a, u, pending);
         pending = 0;
       }
       const int qo = (int)(qb0 - sb0);  // quad offset within the superquad
@@ -736,17 +748,28 @@ __device__ void wave_run(const Plan& P, WaveLdsT<NSLM, SQB, RQ, QCAP>& W, const 
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           if (r >= a.G) break;
-          float v = best[r];
-          float* dst = a.ws.samp + ((int64_t)u * a.G + r) * kSmpRow + sidx * kSmpW;
-          for (int t = 0; t < kSmpW; ++t) {
-            float m = v;
-#pragma unroll
-            for (int o = 32; o >= 1; o >>= 1) m = fmaxf(m, __shfl_xor(m, o, kWave));
-            const uint64_t wb = __ballot(v == m);
-            const int wlane = __ffsll((unsigned long long)wb) - 1;
-            if (lane == 0) gstore(dst + t, m);
-            if (lane == wlane) v = kNegInf;
+          // the kSmpW largest lane values: threshold = the kSmpW-th largest key
+          // (bitwise search with ballot counts), then the lanes above it
+          const uint32_t key = best[r] > kNegInf ? score_key(best[r]) | 1u : 0u;
+          uint32_t prefix = 0u;
+          for (int bit = 31; bit >= 0; --bit) {
+            const uint32_t cand = prefix | (1u << bit);
+            if (__popcll(__ballot(key >= cand)) >= kSmpW) prefix = cand;
           }
+          const bool above = key > prefix && key != 0u;
+          const uint64_t ma = __ballot(above);
+          const int na = __popcll(ma);                       // < kSmpW
+          const uint64_t me = __ballot(key == prefix && key != 0u);
+          float* dst = a.ws.samp + ((int64_t)u * a.G + r) * kSmpRow + sidx * kSmpW;
+          int pos = -1;
+          if (above) pos = __popcll(ma & lanemask_lt(lane));
+          else if (key == prefix && key != 0u) {
+            const int e = __popcll(me & lanemask_lt(lane));
+            if (na + e < kSmpW) pos = na + e;
+          }
+          if (pos >= 0) gstore(dst + pos, best[r]);
+          const int nw = na + __popcll(me) < kSmpW ? na + __popcll(me) : kSmpW;
+          if (lane >= nw && lane < kSmpW) gstore(dst + lane, kNegInf);
         }
       } else {
         bool fl[4];
@@ -762,14 +785,17 @@ __device__ void wave_run(const Plan& P, WaveLdsT<NSLM, SQB, RQ, QCAP>& W, const 
           tot += __popcll(M[mu]);
         }
         if (tot > 0) {
+          if (pending + tot > QCAP) {  // make room (rare: the flush at the top of a quad usually does)
+            rescore_batch<SQB>(P, W, a, u, pending);
+            pending = 0;
+          }
           if (pending == 0) oldest = sqi;
-          const bool fits = pending + tot <= QCAP;
           const uint32_t meta = (uint32_t)rslot << 8 | (uint32_t)(qo + lb) << 12;
 #pragma unroll
           for (int mu = 0; mu < 4; ++mu) {
             if (M[mu]) {
-              if (!fits && pending + __popcll(M[mu]) > QCAP) {  // this quad overflows the queue
-                rescore_batch_call<SQB>(P, W, a, u, pending, (slot0 + batches++) % kSlots);
+              if (pending + __popcll(M[mu]) > QCAP) {  // more than QCAP in one quad
+                rescore_batch<SQB>(P, W, a, u, pending);
                 pending = 0;
                 oldest = sqi;
               }
@@ -791,7 +817,7 @@ __device__ void wave_run(const Plan& P, WaveLdsT<NSLM, SQB, RQ, QCAP>& W, const 
       }
     }
   }
-  if (!SAMPLE && pending > 0) rescore_batch<SQB>(P, W, a, u, pending, (slot0 + batches++) % kSlots);
+  if (!SAMPLE && pending > 0) rescore_batch<SQB>(P, W, a, u, pending);
 }
 
 // ---------------------------------------------------------------- pass 1
@@ -819,7 +845,7 @@ __global__ __launch_bounds__(kFT) void fused_sample_kernel(FusedArgs a) {
       if (lane < kSmpW) gstore(a.ws.samp + ((int64_t)u * a.G + r) * kSmpRow + sq * kSmpW + lane, kNegInf);
     return;
   }
-  wave_run<QF16, true, kMaxSl, kQB, 1, 0>(P, WL[wave], a, u, b0, b0 + kQB, nbu, lo, hi, sq, 0);
+  wave_run<QF16, true, kMaxSl, kQB, 1, 0>(P, WL[wave], a, u, b0, b0 + kQB, nbu, lo, hi, sq);
 }
 
 // ---------------------------------------------------------------- pass 2
@@ -834,7 +860,10 @@ __global__ __launch_bounds__(kTauThreads) void fused_tau_kernel(FusedArgs a) {
   __shared__ int sA;
   __shared__ int64_t sm;
   const int r = blockIdx.x, G = a.G, u = r / G, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  if (tid < kSlots) a.ws.cnt[r * kSlots + tid] = 0u;
+  if (tid < kSlots) {
+    a.ws.cnt[r * kSlots + tid] = 0u;
+    a.ws.bnd[r * kSlots + tid] = 0u;
+  }
   int64_t nu, lo, hi;
   row_window(a, u, &nu, &lo, &hi, false);
   if (tid == 0) sA = 0;
@@ -919,6 +948,10 @@ __global__ __launch_bounds__(kFT) void fused_main_kernel(FusedArgs a) {
   if (gw * a.ws.qpw >= qhi || (gw + kFW) * a.ws.qpw <= qlo) return;
   plan_setup(P, a, u);
   if (tid < 4) P.tau[tid] = tid < a.G ? gload(a.ws.tau + u * a.G + tid) : kNegInf;
+  if (tid < 4 * kSlots) {
+    const int h = tid / kSlots;
+    P.bnd[h][tid % kSlots] = h < a.G ? gload(a.ws.bnd + (u * a.G + h) * kSlots + tid % kSlots) : 0u;
+  }
   __syncthreads();
   if (!P.ok || P.A == 0 || P.nsl > NSLM) return;
   bool any = false;
@@ -928,8 +961,8 @@ __global__ __launch_bounds__(kFT) void fused_main_kernel(FusedArgs a) {
   if (q0 < qlo) q0 = qlo;
   if (q1 > qhi) q1 = qhi;
   if (q0 >= q1) return;
-  wave_run<QF16, false, NSLM, SQB, kRing, kQCap>(P, WL[wave], a, u, q0 * kQB, q1 * kQB < nbu ? q1 * kQB : nbu, nbu, lo, hi, 0,
-                                   (int)((gw + wave) % kSlots));
+  wave_run<QF16, false, NSLM, SQB, kRing, kQCap>(P, WL[wave], a, u, q0 * kQB, q1 * kQB < nbu ? q1 * kQB : nbu, nbu,
+                                                  lo, hi, 0);
 }
 
 // ---------------------------------------------------------------- pass 4
@@ -999,46 +1032,48 @@ __device__ __forceinline__ float exact_score1(const int* act, int A, const float
   return acc;
 }
 
-// Pass 4, rows not done by fused_rank_kernel, one workgroup per row: a row with
-// no more eligible keys than the survivor list holds is scored directly, and a
-// row whose filter under-collected (or whose lists overflowed) is recomputed
-// exactly, both with a streaming top-k over exact scores.
+// The survivors of row r (bucket counts cnt8) hold its top k exactly when no
+// bucket overflowed, at least k were found and the filter ran for the row.
+__device__ __forceinline__ bool survivors_complete(const uint32_t* cnt8, const FusedArgs& a, float tau, uint32_t ovf) {
+  uint32_t C = 0;
+  bool over = false;
+#pragma unroll
+  for (int z = 0; z < kSlots; ++z) {
+    C += cnt8[z];
+    over |= cnt8[z] > (uint32_t)a.ws.scap;
+  }
+  return !over && C >= (uint32_t)a.k && (ovf & 1u) == 0u && tau != kNegInf;
+}
+
+// Pass 4 (exact rows), one 1024-thread workgroup per row.  A row with no more
+// eligible keys than the survivor lists hold is scored directly, and a row
+// whose filter under-collected (or whose lists overflowed) is recomputed
+// exactly, both with a streaming top-k over exact scores.  Every other row is
+// left to fused_rank_kernel.
 __global__ __launch_bounds__(kSelThreads) void fused_select_kernel(FusedArgs a, int32_t* __restrict__ idx,
                                                                    float* __restrict__ val) {
   extern __shared__ uint64_t buf[];
   __shared__ int act[kD];          // active channels ascending (streaming path)
   __shared__ float qa[kD];         // q of this row's head per active channel
   __shared__ int nact;
-  __shared__ int s_count, s_above;
+  __shared__ int s_count;
   __shared__ uint64_t s_thr;
   __shared__ int wc[2];
   __shared__ uint32_t s_sub[kSlots];
   const int G = a.G;
-  const int part = blockIdx.x, r = blockIdx.y, u = r / G, h = r % G, tid = threadIdx.x, lane = tid & 63,
-            wave = tid >> 6;
+  const int r = blockIdx.x, u = r / G, h = r % G, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   int64_t nu, lo, hi;
   row_window(a, u, &nu, &lo, &hi, false);
   const int k = a.k;
   if (tid < kSlots) s_sub[tid] = gload(a.ws.cnt + r * kSlots + tid);
   if (tid == 0) {
     s_count = 0;
-    s_above = 0;
     s_thr = 0ull;
   }
   __syncthreads();
-  uint32_t C = 0;
-  bool sub_over = false;
-  for (int q2 = 0; q2 < kSlots; ++q2) {
-    C += s_sub[q2];
-    sub_over |= s_sub[q2] > (uint32_t)a.ws.scap;
-  }
-  const float tau = gload(a.ws.tau + r);
   const bool direct = hi - lo <= a.ws.cap;
-  const bool fallback =
-      !direct && (sub_over || C > (uint32_t)kSelCap || C < (uint32_t)k || (gload(a.ws.uovf + u) & 1u) != 0u ||
-                  tau == kNegInf);
-  if (!direct && !fallback) return;  // done by fused_rank_kernel
-  if (part != 0) return;
+  const bool fallback = !direct && !survivors_complete(s_sub, a, gload(a.ws.tau + r), gload(a.ws.uovf + u));
+  if (!direct && !fallback) return;
   // streaming top-k over all eligible keys with exact scores
   {
     int t = 0;
@@ -1116,105 +1151,121 @@ __global__ __launch_bounds__(kSelThreads) void fused_select_kernel(FusedArgs a, 
   if (__syncthreads_or(shortfall) && tid == 0) set_status(a.st, FATHOM_DEV_TOPK_SHORT);
 }
 
-// Pass 4, normal rows: one 256-thread workgroup per (score range, row).  The
-// survivors of a row are split by the boundaries from pass 2; workgroup b
-// sorts the survivors of range b and writes them after the ones of the ranges
-// above.  Rows that are scored directly or need the exact fallback are left
-// to fused_select_kernel, as is every row of a unit whose range overflowed
-// this kernel's buffer (uovf[u] bit 0).
+// Pass 4 (filtered rows): workgroup (z, r) orders the survivors of value
+// bucket z of row r.  Every survivor of a higher bucket outscores every one of
+// bucket z, so a survivor's output position is (survivors of the buckets
+// above) + (survivors of its own bucket with a larger composite).  Within the
+// bucket a counting sort on an interpolated sub-bucket of the score key
+// (monotone in the key) groups the survivors; only survivors sharing a
+// sub-bucket are compared.  Composites are distinct (they carry the index), so
+// the positions are a permutation.
 constexpr int kRankThreads = 256;
-constexpr int kRankCap = 4096;
+constexpr int kRankCap = kSelCap / 4;  // bucket capacity (largest scap)
+constexpr int kRankSub = 2048;         // sub-buckets at most
 __global__ __launch_bounds__(kRankThreads) void fused_rank_kernel(FusedArgs a, int32_t* __restrict__ idx,
                                                                  float* __restrict__ val) {
-  __shared__ uint64_t buf[kRankCap];
-  __shared__ uint32_t s_cnt[kSlots], s_sub[kSlots + 1], s_b[2];
+  __shared__ uint64_t buf[kRankCap], grp[kRankCap];
+  __shared__ uint32_t hist[kRankSub];
+  __shared__ uint32_t s_cnt[kSlots], s_red[2][kRankThreads / kWave], s_part[kRankThreads / kWave];
   __shared__ float s_tau;
+  __shared__ uint32_t s_ovf;
   __shared__ int64_t s_n;
-  __shared__ int s_count, s_above;
   const int G = a.G;
-  const int part = blockIdx.x, r = blockIdx.y, u = r / G, tid = threadIdx.x, lane = tid & 63;
-  // every scalar this workgroup needs, loaded at once
+  const int z = blockIdx.x, r = blockIdx.y, u = r / G, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   if (tid < kSlots) s_cnt[tid] = gload(a.ws.cnt + r * kSlots + tid);
   else if (tid == kSlots) s_tau = gload(a.ws.tau + r);
-  else if (tid == kSlots + 1) s_b[0] = gload(a.ws.bnd + r * kSlots + part);
-  else if (tid == kSlots + 2) s_b[1] = part + 1 < kSlots ? gload(a.ws.bnd + r * kSlots + part + 1) : 0u;
-  else if (tid == kSlots + 3) s_n = gload(a.n + u);
-  else if (tid == kSlots + 4) {
-    s_count = 0;
-    s_above = 0;
-  }
-  __syncthreads();
-  if (tid == 0) {
-    uint32_t c = 0;
-    bool over = false;
-    for (int q2 = 0; q2 < kSlots; ++q2) {
-      over |= s_cnt[q2] > (uint32_t)a.ws.scap;
-      s_sub[q2] = c;
-      c += s_cnt[q2];
-    }
-    s_sub[kSlots] = over ? 0xFFFFFFFFu : c;
-  }
+  else if (tid == kSlots + 1) s_ovf = gload(a.ws.uovf + u);
+  else if (tid == kSlots + 2) s_n = gload(a.n + u);
   __syncthreads();
   int64_t nu = s_n;
   if (nu < 0 || nu > a.nb_cap * kBlockTokens) nu = 0;
   int64_t lo = a.lo, hi = nu - a.tail;
   if (hi < lo) hi = lo;
-  if (hi - lo <= a.ws.cap || s_tau == kNegInf) return;
-  const uint32_t C = s_sub[kSlots];
-  const int k = a.k;
-  if (C == 0xFFFFFFFFu || C > (uint32_t)kSelCap || C < (uint32_t)k) return;  // fallback rows
-  const uint32_t ub = s_b[0], lb = s_b[1];
-  int above = 0;
-  constexpr int kL = 16;  // loads in flight per thread
-  for (uint32_t i0 = 0; i0 < C; i0 += kL * kRankThreads) {
-    uint64_t v[kL];
-#pragma unroll
-    for (int c = 0; c < kL; ++c) {  // element i of the concatenated sub-lists
-      const uint32_t i = i0 + c * kRankThreads + tid;
-      v[c] = 0ull;
-      if (i < C) {
-        int q2 = 0;
-#pragma unroll
-        for (int z = 1; z < kSlots; ++z) q2 += i >= s_sub[z];
-        v[c] = gload(a.ws.cand + ((int64_t)r * kSlots + q2) * a.ws.scap + (i - s_sub[q2]));
-      }
-    }
-#pragma unroll
-    for (int c = 0; c < kL; ++c) {
-      const bool on = i0 + c * kRankThreads + tid < C;
-      const uint32_t key = (uint32_t)(v[c] >> 32);
-      above += on && key > ub;
-      const bool mine = on && key <= ub && key > lb;
-      const uint64_t bm = __ballot(mine);
-      if (bm) {
-        int base = 0;
-        const int leader = __ffsll((unsigned long long)bm) - 1;
-        if (lane == leader) base = atomicAdd(&s_count, __popcll(bm));
-        base = __shfl(base, leader, kWave);
-        const int pos = base + __popcll(bm & lanemask_lt(lane));
-        if (mine && pos < kRankCap) buf[pos] = v[c];
-      }
-    }
+  if (hi - lo <= a.ws.cap || !survivors_complete(s_cnt, a, s_tau, s_ovf)) return;
+  uint32_t off0 = 0;
+  for (int y = 0; y < z; ++y) off0 += s_cnt[y];
+  const int c = (int)s_cnt[z], k = a.k;
+  if (off0 >= (uint32_t)k || c == 0) return;
+  // load, and the bucket's key range
+  const uint64_t* src = a.ws.cand + ((int64_t)r * kSlots + z) * a.ws.scap;
+  uint32_t kmin = 0xFFFFFFFFu, kmax = 0u;
+  for (int e = tid; e < c; e += kRankThreads) {
+    const uint64_t v = gload(src + e);
+    buf[e] = v;
+    const uint32_t key = (uint32_t)(v >> 32);
+    kmin = key < kmin ? key : kmin;
+    kmax = key > kmax ? key : kmax;
   }
+  int ns = 64;  // sub-buckets: a power of two, about twice the survivors
+  while (ns < 2 * c && ns < kRankSub) ns <<= 1;
+  for (int x = tid; x < ns; x += kRankThreads) hist[x] = 0u;
 #pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) above += __shfl_xor(above, o, kWave);
-  if (lane == 0 && above) atomicAdd(&s_above, above);
-  __syncthreads();
-  const int off0 = s_above, cnt = s_count;
-  if (cnt > kRankCap) {  // this range does not fit: the whole unit goes to the exact path
-    if (tid == 0) set_status(a.ws.uovf + u, 1u);
-    return;
+  for (int o = 32; o >= 1; o >>= 1) {
+    const uint32_t m0 = __shfl_xor(kmin, o, kWave), m1 = __shfl_xor(kmax, o, kWave);
+    kmin = m0 < kmin ? m0 : kmin;
+    kmax = m1 > kmax ? m1 : kmax;
   }
-  if (off0 >= k || cnt == 0) return;
-  int P2 = 1;
-  while (P2 < cnt) P2 <<= 1;
-  for (int i = cnt + tid; i < P2; i += kRankThreads) buf[i] = 0ull;
+  if (lane == 0) {
+    s_red[0][wave] = kmin;
+    s_red[1][wave] = kmax;
+  }
   __syncthreads();
-  bitonic_desc(buf, P2 > 1 ? P2 : 2);
-  for (int x = tid; x < cnt && off0 + x < k; x += kRankThreads) {
-    const uint64_t c = buf[x];
-    idx[(int64_t)r * k + off0 + x] = (int32_t)(~(uint32_t)(c & 0xFFFFFFFFull));
-    if (val) val[(int64_t)r * k + off0 + x] = key_to_score((uint32_t)(c >> 32));
+  kmin = s_red[0][0];
+  kmax = s_red[1][0];
+#pragma unroll
+  for (int w = 1; w < kRankThreads / kWave; ++w) {
+    kmin = s_red[0][w] < kmin ? s_red[0][w] : kmin;
+    kmax = s_red[1][w] > kmax ? s_red[1][w] : kmax;
+  }
+  // sub-bucket: floor((kmax - key) * scale), non-decreasing as the key falls
+  const float scale = kmax > kmin ? (float)(ns - 1) / (float)(kmax - kmin) : 0.0f;
+  auto sub_of = [&](uint64_t v) {
+    const int sb = (int)__fmul_rn((float)(kmax - (uint32_t)(v >> 32)), scale);
+    return sb < ns - 1 ? sb : ns - 1;
+  };
+  for (int e = tid; e < c; e += kRankThreads) atomicAdd(&hist[sub_of(buf[e])], 1u);
+  __syncthreads();
+  // exclusive prefix over the sub-buckets (thread t owns a run of ns / 256, or one)
+  {
+    const int per = ns / kRankThreads > 0 ? ns / kRankThreads : 1;
+    const int x0 = tid * per;
+    uint32_t run = 0;
+    for (int x = 0; x < per; ++x)
+      if (x0 + x < ns) run += hist[x0 + x];
+    uint32_t inc = run;
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+      const uint32_t t = __shfl_up(inc, o, kWave);
+      if (lane >= o) inc += t;
+    }
+    if (lane == kWave - 1) s_part[wave] = inc;
+    __syncthreads();
+    uint32_t acc = inc - run;
+    for (int w = 0; w < wave; ++w) acc += s_part[w];
+    for (int x = 0; x < per; ++x)
+      if (x0 + x < ns) {
+        const uint32_t h0 = hist[x0 + x];
+        hist[x0 + x] = acc;
+        acc += h0;
+      }
+  }
+  __syncthreads();
+  for (int e = tid; e < c; e += kRankThreads) {  // group by sub-bucket; hist[s] ends at the group's end
+    const uint64_t v = buf[e];
+    grp[atomicAdd(&hist[sub_of(v)], 1u)] = v;
+  }
+  __syncthreads();
+  for (int j = tid; j < c; j += kRankThreads) {
+    const uint64_t v = grp[j];
+    const int sb = sub_of(v);
+    const uint32_t g0 = sb > 0 ? hist[sb - 1] : 0u, g1 = hist[sb];
+    uint32_t rank = g0;
+    for (uint32_t x = g0; x < g1; ++x) rank += grp[x] > v;
+    const uint32_t p = off0 + rank;
+    if (p < (uint32_t)k) {
+      idx[(int64_t)r * k + p] = (int32_t)(~(uint32_t)(v & 0xFFFFFFFFull));
+      if (val) val[(int64_t)r * k + p] = key_to_score((uint32_t)(v >> 32));
+    }
   }
 }
 
@@ -1279,7 +1330,7 @@ fathom_status launch_scan_topk_fused(const uint64_t* planes, const uint16_t* sca
     }
   }
   hipLaunchKernelGGL(fused_rank_kernel, dim3(kSlots, R), dim3(kRankThreads), 0, s, fa, idx, val);
-  hipLaunchKernelGGL(fused_select_kernel, dim3(1, R), dim3(kSelThreads), (size_t)kSelCap * 8, s, fa, idx, val);
+  hipLaunchKernelGGL(fused_select_kernel, dim3(R), dim3(kSelThreads), (size_t)kSelCap * 8, s, fa, idx, val);
   FATHOM_LAUNCH_CHECK();
   return FATHOM_OK;
 }
