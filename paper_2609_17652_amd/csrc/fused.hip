@@ -34,15 +34,18 @@
 // its four accumulators is >= 0.
 //
 // Candidates are queued per wave in LDS with their digits; full batches are
-// scored exactly (channels ascending, scales re-read through L2) and the keys
-// with score >= tau are appended to the row's survivor lists.
+// scored exactly (channels ascending, scales kept in an LDS ring) and the keys
+// with score >= tau are appended to one of 8 value buckets of their row.
 //
 // Passes: (1) sample: proxies of every s-th quad, the 8 largest per (wave,
-// head); (2) tau per row: the m-th largest sample, m ~ 1.25 k * sampled /
-// eligible + 16, plus range boundaries that split the survivors; (3) the full
-// pass above; (4) per row, the survivors are sorted and the first k written.
-// If fewer than k keys reach tau (or a list overflows), pass (4) recomputes
-// the row exactly (FATHOM_DEV_TOPK_FALLBACK).  The result never depends on tau.
+// head); (2) per row, tau = the m-th largest sample, m ~ 1.25 k * sampled /
+// eligible + 16, and 7 sample values that bound the value buckets; (3) the
+// full pass above; (4) one workgroup per (bucket, row) orders its bucket and
+// writes each survivor at (survivors of the buckets above) + (its rank in the
+// bucket), when that is below k.  If fewer than k keys reach tau (or a bucket
+// overflows), pass (4) recomputes the row exactly with a streaming top-k
+// (FATHOM_DEV_TOPK_FALLBACK).  The result never depends on tau or the bucket
+// bounds; they only decide how much work is saved.
 #include "common.hpp"
 
 namespace fathom {
