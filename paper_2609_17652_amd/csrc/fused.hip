@@ -70,6 +70,8 @@ constexpr int kThrMax = 1 << 18;   // |S| < 2^17 for A <= 128
 constexpr int kNoBound = 1 << 30;  // accumulator start: always (+) or never (-) a candidate
 constexpr int kMainWavesTarget = 2048;  // full-pass waves in flight over all units
 constexpr int kNarrow = 3;         // slices of the narrow full-pass instantiation (A <= 48)
+constexpr int kOneRows = 16;       // narrow: row groups at most (all staged in one 64-lane pass)
+constexpr int64_t kOneNbMax = (int64_t)1 << 20;  // narrow: byte offsets within a unit's planes fit 32 bits
 constexpr float kNegInf = -__builtin_huge_valf();
 
 struct FusedWs {
@@ -77,7 +79,7 @@ struct FusedWs {
   uint32_t* cnt;    // [R][kSlots] survivors appended to value bucket z
   uint64_t* cand;   // [R][kSlots][scap] survivors by bucket: score_key << 32 | ~index
   uint32_t* bnd;    // [R][kSlots] score keys splitting a row's survivors into kSlots value buckets
-  uint32_t* uovf;   // [U] from pass 2: (slices of the unit's filter) << 1, 0 = no filter; bit 0 unused
+  uint32_t* uovf;   // [U] from pass 2: (slices of the unit's filter, at least kNarrow + 1 for the wide pass) << 1, 0 = no filter
   float* samp;      // [R][kSmpRow] sampled proxies
   int cap, scap;    // rows with at most cap eligible keys are scored directly; bucket capacity
   int64_t s_stride; // sample every s_stride-th quad
@@ -337,7 +339,7 @@ __device__ void plan_setup(Plan& P, const FusedArgs& a, int u) {
 template <int NSLM, int SQB, int RQ, int QCAP>
 struct alignas(16) WaveLdsT {
   uint32_t st[16][kStP];                     // staged row groups of one slice, slot 4 (d mod 4) + p
-  uint32_t W[SQB * 4 * 4 * NSLM];            // int8 weights [block][head][dword] of the superquad
+  uint32_t W[SQB * 4 * 4 * NSLM];            // int8 weights [block][head][dword < 4 nsl] of the superquad
   int32_t ci[SQB][4][4];                     // [block][mu][head] accumulator start; sample: [b][0][h] bias, [b][1][h] ok
   uint16_t scl[RQ * SQB * 16 * NSLM];        // fp16 scales [ring slot][block][proxy channel]
   float amx[16 * NSLM];                      // per proxy channel: largest scale of the superquad
@@ -450,10 +452,10 @@ __device__ SqInfo scl_commit(const SclRegs<NCH, SQB>& r, const Plan& P, WL& W, i
 template <bool QF16, bool SAMPLE, int SQB, class WL>
 __device__ void superquad_weights(const Plan& P, WL& W, const FusedArgs& a, const SqInfo& si, int slot) {
   const int lane = threadIdx.x & 63, beta = lane & 15, h = lane >> 4;
-  const int ndw = uni(P.ndw), ap = 4 * ndw;
+  const int ndw = uni(P.ndw), ap = 4 * ndw, ws = 4 * uni(P.nsl);
   if (beta < SQB) {
     int bias = 0;
-    uint32_t* wdst = &W.W[(beta * 4 + h) * ndw];
+    uint32_t* wdst = &W.W[(beta * 4 + h) * ws];  // dwords ndw .. ws - 1 stay zero
     const uint16_t* srow = &W.scl[(slot * SQB + beta) * ap];
     if (si.valid) {
       if (QF16) {
@@ -484,6 +486,7 @@ __device__ void superquad_weights(const Plan& P, WL& W, const FusedArgs& a, cons
     } else {
       for (int d = 0; d < ndw; ++d) wdst[d] = 0u;
     }
+    for (int d = ndw; d < ws; ++d) wdst[d] = 0u;
     const bool hv = h < a.G && P.tau[h] != kNegInf;
     if (SAMPLE) {
       W.ci[beta][0][h] = bias;
@@ -567,6 +570,105 @@ __device__ __forceinline__ void task_stage(const uint64_t (&w)[4], const Plan& P
     }
   }
 }
+
+// Narrow full pass: every row group of the unit is staged in one pass, lane =
+// (row group g = lane >> 2, block beta = lane & 3).  The per-lane constants
+// are fixed for the whole unit.
+struct StageLane {
+  uint32_t boff[4];   // byte offset of row K for block beta from the quad's first plane word (pad rows: row 0)
+  uint32_t sel[4];    // first transpose stage (rows 0-1 lo/hi, rows 2-3 lo/hi); pad rows select zero bytes
+  uint32_t shl, shr;  // nibble shifts 3 - p and 1 + p
+  uint32_t* dst;      // &W.st[g][16 beta]
+  bool on;            // the lane's row group exists
+};
+
+template <class WL>
+__device__ __forceinline__ void stage_lane_setup(StageLane& L, const Plan& P, WL& W, const FusedArgs& a) {
+  const int lane = threadIdx.x & 63, g = lane >> 2, beta = lane & 3;
+  L.on = g < uni(P.slrg[kMaxSl]);
+  const int gg = L.on ? g : 0;
+  const uint32_t rr0 = P.rgrow[gg][0], rr1 = P.rgrow[gg][1];
+  const uint32_t rows[4] = {rr0 & 0xFFFFu, rr0 >> 16, rr1 & 0xFFFFu, rr1 >> 16};
+  // row 0 of a row group always exists (the dword's first channel is its deepest)
+#pragma unroll
+  for (int K = 0; K < 4; ++K) {
+    const uint32_t rk = rows[K] == kPadRow ? rows[0] : rows[K];
+    L.boff[K] = (rk * (uint32_t)a.nb_cap + (uint32_t)beta) * 8u;
+  }
+  // v_perm bytes: 0-3 from the second operand (rows 0, 2), 4-7 from the first
+  // (rows 1, 3); selector 0x0c yields a zero byte
+  uint32_t s01l = 0x05010400u, s01h = 0x07030602u, s23l = 0x05010400u, s23h = 0x07030602u;
+  if (rows[1] == kPadRow) {
+    s01l = (s01l & 0x00FF00FFu) | 0x0C000C00u;
+    s01h = (s01h & 0x00FF00FFu) | 0x0C000C00u;
+  }
+  if (rows[2] == kPadRow) {
+    s23l = (s23l & 0xFF00FF00u) | 0x000C000Cu;
+    s23h = (s23h & 0xFF00FF00u) | 0x000C000Cu;
+  }
+  if (rows[3] == kPadRow) {
+    s23l = (s23l & 0x00FF00FFu) | 0x0C000C00u;
+    s23h = (s23h & 0x00FF00FFu) | 0x0C000C00u;
+  }
+  L.sel[0] = s01l;
+  L.sel[1] = s01h;
+  L.sel[2] = s23l;
+  L.sel[3] = s23h;
+  const int p = P.rgp[gg];
+  L.shl = (uint32_t)(3 - p);
+  L.shr = (uint32_t)(1 + p);
+  L.dst = &W.st[gg][16 * beta];
+}
+
+// Plane words of the lane's row group for the quad whose first plane word of
+// row 0 is at qaddr, through a buffer descriptor covering the rest of the
+// unit's planes (`bytes`): loads past it (blocks beyond the store in the last
+// row) return zero, and every other load stays inside the unit.  Lanes without
+// a row group load row group 0's words (staged nowhere).
+typedef unsigned int v2u32 __attribute__((ext_vector_type(2)));
+constexpr int kRawBufferFlags = 0x00020000;  // raw buffer, 32-bit data format
+__device__ __forceinline__ void stage_one_issue(uint64_t (&w)[4], const StageLane& L, uint64_t qaddr, uint32_t bytes) {
+  const uint32_t alo = (uint32_t)uni((int)(uint32_t)qaddr), ahi = (uint32_t)uni((int)(uint32_t)(qaddr >> 32));
+  const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+      reinterpret_cast<void*>(((uint64_t)ahi << 32) | alo), (short)0, (int)(uint32_t)uni((int)bytes), kRawBufferFlags);
+#pragma unroll
+  for (int K = 0; K < 4; ++K) {
+    const v2u32 v = __builtin_amdgcn_raw_buffer_load_b64(rs, (int)L.boff[K], 0, 0);
+    w[K] = ((uint64_t)v.y << 32) | v.x;
+  }
+}
+
+// Byte transpose and nibble copies of the lane's row group (as task_stage).
+__device__ __forceinline__ void stage_one(const uint64_t (&w)[4], const StageLane& L) {
+  if (L.on) {
+    uint32_t* dst = L.dst;
+#pragma unroll
+    for (int hw = 0; hw < 2; ++hw) {
+      const uint32_t a0 = (uint32_t)(w[0] >> (32 * hw)), a1 = (uint32_t)(w[1] >> (32 * hw));
+      const uint32_t a2 = (uint32_t)(w[2] >> (32 * hw)), a3 = (uint32_t)(w[3] >> (32 * hw));
+      const uint32_t t01l = __builtin_amdgcn_perm(a1, a0, L.sel[0]);
+      const uint32_t t01h = __builtin_amdgcn_perm(a1, a0, L.sel[1]);
+      const uint32_t t23l = __builtin_amdgcn_perm(a3, a2, L.sel[2]);
+      const uint32_t t23h = __builtin_amdgcn_perm(a3, a2, L.sel[3]);
+      uint32_t T[4];
+      T[0] = __builtin_amdgcn_perm(t23l, t01l, 0x05040100u);
+      T[1] = __builtin_amdgcn_perm(t23l, t01l, 0x07060302u);
+      T[2] = __builtin_amdgcn_perm(t23h, t01h, 0x05040100u);
+      T[3] = __builtin_amdgcn_perm(t23h, t01h, 0x07060302u);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int m = 4 * hw + j;
+        dst[2 * m] = T[j] << L.shl;
+        dst[2 * m + 1] = T[j] >> L.shr;
+      }
+    }
+  }
+}
+
+// Orders LDS accesses in the compiler only: a wave's LDS instructions are
+// executed in program order, so a wave reading rows it staged itself (or
+// restaging rows it has read) needs no wait.
+__device__ __forceinline__ void lds_program_order() { asm volatile("" ::: "memory"); }
 
 // Exact documented scores of the queued keys (lane e < nq), from their queued
 // digits and the scales kept in the ring, and their appends to the survivor
@@ -666,10 +768,27 @@ __device__ void wave_run(const Plan& P, WaveLdsT<NSLM, SQB, RQ, QCAP>& W, const 
   int pending = 0, oldest = 0;
   SclRegs<NCH, SQB> sr;
   scl_issue(sr, P, a, u, b0);
-  uint64_t ring[NSLM][4];
+  // kOne: all row groups staged in one pass (narrow full pass); otherwise one
+  // staging pass per slice
+  constexpr bool kOne = !SAMPLE && NSLM <= kNarrow;
+  uint64_t ring[kOne ? 1 : NSLM][4];
+  StageLane L;
+  int g0s[NSLM], smk[NSLM];
+  const uint64_t ubase = reinterpret_cast<uint64_t>(a.planes + (int64_t)u * kD * kPlanes * a.nb_cap);
+  const uint32_t ubytes = (uint32_t)(kD * kPlanes * 8) * (uint32_t)a.nb_cap;  // kOne: nb_cap < kOneNbMax
+  if constexpr (kOne) {
+    stage_lane_setup(L, P, W, a);
 #pragma unroll
-  for (int sl = 0; sl < NSLM; ++sl)
-    if (sl < nsl) task_issue(ring[sl], P, a, u, b0, sl);
+    for (int sl = 0; sl < NSLM; ++sl) {
+      g0s[sl] = uni(P.slrg[sl]);
+      smk[sl] = uni(P.slmask[sl]);
+    }
+    stage_one_issue(ring[0], L, ubase + (uint64_t)b0 * 8u, ubytes - (uint32_t)b0 * 8u);
+  } else {
+#pragma unroll
+    for (int sl = 0; sl < NSLM; ++sl)
+      if (sl < nsl) task_issue(ring[sl], P, a, u, b0, sl);
+  }
   int sqi = 0;
   for (int64_t sb0 = b0; sb0 < b1; sb0 += SQB, ++sqi) {
     const int rslot = sqi % RQ;
@@ -695,14 +814,22 @@ __device__ void wave_run(const Plan& P, WaveLdsT<NSLM, SQB, RQ, QCAP>& W, const 
         if (SAMPLE) acc[mu] = v4i{0, 0, 0, 0};
         else acc[mu] = *reinterpret_cast<const v4i*>(&W.ci[qo + lb][mu][0]);
       }
+      if constexpr (kOne) {
+        stage_one(ring[0], L);
+        if (more) stage_one_issue(ring[0], L, ubase + (uint64_t)(qb0 + kQB) * 8u, ubytes - (uint32_t)(qb0 + kQB) * 8u);
+        lds_program_order();
+      }
 #pragma unroll
       for (int sl = 0; sl < NSLM; ++sl) {
         if (sl < nsl) {
-          task_stage(ring[sl], P, W, sl);
-          if (more) task_issue(ring[sl], P, a, u, qb0 + kQB, sl);
-          wave_lds_sync();
+          if constexpr (!kOne) {
+            task_stage(ring[sl], P, W, sl);
+            if (more) task_issue(ring[sl], P, a, u, qb0 + kQB, sl);
+            wave_lds_sync();
+          }
           uint32_t Z[4][4];
-          const int smask = uni(P.slmask[sl]);
+          const int smask = kOne ? smk[sl] : uni(P.slmask[sl]);
+          int g = kOne ? g0s[sl] : 0;  // kOne: staged row of the next present (dword, plane)
 #pragma unroll
           for (int dd = 0; dd < 4; ++dd) {
 #pragma unroll
@@ -710,7 +837,8 @@ __device__ void wave_run(const Plan& P, WaveLdsT<NSLM, SQB, RQ, QCAP>& W, const 
 #pragma unroll
             for (int p = 0; p < 4; ++p) {
               if (smask & (1 << (4 * dd + p))) {
-                const uint32_t x = W.st[4 * dd + p][lane];
+                const uint32_t x = kOne ? W.st[g][lane] : W.st[4 * dd + p][lane];
+                ++g;
 #pragma unroll
                 for (int mu = 0; mu < 4; ++mu) Z[mu][dd] |= x & (0x01010101u << (mu + 3 - p));
               }
@@ -719,16 +847,13 @@ __device__ void wave_run(const Plan& P, WaveLdsT<NSLM, SQB, RQ, QCAP>& W, const 
 #pragma unroll
           for (int mu = 0; mu < 4; ++mu) dig[mu][sl] = v4i{(int)Z[mu][0], (int)Z[mu][1], (int)Z[mu][2], (int)Z[mu][3]};
           v4i wv = v4i{0, 0, 0, 0};
-          if (wl) {
-            const uint32_t* wp = &W.W[((qo + lb) * 4 + wh) * ndw + 4 * sl];
-            wv = v4i{(int)wp[0], (int)(4 * sl + 1 < ndw ? wp[1] : 0u), (int)(4 * sl + 2 < ndw ? wp[2] : 0u),
-                     (int)(4 * sl + 3 < ndw ? wp[3] : 0u)};
-          }
+          if (wl) wv = *reinterpret_cast<const v4i*>(&W.W[((qo + lb) * 4 + wh) * stride + 4 * sl]);
 #pragma unroll
           for (int mu = 0; mu < 4; ++mu) acc[mu] = __builtin_amdgcn_mfma_i32_16x16x64_i8(wv, dig[mu][sl], acc[mu], 0, 0, 0);
-          wave_lds_sync();  // staged reads done before the next slice is staged
+          if constexpr (!kOne) wave_lds_sync();  // staged reads done before the next slice is staged
         }
       }
+      if constexpr (kOne) lds_program_order();
       const int64_t kbase = (qb0 + lb) * kBlockTokens + kb;  // key of mu = 0
       const bool inner = qb0 * kBlockTokens >= lo && (qb0 + kQB) * kBlockTokens <= hi && qb0 + kQB <= nbu;
       if (SAMPLE) {
@@ -860,8 +985,7 @@ __global__ __launch_bounds__(kFT) void fused_sample_kernel(FusedArgs a) {
 constexpr int kTauThreads = kSlots * kWave;
 constexpr int kTauPer = kSmpRow / kWave;  // sampled values per lane
 __global__ __launch_bounds__(kTauThreads) void fused_tau_kernel(FusedArgs a) {
-  __shared__ int sA;
-  __shared__ int64_t sm;
+  __shared__ int sc[kPlanes + 1];  // active channels by depth
   const int r = blockIdx.x, G = a.G, u = r / G, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   if (tid < kSlots) {
     a.ws.cnt[r * kSlots + tid] = 0u;
@@ -869,13 +993,27 @@ __global__ __launch_bounds__(kTauThreads) void fused_tau_kernel(FusedArgs a) {
   }
   int64_t nu, lo, hi;
   row_window(a, u, &nu, &lo, &hi, false);
-  if (tid == 0) sA = 0;
+  if (tid <= kPlanes) sc[tid] = 0;
   __syncthreads();
-  if (tid < kD && gload(a.depths + (int64_t)u * kD + tid) > 0) atomicAdd(&sA, 1);
+  if (tid < kD) {
+    const int t = gload(a.depths + (int64_t)u * kD + tid);
+    if (t > 0) atomicAdd(&sc[t > kPlanes ? kPlanes : t], 1);
+  }
   __syncthreads();
-  const int A = sA;
+  const int A = sc[1] + sc[2] + sc[3] + sc[4];
   const bool ok = G <= 4 && A > 0 && hi - lo > a.ws.cap;
-  if (tid == 0 && r % G == 0) a.ws.uovf[u] = ok ? (uint32_t)((A + 15) >> 4) << 1 : 0u;
+  if (tid == 0 && r % G == 0) {
+    uint32_t cls = 0u;
+    if (ok) {
+      cls = (uint32_t)((A + 15) >> 4);
+      // row groups: the depth of each dword's first channel in the proxy order
+      // (depth descending); the narrow pass stages at most kOneRows of them
+      int rows = 0;
+      for (int x = 0; x < A; x += 4) rows += x < sc[4] ? 4 : x < sc[4] + sc[3] ? 3 : x < sc[4] + sc[3] + sc[2] ? 2 : 1;
+      if (cls <= (uint32_t)kNarrow && (rows > kOneRows || a.nb_cap >= kOneNbMax)) cls = kNarrow + 1;
+    }
+    a.ws.uovf[u] = cls << 1;
+  }
   if (!ok) {
     if (tid == 0) a.ws.tau[r] = kNegInf;
     return;
@@ -957,6 +1095,7 @@ __global__ __launch_bounds__(kFT) void fused_main_kernel(FusedArgs a) {
   }
   __syncthreads();
   if (!P.ok || P.A == 0 || P.nsl > NSLM) return;
+  if (NSLM <= kNarrow && (P.slrg[kMaxSl] > kOneRows || a.nb_cap >= kOneNbMax)) return;  // the wide pass's units
   bool any = false;
   for (int h = 0; h < a.G; ++h) any |= P.tau[h] != kNegInf;
   if (!any) return;
