@@ -206,6 +206,7 @@ struct alignas(16) Plan {
   int rgp[kMaxRg];             // row group g: plane p
   int rgslot[kMaxRg];          // row group g: staging slot 4 * (d mod 4) + p within its slice
   int slmask[kMaxSl];          // slice s: bit 4 dd + p set iff dword 4s + dd has plane p
+  int slshp[kMaxSl];           // slice s: bits 4p..4p+3 = c_p, the dwords with plane p (a prefix dd < c_p)
   float tau[4];
   uint32_t bnd[4][kSlots];     // head h: score keys splitting its survivors into value buckets
 };
@@ -299,11 +300,16 @@ __device__ void plan_setup(Plan& P, const FusedArgs& a, int u) {
       int g = 0;
       for (int s = 0; s < kMaxSl; ++s) {
         P.slrg[s] = g;
-        int msk = 0;
-        for (int dd = 0; dd < 4; ++dd) {
-          const int d = 4 * s + dd;
-          const int nr = d < ndw ? (P.act[4 * d] >> 8) : 0;
-          for (int p = 0; p < nr; ++p) {
+        int msk = 0, shp = 0;
+        // plane-major: depths never increase along the proxy order, so the
+        // dwords with plane p are dd < c_p
+        for (int p = 0; p < kPlanes; ++p) {
+          int c = 0;
+          for (int dd = 0; dd < 4; ++dd) {
+            const int d = 4 * s + dd;
+            const int nr = d < ndw ? (P.act[4 * d] >> 8) : 0;
+            if (nr <= p) continue;
+            ++c;
             msk |= 1 << (4 * dd + p);
             P.rgslot[g] = 4 * dd + p;
             uint32_t h2[2] = {0u, 0u};
@@ -319,8 +325,10 @@ __device__ void plan_setup(Plan& P, const FusedArgs& a, int u) {
             P.rgp[g] = p;
             ++g;
           }
+          shp |= c << (4 * p);
         }
         P.slmask[s] = msk;
+        P.slshp[s] = shp;
       }
       P.slrg[kMaxSl] = g;
       double zs = 0.0;
@@ -336,9 +344,12 @@ __device__ void plan_setup(Plan& P, const FusedArgs& a, int u) {
 // NSLM slices (16 NSLM proxy channels at most), superquads of SQB blocks, RQ
 // superquads of scales kept for re-scoring, QCAP queued candidates (0: the
 // sample pass, no queue).
+// Staged rows: one slice's 16 slots, or (narrow pass) every row group of the
+// unit plus 3 rows that plane segments may read past the last one.
+constexpr int st_rows(int nslm) { return nslm <= kNarrow ? kOneRows + 3 : 16; }
 template <int NSLM, int SQB, int RQ, int QCAP>
 struct alignas(16) WaveLdsT {
-  uint32_t st[16][kStP];                     // staged row groups of one slice, slot 4 (d mod 4) + p
+  uint32_t st[st_rows(NSLM)][kStP];          // staged row groups (per-slice slot 4 (d mod 4) + p, or row group g)
   uint32_t W[SQB * 4 * 4 * NSLM];            // int8 weights [block][head][dword < 4 nsl] of the superquad
   int32_t ci[SQB][4][4];                     // [block][mu][head] accumulator start; sample: [b][0][h] bias, [b][1][h] ok
   uint16_t scl[RQ * SQB * 16 * NSLM];        // fp16 scales [ring slot][block][proxy channel]
@@ -670,6 +681,20 @@ __device__ __forceinline__ void stage_one(const uint64_t (&w)[4], const StageLan
 // restaging rows it has read) needs no wait.
 __device__ __forceinline__ void lds_program_order() { asm volatile("" ::: "memory"); }
 
+// A uniform value kept in a VGPR (opaque to the compiler) and read back per
+// use: loop-invariant uniforms otherwise stay live in SGPRs across the whole
+// loop, and this kernel has none to spare.
+__device__ __forceinline__ uint32_t to_vgpr(uint32_t x) {
+  uint32_t v;
+  asm volatile("v_mov_b32 %0, %1" : "=v"(v) : "v"(x));
+  return v;
+}
+__device__ __forceinline__ int from_vgpr(uint32_t v) {
+  int x;
+  asm volatile("v_readfirstlane_b32 %0, %1" : "=s"(x) : "v"(v));
+  return x;
+}
+
 // Exact documented scores of the queued keys (lane e < nq), from their queued
 // digits and the scales kept in the ring, and their appends to the survivor
 // lists.
@@ -773,15 +798,16 @@ __device__ void wave_run(const Plan& P, WaveLdsT<NSLM, SQB, RQ, QCAP>& W, const 
   constexpr bool kOne = !SAMPLE && NSLM <= kNarrow;
   uint64_t ring[kOne ? 1 : NSLM][4];
   StageLane L;
-  int g0s[NSLM], smk[NSLM];
+  uint32_t shpv[NSLM];          // kOne: slice shapes (c_p fields), kept in VGPRs
+  const uint32_t* rb0[NSLM];     // kOne: first staged row of each slice, this lane's column
   const uint64_t ubase = reinterpret_cast<uint64_t>(a.planes + (int64_t)u * kD * kPlanes * a.nb_cap);
   const uint32_t ubytes = (uint32_t)(kD * kPlanes * 8) * (uint32_t)a.nb_cap;  // kOne: nb_cap < kOneNbMax
   if constexpr (kOne) {
     stage_lane_setup(L, P, W, a);
 #pragma unroll
     for (int sl = 0; sl < NSLM; ++sl) {
-      g0s[sl] = uni(P.slrg[sl]);
-      smk[sl] = uni(P.slmask[sl]);
+      shpv[sl] = to_vgpr((uint32_t)P.slshp[sl]);
+      rb0[sl] = &W.st[uni(P.slrg[sl])][lane];
     }
     stage_one_issue(ring[0], L, ubase + (uint64_t)b0 * 8u, ubytes - (uint32_t)b0 * 8u);
   } else {
@@ -828,19 +854,41 @@ __device__ void wave_run(const Plan& P, WaveLdsT<NSLM, SQB, RQ, QCAP>& W, const 
             wave_lds_sync();
           }
           uint32_t Z[4][4];
-          const int smask = kOne ? smk[sl] : uni(P.slmask[sl]);
-          int g = kOne ? g0s[sl] : 0;  // kOne: staged row of the next present (dword, plane)
 #pragma unroll
-          for (int dd = 0; dd < 4; ++dd) {
+          for (int dd = 0; dd < 4; ++dd)
 #pragma unroll
             for (int mu = 0; mu < 4; ++mu) Z[mu][dd] = 0u;
+          if constexpr (kOne) {
+            // plane segments: rows of plane p are the next c_p staged rows (dd < c_p);
+            // all 4 candidate rows of a segment are read together
+            const int cs = from_vgpr(shpv[sl]);
+            const uint32_t* rb = rb0[sl];
 #pragma unroll
             for (int p = 0; p < 4; ++p) {
-              if (smask & (1 << (4 * dd + p))) {
-                const uint32_t x = kOne ? W.st[g][lane] : W.st[4 * dd + p][lane];
-                ++g;
+              const int c = (cs >> (4 * p)) & 15;
+              if (c == 0) break;
+              uint32_t x[4];
 #pragma unroll
-                for (int mu = 0; mu < 4; ++mu) Z[mu][dd] |= x & (0x01010101u << (mu + 3 - p));
+              for (int dd = 0; dd < 4; ++dd) x[dd] = rb[dd * kStP];
+#pragma unroll
+              for (int dd = 1; dd < 4; ++dd) x[dd] = dd < c ? x[dd] : 0u;  // rows past the segment
+#pragma unroll
+              for (int dd = 0; dd < 4; ++dd)
+#pragma unroll
+                for (int mu = 0; mu < 4; ++mu) Z[mu][dd] |= x[dd] & (0x01010101u << (mu + 3 - p));
+              rb += c * kStP;
+            }
+          } else {
+            const int smask = uni(P.slmask[sl]);
+#pragma unroll
+            for (int dd = 0; dd < 4; ++dd) {
+#pragma unroll
+              for (int p = 0; p < 4; ++p) {
+                if (smask & (1 << (4 * dd + p))) {
+                  const uint32_t x = W.st[4 * dd + p][lane];
+#pragma unroll
+                  for (int mu = 0; mu < 4; ++mu) Z[mu][dd] |= x & (0x01010101u << (mu + 3 - p));
+                }
               }
             }
           }
