@@ -295,46 +295,62 @@ __device__ void plan_setup(Plan& P, const FusedArgs& a, int u) {
     for (int K = 0; K < 4; ++K) w |= (uint32_t)(4 * tid + K < A ? P.pord[4 * tid + K] : 0) << (8 * K);
     P.pordb[tid] = w;
   }
-  if (wave == 0) {  // row groups, slice by slice
-    if (lane == 0) {
-      int g = 0;
-      for (int s = 0; s < kMaxSl; ++s) {
-        P.slrg[s] = g;
-        int msk = 0, shp = 0;
-        // plane-major: depths never increase along the proxy order, so the
-        // dwords with plane p are dd < c_p
-        for (int p = 0; p < kPlanes; ++p) {
-          int c = 0;
-          for (int dd = 0; dd < 4; ++dd) {
-            const int d = 4 * s + dd;
-            const int nr = d < ndw ? (P.act[4 * d] >> 8) : 0;
-            if (nr <= p) continue;
-            ++c;
-            msk |= 1 << (4 * dd + p);
-            P.rgslot[g] = 4 * dd + p;
-            uint32_t h2[2] = {0u, 0u};
+  // row groups, in parallel.  Depths never increase along the proxy order, so
+  // within slice s the dwords with plane p are dd < c_p (plane-major order):
+  // row group (d = 4 s + dd, p) has index slrg[s] + c_0 + .. + c_(p-1) + dd.
+  __shared__ int snr[kMaxDw], scp[kMaxSl][kPlanes], srows[kMaxSl];
+  if (tid < kMaxDw) snr[tid] = tid < ndw ? (P.act[4 * tid] >> 8) : 0;  // planes of dword tid
+  int zpart = 0;  // sum of zmax over the active channels (wave 0)
+  if (wave == 0) {
+    zpart = (lane < A ? (int)(P.zm16[lane] * 16.0f) : 0) + (lane + kWave < A ? (int)(P.zm16[lane + kWave] * 16.0f) : 0);
+    zpart = wave_sum_int(zpart);
+  }
+  __syncthreads();
+  if (tid < kMaxSl * kPlanes) {  // c_p of slice tid / 4
+    const int sl = tid >> 2, p = tid & 3;
+    int c = 0;
 #pragma unroll
-            for (int K = 0; K < 4; ++K) {
-              const int x = 4 * d + K;
-              uint32_t r = kPadRow;
-              if (x < A && (P.act[x] >> 8) > p) r = (uint32_t)(4 * (P.act[x] & 0xFF) + p);
-              h2[K >> 1] |= r << (16 * (K & 1));
-            }
-            P.rgrow[g][0] = h2[0];
-            P.rgrow[g][1] = h2[1];
-            P.rgp[g] = p;
-            ++g;
-          }
-          shp |= c << (4 * p);
-        }
-        P.slmask[s] = msk;
-        P.slshp[s] = shp;
+    for (int dd = 0; dd < 4; ++dd) c += snr[4 * sl + dd] > p;
+    scp[sl][p] = c;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    int g = 0;
+    for (int sl = 0; sl < kMaxSl; ++sl) {
+      P.slrg[sl] = g;
+      srows[sl] = g;
+      int shp = 0, msk = 0;
+      for (int p = 0; p < kPlanes; ++p) {
+        shp |= scp[sl][p] << (4 * p);
+        g += scp[sl][p];
       }
-      P.slrg[kMaxSl] = g;
-      double zs = 0.0;
-      for (int x = 0; x < A; ++x) zs += (double)P.zm16[x] * 16.0;
-      P.Ku = (zs / 32.0 + (double)A * (double)A * 127.0 * 0x1p-24) * (1.0 + 0x1p-20);
-      P.Eabs = (double)A * 0x1p-120;
+      for (int dd = 0; dd < 4; ++dd) msk |= ((1 << snr[4 * sl + dd]) - 1) << (4 * dd);
+      P.slshp[sl] = shp;
+      P.slmask[sl] = msk;
+    }
+    P.slrg[kMaxSl] = g;
+    const double zs = (double)zpart;
+    P.Ku = (zs / 32.0 + (double)A * (double)A * 127.0 * 0x1p-24) * (1.0 + 0x1p-20);
+    P.Eabs = (double)A * 0x1p-120;
+  }
+  __syncthreads();
+  if (tid < kMaxDw * kPlanes) {  // row group (dword d, plane p)
+    const int d = tid >> 2, p = tid & 3, sl = d >> 2, dd = d & 3;
+    if (snr[d] > p) {
+      int g = srows[sl] + dd;
+      for (int p2 = 0; p2 < p; ++p2) g += scp[sl][p2];
+      P.rgslot[g] = 4 * dd + p;
+      uint32_t h2[2] = {0u, 0u};
+#pragma unroll
+      for (int K = 0; K < 4; ++K) {
+        const int x = 4 * d + K;
+        uint32_t r = kPadRow;
+        if (x < A && (P.act[x] >> 8) > p) r = (uint32_t)(4 * (P.act[x] & 0xFF) + p);
+        h2[K >> 1] |= r << (16 * (K & 1));
+      }
+      P.rgrow[g][0] = h2[0];
+      P.rgrow[g][1] = h2[1];
+      P.rgp[g] = p;
     }
   }
   __syncthreads();
