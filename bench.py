@@ -98,6 +98,8 @@ def main():
     cfg = synth.WORKLOADS["layer1m"]
     mode = {"waterfill": F.FATHOM_WATERFILL, "r16": F.FATHOM_UNIFORM_TOPR, "r32": F.FATHOM_UNIFORM_TOPR}[args.mode]
     B = {"waterfill": args.budget, "r16": 16, "r32": 32}[args.mode]
+    # depth bits per unit at most: the budget (water-filling), or 4 planes x r channels
+    max_bits = B if args.mode == "waterfill" else 4 * B
     k = cfg.k
     log(f"[bench] generating inputs: 8 KV heads x n=2^20, G=4, mode={args.mode} B/r={B}, k={k}")
     data = synth.device_units(cfg, with_values=True)
@@ -139,7 +141,7 @@ def main():
         if evs is not None:
             evs[0].record(stream)
         F.fathom_alloc_depths(q, var, mode, B, d, theta, st)
-        F.fathom_scan_topk(planes[c], scales[c], n, q, d, k, 0, 0, idx, val, ws, st)
+        F.fathom_scan_topk(planes[c], scales[c], n, q, d, k, 0, 0, idx, val, ws, st, max_unit_bits=max_bits)
         if evs is not None:
             evs[1].record(stream)
         F.fathom_sparse_attn(q, K16, V, n, idx, 0, 0, None, out, st)
@@ -167,7 +169,7 @@ def main():
     tev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
     for r in range(reps):
         tev[r][0].record(stream)
-        F.fathom_scan_topk(planes[r % R], scales[r % R], n, q, d, k, 0, 0, idx, val, ws, st)
+        F.fathom_scan_topk(planes[r % R], scales[r % R], n, q, d, k, 0, 0, idx, val, ws, st, max_unit_bits=max_bits)
         tev[r][1].record(stream)
     torch.cuda.synchronize()
     st_ms = float(np.mean([a.elapsed_time(b) for a, b in tev]))

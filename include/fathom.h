@@ -166,6 +166,22 @@ fathom_status fathom_scan_topk(const uint64_t* planes, const uint16_t* scales, c
 size_t fathom_scan_topk_workspace_size(int U, int G, int64_t max_n, int k);
 
 /*
+ * fathom_scan_topk_ex -- fathom_scan_topk with a caller's bound on the depth
+ * bits of every unit, max_unit_bits >= sum_j min(depths[u][j], 4) for all u
+ * (0: no bound).  The outputs are those of fathom_scan_topk for any bound;
+ * the bound only selects work: with max_unit_bits <= 48 the filter pass for
+ * units of more channels or row groups is not launched, so a unit that
+ * exceeds a wrong bound is recomputed by the exact path (TOPK_FALLBACK).
+ * Water-filling at budget B (Sec. 3.3) gives every unit at most B bits.
+ * Errors: as fathom_scan_topk; max_unit_bits < 0 is FATHOM_ERR_INVALID.
+ */
+fathom_status fathom_scan_topk_ex(const uint64_t* planes, const uint16_t* scales, const int64_t* n,
+                                  int U, int D, int64_t nb_cap, const void* q, fathom_dtype qdt,
+                                  int G, const uint8_t* depths, int k, int64_t lo, int64_t tail,
+                                  int max_unit_bits, int32_t* idx, float* val, void* ws,
+                                  size_t ws_bytes, uint32_t* dev_status, void* stream);
+
+/*
  * fathom_sparse_attn -- Sec. 2 (top-k decoding) and Sec. 4 (fidelity metric):
  * exact attention of each query head over its selected set
  *   S_h = sink [0, ns) U local [l0, n) U {idx[u][h][r] in [ns, l0)},

@@ -37,7 +37,7 @@ FATHOM_DEV_BAD_N = 16
 
 EXPORTED = (
     "fathom_pack", "fathom_alloc_depths", "fathom_scan", "fathom_topk", "fathom_topk_workspace_size",
-    "fathom_scan_topk", "fathom_scan_topk_workspace_size", "fathom_sparse_attn",
+    "fathom_scan_topk", "fathom_scan_topk_ex", "fathom_scan_topk_workspace_size", "fathom_sparse_attn",
     "fathom_sparse_attn_workspace_size", "fathom_status_string", "fathom_version",
 )
 
@@ -67,6 +67,8 @@ def lib() -> C.CDLL:
             "fathom_scan": [P, P, P, i32, i32, i64, P, i32, i32, P, P, i64, P, P],
             "fathom_topk": [P, i64, P, i32, i32, i32, i64, i64, P, P, P, C.c_size_t, P, P],
             "fathom_scan_topk": [P, P, P, i32, i32, i64, P, i32, i32, P, i32, i64, i64, P, P, P, C.c_size_t, P, P],
+            "fathom_scan_topk_ex": [P, P, P, i32, i32, i64, P, i32, i32, P, i32, i64, i64, i32, P, P, P, C.c_size_t, P,
+                                    P],
             "fathom_sparse_attn": [P, i32, P, P, i64, i64, P, i32, i32, i32, P, i32, i32, i32, C.c_float, P, P,
                                    C.c_size_t, P, P],
         }
@@ -206,8 +208,9 @@ def fathom_topk(scores, n, k, lo=0, tail=0, idx=None, val=None, ws=None, dev_sta
 
 
 def fathom_scan_topk(planes, scales, n, q, depths, k, lo=0, tail=0, idx=None, val=None, ws=None, dev_status=None,
-                     stream=None):
-    """fathom_scan + fathom_topk in one call (no score array output)."""
+                     stream=None, max_unit_bits=0):
+    """fathom_scan + fathom_topk in one call (no score array output).  max_unit_bits: the caller's
+    bound on every unit's depth bits (0: none); it selects work only, never the result."""
     _dev(planes, scales, n, q, depths)
     U, D, _, nb_cap = planes.shape
     G = q.shape[1]
@@ -216,9 +219,10 @@ def fathom_scan_topk(planes, scales, n, q, depths, k, lo=0, tail=0, idx=None, va
     if val is None:
         val = torch.empty((U, G, k), dtype=torch.float32, device=q.device)
     ws = _ws(fathom_scan_topk_workspace_size(U, G, 64 * nb_cap, k), ws, q.device)
-    _check(lib().fathom_scan_topk(_p(planes), _p(scales), _p(n), U, D, nb_cap, _p(q), _dt(q), G, _p(depths), int(k),
-                                  int(lo), int(tail), _p(idx), _p(val), _p(ws), ws.numel() * ws.element_size(),
-                                  _p(dev_status), _stream(stream)), "fathom_scan_topk")
+    _check(lib().fathom_scan_topk_ex(_p(planes), _p(scales), _p(n), U, D, nb_cap, _p(q), _dt(q), G, _p(depths),
+                                     int(k), int(lo), int(tail), int(max_unit_bits), _p(idx), _p(val), _p(ws),
+                                     ws.numel() * ws.element_size(), _p(dev_status), _stream(stream)),
+           "fathom_scan_topk")
     return idx, val
 
 

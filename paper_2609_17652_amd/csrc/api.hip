@@ -18,8 +18,8 @@ size_t attn_ws_bytes(int U, int G, int k, int n_sink, int n_local);
 size_t topk_ws_bytes(int R, int64_t max_n, int k);
 size_t fused_ws_bytes(int R, int U, int64_t nb_cap, int k);
 fathom_status launch_scan_topk_fused(const uint64_t*, const uint16_t*, const int64_t*, int, int64_t, const void*,
-                                     fathom_dtype, int, const uint8_t*, int, int64_t, int64_t, int32_t*, float*, void*,
-                                     uint32_t*, hipStream_t);
+                                     fathom_dtype, int, const uint8_t*, int, int64_t, int64_t, int, int32_t*, float*,
+                                     void*, uint32_t*, hipStream_t);
 int attn_max_sink_local();
 }  // namespace fathom
 
@@ -137,19 +137,27 @@ size_t fathom_scan_topk_workspace_size(int U, int G, int64_t max_n, int k) {
   return scan_topk_ws(U, G, max_n, k);
 }
 
-fathom_status fathom_scan_topk(const uint64_t* planes, const uint16_t* scales, const int64_t* n, int U, int D,
-                               int64_t nb_cap, const void* q, fathom_dtype qdt, int G, const uint8_t* depths, int k,
-                               int64_t lo, int64_t tail, int32_t* idx, float* val, void* ws, size_t ws_bytes,
-                               uint32_t* dev_status, void* stream) {
+fathom_status fathom_scan_topk_ex(const uint64_t* planes, const uint16_t* scales, const int64_t* n, int U, int D,
+                                  int64_t nb_cap, const void* q, fathom_dtype qdt, int G, const uint8_t* depths, int k,
+                                  int64_t lo, int64_t tail, int max_unit_bits, int32_t* idx, float* val, void* ws,
+                                  size_t ws_bytes, uint32_t* dev_status, void* stream) {
   fathom_status e = check_store(planes, scales, n, U, D, nb_cap, q, qdt, G, depths);
   if (e != FATHOM_OK) return e;
-  if (lo < 0 || tail < 0 || k < 1) return FATHOM_ERR_INVALID;
+  if (lo < 0 || tail < 0 || k < 1 || max_unit_bits < 0) return FATHOM_ERR_INVALID;
   if (k > FATHOM_MAX_K) return FATHOM_ERR_UNSUPPORTED;
   if (U == 0) return FATHOM_OK;
   if (!idx || !ws || !aligned(idx, 4) || (val && !aligned(val, 4)) || !aligned(ws, 256)) return FATHOM_ERR_INVALID;
   if (ws_bytes < scan_topk_ws(U, G, nb_cap * 64, k)) return FATHOM_ERR_WORKSPACE;
-  return launch_scan_topk_fused(planes, scales, n, U, nb_cap, q, qdt, G, depths, k, lo, tail, idx, val, ws,
-                                dev_status, as_stream(stream));
+  return launch_scan_topk_fused(planes, scales, n, U, nb_cap, q, qdt, G, depths, k, lo, tail, max_unit_bits, idx, val,
+                                ws, dev_status, as_stream(stream));
+}
+
+fathom_status fathom_scan_topk(const uint64_t* planes, const uint16_t* scales, const int64_t* n, int U, int D,
+                               int64_t nb_cap, const void* q, fathom_dtype qdt, int G, const uint8_t* depths, int k,
+                               int64_t lo, int64_t tail, int32_t* idx, float* val, void* ws, size_t ws_bytes,
+                               uint32_t* dev_status, void* stream) {
+  return fathom_scan_topk_ex(planes, scales, n, U, D, nb_cap, q, qdt, G, depths, k, lo, tail, 0, idx, val, ws,
+                             ws_bytes, dev_status, stream);
 }
 
 size_t fathom_sparse_attn_workspace_size(int U, int G, int k, int n_sink, int n_local) {

@@ -216,9 +216,13 @@ __device__ void plan_setup(Plan& P, const FusedArgs& a, int u) {
   const int G = a.G;
   __shared__ int cnt[2][5];
   int t = 0;
+  float qv4[4] = {0.0f, 0.0f, 0.0f, 0.0f};  // this channel's q, loaded with its depth
   if (tid < kD) {
     t = gload(a.depths + (int64_t)u * kD + tid);
     t = t > kPlanes ? kPlanes : t;
+#pragma unroll
+    for (int h = 0; h < 4; ++h)
+      if (h < G) qv4[h] = load_q(a.q, a.qdt, ((int64_t)u * G + h) * kD + tid);
   }
   uint64_t bal[5];
 #pragma unroll
@@ -243,27 +247,28 @@ __device__ void plan_setup(Plan& P, const FusedArgs& a, int u) {
       P.ok = G <= 4;
     }
   }
-  if (tid < kD && t > 0) {
+  if (tid < kD && t > 0) {  // this channel's proxy index a_
     const int a_ = first[t] + (wave == 1 ? cnt[0][t] : 0) + __popcll(bal[t] & lanemask_lt(lane));
     P.act[a_] = tid | (t << 8);
     const uint64_t on = bal[1] | bal[2] | bal[3] | bal[4];
     const int w0 = cnt[0][1] + cnt[0][2] + cnt[0][3] + cnt[0][4];
     P.pord[(wave == 1 ? w0 : 0) + __popcll(on & lanemask_lt(lane))] = a_;
+#pragma unroll
+    for (int h = 0; h < 4; ++h) P.qp[a_][h] = qv4[h];
+    P.zm16[a_] = (float)(16 - (16 >> t)) * 0.0625f;
+  }
+  {
+    int nact = 0;
+#pragma unroll
+    for (int v = 1; v <= 4; ++v) nact += cnt[0][v] + cnt[1][v];
+    if (tid >= nact && tid < kD) {  // proxy indices past the active channels
+#pragma unroll
+      for (int h = 0; h < 4; ++h) P.qp[tid][h] = 0.0f;
+      P.zm16[tid] = 0.0f;
+    }
   }
   __syncthreads();
   const int A = P.A, ndw = P.ndw;
-  for (int x = tid; x < kD * 4; x += kFT) {
-    const int ai = x >> 2, h = x & 3;
-    float qv = 0.0f;
-    if (ai < A && h < G) qv = load_q(a.q, a.qdt, ((int64_t)u * G + h) * kD + (P.act[ai] & 0xFF));
-    P.qp[ai][h] = qv;
-  }
-  if (tid < kD) {
-    const int tt = tid < A ? (P.act[tid] >> 8) : 0;
-    const int zm = tt > 0 ? 16 - (16 >> tt) : 0;
-    P.zm16[tid] = (float)zm * 0.0625f;
-  }
-  __syncthreads();
   if (tid < kMaxDw * 4) {  // q16 pairs and zmax bytes
     const int d = tid >> 2, h = tid & 3;
     uint32_t pr[2] = {0u, 0u};
@@ -1151,13 +1156,13 @@ __global__ __launch_bounds__(kFT) void fused_main_kernel(FusedArgs a) {
   const int64_t qlo = lo / (kQB * kBlockTokens);       // first quad with eligible keys
   const int64_t qhi = (hi + kQB * kBlockTokens - 1) / (kQB * kBlockTokens);
   if (gw * a.ws.qpw >= qhi || (gw + kFW) * a.ws.qpw <= qlo) return;
-  plan_setup(P, a, u);
+  // tau and the bucket bounds first: their loads overlap the plan (its barriers order them)
   if (tid < 4) P.tau[tid] = tid < a.G ? gload(a.ws.tau + u * a.G + tid) : kNegInf;
-  if (tid < 4 * kSlots) {
-    const int h = tid / kSlots;
-    P.bnd[h][tid % kSlots] = h < a.G ? gload(a.ws.bnd + (u * a.G + h) * kSlots + tid % kSlots) : 0u;
+  if (tid >= kWave && tid < kWave + 4 * kSlots) {
+    const int x = tid - kWave, h = x / kSlots;
+    P.bnd[h][x % kSlots] = h < a.G ? gload(a.ws.bnd + (u * a.G + h) * kSlots + x % kSlots) : 0u;
   }
-  __syncthreads();
+  plan_setup(P, a, u);
   if (!P.ok || P.A == 0 || P.nsl > NSLM) return;
   if (NSLM <= kNarrow && (P.slrg[kMaxSl] > kOneRows || a.nb_cap >= kOneNbMax)) return;  // the wide pass's units
   bool any = false;
@@ -1488,8 +1493,8 @@ __global__ void fused_empty_kernel(const int64_t* __restrict__ n, int G, int k, 
 
 fathom_status launch_scan_topk_fused(const uint64_t* planes, const uint16_t* scales, const int64_t* n, int U,
                                      int64_t nb_cap, const void* q, fathom_dtype qdt, int G, const uint8_t* depths,
-                                     int k, int64_t lo, int64_t tail, int32_t* idx, float* val, void* ws,
-                                     uint32_t* st, hipStream_t s) {
+                                     int k, int64_t lo, int64_t tail, int max_unit_bits, int32_t* idx, float* val,
+                                     void* ws, uint32_t* st, hipStream_t s) {
   if (U == 0) return FATHOM_OK;
   if (nb_cap == 0) {
     hipLaunchKernelGGL(fused_empty_kernel, dim3(U * G), dim3(256), 0, s, n, G, k, idx, val, st);
@@ -1526,13 +1531,18 @@ fathom_status launch_scan_topk_fused(const uint64_t* planes, const uint16_t* sca
   }
   hipLaunchKernelGGL(fused_tau_kernel, dim3(R), dim3(kTauThreads), 0, s, fa);
   if (G <= 4) {
+    // a unit with at most 48 depth bits has A <= 48 channels and at most
+    // 4 + 48 / 4 = 16 row groups: the narrow pass takes every unit, and the
+    // wide launch is skipped.  (A unit above the caller's bound is left to the
+    // exact path of pass 4.)
+    const bool wide = !(max_unit_bits > 0 && max_unit_bits <= 16 * kNarrow && nb_cap < kOneNbMax);
     dim3 gm((unsigned)fa.ws.nwg, (unsigned)U);
     if (f16) {
       hipLaunchKernelGGL((fused_main_kernel<true, kNarrow, 16>), gm, dim3(kFT), 0, s, fa);
-      hipLaunchKernelGGL((fused_main_kernel<true, kMaxSl, 8>), gm, dim3(kFT), 0, s, fa);
+      if (wide) hipLaunchKernelGGL((fused_main_kernel<true, kMaxSl, 8>), gm, dim3(kFT), 0, s, fa);
     } else {
       hipLaunchKernelGGL((fused_main_kernel<false, kNarrow, 16>), gm, dim3(kFT), 0, s, fa);
-      hipLaunchKernelGGL((fused_main_kernel<false, kMaxSl, 8>), gm, dim3(kFT), 0, s, fa);
+      if (wide) hipLaunchKernelGGL((fused_main_kernel<false, kMaxSl, 8>), gm, dim3(kFT), 0, s, fa);
     }
   }
   hipLaunchKernelGGL(fused_rank_kernel, dim3(kSlots, R), dim3(kRankThreads), 0, s, fa, idx, val);

@@ -551,3 +551,31 @@ def test_scan_topk_filter_misses_no_survivor(case):
             assert int(cnt[r]) == int(np.count_nonzero(ref[h] >= tau[r])), (case, u, h)
             oi, ov, _ = oracle.topk(ref[h], k)
             assert np.array_equal(idx[u, h].cpu().numpy(), oi), (case, u, h)
+
+
+def test_scan_topk_unit_bits_hint():
+    """fathom_scan_topk_ex's bound on the depth bits of a unit selects work only:
+    the right bound (48 for water-filling at B = 48) gives the same outputs bit
+    for bit; a bound below the units' bits (water-filling at 200) still gives
+    the exact top-k, through the exact path (TOPK_FALLBACK)."""
+    ns = [70000, 33333]
+    K, nt, planes, scales = _store(ns, 91)
+    rng = np.random.default_rng(92)
+    U, G, k = len(ns), 4, 300
+    q = rng.standard_normal((U, G, 128)).astype(np.float16)
+    qt = torch.from_numpy(q).to(DEV)
+    var = torch.from_numpy(np.exp(rng.standard_normal((U, 128))).astype(np.float32)).to(DEV)
+    for B, fallback in [(48, False), (200, True)]:
+        d, _ = F.fathom_alloc_depths(qt, var, F.FATHOM_WATERFILL, B)
+        st0, st1 = F.new_status(), F.new_status()
+        i0, v0 = F.fathom_scan_topk(planes, scales, nt, qt, d, k, dev_status=st0)
+        i1, v1 = F.fathom_scan_topk(planes, scales, nt, qt, d, k, dev_status=st1, max_unit_bits=48)
+        assert torch.equal(i0, i1) and torch.equal(v0.view(torch.int32), v1.view(torch.int32)), B
+        assert status(st0) == 0, B
+        assert bool(status(st1) & F.FATHOM_DEV_TOPK_FALLBACK) == fallback, (B, status(st1))
+        P, Sc, dn = u64(planes), u16(scales), d.cpu().numpy()
+        for u, n in enumerate(ns):
+            ref = oracle.scores_f32(P[u], Sc[u], n, q[u].astype(np.float32), dn[u])
+            for h in range(G):
+                oi, _, _ = oracle.topk(ref[h], k)
+                assert np.array_equal(i1[u, h].cpu().numpy(), oi), (B, u, h)
