@@ -730,28 +730,32 @@ __device__ __forceinline__ void rescore_batch(const Plan& P, WL& W, const FusedA
   const int A = uni(P.A), ndw = uni(P.ndw), ap = 4 * ndw, stride = 4 * uni(P.nsl);
   const uint8_t* dg = reinterpret_cast<const uint8_t*>(&W.qd[(on ? lane : 0) * stride]);
   const uint16_t* sv = &W.scl[(rs * SQB + bq) * ap];
+  // heads h >= G have q = 0 and are never kept: all four chains run
   float s[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-  constexpr int kC = 4;  // channels whose reads are issued together
+  constexpr int kC = 8;  // channels whose reads are issued together
   for (int x0 = 0; x0 < A; x0 += kC) {
-    const uint32_t p0 = (uint32_t)uni((int)P.pordb[x0 >> 2]);
+    const uint32_t p0 = (uint32_t)uni((int)P.pordb[x0 >> 2]), p1 = (uint32_t)uni((int)P.pordb[(x0 >> 2) + 1]);
     uint32_t dv[kC], hv[kC];
+    float4 q4[kC];
+    float zz[kC];
 #pragma unroll
-    for (int c = 0; c < kC; ++c) {
-      const int ai = (int)((p0 >> (8 * c)) & 0xFFu);
+    for (int c = 0; c < kC; ++c) {  // positions past A read valid entries that are not used
+      const int ai = (int)(((c < 4 ? p0 : p1) >> (8 * (c & 3))) & 0xFFu);
       dv[c] = dg[ai];
       hv[c] = sv[ai];
+      q4[c] = *reinterpret_cast<const float4*>(&P.qa[x0 + c][0]);
+      zz[c] = P.za[x0 + c];
     }
 #pragma unroll
     for (int c = 0; c < kC; ++c) {
       if (x0 + c < A) {
-        const float4 q4 = *reinterpret_cast<const float4*>(&P.qa[x0 + c][0]);
         const uint32_t u4 = (dv[c] >> mu) & 15u;
         const float af = half_bits_to_float((uint16_t)hv[c]);
-        const float khat = __fmaf_rn((float)u4, __fmul_rn(af, 0.125f), -__fmul_rn(af, P.za[x0 + c]));
-        s[0] = __fmaf_rn(q4.x, khat, s[0]);
-        if (G > 1) s[1] = __fmaf_rn(q4.y, khat, s[1]);
-        if (G > 2) s[2] = __fmaf_rn(q4.z, khat, s[2]);
-        if (G > 3) s[3] = __fmaf_rn(q4.w, khat, s[3]);
+        const float khat = __fmaf_rn((float)u4, __fmul_rn(af, 0.125f), -__fmul_rn(af, zz[c]));
+        s[0] = __fmaf_rn(q4[c].x, khat, s[0]);
+        s[1] = __fmaf_rn(q4[c].y, khat, s[1]);
+        s[2] = __fmaf_rn(q4[c].z, khat, s[2]);
+        s[3] = __fmaf_rn(q4[c].w, khat, s[3]);
       }
     }
   }
