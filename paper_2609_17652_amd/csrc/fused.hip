@@ -373,7 +373,7 @@ struct alignas(16) WaveLdsT {
   uint32_t st[st_rows(NSLM)][kStP];          // staged row groups (per-slice slot 4 (d mod 4) + p, or row group g)
   uint32_t W[SQB * 4 * 4 * NSLM];            // int8 weights [block][head][dword < 4 nsl] of the superquad
   int32_t ci[SQB][4][4];                     // [block][mu][head] accumulator start; sample: [b][0][h] bias, [b][1][h] ok
-  uint16_t scl[RQ * SQB * 16 * NSLM];        // fp16 scales [ring slot][block][proxy channel]
+  uint16_t scl[RQ * SQB * (16 * NSLM + 2)];  // fp16 scales [ring slot][block][proxy channel], rows of 4 ndw + 2
   float amx[16 * NSLM];                      // per proxy channel: largest scale of the superquad
   uint32_t qd[QCAP > 0 ? QCAP * 4 * NSLM : 4];  // queued digit dwords, 4 nsl per entry
   uint32_t qi[QCAP > 0 ? QCAP : 1];          // queued key index
@@ -440,8 +440,8 @@ __device__ __forceinline__ void scl_issue(SclRegs<NCH, SQB>& r, const Plan& P, c
 template <bool QF16, int NCH, int SQB, class WL>
 __device__ SqInfo scl_commit(const SclRegs<NCH, SQB>& r, const Plan& P, WL& W, int slot) {
   const int lane = threadIdx.x & 63;
-  const int A = uni(P.A), ap = 4 * uni(P.ndw);
-  uint16_t* sdst = &W.scl[slot * SQB * ap];
+  const int A = uni(P.A), ap = 4 * uni(P.ndw), aps = ap + 2;  // row stride: an odd number of dwords
+  uint16_t* sdst = &W.scl[slot * SQB * aps];
   bool nf = false;
 #pragma unroll
   for (int c = 0; c < NCH; ++c) {
@@ -451,7 +451,7 @@ __device__ SqInfo scl_commit(const SclRegs<NCH, SQB>& r, const Plan& P, WL& W, i
 #pragma unroll
       for (int b = 0; b < SQB; ++b) {
         const uint32_t h = (r.v[c][b >> 1] >> (16 * (b & 1))) & 0xFFFFu;
-        sdst[b * ap + x] = (uint16_t)h;
+        sdst[b * aps + x] = (uint16_t)h;
         const uint32_t m = h & 0x7FFFu;
         mx = m > mx ? m : mx;
       }
@@ -484,18 +484,19 @@ __device__ SqInfo scl_commit(const SclRegs<NCH, SQB>& r, const Plan& P, WL& W, i
 template <bool QF16, bool SAMPLE, int SQB, class WL>
 __device__ void superquad_weights(const Plan& P, WL& W, const FusedArgs& a, const SqInfo& si, int slot) {
   const int lane = threadIdx.x & 63, beta = lane & 15, h = lane >> 4;
-  const int ndw = uni(P.ndw), ap = 4 * ndw, ws = 4 * uni(P.nsl);
+  const int ndw = uni(P.ndw), aps = 4 * ndw + 2, ws = 4 * uni(P.nsl);
   if (beta < SQB) {
     int bias = 0;
     uint32_t* wdst = &W.W[(beta * 4 + h) * ws];  // dwords ndw .. ws - 1 stay zero
-    const uint16_t* srow = &W.scl[(slot * SQB + beta) * ap];
+    const uint16_t* srow = &W.scl[(slot * SQB + beta) * aps];
     if (si.valid) {
       if (QF16) {
         const uint32_t cb = (uint32_t)((si.e + 25) << 10 | 0x200);
         const uint32_t c2 = cb | cb << 16;
         for (int d = 0; d < ndw; ++d) {
           const uint2 qq = *reinterpret_cast<const uint2*>(&P.q16[d][h][0]);
-          const uint2 aa = *reinterpret_cast<const uint2*>(&srow[4 * d]);
+          const uint2 aa = make_uint2(*reinterpret_cast<const uint32_t*>(&srow[4 * d]),
+                                      *reinterpret_cast<const uint32_t*>(&srow[4 * d + 2]));  // rows: 4-byte aligned
           const uint32_t r0 = pkfma16(qq.x, aa.x, c2), r1 = pkfma16(qq.y, aa.y, c2);
           const uint32_t wd = __builtin_amdgcn_perm(r1, r0, 0x06040200u);
           wdst[d] = wd;
@@ -729,7 +730,7 @@ __device__ __forceinline__ void rescore_batch(const Plan& P, WL& W, const FusedA
   const int rs = (int)((f >> 8) & 15u), bq = (int)((f >> 12) & 15u);
   const int A = uni(P.A), ndw = uni(P.ndw), ap = 4 * ndw, stride = 4 * uni(P.nsl);
   const uint8_t* dg = reinterpret_cast<const uint8_t*>(&W.qd[(on ? lane : 0) * stride]);
-  const uint16_t* sv = &W.scl[(rs * SQB + bq) * ap];
+  const uint16_t* sv = &W.scl[(rs * SQB + bq) * (ap + 2)];  // scale rows of 4 ndw + 2 halves
   // heads h >= G have q = 0 and are never kept: all four chains run
   float s[4] = {0.0f, 0.0f, 0.0f, 0.0f};
   constexpr int kC = 8;  // channels whose reads are issued together
