@@ -1061,6 +1061,15 @@ constexpr int kTauPer = kSmpRow / kWave;  // sampled values per lane
 __global__ __launch_bounds__(kTauThreads) void fused_tau_kernel(FusedArgs a) {
   __shared__ int sc[kPlanes + 1];  // active channels by depth
   const int r = blockIdx.x, G = a.G, u = r / G, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // every load first: the samples (each wave keeps the row's 512), the depths, n
+  const int ns = a.ws.s_quads * kSmpW;
+  float sv[kTauPer];
+#pragma unroll
+  for (int x = 0; x < kTauPer; ++x) {
+    const int i = lane + kWave * x;
+    sv[x] = i < ns ? gload(a.ws.samp + (int64_t)r * kSmpRow + i) : kNegInf;
+  }
+  const int t = tid < kD ? gload(a.depths + (int64_t)u * kD + tid) : 0;
   if (tid < kSlots) {
     a.ws.cnt[r * kSlots + tid] = 0u;
     a.ws.bnd[r * kSlots + tid] = 0u;
@@ -1069,10 +1078,7 @@ __global__ __launch_bounds__(kTauThreads) void fused_tau_kernel(FusedArgs a) {
   row_window(a, u, &nu, &lo, &hi, false);
   if (tid <= kPlanes) sc[tid] = 0;
   __syncthreads();
-  if (tid < kD) {
-    const int t = gload(a.depths + (int64_t)u * kD + tid);
-    if (t > 0) atomicAdd(&sc[t > kPlanes ? kPlanes : t], 1);
-  }
+  if (tid < kD && t > 0) atomicAdd(&sc[t > kPlanes ? kPlanes : t], 1);
   __syncthreads();
   const int A = sc[1] + sc[2] + sc[3] + sc[4];
   const bool ok = G <= 4 && A > 0 && hi - lo > a.ws.cap;
@@ -1093,17 +1099,11 @@ __global__ __launch_bounds__(kTauThreads) void fused_tau_kernel(FusedArgs a) {
     return;
   }
   // every wave: the row's samples as keys (0 = no sample) and m
-  const int ns = a.ws.s_quads * kSmpW;
   uint32_t key[kTauPer];
   int nv = 0;
 #pragma unroll
   for (int x = 0; x < kTauPer; ++x) {
-    const int i = lane + kWave * x;
-    key[x] = 0u;
-    if (i < ns) {
-      const float v = gload(a.ws.samp + (int64_t)r * kSmpRow + i);
-      if (v > kNegInf) key[x] = score_key(v) | 1u;  // proxies are never NaN; keep 0 free
-    }
+    key[x] = sv[x] > kNegInf ? score_key(sv[x]) | 1u : 0u;  // proxies are never NaN; keep 0 free
     nv += __popcll(__ballot(key[x] != 0u));
   }
   int64_t m_s = 0;  // eligible keys in the sampled quads
@@ -1388,6 +1388,16 @@ __global__ __launch_bounds__(kRankThreads) void fused_rank_kernel(FusedArgs a, i
   __shared__ int64_t s_n;
   const int G = a.G;
   const int z = blockIdx.x, r = blockIdx.y, u = r / G, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // the bucket's slots up to its capacity are read with the counts (slots past
+  // the count are not used)
+  constexpr int kPer = kRankCap / kRankThreads;
+  const uint64_t* src = a.ws.cand + ((int64_t)r * kSlots + z) * a.ws.scap;
+  uint64_t pv[kPer];
+#pragma unroll
+  for (int j = 0; j < kPer; ++j) {
+    const int e = tid + kRankThreads * j;
+    pv[j] = e < a.ws.scap ? gload(src + e) : 0ull;
+  }
   if (tid < kSlots) s_cnt[tid] = gload(a.ws.cnt + r * kSlots + tid);
   else if (tid == kSlots) s_tau = gload(a.ws.tau + r);
   else if (tid == kSlots + 1) s_ovf = gload(a.ws.uovf + u);
@@ -1402,15 +1412,17 @@ __global__ __launch_bounds__(kRankThreads) void fused_rank_kernel(FusedArgs a, i
   for (int y = 0; y < z; ++y) off0 += s_cnt[y];
   const int c = (int)s_cnt[z], k = a.k;
   if (off0 >= (uint32_t)k || c == 0) return;
-  // load, and the bucket's key range
-  const uint64_t* src = a.ws.cand + ((int64_t)r * kSlots + z) * a.ws.scap;
+  // the bucket, and its key range
   uint32_t kmin = 0xFFFFFFFFu, kmax = 0u;
-  for (int e = tid; e < c; e += kRankThreads) {
-    const uint64_t v = gload(src + e);
-    buf[e] = v;
-    const uint32_t key = (uint32_t)(v >> 32);
-    kmin = key < kmin ? key : kmin;
-    kmax = key > kmax ? key : kmax;
+#pragma unroll
+  for (int j = 0; j < kPer; ++j) {
+    const int e = tid + kRankThreads * j;
+    if (e < c) {
+      buf[e] = pv[j];
+      const uint32_t key = (uint32_t)(pv[j] >> 32);
+      kmin = key < kmin ? key : kmin;
+      kmax = key > kmax ? key : kmax;
+    }
   }
   int ns = 64;  // sub-buckets: a power of two, about twice the survivors
   while (ns < 2 * c && ns < kRankSub) ns <<= 1;
