@@ -38,7 +38,7 @@ fathom_status check_store(const uint64_t* planes, const uint16_t* scales, const 
                           int64_t nb_cap, const void* q, fathom_dtype qdt, int G, const uint8_t* depths) {
   if (U < 0 || nb_cap < 0) return FATHOM_ERR_INVALID;
   if (D != kD) return FATHOM_ERR_UNSUPPORTED;
-  if (G < 1 || G > 8 || !dtype_ok(qdt)) return FATHOM_ERR_UNSUPPORTED;
+  if (G < 1 || G > kMaxG || !dtype_ok(qdt)) return FATHOM_ERR_UNSUPPORTED;
   if (nb_cap > ((int64_t)1 << 25)) return FATHOM_ERR_UNSUPPORTED;  // 2^31 tokens per unit
   if (U == 0 || nb_cap == 0) return FATHOM_OK;
   if (!planes || !scales || !n || !q || !depths) return FATHOM_ERR_INVALID;
@@ -90,7 +90,7 @@ fathom_status fathom_alloc_depths(const void* q, fathom_dtype qdt, int U, int G,
                                   uint32_t* dev_status, void* stream) {
   if (U < 0) return FATHOM_ERR_INVALID;
   if (D != kD) return FATHOM_ERR_UNSUPPORTED;
-  if (G < 1 || G > 8 || !dtype_ok(qdt)) return FATHOM_ERR_UNSUPPORTED;
+  if (G < 1 || G > kMaxG || !dtype_ok(qdt)) return FATHOM_ERR_UNSUPPORTED;
   if (mode != FATHOM_WATERFILL && mode != FATHOM_UNIFORM_TOPR) return FATHOM_ERR_UNSUPPORTED;
   if (mode == FATHOM_WATERFILL && (budget_or_r < 0 || budget_or_r > 4 * D)) return FATHOM_ERR_RANGE;
   if (mode == FATHOM_UNIFORM_TOPR && (budget_or_r < 0 || budget_or_r > D)) return FATHOM_ERR_RANGE;
@@ -121,7 +121,7 @@ fathom_status fathom_topk(const float* scores, int64_t ld_s, const int64_t* n, i
                           int64_t tail, int32_t* idx, float* val, void* ws, size_t ws_bytes, uint32_t* dev_status,
                           void* stream) {
   if (U < 0 || ld_s < 1 || lo < 0 || tail < 0 || k < 1) return FATHOM_ERR_INVALID;
-  if (G < 1 || G > 8) return FATHOM_ERR_UNSUPPORTED;
+  if (G < 1 || G > kMaxG) return FATHOM_ERR_UNSUPPORTED;
   if (k > FATHOM_MAX_K) return FATHOM_ERR_UNSUPPORTED;
   if (ld_s > ((int64_t)1 << 31) - 1) return FATHOM_ERR_UNSUPPORTED;
   if (U == 0) return FATHOM_OK;
@@ -171,7 +171,7 @@ fathom_status fathom_sparse_attn(const void* q, fathom_dtype qdt, const uint16_t
                                  void* ws, size_t ws_bytes, uint32_t* dev_status, void* stream) {
   if (U < 0 || k < 0 || n_sink < 0 || n_local < 0) return FATHOM_ERR_INVALID;
   if (D != kD) return FATHOM_ERR_UNSUPPORTED;
-  if (G < 1 || G > 8 || !dtype_ok(qdt)) return FATHOM_ERR_UNSUPPORTED;
+  if (G < 1 || G > kMaxG || !dtype_ok(qdt)) return FATHOM_ERR_UNSUPPORTED;
   if (k > FATHOM_MAX_K || n_sink + n_local > attn_max_sink_local()) return FATHOM_ERR_UNSUPPORTED;
   if (U == 0) return FATHOM_OK;
   if (!q || !Krows || !Vrows || !n || !out || (k > 0 && !idx)) return FATHOM_ERR_INVALID;

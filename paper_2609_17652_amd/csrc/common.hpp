@@ -13,6 +13,7 @@ constexpr int kWave = 64;
 constexpr int kBlockTokens = 64;  // tokens per quantisation block (Sec. 3.2)
 constexpr int kPlanes = 4;        // 4-bit codes
 constexpr int kD = 128;           // supported head dimension
+constexpr int kMaxG = 8;          // query heads per KV head accepted by every entry point
 
 #define FATHOM_LAUNCH_CHECK()                                   \
   do {                                                          \

@@ -821,7 +821,7 @@ __device__ void wave_run(const Plan& P, WaveLdsT<NSLM, SQB, RQ, QCAP>& W, const 
   scl_issue(sr, P, a, u, b0);
   // kOne: all row groups staged in one pass (narrow full pass); otherwise one
   // staging pass per slice
-  constexpr bool kOne = !SAMPLE && NSLM <= kNarrow;
+  constexpr bool kOne = NSLM <= kNarrow;
   uint64_t ring[kOne ? 1 : NSLM][4];
   StageLane L;
   uint32_t shpv[NSLM];          // kOne: slice shapes (c_p fields), kept in VGPRs
@@ -1023,12 +1023,13 @@ __device__ void wave_run(const Plan& P, WaveLdsT<NSLM, SQB, RQ, QCAP>& W, const 
 }
 
 // ---------------------------------------------------------------- pass 1
-typedef WaveLdsT<kMaxSl, kQB, 1, 0> SampleLds;
-
-template <bool QF16>
+// NSLM = kNarrow when the caller's bound leaves no unit to the wide full pass:
+// a unit the narrow instantiation cannot take gets no samples (its rows are
+// then computed exactly by pass 4, as in the full pass).
+template <bool QF16, int NSLM>
 __global__ __launch_bounds__(kFT) void fused_sample_kernel(FusedArgs a) {
   __shared__ Plan P;
-  __shared__ SampleLds WL[kFW];
+  __shared__ WaveLdsT<NSLM, kQB, 1, 0> WL[kFW];
   const int u = blockIdx.y, wave = uni(threadIdx.x >> 6);
   int64_t nu, lo, hi;
   row_window(a, u, &nu, &lo, &hi, false);
@@ -1041,13 +1042,14 @@ __global__ __launch_bounds__(kFT) void fused_sample_kernel(FusedArgs a) {
   const int64_t sq = (int64_t)blockIdx.x * kFW + wave;
   if (sq >= a.ws.s_quads) return;
   const int64_t b0 = sq * a.ws.s_stride * kQB;
-  if (b0 >= nbu || b0 * kBlockTokens >= hi || (b0 + kQB) * kBlockTokens <= lo) {
+  const bool fits = P.nsl <= NSLM && (NSLM > kNarrow || (P.slrg[kMaxSl] <= kOneRows && a.nb_cap < kOneNbMax));
+  if (!fits || b0 >= nbu || b0 * kBlockTokens >= hi || (b0 + kQB) * kBlockTokens <= lo) {
     const int lane = threadIdx.x & 63;
     for (int r = 0; r < a.G; ++r)
       if (lane < kSmpW) gstore(a.ws.samp + ((int64_t)u * a.G + r) * kSmpRow + sq * kSmpW + lane, kNegInf);
     return;
   }
-  wave_run<QF16, true, kMaxSl, kQB, 1, 0>(P, WL[wave], a, u, b0, b0 + kQB, nbu, lo, hi, sq);
+  wave_run<QF16, true, NSLM, kQB, 1, 0>(P, WL[wave], a, u, b0, b0 + kQB, nbu, lo, hi, sq);
 }
 
 // ---------------------------------------------------------------- pass 2
@@ -1541,18 +1543,23 @@ fathom_status launch_scan_topk_fused(const uint64_t* planes, const uint16_t* sca
   fa.st = st;
   const int R = U * G;
   const bool f16 = qdt == FATHOM_F16;
+  // a unit with at most 48 depth bits has A <= 48 channels and at most
+  // 4 + 48 / 4 = 16 row groups: the narrow pass takes every unit, and the
+  // wide launches are skipped.  (A unit above the caller's bound is left to the
+  // exact path of pass 4.)
+  const bool wide = !(max_unit_bits > 0 && max_unit_bits <= 16 * kNarrow && nb_cap < kOneNbMax);
   if (G <= 4) {
     dim3 gs((unsigned)((fa.ws.s_quads + kFW - 1) / kFW), (unsigned)U);
-    if (f16) hipLaunchKernelGGL(fused_sample_kernel<true>, gs, dim3(kFT), 0, s, fa);
-    else hipLaunchKernelGGL(fused_sample_kernel<false>, gs, dim3(kFT), 0, s, fa);
+    if (f16) {
+      if (wide) hipLaunchKernelGGL((fused_sample_kernel<true, kMaxSl>), gs, dim3(kFT), 0, s, fa);
+      else hipLaunchKernelGGL((fused_sample_kernel<true, kNarrow>), gs, dim3(kFT), 0, s, fa);
+    } else {
+      if (wide) hipLaunchKernelGGL((fused_sample_kernel<false, kMaxSl>), gs, dim3(kFT), 0, s, fa);
+      else hipLaunchKernelGGL((fused_sample_kernel<false, kNarrow>), gs, dim3(kFT), 0, s, fa);
+    }
   }
   hipLaunchKernelGGL(fused_tau_kernel, dim3(R), dim3(kTauThreads), 0, s, fa);
   if (G <= 4) {
-    // a unit with at most 48 depth bits has A <= 48 channels and at most
-    // 4 + 48 / 4 = 16 row groups: the narrow pass takes every unit, and the
-    // wide launch is skipped.  (A unit above the caller's bound is left to the
-    // exact path of pass 4.)
-    const bool wide = !(max_unit_bits > 0 && max_unit_bits <= 16 * kNarrow && nb_cap < kOneNbMax);
     dim3 gm((unsigned)fa.ws.nwg, (unsigned)U);
     if (f16) {
       hipLaunchKernelGGL((fused_main_kernel<true, kNarrow, 16>), gm, dim3(kFT), 0, s, fa);
