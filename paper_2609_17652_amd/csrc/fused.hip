@@ -211,19 +211,42 @@ struct alignas(16) Plan {
   uint32_t bnd[4][kSlots];     // head h: score keys splitting its survivors into value buckets
 };
 
-__device__ void plan_setup(Plan& P, const FusedArgs& a, int u) {
+// The plan's global reads (thread j < 128: channel j's depth and its q for
+// every head), issued by a kernel before its other preamble work.
+struct PlanPre {
+  int t;
+  float q[4];
+};
+template <bool QF16>
+__device__ __forceinline__ PlanPre plan_load(const FusedArgs& a, int u) {
+  const int tid = threadIdx.x, G = a.G;
+  PlanPre r;
+  r.t = 0;
+  float x[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+  if (tid < kD) {
+    r.t = gload(a.depths + (int64_t)u * kD + tid);
+#pragma unroll
+    for (int h = 0; h < 4; ++h) {  // heads past G (at most 4 here) re-read head 0
+      const int64_t i = ((int64_t)u * G + (h < G ? h : 0)) * kD + tid;
+      if (QF16)
+        x[h] = __half2float(__ushort_as_half(((const __attribute__((address_space(1))) uint16_t*)a.q)[i]));
+      else
+        x[h] = ((const __attribute__((address_space(1))) float*)a.q)[i];
+    }
+  }
+#pragma unroll
+  for (int h = 0; h < 4; ++h) r.q[h] = h < G ? x[h] : 0.0f;
+  return r;
+}
+
+__device__ void plan_setup(Plan& P, const FusedArgs& a, int u, const PlanPre& pre) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int G = a.G;
   __shared__ int cnt[2][5];
-  int t = 0;
-  float qv4[4] = {0.0f, 0.0f, 0.0f, 0.0f};  // this channel's q, loaded with its depth
-  if (tid < kD) {
-    t = gload(a.depths + (int64_t)u * kD + tid);
-    t = t > kPlanes ? kPlanes : t;
+  const int t = pre.t > kPlanes ? kPlanes : pre.t;
+  float qv4[4];  // this channel's q, loaded with its depth
 #pragma unroll
-    for (int h = 0; h < 4; ++h)
-      if (h < G) qv4[h] = load_q(a.q, a.qdt, ((int64_t)u * G + h) * kD + tid);
-  }
+  for (int h = 0; h < 4; ++h) qv4[h] = pre.q[h];
   uint64_t bal[5];
 #pragma unroll
   for (int v = 1; v <= 4; ++v) bal[v] = __ballot(tid < kD && t == v);
@@ -1031,10 +1054,11 @@ __global__ __launch_bounds__(kFT) void fused_sample_kernel(FusedArgs a) {
   __shared__ Plan P;
   __shared__ WaveLdsT<NSLM, kQB, 1, 0> WL[kFW];
   const int u = blockIdx.y, wave = uni(threadIdx.x >> 6);
+  const PlanPre pre = plan_load<QF16>(a, u);
   int64_t nu, lo, hi;
   row_window(a, u, &nu, &lo, &hi, false);
   if (hi - lo <= a.ws.cap) return;  // computed directly by pass 4
-  plan_setup(P, a, u);
+  plan_setup(P, a, u, pre);
   if (!P.ok || P.A == 0) return;
   if (threadIdx.x < 4) P.tau[threadIdx.x] = 0.0f;
   __syncthreads();
@@ -1153,23 +1177,26 @@ __global__ __launch_bounds__(kFT) void fused_main_kernel(FusedArgs a) {
   __shared__ Plan P;
   __shared__ WaveLdsT<NSLM, SQB, kRing, kQCap> WL[kFW];
   const int u = blockIdx.y, tid = threadIdx.x, wave = uni(tid >> 6);
-  const int ucls = (int)(gload(a.ws.uovf + u) >> 1);  // slices, or 0
-  if (ucls == 0 || ucls > NSLM || (NSLM > kNarrow && ucls <= kNarrow)) return;
+  // every global read of the preamble first: unit class, n, tau, bucket
+  // bounds, depths and q (the plan's barriers order the LDS writes)
+  const uint32_t uo = gload(a.ws.uovf + u);
+  if (tid < 4) P.tau[tid] = tid < a.G ? gload(a.ws.tau + u * a.G + tid) : kNegInf;
+  if (tid >= kWave && tid < kWave + 4 * kSlots) {
+    const int x = tid - kWave, h = x / kSlots;
+    P.bnd[h][x % kSlots] = h < a.G ? gload(a.ws.bnd + (u * a.G + h) * kSlots + x % kSlots) : 0u;
+  }
+  const PlanPre pre = plan_load<QF16>(a, u);
   int64_t nu, lo, hi;
   row_window(a, u, &nu, &lo, &hi, blockIdx.x == 0 && tid == 0);
+  const int ucls = (int)(uo >> 1);  // slices, or 0
+  if (ucls == 0 || ucls > NSLM || (NSLM > kNarrow && ucls <= kNarrow)) return;
   if (hi - lo <= a.ws.cap) return;
   const int64_t nbu = (nu + kBlockTokens - 1) / kBlockTokens;
   const int64_t gw = (int64_t)blockIdx.x * kFW;       // first wave of this workgroup
   const int64_t qlo = lo / (kQB * kBlockTokens);       // first quad with eligible keys
   const int64_t qhi = (hi + kQB * kBlockTokens - 1) / (kQB * kBlockTokens);
   if (gw * a.ws.qpw >= qhi || (gw + kFW) * a.ws.qpw <= qlo) return;
-  // tau and the bucket bounds first: their loads overlap the plan (its barriers order them)
-  if (tid < 4) P.tau[tid] = tid < a.G ? gload(a.ws.tau + u * a.G + tid) : kNegInf;
-  if (tid >= kWave && tid < kWave + 4 * kSlots) {
-    const int x = tid - kWave, h = x / kSlots;
-    P.bnd[h][x % kSlots] = h < a.G ? gload(a.ws.bnd + (u * a.G + h) * kSlots + x % kSlots) : 0u;
-  }
-  plan_setup(P, a, u);
+  plan_setup(P, a, u, pre);
   if (!P.ok || P.A == 0 || P.nsl > NSLM) return;
   if (NSLM <= kNarrow && (P.slrg[kMaxSl] > kOneRows || a.nb_cap >= kOneNbMax)) return;  // the wide pass's units
   bool any = false;
