@@ -49,6 +49,10 @@ def parse():
     ap.add_argument("--scan-reps", type=int, default=32, help="extra scan-only launches timed for the roofline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-units", type=int, default=4, help="units in the oracle's CPU-baseline sample")
+    ap.add_argument("--traffic-calib", type=int, default=0, metavar="MIB",
+                    help="end with one plain device-to-device copy of MIB MiB (counter calibration)")
+    ap.add_argument("--traffic-summary", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="write the HBM-traffic summary from two rocprofv3 --pmc counter files and exit")
     return ap.parse_args()
 
 
@@ -86,8 +90,71 @@ def cpu_baseline(planes, scales, q, var, n, mode, B, k, units):
                       f"({dt:.1f} s wall)"}
 
 
+TRAFFIC_JSON = os.path.join(ROOT, "profiles", "scan_topk_layer1m_b48_traffic.json")
+TRAFFIC_SOURCES = ("paper_2609_17652_amd/csrc/fused.hip", "paper_2609_17652_amd/csrc/common.hpp")
+SCAN_TOPK_KERNELS = ("fused_sample_kernel", "fused_tau_kernel", "fused_main_kernel", "fused_rank_kernel",
+                     "fused_select_kernel")
+
+
+def kernel_source_hash():
+    import hashlib
+    h = hashlib.sha256()
+    for f in TRAFFIC_SOURCES:
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def traffic_summary(fetch_csv, write_csv, calib_mib):
+    """HBM bytes per fathom_scan_topk call from FETCH_SIZE / WRITE_SIZE (KiB per
+    dispatch), each scaled so that the calibration copy of calib_mib MiB (the
+    last copyBuffer dispatch of at least a quarter of that size) reads and
+    writes exactly its size."""
+    import csv
+    from collections import defaultdict
+
+    calib = float(calib_mib) * 1024.0  # KiB
+    out = {}
+    for name, path in (("FETCH_SIZE", fetch_csv), ("WRITE_SIZE", write_csv)):
+        rows = sorted((r for r in csv.DictReader(open(path)) if r["Counter_Name"] == name),
+                      key=lambda r: int(r["Dispatch_Id"]))
+        vals = defaultdict(list)
+        for r in rows:
+            vals[r["Kernel_Name"]].append(float(r["Counter_Value"]))
+        copies = [float(r["Counter_Value"]) for r in rows
+                  if "copyBuffer" in r["Kernel_Name"] and float(r["Counter_Value"]) >= calib / 4]
+        factor = calib / copies[-1]
+        per = {}
+        for k, vs in vals.items():
+            short = next((t for t in SCAN_TOPK_KERNELS if t in k), None)
+            if short is None:
+                continue
+            key = short + ("<narrow>" if "fused_main_kernel" in k and ", 3," in k else "")
+            per[key] = per.get(key, 0.0) + float(np.mean(vs)) * 1024.0 * factor
+        out[name] = {"factor": factor, "calib_raw_kib": copies[-1], "per_kernel_bytes": per}
+    total = sum(out["FETCH_SIZE"]["per_kernel_bytes"].values()) + sum(out["WRITE_SIZE"]["per_kernel_bytes"].values())
+    return {"bytes_per_call": total, "counters": out, "source_sha256": kernel_source_hash(),
+            "sources": list(TRAFFIC_SOURCES), "calib_mib": calib_mib}
+
+
+def measured_traffic():
+    """The committed per-call HBM traffic, or None once the kernel sources changed."""
+    try:
+        with open(TRAFFIC_JSON) as fh:
+            t = json.load(fh)
+    except (OSError, ValueError):
+        return None
+    return t["bytes_per_call"] if t.get("source_sha256") == kernel_source_hash() else None
+
+
 def main():
     args = parse()
+    if args.traffic_summary:
+        t = traffic_summary(args.traffic_summary[0], args.traffic_summary[1], args.traffic_calib or 256)
+        with open(TRAFFIC_JSON, "w") as fh:
+            json.dump(t, fh, indent=1)
+        print(json.dumps(t))
+        return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus > 1 or world > 1:
         print(json.dumps({"error": "this build runs on one GPU only: --gpus must be 1 "
@@ -217,10 +284,18 @@ def main():
         "active_channels_mean": active,
         "plane_bits_per_key_mean": float(dn.sum(1).mean()),
         "device_status": status,
-        "roofline": {"bound": "hbm", "kernel": "fathom_scan_topk (sample, tau, full, select launches)",
+        "roofline": {"bound": "hbm", "kernel": "fathom_scan_topk (sample, tau, full, rank, select launches)",
                      "achieved": st_gbps, "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": st_gbps / HBM_PEAK_GBPS,
-                     "traffic": None, "alg_bytes_per_launch": alg_bytes, "avg_launch_ms": st_ms},
+                     "traffic": measured_traffic(), "alg_bytes_per_launch": alg_bytes, "avg_launch_ms": st_ms},
     }
+    if args.traffic_calib > 0:
+        nbytes = args.traffic_calib << 20
+        src = torch.ones((nbytes,), dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     if not args.no_cpu_baseline:
         log(f"[bench] cpu baseline: oracle on {args.cpu_units} units")
         res["cpu_baseline"] = cpu_baseline(planes[0], scales[0], q, var, n, mode, B, k, args.cpu_units)
