@@ -579,3 +579,61 @@ def test_scan_topk_unit_bits_hint():
             for h in range(G):
                 oi, _, _ = oracle.topk(ref[h], k)
                 assert np.array_equal(i1[u, h].cpu().numpy(), oi), (B, u, h)
+
+
+def _assert_rows_match(idx, val, planes, scales, ns, q, d, k, lo, tail):
+    """Every (unit, head) row: indices bit-exact to the oracle, values bit-exact
+    where finite, NaN where the oracle pads a short row."""
+    P, Sc, dn = u64(planes), u16(scales), d.cpu().numpy()
+    ix, vx = idx.cpu().numpy(), val.cpu().numpy()
+    for u, n in enumerate(ns):
+        ref = oracle.scores_f32(P[u], Sc[u], n, q[u].astype(np.float32), dn[u])
+        for h in range(q.shape[1]):
+            oi, ov, _ = oracle.topk(ref[h], k, lo, tail)
+            assert np.array_equal(ix[u, h], oi), (k, lo, tail, u, h)
+            pad = np.isnan(ov)
+            assert np.array_equal(np.isnan(vx[u, h]), pad), (u, h)
+            assert np.array_equal(vx[u, h][~pad].view(np.uint32), ov[~pad].view(np.uint32)), (u, h)
+
+
+@pytest.mark.parametrize("G,qdt", [(1, np.float32), (2, np.float16), (3, np.float32), (4, np.float32),
+                                   (8, np.float16)])
+def test_scan_topk_heads_and_query_dtypes(G, qdt):
+    """The filter path for every head count it serves (G <= 4) with fp16 and fp32
+    queries, and the exact path that G > 4 takes: ragged units whose eligible
+    ranges exceed the survivor lists (n = 40000 and 23456, k = 300)."""
+    ns = [40000, 23456]
+    K, nt, planes, scales = _store(ns, 61 + G)
+    rng = np.random.default_rng(62 + G)
+    q = rng.standard_normal((len(ns), G, 128)).astype(qdt)
+    qt = torch.from_numpy(q).to(DEV)
+    var = torch.from_numpy(np.exp(rng.standard_normal((len(ns), 128))).astype(np.float32)).to(DEV)
+    d, _ = F.fathom_alloc_depths(qt, var, F.FATHOM_WATERFILL, 48)
+    for k, lo, tail in [(300, 0, 0), (300, 4, 32)]:
+        st = F.new_status()
+        idx, val = F.fathom_scan_topk(planes, scales, nt, qt, d, k, lo, tail, dev_status=st, max_unit_bits=48)
+        s = status(st)
+        assert s & ~F.FATHOM_DEV_TOPK_FALLBACK == 0, hex(s)
+        if G > 4:
+            assert s & F.FATHOM_DEV_TOPK_FALLBACK  # no filter for more than 4 query heads
+        _assert_rows_match(idx, val, planes, scales, ns, q, d, k, lo, tail)
+
+
+def test_scan_topk_empty_and_short_rows():
+    """n = 0, n below lo + tail, fewer eligible keys than k, beside a filtered unit
+    in the same launch: short rows hold their eligible keys in order, then index
+    -1 and value NaN, and the call reports TOPK_SHORT."""
+    ns = [0, 30, 500, 30000]
+    K, nt, planes, scales = _store(ns, 71)
+    rng = np.random.default_rng(72)
+    q = rng.standard_normal((len(ns), 4, 128)).astype(np.float16)
+    qt = torch.from_numpy(q).to(DEV)
+    var = torch.from_numpy(np.exp(rng.standard_normal((len(ns), 128))).astype(np.float32)).to(DEV)
+    d, _ = F.fathom_alloc_depths(qt, var, F.FATHOM_WATERFILL, 48)
+    k, lo, tail = 600, 4, 32
+    st = F.new_status()
+    idx, val = F.fathom_scan_topk(planes, scales, nt, qt, d, k, lo, tail, dev_status=st)
+    s = status(st)
+    assert s & F.FATHOM_DEV_TOPK_SHORT, hex(s)
+    assert s & ~(F.FATHOM_DEV_TOPK_SHORT | F.FATHOM_DEV_TOPK_FALLBACK) == 0, hex(s)
+    _assert_rows_match(idx, val, planes, scales, ns, q, d, k, lo, tail)
