@@ -46,6 +46,8 @@
 // overflows), pass (4) recomputes the row exactly with a streaming top-k
 // (FATHOM_DEV_TOPK_FALLBACK).  The result never depends on tau or the bucket
 // bounds; they only decide how much work is saved.
+#include <atomic>
+
 #include "common.hpp"
 
 namespace fathom {
@@ -1547,12 +1549,17 @@ fathom_status launch_scan_topk_fused(const uint64_t* planes, const uint16_t* sca
     FATHOM_LAUNCH_CHECK();
     return FATHOM_OK;
   }
-  static bool attr = false;
-  if (!attr) {
+  // the select kernel's dynamic LDS limit, raised once per device (racing
+  // callers may both set it; the call is idempotent)
+  static std::atomic<uint64_t> attr_set{0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return FATHOM_ERR_HIP;
+  const uint64_t bit = dev < 64 ? 1ull << dev : 0ull;
+  if (!bit || !(attr_set.load(std::memory_order_acquire) & bit)) {
     if (hipFuncSetAttribute(reinterpret_cast<const void*>(&fused_select_kernel),
                             hipFuncAttributeMaxDynamicSharedMemorySize, kSelCap * 8) != hipSuccess)
       return FATHOM_ERR_HIP;
-    attr = true;
+    attr_set.fetch_or(bit, std::memory_order_release);
   }
   FusedArgs fa;
   fa.planes = planes;
