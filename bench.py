@@ -256,6 +256,31 @@ def main():
     scan_ms = float(np.mean([a.elapsed_time(b) for a, b in sev]))
     st_gbps = alg_bytes / (st_ms * 1e-3) / 1e9
 
+    # ---- decode-time append of one token per unit: n - 1 -> n re-packs each
+    # unit's last block from the fp16 rows (after every scan measurement above)
+    n_prev = (n - 1).clamp(min=0)
+    aev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+    for r in range(reps):
+        aev[r][0].record(stream)
+        F.fathom_pack_append(K16, n_prev, n, 1, planes[r % R], scales[r % R], st)
+        aev[r][1].record(stream)
+    torch.cuda.synchronize()
+    append_ms = float(np.median([a_.elapsed_time(b_) for a_, b_ in aev]))
+
+    # ---- a streaming-read reference on the same GPU: torch's sum over 2 GiB
+    big = torch.ones((1 << 29,), dtype=torch.float32, device=dev)
+    big.sum()
+    torch.cuda.synchronize()
+    rev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(5)]
+    for a_, b_ in rev:
+        a_.record(stream)
+        big.sum()
+        b_.record(stream)
+    torch.cuda.synchronize()
+    stream_gbps = big.numel() * 4 / (float(np.median([a_.elapsed_time(b_) for a_, b_ in rev])) * 1e-3) / 1e9
+    del big
+    torch.cuda.empty_cache()
+
     keys = float(nh.sum())
     res = {
         "metric": METRIC,
@@ -277,8 +302,11 @@ def main():
         "hbm_gbps": alg_bytes / (scan_topk_ms * 1e-3) / 1e9,
         "hbm_frac": alg_bytes / (scan_topk_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS,
         "step_keys_per_s": keys / (ms_per_step * 1e-3),
+        "scored_pairs_per_s": G * keys / (scan_topk_ms * 1e-3),
+        "stream_read_gbps": stream_gbps,
+        "hbm_frac_of_stream_read": alg_bytes / (scan_topk_ms * 1e-3) / 1e9 / stream_gbps,
         "stages_ms": {"alloc+scan_topk": scan_topk_ms, "sparse_attn": attn_ms, "scan_topk_call": st_ms,
-                      "exact_scan_kernel": scan_ms,
+                      "exact_scan_kernel": scan_ms, "pack_append_1_token_per_unit": append_ms,
                       "prefill_pack_per_store": pack_ms},
         "prefill_pack_gbps": pack_bytes / (pack_ms * 1e-3) / 1e9,
         "active_channels_mean": active,

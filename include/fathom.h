@@ -89,6 +89,30 @@ fathom_status fathom_pack(const void* K, fathom_dtype kdt, int64_t ld_tok, int64
                           uint16_t* scales, uint32_t* dev_status, void* stream);
 
 /*
+ * fathom_pack_append -- decode-time growth of a store built by fathom_pack
+ * (Sec. 3.2, Eq. (2) applied to a growing cache).  Every unit grows from
+ * n_old[u] to n[u] tokens.  A block's fp16 scale depends on all of its tokens,
+ * so blocks floor(n_old/64) .. ceil(n/64)-1 are re-packed from K (the last
+ * partial block together with the new tokens; only those rows are read).
+ * Afterwards the store equals fathom_pack of the first n[u] tokens, bit for
+ * bit, provided it held fathom_pack of the first n_old[u] (or earlier appends
+ * reaching n_old[u]).  Blocks past ceil(n/64) are not written.
+ *
+ *   K, ld_tok, ld_unit, kdt, nb_cap, planes, scales: as fathom_pack; rows
+ *            [64 floor(n_old/64), n) of each unit must hold its keys.
+ *   n_old    [U] int64 (device): tokens already in the store.
+ *   n        [U] int64 (device): tokens after the append.
+ *   max_new  host bound on n[u] - n_old[u] over all units; sizes the launch.
+ * Device status: BAD_N (n outside [0, 64 nb_cap], n_old outside [0, n], or
+ * more new blocks than max_new allows: that unit is left unchanged),
+ * SCALE_OVERFLOW, NONFINITE.
+ */
+fathom_status fathom_pack_append(const void* K, fathom_dtype kdt, int64_t ld_tok, int64_t ld_unit,
+                                 const int64_t* n_old, const int64_t* n, int64_t max_new, int U, int D,
+                                 int64_t nb_cap, uint64_t* planes, uint16_t* scales, uint32_t* dev_status,
+                                 void* stream);
+
+/*
  * fathom_alloc_depths -- Sec. 3.3, Eq. (g) and Eq. (wf): the per-query read
  * depth of every channel, shared by the G query heads of a unit.
  *

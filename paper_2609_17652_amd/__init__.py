@@ -36,7 +36,7 @@ FATHOM_DEV_TOPK_SHORT = 8
 FATHOM_DEV_BAD_N = 16
 
 EXPORTED = (
-    "fathom_pack", "fathom_alloc_depths", "fathom_scan", "fathom_topk", "fathom_topk_workspace_size",
+    "fathom_pack", "fathom_pack_append", "fathom_alloc_depths", "fathom_scan", "fathom_topk", "fathom_topk_workspace_size",
     "fathom_scan_topk", "fathom_scan_topk_ex", "fathom_scan_topk_workspace_size", "fathom_sparse_attn",
     "fathom_sparse_attn_workspace_size", "fathom_status_string", "fathom_version",
 )
@@ -63,6 +63,7 @@ def lib() -> C.CDLL:
         P, i64, i32, st = C.c_void_p, C.c_int64, C.c_int, C.c_int
         sig = {
             "fathom_pack": [P, i32, i64, i64, P, i32, i32, i64, P, P, P, P],
+            "fathom_pack_append": [P, i32, i64, i64, P, P, i64, i32, i32, i64, P, P, P, P],
             "fathom_alloc_depths": [P, i32, i32, i32, i32, P, i32, i32, P, P, P, P],
             "fathom_scan": [P, P, P, i32, i32, i64, P, i32, i32, P, P, i64, P, P],
             "fathom_topk": [P, i64, P, i32, i32, i32, i64, i64, P, P, P, C.c_size_t, P, P],
@@ -145,6 +146,20 @@ def fathom_pack(K, n, nb_cap=None, planes=None, scales=None, dev_status=None, st
         scales = torch.empty((U, D, nb_cap), dtype=torch.int16, device=K.device)
     _check(lib().fathom_pack(_p(K), _dt(K), K.stride(1), K.stride(0), _p(n), U, D, nb_cap, _p(planes), _p(scales),
                              _p(dev_status), _stream(stream)), "fathom_pack")
+    return planes, scales
+
+
+def fathom_pack_append(K, n_old, n, max_new, planes, scales, dev_status=None, stream=None):
+    """Sec. 3.2 on a growing cache: re-packs, per unit, blocks floor(n_old/64) .. ceil(n/64)-1 of
+    (planes, scales) from K [U][>= n][D]; afterwards they equal fathom_pack of the first n tokens."""
+    _dev(K, n_old, n, planes, scales)
+    U, _, D = K.shape
+    if K.stride(2) != 1:
+        raise ValueError("K channel stride must be 1")
+    nb_cap = planes.shape[-1]
+    _check(lib().fathom_pack_append(_p(K), _dt(K), K.stride(1), K.stride(0), _p(n_old), _p(n), int(max_new), U, D,
+                                    nb_cap, _p(planes), _p(scales), _p(dev_status), _stream(stream)),
+           "fathom_pack_append")
     return planes, scales
 
 

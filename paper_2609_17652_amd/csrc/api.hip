@@ -3,8 +3,8 @@
 #include "common.hpp"
 
 namespace fathom {
-fathom_status launch_pack(const void*, fathom_dtype, int64_t, int64_t, const int64_t*, int, int64_t, uint64_t*,
-                          uint16_t*, uint32_t*, hipStream_t);
+fathom_status launch_pack(const void*, fathom_dtype, int64_t, int64_t, const int64_t*, const int64_t*, int64_t, int,
+                          int64_t, uint64_t*, uint16_t*, uint32_t*, hipStream_t);
 fathom_status launch_alloc(const void*, fathom_dtype, int, int, const float*, fathom_mode, int, uint8_t*, float*,
                            uint32_t*, hipStream_t);
 fathom_status launch_scan(const uint64_t*, const uint16_t*, const int64_t*, int, int64_t, const void*,
@@ -82,7 +82,26 @@ fathom_status fathom_pack(const void* K, fathom_dtype kdt, int64_t ld_tok, int64
   const int64_t vec = 16 / (int64_t)dtype_size(kdt);  // elements per 16-byte load
   if (ld_tok < D || ld_tok % vec || ld_unit < 0 || ld_unit % vec) return FATHOM_ERR_INVALID;
   if (!aligned(K, 16) || !aligned(planes, 8) || !aligned(scales, 2) || !aligned(n, 8)) return FATHOM_ERR_INVALID;
-  return launch_pack(K, kdt, ld_tok, ld_unit, n, U, nb_cap, planes, scales, dev_status, as_stream(stream));
+  return launch_pack(K, kdt, ld_tok, ld_unit, n, nullptr, 0, U, nb_cap, planes, scales, dev_status,
+                     as_stream(stream));
+}
+
+fathom_status fathom_pack_append(const void* K, fathom_dtype kdt, int64_t ld_tok, int64_t ld_unit,
+                                 const int64_t* n_old, const int64_t* n, int64_t max_new, int U, int D,
+                                 int64_t nb_cap, uint64_t* planes, uint16_t* scales, uint32_t* dev_status,
+                                 void* stream) {
+  if (U < 0 || nb_cap < 0 || max_new < 0) return FATHOM_ERR_INVALID;
+  if (D != kD) return FATHOM_ERR_UNSUPPORTED;
+  if (!dtype_ok(kdt)) return FATHOM_ERR_UNSUPPORTED;
+  if (nb_cap > ((int64_t)1 << 25)) return FATHOM_ERR_UNSUPPORTED;
+  if (U == 0 || nb_cap == 0) return FATHOM_OK;
+  if (!K || !n || !n_old || !planes || !scales) return FATHOM_ERR_INVALID;
+  const int64_t vec = 16 / (int64_t)dtype_size(kdt);
+  if (ld_tok < D || ld_tok % vec || ld_unit < 0 || ld_unit % vec) return FATHOM_ERR_INVALID;
+  if (!aligned(K, 16) || !aligned(planes, 8) || !aligned(scales, 2) || !aligned(n, 8) || !aligned(n_old, 8))
+    return FATHOM_ERR_INVALID;
+  return launch_pack(K, kdt, ld_tok, ld_unit, n, n_old, max_new, U, nb_cap, planes, scales, dev_status,
+                     as_stream(stream));
 }
 
 fathom_status fathom_alloc_depths(const void* q, fathom_dtype qdt, int U, int G, int D, const float* var,

@@ -9,6 +9,11 @@
 // multiples of the cell width give the code, and four ballots give the plane
 // words (ballot bit i = lane i = token 64b + i).  Words and scales collect in
 // LDS and leave as contiguous runs of kBlocksPerWG words per (channel, plane).
+//
+// Append (n_old given): a block's fp16 scale depends on every token in it, so
+// a unit growing from n_old to n tokens re-packs blocks floor(n_old/64) ..
+// ceil(n/64)-1 from the keys (the last partial block together with the new
+// tokens); the grid then covers at most max_blocks blocks per unit.
 #include "common.hpp"
 
 namespace fathom {
@@ -20,6 +25,7 @@ constexpr int kTilePitch = kD + 1;
 template <typename KT>
 __global__ __launch_bounds__(kPackThreads) void pack_kernel(const KT* __restrict__ K, int64_t ld_tok,
                                                            int64_t ld_unit, const int64_t* __restrict__ n,
+                                                           const int64_t* __restrict__ n_old, int64_t max_blocks,
                                                            int64_t nb_cap, uint64_t* __restrict__ planes,
                                                            uint16_t* __restrict__ scales,
                                                            uint32_t* __restrict__ st) {
@@ -29,14 +35,27 @@ __global__ __launch_bounds__(kPackThreads) void pack_kernel(const KT* __restrict
 
   const int u = blockIdx.y;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int64_t b0 = (int64_t)blockIdx.x * kBlocksPerWG;
   const int64_t nu = unit_tokens(n, u, nb_cap * kBlockTokens, tid == 0 ? st : nullptr);
+  // blocks [bs, be) of this unit are written: all of them, or (append) the
+  // ones from the first block holding a new token
+  int64_t bs = 0, be = nb_cap;
+  if (n_old) {
+    const int64_t no = n_old[u];
+    if (no < 0 || no > nu || (nu + kBlockTokens - 1) / kBlockTokens - no / kBlockTokens > max_blocks) {
+      if (tid == 0) set_status(st, FATHOM_DEV_BAD_N);
+      return;  // the unit is left as it was
+    }
+    bs = no / kBlockTokens;
+    be = (nu + kBlockTokens - 1) / kBlockTokens;
+  }
+  const int64_t b0 = bs + (int64_t)blockIdx.x * kBlocksPerWG;
+  if (b0 >= be) return;
   const KT* Ku = K + (int64_t)u * ld_unit;
   uint32_t flags = 0;
 
   for (int bb = 0; bb < kBlocksPerWG; ++bb) {
     const int64_t b = b0 + bb;
-    if (b >= nb_cap) break;
+    if (b >= be) break;
     const int64_t tok0 = b * kBlockTokens;
     // ---- stage the 64 x 128 tile (invalid rows as zeros) ----
     if constexpr (sizeof(KT) == 4) {
@@ -106,7 +125,7 @@ __global__ __launch_bounds__(kPackThreads) void pack_kernel(const KT* __restrict
     __syncthreads();
   }
   // ---- contiguous runs of kBlocksPerWG words per (channel, plane) ----
-  const int64_t nbw = nb_cap - b0 < kBlocksPerWG ? nb_cap - b0 : kBlocksPerWG;
+  const int64_t nbw = be - b0 < kBlocksPerWG ? be - b0 : kBlocksPerWG;
   uint64_t* Pu = planes + (int64_t)u * kD * kPlanes * nb_cap;
   for (int w = tid; w < kD * kPlanes * kBlocksPerWG; w += kPackThreads) {
     const int row = w / kBlocksPerWG, e = w % kBlocksPerWG;
@@ -128,16 +147,22 @@ __global__ __launch_bounds__(kPackThreads) void pack_kernel(const KT* __restrict
 }
 
 fathom_status launch_pack(const void* K, fathom_dtype kdt, int64_t ld_tok, int64_t ld_unit,
-                          const int64_t* n, int U, int64_t nb_cap, uint64_t* planes,
-                          uint16_t* scales, uint32_t* st, hipStream_t s) {
+                          const int64_t* n, const int64_t* n_old, int64_t max_new, int U, int64_t nb_cap,
+                          uint64_t* planes, uint16_t* scales, uint32_t* st, hipStream_t s) {
   if (U == 0 || nb_cap == 0) return FATHOM_OK;
-  dim3 grid((unsigned)((nb_cap + kBlocksPerWG - 1) / kBlocksPerWG), (unsigned)U);
+  // append: new tokens span at most ceil(max_new / 64) + 1 blocks per unit
+  int64_t mb = nb_cap;
+  if (n_old) {
+    mb = (max_new + kBlockTokens - 1) / kBlockTokens + 1;
+    if (mb > nb_cap) mb = nb_cap;
+  }
+  dim3 grid((unsigned)((mb + kBlocksPerWG - 1) / kBlocksPerWG), (unsigned)U);
   if (kdt == FATHOM_F32)
     hipLaunchKernelGGL(pack_kernel<float>, grid, dim3(kPackThreads), 0, s,
-                       reinterpret_cast<const float*>(K), ld_tok, ld_unit, n, nb_cap, planes, scales, st);
+                       reinterpret_cast<const float*>(K), ld_tok, ld_unit, n, n_old, mb, nb_cap, planes, scales, st);
   else
     hipLaunchKernelGGL(pack_kernel<__half>, grid, dim3(kPackThreads), 0, s,
-                       reinterpret_cast<const __half*>(K), ld_tok, ld_unit, n, nb_cap, planes, scales, st);
+                       reinterpret_cast<const __half*>(K), ld_tok, ld_unit, n, n_old, mb, nb_cap, planes, scales, st);
   FATHOM_LAUNCH_CHECK();
   return FATHOM_OK;
 }

@@ -82,6 +82,13 @@ def test_host_validation(fl):
     assert L.fathom_pack(FAKE, 0, 100, 0, FAKE, 1, 128, 1, FAKE, FAKE, NULL, S) == fl.FATHOM_ERR_INVALID
     assert L.fathom_pack(FAKE, 0, 130, 0, FAKE, 1, 128, 1, FAKE, FAKE, NULL, S) == fl.FATHOM_ERR_INVALID
     assert L.fathom_pack(NULL, 0, 128, 0, NULL, 0, 128, 1, NULL, NULL, NULL, S) == fl.FATHOM_OK  # U = 0: no-op
+    # pack_append: as pack, plus n_old and a non-negative bound on new tokens
+    assert L.fathom_pack_append(FAKE, 0, 128, 0, NULL, FAKE, 1, 1, 128, 1, FAKE, FAKE, NULL, S) == fl.FATHOM_ERR_INVALID
+    assert L.fathom_pack_append(FAKE, 0, 128, 0, FAKE, FAKE, -1, 1, 128, 1, FAKE, FAKE, NULL, S) == fl.FATHOM_ERR_INVALID
+    assert L.fathom_pack_append(FAKE, 0, 128, 0, FAKE, FAKE, 1, 1, 64, 1, FAKE, FAKE, NULL, S) == fl.FATHOM_ERR_UNSUPPORTED
+    assert L.fathom_pack_append(FAKE, 0, 128, 0, C.c_void_p(0x1004), FAKE, 1, 1, 128, 1, FAKE, FAKE, NULL,
+                                S) == fl.FATHOM_ERR_INVALID
+    assert L.fathom_pack_append(NULL, 0, 128, 0, NULL, NULL, 1, 0, 128, 1, NULL, NULL, NULL, S) == fl.FATHOM_OK
     # alloc: budget / r range, G range, mode
     assert L.fathom_alloc_depths(FAKE, 0, 1, 4, 128, FAKE, 0, 513, FAKE, NULL, NULL, S) == fl.FATHOM_ERR_RANGE
     assert L.fathom_alloc_depths(FAKE, 0, 1, 4, 128, FAKE, 0, -1, FAKE, NULL, NULL, S) == fl.FATHOM_ERR_RANGE

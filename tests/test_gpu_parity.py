@@ -76,6 +76,62 @@ def test_pack_ragged_units(kdt):
         assert np.array_equal(Sc[u], os_), f"scales unit {u} n={n}"
 
 
+@pytest.mark.parametrize("kdt", [np.float32, np.float16])
+def test_pack_append_equals_full_pack(kdt):
+    """Decode-time growth: a store packed at n_old and grown by fathom_pack_append
+    equals the oracle's pack of the longer prefix bit for bit after every step --
+    one-token steps across block boundaries, multi-block jumps, a no-op, three
+    units with different lengths in each launch."""
+    rng = np.random.default_rng(81)
+    nmax = 1000
+    nb_cap = (nmax + 63) // 64 + 1
+    lens = [[0, 1, 2, 63, 64, 65, 128, 1000],
+            [100, 100, 129, 191, 192, 193, 700, 701],
+            [640, 641, 642, 700, 768, 769, 770, 1000]]
+    U = len(lens)
+    K = np.zeros((U, nmax, 128), kdt)
+    for u in range(U):
+        K[u] = special_keys(rng, nmax, kdt)
+    Kt = torch.from_numpy(K).to(DEV)
+    st = F.new_status()
+    n0 = torch.tensor([l[0] for l in lens], dtype=torch.int64, device=DEV)
+    planes, scales = F.fathom_pack(Kt, n0, nb_cap=nb_cap, dev_status=st)
+    for step in range(1, len(lens[0])):
+        no = torch.tensor([l[step - 1] for l in lens], dtype=torch.int64, device=DEV)
+        nn = torch.tensor([l[step] for l in lens], dtype=torch.int64, device=DEV)
+        max_new = max(l[step] - l[step - 1] for l in lens)
+        F.fathom_pack_append(Kt, no, nn, max_new, planes, scales, dev_status=st)
+        assert status(st) == 0
+        P, Sc = u64(planes), u16(scales)
+        for u in range(U):
+            n = lens[u][step]
+            op, os_, _ = oracle.pack(K[u, :n].astype(np.float32), nb_cap=nb_cap)
+            assert np.array_equal(P[u], op), f"planes unit {u} n={n}"
+            assert np.array_equal(Sc[u], os_), f"scales unit {u} n={n}"
+
+
+def test_pack_append_rejects_bad_lengths():
+    """A unit whose new blocks exceed the caller's max_new bound, or whose n_old
+    exceeds n, is left unchanged and flags BAD_N; the other units still grow."""
+    rng = np.random.default_rng(82)
+    nmax, nb_cap = 600, 10
+    K = np.stack([special_keys(rng, nmax) for _ in range(3)])
+    Kt = torch.from_numpy(K).to(DEV)
+    st = F.new_status()
+    planes, scales = F.fathom_pack(Kt, torch.tensor([100, 100, 300], dtype=torch.int64, device=DEV),
+                                   nb_cap=nb_cap, dev_status=st)
+    before = (u64(planes).copy(), u16(scales).copy())
+    no = torch.tensor([100, 100, 300], dtype=torch.int64, device=DEV)
+    nn = torch.tensor([130, 600, 200], dtype=torch.int64, device=DEV)  # unit 1: 500 new > bound; unit 2: shrinks
+    F.fathom_pack_append(Kt, no, nn, 30, planes, scales, dev_status=st)
+    assert status(st) == F.FATHOM_DEV_BAD_N
+    P, Sc = u64(planes), u16(scales)
+    op, os_, _ = oracle.pack(K[0, :130], nb_cap=nb_cap)
+    assert np.array_equal(P[0], op) and np.array_equal(Sc[0], os_)
+    for u in (1, 2):
+        assert np.array_equal(P[u], before[0][u]) and np.array_equal(Sc[u], before[1][u]), u
+
+
 def test_pack_flags_overflow_nan():
     K = np.random.default_rng(3).standard_normal((2, 200, 128)).astype(np.float32)
     K[0, 70, 3] = 70000.0  # block 1 of channel 3 overflows fp16
