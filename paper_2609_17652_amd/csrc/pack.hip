@@ -13,7 +13,9 @@
 // Append (n_old given): a block's fp16 scale depends on every token in it, so
 // a unit growing from n_old to n tokens re-packs blocks floor(n_old/64) ..
 // ceil(n/64)-1 from the keys (the last partial block together with the new
-// tokens); the grid then covers at most max_blocks blocks per unit.
+// tokens); the grid then covers at most max_blocks blocks per unit, and the
+// 128 channels are split over kAppendGroups workgroups (blockIdx.z): an
+// append packs few blocks, so its time is one workgroup's channel loop.
 #include "common.hpp"
 
 namespace fathom {
@@ -21,6 +23,7 @@ namespace fathom {
 constexpr int kPackThreads = 256;
 constexpr int kBlocksPerWG = 4;
 constexpr int kTilePitch = kD + 1;
+constexpr int kAppendGroups = 16;
 
 template <typename KT>
 __global__ __launch_bounds__(kPackThreads) void pack_kernel(const KT* __restrict__ K, int64_t ld_tok,
@@ -35,6 +38,8 @@ __global__ __launch_bounds__(kPackThreads) void pack_kernel(const KT* __restrict
 
   const int u = blockIdx.y;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // channels [c0, c0 + cpw * 4) of this workgroup, cpw per wave
+  const int ngr = (int)gridDim.z, cpw = 32 / ngr, c0 = (int)blockIdx.z * (kD / ngr);
   const int64_t nu = unit_tokens(n, u, nb_cap * kBlockTokens, tid == 0 ? st : nullptr);
   // blocks [bs, be) of this unit are written: all of them, or (append) the
   // ones from the first block holding a new token
@@ -87,8 +92,8 @@ __global__ __launch_bounds__(kPackThreads) void pack_kernel(const KT* __restrict
     __syncthreads();
     // ---- quantise: wave w owns channels 32w .. 32w+31, lane = token ----
     const bool valid = tok0 + lane < nu;
-    for (int jj = 0; jj < 32; ++jj) {
-      const int j = wave * 32 + jj;
+    for (int jj = 0; jj < cpw; ++jj) {
+      const int j = c0 + wave * cpw + jj;
       const float v = tile[lane * kTilePitch + j];
       const bool isn = v != v;
       if (valid && !(fabsf(v) <= 3.402823466e38f)) flags |= FATHOM_DEV_NONFINITE;
@@ -127,12 +132,13 @@ __global__ __launch_bounds__(kPackThreads) void pack_kernel(const KT* __restrict
   // ---- contiguous runs of kBlocksPerWG words per (channel, plane) ----
   const int64_t nbw = be - b0 < kBlocksPerWG ? be - b0 : kBlocksPerWG;
   uint64_t* Pu = planes + (int64_t)u * kD * kPlanes * nb_cap;
-  for (int w = tid; w < kD * kPlanes * kBlocksPerWG; w += kPackThreads) {
+  const int wc = kD / ngr;  // channels of this workgroup
+  for (int w = c0 * kPlanes * kBlocksPerWG + tid; w < (c0 + wc) * kPlanes * kBlocksPerWG; w += kPackThreads) {
     const int row = w / kBlocksPerWG, e = w % kBlocksPerWG;
     if (e < nbw) Pu[(int64_t)row * nb_cap + b0 + e] = outw[w];
   }
   uint16_t* Su = scales + (int64_t)u * kD * nb_cap;
-  for (int w = tid; w < kD * kBlocksPerWG; w += kPackThreads) {
+  for (int w = c0 * kBlocksPerWG + tid; w < (c0 + wc) * kBlocksPerWG; w += kPackThreads) {
     const int row = w / kBlocksPerWG, e = w % kBlocksPerWG;
     if (e < nbw) Su[(int64_t)row * nb_cap + b0 + e] = outs[w];
   }
@@ -156,7 +162,7 @@ fathom_status launch_pack(const void* K, fathom_dtype kdt, int64_t ld_tok, int64
     mb = (max_new + kBlockTokens - 1) / kBlockTokens + 1;
     if (mb > nb_cap) mb = nb_cap;
   }
-  dim3 grid((unsigned)((mb + kBlocksPerWG - 1) / kBlocksPerWG), (unsigned)U);
+  dim3 grid((unsigned)((mb + kBlocksPerWG - 1) / kBlocksPerWG), (unsigned)U, n_old ? kAppendGroups : 1);
   if (kdt == FATHOM_F32)
     hipLaunchKernelGGL(pack_kernel<float>, grid, dim3(kPackThreads), 0, s,
                        reinterpret_cast<const float*>(K), ld_tok, ld_unit, n, n_old, mb, nb_cap, planes, scales, st);
