@@ -51,6 +51,8 @@ def parse():
     ap.add_argument("--cpu-units", type=int, default=4, help="units in the oracle's CPU-baseline sample")
     ap.add_argument("--traffic-calib", type=int, default=0, metavar="MIB",
                     help="end with one plain device-to-device copy of MIB MiB (counter calibration)")
+    ap.add_argument("--fidelity", action="store_true",
+                    help="attention fidelity vs dense at equal bytes (water-filling vs uniform depth), then exit")
     ap.add_argument("--traffic-summary", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="write the HBM-traffic summary from two rocprofv3 --pmc counter files and exit")
     return ap.parse_args()
@@ -147,8 +149,49 @@ def measured_traffic():
     return t["bytes_per_call"] if t.get("source_sha256") == kernel_source_hash() else None
 
 
+def fidelity(dev="cuda:0"):
+    """Relative L2 error of top-k sparse attention against dense attention (fp32,
+    all n keys), per (unit, head), on one 8-KV-head layer at n = 131072, k = 1024
+    (Sec. 4's measure of what the selection keeps): water-filled depths at
+    B code bits per key against the uniform top-r rule at the same bytes
+    (4 r = B), and top-k by exact fp32 q.k as the selection's bound."""
+    cfg = synth.WORKLOADS["layer128k"]
+    data = synth.device_units(cfg, with_values=True)
+    K, V, q, var, n = data["K"], data["V"], data["q"], data["var"], data["n"]
+    U, N, D = K.shape
+    G = q.shape[1]
+    k = cfg.k
+    sm = 1.0 / float(np.sqrt(D))
+    K16, qf = K.half(), q.float()
+    Kd, Vd = K16.float(), V.float()
+    logits = torch.matmul(qf, Kd.transpose(1, 2).contiguous()) * sm          # [U][G][N]
+    dense = torch.matmul(torch.softmax(logits, dim=-1), Vd)                   # [U][G][D]
+
+    def err(idx):
+        o = F.fathom_sparse_attn(q, K16, V, n, idx)
+        return (torch.linalg.vector_norm(o - dense, dim=-1) / torch.linalg.vector_norm(dense, dim=-1)).cpu()
+
+    planes, scales = F.fathom_pack(K, n)
+    rows = {}
+    for B in (32, 48, 80):
+        for name, mode, arg in (("waterfill", F.FATHOM_WATERFILL, B), ("uniform", F.FATHOM_UNIFORM_TOPR, B // 4)):
+            d, _ = F.fathom_alloc_depths(q, var, mode, arg)
+            idx, _ = F.fathom_scan_topk(planes, scales, n, q, d, k)
+            e = err(idx)
+            rows[f"{name}_B{B}"] = {"mean": float(e.mean()), "max": float(e.max())}
+    exact = torch.topk(torch.matmul(qf, K.transpose(1, 2).contiguous()), k, dim=-1).indices.int()
+    e = err(exact)
+    rows["exact_topk"] = {"mean": float(e.mean()), "max": float(e.max())}
+    return {"fidelity": "relative L2 of sparse vs dense attention output, per (unit, head)",
+            "workload": cfg.name, "k": k, "results": rows}
+
+
 def main():
     args = parse()
+    if args.fidelity:
+        torch.cuda.set_device(0)
+        print(json.dumps(fidelity()), flush=True)
+        return
     if args.traffic_summary:
         t = traffic_summary(args.traffic_summary[0], args.traffic_summary[1], args.traffic_calib or 256)
         with open(TRAFFIC_JSON, "w") as fh:
