@@ -310,6 +310,26 @@ def main():
     torch.cuda.synchronize()
     append_ms = float(np.median([a_.elapsed_time(b_) for a_, b_ in aev]))
 
+    # ---- host-resident store (Sec. 3.6): one step's rows gathered from pinned
+    # host memory into a device store (reported beside the metric, never in it)
+    hp = torch.empty(planes[0].shape, dtype=planes[0].dtype, pin_memory=True)
+    hs = torch.empty(scales[0].shape, dtype=scales[0].dtype, pin_memory=True)
+    hp.copy_(planes[0])
+    hs.copy_(scales[0])
+    gp, gs = torch.empty_like(planes[0]), torch.empty_like(scales[0])
+    F.fathom_gather_store(hp, hs, d, gp, gs)
+    torch.cuda.synchronize()
+    gev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(5)]
+    for a_, b_ in gev:
+        a_.record(stream)
+        F.fathom_gather_store(hp, hs, d, gp, gs)
+        b_.record(stream)
+    torch.cuda.synchronize()
+    gather_ms = float(np.median([a_.elapsed_time(b_) for a_, b_ in gev]))
+    tcl = np.minimum(dn, 4)
+    gather_bytes = float(tcl.sum() * nb_cap * 8 + (tcl > 0).sum() * nb_cap * 2)
+    del hp, hs, gp, gs
+
     # ---- a streaming-read reference on the same GPU: torch's sum over 2 GiB
     big = torch.ones((1 << 29,), dtype=torch.float32, device=dev)
     big.sum()
@@ -347,9 +367,12 @@ def main():
         "step_keys_per_s": keys / (ms_per_step * 1e-3),
         "scored_pairs_per_s": G * keys / (scan_topk_ms * 1e-3),
         "stream_read_gbps": stream_gbps,
+        "gather_host_store_gbps": gather_bytes / (gather_ms * 1e-3) / 1e9,
+        "gather_host_store_bytes": gather_bytes,
         "hbm_frac_of_stream_read": alg_bytes / (scan_topk_ms * 1e-3) / 1e9 / stream_gbps,
         "stages_ms": {"alloc+scan_topk": scan_topk_ms, "sparse_attn": attn_ms, "scan_topk_call": st_ms,
                       "exact_scan_kernel": scan_ms, "pack_append_1_token_per_unit": append_ms,
+                      "gather_host_store": gather_ms,
                       "prefill_pack_per_store": pack_ms},
         "prefill_pack_gbps": pack_bytes / (pack_ms * 1e-3) / 1e9,
         "active_channels_mean": active,

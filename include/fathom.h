@@ -113,6 +113,26 @@ fathom_status fathom_pack_append(const void* K, fathom_dtype kdt, int64_t ld_tok
                                  void* stream);
 
 /*
+ * fathom_gather_store -- Sec. 3.6 (host-resident store): per decode step only
+ * the bytes the depths read cross the host link.  For every unit u and channel
+ * j with t = min(depths[u][j], 4) > 0, copies planes[u][j][0..t-1][*] (one
+ * contiguous run) and scales[u][j][*] from the host store to the device store
+ * of the same shape; other rows of the device store are not written.  A scan
+ * over the device store then reads exactly what it would read from the full
+ * store, so fathom_scan / fathom_scan_topk results are unchanged.
+ *
+ *   host_planes  [U][D][4][nb_cap] uint64, host_scales [U][D][nb_cap] uint16:
+ *                pinned host memory (hipHostMalloc; torch pin_memory), the
+ *                bases 16-byte aligned.  Other host memory: FATHOM_ERR_INVALID.
+ *   depths       [U][D] uint8 (device).
+ *   planes, scales  the device store (device, 16-byte aligned, written).
+ * Device status: none.
+ */
+fathom_status fathom_gather_store(const uint64_t* host_planes, const uint16_t* host_scales,
+                                  const uint8_t* depths, int U, int D, int64_t nb_cap,
+                                  uint64_t* planes, uint16_t* scales, void* stream);
+
+/*
  * fathom_alloc_depths -- Sec. 3.3, Eq. (g) and Eq. (wf): the per-query read
  * depth of every channel, shared by the G query heads of a unit.
  *

@@ -36,7 +36,7 @@ FATHOM_DEV_TOPK_SHORT = 8
 FATHOM_DEV_BAD_N = 16
 
 EXPORTED = (
-    "fathom_pack", "fathom_pack_append", "fathom_alloc_depths", "fathom_scan", "fathom_topk", "fathom_topk_workspace_size",
+    "fathom_pack", "fathom_pack_append", "fathom_gather_store", "fathom_alloc_depths", "fathom_scan", "fathom_topk", "fathom_topk_workspace_size",
     "fathom_scan_topk", "fathom_scan_topk_ex", "fathom_scan_topk_workspace_size", "fathom_sparse_attn",
     "fathom_sparse_attn_workspace_size", "fathom_status_string", "fathom_version",
 )
@@ -64,6 +64,7 @@ def lib() -> C.CDLL:
         sig = {
             "fathom_pack": [P, i32, i64, i64, P, i32, i32, i64, P, P, P, P],
             "fathom_pack_append": [P, i32, i64, i64, P, P, i64, i32, i32, i64, P, P, P, P],
+            "fathom_gather_store": [P, P, P, i32, i32, i64, P, P, P],
             "fathom_alloc_depths": [P, i32, i32, i32, i32, P, i32, i32, P, P, P, P],
             "fathom_scan": [P, P, P, i32, i32, i64, P, i32, i32, P, P, i64, P, P],
             "fathom_topk": [P, i64, P, i32, i32, i32, i64, i64, P, P, P, C.c_size_t, P, P],
@@ -160,6 +161,19 @@ def fathom_pack_append(K, n_old, n, max_new, planes, scales, dev_status=None, st
     _check(lib().fathom_pack_append(_p(K), _dt(K), K.stride(1), K.stride(0), _p(n_old), _p(n), int(max_new), U, D,
                                     nb_cap, _p(planes), _p(scales), _p(dev_status), _stream(stream)),
            "fathom_pack_append")
+    return planes, scales
+
+
+def fathom_gather_store(host_planes, host_scales, depths, planes, scales, stream=None):
+    """Sec. 3.6: copy the rows the depths read from a pinned host store into the device store."""
+    if not (host_planes.is_pinned() and host_scales.is_pinned()):
+        raise ValueError("the host store must be pinned host memory")
+    _dev(depths, planes, scales)
+    U, D, _, nb_cap = planes.shape
+    if tuple(host_planes.shape) != tuple(planes.shape) or tuple(host_scales.shape) != tuple(scales.shape):
+        raise ValueError("host and device stores must have the same shape")
+    _check(lib().fathom_gather_store(_p(host_planes), _p(host_scales), _p(depths), U, D, nb_cap, _p(planes),
+                                     _p(scales), _stream(stream)), "fathom_gather_store")
     return planes, scales
 
 

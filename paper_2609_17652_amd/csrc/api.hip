@@ -3,6 +3,8 @@
 #include "common.hpp"
 
 namespace fathom {
+fathom_status launch_gather(const uint64_t*, const uint16_t*, const uint8_t*, int, int64_t, uint64_t*, uint16_t*,
+                            hipStream_t);
 fathom_status launch_pack(const void*, fathom_dtype, int64_t, int64_t, const int64_t*, const int64_t*, int64_t, int,
                           int64_t, uint64_t*, uint16_t*, uint32_t*, hipStream_t);
 fathom_status launch_alloc(const void*, fathom_dtype, int, int, const float*, fathom_mode, int, uint8_t*, float*,
@@ -102,6 +104,18 @@ fathom_status fathom_pack_append(const void* K, fathom_dtype kdt, int64_t ld_tok
     return FATHOM_ERR_INVALID;
   return launch_pack(K, kdt, ld_tok, ld_unit, n, n_old, max_new, U, nb_cap, planes, scales, dev_status,
                      as_stream(stream));
+}
+
+fathom_status fathom_gather_store(const uint64_t* host_planes, const uint16_t* host_scales, const uint8_t* depths,
+                                 int U, int D, int64_t nb_cap, uint64_t* planes, uint16_t* scales, void* stream) {
+  if (U < 0 || nb_cap < 0) return FATHOM_ERR_INVALID;
+  if (D != kD) return FATHOM_ERR_UNSUPPORTED;
+  if (nb_cap > ((int64_t)1 << 25)) return FATHOM_ERR_UNSUPPORTED;
+  if (U == 0 || nb_cap == 0) return FATHOM_OK;
+  if (!host_planes || !host_scales || !depths || !planes || !scales) return FATHOM_ERR_INVALID;
+  if (!aligned(host_planes, 16) || !aligned(planes, 16) || !aligned(host_scales, 16) || !aligned(scales, 16))
+    return FATHOM_ERR_INVALID;
+  return launch_gather(host_planes, host_scales, depths, U, nb_cap, planes, scales, as_stream(stream));
 }
 
 fathom_status fathom_alloc_depths(const void* q, fathom_dtype qdt, int U, int G, int D, const float* var,

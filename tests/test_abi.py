@@ -82,6 +82,11 @@ def test_host_validation(fl):
     assert L.fathom_pack(FAKE, 0, 100, 0, FAKE, 1, 128, 1, FAKE, FAKE, NULL, S) == fl.FATHOM_ERR_INVALID
     assert L.fathom_pack(FAKE, 0, 130, 0, FAKE, 1, 128, 1, FAKE, FAKE, NULL, S) == fl.FATHOM_ERR_INVALID
     assert L.fathom_pack(NULL, 0, 128, 0, NULL, 0, 128, 1, NULL, NULL, NULL, S) == fl.FATHOM_OK  # U = 0: no-op
+    # gather_store: D, null pointers, misaligned bases (rejected before any HIP call)
+    assert L.fathom_gather_store(FAKE, FAKE, FAKE, 1, 64, 1, FAKE, FAKE, S) == fl.FATHOM_ERR_UNSUPPORTED
+    assert L.fathom_gather_store(NULL, FAKE, FAKE, 1, 128, 1, FAKE, FAKE, S) == fl.FATHOM_ERR_INVALID
+    assert L.fathom_gather_store(C.c_void_p(0x1008), FAKE, FAKE, 1, 128, 1, FAKE, FAKE, S) == fl.FATHOM_ERR_INVALID
+    assert L.fathom_gather_store(NULL, NULL, NULL, 0, 128, 1, NULL, NULL, S) == fl.FATHOM_OK  # U = 0: no-op
     # pack_append: as pack, plus n_old and a non-negative bound on new tokens
     assert L.fathom_pack_append(FAKE, 0, 128, 0, NULL, FAKE, 1, 1, 128, 1, FAKE, FAKE, NULL, S) == fl.FATHOM_ERR_INVALID
     assert L.fathom_pack_append(FAKE, 0, 128, 0, FAKE, FAKE, -1, 1, 128, 1, FAKE, FAKE, NULL, S) == fl.FATHOM_ERR_INVALID

@@ -693,3 +693,40 @@ def test_scan_topk_empty_and_short_rows():
     assert s & F.FATHOM_DEV_TOPK_SHORT, hex(s)
     assert s & ~(F.FATHOM_DEV_TOPK_SHORT | F.FATHOM_DEV_TOPK_FALLBACK) == 0, hex(s)
     _assert_rows_match(idx, val, planes, scales, ns, q, d, k, lo, tail)
+
+
+def test_gather_host_store_leaves_scan_topk_unchanged():
+    """Sec. 3.6: the store in pinned host memory; gathering the rows the depths
+    read into a zeroed device store copies exactly the active runs (first t
+    planes and the scales of every active channel), writes nothing else, and
+    scan_topk over it is bit-identical.  Pageable host memory is refused before
+    any launch."""
+    import ctypes as C
+    ns = [40000, 9000]  # nb_cap 625: scale rows start off 16-byte boundaries
+    K, nt, planes, scales = _store(ns, 91)
+    rng = np.random.default_rng(92)
+    q = torch.from_numpy(rng.standard_normal((len(ns), 4, 128)).astype(np.float16)).to(DEV)
+    var = torch.from_numpy(np.exp(rng.standard_normal((len(ns), 128))).astype(np.float32)).to(DEV)
+    d, _ = F.fathom_alloc_depths(q, var, F.FATHOM_WATERFILL, 48)
+    hp = torch.empty(planes.shape, dtype=planes.dtype, pin_memory=True)
+    hs = torch.empty(scales.shape, dtype=scales.dtype, pin_memory=True)
+    hp.copy_(planes)
+    hs.copy_(scales)
+    gp, gs = torch.zeros_like(planes), torch.zeros_like(scales)
+    F.fathom_gather_store(hp, hs, d, gp, gs)
+    torch.cuda.synchronize()
+    P, Sc, GP, GS, dn = u64(planes), u16(scales), u64(gp), u16(gs), d.cpu().numpy()
+    for u in range(len(ns)):
+        for j in range(128):
+            t = min(int(dn[u, j]), 4)
+            assert np.array_equal(GP[u, j, :t], P[u, j, :t]) and not GP[u, j, t:].any(), (u, j)
+            assert np.array_equal(GS[u, j], Sc[u, j] if t else np.zeros_like(Sc[u, j])), (u, j)
+    a = F.fathom_scan_topk(planes, scales, nt, q, d, 300)
+    b = F.fathom_scan_topk(gp, gs, nt, q, d, 300)
+    assert torch.equal(a[0], b[0]) and torch.equal(a[1].view(torch.int32), b[1].view(torch.int32))
+    pageable = np.zeros(planes.numel() + 2, np.uint64)
+    p16 = pageable.ctypes.data + (-pageable.ctypes.data) % 16
+    r = F.lib().fathom_gather_store(C.c_void_p(p16), C.c_void_p(p16), C.c_void_p(d.data_ptr()), len(ns), 128,
+                                    planes.shape[-1], C.c_void_p(gp.data_ptr()), C.c_void_p(gs.data_ptr()),
+                                    C.c_void_p(torch.cuda.current_stream().cuda_stream))
+    assert r == F.FATHOM_ERR_INVALID
