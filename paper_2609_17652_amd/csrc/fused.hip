@@ -1553,12 +1553,17 @@ fathom_status launch_scan_topk_fused(const uint64_t* planes, const uint16_t* sca
   // callers may both set it; the call is idempotent)
   static std::atomic<uint64_t> attr_set{0};
   int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess) return FATHOM_ERR_HIP;
+  if (hipGetDevice(&dev) != hipSuccess) {
+    (void)hipGetLastError();
+    return FATHOM_ERR_HIP;
+  }
   const uint64_t bit = dev < 64 ? 1ull << dev : 0ull;
   if (!bit || !(attr_set.load(std::memory_order_acquire) & bit)) {
     if (hipFuncSetAttribute(reinterpret_cast<const void*>(&fused_select_kernel),
-                            hipFuncAttributeMaxDynamicSharedMemorySize, kSelCap * 8) != hipSuccess)
+                            hipFuncAttributeMaxDynamicSharedMemorySize, kSelCap * 8) != hipSuccess) {
+      (void)hipGetLastError();
       return FATHOM_ERR_HIP;
+    }
     attr_set.fetch_or(bit, std::memory_order_release);
   }
   FusedArgs fa;

@@ -50,9 +50,13 @@ fathom_status launch_gather(const uint64_t* hplanes, const uint16_t* hscales, co
   if (U == 0 || nb_cap == 0) return FATHOM_OK;
   void* dp = nullptr;
   void* ds = nullptr;
-  // pinned host memory only: anything else fails here, before a launch
-  if (hipHostGetDevicePointer(&dp, const_cast<uint64_t*>(hplanes), 0) != hipSuccess || !dp) return FATHOM_ERR_INVALID;
-  if (hipHostGetDevicePointer(&ds, const_cast<uint16_t*>(hscales), 0) != hipSuccess || !ds) return FATHOM_ERR_INVALID;
+  // pinned host memory only: anything else fails here, before a launch (the
+  // runtime's error is cleared so that it is not reported by a later call)
+  if (hipHostGetDevicePointer(&dp, const_cast<uint64_t*>(hplanes), 0) != hipSuccess || !dp ||
+      hipHostGetDevicePointer(&ds, const_cast<uint16_t*>(hscales), 0) != hipSuccess || !ds) {
+    (void)hipGetLastError();
+    return FATHOM_ERR_INVALID;
+  }
   hipLaunchKernelGGL(gather_kernel, dim3(kD, U), dim3(kGatherThreads), 0, s, static_cast<const uint64_t*>(dp),
                      static_cast<const uint16_t*>(ds), depths, nb_cap, planes, scales);
   FATHOM_LAUNCH_CHECK();

@@ -730,6 +730,8 @@ def test_gather_host_store_leaves_scan_topk_unchanged():
                                     planes.shape[-1], C.c_void_p(gp.data_ptr()), C.c_void_p(gs.data_ptr()),
                                     C.c_void_p(torch.cuda.current_stream().cuda_stream))
     assert r == F.FATHOM_ERR_INVALID
+    # the refused call leaves no error behind for the next one
+    F.fathom_pack(torch.from_numpy(K).to(DEV), nt, nb_cap=planes.shape[-1])
 
 
 def test_graph_replays_match_eager():
