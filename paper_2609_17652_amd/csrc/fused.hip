@@ -1144,7 +1144,12 @@ __global__ __launch_bounds__(kTauThreads) void fused_tau_kernel(FusedArgs a) {
   for (int o = 32; o >= 1; o >>= 1) m_s += __shfl_xor(m_s, o, kWave);
   const int64_t m_e = hi - lo;
   int64_t m = m_s > 0 ? (5 * (int64_t)a.k * m_s + 4 * m_e - 1) / (4 * m_e) + 16 : 0;
-  if (m > nv) m = nv;
+  if (m > nv) {
+    // the samples cannot reach rank m: the smallest sample is used only when
+    // the keys expected above it (nv m_e / m_s) are at least 1.1 k, else the
+    // row is left unfiltered (exact path) instead of filtered in vain
+    m = 10 * (int64_t)nv * m_e >= 11 * (int64_t)a.k * m_s ? nv : 0;
+  }
   if (m == 0) {
     if (tid == 0) a.ws.tau[r] = kNegInf;
     return;
