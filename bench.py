@@ -244,6 +244,7 @@ def main():
     val = torch.empty((U, G, k), dtype=torch.float32, device=dev)
     out = torch.empty((U, G, D), dtype=torch.float32, device=dev)
     ws = torch.empty((F.fathom_scan_topk_workspace_size(U, G, 64 * nb_cap, k),), dtype=torch.uint8, device=dev)
+    ws_attn = torch.empty((F.fathom_sparse_attn_workspace_size(U, G, k),), dtype=torch.uint8, device=dev)
 
     nev = 4
     def step(i, evs=None):
@@ -254,7 +255,7 @@ def main():
         F.fathom_scan_topk(planes[c], scales[c], n, q, d, k, 0, 0, idx, val, ws, st, max_unit_bits=max_bits)
         if evs is not None:
             evs[1].record(stream)
-        F.fathom_sparse_attn(q, K16, V, n, idx, 0, 0, None, out, st)
+        F.fathom_sparse_attn(q, K16, V, n, idx, 0, 0, None, out, st, ws=ws_attn)
         if evs is not None:
             evs[2].record(stream)
 
