@@ -15,6 +15,11 @@ Parity status per function (what pins it to the paper, in ``tests/``):
   scores_f32      within its fp32 error bound of scores_f64 (order is a reading)
   topk            brute-force sort on tiny inputs; App. A top-2 sets
   sparse_attn     k = n equals dense softmax attention; one-row set = V row
+  klt_calibrate   Hadamard-design keys with known mean and covariance give the
+                  known eigenvalues and eigenvectors (``klt.py``, Sec. 3.5)
+  klt_rotate_*    identity / permutation bases exact; fp32 error bound; q'.k'
+                  equals q.(k - mu)
 """
 from .oracle import *  # noqa: F401,F403
 from .oracle import build, lib_path  # noqa: F401
+from .klt import *  # noqa: F401,F403
