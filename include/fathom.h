@@ -251,6 +251,61 @@ fathom_status fathom_sparse_attn(const void* q, fathom_dtype qdt, const uint16_t
                                  size_t ws_bytes, uint32_t* dev_status, void* stream);
 size_t fathom_sparse_attn_workspace_size(int U, int G, int k, int n_sink, int n_local);
 
+/*
+ * KLT-rotated store -- Sec. 3.5 (basis rule).  The rotated variant of the
+ * method stores the planes of (k - mu) V instead of k, with mu the mean and V
+ * the orthonormal eigenbasis of the covariance of a unit's calibration keys,
+ * and allocates depths with g_j = sum_h ((q_h V)_j)^2 lambda_j, lambda_j the
+ * eigenvalue of column j.  Nothing else changes: pack the rotated keys with
+ * fathom_pack (fp32), pass the rotated queries and var = lambda to
+ * fathom_alloc_depths, and the rotated queries to the scan.  Scores are then
+ * q . (k - mu): per head they differ from q . k by the constant q . mu, so the
+ * top-k order is that of q . k (up to the quantisation).
+ *
+ * fathom_klt_calibrate -- per unit: mu = mean of its n[u] keys, covariance
+ * C = (1/n) sum (k - mu)(k - mu)^T (fp64 sums), and its eigen-decomposition
+ * (fp32 cyclic Jacobi, 12 sweeps).  Columns are ordered by eigenvalue,
+ * largest first (the paper orders by calibration score variance, the same
+ * order for isotropic queries); each column's largest-magnitude entry is
+ * positive.  A unit with n[u] = 0 gets mu = 0, V = I, lambda = 0.
+ *   K        [U][n][D] keys (kdt), element (u, i, c) at K[u*ld_unit + i*ld_tok + c];
+ *            ld_tok >= D, ld_unit >= 0; element-aligned.
+ *   n        [U] int64 (device), 0 <= n[u] <= n_cap, else BAD_N and the unit is empty.
+ *   mu       [U][D] fp32, V [U][D][D] fp32 (V[u][j][c]: entry j of eigenvector c),
+ *   lam      [U][D] fp32 -- written.
+ *   ws       device workspace of fathom_klt_calibrate_workspace_size(U) bytes,
+ *            256-byte aligned (chunk partial sums; contents on entry unused).
+ * One-time per store (prefill); about 4 MiB of workspace per unit.
+ */
+fathom_status fathom_klt_calibrate(const void* K, fathom_dtype kdt, int64_t ld_tok, int64_t ld_unit,
+                                   const int64_t* n, int64_t n_cap, int U, int D, float* mu, float* V,
+                                   float* lam, void* ws, size_t ws_bytes, uint32_t* dev_status, void* stream);
+size_t fathom_klt_calibrate_workspace_size(int U);
+
+/*
+ * fathom_klt_rotate_keys -- the stored coordinates (k - mu) V of every key,
+ * fp32, in a fixed order: d_j = fl(k_j - mu_j); for j = 0 .. D-1,
+ * acc_c = fl(acc_c + fl(d_j * V[j][c])) from acc_c = +0 (no fused multiply-add).
+ *   K, ld_tok, ld_unit, n, n_cap   as fathom_klt_calibrate.
+ *   mu [U][D], V [U][D][D] fp32    (from fathom_klt_calibrate or the caller).
+ *   out      [U] blocks of ld_out_unit floats (ld_out_unit >= n_cap * D): row i of
+ *            unit u at out[u*ld_out_unit + i*D]; rows i < n[u] are written, the
+ *            rest left as they were.  Pack it with fathom_pack (FATHOM_F32,
+ *            ld_tok = D, ld_unit = ld_out_unit).
+ * Device status: BAD_N.
+ */
+fathom_status fathom_klt_rotate_keys(const void* K, fathom_dtype kdt, int64_t ld_tok, int64_t ld_unit,
+                                     const int64_t* n, int64_t n_cap, int U, int D, const float* mu,
+                                     const float* V, float* out, int64_t ld_out_unit, uint32_t* dev_status,
+                                     void* stream);
+
+/*
+ * fathom_klt_rotate_q -- q_h V per (unit, head), fp32 [U][G][D], in the order of
+ * fathom_klt_rotate_keys (no mean).  q [U][G][D] (qdt), V [U][D][D] fp32.
+ */
+fathom_status fathom_klt_rotate_q(const void* q, fathom_dtype qdt, int U, int G, int D, const float* V,
+                                  float* out, void* stream);
+
 /* Human-readable name of a status code (static storage). */
 const char* fathom_status_string(fathom_status s);
 

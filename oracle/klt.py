@@ -67,7 +67,7 @@ def klt_calibrate(K: np.ndarray):
     C = (X.T @ X) / n
     lam, V = np.linalg.eigh(C)  # ascending eigenvalues, orthonormal columns
     order = np.argsort(-lam, kind="stable")
-    return mu, klt_fix_signs(V[:, order]), lam[order]
+    return mu, np.ascontiguousarray(klt_fix_signs(V[:, order])), lam[order]
 
 
 def _rotate_f32(X: np.ndarray, V: np.ndarray) -> np.ndarray:

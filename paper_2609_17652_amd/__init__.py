@@ -38,7 +38,8 @@ FATHOM_DEV_BAD_N = 16
 EXPORTED = (
     "fathom_pack", "fathom_pack_append", "fathom_gather_store", "fathom_alloc_depths", "fathom_scan", "fathom_topk", "fathom_topk_workspace_size",
     "fathom_scan_topk", "fathom_scan_topk_ex", "fathom_scan_topk_workspace_size", "fathom_sparse_attn",
-    "fathom_sparse_attn_workspace_size", "fathom_status_string", "fathom_version",
+    "fathom_sparse_attn_workspace_size", "fathom_klt_calibrate", "fathom_klt_calibrate_workspace_size",
+    "fathom_klt_rotate_keys", "fathom_klt_rotate_q", "fathom_status_string", "fathom_version",
 )
 
 
@@ -73,6 +74,9 @@ def lib() -> C.CDLL:
                                     P],
             "fathom_sparse_attn": [P, i32, P, P, i64, i64, P, i32, i32, i32, P, i32, i32, i32, C.c_float, P, P,
                                    C.c_size_t, P, P],
+            "fathom_klt_calibrate": [P, i32, i64, i64, P, i64, i32, i32, P, P, P, P, C.c_size_t, P, P],
+            "fathom_klt_rotate_keys": [P, i32, i64, i64, P, i64, i32, i32, P, P, P, i64, P, P],
+            "fathom_klt_rotate_q": [P, i32, i32, i32, i32, P, P, P],
         }
         for name, args in sig.items():
             f = getattr(L, name)
@@ -84,6 +88,8 @@ def lib() -> C.CDLL:
             f.restype = C.c_size_t
         L.fathom_sparse_attn_workspace_size.argtypes = [i32, i32, i32, i32, i32]
         L.fathom_sparse_attn_workspace_size.restype = C.c_size_t
+        L.fathom_klt_calibrate_workspace_size.argtypes = [i32]
+        L.fathom_klt_calibrate_workspace_size.restype = C.c_size_t
         L.fathom_status_string.argtypes = [st]
         L.fathom_status_string.restype = C.c_char_p
         L.fathom_version.argtypes = []
@@ -278,4 +284,58 @@ def fathom_sparse_attn(q, Krows, Vrows, n, idx, n_sink=0, n_local=0, sm_scale=No
     _check(lib().fathom_sparse_attn(_p(q), _dt(q), _p(Krows), _p(Vrows), Krows.stride(1), Krows.stride(0), _p(n),
                                     U, G, D, _p(idx), k, int(n_sink), int(n_local), C.c_float(sm_scale), _p(out),
                                     _p(ws), ws.numel(), _p(dev_status), _stream(stream)), "fathom_sparse_attn")
+    return out
+
+
+# ---------------------------------------------------------------- KLT-rotated store (Sec. 3.5)
+def fathom_klt_calibrate_workspace_size(U) -> int:
+    return int(lib().fathom_klt_calibrate_workspace_size(int(U)))
+
+
+def fathom_klt_calibrate(K, n, mu=None, V=None, lam=None, ws=None, dev_status=None, stream=None):
+    """Sec. 3.5: per unit, the mean mu [U][D], eigenbasis V [U][D][D] (column c = eigenvector c) and
+    eigenvalues lam [U][D] (descending) of the first n[u] keys of K [U][n_cap][D] (fp32 or fp16)."""
+    _dev(K, n)
+    U, ncap, D = K.shape
+    if K.stride(2) != 1:
+        raise ValueError("K channel stride must be 1")
+    f32 = dict(dtype=torch.float32, device=K.device)
+    mu = torch.empty((U, D), **f32) if mu is None else mu
+    V = torch.empty((U, D, D), **f32) if V is None else V
+    lam = torch.empty((U, D), **f32) if lam is None else lam
+    ws = _ws(fathom_klt_calibrate_workspace_size(U), ws, K.device)
+    _check(lib().fathom_klt_calibrate(_p(K), _dt(K), K.stride(1), K.stride(0), _p(n), ncap, U, D, _p(mu), _p(V),
+                                      _p(lam), _p(ws), ws.numel(), _p(dev_status), _stream(stream)),
+           "fathom_klt_calibrate")
+    return mu, V, lam
+
+
+def fathom_klt_rotate_keys(K, n, mu, V, out=None, dev_status=None, stream=None):
+    """Sec. 3.5: (k - mu) V for the first n[u] keys of each unit -> fp32 [U][n_cap][D] (rows past n[u]
+    are left as they were); pack it with fathom_pack."""
+    _dev(K, n, mu, V)
+    U, ncap, D = K.shape
+    if K.stride(2) != 1 or not mu.is_contiguous() or not V.is_contiguous():
+        raise ValueError("K channel stride 1; mu and V contiguous")
+    if mu.dtype != torch.float32 or V.dtype != torch.float32:
+        raise TypeError("mu and V must be fp32")
+    if out is None:
+        out = torch.empty((U, ncap, D), dtype=torch.float32, device=K.device)
+    if out.dtype != torch.float32 or out.stride(2) != 1 or out.stride(1) != D:
+        raise ValueError("out must be fp32 rows of D floats")
+    _check(lib().fathom_klt_rotate_keys(_p(K), _dt(K), K.stride(1), K.stride(0), _p(n), ncap, U, D, _p(mu), _p(V),
+                                        _p(out), out.stride(0), _p(dev_status), _stream(stream)),
+           "fathom_klt_rotate_keys")
+    return out
+
+
+def fathom_klt_rotate_q(q, V, out=None, stream=None):
+    """Sec. 3.5: q_h V per (unit, head) -> fp32 [U][G][D]."""
+    _dev(q, V)
+    U, G, D = q.shape
+    if not q.is_contiguous() or not V.is_contiguous() or V.dtype != torch.float32:
+        raise ValueError("q contiguous; V contiguous fp32")
+    if out is None:
+        out = torch.empty((U, G, D), dtype=torch.float32, device=q.device)
+    _check(lib().fathom_klt_rotate_q(_p(q), _dt(q), U, G, D, _p(V), _p(out), _stream(stream)), "fathom_klt_rotate_q")
     return out

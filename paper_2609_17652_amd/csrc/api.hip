@@ -23,6 +23,12 @@ fathom_status launch_scan_topk_fused(const uint64_t*, const uint16_t*, const int
                                      fathom_dtype, int, const uint8_t*, int, int64_t, int64_t, int, int32_t*, float*,
                                      void*, uint32_t*, hipStream_t);
 int attn_max_sink_local();
+size_t klt_ws_bytes(int U);
+fathom_status launch_klt_calibrate(const void*, fathom_dtype, int64_t, int64_t, const int64_t*, int64_t, int, float*,
+                                   float*, float*, void*, uint32_t*, hipStream_t);
+fathom_status launch_klt_rotate_keys(const void*, fathom_dtype, int64_t, int64_t, const int64_t*, int64_t, int,
+                                     const float*, const float*, float*, int64_t, uint32_t*, hipStream_t);
+fathom_status launch_klt_rotate_q(const void*, fathom_dtype, int, int, const float*, float*, hipStream_t);
 }  // namespace fathom
 
 using namespace fathom;
@@ -57,6 +63,59 @@ size_t scan_topk_ws(int U, int G, int64_t max_n, int k) {
 }  // namespace
 
 extern "C" {
+
+// KLT-rotated store (Sec. 3.5): keys as in fathom_pack, read element by element.
+static fathom_status check_klt_keys(const void* K, fathom_dtype kdt, int64_t ld_tok, int64_t ld_unit,
+                                    const int64_t* n, int64_t n_cap, int U, int D) {
+  if (U < 0 || n_cap < 0) return FATHOM_ERR_INVALID;
+  if (D != kD) return FATHOM_ERR_UNSUPPORTED;
+  if (!dtype_ok(kdt)) return FATHOM_ERR_UNSUPPORTED;
+  if (n_cap > ((int64_t)1 << 31)) return FATHOM_ERR_UNSUPPORTED;
+  if (U == 0) return FATHOM_OK;
+  if (!n || !aligned(n, 8)) return FATHOM_ERR_INVALID;
+  if (n_cap > 0) {
+    if (!K || !aligned(K, dtype_size(kdt))) return FATHOM_ERR_INVALID;
+    if (ld_tok < D || ld_unit < 0) return FATHOM_ERR_INVALID;
+  }
+  return FATHOM_OK;
+}
+
+size_t fathom_klt_calibrate_workspace_size(int U) { return U > 0 ? klt_ws_bytes(U) : 0; }
+
+fathom_status fathom_klt_calibrate(const void* K, fathom_dtype kdt, int64_t ld_tok, int64_t ld_unit,
+                                   const int64_t* n, int64_t n_cap, int U, int D, float* mu, float* V, float* lam,
+                                   void* ws, size_t ws_bytes, uint32_t* dev_status, void* stream) {
+  const fathom_status e = check_klt_keys(K, kdt, ld_tok, ld_unit, n, n_cap, U, D);
+  if (e != FATHOM_OK || U == 0) return e;
+  if (!mu || !V || !lam || !ws) return FATHOM_ERR_INVALID;
+  if (!aligned(mu, 4) || !aligned(V, 4) || !aligned(lam, 4) || !aligned(ws, 256)) return FATHOM_ERR_INVALID;
+  if (ws_bytes < klt_ws_bytes(U)) return FATHOM_ERR_WORKSPACE;
+  return launch_klt_calibrate(K, kdt, ld_tok, ld_unit, n, n_cap, U, mu, V, lam, ws, dev_status, as_stream(stream));
+}
+
+fathom_status fathom_klt_rotate_keys(const void* K, fathom_dtype kdt, int64_t ld_tok, int64_t ld_unit,
+                                     const int64_t* n, int64_t n_cap, int U, int D, const float* mu,
+                                     const float* V, float* out, int64_t ld_out_unit, uint32_t* dev_status,
+                                     void* stream) {
+  const fathom_status e = check_klt_keys(K, kdt, ld_tok, ld_unit, n, n_cap, U, D);
+  if (e != FATHOM_OK || U == 0 || n_cap == 0) return e;
+  if (!mu || !V || !out) return FATHOM_ERR_INVALID;
+  if (!aligned(mu, 4) || !aligned(V, 4) || !aligned(out, 4)) return FATHOM_ERR_INVALID;
+  if (ld_out_unit < n_cap * D) return FATHOM_ERR_INVALID;
+  return launch_klt_rotate_keys(K, kdt, ld_tok, ld_unit, n, n_cap, U, mu, V, out, ld_out_unit, dev_status,
+                                as_stream(stream));
+}
+
+fathom_status fathom_klt_rotate_q(const void* q, fathom_dtype qdt, int U, int G, int D, const float* V, float* out,
+                                  void* stream) {
+  if (U < 0) return FATHOM_ERR_INVALID;
+  if (D != kD) return FATHOM_ERR_UNSUPPORTED;
+  if (G < 1 || G > kMaxG || !dtype_ok(qdt)) return FATHOM_ERR_UNSUPPORTED;
+  if (U == 0) return FATHOM_OK;
+  if (!q || !V || !out) return FATHOM_ERR_INVALID;
+  if (!aligned(q, dtype_size(qdt)) || !aligned(V, 4) || !aligned(out, 4)) return FATHOM_ERR_INVALID;
+  return launch_klt_rotate_q(q, qdt, U, G, V, out, as_stream(stream));
+}
 
 const char* fathom_status_string(fathom_status s) {
   switch (s) {

@@ -130,6 +130,41 @@ def test_host_validation(fl):
                                 FAKE, FAKE, wsa - 1, NULL, S) == fl.FATHOM_ERR_WORKSPACE
 
 
+def test_klt_host_validation(fl):
+    L = fl.lib()
+    wsk = fl.fathom_klt_calibrate_workspace_size(2)
+    assert wsk >= 2 * 32 * 128 * 128 * 8 and fl.fathom_klt_calibrate_workspace_size(0) == 0
+    A256 = C.c_void_p(0x10000)
+    # calibrate: D, dtype, U < 0, null outputs, short or misaligned workspace, ld_tok < D
+    assert L.fathom_klt_calibrate(FAKE, 0, 128, 0, FAKE, 64, 2, 64, FAKE, FAKE, FAKE, A256, wsk, NULL,
+                                  S) == fl.FATHOM_ERR_UNSUPPORTED
+    assert L.fathom_klt_calibrate(FAKE, 5, 128, 0, FAKE, 64, 2, 128, FAKE, FAKE, FAKE, A256, wsk, NULL,
+                                  S) == fl.FATHOM_ERR_UNSUPPORTED
+    assert L.fathom_klt_calibrate(FAKE, 0, 128, 0, FAKE, 64, -1, 128, FAKE, FAKE, FAKE, A256, wsk, NULL,
+                                  S) == fl.FATHOM_ERR_INVALID
+    assert L.fathom_klt_calibrate(FAKE, 0, 128, 0, FAKE, 64, 2, 128, FAKE, NULL, FAKE, A256, wsk, NULL,
+                                  S) == fl.FATHOM_ERR_INVALID
+    assert L.fathom_klt_calibrate(FAKE, 0, 128, 0, FAKE, 64, 2, 128, FAKE, FAKE, FAKE, A256, wsk - 1, NULL,
+                                  S) == fl.FATHOM_ERR_WORKSPACE
+    assert L.fathom_klt_calibrate(FAKE, 0, 128, 0, FAKE, 64, 2, 128, FAKE, FAKE, FAKE, C.c_void_p(0x10080), wsk,
+                                  NULL, S) == fl.FATHOM_ERR_INVALID
+    assert L.fathom_klt_calibrate(FAKE, 0, 100, 0, FAKE, 64, 2, 128, FAKE, FAKE, FAKE, A256, wsk, NULL,
+                                  S) == fl.FATHOM_ERR_INVALID
+    assert L.fathom_klt_calibrate(NULL, 0, 128, 0, NULL, 0, 0, 128, NULL, NULL, NULL, NULL, 0, NULL,
+                                  S) == fl.FATHOM_OK  # U = 0: no-op
+    # rotate keys: output block shorter than n_cap rows, null mu, misaligned fp16 keys
+    assert L.fathom_klt_rotate_keys(FAKE, 0, 128, 0, FAKE, 64, 1, 128, FAKE, FAKE, FAKE, 63 * 128, NULL,
+                                    S) == fl.FATHOM_ERR_INVALID
+    assert L.fathom_klt_rotate_keys(FAKE, 0, 128, 0, FAKE, 64, 1, 128, NULL, FAKE, FAKE, 64 * 128, NULL,
+                                    S) == fl.FATHOM_ERR_INVALID
+    assert L.fathom_klt_rotate_keys(C.c_void_p(0x1001), 1, 128, 0, FAKE, 64, 1, 128, FAKE, FAKE, FAKE, 64 * 128,
+                                    NULL, S) == fl.FATHOM_ERR_INVALID
+    # rotate q: G outside 1..8, D != 128, null V
+    assert L.fathom_klt_rotate_q(FAKE, 0, 1, 9, 128, FAKE, FAKE, S) == fl.FATHOM_ERR_UNSUPPORTED
+    assert L.fathom_klt_rotate_q(FAKE, 0, 1, 4, 64, FAKE, FAKE, S) == fl.FATHOM_ERR_UNSUPPORTED
+    assert L.fathom_klt_rotate_q(FAKE, 0, 1, 4, 128, NULL, FAKE, S) == fl.FATHOM_ERR_INVALID
+
+
 def test_synth_is_deterministic_and_shaped():
     from paper_2609_17652_amd import synth
     cfg = synth.WORKLOADS["head4k"]
