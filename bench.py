@@ -186,11 +186,72 @@ def fidelity(dev="cuda:0"):
             "workload": cfg.name, "k": k, "results": rows}
 
 
+def fidelity_basis(dev="cuda:0"):
+    """Sec. 3.5's basis rule on a layer whose keys are not normalised per channel:
+    the layer of fidelity() with each unit's keys and queries turned by a seeded
+    random rotation R (k R^T, q R^T: every score is unchanged, but the channels'
+    variance is spread over all raw channels).  Raw planes water-filled with the
+    mixed keys' per-channel variance against KLT-rotated planes (calibrated on
+    the unit's own keys) water-filled with the eigenvalues, at the same code
+    bits per key; relative L2 of the sparse attention output against dense
+    attention over the same (mixed, fp16) keys.  Also times the calibration and
+    the rotations."""
+    cfg = synth.WORKLOADS["layer128k"]
+    data = synth.device_units(cfg, with_values=True)
+    K, V, q, n = data["K"], data["V"], data["q"], data["n"]
+    U, N, D = K.shape
+    k = cfg.k
+    R = torch.from_numpy(np.stack([synth.mixing_rotation(cfg, u) for u in range(U)])).to(dev)
+    Rt = R.transpose(1, 2).contiguous()
+    Km = torch.matmul(K, Rt)
+    del K
+    qm = torch.matmul(q.float(), Rt)
+    var_m = Km.var(dim=1, unbiased=False)  # per-channel variance of the mixed keys
+    Km16 = Km.half()
+    sm = 1.0 / float(np.sqrt(D))
+    logits = torch.matmul(qm, Km16.float().transpose(1, 2).contiguous()) * sm
+    dense = torch.matmul(torch.softmax(logits, dim=-1), V.float())
+    del logits
+
+    def err(idx):
+        o = F.fathom_sparse_attn(qm, Km16, V, n, idx)
+        return (torch.linalg.vector_norm(o - dense, dim=-1) / torch.linalg.vector_norm(dense, dim=-1)).cpu()
+
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+    torch.cuda.synchronize()
+    ev[0].record()
+    mu, Vb, lam = F.fathom_klt_calibrate(Km, n)
+    ev[1].record()
+    Kr = F.fathom_klt_rotate_keys(Km, n, mu, Vb)
+    ev[2].record()
+    qr = F.fathom_klt_rotate_q(qm, Vb)
+    ev[3].record()
+    torch.cuda.synchronize()
+    times = {"klt_calibrate": ev[0].elapsed_time(ev[1]), "klt_rotate_keys": ev[1].elapsed_time(ev[2]),
+             "klt_rotate_q": ev[2].elapsed_time(ev[3])}
+    raw_p, raw_s = F.fathom_pack(Km, n)
+    rot_p, rot_s = F.fathom_pack(Kr, n)
+    rows = {}
+    for B in (32, 48, 80):
+        d, _ = F.fathom_alloc_depths(qm, var_m, F.FATHOM_WATERFILL, B)
+        idx, _ = F.fathom_scan_topk(raw_p, raw_s, n, qm, d, k)
+        e = err(idx)
+        rows[f"raw_B{B}"] = {"mean": float(e.mean()), "max": float(e.max())}
+        d, _ = F.fathom_alloc_depths(qr, lam, F.FATHOM_WATERFILL, B)
+        idx, _ = F.fathom_scan_topk(rot_p, rot_s, n, qr, d, k)
+        e = err(idx)
+        rows[f"klt_B{B}"] = {"mean": float(e.mean()), "max": float(e.max())}
+    return {"fidelity": "relative L2 of sparse vs dense attention output, per (unit, head), keys mixed by a "
+                        "random rotation per unit", "workload": cfg.name + ", channels mixed", "k": k,
+            "results": rows, "ms_at_this_size": times, "keys_per_unit": N}
+
+
 def main():
     args = parse()
     if args.fidelity:
         torch.cuda.set_device(0)
         print(json.dumps(fidelity()), flush=True)
+        print(json.dumps(fidelity_basis()), flush=True)
         return
     if args.traffic_summary:
         t = traffic_summary(args.traffic_summary[0], args.traffic_summary[1], args.traffic_calib or 256)

@@ -301,7 +301,8 @@ fathom_status fathom_klt_rotate_keys(const void* K, fathom_dtype kdt, int64_t ld
 
 /*
  * fathom_klt_rotate_q -- q_h V per (unit, head), fp32 [U][G][D], in the order of
- * fathom_klt_rotate_keys (no mean).  q [U][G][D] (qdt), V [U][D][D] fp32.
+ * fathom_klt_rotate_keys (no mean).  q [U][G][D] (qdt), V [U][D][D] fp32,
+ * 16-byte aligned.  Runs once per decode step, before fathom_alloc_depths.
  */
 fathom_status fathom_klt_rotate_q(const void* q, fathom_dtype qdt, int U, int G, int D, const float* V,
                                   float* out, void* stream);

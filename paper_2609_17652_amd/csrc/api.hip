@@ -113,7 +113,7 @@ fathom_status fathom_klt_rotate_q(const void* q, fathom_dtype qdt, int U, int G,
   if (G < 1 || G > kMaxG || !dtype_ok(qdt)) return FATHOM_ERR_UNSUPPORTED;
   if (U == 0) return FATHOM_OK;
   if (!q || !V || !out) return FATHOM_ERR_INVALID;
-  if (!aligned(q, dtype_size(qdt)) || !aligned(V, 4) || !aligned(out, 4)) return FATHOM_ERR_INVALID;
+  if (!aligned(q, dtype_size(qdt)) || !aligned(V, 16) || !aligned(out, 4)) return FATHOM_ERR_INVALID;
   return launch_klt_rotate_q(q, qdt, U, G, V, out, as_stream(stream));
 }
 

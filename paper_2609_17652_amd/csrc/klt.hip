@@ -290,16 +290,28 @@ __global__ __launch_bounds__(kRotThreads) void klt_rotate_keys_kernel(const KT* 
   }
 }
 
+// One workgroup per unit: V and the unit's queries are staged in LDS with all
+// loads in flight, then thread (h, c) forms its dot product from LDS.
 __global__ __launch_bounds__(kMaxG * kD) void klt_rotate_q_kernel(const void* __restrict__ q, fathom_dtype qdt,
                                                                  int G, const float* __restrict__ V,
                                                                  float* __restrict__ out) {
+  __shared__ float4 Vs4[kD * kD / 4];
+  __shared__ float qs[kMaxG * kD];
   const int u = blockIdx.x, tid = threadIdx.x, h = tid / kD, c = tid % kD;
+  const float4* Vu = reinterpret_cast<const float4*>(V + (int64_t)u * kD * kD);
+  float4 r[kD * kD / 4 / (kMaxG * kD)];
+#pragma unroll
+  for (int x = 0; x < kD * kD / 4 / (kMaxG * kD); ++x) r[x] = Vu[tid + x * kMaxG * kD];
+  const int64_t qo = (int64_t)u * G * kD;
+  if (h < G) qs[tid] = load_q(q, qdt, qo + tid);
+#pragma unroll
+  for (int x = 0; x < kD * kD / 4 / (kMaxG * kD); ++x) Vs4[tid + x * kMaxG * kD] = r[x];
+  __syncthreads();
   if (h >= G) return;
-  const float* Vu = V + (int64_t)u * kD * kD;
-  const int64_t qo = ((int64_t)u * G + h) * kD;
+  const float* Vs = reinterpret_cast<const float*>(Vs4);
   float acc = 0.0f;
-  for (int j = 0; j < kD; ++j) acc = __fadd_rn(acc, __fmul_rn(load_q(q, qdt, qo + j), Vu[j * kD + c]));
-  out[qo + c] = acc;
+  for (int j = 0; j < kD; ++j) acc = __fadd_rn(acc, __fmul_rn(qs[h * kD + j], Vs[j * kD + c]));
+  out[qo + tid] = acc;
 }
 
 // ---------------------------------------------------------------- launches

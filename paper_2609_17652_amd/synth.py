@@ -97,6 +97,18 @@ def values_host(rng: np.random.Generator, n: int) -> np.ndarray:
     return rng.standard_normal((n, D), dtype=np.float32).astype(np.float16)
 
 
+def mixing_rotation(cfg: Config, unit: int, seed: int = 0) -> np.ndarray:
+    """A seeded random orthogonal D x D matrix for unit `unit` (QR of a Gaussian
+    draw, column signs fixed by the triangular factor's diagonal), fp32.  Keys
+    k R^T and queries q R^T keep every score q . k but spread the generator's
+    independent channels over all raw channels: the covariance of a layer whose
+    keys are not normalised per channel (the case for the rotated store)."""
+    ids = list(unit_ids(cfg))
+    rng = unit_rng(cfg.seed_key, *ids[unit], seed=seed + 7919)
+    Q, T = np.linalg.qr(rng.standard_normal((D, D)))
+    return (Q * np.sign(np.diag(T))).astype(np.float32)
+
+
 def ragged_lengths(cfg: Config, seed: int = 0) -> np.ndarray:
     """Per-session lengths uniform in n_range (inclusive), one draw per session."""
     rng = np.random.default_rng(np.random.SeedSequence(seed, spawn_key=(cfg.seed_key, 10 ** 6)))
