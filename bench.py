@@ -53,6 +53,10 @@ def parse():
                     help="end with one plain device-to-device copy of MIB MiB (counter calibration)")
     ap.add_argument("--fidelity", action="store_true",
                     help="attention fidelity vs dense at equal bytes (water-filling vs uniform depth), then exit")
+    ap.add_argument("--decode-step", action="store_true",
+                    help="time the full decode step of 4 sessions x 36 layers x 8 KV heads at n = 2^20, then exit")
+    ap.add_argument("--ragged", action="store_true",
+                    help="time one batched step of 16 resident sessions with ragged n, then exit")
     ap.add_argument("--traffic-summary", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="write the HBM-traffic summary from two rocprofv3 --pmc counter files and exit")
     return ap.parse_args()
@@ -246,8 +250,129 @@ def fidelity_basis(dev="cuda:0"):
             "results": rows, "ms_at_this_size": times, "keys_per_unit": N}
 
 
+def _timed(fn, steps, warmup):
+    """Mean GPU time (ms) of fn() over `steps` calls after `warmup`, HIP events on the current stream."""
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(steps):
+        fn()
+    e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / steps
+
+
+def decode_step(steps=5, warmup=2, B=48):
+    """The full decode step of the 4-session workload: 36 layers, each one launch of
+    depth allocation + scan/top-k + sparse attention over its 32 units (4 sessions
+    x 8 KV heads) at n = 2^20, run in layer order as a decoder would, with the
+    paper's protocol (4 sink + 32 local tokens, the top k - 36 of the rest).  Every
+    layer has its own store in HBM (planes + scales, about 82 GB in all).  fp16
+    K/V rows for attention come from one layer-sized row pool reused by every
+    layer (all 36 layers' rows would not fit in 288 GB)."""
+    cfg = synth.WORKLOADS["step4x1m"]
+    L, S, H, n, k = cfg.layers, cfg.sessions, cfg.kv_heads, cfg.n, cfg.k
+    lo, tail = cfg.n_sink, cfg.n_local
+    sel = k - lo - tail
+    planes, scales, qs, vs = [], [], [], []
+    t0 = time.perf_counter()
+    for l in range(L):
+        units = [(s * L + l) * H + h for s in range(S) for h in range(H)]
+        last = l == L - 1
+        d = synth.device_units(cfg, units=units, with_values=last, key_dtype=torch.float16)
+        p, sc = F.fathom_pack(d["K"], d["n"])
+        planes.append(p)
+        scales.append(sc)
+        qs.append(d["q"])
+        vs.append(d["var"])
+        if last:
+            K16, V, nt = d["K"], d["V"], d["n"]
+        del d
+    torch.cuda.synchronize()
+    log(f"[decode-step] {L} layer stores packed in {time.perf_counter() - t0:.1f} s")
+    U, G = S * H, cfg.G
+    dev = K16.device
+    st = F.new_status()
+    dep = torch.empty((U, 128), dtype=torch.uint8, device=dev)
+    theta = torch.empty((U,), dtype=torch.float32, device=dev)
+    idx = torch.empty((U, G, sel), dtype=torch.int32, device=dev)
+    val = torch.empty((U, G, sel), dtype=torch.float32, device=dev)
+    out = torch.empty((U, G, 128), dtype=torch.float32, device=dev)
+    ws = torch.empty((F.fathom_scan_topk_workspace_size(U, G, n, sel),), dtype=torch.uint8, device=dev)
+    wsa = torch.empty((F.fathom_sparse_attn_workspace_size(U, G, sel, lo, tail),), dtype=torch.uint8, device=dev)
+    bits = []
+
+    def step():
+        for l in range(L):
+            F.fathom_alloc_depths(qs[l], vs[l], F.FATHOM_WATERFILL, B, dep, theta, st)
+            F.fathom_scan_topk(planes[l], scales[l], nt, qs[l], dep, sel, lo, tail, idx, val, ws, st,
+                               max_unit_bits=B)
+            F.fathom_sparse_attn(qs[l], K16, V, nt, idx, lo, tail, None, out, st, ws=wsa)
+
+    ms = _timed(step, steps, warmup)
+    for l in range(L):  # plane bits actually read per key, per layer
+        F.fathom_alloc_depths(qs[l], vs[l], F.FATHOM_WATERFILL, B, dep, theta, st)
+        bits.append(dep.int().sum().item())
+    status = int(st.item()) & 0xFFFFFFFF
+    keys = L * U * n
+    plane_bytes = sum(bits) * n / 8
+    return {"workload": cfg.name, "ms_per_decode_step": ms, "keys_per_s": keys / (ms * 1e-3),
+            "plane_gbps": plane_bytes / (ms * 1e-3) / 1e9, "plane_bytes_per_step": plane_bytes,
+            "layers": L, "units_per_layer": U, "k_selected": sel, "device_status": status,
+            "store_bytes": sum(p.numel() * 8 + s.numel() * 2 for p, s in zip(planes, scales)),
+            "timing": f"HIP events, mean of {steps} steps after {warmup}"}
+
+
+def ragged(steps=20, warmup=3):
+    """One batched decode step of 16 resident sessions (ragged n, 8 KV heads each:
+    128 units in one launch), B = 40, k = 1024: depth allocation + scan/top-k +
+    sparse attention."""
+    cfg = synth.WORKLOADS["ragged16"]
+    d = synth.device_units(cfg, with_values=True, key_dtype=torch.float16)
+    K16, V, q, var, nt = d["K"], d["V"], d["q"], d["var"], d["n"]
+    U, G = K16.shape[0], cfg.G
+    B, k = cfg.budgets[0], cfg.k
+    planes, scales = F.fathom_pack(K16, nt)
+    dev = K16.device
+    st = F.new_status()
+    dep = torch.empty((U, 128), dtype=torch.uint8, device=dev)
+    theta = torch.empty((U,), dtype=torch.float32, device=dev)
+    idx = torch.empty((U, G, k), dtype=torch.int32, device=dev)
+    val = torch.empty((U, G, k), dtype=torch.float32, device=dev)
+    out = torch.empty((U, G, 128), dtype=torch.float32, device=dev)
+    ws = torch.empty((F.fathom_scan_topk_workspace_size(U, G, K16.shape[1], k),), dtype=torch.uint8, device=dev)
+    wsa = torch.empty((F.fathom_sparse_attn_workspace_size(U, G, k),), dtype=torch.uint8, device=dev)
+
+    def sel():
+        F.fathom_alloc_depths(q, var, F.FATHOM_WATERFILL, B, dep, theta, st)
+        F.fathom_scan_topk(planes, scales, nt, q, dep, k, 0, 0, idx, val, ws, st, max_unit_bits=B)
+
+    def step():
+        sel()
+        F.fathom_sparse_attn(q, K16, V, nt, idx, 0, 0, None, out, st, ws=wsa)
+
+    ms_sel = _timed(sel, steps, warmup)
+    ms = _timed(step, steps, warmup)
+    keys = int(d["n_host"].sum())
+    bits = dep.int().sum(dim=1).cpu().numpy()
+    plane_bytes = float((bits * d["n_host"]).sum()) / 8
+    return {"workload": cfg.name, "units": U, "keys": keys, "ms_alloc_scan_topk": ms_sel,
+            "keys_per_s": keys / (ms_sel * 1e-3), "plane_gbps": plane_bytes / (ms_sel * 1e-3) / 1e9,
+            "ms_with_attention": ms, "device_status": int(st.item()) & 0xFFFFFFFF,
+            "timing": f"HIP events, mean of {steps} calls after {warmup}"}
+
+
 def main():
     args = parse()
+    if args.decode_step or args.ragged:
+        torch.cuda.set_device(0)
+        if args.ragged:
+            print(json.dumps(ragged()), flush=True)
+        if args.decode_step:
+            print(json.dumps(decode_step()), flush=True)
+        return
     if args.fidelity:
         torch.cuda.set_device(0)
         print(json.dumps(fidelity()), flush=True)
