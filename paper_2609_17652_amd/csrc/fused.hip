@@ -1293,13 +1293,19 @@ __device__ __forceinline__ float exact_score1(const int* act, int A, const float
 
 // The survivors of row r (bucket counts cnt8) hold its top k exactly when no
 // bucket overflowed, at least k were found and the filter ran for the row.
+// The row's survivor lists determine its top k exactly when at least k keys
+// survived and every bucket that starts above rank k (fewer than k survivors
+// in the buckets before it) kept all of its keys: buckets entirely below the
+// k-th key are never read, so their overflow does not matter.  The counts are
+// exact even for an overflowing bucket (keys past its capacity are counted,
+// not stored).
 __device__ __forceinline__ bool survivors_complete(const uint32_t* cnt8, const FusedArgs& a, float tau, uint32_t ovf) {
   uint32_t C = 0;
   bool over = false;
 #pragma unroll
   for (int z = 0; z < kSlots; ++z) {
+    over |= C < (uint32_t)a.k && cnt8[z] > (uint32_t)a.ws.scap;
     C += cnt8[z];
-    over |= cnt8[z] > (uint32_t)a.ws.scap;
   }
   return !over && C >= (uint32_t)a.k && (ovf & 1u) == 0u && tau != kNegInf;
 }

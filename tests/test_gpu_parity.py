@@ -536,6 +536,40 @@ def test_scan_topk_fallback_is_exact(scale):
         assert np.array_equal(val[0, h].cpu().numpy(), ov), h
 
 
+def test_bucket_overflow_below_rank_k_keeps_the_filter():
+    """A decode-step row (4-session workload: layer 33, session 0, KV head 4,
+    query head 1) whose lowest survivor bucket receives more keys than its
+    capacity while the buckets above it already hold k: no bucket the top k
+    reads is incomplete, so the row keeps the filter (no TOPK_FALLBACK) and its
+    top k equals the oracle's."""
+    cfg = synth.WORKLOADS["step4x1m"]
+    unit = (0 * cfg.layers + 33) * cfg.kv_heads + 4
+    data = synth.device_units(cfg, units=[unit], with_values=False, key_dtype=torch.float16)
+    K, q, var, nt = data["K"], data["q"], data["var"], data["n"]
+    n, lo, tail = int(data["n_host"][0]), cfg.n_sink, cfg.n_local
+    sel = cfg.k - lo - tail
+    planes, scales = F.fathom_pack(K, nt)
+    d, _ = F.fathom_alloc_depths(q, var, F.FATHOM_WATERFILL, 48)
+    G = q.shape[1]
+    ws = torch.zeros((F.fathom_scan_topk_workspace_size(1, G, n, sel),), dtype=torch.uint8, device=DEV)
+    st = F.new_status()
+    idx, val = F.fathom_scan_topk(planes, scales, nt, q, d, sel, lo, tail, ws=ws, dev_status=st, max_unit_bits=48)
+    assert status(st) == 0
+    # the case itself, from the workspace (threshold per row, then 8 bucket counts per row)
+    w = ws.cpu().numpy()
+    cnt = w[256:256 + G * 8 * 4].view(np.uint32).reshape(G, 8).astype(np.int64)
+    scap = min(2 * sel + 2048, 16384) // 4
+    over = [z for z in range(8) if cnt[1, z] > scap]
+    assert over and all(cnt[1, :z].sum() >= sel for z in over), cnt[1]
+    ref = oracle.scores_f32(u64(planes)[0], u16(scales)[0], n, q[0].cpu().numpy().astype(np.float32),
+                            d.cpu().numpy()[0])
+    ix, vx = idx.cpu().numpy()[0], val.cpu().numpy()[0]
+    for h in range(G):
+        oi, ov, _ = oracle.topk(ref[h], sel, lo, tail)
+        assert np.array_equal(ix[h], oi), h
+        assert np.array_equal(vx[h].view(np.uint32), ov.view(np.uint32)), h
+
+
 def test_scan_topk_no_fallback_on_workload_data():
     """On the synthetic workloads the sampled threshold never needs the fallback."""
     cfg = synth.WORKLOADS["layer128k"]
