@@ -319,7 +319,8 @@ def decode_step(steps=5, warmup=2, B=48):
     keys = L * U * n
     plane_bytes = sum(bits) * n / 8
     return {"workload": cfg.name, "ms_per_decode_step": ms, "keys_per_s": keys / (ms * 1e-3),
-            "plane_gbps": plane_bytes / (ms * 1e-3) / 1e9, "plane_bytes_per_step": plane_bytes,
+            "plane_gbps": plane_bytes / (ms * 1e-3) / 1e9, "hbm_frac": plane_bytes / (ms * 1e-3) / 8e12,
+            "plane_bytes_per_step": plane_bytes,
             "layers": L, "units_per_layer": U, "k_selected": sel, "device_status": status,
             "store_bytes": sum(p.numel() * 8 + s.numel() * 2 for p, s in zip(planes, scales)),
             "timing": f"HIP events, mean of {steps} steps after {warmup}"}
@@ -360,6 +361,7 @@ def ragged(steps=20, warmup=3):
     plane_bytes = float((bits * d["n_host"]).sum()) / 8
     return {"workload": cfg.name, "units": U, "keys": keys, "ms_alloc_scan_topk": ms_sel,
             "keys_per_s": keys / (ms_sel * 1e-3), "plane_gbps": plane_bytes / (ms_sel * 1e-3) / 1e9,
+            "hbm_frac": plane_bytes / (ms_sel * 1e-3) / 8e12,
             "ms_with_attention": ms, "device_status": int(st.item()) & 0xFFFFFFFF,
             "timing": f"HIP events, mean of {steps} calls after {warmup}"}
 
