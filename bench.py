@@ -55,6 +55,8 @@ def parse():
                     help="attention fidelity vs dense at equal bytes (water-filling vs uniform depth), then exit")
     ap.add_argument("--decode-step", action="store_true",
                     help="time the full decode step of 4 sessions x 36 layers x 8 KV heads at n = 2^20, then exit")
+    ap.add_argument("--klt", action="store_true",
+                    help="time the KLT-rotated store at the 2^20-token layer (prefill and per step), then exit")
     ap.add_argument("--ragged", action="store_true",
                     help="time one batched step of 16 resident sessions with ragged n, then exit")
     ap.add_argument("--traffic-summary", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
@@ -366,8 +368,59 @@ def ragged(steps=20, warmup=3):
             "timing": f"HIP events, mean of {steps} calls after {warmup}"}
 
 
+def klt_layer(steps=30, warmup=5, B=48):
+    """Sec. 3.5's rotated store at the 2^20-token layer (8 KV heads x 4 query
+    heads, k = 2048): one-time calibration, key rotation and pack, then the
+    decode-step work, query rotation + water-filling with var = lambda + fused
+    scan/top-k on the rotated planes, timed like the contract line."""
+    cfg = synth.WORKLOADS["layer1m"]
+    data = synth.device_units(cfg, with_values=False)
+    K, q, n = data["K"], data["q"], data["n"]
+    U, N, D = K.shape
+    G, k = q.shape[1], cfg.k
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+    torch.cuda.synchronize()
+    ev[0].record()
+    mu, V, lam = F.fathom_klt_calibrate(K, n)
+    ev[1].record()
+    Kr = F.fathom_klt_rotate_keys(K, n, mu, V)
+    ev[2].record()
+    planes, scales = F.fathom_pack(Kr, n)
+    ev[3].record()
+    torch.cuda.synchronize()
+    pre = {"klt_calibrate_ms": ev[0].elapsed_time(ev[1]), "klt_rotate_keys_ms": ev[1].elapsed_time(ev[2]),
+           "pack_rotated_ms": ev[2].elapsed_time(ev[3])}
+    del K, Kr
+    dev = q.device
+    st = F.new_status()
+    qr = torch.empty((U, G, D), dtype=torch.float32, device=dev)
+    dep = torch.empty((U, D), dtype=torch.uint8, device=dev)
+    theta = torch.empty((U,), dtype=torch.float32, device=dev)
+    idx = torch.empty((U, G, k), dtype=torch.int32, device=dev)
+    val = torch.empty((U, G, k), dtype=torch.float32, device=dev)
+    ws = torch.empty((F.fathom_scan_topk_workspace_size(U, G, N, k),), dtype=torch.uint8, device=dev)
+
+    def step():
+        F.fathom_klt_rotate_q(q, V, qr)
+        F.fathom_alloc_depths(qr, lam, F.FATHOM_WATERFILL, B, dep, theta, st)
+        F.fathom_scan_topk(planes, scales, n, qr, dep, k, 0, 0, idx, val, ws, st, max_unit_bits=B)
+
+    ms = _timed(step, steps, warmup)
+    keys = int(data["n_host"].sum())
+    plane_bytes = float(dep.int().sum().item()) * N / 8
+    return {"workload": cfg.name + ", KLT-rotated store", "ms_per_step": ms, "keys_per_s": keys / (ms * 1e-3),
+            "plane_gbps": plane_bytes / (ms * 1e-3) / 1e9, "hbm_frac": plane_bytes / (ms * 1e-3) / 8e12,
+            "prefill": pre, "device_status": int(st.item()) & 0xFFFFFFFF,
+            "step": "fathom_klt_rotate_q + fathom_alloc_depths (var = lambda) + fathom_scan_topk_ex",
+            "timing": f"HIP events, mean of {steps} steps after {warmup}; one store (no copies rotated)"}
+
+
 def main():
     args = parse()
+    if args.klt:
+        torch.cuda.set_device(0)
+        print(json.dumps(klt_layer()), flush=True)
+        return
     if args.decode_step or args.ragged:
         torch.cuda.set_device(0)
         if args.ragged:
