@@ -48,7 +48,7 @@ def parse():
     ap.add_argument("--copies", type=int, default=8, help="distinct store copies rotated across steps")
     ap.add_argument("--scan-reps", type=int, default=32, help="extra scan-only launches timed for the roofline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-units", type=int, default=4, help="units in the oracle's CPU-baseline sample")
+    ap.add_argument("--cpu-units", type=int, default=8, help="units (KV heads) in the oracle's CPU baseline")
     ap.add_argument("--traffic-calib", type=int, default=0, metavar="MIB",
                     help="end with one plain device-to-device copy of MIB MiB (counter calibration)")
     ap.add_argument("--fidelity", action="store_true",
@@ -61,12 +61,17 @@ def parse():
                     help="time one batched step of 16 resident sessions with ragged n, then exit")
     ap.add_argument("--traffic-summary", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="write the HBM-traffic summary from two rocprofv3 --pmc counter files and exit")
+    ap.add_argument("--sq-summary", nargs="+", metavar="CSV",
+                    help="write the SQ counter summary of the fused call from rocprofv3 --pmc files and exit")
     return ap.parse_args()
 
 
 def cpu_baseline(planes, scales, q, var, n, mode, B, k, units):
     """The oracle as it stands (depth allocation + fp32 score replica + top-k per
-    head), one thread per sampled unit; ctypes calls release the GIL."""
+    head) over `units` KV heads at the full n.  Each unit's keys are scored in
+    independent block ranges (the scores of a key depend on its own block only),
+    so the work spreads over every CPU this process may run on (at most 16, the
+    GPU machine's share per GPU); ctypes calls release the GIL."""
     import concurrent.futures as cf
 
     import oracle
@@ -76,41 +81,96 @@ def cpu_baseline(planes, scales, q, var, n, mode, B, k, units):
     qh = q[:units].cpu().numpy().astype(np.float32)
     vh = var[:units].cpu().numpy()
     nh = n[:units].cpu().numpy()
-
-    def one(u):
-        if mode == F.FATHOM_WATERFILL:
-            d, _, _ = oracle.alloc_waterfill(qh[u], vh[u], B)
-        else:
-            d, _, _ = oracle.alloc_topr(qh[u], B)
-        s = oracle.scores_f32(P[u], S[u], int(nh[u]), qh[u], d)
-        for h in range(qh.shape[1]):
-            oracle.topk(s[h], k)
-        return int(nh[u])
-
+    G = qh.shape[1]
+    avail = len(os.sched_getaffinity(0))
+    threads = max(1, min(avail, 16))
     oracle.build() if not os.path.exists(oracle.lib_path()) else None
     t0 = time.perf_counter()
-    with cf.ThreadPoolExecutor(max_workers=units) as ex:
-        keys = sum(ex.map(one, range(units)))
+    with cf.ThreadPoolExecutor(max_workers=threads) as ex:
+        def depths(u):
+            if mode == F.FATHOM_WATERFILL:
+                return oracle.alloc_waterfill(qh[u], vh[u], B)[0]
+            return oracle.alloc_topr(qh[u], B)[0]
+
+        dep = list(ex.map(depths, range(units)))
+        nb = [(int(nh[u]) + 63) // 64 for u in range(units)]
+        pieces = max(1, -(-2 * threads // units))  # block ranges per unit
+
+        def score(arg):
+            u, r = arg
+            b0, b1 = nb[u] * r // pieces, nb[u] * (r + 1) // pieces
+            m = min(int(nh[u]), 64 * b1) - 64 * b0
+            if m <= 0:
+                return u, r, np.zeros((G, 0), np.float32)
+            Pp = np.ascontiguousarray(P[u][:, :, b0:b1])
+            Sp = np.ascontiguousarray(S[u][:, b0:b1])
+            return u, r, oracle.scores_f32(Pp, Sp, m, qh[u], dep[u])
+
+        parts = {}
+        for u, r, sc in ex.map(score, [(u, r) for u in range(units) for r in range(pieces)]):
+            parts[(u, r)] = sc
+        full = [np.concatenate([parts[(u, r)] for r in range(pieces)], axis=1) for u in range(units)]
+        list(ex.map(lambda a: oracle.topk(full[a[0]][a[1]], k), [(u, h) for u in range(units) for h in range(G)]))
     dt = time.perf_counter() - t0
-    return {"value": keys / dt, "unit": "keys/s", "cores": units, "kind": "oracle",
-            "sample": f"{units} of 8 KV heads at the full n = {int(nh[0])}, all {qh.shape[1]} query heads: "
-                      f"oracle depth allocation + fp32 score replica + top-{k}, one thread per head "
-                      f"({dt:.1f} s wall)"}
+    keys = int(nh.sum())
+    return {"value": keys / dt, "unit": "keys/s", "cores": threads, "kind": "oracle",
+            "cpus_available": avail,
+            "sample": f"the whole workload: all {units} KV heads at the full n = {int(nh[0])}, all {G} query heads: "
+                      f"oracle depth allocation + fp32 score replica + top-{k} ({dt:.1f} s wall on {threads} "
+                      f"threads; each unit's blocks in {pieces} independent ranges)"}
 
 
 TRAFFIC_JSON = os.path.join(ROOT, "profiles", "scan_topk_layer1m_b48_traffic.json")
-TRAFFIC_SOURCES = ("paper_2609_17652_amd/csrc/fused.hip", "paper_2609_17652_amd/csrc/common.hpp")
-SCAN_TOPK_KERNELS = ("fused_sample_kernel", "fused_tau_kernel", "fused_main_kernel", "fused_rank_kernel",
-                     "fused_select_kernel")
+SQ_JSON = os.path.join(ROOT, "profiles", "scan_topk_layer1m_b48_sq.json")
+KERNEL_SOURCES = ("paper_2609_17652_amd/csrc/fused.hip", "paper_2609_17652_amd/csrc/common.hpp")
+# the three counter passes behind SQ_JSON (at most 8 SQ counters per pass)
+SQ_PASSES = (
+    ("SQ_WAVES", "SQ_WAVE_CYCLES", "SQ_BUSY_CYCLES", "SQ_WAIT_ANY", "SQ_INSTS_VALU", "SQ_INSTS_SALU",
+     "SQ_INSTS_LDS", "SQ_INSTS_VMEM_RD"),
+    ("SQ_ACTIVE_INST_VALU", "SQ_ACTIVE_INST_LDS", "SQ_ACTIVE_INST_SCA", "SQ_INSTS_MFMA", "SQ_WAIT_INST_ANY",
+     "SQ_WAIT_INST_LDS", "SQ_INSTS_BRANCH", "SQ_ACTIVE_INST_MISC"),
+    ("SQ_LDS_BANK_CONFLICT", "SQ_LDS_IDX_ACTIVE", "SQ_LDS_ADDR_CONFLICT", "SQ_VALU_MFMA_BUSY_CYCLES",
+     "SQ_INSTS_SMEM", "SQ_IFETCH", "SQ_INST_CYCLES_SALU", "SQ_INSTS_VALU_MFMA_I8"),
+)
+VALU_PEAK_LANE_OPS = 256 * 4 * 16 * 2.4e9  # CUs x SIMDs x lanes x clock: one wave64 VALU op per SIMD per 4 cycles
 
 
 def kernel_source_hash():
     import hashlib
     h = hashlib.sha256()
-    for f in TRAFFIC_SOURCES:
+    for f in KERNEL_SOURCES:
         with open(os.path.join(ROOT, f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()
+
+
+def scan_topk_kernel(name):
+    """The short name of a kernel of the fused scan + top-k call (its function
+    name with template arguments), or None for any other kernel."""
+    if "fathom::fused_" not in name:
+        return None
+    short = name.split("fathom::", 1)[1]
+    return short.split("(", 1)[0]
+
+
+def _counter_rows(path, names):
+    import csv
+    from collections import defaultdict
+
+    vals = defaultdict(lambda: defaultdict(list))
+    copies = defaultdict(list)
+    with open(path) as fh:
+        for r in csv.DictReader(fh):
+            c = r["Counter_Name"]
+            if c not in names:
+                continue
+            v = float(r["Counter_Value"])
+            if "copyBuffer" in r["Kernel_Name"]:
+                copies[c].append((int(r["Dispatch_Id"]), v))
+            k = scan_topk_kernel(r["Kernel_Name"])
+            if k is not None:
+                vals[c][k].append(v)
+    return vals, copies
 
 
 def traffic_summary(fetch_csv, write_csv, calib_mib):
@@ -118,44 +178,66 @@ def traffic_summary(fetch_csv, write_csv, calib_mib):
     dispatch), each scaled so that the calibration copy of calib_mib MiB (the
     last copyBuffer dispatch of at least a quarter of that size) reads and
     writes exactly its size."""
-    import csv
-    from collections import defaultdict
-
     calib = float(calib_mib) * 1024.0  # KiB
     out = {}
     for name, path in (("FETCH_SIZE", fetch_csv), ("WRITE_SIZE", write_csv)):
-        rows = sorted((r for r in csv.DictReader(open(path)) if r["Counter_Name"] == name),
-                      key=lambda r: int(r["Dispatch_Id"]))
-        vals = defaultdict(list)
-        for r in rows:
-            vals[r["Kernel_Name"]].append(float(r["Counter_Value"]))
-        copies = [float(r["Counter_Value"]) for r in rows
-                  if "copyBuffer" in r["Kernel_Name"] and float(r["Counter_Value"]) >= calib / 4]
-        factor = calib / copies[-1]
-        per = {}
-        for k, vs in vals.items():
-            short = next((t for t in SCAN_TOPK_KERNELS if t in k), None)
-            if short is None:
-                continue
-            key = short + ("<narrow>" if "fused_main_kernel" in k and ", 3," in k else "")
-            per[key] = per.get(key, 0.0) + float(np.mean(vs)) * 1024.0 * factor
-        out[name] = {"factor": factor, "calib_raw_kib": copies[-1], "per_kernel_bytes": per}
+        vals, copies = _counter_rows(path, {name})
+        cp = [v for _, v in sorted(copies[name]) if v >= calib / 4]
+        factor = calib / cp[-1]
+        per = {k: float(np.mean(vs)) * 1024.0 * factor for k, vs in vals[name].items()}
+        out[name] = {"factor": factor, "calib_raw_kib": cp[-1], "per_kernel_bytes": per}
     total = sum(out["FETCH_SIZE"]["per_kernel_bytes"].values()) + sum(out["WRITE_SIZE"]["per_kernel_bytes"].values())
     return {"bytes_per_call": total, "counters": out, "source_sha256": kernel_source_hash(),
-            "sources": list(TRAFFIC_SOURCES), "calib_mib": calib_mib}
+            "sources": list(KERNEL_SOURCES), "calib_mib": calib_mib}
 
 
-def measured_traffic():
-    """The committed per-call HBM traffic, or None once the kernel sources changed."""
+def sq_summary(csvs):
+    """Per kernel of the fused call, the mean per dispatch of every SQ counter in
+    the passes' files, and per call the VALU instructions issued (the issue-side
+    roofline's numerator)."""
+    names = {c for p in SQ_PASSES for c in p}
+    per = {}
+    for path in csvs:
+        vals, _ = _counter_rows(path, names)
+        for c, byk in vals.items():
+            for k, vs in byk.items():
+                per.setdefault(k, {})[c] = float(np.mean(vs))
+    derived = {}
+    for k, c in per.items():
+        d = {}
+        if c.get("SQ_WAVE_CYCLES"):
+            for x in ("SQ_WAIT_ANY", "SQ_ACTIVE_INST_VALU", "SQ_ACTIVE_INST_LDS", "SQ_ACTIVE_INST_SCA"):
+                if x in c:
+                    d[x + "/SQ_WAVE_CYCLES"] = c[x] / c["SQ_WAVE_CYCLES"]
+        if c.get("SQ_LDS_IDX_ACTIVE") and "SQ_LDS_BANK_CONFLICT" in c:
+            d["SQ_LDS_BANK_CONFLICT/SQ_LDS_IDX_ACTIVE"] = c["SQ_LDS_BANK_CONFLICT"] / c["SQ_LDS_IDX_ACTIVE"]
+        derived[k] = d
+    valu = sum(c.get("SQ_INSTS_VALU", 0.0) for c in per.values())
+    return {"valu_insts_per_call": valu, "per_kernel": per, "derived": derived,
+            "source_sha256": kernel_source_hash(), "sources": list(KERNEL_SOURCES)}
+
+
+def _committed(path):
+    """A committed counter summary, or None once the kernel sources changed."""
     try:
-        with open(TRAFFIC_JSON) as fh:
+        with open(path) as fh:
             t = json.load(fh)
     except (OSError, ValueError):
         return None
-    return t["bytes_per_call"] if t.get("source_sha256") == kernel_source_hash() else None
+    return t if t.get("source_sha256") == kernel_source_hash() else None
 
 
-def fidelity(dev="cuda:0"):
+def measured_traffic():
+    t = _committed(TRAFFIC_JSON)
+    return None if t is None else t["bytes_per_call"]
+
+
+def measured_valu_insts():
+    t = _committed(SQ_JSON)
+    return None if t is None else t["valu_insts_per_call"]
+
+
+def fidelity(dev="cuda:0", refs_for=None):
     """Relative L2 error of top-k sparse attention against dense attention (fp32,
     all n keys), per (unit, head), on one 8-KV-head layer at n = 131072, k = 1024
     (Sec. 4's measure of what the selection keeps): water-filled depths at
@@ -188,8 +270,13 @@ def fidelity(dev="cuda:0"):
     exact = torch.topk(torch.matmul(qf, K.transpose(1, 2).contiguous()), k, dim=-1).indices.int()
     e = err(exact)
     rows["exact_topk"] = {"mean": float(e.mean()), "max": float(e.max())}
-    return {"fidelity": "relative L2 of sparse vs dense attention output, per (unit, head)",
-            "workload": cfg.name, "k": k, "results": rows}
+    res = {"fidelity": "relative L2 of sparse vs dense attention output, per (unit, head)",
+           "workload": cfg.name, "k": k, "results": rows}
+    if refs_for is not None:  # host copies of the references for the listed units (checked by the tests)
+        res["refs"] = {u: {"q": q[u].cpu().numpy(), "K": K[u].cpu().numpy(), "K16": K16[u].cpu().numpy(),
+                           "V16": V[u].cpu().numpy(), "dense": dense[u].cpu().numpy(),
+                           "exact_idx": exact[u].cpu().numpy()} for u in refs_for}
+    return res
 
 
 def fidelity_basis(dev="cuda:0"):
@@ -250,6 +337,51 @@ def fidelity_basis(dev="cuda:0"):
     return {"fidelity": "relative L2 of sparse vs dense attention output, per (unit, head), keys mixed by a "
                         "random rotation per unit", "workload": cfg.name + ", channels mixed", "k": k,
             "results": rows, "ms_at_this_size": times, "keys_per_unit": N}
+
+
+def stream_read_gbps(dev, stream, nbytes=4 << 30, reps=5):
+    """HBM read rate of a plain coalesced stream (the probe library's kernel:
+    16-byte loads, 8 in flight per thread, one pass over nbytes), median of reps."""
+    import ctypes as C
+
+    from paper_2609_17652_amd import build as hip_build
+
+    lib = C.CDLL(hip_build.PROBE_LIB)
+    lib.probe_stream_read.restype = C.c_int
+    lib.probe_stream_read.argtypes = [C.c_void_p, C.c_int64, C.c_void_p, C.c_void_p]
+    buf = torch.ones((nbytes // 4,), dtype=torch.int32, device=dev)
+    out = torch.empty((lib.probe_stream_read_groups(),), dtype=torch.int32, device=dev)
+    sp = C.c_void_p(stream.cuda_stream)
+
+    def run():
+        rc = lib.probe_stream_read(C.c_void_p(buf.data_ptr()), nbytes // 16, C.c_void_p(out.data_ptr()), sp)
+        if rc != 0:
+            raise RuntimeError(f"probe_stream_read failed ({rc})")
+
+    run()
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+    for a_, b_ in ev:
+        a_.record(stream)
+        run()
+        b_.record(stream)
+    torch.cuda.synchronize()
+    ms = float(np.median([a_.elapsed_time(b_) for a_, b_ in ev]))
+    del buf, out
+    return nbytes / (ms * 1e-3) / 1e9
+
+
+def issue_side(call_ms):
+    """VALU issue rate of the fused call: its VALU instructions (SQ_INSTS_VALU
+    summed over the call's kernels, from the committed counter summary of the
+    same sources) x 64 lanes / the call's live time, against the chip's
+    one-instruction-per-SIMD-per-4-cycles rate.  None when no summary matches."""
+    v = measured_valu_insts()
+    if v is None:
+        return None
+    ach = v * 64 / (call_ms * 1e-3)
+    return {"bound": "valu", "achieved": ach, "peak": VALU_PEAK_LANE_OPS, "unit": "lane-ops/s",
+            "frac": ach / VALU_PEAK_LANE_OPS, "valu_insts_per_call": v}
 
 
 def _timed(fn, steps, warmup):
@@ -433,6 +565,12 @@ def main():
         print(json.dumps(fidelity()), flush=True)
         print(json.dumps(fidelity_basis()), flush=True)
         return
+    if args.sq_summary:
+        t = sq_summary(args.sq_summary)
+        with open(SQ_JSON, "w") as fh:
+            json.dump(t, fh, indent=1)
+        print(json.dumps(t))
+        return
     if args.traffic_summary:
         t = traffic_summary(args.traffic_summary[0], args.traffic_summary[1], args.traffic_calib or 256)
         with open(TRAFFIC_JSON, "w") as fh:
@@ -601,18 +739,9 @@ def main():
     gather_bytes = float(tcl.sum() * nb_cap * 8 + (tcl > 0).sum() * nb_cap * 2)
     del hp, hs, gp, gs
 
-    # ---- a streaming-read reference on the same GPU: torch's sum over 2 GiB
-    big = torch.ones((1 << 29,), dtype=torch.float32, device=dev)
-    big.sum()
-    torch.cuda.synchronize()
-    rev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(5)]
-    for a_, b_ in rev:
-        a_.record(stream)
-        big.sum()
-        b_.record(stream)
-    torch.cuda.synchronize()
-    stream_gbps = big.numel() * 4 / (float(np.median([a_.elapsed_time(b_) for a_, b_ in rev])) * 1e-3) / 1e9
-    del big
+    # ---- a streaming-read reference on the same GPU: a plain HIP kernel
+    # reading 4 GiB once with 16-byte loads
+    stream_gbps = stream_read_gbps(dev, stream)
     torch.cuda.empty_cache()
 
     keys = float(nh.sum())
@@ -650,9 +779,10 @@ def main():
         "active_channels_mean": active,
         "plane_bits_per_key_mean": float(dn.sum(1).mean()),
         "device_status": status,
-        "roofline": {"bound": "hbm", "kernel": "fathom_scan_topk (sample, tau, full, rank, select launches)",
+        "roofline": {"bound": "hbm", "kernel": "fathom_scan_topk (every launch of one call)",
                      "achieved": st_gbps, "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": st_gbps / HBM_PEAK_GBPS,
-                     "traffic": measured_traffic(), "alg_bytes_per_launch": alg_bytes, "avg_launch_ms": st_ms},
+                     "traffic": measured_traffic(), "alg_bytes_per_launch": alg_bytes, "avg_launch_ms": st_ms,
+                     "issue": issue_side(st_ms)},
     }
     if args.traffic_calib > 0:
         nbytes = args.traffic_calib << 20

@@ -6,7 +6,9 @@ this package never imports the product.  See ``oracle/fathom_oracle.c`` for
 the arithmetic and the paper passages each function follows.
 
 Parity status per function (what pins it to the paper, in ``tests/``):
-  pack            App. A codes, Sec. 3.2 prefix-quantiser invariant, MSB = sign
+  f32_to_f16_*    numpy binary16 conversion on every half, midpoint and neighbour
+  pack            App. A codes, Sec. 3.2 prefix-quantiser invariant, MSB = sign,
+                  fp16-subnormal and near-65504 block scales
   alloc_waterfill App. A g, theta, depths at B = 8 and 6; brute force; Eq. (wf)
   bisect          App. A bisection trace, row by row
   alloc_topr      App. A SparQ tie rule and sum |q|

@@ -53,6 +53,11 @@ uint16_t orc_f32_to_f16(float xf) {
   return sign | (uint16_t)(((e + 15) << 10) | ((int)m - 1024));
 }
 
+/* The conversion above applied element by element (for exhaustive checks). */
+void orc_f32_to_f16_n(const float* x, int64_t n, uint16_t* out) {
+  for (int64_t i = 0; i < n; ++i) out[i] = orc_f32_to_f16(x[i]);
+}
+
 double orc_f16_to_f64(uint16_t h) {
   int sign = (h >> 15) & 1, e = (h >> 10) & 31, f = h & 1023;
   double v;

@@ -13,7 +13,7 @@ import subprocess
 import numpy as np
 
 __all__ = [
-    "build", "lib_path", "f32_to_f16_bits", "f16_bits_to_f64", "pack", "dequant",
+    "build", "lib_path", "f32_to_f16_bits", "f32_to_f16_bits_array", "f16_bits_to_f64", "pack", "dequant",
     "importance", "alloc_waterfill", "depths_at", "bisect", "alloc_topr",
     "scores_f64", "scores_f32", "topk", "sparse_attn",
     "SCALE_OVERFLOW", "NONFINITE", "TOPK_SHORT",
@@ -55,6 +55,8 @@ def _load():
         i64, i32, u32 = C.c_int64, C.c_int, C.c_uint32
         lib.orc_f32_to_f16.restype = C.c_uint16
         lib.orc_f32_to_f16.argtypes = [C.c_float]
+        lib.orc_f32_to_f16_n.restype = None
+        lib.orc_f32_to_f16_n.argtypes = [P, i64, P]
         lib.orc_f16_to_f64.restype = C.c_double
         lib.orc_f16_to_f64.argtypes = [C.c_uint16]
         lib.orc_pack.restype = u32
@@ -94,6 +96,14 @@ def _c(a, dtype):
 
 def f32_to_f16_bits(x: float) -> int:
     return int(_load().orc_f32_to_f16(float(np.float32(x))))
+
+
+def f32_to_f16_bits_array(x: np.ndarray) -> np.ndarray:
+    """orc_f32_to_f16 over an array of fp32 values (binary16 bit patterns)."""
+    x = _c(x, np.float32).ravel()
+    out = np.zeros(x.shape, np.uint16)
+    _load().orc_f32_to_f16_n(_ptr(x), x.size, _ptr(out))
+    return out
 
 
 def f16_bits_to_f64(h: int) -> float:

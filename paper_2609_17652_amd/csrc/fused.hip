@@ -1396,11 +1396,11 @@ __global__ __launch_bounds__(kSelThreads) void fused_select_kernel(FusedArgs a, 
     }
   }
   const int count = s_count;
-  int P2 = 1;
+  int P2 = 2;  // the sort takes at least one pair; every slot past count is zeroed
   while (P2 < count) P2 <<= 1;
   for (int x = count + tid; x < P2; x += kSelThreads) buf[x] = 0ull;
   __syncthreads();
-  bitonic_desc(buf, P2 > 1 ? P2 : 2);
+  bitonic_desc(buf, P2);
   bool shortfall = false;
   for (int x = tid; x < k; x += kSelThreads) {
     const uint64_t c = x < count ? buf[x] : 0ull;

@@ -51,9 +51,9 @@ def test_traffic_summary_scales_by_the_last_calibration_copy(tmp_path):
     f, w = t["counters"]["FETCH_SIZE"], t["counters"]["WRITE_SIZE"]
     assert f["factor"] == pytest.approx(2.0) and w["factor"] == pytest.approx(1.0)
     # per kernel: the mean over its dispatches, in bytes, times the factor
-    assert f["per_kernel_bytes"]["fused_main_kernel<narrow>"] == pytest.approx(2000.0 * 1024 * 2.0)
-    assert f["per_kernel_bytes"]["fused_sample_kernel"] == pytest.approx(100.0 * 1024 * 2.0)
-    assert w["per_kernel_bytes"]["fused_main_kernel<narrow>"] == pytest.approx(20.0 * 1024)
+    assert f["per_kernel_bytes"]["fused_main_kernel<true, 3, 16>"] == pytest.approx(2000.0 * 1024 * 2.0)
+    assert f["per_kernel_bytes"]["fused_sample_kernel<true, 3>"] == pytest.approx(100.0 * 1024 * 2.0)
+    assert w["per_kernel_bytes"]["fused_main_kernel<true, 3, 16>"] == pytest.approx(20.0 * 1024)
     expect = (100 + 2000 + 50) * 1024 * 2.0 + (1 + 20 + 5) * 1024 * 1.0
     assert t["bytes_per_call"] == pytest.approx(expect)
     assert t["source_sha256"] == bench.kernel_source_hash()
@@ -68,3 +68,35 @@ def test_measured_traffic_is_null_once_the_kernel_sources_change(tmp_path, monke
     assert bench.measured_traffic() == 123.0
     p.write_text(json.dumps({"bytes_per_call": 123.0, "source_sha256": "0" * 64}))
     assert bench.measured_traffic() is None
+
+
+def test_sq_summary_means_per_kernel_and_valu_per_call(tmp_path):
+    """SQ counters from several passes: per kernel of the fused call, the mean
+    over its dispatches; VALU instructions per call = the sum over the call's
+    kernels; other kernels ignored; the issue-side fraction uses 64 lanes per
+    instruction against 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz."""
+    bench = load_bench()
+    main = "void fathom::fused_main_kernel<true, 3, 16>(fathom::FusedArgs)"
+    rank = "fathom::fused_rank_kernel(fathom::FusedArgs, int*, float*)"
+    a, b = tmp_path / "a.csv", tmp_path / "b.csv"
+    write_counters(a, "SQ_INSTS_VALU", [(main, 1000.0), (main, 3000.0), (rank, 10.0), ("pack_kernel", 7.0)])
+    with open(a, "a", newline="") as fh:
+        w = csv.writer(fh)
+        w.writerow([9, main, "SQ_WAVE_CYCLES", 400.0])
+        w.writerow([10, main, "SQ_WAIT_ANY", 100.0])
+    write_counters(b, "SQ_LDS_BANK_CONFLICT", [(main, 30.0)])
+    with open(b, "a", newline="") as fh:
+        csv.writer(fh).writerow([2, main, "SQ_LDS_IDX_ACTIVE", 120.0])
+    t = bench.sq_summary([str(a), str(b)])
+    assert t["per_kernel"]["fused_main_kernel<true, 3, 16>"]["SQ_INSTS_VALU"] == pytest.approx(2000.0)
+    assert t["valu_insts_per_call"] == pytest.approx(2010.0)
+    d = t["derived"]["fused_main_kernel<true, 3, 16>"]
+    assert d["SQ_WAIT_ANY/SQ_WAVE_CYCLES"] == pytest.approx(0.25)
+    assert d["SQ_LDS_BANK_CONFLICT/SQ_LDS_IDX_ACTIVE"] == pytest.approx(0.25)
+    p = tmp_path / "sq.json"
+    p.write_text(json.dumps(t))
+    bench.SQ_JSON = str(p)
+    iss = bench.issue_side(0.1)
+    assert iss["frac"] == pytest.approx(2010.0 * 64 / 1e-4 / (256 * 4 * 16 * 2.4e9))
+    p.write_text(json.dumps(dict(t, source_sha256="0" * 64)))
+    assert bench.issue_side(0.1) is None

@@ -11,6 +11,7 @@ import numpy as np
 import pytest
 import torch
 
+import edge_inputs
 import oracle
 import paper_2609_17652_amd as F
 from paper_2609_17652_amd import synth
@@ -154,6 +155,40 @@ def test_pack_bad_n_flag():
     planes, scales = F.fathom_pack(K, nt, nb_cap=2, dev_status=st)
     assert status(st) & F.FATHOM_DEV_BAD_N
     assert (u64(planes)[1] == 0).all()
+
+
+@pytest.mark.parametrize("kdt", [np.float32, np.float16])
+def test_pack_fp16_scale_edges(kdt):
+    """Sec. 3.2's fp16 block scales at their edges, GPU against the oracle bit
+    for bit: block absmax in the binary16 subnormal range (including below half
+    the smallest subnormal, which rounds to a zero scale), in [65504, 65520)
+    (rounds to 65504), fp32 subnormal keys beside a subnormal-scale channel;
+    fp16 keys hold the subnormal halves exactly.  One extra unit has an absmax
+    of exactly 65520 (fp16 infinity: codes 8, SCALE_OVERFLOW)."""
+    rng = np.random.default_rng(1200)
+    ns = [1000, 64, 200]
+    nmax = max(ns)
+    K = np.zeros((len(ns), nmax, 128), np.float32)
+    for u, n in enumerate(ns):
+        K[u, :n] = edge_inputs.scale_edge_keys(rng, n, D=128)
+        K[u, :n, 64:76] = edge_inputs.scale_edge_keys(rng, n, D=12)  # a second copy, other blocks' draws
+    if kdt == np.float16:
+        K = np.clip(K, -65504.0, 65504.0).astype(np.float16)
+    over = K.copy()
+    over[2, 70, 3] = 65504.0 if kdt == np.float16 else 65520.0
+    for arr, expect_over in [(K, False), (over, kdt == np.float32)]:
+        nt = torch.tensor(ns, dtype=torch.int64, device=DEV)
+        st = F.new_status()
+        planes, scales = F.fathom_pack(torch.from_numpy(arr).to(DEV), nt, dev_status=st)
+        s = status(st)
+        assert bool(s & F.FATHOM_DEV_SCALE_OVERFLOW) == expect_over, hex(s)
+        P, Sc = u64(planes), u16(scales)
+        for u, n in enumerate(ns):
+            op, os_, _ = oracle.pack(arr[u, :n].astype(np.float32), nb_cap=planes.shape[-1])
+            assert np.array_equal(Sc[u], os_), f"scales unit {u} n={n}"
+            assert np.array_equal(P[u], op), f"planes unit {u} n={n}"
+        subn = (Sc[:, :, :] & 0x7C00) == 0
+        assert (subn & (Sc != 0)).any()  # the subnormal scales are really there
 
 
 # ---------------------------------------------------------------------- depths
@@ -383,8 +418,10 @@ def test_head4k_end_to_end():
 @pytest.mark.parametrize("name", ["layer128k", "layer1m"])
 def test_layer_full_size_sampled(name):
     """One Qwen3-8B layer at n = 131072 and at n = 2^20: all 8 KV heads in one
-    launch, as timed by the bench; oracle on sampled units / blocks, every budget
-    and mode."""
+    launch, as timed by the bench; every budget (40/48/80 and 48/80 bits) and
+    the uniform-depth modes (r = 16 and 32 channels at 4 planes, the 68- and
+    136-bit scans): depths of all 8 units, top-k and attention of one sampled
+    unit per mode against the oracle; planes and scales on sampled blocks."""
     cfg = synth.WORKLOADS[name]
     data = synth.device_units(cfg, with_values=True)
     K, q, var, nt = data["K"], data["q"], data["var"], data["n"]
@@ -399,9 +436,9 @@ def test_layer_full_size_sampled(name):
             assert np.array_equal(u16(scales[u, :, b0:b0 + 3]), os_), (u, b0)
     qh, vh = q.cpu().numpy().astype(np.float32), var.cpu().numpy()
     modes = [(F.FATHOM_WATERFILL, B) for B in cfg.budgets] + [(F.FATHOM_UNIFORM_TOPR, r) for r in cfg.uniform_r]
-    su = 3
-    Psu, Ssu = u64(planes[su]), u16(scales[su])
-    for mode, B in modes:
+    for mi, (mode, B) in enumerate(modes):
+        su = [3, 5, 1, 6, 2][mi % 5]  # the sampled unit of this mode
+        Psu, Ssu = u64(planes[su]), u16(scales[su])
         st = F.new_status()
         d, th = F.fathom_alloc_depths(q, var, mode, B, dev_status=st)
         idx, val = F.fathom_scan_topk(planes, scales, nt, q, d, cfg.k, dev_status=st)
@@ -427,8 +464,7 @@ def test_layer_full_size_sampled(name):
         oo = oracle.sparse_attn(qh[su], Kh, Vh, ix, 0, 0, 1 / np.sqrt(128))
         tol = _attn_tol(qh[su], Kh, Vh, ix, 0, 0, np.float32(1 / np.sqrt(128)))
         assert (np.abs(out.cpu().numpy()[0] - oo) <= tol).all()
-        if name == "layer1m":
-            break  # the full-size run checks one budget end to end; depths for all modes above
+        del Psu, Ssu, ref
     del data, K, planes, scales
     torch.cuda.empty_cache()
 
@@ -709,24 +745,60 @@ def test_scan_topk_heads_and_query_dtypes(G, qdt):
         _assert_rows_match(idx, val, planes, scales, ns, q, d, k, lo, tail)
 
 
+@pytest.mark.parametrize("G,qdt", [(1, np.float32), (4, np.float16)])
+def test_scan_topk_uniform_depth_mode(G, qdt):
+    """Sec. 2 (SparQ grouped rule) through the fused scan + top-k: r channels at
+    all 4 planes, r in {0, 1, 16, 32, 128} (16 and 32 are the 68- and 136-bit
+    scans; r = 32 and 128 take the wide filter instantiation), with heavily tied
+    sum_h |q_hj| (query entries from {0, +-1, +-2}), on ragged units that span
+    many superquads and a ragged tail; depths and top-k against the oracle."""
+    ns = [50000, 33333, 65536]
+    K, nt, planes, scales = _store(ns, 131)
+    rng = np.random.default_rng(132)
+    U = len(ns)
+    q = rng.choice(np.array([0.0, 1.0, -1.0, 2.0, -2.0], np.float32), (U, G, 128)).astype(qdt)
+    q[:, :, 7] = 0
+    qt = torch.from_numpy(q).to(DEV)
+    k = 512
+    for r in [0, 1, 16, 32, 128]:
+        st = F.new_status()
+        d, _ = F.fathom_alloc_depths(qt, None, F.FATHOM_UNIFORM_TOPR, r, dev_status=st)
+        dn = d.cpu().numpy()
+        for u in range(U):
+            od, _, _ = oracle.alloc_topr(q[u].astype(np.float32), r)
+            assert np.array_equal(dn[u], od), (r, u)
+        idx, val = F.fathom_scan_topk(planes, scales, nt, qt, d, k, dev_status=st)
+        assert status(st) & ~F.FATHOM_DEV_TOPK_FALLBACK == 0
+        _assert_rows_match(idx, val, planes, scales, ns, q, d, k, 0, 0)
+
+
 def test_scan_topk_empty_and_short_rows():
-    """n = 0, n below lo + tail, fewer eligible keys than k, beside a filtered unit
-    in the same launch: short rows hold their eligible keys in order, then index
-    -1 and value NaN, and the call reports TOPK_SHORT."""
-    ns = [0, 30, 500, 30000]
+    """n = 0, n below lo + tail, exactly one and two eligible keys (n = 37 and 38
+    with lo = 4, tail = 32), fewer eligible keys than k, beside a filtered unit
+    and a unit recomputed by the exact path (its depths exceed the caller's bit
+    bound) in the same launch: short rows hold their eligible keys in order, then
+    index -1 and value NaN, and the call reports TOPK_SHORT and TOPK_FALLBACK."""
+    ns = [37, 40000, 0, 30, 36, 38, 500, 30000]
     K, nt, planes, scales = _store(ns, 71)
     rng = np.random.default_rng(72)
     q = rng.standard_normal((len(ns), 4, 128)).astype(np.float16)
     qt = torch.from_numpy(q).to(DEV)
     var = torch.from_numpy(np.exp(rng.standard_normal((len(ns), 128))).astype(np.float32)).to(DEV)
     d, _ = F.fathom_alloc_depths(qt, var, F.FATHOM_WATERFILL, 48)
-    k, lo, tail = 600, 4, 32
-    st = F.new_status()
-    idx, val = F.fathom_scan_topk(planes, scales, nt, qt, d, k, lo, tail, dev_status=st)
-    s = status(st)
-    assert s & F.FATHOM_DEV_TOPK_SHORT, hex(s)
-    assert s & ~(F.FATHOM_DEV_TOPK_SHORT | F.FATHOM_DEV_TOPK_FALLBACK) == 0, hex(s)
-    _assert_rows_match(idx, val, planes, scales, ns, q, d, k, lo, tail)
+    d[1] = torch.from_numpy(rng.integers(1, 5, 128).astype(np.uint8)).to(DEV)  # far above 48 bits
+    for k, lo, tail in [(600, 4, 32), (300, 4, 32), (1, 4, 32)]:
+        st = F.new_status()
+        idx, val = F.fathom_scan_topk(planes, scales, nt, qt, d, k, lo, tail, dev_status=st, max_unit_bits=48)
+        s = status(st)
+        assert s & F.FATHOM_DEV_TOPK_SHORT and s & F.FATHOM_DEV_TOPK_FALLBACK, hex(s)
+        assert s & ~(F.FATHOM_DEV_TOPK_SHORT | F.FATHOM_DEV_TOPK_FALLBACK) == 0, hex(s)
+        _assert_rows_match(idx, val, planes, scales, ns, q, d, k, lo, tail)
+        ix = idx.cpu().numpy()
+        assert (ix[0, :, 0] == 4).all() and (ix[0, :, 1:] == -1).all()  # the one eligible key
+        # the same rows through the unfused scan + top-k
+        sc = F.fathom_scan(planes, scales, nt, qt, d)
+        i2, v2 = F.fathom_topk(sc, nt, k, lo, tail)
+        assert torch.equal(idx, i2)
 
 
 def test_gather_host_store_leaves_scan_topk_unchanged():
@@ -734,7 +806,8 @@ def test_gather_host_store_leaves_scan_topk_unchanged():
     read into a zeroed device store copies exactly the active runs (first t
     planes and the scales of every active channel), writes nothing else, and
     scan_topk over it is bit-identical.  Pageable host memory is refused before
-    any launch."""
+    any launch.  The top-k over the gathered store equals the oracle's top-k
+    over the host planes."""
     import ctypes as C
     ns = [40000, 9000]  # nb_cap 625: scale rows start off 16-byte boundaries
     K, nt, planes, scales = _store(ns, 91)
@@ -758,6 +831,15 @@ def test_gather_host_store_leaves_scan_topk_unchanged():
     a = F.fathom_scan_topk(planes, scales, nt, q, d, 300)
     b = F.fathom_scan_topk(gp, gs, nt, q, d, 300)
     assert torch.equal(a[0], b[0]) and torch.equal(a[1].view(torch.int32), b[1].view(torch.int32))
+    # the oracle on the host store's own planes (what the gather read) gives the same top-k
+    HP, HS, qn = hp.numpy().view(np.uint64), hs.numpy().view(np.uint16), q.cpu().numpy().astype(np.float32)
+    bi, bv = b[0].cpu().numpy(), b[1].cpu().numpy()
+    for u, n in enumerate(ns):
+        ref = oracle.scores_f32(HP[u], HS[u], n, qn[u], dn[u])
+        for h in range(4):
+            oi, ov, _ = oracle.topk(ref[h], 300)
+            assert np.array_equal(bi[u, h], oi), (u, h)
+            assert np.array_equal(bv[u, h].view(np.uint32), ov.view(np.uint32)), (u, h)
     pageable = np.zeros(planes.numel() + 2, np.uint64)
     p16 = pageable.ctypes.data + (-pageable.ctypes.data) % 16
     r = F.lib().fathom_gather_store(C.c_void_p(p16), C.c_void_p(p16), C.c_void_p(d.data_ptr()), len(ns), 128,

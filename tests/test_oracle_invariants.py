@@ -9,6 +9,8 @@ import itertools
 import numpy as np
 import pytest
 
+from edge_inputs import scale_edge_keys
+
 
 def _keys(rng, n, D, scale=None):
     sig = np.exp(rng.standard_normal(D)) if scale is None else np.full(D, scale)
@@ -266,3 +268,74 @@ def test_nonfinite_and_overflow_flags(orc):
     assert st & orc.SCALE_OVERFLOW and st & orc.NONFINITE
     c = _codes(planes, 64)
     assert (c[:, 0] == 8).all() and c[9, 1] == 8 and c[0, 1] == 15
+
+
+def _f16_edge_inputs():
+    """Every finite binary16 value, every midpoint between neighbours (exact in
+    fp32: 12 significant bits), the fp32 neighbours of each midpoint, values
+    past the largest finite half, and the signed zeros."""
+    h = np.arange(0, 0x7C00, dtype=np.uint32).astype(np.uint16)  # +0 .. 65504
+    v = h.view(np.float16).astype(np.float32)
+    mids = ((v[:-1].astype(np.float64) + v[1:].astype(np.float64)) / 2).astype(np.float32)
+    assert (mids.astype(np.float64) == (v[:-1].astype(np.float64) + v[1:]) / 2).all()
+    top = np.float32(65520.0)  # halfway between 65504 and the first power past the range
+    extra = np.array([top, 70000.0, 3.0e38, np.inf, 2.0 ** -25, 2.0 ** -26, 1e-40, 1e-45], np.float32)
+    pos = np.concatenate([v, mids, np.nextafter(mids, np.float32(np.inf)),
+                          np.nextafter(mids, np.float32(0)), extra,
+                          np.nextafter(np.float32(top), np.float32(0))[None]])
+    return np.concatenate([pos, -pos]).astype(np.float32)
+
+
+def test_f32_to_f16_exhaustive_against_numpy(orc):
+    """Sec. 3.2 stores fp16 block scales: the oracle's binary16 conversion,
+    written from the format's definition, equals numpy's round-to-nearest-even
+    conversion on every finite half, every midpoint (ties to even), the fp32
+    neighbours of every midpoint, the subnormal range down to 2^-26 and fp32
+    subnormals, and the overflow edge (65504 + 16 = 65520 rounds to infinity,
+    the fp32 value just below it to 65504)."""
+    x = _f16_edge_inputs()
+    got = orc.f32_to_f16_bits_array(x)
+    with np.errstate(over="ignore"):
+        want = x.astype(np.float16).view(np.uint16)
+    assert np.array_equal(got, want)
+    # spot values that a wrong rounding or range test would move
+    below = np.nextafter(np.float32(65520.0), np.float32(0))
+    assert orc.f32_to_f16_bits(below) == 0x7BFF and orc.f32_to_f16_bits(65520.0) == 0x7C00
+    assert orc.f32_to_f16_bits(2.0 ** -25) == 0 and orc.f32_to_f16_bits(3 * 2.0 ** -26) == 1
+    assert orc.f32_to_f16_bits(-(2.0 ** -24)) == 0x8001
+    assert orc.f32_to_f16_bits(float("nan")) & 0x7C00 == 0x7C00 and orc.f32_to_f16_bits(float("nan")) & 0x3FF
+    for h in range(0, 0x7C00, 97):  # the inverse is exact on finite halves
+        assert orc.f16_bits_to_f64(h) == float(np.uint16(h).view(np.float16))
+
+
+@pytest.mark.parametrize("n", [64, 200])
+def test_pack_fp16_scale_edges(orc, n):
+    """Sec. 3.2, Eq. (2) at the edges of the fp16 scale: the stored scale is
+    numpy's fp16 of the block absmax, the codes are the exact real floor against
+    that scale (checked per prefix as the t-bit quantiser, from the keys), and an
+    absmax that rounds to infinity gives zero codes (8) and SCALE_OVERFLOW."""
+    rng = np.random.default_rng(1000 + n)
+    K = scale_edge_keys(rng, n)
+    nb = (n + 63) // 64
+    planes, scales, st = orc.pack(K, nb_cap=nb)
+    assert st == 0
+    c = _codes(planes, n)
+    for b in range(nb):
+        blk = K[64 * b:min(n, 64 * b + 64)]
+        a16 = np.abs(blk).max(0).astype(np.float16)
+        assert (scales[:, b] == a16.view(np.uint16)).all(), b
+        a = a16.astype(np.float64)
+        kk = blk.astype(np.float64)
+        cb = c[64 * b:64 * b + blk.shape[0]]
+        for t in range(1, 5):
+            h = 2.0 ** (t - 1)
+            with np.errstate(divide="ignore", invalid="ignore"):
+                want = np.clip(np.floor(h * kk / a), -h, h - 1) + h
+            want = np.where(a > 0, want, h)
+            assert ((cb >> (4 - t)) == want).all(), (b, t)
+    # absmax exactly 65520: fp16 infinity, codes 8, flagged
+    K2 = K.copy()
+    K2[5, 3] = np.float32(65520.0)
+    p2, s2, st2 = orc.pack(K2, nb_cap=nb)
+    assert st2 & 1 and s2[3, 0] == 0x7C00
+    assert (_codes(p2, n)[:min(n, 64), 3] == 8).all()
