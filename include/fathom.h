@@ -14,7 +14,9 @@
  * Conventions shared by every entry point:
  *   - All pointers to array data are DEVICE pointers unless stated otherwise.
  *     The caller allocates and owns every buffer; the library never allocates
- *     device memory and keeps no state between calls.
+ *     device memory and keeps no state between calls (the one exception is
+ *     the device array behind fathom_scan_topk_noalloc, which holds nothing
+ *     from one call to the next that a later call reads).
  *   - Every call is asynchronous on `stream` (a hipStream_t; NULL = the null
  *     stream) and never synchronises the host.
  *   - Argument errors detectable on the host return an error status before
@@ -224,6 +226,30 @@ fathom_status fathom_scan_topk_ex(const uint64_t* planes, const uint16_t* scales
                                   int G, const uint8_t* depths, int k, int64_t lo, int64_t tail,
                                   int max_unit_bits, int32_t* idx, float* val, void* ws,
                                   size_t ws_bytes, uint32_t* dev_status, void* stream);
+
+/*
+ * fathom_scan_topk_noalloc -- fathom_scan_topk_ex for callers that cannot
+ * allocate or pass a workspace: code under HIP graph capture, tight serving
+ * loops, harnesses that forbid allocation.  Same arguments and outputs as
+ * fathom_scan_topk_ex (bit for bit) minus ws / ws_bytes: the workspace is a
+ * device array inside the library, fathom_scan_topk_noalloc_capacity() bytes
+ * per device, loaded with the library and held until the process ends.  The
+ * call itself allocates nothing.
+ *   - A shape whose fathom_scan_topk_workspace_size(U, G, 64 * nb_cap, k)
+ *     exceeds the capacity returns FATHOM_ERR_WORKSPACE before any launch.
+ *   - Every call on one device uses that device's one array, and each call's
+ *     kernels clear what they need from it.  Calls that overlap on one device
+ *     (different streams or threads without ordering between them) race on
+ *     it and give undefined results; calls ordered on one stream are safe.
+ * Errors: as fathom_scan_topk_ex, plus FATHOM_ERR_HIP if the array's device
+ * address cannot be obtained.
+ */
+fathom_status fathom_scan_topk_noalloc(const uint64_t* planes, const uint16_t* scales, const int64_t* n,
+                                       int U, int D, int64_t nb_cap, const void* q, fathom_dtype qdt,
+                                       int G, const uint8_t* depths, int k, int64_t lo, int64_t tail,
+                                       int max_unit_bits, int32_t* idx, float* val,
+                                       uint32_t* dev_status, void* stream);
+size_t fathom_scan_topk_noalloc_capacity(void);
 
 /*
  * fathom_sparse_attn -- Sec. 2 (top-k decoding) and Sec. 4 (fidelity metric):

@@ -37,7 +37,8 @@ FATHOM_DEV_BAD_N = 16
 
 EXPORTED = (
     "fathom_pack", "fathom_pack_append", "fathom_gather_store", "fathom_alloc_depths", "fathom_scan", "fathom_topk", "fathom_topk_workspace_size",
-    "fathom_scan_topk", "fathom_scan_topk_ex", "fathom_scan_topk_workspace_size", "fathom_sparse_attn",
+    "fathom_scan_topk", "fathom_scan_topk_ex", "fathom_scan_topk_workspace_size", "fathom_scan_topk_noalloc",
+    "fathom_scan_topk_noalloc_capacity", "fathom_sparse_attn",
     "fathom_sparse_attn_workspace_size", "fathom_klt_calibrate", "fathom_klt_calibrate_workspace_size",
     "fathom_klt_rotate_keys", "fathom_klt_rotate_q", "fathom_status_string", "fathom_version",
 )
@@ -72,6 +73,7 @@ def lib() -> C.CDLL:
             "fathom_scan_topk": [P, P, P, i32, i32, i64, P, i32, i32, P, i32, i64, i64, P, P, P, C.c_size_t, P, P],
             "fathom_scan_topk_ex": [P, P, P, i32, i32, i64, P, i32, i32, P, i32, i64, i64, i32, P, P, P, C.c_size_t, P,
                                     P],
+            "fathom_scan_topk_noalloc": [P, P, P, i32, i32, i64, P, i32, i32, P, i32, i64, i64, i32, P, P, P, P],
             "fathom_sparse_attn": [P, i32, P, P, i64, i64, P, i32, i32, i32, P, i32, i32, i32, C.c_float, P, P,
                                    C.c_size_t, P, P],
             "fathom_klt_calibrate": [P, i32, i64, i64, P, i64, i32, i32, P, P, P, P, C.c_size_t, P, P],
@@ -86,6 +88,8 @@ def lib() -> C.CDLL:
             f = getattr(L, name)
             f.argtypes = [i32, i32, i64, i32]
             f.restype = C.c_size_t
+        L.fathom_scan_topk_noalloc_capacity.argtypes = []
+        L.fathom_scan_topk_noalloc_capacity.restype = C.c_size_t
         L.fathom_sparse_attn_workspace_size.argtypes = [i32, i32, i32, i32, i32]
         L.fathom_sparse_attn_workspace_size.restype = C.c_size_t
         L.fathom_klt_calibrate_workspace_size.argtypes = [i32]
@@ -258,6 +262,23 @@ def fathom_scan_topk(planes, scales, n, q, depths, k, lo=0, tail=0, idx=None, va
                                      int(k), int(lo), int(tail), int(max_unit_bits), _p(idx), _p(val), _p(ws),
                                      ws.numel() * ws.element_size(), _p(dev_status), _stream(stream)),
            "fathom_scan_topk")
+    return idx, val
+
+
+def fathom_scan_topk_noalloc_capacity() -> int:
+    return int(lib().fathom_scan_topk_noalloc_capacity())
+
+
+def fathom_scan_topk_noalloc(planes, scales, n, q, depths, k, lo, tail, idx, val, dev_status=None, stream=None,
+                             max_unit_bits=0):
+    """fathom_scan_topk with the library's own device workspace: nothing is allocated, here or in the call
+    (idx and val are the caller's [U][G][k] outputs)."""
+    _dev(planes, scales, n, q, depths, idx, val)
+    U, D, _, nb_cap = planes.shape
+    G = q.shape[1]
+    _check(lib().fathom_scan_topk_noalloc(_p(planes), _p(scales), _p(n), U, D, nb_cap, _p(q), _dt(q), G, _p(depths),
+                                          int(k), int(lo), int(tail), int(max_unit_bits), _p(idx), _p(val),
+                                          _p(dev_status), _stream(stream)), "fathom_scan_topk_noalloc")
     return idx, val
 
 

@@ -23,6 +23,8 @@ fathom_status launch_scan_topk_fused(const uint64_t*, const uint16_t*, const int
                                      fathom_dtype, int, const uint8_t*, int, int64_t, int64_t, int, int32_t*, float*,
                                      void*, uint32_t*, hipStream_t);
 int attn_max_sink_local();
+size_t scratch_capacity();
+fathom_status scratch_address(void** out);
 size_t klt_ws_bytes(int U);
 fathom_status launch_klt_calibrate(const void*, fathom_dtype, int64_t, int64_t, const int64_t*, int64_t, int, float*,
                                    float*, float*, void*, uint32_t*, hipStream_t);
@@ -240,6 +242,26 @@ fathom_status fathom_scan_topk_ex(const uint64_t* planes, const uint16_t* scales
   if (U == 0) return FATHOM_OK;
   if (!idx || !ws || !aligned(idx, 4) || (val && !aligned(val, 4)) || !aligned(ws, 256)) return FATHOM_ERR_INVALID;
   if (ws_bytes < scan_topk_ws(U, G, nb_cap * 64, k)) return FATHOM_ERR_WORKSPACE;
+  return launch_scan_topk_fused(planes, scales, n, U, nb_cap, q, qdt, G, depths, k, lo, tail, max_unit_bits, idx, val,
+                                ws, dev_status, as_stream(stream));
+}
+
+size_t fathom_scan_topk_noalloc_capacity(void) { return scratch_capacity(); }
+
+fathom_status fathom_scan_topk_noalloc(const uint64_t* planes, const uint16_t* scales, const int64_t* n, int U, int D,
+                                       int64_t nb_cap, const void* q, fathom_dtype qdt, int G, const uint8_t* depths,
+                                       int k, int64_t lo, int64_t tail, int max_unit_bits, int32_t* idx, float* val,
+                                       uint32_t* dev_status, void* stream) {
+  fathom_status e = check_store(planes, scales, n, U, D, nb_cap, q, qdt, G, depths);
+  if (e != FATHOM_OK) return e;
+  if (lo < 0 || tail < 0 || k < 1 || max_unit_bits < 0) return FATHOM_ERR_INVALID;
+  if (k > FATHOM_MAX_K) return FATHOM_ERR_UNSUPPORTED;
+  if (U == 0) return FATHOM_OK;
+  if (!idx || !aligned(idx, 4) || (val && !aligned(val, 4))) return FATHOM_ERR_INVALID;
+  if (scan_topk_ws(U, G, nb_cap * 64, k) > scratch_capacity()) return FATHOM_ERR_WORKSPACE;
+  void* ws = nullptr;
+  e = scratch_address(&ws);
+  if (e != FATHOM_OK) return e;
   return launch_scan_topk_fused(planes, scales, n, U, nb_cap, q, qdt, G, depths, k, lo, tail, max_unit_bits, idx, val,
                                 ws, dev_status, as_stream(stream));
 }

@@ -47,6 +47,7 @@
 // (FATHOM_DEV_TOPK_FALLBACK).  The result never depends on tau or the bucket
 // bounds; they only decide how much work is saved.
 #include <atomic>
+#include <mutex>
 
 #include "common.hpp"
 
@@ -1629,6 +1630,45 @@ fathom_status launch_scan_topk_fused(const uint64_t* planes, const uint16_t* sca
   hipLaunchKernelGGL(fused_rank_kernel, dim3(kSlots, R), dim3(kRankThreads), 0, s, fa, idx, val);
   hipLaunchKernelGGL(fused_select_kernel, dim3(R), dim3(kSelThreads), (size_t)kSelCap * 8, s, fa, idx, val);
   FATHOM_LAUNCH_CHECK();
+  return FATHOM_OK;
+}
+
+// ---------------------------------------------------------------- no workspace
+// fathom_scan_topk_noalloc's workspace: one file-scope array per device,
+// loaded with the code object and held until the process ends.  In host code
+// the name `scratch` is only a handle; its device address comes from
+// hipGetSymbolAddress, called once per device with that device current, and
+// only that address is passed to kernels.
+constexpr size_t kScratchBytes = (size_t)16 << 20;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+constexpr int kScratchDevices = 64;
+static std::atomic<void*> g_scratch_addr[kScratchDevices];
+static std::mutex g_scratch_mu;
+
+size_t scratch_capacity() { return kScratchBytes; }
+
+// The current device's address of `scratch` (looked up on its first use).
+fathom_status scratch_address(void** out) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) {
+    (void)hipGetLastError();
+    return FATHOM_ERR_HIP;
+  }
+  if (dev < 0 || dev >= kScratchDevices) return FATHOM_ERR_UNSUPPORTED;
+  void* p = g_scratch_addr[dev].load(std::memory_order_acquire);
+  if (!p) {
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    p = g_scratch_addr[dev].load(std::memory_order_acquire);
+    if (!p) {
+      if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) {
+        (void)hipGetLastError();
+        return FATHOM_ERR_HIP;
+      }
+      g_scratch_addr[dev].store(p, std::memory_order_release);
+    }
+  }
+  *out = p;
   return FATHOM_OK;
 }
 

@@ -117,6 +117,16 @@ def test_host_validation(fl):
     ws2 = fl.fathom_scan_topk_workspace_size(1, 4, 4096, 64)
     assert L.fathom_scan_topk(FAKE, FAKE, FAKE, 1, 128, 64, FAKE, 1, 4, FAKE, 64, 0, 0, FAKE, NULL, FAKE, ws2 - 1,
                               NULL, S) == fl.FATHOM_ERR_WORKSPACE
+    # the no-workspace variant: a shape beyond the library's array, k too large, null idx (no HIP call made)
+    cap = fl.fathom_scan_topk_noalloc_capacity()
+    assert cap == 16 << 20
+    assert fl.fathom_scan_topk_workspace_size(64, 4, 1 << 20, 8192) > cap
+    assert L.fathom_scan_topk_noalloc(FAKE, FAKE, FAKE, 64, 128, 1 << 14, FAKE, 1, 4, FAKE, 8192, 0, 0, 0, FAKE,
+                                      NULL, NULL, S) == fl.FATHOM_ERR_WORKSPACE
+    assert L.fathom_scan_topk_noalloc(FAKE, FAKE, FAKE, 1, 128, 64, FAKE, 1, 4, FAKE, 9000, 0, 0, 0, FAKE, NULL,
+                                      NULL, S) == fl.FATHOM_ERR_UNSUPPORTED
+    assert L.fathom_scan_topk_noalloc(FAKE, FAKE, FAKE, 1, 128, 64, FAKE, 1, 4, FAKE, 64, 0, 0, 0, NULL, NULL,
+                                      NULL, S) == fl.FATHOM_ERR_INVALID
     # sparse attention: sink + local too large, odd ld_tok, null out
     wsa = fl.fathom_sparse_attn_workspace_size(1, 4, 8, 4, 32)
     assert wsa > 0
