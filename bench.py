@@ -693,6 +693,22 @@ def main():
     torch.cuda.synchronize()
     st_ms = float(np.mean([a.elapsed_time(b) for a, b in tev]))
 
+    # ---- the same call with one unit's 4 rows on the exact pass (its depths
+    # set to 100 bits, above the bound of 48): what a row the filter cannot
+    # serve costs
+    dx = d.clone()
+    dx[0] = torch.where(torch.arange(D, device=dev) < 25, 4, 0).to(torch.uint8)
+    stx = F.new_status(dev)
+    xev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+    for r in range(reps):
+        xev[r][0].record(stream)
+        F.fathom_scan_topk(planes[r % R], scales[r % R], n, q, dx, k, 0, 0, idx, val, ws, stx, max_unit_bits=max_bits)
+        xev[r][1].record(stream)
+    torch.cuda.synchronize()
+    exact_rows_ms = float(np.median([a.elapsed_time(b) for a, b in xev]))
+    exact_rows_status = int(stx.item()) & 0xFFFFFFFF
+    del dx
+
     # ---- the exact (unfused) scan kernel alone, for comparison
     dn = d.cpu().numpy().astype(np.int64)
     nh = n.cpu().numpy()
@@ -772,6 +788,7 @@ def main():
         "hbm_frac_of_stream_read": alg_bytes / (scan_topk_ms * 1e-3) / 1e9 / stream_gbps,
         "stages_ms": {"alloc+scan_topk": scan_topk_ms,
                       "alloc+scan_topk_graph_replay_median": float(np.median(graph_ms)), "sparse_attn": attn_ms, "scan_topk_call": st_ms,
+                      "scan_topk_call_one_unit_exact": exact_rows_ms,
                       "exact_scan_kernel": scan_ms, "pack_append_1_token_per_unit": append_ms,
                       "gather_host_store": gather_ms,
                       "prefill_pack_per_store": pack_ms},
@@ -779,6 +796,7 @@ def main():
         "active_channels_mean": active,
         "plane_bits_per_key_mean": float(dn.sum(1).mean()),
         "device_status": status,
+        "exact_rows_device_status": exact_rows_status,
         "roofline": {"bound": "hbm", "kernel": "fathom_scan_topk (every launch of one call)",
                      "achieved": st_gbps, "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": st_gbps / HBM_PEAK_GBPS,
                      "traffic": measured_traffic(), "alg_bytes_per_launch": alg_bytes, "avg_launch_ms": st_ms,

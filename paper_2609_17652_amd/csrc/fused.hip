@@ -67,8 +67,7 @@ constexpr int kSlots = 8;          // survivor value buckets per row
 constexpr int kSmpW = 8;           // sample proxies kept per (sampled wave, head)
 constexpr int kSampleQuads = 64;   // at most this many sampled quads per unit
 constexpr int kSmpRow = kSampleQuads * kSmpW;
-constexpr int kSelThreads = 1024;
-constexpr int kSelCap = 16384;     // LDS composites in the select kernel
+constexpr int kSelCap = 16384;     // survivor capacity of a row at most (4 buckets of the rank pass)
 constexpr int kThrMax = 1 << 18;   // |S| < 2^17 for A <= 128
 constexpr int kNoBound = 1 << 30;  // accumulator start: always (+) or never (-) a candidate
 constexpr int kMainWavesTarget = 2048;  // full-pass waves in flight over all units
@@ -86,6 +85,12 @@ struct FusedWs {
   uint32_t* bnd;    // [R][kSlots] score keys splitting a row's survivors into kSlots value buckets
   uint32_t* uovf;   // [U] from pass 2: (slices of the unit's filter, at least kNarrow + 1 for the wide pass) << 1, 0 = no filter
   float* samp;      // [R][kSmpRow] sampled proxies
+  uint32_t* xctl;   // [1 + R]: exact rows listed by pass 4, then per listed row the chunks merged so far
+  uint32_t* xrows;  // [R] rows the exact pass computes: row | kXDirect (direct rows) in list order
+  uint64_t* part;   // [R][xch][pk] per listed row and chunk: the chunk's top pk composites
+  uint32_t* pcnt;   // [R][xch] composites in each partial list
+  uint64_t* pmin;   // [R][xch] a lower bound on each full partial list's smallest composite (0: list not full)
+  int xch, pk;      // exact pass: chunks per row at most, partial list length
   int cap, scap;    // rows with at most cap eligible keys are scored directly; bucket capacity
   int64_t s_stride; // sample every s_stride-th quad
   int s_quads;      // sampled quads per unit
@@ -122,10 +127,41 @@ static inline void fused_geometry(int U, int64_t nb_cap, int64_t* stride, int* s
   *nwg = (waves + kFW - 1) / kFW;
 }
 
+// Exact pass geometry: a row's blocks in chunks of kXBlocks (one workgroup
+// each, at most kXChunks per row); each chunk keeps its top min(k, chunk keys).
+constexpr int kXBlocks = 256;
+constexpr int kXKeys = kXBlocks * kBlockTokens;  // 16384 keys per chunk
+constexpr int kXChunks = 64;
+constexpr uint32_t kXDirect = 0x80000000u;
+static inline int exact_chunks(int64_t nb_cap) {
+  const int64_t c = (nb_cap + kXBlocks - 1) / kXBlocks;
+  return (int)(c < 1 ? 1 : c > kXChunks ? kXChunks : c);
+}
+static inline int exact_pk(int k) { return k < kXKeys ? k : kXKeys; }
+// The head of every chunk's list: its top xs composites.  The merge reads the
+// heads, and a chunk's other composites only when its xs-th composite lies
+// above the k-th composite of the heads (so a chunk with more than xs of the
+// row's top k is read whole).
+__host__ __device__ inline int exact_pow2(int k) {  // the merge's sort length
+  int p = 2;
+  while (p < k) p <<= 1;
+  return p;
+}
+__host__ __device__ inline int exact_split(int k, int nz) {
+  int s = (2 * k + nz - 1) / nz;
+  if (s < 64) s = 64;
+  const int room = (2 * FATHOM_MAX_K - exact_pow2(k)) / nz;  // the heads share LDS with the sorted top k
+  if (s > room) s = room;
+  return s < k ? s : k;
+}
+
 size_t fused_ws_bytes(int R, int U, int64_t nb_cap, int k) {
   if (nb_cap < 1) nb_cap = 1;
+  const size_t xch = (size_t)exact_chunks(nb_cap), pk = (size_t)exact_pk(k);
   return a256((size_t)R * 4) + a256((size_t)R * kSlots * 4) + a256((size_t)R * kSlots * fused_scap(k) * 8) +
-         a256((size_t)U * 4) + a256((size_t)R * kSlots * 4) + a256((size_t)R * kSmpRow * 4);
+         a256((size_t)U * 4) + a256((size_t)R * kSlots * 4) + a256((size_t)R * kSmpRow * 4) +
+         a256((size_t)(1 + R) * 4) + a256((size_t)R * 4) + a256((size_t)R * xch * pk * 8) + a256((size_t)R * xch * 4) +
+         a256((size_t)R * xch * 8);
 }
 
 static FusedWs fused_carve(void* ws, int R, int U, int64_t nb_cap, int k) {
@@ -140,7 +176,14 @@ static FusedWs fused_carve(void* ws, int R, int U, int64_t nb_cap, int k) {
   w.cand = reinterpret_cast<uint64_t*>(p); p += a256((size_t)R * kSlots * w.scap * 8);
   w.uovf = reinterpret_cast<uint32_t*>(p); p += a256((size_t)U * 4);
   w.bnd = reinterpret_cast<uint32_t*>(p); p += a256((size_t)R * kSlots * 4);
-  w.samp = reinterpret_cast<float*>(p);
+  w.samp = reinterpret_cast<float*>(p); p += a256((size_t)R * kSmpRow * 4);
+  w.xch = exact_chunks(nb_cap);
+  w.pk = exact_pk(k);
+  w.xctl = reinterpret_cast<uint32_t*>(p); p += a256((size_t)(1 + R) * 4);
+  w.xrows = reinterpret_cast<uint32_t*>(p); p += a256((size_t)R * 4);
+  w.part = reinterpret_cast<uint64_t*>(p); p += a256((size_t)R * w.xch * w.pk * 8);
+  w.pcnt = reinterpret_cast<uint32_t*>(p); p += a256((size_t)R * w.xch * 4);
+  w.pmin = reinterpret_cast<uint64_t*>(p);
   return w;
 }
 
@@ -1109,6 +1152,9 @@ __global__ __launch_bounds__(kTauThreads) void fused_tau_kernel(FusedArgs a) {
   if (tid < kSlots) {
     a.ws.cnt[r * kSlots + tid] = 0u;
     a.ws.bnd[r * kSlots + tid] = 0u;
+  } else if (tid == kSlots) {
+    a.ws.xctl[1 + r] = 0u;
+    if (r == 0) a.ws.xctl[0] = 0u;
   }
   int64_t nu, lo, hi;
   row_window(a, u, &nu, &lo, &hi, false);
@@ -1273,25 +1319,6 @@ __device__ __forceinline__ float key_to_score(uint32_t key) {
   return __uint_as_float((key & 0x80000000u) ? (key & 0x7FFFFFFFu) : ~key);
 }
 
-// Exact documented score of key (block b, bit) for head h of unit u, for
-// the fallback path (channels ascending from the act list).
-__device__ __forceinline__ float exact_score1(const int* act, int A, const float* qh, const FusedArgs& a, int u,
-                                              int64_t b, int bit) {
-  const uint64_t* Pu = a.planes + (int64_t)u * kD * kPlanes * a.nb_cap + b;
-  const uint16_t* Su = a.scales + (int64_t)u * kD * a.nb_cap + b;
-  float acc = 0.0f;
-  for (int ai = 0; ai < A; ++ai) {
-    const int e = act[ai], j = e & 0xFF, t = e >> 8;
-    const float af = half_bits_to_float(Su[(int64_t)j * a.nb_cap]);
-    uint32_t c = 0;
-    for (int p = 0; p < t; ++p) c = 2u * c + (uint32_t)((Pu[(int64_t)(4 * j + p) * a.nb_cap] >> bit) & 1ull);
-    const float y = (float)c + (0.5f - (float)(1 << (t - 1)));
-    const float khat = __fmul_rn(y, __fmul_rn(af, __uint_as_float((uint32_t)(128 - t) << 23)));
-    acc = __fmaf_rn(qh[ai], khat, acc);
-  }
-  return acc;
-}
-
 // The survivors of row r (bucket counts cnt8) hold its top k exactly when no
 // bucket overflowed, at least k were found and the filter ran for the row.
 // The row's survivor lists determine its top k exactly when at least k keys
@@ -1309,112 +1336,6 @@ __device__ __forceinline__ bool survivors_complete(const uint32_t* cnt8, const F
     C += cnt8[z];
   }
   return !over && C >= (uint32_t)a.k && (ovf & 1u) == 0u && tau != kNegInf;
-}
-
-// Pass 4 (exact rows), one 1024-thread workgroup per row.  A row with no more
-// eligible keys than the survivor lists hold is scored directly, and a row
-// whose filter under-collected (or whose lists overflowed) is recomputed
-// exactly, both with a streaming top-k over exact scores.  Every other row is
-// left to fused_rank_kernel.
-__global__ __launch_bounds__(kSelThreads) void fused_select_kernel(FusedArgs a, int32_t* __restrict__ idx,
-                                                                   float* __restrict__ val) {
-  extern __shared__ uint64_t buf[];
-  __shared__ int act[kD];          // active channels ascending (streaming path)
-  __shared__ float qa[kD];         // q of this row's head per active channel
-  __shared__ int nact;
-  __shared__ int s_count;
-  __shared__ uint64_t s_thr;
-  __shared__ int wc[2];
-  __shared__ uint32_t s_sub[kSlots];
-  const int G = a.G;
-  const int r = blockIdx.x, u = r / G, h = r % G, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  int64_t nu, lo, hi;
-  row_window(a, u, &nu, &lo, &hi, false);
-  const int k = a.k;
-  if (tid < kSlots) s_sub[tid] = gload(a.ws.cnt + r * kSlots + tid);
-  if (tid == 0) {
-    s_count = 0;
-    s_thr = 0ull;
-  }
-  __syncthreads();
-  const bool direct = hi - lo <= a.ws.cap;
-  const bool fallback = !direct && !survivors_complete(s_sub, a, gload(a.ws.tau + r), gload(a.ws.uovf + u));
-  if (!direct && !fallback) return;
-  // streaming top-k over all eligible keys with exact scores
-  {
-    int t = 0;
-    if (tid < kD) {
-      t = gload(a.depths + (int64_t)u * kD + tid);
-      t = t > kPlanes ? kPlanes : t;
-    }
-    const bool on = tid < kD && t > 0;
-    const uint64_t m = __ballot(on);
-    if (tid < kD && lane == 0) wc[wave] = __popcll(m);
-    __syncthreads();
-    if (on) act[(wave == 1 ? wc[0] : 0) + __popcll(m & lanemask_lt(lane))] = tid | (t << 8);
-    if (tid == 0) {
-      nact = wc[0] + wc[1];
-      if (fallback) set_status(a.st, FATHOM_DEV_TOPK_FALLBACK);
-    }
-    __syncthreads();
-    for (int x = tid; x < nact; x += kSelThreads)
-      qa[x] = load_q(a.q, a.qdt, ((int64_t)u * G + h) * kD + (act[x] & 0xFF));
-    __syncthreads();
-  }
-  const int A = nact;
-  const int nwaves = kSelThreads / kWave;
-  const int64_t bfirst = lo / kBlockTokens, bend = (hi + kBlockTokens - 1) / kBlockTokens;
-  for (int64_t bb = bfirst; bb < bend; bb += nwaves) {
-    const int64_t b = bb + wave;
-    const int64_t i = b * kBlockTokens + lane;
-    const bool elig = b < bend && i >= lo && i < hi;
-    uint64_t comp = 0ull;
-    if (elig) {
-      const float s = exact_score1(act, A, qa, a, u, b, lane);
-      comp = ((uint64_t)score_key(s) << 32) | (uint64_t)(~(uint32_t)i);
-    }
-    const uint64_t thr = s_thr;
-    const bool add = elig && comp > thr;
-    const uint64_t bm = __ballot(add);
-    if (bm) {
-      int basep = 0;
-      const int leader = __ffsll((unsigned long long)bm) - 1;
-      if (lane == leader) basep = atomicAdd(&s_count, __popcll(bm));
-      basep = __shfl(basep, leader, kWave);
-      if (add) buf[basep + __popcll(bm & lanemask_lt(lane))] = comp;
-    }
-    __syncthreads();
-    if (s_count > kSelCap - kSelThreads) {  // room for one more round
-      for (int x = s_count + tid; x < kSelCap; x += kSelThreads) buf[x] = 0ull;
-      __syncthreads();
-      bitonic_desc(buf, kSelCap);
-      if (tid == 0) {
-        s_count = k;
-        s_thr = buf[k - 1];
-      }
-      for (int x = k + tid; x < kSelCap; x += kSelThreads) buf[x] = 0ull;
-      __syncthreads();
-    }
-  }
-  const int count = s_count;
-  int P2 = 2;  // the sort takes at least one pair; every slot past count is zeroed
-  while (P2 < count) P2 <<= 1;
-  for (int x = count + tid; x < P2; x += kSelThreads) buf[x] = 0ull;
-  __syncthreads();
-  bitonic_desc(buf, P2);
-  bool shortfall = false;
-  for (int x = tid; x < k; x += kSelThreads) {
-    const uint64_t c = x < count ? buf[x] : 0ull;
-    if (c == 0ull) {
-      idx[(int64_t)r * k + x] = -1;
-      if (val) val[(int64_t)r * k + x] = __uint_as_float(0x7FC00000u);
-      shortfall = true;
-    } else {
-      idx[(int64_t)r * k + x] = (int32_t)(~(uint32_t)(c & 0xFFFFFFFFull));
-      if (val) val[(int64_t)r * k + x] = key_to_score((uint32_t)(c >> 32));
-    }
-  }
-  if (__syncthreads_or(shortfall) && tid == 0) set_status(a.st, FATHOM_DEV_TOPK_SHORT);
 }
 
 // Pass 4 (filtered rows): workgroup (z, r) orders the survivors of value
@@ -1457,7 +1378,14 @@ __global__ __launch_bounds__(kRankThreads) void fused_rank_kernel(FusedArgs a, i
   if (nu < 0 || nu > a.nb_cap * kBlockTokens) nu = 0;
   int64_t lo = a.lo, hi = nu - a.tail;
   if (hi < lo) hi = lo;
-  if (hi - lo <= a.ws.cap || !survivors_complete(s_cnt, a, s_tau, s_ovf)) return;
+  const bool direct = hi - lo <= a.ws.cap;
+  if (direct || !survivors_complete(s_cnt, a, s_tau, s_ovf)) {
+    if (z == 0 && tid == 0) {  // the exact pass computes this row
+      const uint32_t j = gatomic_add(a.ws.xctl, 1u);
+      gstore(a.ws.xrows + j, (uint32_t)r | (direct ? kXDirect : 0u));
+    }
+    return;
+  }
   uint32_t off0 = 0;
   for (int y = 0; y < z; ++y) off0 += s_cnt[y];
   const int c = (int)s_cnt[z], k = a.k;
@@ -1547,6 +1475,409 @@ __global__ __launch_bounds__(kRankThreads) void fused_rank_kernel(FusedArgs a, i
   }
 }
 
+// ---------------------------------------------------------------- pass 5
+// The exact pass: the rows pass 4 listed (direct rows, and rows whose survivor
+// lists do not determine the top k) are computed from exact documented scores.
+// Workgroup (z, s) takes chunk z of the listed rows s, s + kXSlots, ...: the
+// exact scores of the chunk's keys go to LDS (kXKeys at a time), and the
+// chunk's top min(k, keys) composites (score key << 32 | ~index) to its
+// partial list; the workgroup that completes a row's last chunk selects the
+// row's top k from its partial lists, orders them and writes the row.  Every
+// selection is exact (a radix select on the composites, which are distinct),
+// so the result is the documented top k whatever the chunking.
+constexpr int kXThreads = 1024;
+constexpr int kXWaves = kXThreads / kWave;  // blocks scored per stage, one per wave
+constexpr int kXSlots = 4;                  // listed rows in flight (grid y)
+constexpr int kXMaxCells = kD * kPlanes;    // (channel, plane) cells of a unit at most
+constexpr int kXPre = kXMaxCells * kXWaves / kXThreads;  // plane words staged per thread at most
+constexpr int kXPreS = kD * kXWaves / kXThreads;         // scales staged per thread at most
+static_assert(kXPre == 8 && kXPreS == 2, "staging registers");
+constexpr size_t kXLdsKeys = (size_t)kXKeys * 4;
+constexpr size_t kXLdsStw = (size_t)kXMaxCells * kXWaves * 8;  // [block][half][4 slots per channel] u32
+constexpr size_t kXLdsSts = (size_t)kD * kXWaves * 8;
+constexpr size_t kXLdsTab = (size_t)kD * 4 * 2 + (size_t)kXMaxCells * 4;
+constexpr size_t kXLdsHist = 2048 * 4;  // radix histogram; the merge's crossing digit
+constexpr size_t kXLdsBytes = kXLdsKeys + kXLdsStw + kXLdsSts + kXLdsTab + kXLdsHist;
+static_assert(kXLdsKeys + kXLdsStw >= (size_t)2 * FATHOM_MAX_K * 8, "merge buffer: candidates, then the top k");
+static_assert(kXLdsBytes <= 156 * 1024, "exact pass LDS (plus its static part) within one CU's 160 KB");
+
+struct XShared {
+  uint32_t part[kXWaves];
+  int digit;
+  uint32_t above;
+  uint32_t cnt;
+  uint32_t last;
+  uint64_t lb;
+  int A, cells;
+  int wc[2], wt[2];
+  uint32_t pc[kXChunks];
+  uint64_t ps[kXChunks];
+};
+
+// The largest composite T with #{v >= T} >= need over the elements `each`
+// visits (every thread visits its share; need <= their number): an MSB-first
+// radix select, 11/11/10 bits per word, that stops once every element with
+// the fixed prefix is needed.  Then #{v >= T} == need exactly (composites
+// are distinct).  hist holds 2048 words.
+template <class Each>
+__device__ uint64_t select_threshold(Each each, uint32_t need, uint32_t* hist, XShared& S) {
+  uint64_t prefix = 0ull, mask = 0ull;
+  const int tid = threadIdx.x, nt = blockDim.x;
+  for (int pass = 0; pass < 6; ++pass) {
+    const int bits = (pass % 3 == 2) ? 10 : 11;
+    const int sh = (pass < 3 ? 32 : 0) + (pass % 3 == 0 ? 21 : pass % 3 == 1 ? 10 : 0);
+    const int nb = 1 << bits;
+    const uint64_t dm = (uint64_t)(nb - 1);
+    for (int x = tid; x < nb; x += nt) hist[x] = 0u;
+    __syncthreads();
+    each([&](uint64_t v) {
+      if ((v & mask) == prefix) atomicAdd(&hist[(v >> sh) & dm], 1u);
+    });
+    __syncthreads();
+    find_crossing(hist, nb, need, S.part, &S.digit, &S.above);
+    const int d = S.digit;
+    const uint32_t above = S.above, at = hist[d];
+    prefix |= (uint64_t)d << sh;
+    mask |= dm << sh;
+    need -= above;
+    __syncthreads();  // hist and the crossing read by all before the next pass
+    if (at == need) break;
+  }
+  return prefix;
+}
+
+__device__ __forceinline__ uint64_t key_composite(uint32_t key, int64_t i) {
+  return ((uint64_t)key << 32) | (uint64_t)(~(uint32_t)i);
+}
+
+__global__ __launch_bounds__(kXThreads) void fused_exact_kernel(FusedArgs a, int32_t* __restrict__ idx,
+                                                                float* __restrict__ val) {
+  extern __shared__ __align__(16) unsigned char xl[];
+  uint32_t* keys = reinterpret_cast<uint32_t*>(xl);
+  uint32_t* stw = reinterpret_cast<uint32_t*>(xl + kXLdsKeys);
+  uint64_t* sel = reinterpret_cast<uint64_t*>(xl + kXLdsKeys);  // a pass's selection (stw is free then)
+  float2* sts = reinterpret_cast<float2*>(xl + kXLdsKeys + kXLdsStw);  // [channel][block] (a16 / 8, z a16 / 8)
+  int* act = reinterpret_cast<int*>(xl + kXLdsKeys + kXLdsStw + kXLdsSts);
+  float* qa = reinterpret_cast<float*>(act + kD);
+  uint32_t* crow = reinterpret_cast<uint32_t*>(qa + kD);  // cell c: plane row 4 j + p | slot 4 a + p << 9
+  uint32_t* hist = reinterpret_cast<uint32_t*>(xl + kXLdsKeys + kXLdsStw + kXLdsSts + kXLdsTab);
+  uint64_t* mbuf = reinterpret_cast<uint64_t*>(xl);  // merge: candidates [0, 2 FATHOM_MAX_K - k), then the top k
+  __shared__ XShared S;
+  const int z = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int G = a.G, k = a.k, pk = a.ws.pk;
+  const uint32_t nx = gload(a.ws.xctl);
+  for (uint32_t j = blockIdx.y; j < nx; j += gridDim.y) {
+    const uint32_t code = gload(a.ws.xrows + j);
+    const int r = (int)(code & ~kXDirect), u = r / G, h = r % G;
+    const bool direct = (code & kXDirect) != 0u;
+    int64_t nu, lo, hi;
+    row_window(a, u, &nu, &lo, &hi, false);
+    const int64_t bfirst = lo / kBlockTokens, bend = hi > lo ? (hi + kBlockTokens - 1) / kBlockTokens : bfirst;
+    const int64_t rb = bend - bfirst;  // blocks holding eligible keys
+    int nz = (int)((rb + kXBlocks - 1) / kXBlocks);
+    if (nz > a.ws.xch) nz = a.ws.xch;
+    if (nz < 1) nz = 1;
+    if (z >= nz) continue;
+    const int64_t cbk = (rb + nz - 1) / nz;  // blocks per chunk
+    const int64_t cb0 = bfirst + z * cbk, cb1 = cb0 + cbk < bend ? cb0 + cbk : bend;
+    // ---- the row's active channels ascending, their q, and their cells: cell
+    // (channel a, plane p) is staged in slot 4 a + p, so a channel's words are
+    // one aligned 16-byte read
+    {
+      int t = 0;
+      if (tid < kD) {
+        t = gload(a.depths + (int64_t)u * kD + tid);
+        t = t > kPlanes ? kPlanes : t;
+      }
+      const int on = tid < kD && t > 0, tc = tid < kD ? t : 0;
+      int ion = on, itc = tc;  // inclusive scans within the wave
+#pragma unroll
+      for (int o = 1; o < kWave; o <<= 1) {
+        const int x0 = __shfl_up(ion, o, kWave), x1 = __shfl_up(itc, o, kWave);
+        if (lane >= o) {
+          ion += x0;
+          itc += x1;
+        }
+      }
+      if (wave < 2 && lane == kWave - 1) {
+        S.wc[wave] = ion;
+        S.wt[wave] = itc;
+      }
+      __syncthreads();
+      if (tid < kD && on) {
+        const int ai = ion - 1 + (wave == 1 ? S.wc[0] : 0);
+        const int c0 = itc - t + (wave == 1 ? S.wt[0] : 0);
+        act[ai] = tid | (t << 8);
+        qa[ai] = load_q(a.q, a.qdt, ((int64_t)u * G + h) * kD + tid);
+        for (int p = 0; p < t; ++p) crow[c0 + p] = (uint32_t)((kPlanes * tid + p) | ((kPlanes * ai + p) << 9));
+      }
+      if (tid == 0) {
+        S.A = S.wc[0] + S.wc[1];
+        S.cells = S.wt[0] + S.wt[1];
+      }
+      __syncthreads();
+    }
+    const int A = S.A, nc = S.cells, ns = kPlanes * A;  // slots per (block, half)
+    const uint64_t* Pu = a.planes + (int64_t)u * kD * kPlanes * a.nb_cap;
+    const uint16_t* Su = a.scales + (int64_t)u * kD * a.nb_cap;
+    uint32_t lcnt = 0;      // composites in this chunk's partial list so far
+    uint64_t lsplit = 0ull; // its top min(lcnt, xs) composites are those >= lsplit
+    uint64_t* plist = a.ws.part + ((int64_t)j * a.ws.xch + z) * pk;
+    for (int64_t pb0 = cb0; pb0 < cb1; pb0 += kXBlocks) {  // passes of at most kXKeys keys
+      const int64_t pb1 = pb0 + kXBlocks < cb1 ? pb0 + kXBlocks : cb1;
+      // ---- exact scores of blocks [pb0, pb1) into keys[]: 16 blocks per stage
+      // (one per wave).  Plane words are staged as 32-bit halves, [block][half]
+      // [slot]; scales as fp32 times 2^(1-t), [channel][block].  The next
+      // stage's words are loaded while this one is scored.
+      uint64_t pw[kXPre];
+      float2 ps[kXPreS];
+      auto issue = [&](int64_t s0) {
+#pragma unroll
+        for (int i = 0; i < kXPre; ++i) {
+          const int x = tid + i * kXThreads;
+          pw[i] = 0ull;
+          const int64_t b = s0 + (x & (kXWaves - 1));
+          if (x < nc * kXWaves && b < pb1)
+            pw[i] = gload(Pu + (int64_t)(crow[x / kXWaves] & 0x1FF) * a.nb_cap + b);
+        }
+#pragma unroll
+        for (int i = 0; i < kXPreS; ++i) {
+          const int x = tid + i * kXThreads;
+          ps[i] = make_float2(0.0f, 0.0f);
+          const int64_t b = s0 + (x & (kXWaves - 1));
+          if (x < A * kXWaves && b < pb1) {
+            // khat = (c^(t) + 1/2 - 2^(t-1)) a16 2^(1-t) = (u + 2^(3-t) - 8) a16 / 8 with
+            // u = c^(t) 2^(4-t) the prefix digit: both terms exact in fp32
+            const int e = act[x / kXWaves], t = e >> 8;
+            const float s8 = __fmul_rn(half_bits_to_float(gload(Su + (int64_t)(e & 0xFF) * a.nb_cap + b)), 0.125f);
+            ps[i] = make_float2(s8, __fmul_rn(__fmul_rn((float)(16 >> t), 0.5f) - 8.0f, s8));
+          }
+        }
+      };
+      for (int x = tid; x < 2 * kXWaves * ns; x += kXThreads) stw[x] = 0u;  // planes p >= t read as 0
+      __syncthreads();
+      issue(pb0);
+      for (int64_t s0 = pb0; s0 < pb1; s0 += kXWaves) {
+#pragma unroll
+        for (int i = 0; i < kXPre; ++i) {
+          const int x = tid + i * kXThreads;
+          if (x < nc * kXWaves) {
+            const int bb = x & (kXWaves - 1), slot = crow[x / kXWaves] >> 9;
+            stw[(2 * bb) * ns + slot] = (uint32_t)pw[i];
+            stw[(2 * bb + 1) * ns + slot] = (uint32_t)(pw[i] >> 32);
+          }
+        }
+#pragma unroll
+        for (int i = 0; i < kXPreS; ++i) {
+          const int x = tid + i * kXThreads;
+          if (x < A * kXWaves) sts[x] = ps[i];
+        }
+        __syncthreads();
+        if (s0 + kXWaves < pb1) issue(s0 + kXWaves);
+        const int64_t b = s0 + wave;
+        if (b < pb1) {
+          // lane's half of every staged word: one aligned 16-byte read per channel
+          const uint4* wrow = reinterpret_cast<const uint4*>(stw) + (2 * wave + (lane >> 5)) * A;
+          const float2* srow = sts + wave;
+          const uint32_t bit = (uint32_t)(lane & 31);
+          float acc = 0.0f;
+#pragma unroll 4
+          for (int ai = 0; ai < A; ++ai) {
+            const uint4 w4 = wrow[ai];
+            const float2 sb = srow[ai * kXWaves];
+            const uint32_t ud = (__builtin_amdgcn_ubfe(w4.x, bit, 1) << 3) | (__builtin_amdgcn_ubfe(w4.y, bit, 1) << 2) |
+                                (__builtin_amdgcn_ubfe(w4.z, bit, 1) << 1) | __builtin_amdgcn_ubfe(w4.w, bit, 1);
+            acc = __fmaf_rn(qa[ai], __fmaf_rn((float)ud, sb.x, sb.y), acc);
+          }
+          keys[(b - pb0) * kBlockTokens + lane] = score_key(acc);
+        }
+        __syncthreads();
+      }
+      // ---- eligible positions of this pass; the chunk's running top pk
+      const int64_t kb = pb0 * kBlockTokens;
+      const int p_lo = (int)(lo > kb ? lo - kb : 0);
+      const int64_t pe = hi - kb < (pb1 - pb0) * kBlockTokens ? hi - kb : (pb1 - pb0) * kBlockTokens;
+      const int p_hi = (int)(pe > p_lo ? pe : p_lo);
+      const uint32_t m = (uint32_t)(p_hi - p_lo) + lcnt;  // candidates: this pass and the list so far
+      const uint32_t take = m < (uint32_t)pk ? m : (uint32_t)pk;
+      auto each = [&](auto f) {
+        for (int p = p_lo + tid; p < p_hi; p += kXThreads) f(key_composite(keys[p], kb + p));
+        for (uint32_t e = tid; e < lcnt; e += kXThreads) f(plist[e]);
+      };
+      uint64_t T = 0ull;
+      if (m > take) T = select_threshold(each, take, hist, S);
+      if (tid == 0) S.cnt = 0u;
+      __syncthreads();
+      each([&](uint64_t v) {
+        if (v >= T) {
+          const uint32_t pos = atomicAdd(&S.cnt, 1u);
+          if (pos < take) sel[pos] = v;
+        }
+      });
+      __syncthreads();
+      lcnt = take;
+      if (pb0 + kXBlocks < cb1) {  // another pass follows: the list as it stands
+        for (uint32_t e = tid; e < take; e += kXThreads) gstore(plist + e, sel[e]);
+        __syncthreads();
+        continue;
+      }
+      // the chunk's final list: its top xs composites (those >= lsplit) first,
+      // then the rest (all below lsplit)
+      const uint32_t xs = (uint32_t)exact_split(k, nz);
+      lsplit = 0ull;
+      if (take > xs) {
+        auto es = [&](auto f) {
+          for (uint32_t e = tid; e < take; e += kXThreads) f(sel[e]);
+        };
+        lsplit = select_threshold(es, xs, hist, S);
+      }
+      if (tid == 0) {
+        S.cnt = 0u;
+        S.above = 0u;
+      }
+      __syncthreads();
+      for (uint32_t e = tid; e < take; e += kXThreads) {
+        const uint64_t v = sel[e];
+        if (v >= lsplit) gstore(plist + atomicAdd(&S.cnt, 1u), v);
+        else gstore(plist + xs + atomicAdd(&S.above, 1u), v);
+      }
+      __syncthreads();
+    }
+    if (tid == 0) {
+      gstore(a.ws.pcnt + (int64_t)j * a.ws.xch + z, lcnt);
+      gstore(a.ws.pmin + (int64_t)j * a.ws.xch + z, lsplit);
+    }
+    // ---- arrive; the last chunk of the row merges
+    __threadfence();
+    __syncthreads();
+    if (tid == 0) {
+      const uint32_t prev = __hip_atomic_fetch_add((__attribute__((address_space(1))) uint32_t*)(a.ws.xctl + 1 + j),
+                                                   1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+      S.last = prev == (uint32_t)(nz - 1) ? 1u : 0u;
+    }
+    __syncthreads();
+    if (S.last) {
+      __threadfence();
+      if (tid < nz) {
+        const int64_t o = (int64_t)j * a.ws.xch + tid;
+        S.pc[tid] = __hip_atomic_load((__attribute__((address_space(1))) uint32_t*)(a.ws.pcnt + o), __ATOMIC_RELAXED,
+                                      __HIP_MEMORY_SCOPE_AGENT);
+        S.ps[tid] = __hip_atomic_load((__attribute__((address_space(1))) uint64_t*)(a.ws.pmin + o), __ATOMIC_RELAXED,
+                                      __HIP_MEMORY_SCOPE_AGENT);
+      }
+      if (tid == 0) {
+        S.cnt = 0u;
+        S.above = 0u;
+      }
+      __syncthreads();
+      const uint64_t* rl = a.ws.part + (int64_t)j * a.ws.xch * pk;
+      const uint32_t xs = (uint32_t)exact_split(k, nz);
+      const uint32_t capm = (uint32_t)(2 * FATHOM_MAX_K - exact_pow2(k));  // candidates in LDS at most
+      uint64_t* top = mbuf + capm;                              // the row's top k, then ordered
+      // (1) the heads (each list's top xs) into LDS
+      for (int y = wave; y < nz; y += kXWaves) {
+        const uint32_t hy = S.pc[y] < xs ? S.pc[y] : xs;
+        uint32_t base = 0u;
+        if (lane == 0) base = atomicAdd(&S.cnt, hy);
+        base = __shfl(base, 0, kWave);
+        for (uint32_t e = lane; e < hy; e += kWave) mbuf[base + e] = gload(rl + (int64_t)y * pk + e);
+      }
+      __syncthreads();
+      const uint32_t H = S.cnt;
+      // (2) L = the k-th composite of the heads: at most the row's k-th composite
+      uint64_t L = 0ull;
+      if (H > (uint32_t)k) {
+        auto eh = [&](auto f) {
+          for (uint32_t e = tid; e < H; e += kXThreads) f(mbuf[e]);
+        };
+        L = select_threshold(eh, (uint32_t)k, hist, S);
+      }
+      // (3) the rest of every list whose xs-th composite lies above L (its
+      // other composites may reach L); composites below L are not needed
+      if (tid == 0) S.cnt = H;
+      __syncthreads();
+      for (int y = wave; y < nz; y += kXWaves) {
+        if (S.pc[y] <= xs || S.ps[y] <= L) continue;  // the rest is below the split, itself <= L
+        const uint64_t* Ly = rl + (int64_t)y * pk;
+        for (uint32_t e0 = xs; e0 < S.pc[y]; e0 += kWave) {
+          const uint32_t e = e0 + lane;
+          const uint64_t v = e < S.pc[y] ? gload(Ly + e) : 0ull;
+          const bool keep = e < S.pc[y] && v >= L;
+          const uint64_t bm = __ballot(keep);
+          if (bm) {
+            uint32_t base = 0u;
+            if (lane == 0) base = atomicAdd(&S.cnt, (uint32_t)__popcll(bm));
+            base = __shfl(base, 0, kWave);
+            const uint32_t pos = base + (uint32_t)__popcll(bm & lanemask_lt(lane));
+            if (keep && pos < capm) mbuf[pos] = v;
+          }
+        }
+      }
+      __syncthreads();
+      const uint32_t M = S.cnt;  // heads and kept rests
+      uint32_t Mall = 0;
+      for (int y = 0; y < nz; ++y) Mall += S.pc[y];
+      const uint32_t take = Mall < (uint32_t)k ? Mall : (uint32_t)k;
+      uint64_t T = 0ull;
+      if (M <= capm) {
+        auto each = [&](auto f) {
+          for (uint32_t e = tid; e < M; e += kXThreads) {
+            const uint64_t v = mbuf[e];
+            if (v >= L) f(v);
+          }
+        };
+        if (Mall > take) T = select_threshold(each, take, hist, S);
+        if (tid == 0) S.cnt = 0u;
+        __syncthreads();
+        each([&](uint64_t v) {
+          if (v >= T) {
+            const uint32_t pos = atomicAdd(&S.cnt, 1u);
+            if (pos < take) top[pos] = v;
+          }
+        });
+      } else {  // more candidates than LDS holds (heavy ties): select from the lists themselves
+        auto each = [&](auto f) {
+          for (int y = 0; y < nz; ++y)
+            for (uint32_t e = tid; e < S.pc[y]; e += kXThreads) {
+              const uint64_t v = rl[(int64_t)y * pk + e];
+              if (v >= L) f(v);
+            }
+        };
+        T = select_threshold(each, take, hist, S);
+        if (tid == 0) S.cnt = 0u;
+        __syncthreads();
+        each([&](uint64_t v) {
+          if (v >= T) {
+            const uint32_t pos = atomicAdd(&S.cnt, 1u);
+            if (pos < take) top[pos] = v;
+          }
+        });
+      }
+      __syncthreads();
+      int P2 = 2;
+      while (P2 < (int)take) P2 <<= 1;
+      for (int x = (int)take + tid; x < P2; x += kXThreads) top[x] = 0ull;
+      __syncthreads();
+      bitonic_desc(top, P2);
+      bool shortfall = false;
+      for (int x = tid; x < k; x += kXThreads) {
+        if (x < (int)take) {
+          const uint64_t c = top[x];
+          idx[(int64_t)r * k + x] = (int32_t)(~(uint32_t)(c & 0xFFFFFFFFull));
+          if (val) val[(int64_t)r * k + x] = key_to_score((uint32_t)(c >> 32));
+        } else {
+          idx[(int64_t)r * k + x] = -1;
+          if (val) val[(int64_t)r * k + x] = __uint_as_float(0x7FC00000u);
+          shortfall = true;
+        }
+      }
+      if (__syncthreads_or(shortfall) && tid == 0) set_status(a.st, FATHOM_DEV_TOPK_SHORT);
+      if (tid == 0 && !direct) set_status(a.st, FATHOM_DEV_TOPK_FALLBACK);
+    }
+    __syncthreads();  // LDS reused by the next listed row
+  }
+}
+
 // nb_cap == 0: every row is empty (n[u] > 0 is out of range for such a store)
 __global__ void fused_empty_kernel(const int64_t* __restrict__ n, int G, int k, int32_t* __restrict__ idx,
                                    float* __restrict__ val, uint32_t* __restrict__ st) {
@@ -1568,7 +1899,7 @@ fathom_status launch_scan_topk_fused(const uint64_t* planes, const uint16_t* sca
     FATHOM_LAUNCH_CHECK();
     return FATHOM_OK;
   }
-  // the select kernel's dynamic LDS limit, raised once per device (racing
+  // the exact pass's dynamic LDS limit, raised once per device (racing
   // callers may both set it; the call is idempotent)
   static std::atomic<uint64_t> attr_set{0};
   int dev = 0;
@@ -1578,8 +1909,8 @@ fathom_status launch_scan_topk_fused(const uint64_t* planes, const uint16_t* sca
   }
   const uint64_t bit = dev < 64 ? 1ull << dev : 0ull;
   if (!bit || !(attr_set.load(std::memory_order_acquire) & bit)) {
-    if (hipFuncSetAttribute(reinterpret_cast<const void*>(&fused_select_kernel),
-                            hipFuncAttributeMaxDynamicSharedMemorySize, kSelCap * 8) != hipSuccess) {
+    if (hipFuncSetAttribute(reinterpret_cast<const void*>(&fused_exact_kernel),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)kXLdsBytes) != hipSuccess) {
       (void)hipGetLastError();
       return FATHOM_ERR_HIP;
     }
@@ -1628,7 +1959,8 @@ fathom_status launch_scan_topk_fused(const uint64_t* planes, const uint16_t* sca
     }
   }
   hipLaunchKernelGGL(fused_rank_kernel, dim3(kSlots, R), dim3(kRankThreads), 0, s, fa, idx, val);
-  hipLaunchKernelGGL(fused_select_kernel, dim3(R), dim3(kSelThreads), (size_t)kSelCap * 8, s, fa, idx, val);
+  hipLaunchKernelGGL(fused_exact_kernel, dim3((unsigned)fa.ws.xch, (unsigned)kXSlots), dim3(kXThreads), kXLdsBytes,
+                     s, fa, idx, val);
   FATHOM_LAUNCH_CHECK();
   return FATHOM_OK;
 }
@@ -1639,7 +1971,7 @@ fathom_status launch_scan_topk_fused(const uint64_t* planes, const uint16_t* sca
 // the name `scratch` is only a handle; its device address comes from
 // hipGetSymbolAddress, called once per device with that device current, and
 // only that address is passed to kernels.
-constexpr size_t kScratchBytes = (size_t)16 << 20;
+constexpr size_t kScratchBytes = (size_t)64 << 20;
 static __device__ __align__(256) unsigned char scratch[kScratchBytes];
 
 constexpr int kScratchDevices = 64;

@@ -61,8 +61,9 @@ def test_workspace_sizes(fl):
     b = fl.fathom_topk_workspace_size(8, 4, 1 << 20, 4096)
     assert 0 < a < b
     s = fl.fathom_scan_topk_workspace_size(8, 4, 1 << 20, 2048)
-    # the fused scan + top-k keeps no score array: far below 8 x 4 x 2^20 fp32 scores
-    assert 0 < s < 8 * 4 * (1 << 20) * 4 // 8
+    # the fused scan + top-k keeps no score array: well below 8 x 4 x 2^20 fp32 scores
+    # (the exact pass's per-chunk partial lists are its largest part)
+    assert 0 < s < 8 * 4 * (1 << 20) * 4 // 3
     assert fl.fathom_topk_workspace_size(0, 4, 10, 10) == 0
 
 
@@ -119,8 +120,9 @@ def test_host_validation(fl):
                               NULL, S) == fl.FATHOM_ERR_WORKSPACE
     # the no-workspace variant: a shape beyond the library's array, k too large, null idx (no HIP call made)
     cap = fl.fathom_scan_topk_noalloc_capacity()
-    assert cap == 16 << 20
+    assert cap == 64 << 20
     assert fl.fathom_scan_topk_workspace_size(64, 4, 1 << 20, 8192) > cap
+    assert fl.fathom_scan_topk_workspace_size(8, 4, 1 << 20, 2048) <= cap
     assert L.fathom_scan_topk_noalloc(FAKE, FAKE, FAKE, 64, 128, 1 << 14, FAKE, 1, 4, FAKE, 8192, 0, 0, 0, FAKE,
                                       NULL, NULL, S) == fl.FATHOM_ERR_WORKSPACE
     assert L.fathom_scan_topk_noalloc(FAKE, FAKE, FAKE, 1, 128, 64, FAKE, 1, 4, FAKE, 9000, 0, 0, 0, FAKE, NULL,

@@ -894,3 +894,57 @@ def test_graph_replays_match_eager():
         assert torch.equal(idx, ref_i) and torch.equal(val.view(torch.int32), ref_v.view(torch.int32)), r
     # the 7000-token unit's few sampled quads may under-collect: its rows then take the exact path
     assert status(st) & ~F.FATHOM_DEV_TOPK_FALLBACK == 0
+
+
+# ---------------------------------------------------------------------- exact pass
+def _big_store(ns, seed, ties=False):
+    rng = np.random.default_rng(seed)
+    nmax = max(ns)
+    K = torch.empty((len(ns), nmax, 128), dtype=torch.float32, device=DEV)
+    g = torch.Generator(device=DEV)
+    g.manual_seed(seed)
+    for u in range(len(ns)):
+        if ties:  # few distinct key values: many equal codes, many equal scores
+            K[u] = torch.randint(-2, 3, (nmax, 128), generator=g, device=DEV).float()
+        else:
+            sig = torch.from_numpy(np.exp(rng.standard_normal(128)).astype(np.float32)).to(DEV)
+            K[u] = torch.randn((nmax, 128), generator=g, device=DEV) * sig
+    nt = torch.tensor(ns, dtype=torch.int64, device=DEV)
+    planes, scales = F.fathom_pack(K, nt)
+    del K
+    return nt, planes, scales
+
+
+@pytest.mark.parametrize("case", ["g8_2e20", "rows_2e21", "ties_2e20"])
+def test_exact_pass_long_rows(case):
+    """The exact pass (rows the filter cannot serve) at full size against the
+    oracle, every row: G = 8 at n = 2^20 (the filter takes at most 4 query
+    heads, so all 16 rows are exact; 64 chunks per row and their merge), a
+    2^21 + 777-token row (chunks of several 16384-key passes, a ragged tail),
+    and a unit forced onto the exact path beside filtered units with heavily
+    tied scores (ties broken by the lower index across chunk boundaries)."""
+    if case == "g8_2e20":
+        ns, G, k, lo, tail, B, bound, force = [1 << 20, (1 << 20) - 1000], 8, 2048, 0, 0, 48, 48, None
+    elif case == "rows_2e21":
+        ns, G, k, lo, tail, B, bound, force = [(1 << 21) + 777], 2, 512, 4, 32, 48, 48, 0
+    else:
+        ns, G, k, lo, tail, B, bound, force = [1 << 20, 300000, 1 << 20], 4, 2048, 0, 0, 48, 48, 1
+    nt, planes, scales = _big_store(ns, 500 + len(case), ties=case.startswith("ties"))
+    rng = np.random.default_rng(501)
+    U = len(ns)
+    if case.startswith("ties"):
+        q = rng.integers(-2, 3, (U, G, 128)).astype(np.float16)
+    else:
+        q = rng.standard_normal((U, G, 128)).astype(np.float16)
+    qt = torch.from_numpy(q).to(DEV)
+    var = torch.from_numpy(np.exp(rng.standard_normal((U, 128))).astype(np.float32)).to(DEV)
+    d, _ = F.fathom_alloc_depths(qt, var, F.FATHOM_WATERFILL, B)
+    if force is not None:  # 100 depth bits: above the caller's bound, so the unit's rows are exact
+        d[force] = torch.from_numpy(np.where(np.arange(128) < 25, 4, 0).astype(np.uint8)).to(DEV)
+    st = F.new_status()
+    idx, val = F.fathom_scan_topk(planes, scales, nt, qt, d, k, lo, tail, dev_status=st, max_unit_bits=bound)
+    s = status(st)
+    assert s & F.FATHOM_DEV_TOPK_FALLBACK and s & ~F.FATHOM_DEV_TOPK_FALLBACK == 0, hex(s)
+    _assert_rows_match(idx, val, planes, scales, ns, q, d, k, lo, tail)
+    del planes, scales
+    torch.cuda.empty_cache()

@@ -64,14 +64,14 @@ def test_noalloc_equals_workspace_call_twice_shrinking():
 
 
 def test_noalloc_rejects_shapes_beyond_its_array():
-    """16 units x 4 heads at k = 8192 need more workspace than the library's
+    """64 units x 4 heads at k = 8192 need more workspace than the library's
     array holds: FATHOM_ERR_WORKSPACE before anything is launched, and the
     outputs are left as they were."""
-    planes, scales, nt, q, d = _case(ns=[1000] * 16, seed=9, G=4, B=48)
-    k = 8192
-    assert F.fathom_scan_topk_workspace_size(16, 4, 64 * planes.shape[-1], k) > F.fathom_scan_topk_noalloc_capacity()
-    idx = torch.full((16, 4, k), -3, dtype=torch.int32, device=DEV)
-    val = torch.zeros((16, 4, k), dtype=torch.float32, device=DEV)
+    U, k = 64, 8192
+    planes, scales, nt, q, d = _case(ns=[1000] * U, seed=9, G=4, B=48)
+    assert F.fathom_scan_topk_workspace_size(U, 4, 64 * planes.shape[-1], k) > F.fathom_scan_topk_noalloc_capacity()
+    idx = torch.full((U, 4, k), -3, dtype=torch.int32, device=DEV)
+    val = torch.zeros((U, 4, k), dtype=torch.float32, device=DEV)
     with pytest.raises(F.FathomError) as e:
         F.fathom_scan_topk_noalloc(planes, scales, nt, q, d, k, 0, 0, idx, val)
     assert e.value.code == F.FATHOM_ERR_WORKSPACE
