@@ -47,6 +47,7 @@
 // (FATHOM_DEV_TOPK_FALLBACK).  The result never depends on tau or the bucket
 // bounds; they only decide how much work is saved.
 #include <atomic>
+#include <type_traits>
 #include <mutex>
 
 #include "common.hpp"
@@ -969,15 +970,22 @@ __device__ void wave_run(const Plan& P, WaveLdsT<NSLM, SQB, RQ, QCAP>& W, const 
             for (int p = 0; p < 4; ++p) {
               const int c = (cs >> (4 * p)) & 15;
               if (c == 0) break;
-              uint32_t x[4];
+              // only the c dwords that have plane p (a prefix, depths never increase
+              // along the proxy order) take this segment's rows
+              auto seg = [&](auto C) {
+                constexpr int cc = decltype(C)::value;
+                uint32_t x[cc];
 #pragma unroll
-              for (int dd = 0; dd < 4; ++dd) x[dd] = rb[dd * kStP];
+                for (int dd = 0; dd < cc; ++dd) x[dd] = rb[dd * kStP];
 #pragma unroll
-              for (int dd = 1; dd < 4; ++dd) x[dd] = dd < c ? x[dd] : 0u;  // rows past the segment
+                for (int dd = 0; dd < cc; ++dd)
 #pragma unroll
-              for (int dd = 0; dd < 4; ++dd)
-#pragma unroll
-                for (int mu = 0; mu < 4; ++mu) Z[mu][dd] |= x[dd] & (0x01010101u << (mu + 3 - p));
+                  for (int mu = 0; mu < 4; ++mu) Z[mu][dd] |= x[dd] & (0x01010101u << (mu + 3 - p));
+              };
+              if (c >= 4) seg(std::integral_constant<int, 4>{});
+              else if (c == 3) seg(std::integral_constant<int, 3>{});
+              else if (c == 2) seg(std::integral_constant<int, 2>{});
+              else seg(std::integral_constant<int, 1>{});
               rb += c * kStP;
             }
           } else {
