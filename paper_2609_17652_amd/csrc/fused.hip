@@ -35,17 +35,18 @@
 //
 // Candidates are queued per wave in LDS with their digits; full batches are
 // scored exactly (channels ascending, scales kept in an LDS ring) and the keys
-// with score >= tau are appended to one of 8 value buckets of their row.
+// with score >= tau are appended to their row's survivor list.
 //
 // Passes: (1) sample: proxies of every s-th quad, the 8 largest per (wave,
 // head); (2) per row, tau = the m-th largest sample, m ~ 1.25 k * sampled /
-// eligible + 16, and 7 sample values that bound the value buckets; (3) the
-// full pass above; (4) one workgroup per (bucket, row) orders its bucket and
-// writes each survivor at (survivors of the buckets above) + (its rank in the
-// bucket), when that is below k.  If fewer than k keys reach tau (or a bucket
-// overflows), pass (4) recomputes the row exactly with a streaming top-k
-// (FATHOM_DEV_TOPK_FALLBACK).  The result never depends on tau or the bucket
-// bounds; they only decide how much work is saved.
+// eligible + 16; (3) the full pass above; (4) 8 workgroups per row share out
+// its top k positions by a histogram of the survivors' scores and order their
+// share in LDS; (5) rows with at most 2k + 2048 eligible keys, and rows whose
+// survivors cannot give the top k (fewer than k reached tau, the list
+// overflowed, or too many equal scores for one workgroup's share;
+// FATHOM_DEV_TOPK_FALLBACK), are computed from exact scores by a chunked
+// selection.  The result never depends on tau; it only decides how much work
+// is saved.
 #include <atomic>
 #include <type_traits>
 #include <mutex>
@@ -64,11 +65,11 @@ constexpr int kMaxRg = kD;         // row groups: at most 4 planes x 32 dwords
 constexpr int kStP = 65;           // LDS dwords per staged row group (64 lanes + pad)
 constexpr int kRing = 3;           // superquads of scales kept for re-scoring
 constexpr int kQCap = 64;          // queued candidates per wave at most
-constexpr int kSlots = 8;          // survivor value buckets per row
 constexpr int kSmpW = 8;           // sample proxies kept per (sampled wave, head)
 constexpr int kSampleQuads = 64;   // at most this many sampled quads per unit
 constexpr int kSmpRow = kSampleQuads * kSmpW;
-constexpr int kSelCap = 16384;     // survivor capacity of a row at most (4 buckets of the rank pass)
+constexpr int kCntStride = 64;     // survivor counters one 256-byte line apart (device-scope atomics)
+constexpr int kSelCap = 16384;     // rows with at most this many eligible keys are computed exactly
 constexpr int kThrMax = 1 << 18;   // |S| < 2^17 for A <= 128
 constexpr int kNoBound = 1 << 30;  // accumulator start: always (+) or never (-) a candidate
 constexpr int kMainWavesTarget = 2048;  // full-pass waves in flight over all units
@@ -80,10 +81,9 @@ constexpr int64_t kOneNbMax = (int64_t)1 << 20;  // narrow: byte offsets within 
 constexpr float kNegInf = -__builtin_huge_valf();
 
 struct FusedWs {
-  float* tau;       // [R] threshold on exact scores (-inf: the row is computed exactly by pass 4)
-  uint32_t* cnt;    // [R][kSlots] survivors appended to value bucket z
-  uint64_t* cand;   // [R][kSlots][scap] survivors by bucket: score_key << 32 | ~index
-  uint32_t* bnd;    // [R][kSlots] score keys splitting a row's survivors into kSlots value buckets
+  float* tau;       // [R] threshold on exact scores (-inf: the row is computed exactly by pass 5)
+  uint32_t* cnt;    // [R][kCntStride] word 0: survivors appended to the row's list (counted past its capacity too)
+  uint64_t* cand;   // [R][lcap] survivors in append order: score_key << 32 | ~index
   uint32_t* uovf;   // [U] from pass 2: (slices of the unit's filter, at least kNarrow + 1 for the wide pass) << 1, 0 = no filter
   float* samp;      // [R][kSmpRow] sampled proxies
   uint32_t* xctl;   // [1 + R]: exact rows listed by pass 4, then per listed row the chunks merged so far
@@ -92,7 +92,7 @@ struct FusedWs {
   uint32_t* pcnt;   // [R][xch] composites in each partial list
   uint64_t* pmin;   // [R][xch] a lower bound on each full partial list's smallest composite (0: list not full)
   int xch, pk;      // exact pass: chunks per row at most, partial list length
-  int cap, scap;    // rows with at most cap eligible keys are scored directly; bucket capacity
+  int cap, lcap;    // rows with at most cap eligible keys are scored directly; survivor list capacity
   int64_t s_stride; // sample every s_stride-th quad
   int s_quads;      // sampled quads per unit
   int qpw;          // full pass: quads per wave (a multiple of 4)
@@ -105,7 +105,7 @@ static inline int fused_cap(int k) {
   const int c = 2 * k + 2048;
   return c < kSelCap ? c : kSelCap;
 }
-static inline int fused_scap(int k) { return fused_cap(k) / 4; }
+static inline int fused_lcap(int k) { return 2 * fused_cap(k); }
 
 static inline void fused_geometry(int U, int64_t nb_cap, int64_t* stride, int* squads, int* qpw, int64_t* nwg) {
   const int64_t nq = (nb_cap + kQB - 1) / kQB;
@@ -159,8 +159,9 @@ __host__ __device__ inline int exact_split(int k, int nz) {
 size_t fused_ws_bytes(int R, int U, int64_t nb_cap, int k) {
   if (nb_cap < 1) nb_cap = 1;
   const size_t xch = (size_t)exact_chunks(nb_cap), pk = (size_t)exact_pk(k);
-  return a256((size_t)R * 4) + a256((size_t)R * kSlots * 4) + a256((size_t)R * kSlots * fused_scap(k) * 8) +
-         a256((size_t)U * 4) + a256((size_t)R * kSlots * 4) + a256((size_t)R * kSmpRow * 4) +
+  return a256((size_t)R * 4) + a256((size_t)R * kCntStride * 4) + a256((size_t)R * fused_lcap(k) * 8) +
+         a256((size_t)U * 4) +
+         a256((size_t)R * kSmpRow * 4) +
          a256((size_t)(1 + R) * 4) + a256((size_t)R * 4) + a256((size_t)R * xch * pk * 8) + a256((size_t)R * xch * 4) +
          a256((size_t)R * xch * 8);
 }
@@ -170,13 +171,12 @@ static FusedWs fused_carve(void* ws, int R, int U, int64_t nb_cap, int k) {
   if (nb_cap < 1) nb_cap = 1;
   fused_geometry(U, nb_cap, &w.s_stride, &w.s_quads, &w.qpw, &w.nwg);
   w.cap = fused_cap(k);
-  w.scap = fused_scap(k);
+  w.lcap = fused_lcap(k);
   char* p = reinterpret_cast<char*>(ws);
   w.tau = reinterpret_cast<float*>(p); p += a256((size_t)R * 4);
-  w.cnt = reinterpret_cast<uint32_t*>(p); p += a256((size_t)R * kSlots * 4);
-  w.cand = reinterpret_cast<uint64_t*>(p); p += a256((size_t)R * kSlots * w.scap * 8);
+  w.cnt = reinterpret_cast<uint32_t*>(p); p += a256((size_t)R * kCntStride * 4);
+  w.cand = reinterpret_cast<uint64_t*>(p); p += a256((size_t)R * w.lcap * 8);
   w.uovf = reinterpret_cast<uint32_t*>(p); p += a256((size_t)U * 4);
-  w.bnd = reinterpret_cast<uint32_t*>(p); p += a256((size_t)R * kSlots * 4);
   w.samp = reinterpret_cast<float*>(p); p += a256((size_t)R * kSmpRow * 4);
   w.xch = exact_chunks(nb_cap);
   w.pk = exact_pk(k);
@@ -262,7 +262,6 @@ struct alignas(16) Plan {
   int slmask[kMaxSl];          // slice s: bit 4 dd + p set iff dword 4s + dd has plane p
   int slshp[kMaxSl];           // slice s: bits 4p..4p+3 = c_p, the dwords with plane p (a prefix dd < c_p)
   float tau[4];
-  uint32_t bnd[4][kSlots];     // head h: score keys splitting its survivors into value buckets
 };
 
 // The plan's global reads (thread j < 128: channel j's depth and its q for
@@ -837,38 +836,28 @@ __device__ __forceinline__ void rescore_batch(const Plan& P, WL& W, const FusedA
       }
     }
   }
-  // value buckets: boundaries bnd[h][1..] descend and bucket z holds keys in
-  // (bnd[h][z+1], bnd[h][z]].  Lane 8 h + z counts head h's survivors in
-  // bucket z, so one atomic instruction reserves every list's slots.
+  // lane h reserves head h's slots in its row's list with one atomic
   uint32_t key[4], pre[4] = {0u, 0u, 0u, 0u}, cl = 0u;
-  int bk[4] = {0, 0, 0, 0};
   bool keep[4];
   bool any = false;
 #pragma unroll
   for (int h = 0; h < 4; ++h) {
     keep[h] = h < G && on && ((hm >> h) & 1) && s[h] >= P.tau[h];
     key[h] = score_key(s[h]);
-    if (__ballot(keep[h]) == 0ull) continue;
+    const uint64_t bm = __ballot(keep[h]);
+    if (bm == 0ull) continue;
     any = true;
-#pragma unroll
-    for (int z = 1; z < kSlots; ++z) bk[h] += key[h] <= P.bnd[h][z];
-#pragma unroll
-    for (int z = 0; z < kSlots; ++z) {
-      const bool mine = keep[h] && bk[h] == z;
-      const uint64_t bm = __ballot(mine);
-      if (lane == kSlots * h + z) cl = (uint32_t)__popcll(bm);
-      if (mine) pre[h] = (uint32_t)__popcll(bm & lanemask_lt(lane));
-    }
+    if (lane == h) cl = (uint32_t)__popcll(bm);
+    pre[h] = (uint32_t)__popcll(bm & lanemask_lt(lane));
   }
   if (any) {
     uint32_t base = 0u;
-    if (cl) base = gatomic_add(&a.ws.cnt[u * G * kSlots + lane], cl);
+    if (cl) base = gatomic_add(&a.ws.cnt[(u * G + lane) * kCntStride], cl);
 #pragma unroll
     for (int h = 0; h < 4; ++h) {
-      const uint32_t pos = __shfl(base, kSlots * h + bk[h], kWave) + pre[h];
-      if (keep[h] && pos < (uint32_t)a.ws.scap)
-        gstore(&a.ws.cand[((int64_t)(u * G + h) * kSlots + bk[h]) * a.ws.scap + pos],
-               ((uint64_t)key[h] << 32) | (uint64_t)(~i));
+      const uint32_t pos = __shfl(base, h, kWave) + pre[h];
+      if (keep[h] && pos < (uint32_t)a.ws.lcap)
+        gstore(&a.ws.cand[(int64_t)(u * G + h) * a.ws.lcap + pos], ((uint64_t)key[h] << 32) | (uint64_t)(~i));
     }
   }
   wave_lds_sync();
@@ -1138,29 +1127,27 @@ __global__ __launch_bounds__(kFT) void fused_sample_kernel(FusedArgs a) {
 }
 
 // ---------------------------------------------------------------- pass 2
-// One workgroup of 8 waves per row.  Zeroes the row's survivor counters;
-// tau = the m-th largest sampled proxy; wave w also finds the value of rank
-// floor(w m / 8) (the boundaries that split the survivors for pass 4), each by
-// a bitwise search over order-preserving keys with ballot counts.  Leaves the
-// unit's slice count (0: no filter) in uovf[u] for pass 3.
-constexpr int kTauThreads = kSlots * kWave;
-constexpr int kTauPer = kSmpRow / kWave;  // sampled values per lane
+// One workgroup of two waves per row (one thread per channel for the depth
+// count).  Zeroes the row's survivor count; tau = the m-th largest sampled
+// proxy, found by wave 0 with a bitwise search over order-preserving keys and
+// ballot counts.  Leaves the unit's slice count (0: no filter) in uovf[u] for
+// pass 3.
+constexpr int kTauThreads = kD;
+constexpr int kTauPer = kSmpRow / kWave;  // sampled values per lane of wave 0
 __global__ __launch_bounds__(kTauThreads) void fused_tau_kernel(FusedArgs a) {
   __shared__ int sc[kPlanes + 1];  // active channels by depth
   const int r = blockIdx.x, G = a.G, u = r / G, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  // every load first: the samples (each wave keeps the row's 512), the depths, n
-  const int ns = a.ws.s_quads * kSmpW;
+  // every load first: the samples (wave 0 keeps the row's 512), the depths, n
+  const int ns = wave == 0 ? a.ws.s_quads * kSmpW : 0;
   float sv[kTauPer];
 #pragma unroll
   for (int x = 0; x < kTauPer; ++x) {
     const int i = lane + kWave * x;
     sv[x] = i < ns ? gload(a.ws.samp + (int64_t)r * kSmpRow + i) : kNegInf;
   }
-  const int t = tid < kD ? gload(a.depths + (int64_t)u * kD + tid) : 0;
-  if (tid < kSlots) {
-    a.ws.cnt[r * kSlots + tid] = 0u;
-    a.ws.bnd[r * kSlots + tid] = 0u;
-  } else if (tid == kSlots) {
+  const int t = gload(a.depths + (int64_t)u * kD + tid);
+  if (tid == 0) {
+    a.ws.cnt[r * kCntStride] = 0u;
     a.ws.xctl[1 + r] = 0u;
     if (r == 0) a.ws.xctl[0] = 0u;
   }
@@ -1168,7 +1155,7 @@ __global__ __launch_bounds__(kTauThreads) void fused_tau_kernel(FusedArgs a) {
   row_window(a, u, &nu, &lo, &hi, false);
   if (tid <= kPlanes) sc[tid] = 0;
   __syncthreads();
-  if (tid < kD && t > 0) atomicAdd(&sc[t > kPlanes ? kPlanes : t], 1);
+  if (t > 0) atomicAdd(&sc[t > kPlanes ? kPlanes : t], 1);
   __syncthreads();
   const int A = sc[1] + sc[2] + sc[3] + sc[4];
   const bool ok = G <= 4 && A > 0 && hi - lo > a.ws.cap;
@@ -1188,7 +1175,8 @@ __global__ __launch_bounds__(kTauThreads) void fused_tau_kernel(FusedArgs a) {
     if (tid == 0) a.ws.tau[r] = kNegInf;
     return;
   }
-  // every wave: the row's samples as keys (0 = no sample) and m
+  if (wave != 0) return;
+  // the row's samples as keys (0 = no sample) and m
   uint32_t key[kTauPer];
   int nv = 0;
 #pragma unroll
@@ -1216,25 +1204,16 @@ __global__ __launch_bounds__(kTauThreads) void fused_tau_kernel(FusedArgs a) {
     if (tid == 0) a.ws.tau[r] = kNegInf;
     return;
   }
-  // wave 0: rank m (tau); wave w >= 1: rank floor(w m / 8) + 1
-  const int64_t rank = wave == 0 ? m : (wave * m) / kSlots + 1;
-  uint32_t prefix = 0u;
+  uint32_t prefix = 0u;  // the largest key with at least m samples at or above it
   for (int bit = 31; bit >= 0; --bit) {
     const uint32_t cand = prefix | (1u << bit);
     int c = 0;
 #pragma unroll
     for (int x = 0; x < kTauPer; ++x) c += __popcll(__ballot(key[x] >= cand));
-    if (c >= rank) prefix = cand;
+    if (c >= m) prefix = cand;
   }
   const uint32_t k0 = prefix & ~1u;  // the forced low bit rounded down
-  if (lane == 0) {
-    if (wave == 0) {
-      a.ws.tau[r] = __uint_as_float((k0 & 0x80000000u) ? (k0 & 0x7FFFFFFFu) : ~k0);
-      a.ws.bnd[r * kSlots] = 0xFFFFFFFFu;
-    } else {
-      a.ws.bnd[r * kSlots + wave] = k0;
-    }
-  }
+  if (lane == 0) a.ws.tau[r] = __uint_as_float((k0 & 0x80000000u) ? (k0 & 0x7FFFFFFFu) : ~k0);
 }
 
 // ---------------------------------------------------------------- pass 3
@@ -1246,14 +1225,10 @@ __global__ __launch_bounds__(kFT) void fused_main_kernel(FusedArgs a) {
   __shared__ Plan P;
   __shared__ WaveLdsT<NSLM, SQB, kRing, kQCap> WL[kFW];
   const int u = blockIdx.y, tid = threadIdx.x, wave = uni(tid >> 6);
-  // every global read of the preamble first: unit class, n, tau, bucket
-  // bounds, depths and q (the plan's barriers order the LDS writes)
+  // every global read of the preamble first: unit class, n, tau, depths and
+  // q (the plan's barriers order the LDS writes)
   const uint32_t uo = gload(a.ws.uovf + u);
   if (tid < 4) P.tau[tid] = tid < a.G ? gload(a.ws.tau + u * a.G + tid) : kNegInf;
-  if (tid >= kWave && tid < kWave + 4 * kSlots) {
-    const int x = tid - kWave, h = x / kSlots;
-    P.bnd[h][x % kSlots] = h < a.G ? gload(a.ws.bnd + (u * a.G + h) * kSlots + x % kSlots) : 0u;
-  }
   const PlanPre pre = plan_load<QF16>(a, u);
   int64_t nu, lo, hi;
   row_window(a, u, &nu, &lo, &hi, blockIdx.x == 0 && tid == 0);
@@ -1327,92 +1302,88 @@ __device__ __forceinline__ float key_to_score(uint32_t key) {
   return __uint_as_float((key & 0x80000000u) ? (key & 0x7FFFFFFFu) : ~key);
 }
 
-// The survivors of row r (bucket counts cnt8) hold its top k exactly when no
-// bucket overflowed, at least k were found and the filter ran for the row.
-// The row's survivor lists determine its top k exactly when at least k keys
-// survived and every bucket that starts above rank k (fewer than k survivors
-// in the buckets before it) kept all of its keys: buckets entirely below the
-// k-th key are never read, so their overflow does not matter.  The counts are
-// exact even for an overflowing bucket (keys past its capacity are counted,
-// not stored).
-__device__ __forceinline__ bool survivors_complete(const uint32_t* cnt8, const FusedArgs& a, float tau, uint32_t ovf) {
-  uint32_t C = 0;
-  bool over = false;
-#pragma unroll
-  for (int z = 0; z < kSlots; ++z) {
-    over |= C < (uint32_t)a.k && cnt8[z] > (uint32_t)a.ws.scap;
-    C += cnt8[z];
-  }
-  return !over && C >= (uint32_t)a.k && (ovf & 1u) == 0u && tau != kNegInf;
-}
-
-// Pass 4 (filtered rows): workgroup (z, r) orders the survivors of value
-// bucket z of row r.  Every survivor of a higher bucket outscores every one of
-// bucket z, so a survivor's output position is (survivors of the buckets
-// above) + (survivors of its own bucket with a larger composite).  Within the
-// bucket a counting sort on an interpolated sub-bucket of the score key
-// (monotone in the key) groups the survivors; only survivors sharing a
-// sub-bucket are compared.  Composites are distinct (they carry the index), so
-// the positions are a permutation.
-constexpr int kRankThreads = 256;
-constexpr int kRankCap = kSelCap / 4;  // bucket capacity (largest scap)
-constexpr int kRankSub = 2048;         // sub-buckets at most
-__global__ __launch_bounds__(kRankThreads) void fused_rank_kernel(FusedArgs a, int32_t* __restrict__ idx,
+// Pass 4 (filtered rows).  The row's survivor list holds its top k exactly
+// when at least k keys survived, the list kept them all (the count goes on
+// past the capacity) and the filter ran for the row.  Its top K = min(c, k)
+// output positions are shared by kRankParts workgroups: each reads the c
+// survivors and builds the same histogram over ns sub-buckets of the score key
+// (interpolated between the row's smallest and largest survivor key, not
+// decreasing as the key falls), so a survivor's output position is (survivors
+// of the sub-buckets before its own) + (survivors of its own sub-bucket with a
+// larger composite).  Part z takes the sub-buckets whose first position lies
+// in [z K / parts, (z + 1) K / parts) and orders their survivors in LDS; only
+// survivors sharing a sub-bucket are compared.  Composites are distinct (they
+// carry the index), so the positions are a permutation.  A row whose share
+// for some part exceeds kRankCap (many equal scores) goes to pass 5 with the
+// rows that the list cannot serve; every part reaches the same decision from
+// the same histogram.  The parts of a row run on one XCD (workgroups are
+// dealt to the 8 XCDs in turn), so the list is read once into that XCD's L2.
+constexpr int kRankParts = 8;
+constexpr int kRankThreads = 512;
+constexpr int kRankPer = 8;      // survivors per thread read with the count (the rest re-read)
+constexpr int kRankCap = 4096;   // survivors one part orders at most
+constexpr int kRankSub = 4096;   // sub-buckets at most
+constexpr int kRankXcd = 8;
+__global__ __launch_bounds__(kRankThreads) void fused_rank_kernel(FusedArgs a, int R, int32_t* __restrict__ idx,
                                                                  float* __restrict__ val) {
-  __shared__ uint64_t buf[kRankCap], grp[kRankCap];
-  __shared__ uint32_t hist[kRankSub];
-  __shared__ uint32_t s_cnt[kSlots], s_red[2][kRankThreads / kWave], s_part[kRankThreads / kWave];
+  __shared__ uint64_t grp[kRankCap];
+  __shared__ uint32_t hist[kRankSub + 1];
+  __shared__ uint32_t s_red[2][kRankThreads / kWave], s_part[kRankThreads / kWave];
+  __shared__ uint32_t s_first[kRankParts + 1];  // part z: sub-buckets [s_first[z], s_first[z + 1])
+  __shared__ uint32_t s_c, s_ovf;
   __shared__ float s_tau;
-  __shared__ uint32_t s_ovf;
   __shared__ int64_t s_n;
   const int G = a.G;
-  const int z = blockIdx.x, r = blockIdx.y, u = r / G, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  // the bucket's slots up to its capacity are read with the counts (slots past
-  // the count are not used)
-  constexpr int kPer = kRankCap / kRankThreads;
-  const uint64_t* src = a.ws.cand + ((int64_t)r * kSlots + z) * a.ws.scap;
-  uint64_t pv[kPer];
+  const int w = blockIdx.x, j = w / kRankXcd;
+  const int z = j % kRankParts, r = (j / kRankParts) * kRankXcd + w % kRankXcd;
+  if (r >= R) return;
+  const int u = r / G, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int lcap = a.ws.lcap;
+  const uint64_t* src = a.ws.cand + (int64_t)r * lcap;
+  uint64_t pv[kRankPer];
 #pragma unroll
-  for (int j = 0; j < kPer; ++j) {
-    const int e = tid + kRankThreads * j;
-    pv[j] = e < a.ws.scap ? gload(src + e) : 0ull;
+  for (int x = 0; x < kRankPer; ++x) {  // slots past the count are read but not used
+    const int e = tid + kRankThreads * x;
+    pv[x] = e < lcap ? gload(src + e) : 0ull;
   }
-  if (tid < kSlots) s_cnt[tid] = gload(a.ws.cnt + r * kSlots + tid);
-  else if (tid == kSlots) s_tau = gload(a.ws.tau + r);
-  else if (tid == kSlots + 1) s_ovf = gload(a.ws.uovf + u);
-  else if (tid == kSlots + 2) s_n = gload(a.n + u);
+  if (tid == 0) s_c = gload(a.ws.cnt + r * kCntStride);
+  else if (tid == 1) s_tau = gload(a.ws.tau + r);
+  else if (tid == 2) s_ovf = gload(a.ws.uovf + u);
+  else if (tid == 3) s_n = gload(a.n + u);
   __syncthreads();
   int64_t nu = s_n;
   if (nu < 0 || nu > a.nb_cap * kBlockTokens) nu = 0;
   int64_t lo = a.lo, hi = nu - a.tail;
   if (hi < lo) hi = lo;
+  const uint32_t c = s_c, k = (uint32_t)a.k;
   const bool direct = hi - lo <= a.ws.cap;
-  if (direct || !survivors_complete(s_cnt, a, s_tau, s_ovf)) {
-    if (z == 0 && tid == 0) {  // the exact pass computes this row
-      const uint32_t j = gatomic_add(a.ws.xctl, 1u);
-      gstore(a.ws.xrows + j, (uint32_t)r | (direct ? kXDirect : 0u));
+  const bool complete = c >= k && c <= (uint32_t)lcap && (s_ovf & 1u) == 0u && s_tau != kNegInf;
+  auto list_exact = [&]() {
+    if (z == 0 && tid == 0) {
+      const uint32_t jx = gatomic_add(a.ws.xctl, 1u);
+      gstore(a.ws.xrows + jx, (uint32_t)r | (direct ? kXDirect : 0u));
     }
+  };
+  if (direct || !complete) {
+    list_exact();
     return;
   }
-  uint32_t off0 = 0;
-  for (int y = 0; y < z; ++y) off0 += s_cnt[y];
-  const int c = (int)s_cnt[z], k = a.k;
-  if (off0 >= (uint32_t)k || c == 0) return;
-  // the bucket, and its key range
-  uint32_t kmin = 0xFFFFFFFFu, kmax = 0u;
+  // visits every survivor: the first kRankPer per thread from registers
+  auto each = [&](auto fn) {
 #pragma unroll
-  for (int j = 0; j < kPer; ++j) {
-    const int e = tid + kRankThreads * j;
-    if (e < c) {
-      buf[e] = pv[j];
-      const uint32_t key = (uint32_t)(pv[j] >> 32);
-      kmin = key < kmin ? key : kmin;
-      kmax = key > kmax ? key : kmax;
-    }
-  }
-  int ns = 64;  // sub-buckets: a power of two, about twice the survivors
-  while (ns < 2 * c && ns < kRankSub) ns <<= 1;
+    for (int x = 0; x < kRankPer; ++x)
+      if (tid + kRankThreads * x < (int)c) fn(pv[x]);
+    for (uint32_t e = tid + kRankThreads * kRankPer; e < c; e += kRankThreads) fn(gload(src + e));
+  };
+  int ns = 64;  // sub-buckets: a power of two, at least the survivors
+  while (ns < (int)c && ns < kRankSub) ns <<= 1;
   for (int x = tid; x < ns; x += kRankThreads) hist[x] = 0u;
+  uint32_t kmin = 0xFFFFFFFFu, kmax = 0u;
+  each([&](uint64_t v) {
+    const uint32_t key = (uint32_t)(v >> 32);
+    kmin = key < kmin ? key : kmin;
+    kmax = key > kmax ? key : kmax;
+  });
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) {
     const uint32_t m0 = __shfl_xor(kmin, o, kWave), m1 = __shfl_xor(kmax, o, kWave);
@@ -1427,19 +1398,23 @@ __global__ __launch_bounds__(kRankThreads) void fused_rank_kernel(FusedArgs a, i
   kmin = s_red[0][0];
   kmax = s_red[1][0];
 #pragma unroll
-  for (int w = 1; w < kRankThreads / kWave; ++w) {
-    kmin = s_red[0][w] < kmin ? s_red[0][w] : kmin;
-    kmax = s_red[1][w] > kmax ? s_red[1][w] : kmax;
+  for (int x = 1; x < kRankThreads / kWave; ++x) {
+    kmin = s_red[0][x] < kmin ? s_red[0][x] : kmin;
+    kmax = s_red[1][x] > kmax ? s_red[1][x] : kmax;
   }
-  // sub-bucket: floor((kmax - key) * scale), non-decreasing as the key falls
+  // sub-bucket: floor((kmax - key) * scale), not decreasing as the key falls
   const float scale = kmax > kmin ? (float)(ns - 1) / (float)(kmax - kmin) : 0.0f;
   auto sub_of = [&](uint64_t v) {
     const int sb = (int)__fmul_rn((float)(kmax - (uint32_t)(v >> 32)), scale);
     return sb < ns - 1 ? sb : ns - 1;
   };
-  for (int e = tid; e < c; e += kRankThreads) atomicAdd(&hist[sub_of(buf[e])], 1u);
+  each([&](uint64_t v) { atomicAdd(&hist[sub_of(v)], 1u); });
   __syncthreads();
-  // exclusive prefix over the sub-buckets (thread t owns a run of ns / 256, or one)
+  // exclusive prefix over the sub-buckets, in place (thread t owns a run of
+  // ns / kRankThreads, or one); hist[ns] = c.  Part z's first sub-bucket is
+  // the first s with hist[s] >= b_z = z K / parts: for b_z > 0 the one after
+  // the sub-bucket whose positions cross b_z.
+  const uint32_t K = c < k ? c : k;
   {
     const int per = ns / kRankThreads > 0 ? ns / kRankThreads : 1;
     const int x0 = tid * per;
@@ -1455,30 +1430,51 @@ __global__ __launch_bounds__(kRankThreads) void fused_rank_kernel(FusedArgs a, i
     if (lane == kWave - 1) s_part[wave] = inc;
     __syncthreads();
     uint32_t acc = inc - run;
-    for (int w = 0; w < wave; ++w) acc += s_part[w];
+    for (int x = 0; x < wave; ++x) acc += s_part[x];
     for (int x = 0; x < per; ++x)
       if (x0 + x < ns) {
         const uint32_t h0 = hist[x0 + x];
         hist[x0 + x] = acc;
+#pragma unroll
+        for (int zz = 1; zz <= kRankParts; ++zz) {
+          const uint32_t b = (uint32_t)(((uint64_t)zz * K) / kRankParts);
+          if (acc < b && acc + h0 >= b) s_first[zz] = (uint32_t)(x0 + x + 1);
+        }
         acc += h0;
       }
+    if (tid == 0) {
+      hist[ns] = c;
+#pragma unroll
+      for (int zz = 0; zz <= kRankParts; ++zz)
+        if (((uint64_t)zz * K) / kRankParts == 0) s_first[zz] = 0u;
+    }
   }
   __syncthreads();
-  for (int e = tid; e < c; e += kRankThreads) {  // group by sub-bucket; hist[s] ends at the group's end
-    const uint64_t v = buf[e];
-    grp[atomicAdd(&hist[sub_of(v)], 1u)] = v;
+  bool over = false;
+#pragma unroll
+  for (int x = 0; x < kRankParts; ++x) over |= hist[s_first[x + 1]] - hist[s_first[x]] > (uint32_t)kRankCap;
+  if (over) {
+    list_exact();
+    return;
   }
-  __syncthreads();
-  for (int j = tid; j < c; j += kRankThreads) {
-    const uint64_t v = grp[j];
+  const int s0 = (int)s_first[z], s1 = (int)s_first[z + 1];
+  if (s0 == s1) return;
+  const uint32_t start = hist[s0], share = hist[s1] - start;
+  __syncthreads();  // every part bound read before hist[s0 .. s1) serve as cursors
+  each([&](uint64_t v) {  // group by sub-bucket; hist[s] ends at the group's end
     const int sb = sub_of(v);
-    const uint32_t g0 = sb > 0 ? hist[sb - 1] : 0u, g1 = hist[sb];
+    if (sb >= s0 && sb < s1) grp[atomicAdd(&hist[sb], 1u) - start] = v;
+  });
+  __syncthreads();
+  for (uint32_t e = tid; e < share; e += kRankThreads) {
+    const uint64_t v = grp[e];
+    const int sb = sub_of(v);
+    const uint32_t g0 = sb > s0 ? hist[sb - 1] : start, g1 = hist[sb];
     uint32_t rank = g0;
-    for (uint32_t x = g0; x < g1; ++x) rank += grp[x] > v;
-    const uint32_t p = off0 + rank;
-    if (p < (uint32_t)k) {
-      idx[(int64_t)r * k + p] = (int32_t)(~(uint32_t)(v & 0xFFFFFFFFull));
-      if (val) val[(int64_t)r * k + p] = key_to_score((uint32_t)(v >> 32));
+    for (uint32_t x = g0; x < g1; ++x) rank += grp[x - start] > v;
+    if (rank < k) {
+      idx[(int64_t)r * k + rank] = (int32_t)(~(uint32_t)(v & 0xFFFFFFFFull));
+      if (val) val[(int64_t)r * k + rank] = key_to_score((uint32_t)(v >> 32));
     }
   }
 }
@@ -1966,7 +1962,8 @@ fathom_status launch_scan_topk_fused(const uint64_t* planes, const uint16_t* sca
       if (wide) hipLaunchKernelGGL((fused_main_kernel<false, kMaxSl, 8>), gm, dim3(kFT), 0, s, fa);
     }
   }
-  hipLaunchKernelGGL(fused_rank_kernel, dim3(kSlots, R), dim3(kRankThreads), 0, s, fa, idx, val);
+  const unsigned rank_wg = (unsigned)((R + kRankXcd - 1) / kRankXcd) * kRankXcd * kRankParts;
+  hipLaunchKernelGGL(fused_rank_kernel, dim3(rank_wg), dim3(kRankThreads), 0, s, fa, R, idx, val);
   hipLaunchKernelGGL(fused_exact_kernel, dim3((unsigned)fa.ws.xch, (unsigned)kXSlots), dim3(kXThreads), kXLdsBytes,
                      s, fa, idx, val);
   FATHOM_LAUNCH_CHECK();

@@ -572,12 +572,14 @@ def test_scan_topk_fallback_is_exact(scale):
         assert np.array_equal(val[0, h].cpu().numpy(), ov), h
 
 
-def test_bucket_overflow_below_rank_k_keeps_the_filter():
-    """A decode-step row (4-session workload: layer 33, session 0, KV head 4,
-    query head 1) whose lowest survivor bucket receives more keys than its
-    capacity while the buckets above it already hold k: no bucket the top k
-    reads is incomplete, so the row keeps the filter (no TOPK_FALLBACK) and its
-    top k equals the oracle's."""
+def test_decode_row_survivors_match_the_oracle_count():
+    """A decode-step row set (4-session workload: layer 33, session 0, KV head
+    4) whose sampled threshold lets many keys through.  White-box: the survivor
+    count per row in the workspace (after the thresholds, in the next 256-byte
+    aligned region: one 256-byte line per row, the count in its first word)
+    equals the oracle's count of scores >= tau and fits the survivor list
+    (2 (2k + 2048) keys at most); the rows keep the filter (no TOPK_FALLBACK)
+    and their top k equals the oracle's."""
     cfg = synth.WORKLOADS["step4x1m"]
     unit = (0 * cfg.layers + 33) * cfg.kv_heads + 4
     data = synth.device_units(cfg, units=[unit], with_values=False, key_dtype=torch.float16)
@@ -591,19 +593,52 @@ def test_bucket_overflow_below_rank_k_keeps_the_filter():
     st = F.new_status()
     idx, val = F.fathom_scan_topk(planes, scales, nt, q, d, sel, lo, tail, ws=ws, dev_status=st, max_unit_bits=48)
     assert status(st) == 0
-    # the case itself, from the workspace (threshold per row, then 8 bucket counts per row)
     w = ws.cpu().numpy()
-    cnt = w[256:256 + G * 8 * 4].view(np.uint32).reshape(G, 8).astype(np.int64)
-    scap = min(2 * sel + 2048, 16384) // 4
-    over = [z for z in range(8) if cnt[1, z] > scap]
-    assert over and all(cnt[1, :z].sum() >= sel for z in over), cnt[1]
+    tau = w[:4 * G].view(np.float32)
+    cnt = w[256:256 + 256 * G].view(np.uint32)[::64].astype(np.int64)
+    lcap = 2 * min(2 * sel + 2048, 16384)
     ref = oracle.scores_f32(u64(planes)[0], u16(scales)[0], n, q[0].cpu().numpy().astype(np.float32),
                             d.cpu().numpy()[0])
     ix, vx = idx.cpu().numpy()[0], val.cpu().numpy()[0]
     for h in range(G):
+        assert sel <= cnt[h] <= lcap, (h, cnt)
+        assert cnt[h] == np.count_nonzero(ref[h][lo:n - tail] >= tau[h]), h
         oi, ov, _ = oracle.topk(ref[h], sel, lo, tail)
         assert np.array_equal(ix[h], oi), h
         assert np.array_equal(vx[h].view(np.uint32), ov.view(np.uint32)), h
+
+
+@pytest.mark.parametrize("tied_blocks", [46, 80])
+def test_equal_scores_top_k(tied_blocks):
+    """Thousands of keys with one and the same documented score (whole blocks
+    of one key vector, which quantise identically) at the top of a row: they
+    share one histogram bin of the ordering pass.  46 blocks (2944 keys) are
+    ordered there (ties by index ascending); 80 blocks (5120 keys) are more
+    than one workgroup's share, so the row goes to the exact pass
+    (TOPK_FALLBACK).  Either way the top k equals the oracle's."""
+    rng = np.random.default_rng(95)
+    n, k = 200000, 2048
+    q = rng.standard_normal((1, 1, 128)).astype(np.float32)
+    K = rng.standard_normal((1, n, 128)).astype(np.float32)
+    v = 30.0 * q[0, 0] / np.linalg.norm(q[0, 0])
+    t0 = 100 * 64
+    K[0, t0:t0 + 64 * tied_blocks] = v
+    nt = torch.tensor([n], dtype=torch.int64, device=DEV)
+    planes, scales = F.fathom_pack(torch.from_numpy(K).to(DEV), nt)
+    qt = torch.from_numpy(q).to(DEV)
+    var = torch.ones((1, 128), dtype=torch.float32, device=DEV)
+    d, _ = F.fathom_alloc_depths(qt, var, F.FATHOM_WATERFILL, 48)
+    st = F.new_status()
+    idx, val = F.fathom_scan_topk(planes, scales, nt, qt, d, k, dev_status=st, max_unit_bits=48)
+    s = status(st)
+    assert s & ~F.FATHOM_DEV_TOPK_FALLBACK == 0
+    assert bool(s & F.FATHOM_DEV_TOPK_FALLBACK) == (tied_blocks * 64 > 4096)
+    ref = oracle.scores_f32(u64(planes)[0], u16(scales)[0], n, q[0], d.cpu().numpy()[0])
+    assert np.count_nonzero(ref[0] == ref[0][t0]) == 64 * tied_blocks
+    oi, ov, _ = oracle.topk(ref[0], k)
+    assert np.array_equal(oi, np.arange(t0, t0 + k))
+    assert np.array_equal(idx[0, 0].cpu().numpy(), oi)
+    assert np.array_equal(val[0, 0].cpu().numpy().view(np.uint32), ov.view(np.uint32))
 
 
 def test_scan_topk_no_fallback_on_workload_data():
@@ -644,9 +679,9 @@ def test_scan_topk_filter_misses_no_survivor(case):
     """White-box check of the fused filter's bound (Sec. 3.2 scores, proxy
     error bound): every eligible key whose documented score reaches the row's
     threshold tau must be kept, so the survivor count the full pass leaves per
-    row equals the oracle's count of scores >= tau.  Reads tau and the
-    per-sub-list counts from the workspace (tau: the first U*G floats; counts:
-    the next 256-byte aligned region, 8 per row)."""
+    row equals the oracle's count of scores >= tau.  Reads tau and the survivor
+    counts from the workspace (tau: the first U*G floats; counts: the next
+    256-byte aligned region, one 256-byte line per row, the count first)."""
     rng = np.random.default_rng(81)
     ns = [131072, 100000, 77777, 131000]
     K, nt, planes, scales = _store(ns, 82)
@@ -667,7 +702,7 @@ def test_scan_topk_filter_misses_no_survivor(case):
     R = U * G
     tau = ws[:4 * R].view(torch.float32).cpu().numpy()
     off = (4 * R + 255) // 256 * 256
-    cnt = ws[off:off + 32 * R].view(torch.int32).view(R, 8).sum(1).cpu().numpy()
+    cnt = ws[off:off + 256 * R].view(torch.int32).cpu().numpy()[::64]
     dd = d.cpu().numpy()
     for u, nu in enumerate(ns):
         ref = oracle.scores_f32(u64(planes)[u], u16(scales)[u], nu, q[u].astype(np.float32), dd[u])
