@@ -1,0 +1,759 @@
+// Full pass of fathom_scan_topk for units of at most 48 active channels and
+// 16 row groups (every unit under water-filling at up to 48 code bits, and
+// uniform depth at r <= 16): an int8 MFMA proxy of every key's four head
+// scores over its plane bits, exact re-scoring of the keys the proxy's bound
+// cannot exclude, and the appends of keys with exact score >= tau to their
+// row's survivor list (Sec. 3.2-3.3 scores, Sec. 2 top-k).
+//
+// Cells.  With khat = a16 sum_{p<t} 2^-p (b_p - 1/2) (the prefix
+// dequantisation of Sec. 3.2 written out; exact), the documented score of a
+// key is, as a real number,
+//   s = sum over cells (x, p) of w (b - 1/2),   w = q_x a16_x 2^-p,
+// one cell per active channel x and plane p < t_x.  Per group (8 blocks)
+// and head, delta = 2^e is the smallest power of two with max |q a16| / delta
+// <= 127; each cell gets its own int8 weight W = rne(w / delta), so with
+// S = sum W b and Wsum = sum W over the cells of a block,
+//   |s - delta (S - Wsum / 2)| <= delta cells / 4 + (A^2 127 2^-24) delta
+// (weight rounding, then the A roundings of the fp32 chain), plus A 2^-120
+// for subnormal results.  A key is a candidate for head h iff
+// S >= thr = floor((floor(2 (tau - E) / delta) - 1 + Wsum) / 2).
+//
+// Layout.  Cells are ordered plane-major, each plane's channels (a prefix of
+// the proxy order: depth descending, channel ascending) padded to a multiple
+// of 4: row group g = plane p_g, proxy channels 4 i_g .. 4 i_g + 3.  The plane
+// words of a quad (4 blocks) are staged in LDS as loaded, cell by cell (pad
+// cells read as zero), and ds_read_b64_tr_b8 hands lane l the bytes of 8
+// cells (two row groups) at octet l & 7 of block l >> 4: within a 16-lane
+// group, output lane 8h + r takes byte r of the words addressed by lanes h,
+// h + 2, ..., h + 14.  So lane l owns the 4 keys 8 o + 4 nib + mu (o = l & 7,
+// nib = (l >> 3) & 1) of block l >> 4, and with pos = 4 nib + mu,
+// X & (0x01010101 << pos) is that key's B operand dword of a row group for
+// v_mfma_i32_16x16x64_i8 (byte value b 2^pos, or -128 b at pos 7).  A is
+// block diagonal: row 4 g' + h of k-group g' holds block g''s head-h weights.
+// The accumulators start at -thr 2^pos (128 thr - 1 at pos 7, where the
+// candidate test flips sign), so a key is a candidate iff one of its four
+// accumulators is >= 0 (< 0 at pos 7).
+//
+// Candidate keys are queued per wave in LDS with their lane's staged dwords; a batch is scored exactly in the documented order (channels
+// ascending, fmaf from +0) with the scales of the last four groups kept in
+// an LDS ring, and keys with score >= tau are appended to their row's list.
+#include "fused.hpp"
+
+namespace fathom {
+
+constexpr int kCG = 16;          // row groups at most
+constexpr int kCA = 48;          // active channels at most
+constexpr int kCSB = 8;          // blocks per group (one delta per head; one loop iteration)
+constexpr int kCSlots = 4;       // groups of scales kept for re-scoring
+constexpr int kCQ = 64;          // queued candidates per wave (one ballot fits)
+constexpr int kCFlush = 48;      // re-score at a quad boundary once this many are queued
+constexpr int kSclRow = kCA + 2; // halfs per scale row: an odd number of dwords
+constexpr int kSv = 16;          // survivors per head buffered in LDS before a list append
+constexpr int kCWaves = 4;       // waves per workgroup
+constexpr int kCThreads = kCWaves * kWave;
+
+struct alignas(16) CellPlan {
+  int A, rg, ns, ok;       // active channels, row groups, 16-cell slices, the unit fits this pass
+  int nd[4];               // row groups of plane p
+  int gp[5];               // first row group of plane p (gp[4] = rg)
+  double Ku, Eabs;         // E = delta Ku + Eabs
+  uint32_t rrow[kCG][2];   // row group g: plane rows 4 j + p of its 4 cells (16-bit halves, kCPad: none)
+  uint32_t rgp[kCG];       // row group g: plane p | proxy dword i << 8
+  float qrg[kCG][4][4];    // row group g, head h, cell k: q (0 for pad cells and heads >= G)
+  float qx[kCA][4];        // q by proxy index and head (delta)
+  int pj[kCA];             // proxy index -> channel
+  int px[kCA];             // ascending position y -> proxy index x (padded to a multiple of 8: x = A)
+  float qa[kCA][4];        // q by ascending position and head (re-scoring; 0 on padding)
+  float zo[kCA];           // 8 - 2^(3 - t) by ascending position: khat = (u - zo) a16 / 8 (0 on padding)
+  float tau[4];
+};
+constexpr uint32_t kCPad = 0xFFFFu;
+
+struct alignas(16) FilterLds {
+  uint64_t raw[4 * kCG][4];               // the quad's plane words: padded cell, block
+  uint32_t zero[kCG];                     // zero dwords (the A operand of lanes that carry no weights)
+  uint32_t W[4][4][kCG];                  // int8 weights: block of the quad, head, row group
+  int32_t ini[4][2][4][4];                // accumulator starts: block, nibble, mu, head
+  uint16_t scl[kCSlots][kCSB][kSclRow];   // fp16 scales: ring slot, block, proxy channel
+  uint32_t qx[kCG][kCQ];                  // queued keys' staged dwords (digits while re-scored): dword, entry
+  uint32_t qi[kCQ];                       // queued key index
+  uint32_t qf[kCQ];                       // pos | heads << 3 | slot << 7 | block of the group << 9
+  uint64_t sv[4][kSv];                    // survivors per head not yet appended to the row's list
+};
+
+typedef __attribute__((ext_vector_type(4))) int v4i;
+typedef unsigned int v2u32 __attribute__((ext_vector_type(2)));
+typedef unsigned int v4u __attribute__((ext_vector_type(4)));
+constexpr int kRawBufferFlags = 0x00020000;  // raw buffer, 32-bit data format
+constexpr uint32_t kPastRange = 0xFFFFFFF0u;  // a buffer offset past every range (loads return zero)
+
+__device__ __forceinline__ int cuni(int v) { return __builtin_amdgcn_readfirstlane(v); }
+__device__ __forceinline__ void lds_wait() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+// Orders LDS accesses in the compiler only: a wave's LDS instructions execute
+// in program order, so a wave reading what it wrote itself needs no wait.
+__device__ __forceinline__ void lds_order() { asm volatile("" ::: "memory"); }
+// Keeps the scheduler from moving instructions across this point.
+__device__ __forceinline__ void sched_fence() { __builtin_amdgcn_sched_barrier(0); }
+__device__ __forceinline__ uint64_t lanes_below(int lane) { return lane == 0 ? 0ull : (~0ull >> (64 - lane)); }
+
+template <int CTRL>
+__device__ __forceinline__ float dpp_f(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
+}
+template <int CTRL>
+__device__ __forceinline__ int dpp_i(int v) {
+  return __builtin_amdgcn_update_dpp(0, v, CTRL, 0xF, 0xF, false);
+}
+// Largest value over the wave of non-negative floats (uniform result).
+__device__ __forceinline__ float wave_max_pos(float v) {
+  v = fmaxf(v, dpp_f<0x128>(v));  // row_ror 8
+  v = fmaxf(v, dpp_f<0x124>(v));  // row_ror 4
+  v = fmaxf(v, dpp_f<0x122>(v));  // row_ror 2
+  v = fmaxf(v, dpp_f<0x121>(v));  // row_ror 1: every lane of a row holds the row's largest
+  const uint32_t a = (uint32_t)__builtin_amdgcn_readlane(__float_as_int(v), 0);
+  const uint32_t b = (uint32_t)__builtin_amdgcn_readlane(__float_as_int(v), 16);
+  const uint32_t c = (uint32_t)__builtin_amdgcn_readlane(__float_as_int(v), 32);
+  const uint32_t d = (uint32_t)__builtin_amdgcn_readlane(__float_as_int(v), 48);
+  const uint32_t m1 = a > b ? a : b, m2 = c > d ? c : d;  // non-negative floats order as their bits
+  return __uint_as_float(m1 > m2 ? m1 : m2);
+}
+
+// ---------------------------------------------------------------- plan
+// Depth and q of channel tid (< 128), read by the kernel before its other
+// preamble work.
+struct CellPre {
+  int t;
+  float q[4];
+};
+__device__ __forceinline__ CellPre cell_load(const FusedArgs& a, int u) {
+  const int tid = threadIdx.x, G = a.G;
+  CellPre r;
+  r.t = 0;
+#pragma unroll
+  for (int h = 0; h < 4; ++h) r.q[h] = 0.0f;
+  if (tid < kD) {
+    r.t = gload(a.depths + (int64_t)u * kD + tid);
+#pragma unroll
+    for (int h = 0; h < 4; ++h)
+      if (h < G) r.q[h] = load_q(a.q, a.qdt, ((int64_t)u * G + h) * kD + tid);
+  }
+  if (r.t > kPlanes) r.t = kPlanes;
+  return r;
+}
+
+// Builds the plan of unit u (all threads of the workgroup).  P.ok is false
+// when the unit exceeds this pass's limits or has no active channel.
+__device__ __forceinline__ void cell_plan(CellPlan& P, const FusedArgs& a, const CellPre& pre) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, G = a.G;
+  __shared__ int cnt[2][kPlanes + 1];
+  __shared__ int sact[kD];  // proxy index -> channel j | depth << 8
+  const int t = pre.t;
+  uint64_t bal[kPlanes + 1];
+#pragma unroll
+  for (int v = 1; v <= kPlanes; ++v) bal[v] = __ballot(tid < kD && t == v);
+  if (tid < kD && lane == 0) {
+#pragma unroll
+    for (int v = 1; v <= kPlanes; ++v) cnt[wave][v] = __popcll(bal[v]);
+  }
+  __syncthreads();
+  int first[kPlanes + 1], A = 0;
+#pragma unroll
+  for (int v = kPlanes; v >= 1; --v) {
+    first[v] = A;
+    A += cnt[0][v] + cnt[1][v];
+  }
+  int np[kPlanes];  // channels with depth > p
+#pragma unroll
+  for (int p = 0; p < kPlanes; ++p) {
+    np[p] = 0;
+#pragma unroll
+    for (int v = p + 1; v <= kPlanes; ++v) np[p] += cnt[0][v] + cnt[1][v];
+  }
+  int nd[kPlanes], gp[kPlanes + 1];
+  gp[0] = 0;
+#pragma unroll
+  for (int p = 0; p < kPlanes; ++p) {
+    nd[p] = (np[p] + 3) >> 2;
+    gp[p + 1] = gp[p] + nd[p];
+  }
+  const int rg = gp[kPlanes];
+  const bool ok = G <= 4 && A > 0 && A <= kCA && rg <= kCG;
+  if (tid == 0) {
+    P.A = A;
+    P.rg = rg;
+    P.ns = (rg + 3) >> 2;
+    P.ok = ok;
+#pragma unroll
+    for (int p = 0; p < kPlanes; ++p) {
+      P.nd[p] = nd[p];
+      P.gp[p] = gp[p];
+    }
+    P.gp[kPlanes] = rg;
+    const double cells = (double)(np[0] + np[1] + np[2] + np[3]);
+    P.Ku = (cells / 4.0 + (double)A * (double)A * 127.0 * 0x1p-24) * (1.0 + 0x1p-20);
+    P.Eabs = (double)A * 0x1p-120;
+  }
+  if (!ok) {
+    __syncthreads();
+    return;
+  }
+  int xp = -1;  // this channel's proxy index
+  if (tid < kD && t > 0) {
+    xp = first[t] + (wave == 1 ? cnt[0][t] : 0) + __popcll(bal[t] & lanes_below(lane));
+    sact[xp] = tid | (t << 8);
+#pragma unroll
+    for (int h = 0; h < 4; ++h) P.qx[xp][h] = pre.q[h];
+    P.pj[xp] = tid;
+    // ascending position: active channels below this one
+    const uint64_t on = bal[1] | bal[2] | bal[3] | bal[4];
+    int y = __popcll(on & lanes_below(lane));
+    if (wave == 1) y += cnt[0][1] + cnt[0][2] + cnt[0][3] + cnt[0][4];
+    P.px[y] = xp;
+    P.zo[y] = 8.0f - ldexpf(1.0f, 3 - t);
+#pragma unroll
+    for (int h = 0; h < 4; ++h) P.qa[y][h] = pre.q[h];
+  }
+  if (tid >= A && tid < ((A + 7) & ~7)) {  // chain padding: q = 0 adds +0 to every head's score
+    P.px[tid] = A;
+    P.zo[tid] = 0.0f;
+#pragma unroll
+    for (int h = 0; h < 4; ++h) P.qa[tid][h] = 0.0f;
+  }
+  __syncthreads();
+  // row groups: thread (g, k) fills cell k of row group g
+  if (tid < 4 * kCG) {
+    const int g = tid >> 2, k = tid & 3;
+    int p = 0;
+#pragma unroll
+    for (int pp = 1; pp < kPlanes; ++pp) p += g >= gp[pp];
+    const int i = g - gp[p], x = 4 * i + k;
+    const bool real = g < rg && x < np[p];
+    const uint32_t row = real ? (uint32_t)(4 * (sact[x] & 0xFF) + p) : kCPad;
+    // cells 0,1 -> rrow[g][0], cells 2,3 -> rrow[g][1] (16-bit halves)
+    const uint32_t part = row << (16 * (k & 1));
+    const uint32_t other = __shfl_xor(part, 1, kWave);
+    if ((k & 1) == 0) P.rrow[g][k >> 1] = part | other;
+#pragma unroll
+    for (int h = 0; h < 4; ++h) P.qrg[g][h][k] = real && h < G ? P.qx[x][h] : 0.0f;
+    if (k == 0) P.rgp[g] = (uint32_t)p | (uint32_t)i << 8;
+  }
+  if (tid < 4) P.tau[tid] = kNegInf;
+  __syncthreads();
+}
+
+// ---------------------------------------------------------------- scales
+// Lane x (< A) holds the 8 scales of proxy channel x for the group at block
+// sb0, two blocks a dword, read through a buffer descriptor over the unit's
+// scale rows (zero past them, and for lanes >= A).  With 16-byte aligned rows
+// (nb_cap a multiple of 8) one 16-byte load per lane; blocks past nb_cap then
+// read the next row's scales, which only the (ineligible) keys of those
+// blocks and delta see.  Otherwise 8 two-byte loads, each past the range
+// beyond nb_cap.
+struct CScl {
+  uint32_t v[kCSB / 2];
+};
+typedef unsigned short u16x1;
+
+template <bool VEC>
+__device__ __forceinline__ void cscl_issue(CScl& r, const FusedArgs& a, int u, int A, int jrow, int sb0) {
+  const int lane = threadIdx.x & 63;
+  const uint64_t base = reinterpret_cast<uint64_t>(a.scales + (int64_t)u * kD * a.nb_cap);
+  const uint32_t alo = (uint32_t)cuni((int)(uint32_t)base), ahi = (uint32_t)cuni((int)(uint32_t)(base >> 32));
+  const uint32_t bytes = (uint32_t)(kD * 2) * (uint32_t)a.nb_cap;
+  const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+      reinterpret_cast<void*>(((uint64_t)ahi << 32) | alo), (short)0, (int)bytes, kRawBufferFlags);
+  const uint32_t off = lane < A ? ((uint32_t)jrow * (uint32_t)a.nb_cap + (uint32_t)sb0) * 2u : kPastRange;
+  if constexpr (VEC) {
+    const v4u x0 = __builtin_amdgcn_raw_buffer_load_b128(rs, (int)off, 0, 0);
+    r.v[0] = x0.x; r.v[1] = x0.y; r.v[2] = x0.z; r.v[3] = x0.w;
+  } else {
+    const int64_t left = a.nb_cap - (int64_t)sb0;  // blocks of the group inside the row
+    uint32_t h[kCSB];
+#pragma unroll
+    for (int b = 0; b < kCSB; ++b)
+      h[b] = __builtin_amdgcn_raw_buffer_load_b16(rs, (int)(b < left ? off + 2u * b : kPastRange), 0, 0);
+#pragma unroll
+    for (int i = 0; i < kCSB / 2; ++i) r.v[i] = (h[2 * i] & 0xFFFFu) | (h[2 * i + 1] << 16);
+  }
+}
+
+// Per group and head: delta = 2^e and whether a bound exists.
+struct CDel {
+  int e;
+  bool valid;
+};
+
+// Writes the group's scales to ring slot `slot` and returns delta of head
+// `hq` (every lane: its own head for the weights).  qv: q of proxy channel
+// `lane` for the four heads (0 past A).
+__device__ __forceinline__ CDel cscl_commit(const CScl& r, FilterLds& L, int slot, int hq, const float (&qv)[4]) {
+  const int lane = threadIdx.x & 63;
+  uint32_t mx = 0u;
+  if (lane < kCA) {
+#pragma unroll
+    for (int b = 0; b < kCSB; ++b) L.scl[slot][b][lane] = (uint16_t)((r.v[b >> 1] >> (16 * (b & 1))) & 0xFFFFu);
+  }
+#pragma unroll
+  for (int i = 0; i < kCSB / 2; ++i) {
+    const uint32_t v = r.v[i] & 0x7FFF7FFFu;
+    const uint32_t m = (v & 0xFFFFu) > (v >> 16) ? (v & 0xFFFFu) : (v >> 16);
+    mx = m > mx ? m : mx;
+  }
+  const bool nf = __ballot(mx >= 0x7C00u) != 0ull;
+  const float am = half_bits_to_float((uint16_t)(mx >= 0x7C00u ? 0u : mx));
+  float M[4];
+#pragma unroll
+  for (int h = 0; h < 4; ++h) M[h] = wave_max_pos(__fmul_rn(fabsf(qv[h]), am));
+  const float Mh = hq == 0 ? M[0] : hq == 1 ? M[1] : hq == 2 ? M[2] : M[3];
+  CDel d;
+  d.e = 0;
+  d.valid = !nf && Mh <= 3.402823466e38f;
+  if (Mh > 0.0f && d.valid) {
+    int E;
+    (void)frexpf(Mh, &E);  // Mh in [2^(E-1), 2^E)
+    d.e = Mh <= 127.0f * ldexpf(1.0f, E - 7) ? E - 7 : E - 6;
+    d.valid = d.e >= -100 && d.e <= 100;
+  }
+  return d;
+}
+
+// ---------------------------------------------------------------- staging
+// Lane (row group g = lane >> 2, block bq = lane & 3 of the quad) loads the
+// plane words of g's 4 cells for its block through a buffer descriptor over
+// the unit's planes, and stores them as raw[4 g + k][bq].  Pad cells (and row
+// groups past the unit's) read past the descriptor's range, which returns
+// zero; every other load stays inside the unit.
+struct CStage {
+  __amdgpu_buffer_rsrc_t rs;  // the unit's planes (ub bytes)
+  uint32_t boff[4];           // byte offset of cell k's word for block bq of a quad starting at block 0
+};
+struct CRaw {
+  uint64_t w[4];  // cell k's word of block bq
+};
+
+// Pad cells get the offset ub: with the quad's offset (at most 8 nb_cap bytes)
+// added it stays past the range without wrapping (ub + 8 nb_cap < 2^32).
+__device__ __forceinline__ void cstage_setup(CStage& S, const CellPlan& P, const FusedArgs& a, uint64_t ubase,
+                                             uint32_t ub) {
+  const int lane = threadIdx.x & 63, g = lane >> 2, bq = lane & 3;
+  const uint32_t alo = (uint32_t)cuni((int)(uint32_t)ubase), ahi = (uint32_t)cuni((int)(uint32_t)(ubase >> 32));
+  S.rs = __builtin_amdgcn_make_buffer_rsrc(reinterpret_cast<void*>(((uint64_t)ahi << 32) | alo), (short)0,
+                                          (int)(uint32_t)cuni((int)ub), kRawBufferFlags);
+  const bool on = g < cuni(P.rg);
+  const uint32_t r0 = P.rrow[on ? g : 0][0], r1 = P.rrow[on ? g : 0][1];
+  const uint32_t rows[4] = {r0 & 0xFFFFu, r0 >> 16, r1 & 0xFFFFu, r1 >> 16};
+#pragma unroll
+  for (int k = 0; k < 4; ++k)
+    S.boff[k] = on && rows[k] != kCPad ? (rows[k] * (uint32_t)a.nb_cap + (uint32_t)bq) * 8u : ub;
+}
+
+// Loads of the quad whose first block is qb0 (issued for every quad the loop
+// could reach, so that the compiler's wait counts stay exact; a quad past the
+// unit's blocks reads other rows' words or zeros and is never used).
+__device__ __forceinline__ void cstage_issue(CRaw& R, const CStage& S, int qb0) {
+  const int so = cuni((int)((uint32_t)qb0 * 8u));
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const v2u32 v = __builtin_amdgcn_raw_buffer_load_b64(S.rs, (int)S.boff[k], so, 0);
+    R.w[k] = ((uint64_t)v.y << 32) | v.x;
+  }
+}
+
+__device__ __forceinline__ void cstage_write(const CRaw& R, FilterLds& L) {
+  const int lane = threadIdx.x & 63, g = lane >> 2, bq = lane & 3;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) L.raw[4 * g + k][bq] = R.w[k];
+}
+
+// Row groups 2 P and 2 P + 1 of this lane's block and octet (v: its two dwords)
+// from the staged words; lane l (as a source) addresses cell 8 P + ((l & 15) >> 1)
+// of block l >> 4.
+typedef int v2i __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ v2i ctr_read(const FilterLds& L, uint32_t src_off, int P) {
+  const unsigned char* base = reinterpret_cast<const unsigned char*>(&L.raw[0][0]) + src_off + P * 8 * 4 * 8;
+  return __builtin_amdgcn_ds_read_tr8_b64_v2i32((__attribute__((address_space(3))) v2i*)(base));
+}
+
+// ---------------------------------------------------------------- weights
+// Lanes (block b = lane >> 4 of the quad, head h = (lane >> 2) & 3, part =
+// lane & 3): the int8 weights of row groups g = part (mod 4) of block b for
+// head h, their sum, and the accumulator starts of (b, h).  M0 = 1.5 2^(23 + e)
+// (plane 0; plane p uses M0 2^p): the low byte of fl(q a16 + M0 2^p) is
+// rne(q a16 2^-p / delta) as a two's complement byte.
+struct CHead {
+  float M0;     // this lane's head: rounding constant of plane 0
+  int X;        // floor(2 (tau - E) / delta) - 1, clamped
+  int mode;     // 0: thresholds; 1: every key a candidate; 2: none
+};
+
+__device__ __forceinline__ void cquad_weights(const CellPlan& P, FilterLds& L, const CHead& H, int slot, int sbq,
+                                              uint32_t wi) {
+  const int lane = threadIdx.x & 63, b = lane >> 4, h = (lane >> 2) & 3, part = lane & 3;
+  const uint16_t* srow = &L.scl[slot][sbq + b][0];
+  // every read first: row groups g = part + 4 k (wi byte k: dword i | plane p << 4 | real << 6)
+  float4 qv[4];
+  uint32_t s01[4], s23[4];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const uint32_t f = (wi >> (8 * k)) & 0xFFu;
+    const int i = (int)(f & 15u), g = part + 4 * k;
+    qv[k] = *reinterpret_cast<const float4*>(&P.qrg[g][h][0]);
+    s01[k] = *reinterpret_cast<const uint32_t*>(&srow[4 * i]);
+    s23[k] = *reinterpret_cast<const uint32_t*>(&srow[4 * i + 2]);
+  }
+  int wsum = 0;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const uint32_t f = (wi >> (8 * k)) & 0xFFu;
+    const int p = (int)((f >> 4) & 3u), g = part + 4 * k;
+    const float Mp = ldexpf(H.M0, p);
+    const float a0 = half_bits_to_float((uint16_t)(s01[k] & 0xFFFFu)), a1 = half_bits_to_float((uint16_t)(s01[k] >> 16));
+    const float a2 = half_bits_to_float((uint16_t)(s23[k] & 0xFFFFu)), a3 = half_bits_to_float((uint16_t)(s23[k] >> 16));
+    const uint32_t r0 = __float_as_uint(__fmaf_rn(qv[k].x, a0, Mp)), r1 = __float_as_uint(__fmaf_rn(qv[k].y, a1, Mp));
+    const uint32_t r2 = __float_as_uint(__fmaf_rn(qv[k].z, a2, Mp)), r3 = __float_as_uint(__fmaf_rn(qv[k].w, a3, Mp));
+    const uint32_t lo = __builtin_amdgcn_perm(r1, r0, 0x0c0c0400u);
+    const uint32_t hi = __builtin_amdgcn_perm(r3, r2, 0x04000c0cu);
+    const uint32_t wd = (H.mode == 0 && (f & 0x40u)) ? (lo | hi) : 0u;
+    L.W[b][h][g] = wd;
+    wsum = __builtin_amdgcn_sdot4((int)wd, 0x01010101, wsum, false);
+  }
+  wsum += dpp_i<0xB1>(wsum);  // quad_perm [1,0,3,2]
+  wsum += dpp_i<0x4E>(wsum);  // quad_perm [2,3,0,1]
+  // part writes the starts of positions 2 part, 2 part + 1 (nibble hb = part >> 1)
+  int thr = (H.X + wsum) >> 1;
+  thr = thr < -kThrMax ? -kThrMax : thr > kThrMax ? kThrMax : thr;
+  const int hb = part >> 1;
+#pragma unroll
+  for (int m2 = 0; m2 < 2; ++m2) {
+    const int mu = 2 * (part & 1) + m2, pos = 4 * hb + mu;
+    int v;
+    if (H.mode == 0) v = pos == 7 ? thr * 128 - 1 : -(thr * (1 << pos));
+    else if (H.mode == 1) v = pos == 7 ? -kNoBound : kNoBound;
+    else v = pos == 7 ? kNoBound : -kNoBound;
+    L.ini[b][hb][mu][h] = v;
+  }
+}
+
+// ---------------------------------------------------------------- survivors
+// Appends the n buffered survivors of head h to row u G + h (one atomic).
+__device__ __forceinline__ void cflush_head(FilterLds& L, const FusedArgs& a, int u, int h, int n) {
+  const int lane = threadIdx.x & 63, G = a.G;
+  if (n <= 0) return;
+  uint32_t base = 0u;
+  if (lane == 0) base = gatomic_add(&a.ws.cnt[(u * G + h) * kCntStride], (uint32_t)n);
+  base = (uint32_t)__shfl((int)base, 0, kWave);
+  if (lane < n && base + lane < (uint32_t)a.ws.lcap)
+    gstore(&a.ws.cand[(int64_t)(u * G + h) * a.ws.lcap + base + lane], L.sv[h][lane]);
+}
+
+// ---------------------------------------------------------------- re-scoring
+// Exact documented scores of the queued keys (lane e < nq) and their appends
+// to the survivor lists.  First each entry's staged dwords become digit
+// dwords in proxy order (u = sum_p b_p 2^(3-p), byte x of the entry, in
+// place: the plane-p dwords of proxy dword i sit at or after dword i), then
+// the chain runs over the active channels ascending (padded to a multiple of
+// 4 with q = 0, which leaves every score unchanged).
+__device__ __forceinline__ void crescore(const CellPlan& P, FilterLds& L, const FusedArgs& a, int u, int nq, int (&svn)[4]) {
+  const int lane = threadIdx.x & 63, G = a.G;
+  const bool on = lane < nq;
+  const int e = on ? lane : 0;
+  const uint32_t ki = L.qi[e], f = L.qf[e];
+  const uint32_t pos = f & 7u;
+  const int hm = on ? (int)((f >> 3) & 15u) : 0, slot = (int)((f >> 7) & 3u), blk = (int)((f >> 9) & 7u);
+  uint32_t* ent = &L.qx[0][e];  // dword i of the entry at ent[i * kCQ] (entries side by side: no bank conflicts)
+  const int nd0 = cuni(P.nd[0]), nd1 = cuni(P.nd[1]), nd2 = cuni(P.nd[2]), nd3 = cuni(P.nd[3]);
+  const int g1 = cuni(P.gp[1]), g2 = cuni(P.gp[2]), g3 = cuni(P.gp[3]);
+  for (int i = 0; i < nd0; ++i) {
+    const uint32_t w0 = ent[i * kCQ];
+    const uint32_t w1 = i < nd1 ? ent[(g1 + i) * kCQ] : 0u;
+    const uint32_t w2 = i < nd2 ? ent[(g2 + i) * kCQ] : 0u;
+    const uint32_t w3 = i < nd3 ? ent[(g3 + i) * kCQ] : 0u;
+    ent[i * kCQ] = ((w0 >> pos) & 0x01010101u) << 3 | ((w1 >> pos) & 0x01010101u) << 2 |
+                   ((w2 >> pos) & 0x01010101u) << 1 | ((w3 >> pos) & 0x01010101u);
+  }
+  // digit of proxy channel x: byte x & 3 of dword x >> 2
+  const uint8_t* dg = reinterpret_cast<const uint8_t*>(ent);
+  const uint16_t* sv = &L.scl[slot][blk][0];
+  const int A4 = (cuni(P.A) + 3) & ~3;
+  float s[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+  for (int y0 = 0; y0 < A4; y0 += 4) {
+    const int4 xa = *reinterpret_cast<const int4*>(&P.px[y0]);
+    const float4 za = *reinterpret_cast<const float4*>(&P.zo[y0]);
+    const int xs[4] = {xa.x, xa.y, xa.z, xa.w};
+    const float zs[4] = {za.x, za.y, za.z, za.w};
+    uint32_t dv[4], hv[4];
+    float4 q4[4];
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      dv[c] = dg[(xs[c] >> 2) * (kCQ * 4) + (xs[c] & 3)];
+      hv[c] = sv[xs[c]];
+      q4[c] = *reinterpret_cast<const float4*>(&P.qa[y0 + c][0]);
+    }
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const float a8 = __fmul_rn(half_bits_to_float((uint16_t)hv[c]), 0.125f);
+      const float khat = __fmaf_rn((float)dv[c], a8, -__fmul_rn(zs[c], a8));
+      s[0] = __fmaf_rn(q4[c].x, khat, s[0]);
+      s[1] = __fmaf_rn(q4[c].y, khat, s[1]);
+      s[2] = __fmaf_rn(q4[c].z, khat, s[2]);
+      s[3] = __fmaf_rn(q4[c].w, khat, s[3]);
+    }
+  }
+  // survivors of each head go to the wave's LDS buffer; a full buffer (and
+  // the wave's end) appends it to the row's list with one atomic
+#pragma unroll
+  for (int h = 0; h < 4; ++h) {
+    const bool keep = h < G && ((hm >> h) & 1) && s[h] >= P.tau[h];
+    const uint64_t bm = __ballot(keep);
+    if (bm == 0ull) continue;
+    const int c = __popcll(bm);
+    if (svn[h] + c > kSv) {
+      cflush_head(L, a, u, h, svn[h]);
+      svn[h] = 0;
+    }
+    const uint64_t comp = ((uint64_t)score_key(s[h]) << 32) | (uint64_t)(~ki);
+    const int rank = __popcll(bm & lanes_below(lane));
+    if (c > kSv) {  // more than a buffer at once: straight to the list
+      uint32_t base = 0u;
+      if (lane == 0) base = gatomic_add(&a.ws.cnt[(u * G + h) * kCntStride], (uint32_t)c);
+      base = (uint32_t)__shfl((int)base, 0, kWave);
+      if (keep && base + rank < (uint32_t)a.ws.lcap) gstore(&a.ws.cand[(int64_t)(u * G + h) * a.ws.lcap + base + rank], comp);
+    } else {
+      if (keep) L.sv[h][svn[h] + rank] = comp;
+      svn[h] += c;
+    }
+  }
+  lds_order();
+}
+
+// ---------------------------------------------------------------- one wave
+// Blocks [b0, b1) of unit u (b0 a multiple of 4), quad by quad in groups of 8
+// blocks from b0 (one loop iteration each).  The plane words of a quad are
+// loaded two quads ahead (two register sets), the scales of a group one group
+// ahead, in the same order on every path into the loop so that the
+// compiler's load counters stay exact.  A wave's LDS accesses execute in
+// program order, so staged data is read back without a wait.  Re-scoring
+// runs at one place: after a quad's candidates, when the queue holds kCFlush,
+// when a quad's candidates do not fit, before the ring slot of the oldest
+// queued key is reused, and at the end.
+template <bool VEC>
+__device__ __forceinline__ void cwave_run(const CellPlan& P, FilterLds& L, const FusedArgs& a, int u, int b0, int b1,
+                                          int nbu, int lo, int hi) {
+  const int lane = threadIdx.x & 63;
+  const int bq = lane >> 4, nib = (lane >> 3) & 1, oct = lane & 7;
+  const int kb = 8 * oct + 4 * nib;                      // key of mu = 0 within its block
+  const bool wl = ((lane & 15) >> 2) == bq;              // carries weights in the A operand
+  const int hq = (lane >> 2) & 3;                        // head of this lane's weights
+  const uint32_t flip = nib ? 0xFFFFFFFFu : 0u;          // mu = 3 sits at pos 7 in nibble 1
+  uint32_t mk[4];
+#pragma unroll
+  for (int mu = 0; mu < 4; ++mu) mk[mu] = 0x01010101u << (4 * nib + mu);
+  const int A = cuni(P.A), rg = cuni(P.rg);
+  const int srow = lane < A ? P.pj[lane] : 0;  // the scale row of proxy channel `lane`
+  float qv[4];
+#pragma unroll
+  for (int h = 0; h < 4; ++h) qv[h] = lane < A ? P.qx[lane][h] : 0.0f;
+  // this lane's weight row groups g = part + 4 k: dword i | plane p << 4 | real << 6
+  uint32_t wi = 0u;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const int g = (lane & 3) + 4 * k;
+    const uint32_t pi = P.rgp[g];
+    const uint32_t f = g < rg ? ((pi >> 8) & 15u) | (pi & 3u) << 4 | 0x40u : 0u;
+    wi |= f << (8 * k);
+  }
+  // as a transpose source: cell (l & 15) >> 1 of pair 0, block l >> 4
+  const uint32_t src_off = (uint32_t)((((lane & 15) >> 1) * 4 + bq) * 8);
+  // the A operand: this lane's weights, or zeros
+  const uint32_t* wsrc = wl ? &L.W[bq][lane & 3][0] : &L.zero[0];
+  const uint64_t ubase = reinterpret_cast<uint64_t>(a.planes + (int64_t)u * kD * kPlanes * a.nb_cap);
+  const uint32_t ubytes = (uint32_t)(kD * kPlanes * 8) * (uint32_t)a.nb_cap;
+  CStage S;
+  cstage_setup(S, P, a, ubase, ubytes);
+  if (lane < kCG) L.zero[lane] = 0u;
+  int pending = 0, oldest = 0;
+  int svn[4] = {0, 0, 0, 0};  // buffered survivors per head
+  // the issue order here (scales, quad 0, quad 1) is the loop's steady-state
+  // order, so the compiler's load counters agree on every path into the loop
+  CScl sr;
+  cscl_issue<VEC>(sr, a, u, A, srow, b0);
+  sched_fence();
+  CRaw R0, R1;
+  cstage_issue(R0, S, b0);
+  sched_fence();
+  cstage_issue(R1, S, b0 + kQB);
+  sched_fence();
+  CHead H;
+  int slot = 0;
+  auto quad = [&](CRaw& R, int qb0, int it) {
+    const int sbq = qb0 - b0 - kCSB * it;  // first block of the quad within its group
+    cstage_write(R, L);
+    sched_fence();
+    cstage_issue(R, S, qb0 + 2 * kQB);
+    sched_fence();
+    cquad_weights(P, L, H, slot, sbq, wi);
+    lds_order();
+    v4i acc[4];
+#pragma unroll
+    for (int mu = 0; mu < 4; ++mu) acc[mu] = *reinterpret_cast<const v4i*>(&L.ini[bq][nib][mu][0]);
+    // every row group of the quad (pads and groups past the unit's are zero)
+    uint32_t xr[kCG];
+#pragma unroll
+    for (int pp = 0; pp < kCG / 2; ++pp) {
+      const v2i v = ctr_read(L, src_off, pp);
+      xr[2 * pp] = (uint32_t)v.x;
+      xr[2 * pp + 1] = (uint32_t)v.y;
+    }
+    v4i wv[kCG / 4];
+#pragma unroll
+    for (int s2 = 0; s2 < kCG / 4; ++s2) wv[s2] = *reinterpret_cast<const v4i*>(wsrc + 4 * s2);
+#pragma unroll
+    for (int s2 = 0; s2 < kCG / 4; ++s2) {
+      v4i bv[4];
+#pragma unroll
+      for (int mu = 0; mu < 4; ++mu)
+        bv[mu] = v4i{(int)(xr[4 * s2] & mk[mu]), (int)(xr[4 * s2 + 1] & mk[mu]), (int)(xr[4 * s2 + 2] & mk[mu]),
+                     (int)(xr[4 * s2 + 3] & mk[mu])};
+#pragma unroll
+      for (int mu = 0; mu < 4; ++mu) acc[mu] = __builtin_amdgcn_mfma_i32_16x16x64_i8(wv[s2], bv[mu], acc[mu], 0, 0, 0);
+    }
+    // candidates: this lane's keys as a mask, its heads per key
+    const int blk = qb0 + bq;
+    const int kbase = blk * kBlockTokens + kb;
+    const bool live = qb0 < b1;
+    const bool inner = live && qb0 * kBlockTokens >= lo && (qb0 + 4) * kBlockTokens <= hi && qb0 + 4 <= nbu;
+    uint32_t kmask = 0u, hbits = 0u;
+#pragma unroll
+    for (int mu = 0; mu < 4; ++mu) {
+      const int i = kbase + mu;
+      const bool el = inner || (live && i >= lo && i < hi && blk < nbu);
+      const uint32_t fx = mu == 3 ? flip : 0u;
+      const uint32_t hm = (uint32_t)(((uint32_t)acc[mu][0] ^ fx) < 0x80000000u) |
+                          (uint32_t)(((uint32_t)acc[mu][1] ^ fx) < 0x80000000u) << 1 |
+                          (uint32_t)(((uint32_t)acc[mu][2] ^ fx) < 0x80000000u) << 2 |
+                          (uint32_t)(((uint32_t)acc[mu][3] ^ fx) < 0x80000000u) << 3;
+      const bool fl = el && hm != 0u;
+      kmask |= (fl ? 1u : 0u) << mu;
+      hbits |= (fl ? hm : 0u) << (4 * mu);
+    }
+    const bool last = qb0 + kQB >= b1;  // the wave's last quad (or one past it)
+    const bool endg = sbq == kCSB - kQB;
+    if (__ballot(kmask != 0u) != 0ull && pending == 0) oldest = it;
+    const uint32_t meta = (uint32_t)slot << 7 | (uint32_t)(sbq + bq) << 9;
+    while (true) {
+      // every lane's lowest remaining key, as many as fit; re-score when the
+      // queue is full and keys remain, or at the flush points
+      const uint64_t want = __ballot(kmask != 0u);
+      if (want != 0ull && pending < kCQ) {
+        const int rank = __popcll(want & lanes_below(lane));
+        const bool mine = kmask != 0u && rank < kCQ - pending;
+        if (mine) {
+          const int mu = __builtin_ctz(kmask);
+          const int qp = pending + rank;
+#pragma unroll
+          for (int i = 0; i < kCG; ++i) L.qx[i][qp] = xr[i];
+          L.qi[qp] = (uint32_t)(kbase + mu);
+          L.qf[qp] = (uint32_t)(4 * nib + mu) | ((hbits >> (4 * mu)) & 15u) << 3 | meta;
+          kmask &= kmask - 1u;
+        }
+        pending += __popcll(__ballot(mine));
+        continue;
+      }
+      // entries of group it - 3 hold ring slot (it + 1) & 3, rewritten next
+      const bool flush = want != 0ull || pending >= kCFlush ||
+                         (pending > 0 && (last || (endg && oldest <= it + 1 - kCSlots)));
+      if (!flush) break;
+      lds_order();
+      crescore(P, L, a, u, pending, svn);
+      pending = 0;
+      oldest = it;
+      if (want == 0ull) break;
+    }
+    lds_order();
+  };
+  // one loop iteration = one group of 8 blocks (two quads): its scales and
+  // delta, then the quads
+  int it = 0;
+  for (int gb0 = b0; gb0 < b1; gb0 += kCSB, ++it) {
+    slot = it & (kCSlots - 1);
+    {
+      const CDel dl = cscl_commit(sr, L, slot, hq, qv);
+      sched_fence();
+      cscl_issue<VEC>(sr, a, u, A, srow, gb0 + kCSB);  // past the range: harmless, never used
+      sched_fence();
+      const float th = P.tau[hq];
+      H.M0 = ldexpf(12582912.0f, dl.e);  // 1.5 * 2^(23 + e)
+      H.X = 0;
+      if (hq >= a.G || th == kNegInf) H.mode = 2;
+      else if (!dl.valid) H.mode = 1;
+      else {
+        H.mode = 0;
+        const double E = ldexp(P.Ku, dl.e) + P.Eabs;
+        double X = ldexp((double)th - E, 1 - dl.e);  // 2 (tau - E) / delta
+        X = floor(X) - 1.0;
+        X = X < -2.0 * kThrMax ? -2.0 * kThrMax : X > 2.0 * kThrMax ? 2.0 * kThrMax : X;
+        H.X = (int)X;
+      }
+    }
+    quad(R0, gb0, it);
+    quad(R1, gb0 + kQB, it);  // past b1 (an odd quad count): staged but no candidates
+  }
+#pragma unroll
+  for (int h = 0; h < 4; ++h) cflush_head(L, a, u, h, svn[h]);
+}
+
+// ---------------------------------------------------------------- kernel
+// Grid (workgroups per unit, U); wave w of workgroup x takes quads
+// [(x kCWaves + w) qpw, + qpw) of its unit.  Units that pass 2 left to another
+// full pass (uovf[u] >> 1 != 1) or to the exact path return at once.
+template <bool VEC>
+__global__ __launch_bounds__(kCThreads, 3) void fused_filter_kernel(FusedArgs a, int qpw) {
+  __shared__ CellPlan P;
+  __shared__ FilterLds WL[kCWaves];
+  const int u = blockIdx.y, tid = threadIdx.x, wave = cuni(tid >> 6);
+  const uint32_t uo = gload(a.ws.uovf + u);
+  float tv = kNegInf;
+  if (tid < 4 && tid < a.G) tv = gload(a.ws.tau + u * a.G + tid);
+  const CellPre pre = cell_load(a, u);
+  int64_t nu, lo, hi;
+  row_window(a, u, &nu, &lo, &hi, blockIdx.x == 0 && tid == 0);
+  if ((uo >> 1) != 1u) return;
+  if (hi - lo <= a.ws.cap) return;
+  const int64_t nbu = (nu + kBlockTokens - 1) / kBlockTokens;
+  const int64_t gw = (int64_t)blockIdx.x * kCWaves;
+  const int64_t qlo = lo / (kQB * kBlockTokens);
+  const int64_t qhi = (hi + kQB * kBlockTokens - 1) / (kQB * kBlockTokens);
+  if (gw * qpw >= qhi || (gw + kCWaves) * qpw <= qlo) return;
+  cell_plan(P, a, pre);
+  if (!P.ok) return;
+  if (tid < 4) P.tau[tid] = tv;
+  __syncthreads();
+  bool any = false;
+  for (int h = 0; h < a.G; ++h) any |= P.tau[h] != kNegInf;
+  if (!any) return;
+  int64_t q0 = (gw + wave) * qpw, q1 = q0 + qpw;
+  if (q0 < qlo) q0 = qlo;
+  if (q1 > qhi) q1 = qhi;
+  if (q0 >= q1) return;
+  const int64_t b1 = q1 * kQB < nbu ? q1 * kQB : nbu;
+  cwave_run<VEC>(P, WL[wave], a, u, (int)(q0 * kQB), (int)b1, (int)nbu, (int)lo, (int)hi);
+}
+
+// Quads per wave: an even count (whole loop iterations), about kFResident
+// waves over all units (three per SIMD of the chip, one round).
+constexpr int64_t kFResident = 3 * 4 * 256;
+void launch_filter(const FusedArgs& fa, int U, hipStream_t s) {
+  const int64_t nq = (fa.nb_cap + kQB - 1) / kQB;
+  int64_t qpw = ((int64_t)U * nq + kFResident - 1) / kFResident;
+  qpw = (qpw + 1) & ~(int64_t)1;  // whole groups of two quads
+  if (qpw < 2) qpw = 2;
+  const int64_t waves = (nq + qpw - 1) / qpw;
+  const unsigned wgs = (unsigned)((waves + kCWaves - 1) / kCWaves);
+  // 16-byte aligned scale rows: one 16-byte scale load per lane and group
+  if ((fa.nb_cap & 7) == 0 && (reinterpret_cast<uintptr_t>(fa.scales) & 15) == 0)
+    hipLaunchKernelGGL(fused_filter_kernel<true>, dim3(wgs, (unsigned)U), dim3(kCThreads), 0, s, fa, (int)qpw);
+  else
+    hipLaunchKernelGGL(fused_filter_kernel<false>, dim3(wgs, (unsigned)U), dim3(kCThreads), 0, s, fa, (int)qpw);
+}
+
+}  // namespace fathom

@@ -7,6 +7,7 @@ set -o pipefail
 R=$(pwd)
 OUT=${1:-$R/gpurun_out/counters}
 mkdir -p "$OUT"
+OUT=$(cd "$OUT" && pwd)  # absolute: the passes run from /tmp
 BENCH="python3 $R/bench.py --steps 3 --warmup 1 --scan-reps 2 --copies 2 --no-cpu-baseline --traffic-calib 256"
 PASSES=(
   "SQ_WAVES,SQ_WAVE_CYCLES,SQ_BUSY_CYCLES,SQ_WAIT_ANY,SQ_INSTS_VALU,SQ_INSTS_SALU,SQ_INSTS_LDS,SQ_INSTS_VMEM_RD"
