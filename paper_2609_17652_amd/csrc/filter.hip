@@ -29,10 +29,12 @@
 // nib = (l >> 3) & 1) of block l >> 4, and with pos = 4 nib + mu,
 // X & (0x01010101 << pos) is that key's B operand dword of a row group for
 // v_mfma_i32_16x16x64_i8 (byte value b 2^pos, or -128 b at pos 7).  A is
-// block diagonal: row 4 g' + h of k-group g' holds block g''s head-h weights.
-// The accumulators start at -thr 2^pos (128 thr - 1 at pos 7, where the
-// candidate test flips sign), so a key is a candidate iff one of its four
-// accumulators is >= 0 (< 0 at pos 7).
+// block diagonal: row 4 g' + h of k-group g' holds block g''s head-h weights,
+// negated (-W), so an accumulator holds start - 2^pos S (start + 128 S at
+// pos 7).  The starts are thr 2^pos - 1 (-128 thr at pos 7), so a key is a
+// candidate for head h iff its accumulator is < 0 (>= 0 at pos 7): the sign
+// bits of a lane's 16 accumulators, gathered a byte per head, are its keys'
+// candidate heads.
 //
 // Candidate keys are queued per wave in LDS with their lane's staged dwords; a batch is scored exactly in the documented order (channels
 // ascending, fmaf from +0) with the scales of the last four groups kept in
@@ -59,12 +61,12 @@ struct alignas(16) CellPlan {
   double Ku, Eabs;         // E = delta Ku + Eabs
   uint32_t rrow[kCG][2];   // row group g: plane rows 4 j + p of its 4 cells (16-bit halves, kCPad: none)
   uint32_t rgp[kCG];       // row group g: plane p | proxy dword i << 8
-  float qrg[kCG][4][4];    // row group g, head h, cell k: q (0 for pad cells and heads >= G)
+  float qrg[kCG][4][4];    // row group g, head h, cell k: -q (0 for pad cells and heads >= G)
   float qx[kCA][4];        // q by proxy index and head (delta)
   int pj[kCA];             // proxy index -> channel
   int px[kCA];             // ascending position y -> proxy index x (padded to a multiple of 8: x = A)
   float qa[kCA][4];        // q by ascending position and head (re-scoring; 0 on padding)
-  float zo[kCA];           // 8 - 2^(3 - t) by ascending position: khat = (u - zo) a16 / 8 (0 on padding)
+  float zo[kCA];           // -(1 - 2^-t) by ascending position: khat = (u / 8 + zo) a16, exact (0 on padding)
   float tau[4];
 };
 constexpr uint32_t kCPad = 0xFFFFu;
@@ -77,7 +79,7 @@ struct alignas(16) FilterLds {
   uint16_t scl[kCSlots][kCSB][kSclRow];   // fp16 scales: ring slot, block, proxy channel
   uint32_t qx[kCG][kCQ];                  // queued keys' staged dwords (digits while re-scored): dword, entry
   uint32_t qi[kCQ];                       // queued key index
-  uint32_t qf[kCQ];                       // pos | heads << 3 | slot << 7 | block of the group << 9
+  uint32_t qf[kCQ];                       // pos | slot << 3 | block of the group << 8 | head h at bit 7 + 8 h
   uint64_t sv[4][kSv];                    // survivors per head not yet appended to the row's list
 };
 
@@ -209,7 +211,7 @@ __device__ __forceinline__ void cell_plan(CellPlan& P, const FusedArgs& a, const
     int y = __popcll(on & lanes_below(lane));
     if (wave == 1) y += cnt[0][1] + cnt[0][2] + cnt[0][3] + cnt[0][4];
     P.px[y] = xp;
-    P.zo[y] = 8.0f - ldexpf(1.0f, 3 - t);
+    P.zo[y] = -(1.0f - ldexpf(1.0f, -t));
 #pragma unroll
     for (int h = 0; h < 4; ++h) P.qa[y][h] = pre.q[h];
   }
@@ -234,7 +236,7 @@ __device__ __forceinline__ void cell_plan(CellPlan& P, const FusedArgs& a, const
     const uint32_t other = __shfl_xor(part, 1, kWave);
     if ((k & 1) == 0) P.rrow[g][k >> 1] = part | other;
 #pragma unroll
-    for (int h = 0; h < 4; ++h) P.qrg[g][h][k] = real && h < G ? P.qx[x][h] : 0.0f;
+    for (int h = 0; h < 4; ++h) P.qrg[g][h][k] = real && h < G ? -P.qx[x][h] : 0.0f;
     if (k == 0) P.rgp[g] = (uint32_t)p | (uint32_t)i << 8;
   }
   if (tid < 4) P.tau[tid] = kNegInf;
@@ -376,14 +378,18 @@ __device__ __forceinline__ v2i ctr_read(const FilterLds& L, uint32_t src_off, in
 
 // ---------------------------------------------------------------- weights
 // Lanes (block b = lane >> 4 of the quad, head h = (lane >> 2) & 3, part =
-// lane & 3): the int8 weights of row groups g = part (mod 4) of block b for
-// head h, their sum, and the accumulator starts of (b, h).  M0 = 1.5 2^(23 + e)
-// (plane 0; plane p uses M0 2^p): the low byte of fl(q a16 + M0 2^p) is
-// rne(q a16 2^-p / delta) as a two's complement byte.
+// lane & 3): the negated int8 weights -W of row groups g = part (mod 4) of
+// block b for head h, their sum, and the accumulator starts of (b, h).  With
+// Mp = 1.5 2^(23 + e + p) the low byte of fl(-q a16 + Mp) is rne(-q a16 2^-p
+// / delta) as a two's complement byte.  Pad cells (q = 0) get weight 0; a
+// group without thresholds (a head past G, no tau, no valid delta) gets fixed
+// starts that no sum of products can cross (|S 2^pos| < 2^21), whatever its
+// weights.
 struct CHead {
-  float M0;     // this lane's head: rounding constant of plane 0
+  float Mp[4];  // rounding constant of this lane's row groups g = part + 4 k
   int X;        // floor(2 (tau - E) / delta) - 1, clamped
-  int mode;     // 0: thresholds; 1: every key a candidate; 2: none
+  bool m0;      // thresholds apply
+  int c0, c1;   // the starts of positions 2 part and 2 part + 1 when they do not
 };
 
 __device__ __forceinline__ void cquad_weights(const CellPlan& P, FilterLds& L, const CHead& H, int slot, int sbq,
@@ -395,8 +401,7 @@ __device__ __forceinline__ void cquad_weights(const CellPlan& P, FilterLds& L, c
   uint32_t s01[4], s23[4];
 #pragma unroll
   for (int k = 0; k < 4; ++k) {
-    const uint32_t f = (wi >> (8 * k)) & 0xFFu;
-    const int i = (int)(f & 15u), g = part + 4 * k;
+    const int i = (int)((wi >> (8 * k)) & 15u), g = part + 4 * k;
     qv[k] = *reinterpret_cast<const float4*>(&P.qrg[g][h][0]);
     s01[k] = *reinterpret_cast<const uint32_t*>(&srow[4 * i]);
     s23[k] = *reinterpret_cast<const uint32_t*>(&srow[4 * i + 2]);
@@ -404,34 +409,26 @@ __device__ __forceinline__ void cquad_weights(const CellPlan& P, FilterLds& L, c
   int wsum = 0;
 #pragma unroll
   for (int k = 0; k < 4; ++k) {
-    const uint32_t f = (wi >> (8 * k)) & 0xFFu;
-    const int p = (int)((f >> 4) & 3u), g = part + 4 * k;
-    const float Mp = ldexpf(H.M0, p);
+    const int g = part + 4 * k;
+    const float Mp = H.Mp[k];
     const float a0 = half_bits_to_float((uint16_t)(s01[k] & 0xFFFFu)), a1 = half_bits_to_float((uint16_t)(s01[k] >> 16));
     const float a2 = half_bits_to_float((uint16_t)(s23[k] & 0xFFFFu)), a3 = half_bits_to_float((uint16_t)(s23[k] >> 16));
     const uint32_t r0 = __float_as_uint(__fmaf_rn(qv[k].x, a0, Mp)), r1 = __float_as_uint(__fmaf_rn(qv[k].y, a1, Mp));
     const uint32_t r2 = __float_as_uint(__fmaf_rn(qv[k].z, a2, Mp)), r3 = __float_as_uint(__fmaf_rn(qv[k].w, a3, Mp));
-    const uint32_t lo = __builtin_amdgcn_perm(r1, r0, 0x0c0c0400u);
-    const uint32_t hi = __builtin_amdgcn_perm(r3, r2, 0x04000c0cu);
-    const uint32_t wd = (H.mode == 0 && (f & 0x40u)) ? (lo | hi) : 0u;
+    const uint32_t wd = __builtin_amdgcn_perm(r1, r0, 0x0c0c0400u) | __builtin_amdgcn_perm(r3, r2, 0x04000c0cu);
     L.W[b][h][g] = wd;
     wsum = __builtin_amdgcn_sdot4((int)wd, 0x01010101, wsum, false);
   }
   wsum += dpp_i<0xB1>(wsum);  // quad_perm [1,0,3,2]
-  wsum += dpp_i<0x4E>(wsum);  // quad_perm [2,3,0,1]
-  // part writes the starts of positions 2 part, 2 part + 1 (nibble hb = part >> 1)
-  int thr = (H.X + wsum) >> 1;
+  wsum += dpp_i<0x4E>(wsum);  // quad_perm [2,3,0,1]: -Wsum of (b, h)
+  // part writes the starts of positions 2 part, 2 part + 1 (nibble hb = part >> 1);
+  // position 7 is part 3's second
+  int thr = (H.X - wsum) >> 1;
   thr = thr < -kThrMax ? -kThrMax : thr > kThrMax ? kThrMax : thr;
-  const int hb = part >> 1;
-#pragma unroll
-  for (int m2 = 0; m2 < 2; ++m2) {
-    const int mu = 2 * (part & 1) + m2, pos = 4 * hb + mu;
-    int v;
-    if (H.mode == 0) v = pos == 7 ? thr * 128 - 1 : -(thr * (1 << pos));
-    else if (H.mode == 1) v = pos == 7 ? -kNoBound : kNoBound;
-    else v = pos == 7 ? kNoBound : -kNoBound;
-    L.ini[b][hb][mu][h] = v;
-  }
+  const int hb = part >> 1, mu0 = 2 * (part & 1);
+  const int t0 = thr * (1 << (4 * hb + mu0)), t1 = thr * (1 << (4 * hb + mu0 + 1));
+  L.ini[b][hb][mu0][h] = H.m0 ? t0 - 1 : H.c0;
+  L.ini[b][hb][mu0 + 1][h] = H.m0 ? (part == 3 ? -t1 : t1 - 1) : H.c1;
 }
 
 // ---------------------------------------------------------------- survivors
@@ -458,8 +455,8 @@ __device__ __forceinline__ void crescore(const CellPlan& P, FilterLds& L, const 
   const bool on = lane < nq;
   const int e = on ? lane : 0;
   const uint32_t ki = L.qi[e], f = L.qf[e];
-  const uint32_t pos = f & 7u;
-  const int hm = on ? (int)((f >> 3) & 15u) : 0, slot = (int)((f >> 7) & 3u), blk = (int)((f >> 9) & 7u);
+  const uint32_t pos = f & 7u, hm = on ? f : 0u;
+  const int slot = (int)((f >> 3) & 3u), blk = (int)((f >> 8) & 7u);
   uint32_t* ent = &L.qx[0][e];  // dword i of the entry at ent[i * kCQ] (entries side by side: no bank conflicts)
   const int nd0 = cuni(P.nd[0]), nd1 = cuni(P.nd[1]), nd2 = cuni(P.nd[2]), nd3 = cuni(P.nd[3]);
   const int g1 = cuni(P.gp[1]), g2 = cuni(P.gp[2]), g3 = cuni(P.gp[3]);
@@ -491,8 +488,10 @@ __device__ __forceinline__ void crescore(const CellPlan& P, FilterLds& L, const 
     }
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
-      const float a8 = __fmul_rn(half_bits_to_float((uint16_t)hv[c]), 0.125f);
-      const float khat = __fmaf_rn((float)dv[c], a8, -__fmul_rn(zs[c], a8));
+      // (u / 8 + zo) has at most 5 significant bits, its product with a16 at
+      // most 16: both steps are exact
+      const float x8 = __fmaf_rn((float)dv[c], 0.125f, zs[c]);
+      const float khat = __fmaf_rn(x8, half_bits_to_float((uint16_t)hv[c]), 0.0f);
       s[0] = __fmaf_rn(q4[c].x, khat, s[0]);
       s[1] = __fmaf_rn(q4[c].y, khat, s[1]);
       s[2] = __fmaf_rn(q4[c].z, khat, s[2]);
@@ -503,7 +502,7 @@ __device__ __forceinline__ void crescore(const CellPlan& P, FilterLds& L, const 
   // the wave's end) appends it to the row's list with one atomic
 #pragma unroll
   for (int h = 0; h < 4; ++h) {
-    const bool keep = h < G && ((hm >> h) & 1) && s[h] >= P.tau[h];
+    const bool keep = h < G && ((hm >> (7 + 8 * h)) & 1u) && s[h] >= P.tau[h];
     const uint64_t bm = __ballot(keep);
     if (bm == 0ull) continue;
     const int c = __popcll(bm);
@@ -548,6 +547,7 @@ __device__ __forceinline__ void cwave_run(const CellPlan& P, FilterLds& L, const
   uint32_t mk[4];
 #pragma unroll
   for (int mu = 0; mu < 4; ++mu) mk[mu] = 0x01010101u << (4 * nib + mu);
+  const bool top = (lane & 3) == 3;  // as a weight lane: its second start is position 7
   const int A = cuni(P.A), rg = cuni(P.rg);
   const int srow = lane < A ? P.pj[lane] : 0;  // the scale row of proxy channel `lane`
   float qv[4];
@@ -617,35 +617,38 @@ __device__ __forceinline__ void cwave_run(const CellPlan& P, FilterLds& L, const
 #pragma unroll
       for (int mu = 0; mu < 4; ++mu) acc[mu] = __builtin_amdgcn_mfma_i32_16x16x64_i8(wv[s2], bv[mu], acc[mu], 0, 0, 0);
     }
-    // candidates: this lane's keys as a mask, its heads per key
+    // candidates: this lane's eligible keys (all four inside the window but
+    // at the unit's edges), and per key its candidate heads
     const int blk = qb0 + bq;
     const int kbase = blk * kBlockTokens + kb;
     const bool live = qb0 < b1;
     const bool inner = live && qb0 * kBlockTokens >= lo && (qb0 + 4) * kBlockTokens <= hi && qb0 + 4 <= nbu;
-    uint32_t kmask = 0u, hbits = 0u;
+    uint32_t em = 0xFu;
+    if (!inner) {
+      const int e0 = min(max(lo - kbase, 0), 4), e1 = min(max(hi - kbase, 0), 4);
+      em = live && blk < nbu ? (0xFu << e0) & ~(0xFu << e1) & 0xFu : 0u;
+    }
+    // byte h of D: bit mu set iff key mu is a candidate for head h (the sign
+    // bytes of the four heads' accumulators side by side, flipped at pos 7)
+    uint32_t D = 0u;
 #pragma unroll
     for (int mu = 0; mu < 4; ++mu) {
-      const int i = kbase + mu;
-      const bool el = inner || (live && i >= lo && i < hi && blk < nbu);
-      const uint32_t fx = mu == 3 ? flip : 0u;
-      const uint32_t hm = (uint32_t)(((uint32_t)acc[mu][0] ^ fx) < 0x80000000u) |
-                          (uint32_t)(((uint32_t)acc[mu][1] ^ fx) < 0x80000000u) << 1 |
-                          (uint32_t)(((uint32_t)acc[mu][2] ^ fx) < 0x80000000u) << 2 |
-                          (uint32_t)(((uint32_t)acc[mu][3] ^ fx) < 0x80000000u) << 3;
-      const bool fl = el && hm != 0u;
-      kmask |= (fl ? 1u : 0u) << mu;
-      hbits |= (fl ? hm : 0u) << (4 * mu);
+      const uint32_t T = __builtin_amdgcn_perm((uint32_t)acc[mu][1], (uint32_t)acc[mu][0], 0x0c0c0703u) |
+                         __builtin_amdgcn_perm((uint32_t)acc[mu][3], (uint32_t)acc[mu][2], 0x07030c0cu);
+      D |= ((mu == 3 ? T ^ flip : T) & 0x80808080u) >> (7 - mu);
     }
+    D &= em * 0x01010101u;
+    uint32_t kmask = (D | D >> 8 | D >> 16 | D >> 24) & 0xFu;
     const bool last = qb0 + kQB >= b1;  // the wave's last quad (or one past it)
     const bool endg = sbq == kCSB - kQB;
     if (__ballot(kmask != 0u) != 0ull && pending == 0) oldest = it;
-    const uint32_t meta = (uint32_t)slot << 7 | (uint32_t)(sbq + bq) << 9;
+    const uint32_t meta = (uint32_t)slot << 3 | (uint32_t)(sbq + bq) << 8;
     while (true) {
       // every lane's lowest remaining key, as many as fit; re-score when the
       // queue is full and keys remain, or at the flush points
       const uint64_t want = __ballot(kmask != 0u);
       if (want != 0ull && pending < kCQ) {
-        const int rank = __popcll(want & lanes_below(lane));
+        const int rank = (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(want >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)want, 0u));
         const bool mine = kmask != 0u && rank < kCQ - pending;
         if (mine) {
           const int mu = __builtin_ctz(kmask);
@@ -653,7 +656,7 @@ __device__ __forceinline__ void cwave_run(const CellPlan& P, FilterLds& L, const
 #pragma unroll
           for (int i = 0; i < kCG; ++i) L.qx[i][qp] = xr[i];
           L.qi[qp] = (uint32_t)(kbase + mu);
-          L.qf[qp] = (uint32_t)(4 * nib + mu) | ((hbits >> (4 * mu)) & 15u) << 3 | meta;
+          L.qf[qp] = (uint32_t)(4 * nib + mu) | meta | ((D >> mu) & 0x01010101u) << 7;
           kmask &= kmask - 1u;
         }
         pending += __popcll(__ballot(mine));
@@ -682,18 +685,22 @@ __device__ __forceinline__ void cwave_run(const CellPlan& P, FilterLds& L, const
       cscl_issue<VEC>(sr, a, u, A, srow, gb0 + kCSB);  // past the range: harmless, never used
       sched_fence();
       const float th = P.tau[hq];
-      H.M0 = ldexpf(12582912.0f, dl.e);  // 1.5 * 2^(23 + e)
+      const float M0 = ldexpf(12582912.0f, dl.e);  // 1.5 * 2^(23 + e)
+#pragma unroll
+      for (int k = 0; k < 4; ++k) H.Mp[k] = ldexpf(M0, (int)((wi >> (8 * k + 4)) & 3u));
       H.X = 0;
-      if (hq >= a.G || th == kNegInf) H.mode = 2;
-      else if (!dl.valid) H.mode = 1;
-      else {
-        H.mode = 0;
+      const bool none = hq >= a.G || th == kNegInf;  // no key of this head is a candidate
+      H.m0 = !none && dl.valid;
+      if (H.m0) {
         const double E = ldexp(P.Ku, dl.e) + P.Eabs;
         double X = ldexp((double)th - E, 1 - dl.e);  // 2 (tau - E) / delta
         X = floor(X) - 1.0;
         X = X < -2.0 * kThrMax ? -2.0 * kThrMax : X > 2.0 * kThrMax ? 2.0 * kThrMax : X;
         H.X = (int)X;
       }
+      // no thresholds: every key a candidate (no valid delta) or none
+      H.c0 = none ? kNoBound : -kNoBound;
+      H.c1 = top ? -H.c0 : H.c0;
     }
     quad(R0, gb0, it);
     quad(R1, gb0 + kQB, it);  // past b1 (an odd quad count): staged but no candidates
