@@ -526,8 +526,11 @@ __device__ __forceinline__ void crescore(const CellPlan& P, FilterLds& L, const 
 }
 
 // ---------------------------------------------------------------- one wave
-// Blocks [b0, b1) of unit u (b0 a multiple of 4), quad by quad in groups of 8
-// blocks from b0 (one loop iteration each).  The plane words of a quad are
+// Blocks [b0, b1) of unit u (b0 a multiple of 4, b1 = b0 for a wave with no
+// blocks), quad by quad in groups of 8 blocks from b0 (one loop iteration
+// each).  `ready` runs once every first load is issued (every wave of the
+// workgroup calls it, so it may hold a barrier); the wave stops if it
+// returns false.  The plane words of a quad are
 // loaded two quads ahead (two register sets), the scales of a group one group
 // ahead, in the same order on every path into the loop so that the
 // compiler's load counters stay exact.  A wave's LDS accesses execute in
@@ -535,9 +538,9 @@ __device__ __forceinline__ void crescore(const CellPlan& P, FilterLds& L, const 
 // runs at one place: after a quad's candidates, when the queue holds kCFlush,
 // when a quad's candidates do not fit, before the ring slot of the oldest
 // queued key is reused, and at the end.
-template <bool VEC>
+template <bool VEC, class Ready>
 __device__ __forceinline__ void cwave_run(const CellPlan& P, FilterLds& L, const FusedArgs& a, int u, int b0, int b1,
-                                          int nbu, int lo, int hi) {
+                                          int nbu, int lo, int hi, Ready&& ready) {
   const int lane = threadIdx.x & 63;
   const int bq = lane >> 4, nib = (lane >> 3) & 1, oct = lane & 7;
   const int kb = 8 * oct + 4 * nib;                      // key of mu = 0 within its block
@@ -583,6 +586,7 @@ __device__ __forceinline__ void cwave_run(const CellPlan& P, FilterLds& L, const
   sched_fence();
   cstage_issue(R1, S, b0 + kQB);
   sched_fence();
+  if (!ready()) return;
   CHead H;
   int slot = 0;
   auto quad = [&](CRaw& R, int qb0, int it) {
@@ -709,6 +713,57 @@ __device__ __forceinline__ void cwave_run(const CellPlan& P, FilterLds& L, const
   for (int h = 0; h < 4; ++h) cflush_head(L, a, u, h, svn[h]);
 }
 
+// ---------------------------------------------------------------- tau
+// Sec. 2 asks for the k largest scores; survivors are the keys whose exact
+// score reaches tau, and the result never depends on tau as long as at least
+// k keys survive (else the row is computed exactly).  tau of a row is about
+// the m-th largest of its sampled proxies (the sample pass keeps the 8
+// largest of every sampled quad), m = ceil(1.25 k sampled / eligible) + 16;
+// when fewer samples exist the smallest one is used if about 1.1 k keys are
+// expected above it, else tau = -inf (no filter).  Wave w of a workgroup
+// finds tau of its unit's row w (w < G) from its lanes' 8 samples each: the
+// largest 16-bit prefix of the order-preserving keys with at least m samples
+// at or above it, by ballot counts, so tau rounds the m-th sample down to 7
+// mantissa bits (a few more survivors, no other effect).
+constexpr int kCTauPer = kSmpRow / kWave;
+
+__device__ __forceinline__ float ctau(const FusedArgs& a, const float (&sv)[kCTauPer], int64_t lo, int64_t hi) {
+  const int lane = threadIdx.x & 63;
+  uint32_t key[kCTauPer];
+  int nv = 0;
+#pragma unroll
+  for (int x = 0; x < kCTauPer; ++x) {
+    key[x] = sv[x] > kNegInf ? score_key(sv[x]) | 1u : 0u;  // proxies are never NaN; keep 0 free
+    nv += __popcll(__ballot(key[x] != 0u));
+  }
+  // eligible keys in the sampled quads (a unit of this pass has fewer than
+  // 2^26 keys and at most kSampleQuads sampled quads: 32-bit products)
+  uint32_t m_s = 0u;
+  for (int x = lane; x < a.ws.s_quads; x += kWave) {
+    const int64_t k0 = x * a.ws.s_stride * kQB * kBlockTokens, k1 = k0 + kQB * kBlockTokens;
+    const int64_t x0 = k0 > lo ? k0 : lo, x1 = k1 < hi ? k1 : hi;
+    m_s += x1 > x0 ? (uint32_t)(x1 - x0) : 0u;
+  }
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) m_s += (uint32_t)__shfl_xor((int)m_s, o, kWave);
+  m_s = (uint32_t)cuni((int)m_s);
+  const uint32_t m_e = (uint32_t)(hi - lo), kk = (uint32_t)a.k;
+  uint32_t m = m_s > 0u ? (5u * kk * m_s + 4u * m_e - 1u) / (4u * m_e) + 16u : 0u;
+  if (m > (uint32_t)nv) m = 10ull * (uint64_t)nv * m_e >= 11ull * kk * m_s ? (uint32_t)nv : 0u;
+  if (m == 0u) return kNegInf;
+  uint32_t prefix = 0u;
+  for (int bit = 31; bit >= 16; --bit) {
+    const uint32_t cand = prefix | (1u << bit);
+    uint32_t c = 0u;
+#pragma unroll
+    for (int x = 0; x < kCTauPer; ++x) c += (uint32_t)__popcll(__ballot(key[x] >= cand));
+    if (c >= m) prefix = cand;
+  }
+  // prefix has a nonzero bit (m <= nv samples lie at or above 2^16): the
+  // smallest key of its range, as a float
+  return __uint_as_float((prefix & 0x80000000u) ? (prefix & 0x7FFFFFFFu) : ~prefix);
+}
+
 // ---------------------------------------------------------------- kernel
 // Grid (workgroups per unit, U); wave w of workgroup x takes quads
 // [(x kCWaves + w) qpw, + qpw) of its unit.  Units that pass 2 left to another
@@ -717,10 +772,16 @@ template <bool VEC>
 __global__ __launch_bounds__(kCThreads, 3) void fused_filter_kernel(FusedArgs a, int qpw) {
   __shared__ CellPlan P;
   __shared__ FilterLds WL[kCWaves];
-  const int u = blockIdx.y, tid = threadIdx.x, wave = cuni(tid >> 6);
+  const int u = blockIdx.y, tid = threadIdx.x, wave = cuni(tid >> 6), lane = tid & 63, G = a.G;
   const uint32_t uo = gload(a.ws.uovf + u);
-  float tv = kNegInf;
-  if (tid < 4 && tid < a.G) tv = gload(a.ws.tau + u * a.G + tid);
+  // this wave's row's sampled proxies first: tau waits on them
+  const int nsm = wave < G ? a.ws.s_quads * kSmpW : 0;
+  float sv[kCTauPer];
+#pragma unroll
+  for (int x = 0; x < kCTauPer; ++x) {
+    const int i = lane + kWave * x;
+    sv[x] = i < nsm ? gload(a.ws.samp + (int64_t)(u * G + wave) * kSmpRow + i) : kNegInf;
+  }
   const CellPre pre = cell_load(a, u);
   int64_t nu, lo, hi;
   row_window(a, u, &nu, &lo, &hi, blockIdx.x == 0 && tid == 0);
@@ -733,17 +794,27 @@ __global__ __launch_bounds__(kCThreads, 3) void fused_filter_kernel(FusedArgs a,
   if (gw * qpw >= qhi || (gw + kCWaves) * qpw <= qlo) return;
   cell_plan(P, a, pre);
   if (!P.ok) return;
-  if (tid < 4) P.tau[tid] = tv;
-  __syncthreads();
-  bool any = false;
-  for (int h = 0; h < a.G; ++h) any |= P.tau[h] != kNegInf;
-  if (!any) return;
   int64_t q0 = (gw + wave) * qpw, q1 = q0 + qpw;
   if (q0 < qlo) q0 = qlo;
   if (q1 > qhi) q1 = qhi;
-  if (q0 >= q1) return;
-  const int64_t b1 = q1 * kQB < nbu ? q1 * kQB : nbu;
-  cwave_run<VEC>(P, WL[wave], a, u, (int)(q0 * kQB), (int)b1, (int)nbu, (int)lo, (int)hi);
+  const int64_t b1 = q0 >= q1 ? q0 * kQB : q1 * kQB < nbu ? q1 * kQB : nbu;
+  // tau while the first loads are in flight: every workgroup finds the same
+  // values; the one holding the window's first quad leaves them for the rank
+  // pass
+  auto ready = [&]() -> bool {
+    if (wave < G) {
+      const float tv = ctau(a, sv, lo, hi);
+      if (lane == 0) {
+        P.tau[wave] = tv;
+        if (gw * qpw <= qlo) gstore(a.ws.tau + u * G + wave, tv);
+      }
+    }
+    __syncthreads();
+    bool any = false;
+    for (int h = 0; h < G; ++h) any |= P.tau[h] != kNegInf;
+    return any;
+  };
+  cwave_run<VEC>(P, WL[wave], a, u, (int)(q0 * kQB), (int)b1, (int)nbu, (int)lo, (int)hi, ready);
 }
 
 // Quads per wave: an even count (whole loop iterations), about kFResident

@@ -923,6 +923,56 @@ __device__ void wave_run(const Plan& P, WaveLdsT<NSLM, SQB, RQ, QCAP>& W, const 
   if (!SAMPLE && pending > 0) rescore_batch<SQB>(P, W, a, u, pending);
 }
 
+// ---------------------------------------------------------------- unit state
+// The full-pass class of a unit with sc[v] active channels of depth v
+// (v = 1..kPlanes): 0 = no filter (its rows are computed exactly), 1 = the
+// cell filter (filter.hip), else the wide pass's slice count (> kNarrow).
+__device__ __forceinline__ uint32_t unit_class(const FusedArgs& a, const int (&sc)[kPlanes + 1], int64_t lo,
+                                               int64_t hi) {
+  const int A = sc[1] + sc[2] + sc[3] + sc[4];
+  if (!(a.G <= 4 && A > 0 && hi - lo > a.ws.cap)) return 0u;
+  uint32_t cls = (uint32_t)((A + 15) >> 4);
+  // row groups: the depth of each dword's first channel in the proxy order
+  // (depth descending); the cell filter stages at most kOneRows of them
+  int rows = 0;
+  for (int x = 0; x < A; x += 4) rows += x < sc[4] ? 4 : x < sc[4] + sc[3] ? 3 : x < sc[4] + sc[3] + sc[2] ? 2 : 1;
+  if (cls <= (uint32_t)kNarrow) cls = (rows <= kOneRows && a.nb_cap < kOneNbMax) ? 1u : (uint32_t)(kNarrow + 1);
+  return cls;
+}
+
+// The per-call state of unit u's rows, set by the sample pass's workgroup 0
+// of the unit (every thread; thread j < 128 holds channel j's depth t): the
+// survivor counts and the exact pass's control words cleared, tau = -inf
+// until the full pass sets it, and the unit's class.  The tau pass sets the
+// same state when it runs.
+__device__ __forceinline__ void unit_reset(const FusedArgs& a, int u, int t, int64_t lo, int64_t hi) {
+  __shared__ int sc2[2][kPlanes + 1];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, G = a.G;
+  if (t > kPlanes) t = kPlanes;
+  uint64_t bal[kPlanes + 1];
+#pragma unroll
+  for (int v = 1; v <= kPlanes; ++v) bal[v] = __ballot(tid < kD && t == v);
+  if (tid < kD && lane == 0) {
+#pragma unroll
+    for (int v = 1; v <= kPlanes; ++v) sc2[wave][v] = __popcll(bal[v]);
+  }
+  if (tid < G) {
+    const int r = u * G + tid;
+    gstore(a.ws.cnt + r * kCntStride, 0u);
+    gstore(a.ws.xctl + 1 + r, 0u);
+    gstore(a.ws.tau + r, kNegInf);
+  }
+  if (u == 0 && tid == 0) gstore(a.ws.xctl, 0u);
+  __syncthreads();
+  if (tid == 0) {
+    int sc[kPlanes + 1];
+    sc[0] = 0;
+#pragma unroll
+    for (int v = 1; v <= kPlanes; ++v) sc[v] = sc2[0][v] + sc2[1][v];
+    gstore(a.ws.uovf + u, unit_class(a, sc, lo, hi) << 1);
+  }
+}
+
 // ---------------------------------------------------------------- pass 1
 // NSLM = kNarrow when the caller's bound leaves no unit to the wide full pass:
 // a unit the narrow instantiation cannot take gets no samples (its rows are
@@ -935,6 +985,7 @@ __global__ __launch_bounds__(kFT) void fused_sample_kernel(FusedArgs a) {
   const PlanPre pre = plan_load<QF16>(a, u);
   int64_t nu, lo, hi;
   row_window(a, u, &nu, &lo, &hi, false);
+  if (blockIdx.x == 0) unit_reset(a, u, pre.t, lo, hi);
   if (hi - lo <= a.ws.cap) return;  // computed directly by pass 4
   plan_setup(P, a, u, pre);
   if (!P.ok || P.A == 0) return;
@@ -988,17 +1039,8 @@ __global__ __launch_bounds__(kTauThreads) void fused_tau_kernel(FusedArgs a) {
   const int A = sc[1] + sc[2] + sc[3] + sc[4];
   const bool ok = G <= 4 && A > 0 && hi - lo > a.ws.cap;
   if (tid == 0 && r % G == 0) {
-    uint32_t cls = 0u;
-    if (ok) {
-      cls = (uint32_t)((A + 15) >> 4);
-      // row groups: the depth of each dword's first channel in the proxy order
-      // (depth descending); the narrow pass stages at most kOneRows of them
-      int rows = 0;
-      for (int x = 0; x < A; x += 4) rows += x < sc[4] ? 4 : x < sc[4] + sc[3] ? 3 : x < sc[4] + sc[3] + sc[2] ? 2 : 1;
-      // the cell filter (filter.hip) takes the units the narrow instantiation could
-      if (cls <= (uint32_t)kNarrow) cls = (rows <= kOneRows && a.nb_cap < kOneNbMax) ? 1u : (uint32_t)(kNarrow + 1);
-    }
-    a.ws.uovf[u] = cls << 1;
+    const int scv[kPlanes + 1] = {0, sc[1], sc[2], sc[3], sc[4]};
+    a.ws.uovf[u] = unit_class(a, scv, lo, hi) << 1;
   }
   if (!ok) {
     if (tid == 0) a.ws.tau[r] = kNegInf;
@@ -1780,7 +1822,9 @@ fathom_status launch_scan_topk_fused(const uint64_t* planes, const uint16_t* sca
       else hipLaunchKernelGGL((fused_sample_kernel<false, kNarrow>), gs, dim3(kFT), 0, s, fa);
     }
   }
-  hipLaunchKernelGGL(fused_tau_kernel, dim3(R), dim3(kTauThreads), 0, s, fa);
+  // narrow: the cell filter finds tau itself and the sample pass sets the
+  // rows' state, so the tau pass runs only for the wide pass or G > 4
+  if (wide || G > 4) hipLaunchKernelGGL(fused_tau_kernel, dim3(R), dim3(kTauThreads), 0, s, fa);
   if (G <= 4) {
     dim3 gm((unsigned)fa.ws.nwg, (unsigned)U);
     launch_filter(fa, U, s);
