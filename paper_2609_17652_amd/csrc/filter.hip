@@ -48,7 +48,7 @@ constexpr int kCA = 48;          // active channels at most
 constexpr int kCSB = 8;          // blocks per group (one delta per head; one loop iteration)
 constexpr int kCSlots = 4;       // groups of scales kept for re-scoring
 constexpr int kCQ = 64;          // queued candidates per wave (one ballot fits)
-constexpr int kCFlush = 48;      // re-score at a quad boundary once this many are queued
+constexpr int kCFlush = 64;      // re-score at a quad boundary once the queue is full
 constexpr int kSclRow = kCA + 2; // halfs per scale row: an odd number of dwords
 constexpr int kSv = 16;          // survivors per head buffered in LDS before a list append
 constexpr int kCWaves = 4;       // waves per workgroup
@@ -98,26 +98,37 @@ __device__ __forceinline__ void lds_order() { asm volatile("" ::: "memory"); }
 __device__ __forceinline__ void sched_fence() { __builtin_amdgcn_sched_barrier(0); }
 __device__ __forceinline__ uint64_t lanes_below(int lane) { return lane == 0 ? 0ull : (~0ull >> (64 - lane)); }
 
+// Lane moves within rows of 16 (rotations and quad permutes: every lane has a
+// source, so the bound control only lets the move fuse into its user).
 template <int CTRL>
-__device__ __forceinline__ float dpp_f(float v) {
-  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
+__device__ __forceinline__ uint32_t dpp_u(uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, CTRL, 0xF, 0xF, true);
 }
 template <int CTRL>
 __device__ __forceinline__ int dpp_i(int v) {
-  return __builtin_amdgcn_update_dpp(0, v, CTRL, 0xF, 0xF, false);
+  return __builtin_amdgcn_update_dpp(0, v, CTRL, 0xF, 0xF, true);
 }
-// Largest value over the wave of non-negative floats (uniform result).
-__device__ __forceinline__ float wave_max_pos(float v) {
-  v = fmaxf(v, dpp_f<0x128>(v));  // row_ror 8
-  v = fmaxf(v, dpp_f<0x124>(v));  // row_ror 4
-  v = fmaxf(v, dpp_f<0x122>(v));  // row_ror 2
-  v = fmaxf(v, dpp_f<0x121>(v));  // row_ror 1: every lane of a row holds the row's largest
-  const uint32_t a = (uint32_t)__builtin_amdgcn_readlane(__float_as_int(v), 0);
-  const uint32_t b = (uint32_t)__builtin_amdgcn_readlane(__float_as_int(v), 16);
-  const uint32_t c = (uint32_t)__builtin_amdgcn_readlane(__float_as_int(v), 32);
-  const uint32_t d = (uint32_t)__builtin_amdgcn_readlane(__float_as_int(v), 48);
-  const uint32_t m1 = a > b ? a : b, m2 = c > d ? c : d;  // non-negative floats order as their bits
-  return __uint_as_float(m1 > m2 ? m1 : m2);
+// Largest value over the wave of four sets of non-negative floats, given and
+// returned as their bits (which order as the values), the four reductions
+// interleaved step by step; uniform results.
+__device__ __forceinline__ void wave_max4_pos(uint32_t (&v)[4]) {
+#pragma unroll
+  for (int h = 0; h < 4; ++h) v[h] = max(v[h], dpp_u<0x128>(v[h]));  // row_ror 8
+#pragma unroll
+  for (int h = 0; h < 4; ++h) v[h] = max(v[h], dpp_u<0x124>(v[h]));  // row_ror 4
+#pragma unroll
+  for (int h = 0; h < 4; ++h) v[h] = max(v[h], dpp_u<0x122>(v[h]));  // row_ror 2
+#pragma unroll
+  for (int h = 0; h < 4; ++h) v[h] = max(v[h], dpp_u<0x121>(v[h]));  // row_ror 1: each lane holds its row's largest
+#pragma unroll
+  for (int h = 0; h < 4; ++h) {
+    const uint32_t a = (uint32_t)__builtin_amdgcn_readlane((int)v[h], 0);
+    const uint32_t b = (uint32_t)__builtin_amdgcn_readlane((int)v[h], 16);
+    const uint32_t c = (uint32_t)__builtin_amdgcn_readlane((int)v[h], 32);
+    const uint32_t d = (uint32_t)__builtin_amdgcn_readlane((int)v[h], 48);
+    const uint32_t m1 = a > b ? a : b, m2 = c > d ? c : d;
+    v[h] = m1 > m2 ? m1 : m2;
+  }
 }
 
 // ---------------------------------------------------------------- plan
@@ -303,10 +314,11 @@ __device__ __forceinline__ CDel cscl_commit(const CScl& r, FilterLds& L, int slo
   }
   const bool nf = __ballot(mx >= 0x7C00u) != 0ull;
   const float am = half_bits_to_float((uint16_t)(mx >= 0x7C00u ? 0u : mx));
-  float M[4];
+  uint32_t M[4];
 #pragma unroll
-  for (int h = 0; h < 4; ++h) M[h] = wave_max_pos(__fmul_rn(fabsf(qv[h]), am));
-  const float Mh = hq == 0 ? M[0] : hq == 1 ? M[1] : hq == 2 ? M[2] : M[3];
+  for (int h = 0; h < 4; ++h) M[h] = __float_as_uint(__fmul_rn(fabsf(qv[h]), am));
+  wave_max4_pos(M);
+  const float Mh = __uint_as_float(hq == 0 ? M[0] : hq == 1 ? M[1] : hq == 2 ? M[2] : M[3]);
   CDel d;
   d.e = 0;
   d.valid = !nf && Mh <= 3.402823466e38f;
