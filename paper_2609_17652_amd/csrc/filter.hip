@@ -98,39 +98,6 @@ __device__ __forceinline__ void lds_order() { asm volatile("" ::: "memory"); }
 __device__ __forceinline__ void sched_fence() { __builtin_amdgcn_sched_barrier(0); }
 __device__ __forceinline__ uint64_t lanes_below(int lane) { return lane == 0 ? 0ull : (~0ull >> (64 - lane)); }
 
-// Lane moves within rows of 16 (rotations and quad permutes: every lane has a
-// source, so the bound control only lets the move fuse into its user).
-template <int CTRL>
-__device__ __forceinline__ uint32_t dpp_u(uint32_t v) {
-  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, CTRL, 0xF, 0xF, true);
-}
-template <int CTRL>
-__device__ __forceinline__ int dpp_i(int v) {
-  return __builtin_amdgcn_update_dpp(0, v, CTRL, 0xF, 0xF, true);
-}
-// Largest value over the wave of four sets of non-negative floats, given and
-// returned as their bits (which order as the values), the four reductions
-// interleaved step by step; uniform results.
-__device__ __forceinline__ void wave_max4_pos(uint32_t (&v)[4]) {
-#pragma unroll
-  for (int h = 0; h < 4; ++h) v[h] = max(v[h], dpp_u<0x128>(v[h]));  // row_ror 8
-#pragma unroll
-  for (int h = 0; h < 4; ++h) v[h] = max(v[h], dpp_u<0x124>(v[h]));  // row_ror 4
-#pragma unroll
-  for (int h = 0; h < 4; ++h) v[h] = max(v[h], dpp_u<0x122>(v[h]));  // row_ror 2
-#pragma unroll
-  for (int h = 0; h < 4; ++h) v[h] = max(v[h], dpp_u<0x121>(v[h]));  // row_ror 1: each lane holds its row's largest
-#pragma unroll
-  for (int h = 0; h < 4; ++h) {
-    const uint32_t a = (uint32_t)__builtin_amdgcn_readlane((int)v[h], 0);
-    const uint32_t b = (uint32_t)__builtin_amdgcn_readlane((int)v[h], 16);
-    const uint32_t c = (uint32_t)__builtin_amdgcn_readlane((int)v[h], 32);
-    const uint32_t d = (uint32_t)__builtin_amdgcn_readlane((int)v[h], 48);
-    const uint32_t m1 = a > b ? a : b, m2 = c > d ? c : d;
-    v[h] = m1 > m2 ? m1 : m2;
-  }
-}
-
 // ---------------------------------------------------------------- plan
 // Depth and q of channel tid (< 128), read by the kernel before its other
 // preamble work.
@@ -317,7 +284,7 @@ __device__ __forceinline__ CDel cscl_commit(const CScl& r, FilterLds& L, int slo
   uint32_t M[4];
 #pragma unroll
   for (int h = 0; h < 4; ++h) M[h] = __float_as_uint(__fmul_rn(fabsf(qv[h]), am));
-  wave_max4_pos(M);
+  wave_max4_u(M);
   const float Mh = __uint_as_float(hq == 0 ? M[0] : hq == 1 ? M[1] : hq == 2 ? M[2] : M[3]);
   CDel d;
   d.e = 0;
@@ -729,8 +696,9 @@ __device__ __forceinline__ void cwave_run(const CellPlan& P, FilterLds& L, const
 // Sec. 2 asks for the k largest scores; survivors are the keys whose exact
 // score reaches tau, and the result never depends on tau as long as at least
 // k keys survive (else the row is computed exactly).  tau of a row is about
-// the m-th largest of its sampled proxies (the sample pass keeps the 8
-// largest of every sampled quad), m = ceil(1.25 k sampled / eligible) + 16;
+// the m-th largest of its samples (the sample pass keeps the two largest
+// exact scores of every block of a sampled quad), m = ceil(1.25 k sampled /
+// eligible) + 16;
 // when fewer samples exist the smallest one is used if about 1.1 k keys are
 // expected above it, else tau = -inf (no filter).  Wave w of a workgroup
 // finds tau of its unit's row w (w < G) from its lanes' 8 samples each: the
@@ -745,7 +713,7 @@ __device__ __forceinline__ float ctau(const FusedArgs& a, const float (&sv)[kCTa
   int nv = 0;
 #pragma unroll
   for (int x = 0; x < kCTauPer; ++x) {
-    key[x] = sv[x] > kNegInf ? score_key(sv[x]) | 1u : 0u;  // proxies are never NaN; keep 0 free
+    key[x] = sv[x] > kNegInf ? score_key(sv[x]) | 1u : 0u;  // samples are never NaN; keep 0 free
     nv += __popcll(__ballot(key[x] != 0u));
   }
   // eligible keys in the sampled quads (a unit of this pass has fewer than
@@ -786,7 +754,7 @@ __global__ __launch_bounds__(kCThreads, 3) void fused_filter_kernel(FusedArgs a,
   __shared__ FilterLds WL[kCWaves];
   const int u = blockIdx.y, tid = threadIdx.x, wave = cuni(tid >> 6), lane = tid & 63, G = a.G;
   const uint32_t uo = gload(a.ws.uovf + u);
-  // this wave's row's sampled proxies first: tau waits on them
+  // this wave's row's samples first: tau waits on them
   const int nsm = wave < G ? a.ws.s_quads * kSmpW : 0;
   float sv[kCTauPer];
 #pragma unroll

@@ -37,9 +37,9 @@
 // scored exactly (channels ascending, scales kept in an LDS ring) and the keys
 // with score >= tau are appended to their row's survivor list.
 //
-// Passes: (1) sample: proxies of every s-th quad, the 8 largest per (wave,
-// head); (2) per row, tau = the m-th largest sample, m ~ 1.25 k * sampled /
-// eligible + 16; (3) the full pass above; (4) 8 workgroups per row share out
+// Passes: (1) sample: exact scores of every s-th quad, the 2 largest per
+// (block, head); (2) per row, tau = the m-th largest sample, m ~ 1.25 k *
+// sampled / eligible + 16; (3) the full pass above; (4) 8 workgroups per row share out
 // its top k positions by a histogram of the survivors' scores and order their
 // share in LDS; (5) rows with at most 2k + 2048 eligible keys, and rows whose
 // survivors cannot give the top k (fewer than k reached tau, the list
@@ -974,43 +974,144 @@ __device__ __forceinline__ void unit_reset(const FusedArgs& a, int u, int t, int
 }
 
 // ---------------------------------------------------------------- pass 1
-// NSLM = kNarrow when the caller's bound leaves no unit to the wide full pass:
-// a unit the narrow instantiation cannot take gets no samples (its rows are
-// then computed exactly by pass 4, as in the full pass).
-template <bool QF16, int NSLM>
+// Samples for tau: workgroup x of unit u takes sampled quad x (blocks
+// 4 x s_stride .. + 3, one block per wave) and computes the documented exact
+// scores of its keys (Sec. 3.2-3.3: prefix dequantisation, fma over the
+// active channels ascending from +0, as the re-scoring of the full pass);
+// per head, the two largest scores of each block are its samples (-inf where
+// the block has fewer eligible keys).  A wave stages its block's plane words
+// in LDS, one lane per (channel, plane) cell, and every lane then reads them
+// back as broadcasts and takes its own key's bit.  Workgroup 0 of each unit
+// also sets the rows' call state (unit_reset).
+typedef unsigned int v4u __attribute__((ext_vector_type(4)));
+struct alignas(16) SampleLds {
+  uint32_t act[kD];                  // ascending position -> channel | depth << 8 (0 on padding)
+  float q[kD][4];                    // q by ascending position and head (0 past G and on padding)
+  float zo[kD];                      // -(1 - 2^-t): khat = (u / 8 + zo) a16, exact (0 on padding)
+  uint32_t w[kFW][2][kD * kPlanes];  // the block's plane words, dword half h of cell 4 y + p
+  uint16_t sc[kFW][kD];              // the block's scales by ascending position (0 on padding)
+  int cnt[2];                        // active channels of channels 0..63, 64..127
+};
+
 __global__ __launch_bounds__(kFT) void fused_sample_kernel(FusedArgs a) {
-  __shared__ Plan P;
-  __shared__ WaveLdsT<NSLM, kQB, 1, 0> WL[kFW];
-  const int u = blockIdx.y, wave = uni(threadIdx.x >> 6);
-  const PlanPre pre = plan_load<QF16>(a, u);
+  __shared__ SampleLds S;
+  const int u = blockIdx.y, tid = threadIdx.x, lane = tid & 63, wave = uni(tid >> 6), G = a.G;
+  int t = 0;
+  float qv[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+  if (tid < kD) {
+    t = gload(a.depths + (int64_t)u * kD + tid);
+    if (t > kPlanes) t = kPlanes;
+#pragma unroll
+    for (int h = 0; h < 4; ++h)
+      if (h < G) qv[h] = load_q(a.q, a.qdt, ((int64_t)u * G + h) * kD + tid);
+  }
   int64_t nu, lo, hi;
   row_window(a, u, &nu, &lo, &hi, false);
-  if (blockIdx.x == 0) unit_reset(a, u, pre.t, lo, hi);
-  if (hi - lo <= a.ws.cap) return;  // computed directly by pass 4
-  plan_setup(P, a, u, pre);
-  if (!P.ok || P.A == 0) return;
-  if (threadIdx.x < 4) P.tau[threadIdx.x] = 0.0f;
+  if (blockIdx.x == 0) unit_reset(a, u, t, lo, hi);
+  if (hi - lo <= a.ws.cap) return;  // computed directly by the exact pass
+  // the active channels in ascending order
+  const uint64_t on = __ballot(tid < kD && t > 0);
+  if (tid < kD && lane == 0) S.cnt[wave] = __popcll(on);
   __syncthreads();
+  const int A = S.cnt[0] + S.cnt[1];
+  if (tid < kD && t > 0) {
+    const int y = __popcll(on & lanemask_lt(lane)) + (wave == 1 ? S.cnt[0] : 0);
+    S.act[y] = (uint32_t)tid | (uint32_t)t << 8;
+#pragma unroll
+    for (int h = 0; h < 4; ++h) S.q[y][h] = qv[h];
+    S.zo[y] = -(1.0f - ldexpf(1.0f, -t));
+  }
+  const int A4 = (A + 3) & ~3;  // the chain in steps of 4 channels; padding adds +0 to every score
+  if (tid >= A && tid < A4) {
+    S.act[tid] = 0u;
+#pragma unroll
+    for (int h = 0; h < 4; ++h) S.q[tid][h] = 0.0f;
+    S.zo[tid] = 0.0f;
+  }
+  __syncthreads();
+  if (A == 0) return;  // no filter for the unit
   const int64_t nbu = (nu + kBlockTokens - 1) / kBlockTokens;
-  const int64_t sq = (int64_t)blockIdx.x * kFW + wave;
-  if (sq >= a.ws.s_quads) return;
-  const int64_t b0 = sq * a.ws.s_stride * kQB;
-  const bool fits = P.nsl <= NSLM && (NSLM > kNarrow || (P.slrg[kMaxSl] <= kOneRows && a.nb_cap < kOneNbMax));
-  if (!fits || b0 >= nbu || b0 * kBlockTokens >= hi || (b0 + kQB) * kBlockTokens <= lo) {
-    const int lane = threadIdx.x & 63;
-    for (int r = 0; r < a.G; ++r)
-      if (lane < kSmpW) gstore(a.ws.samp + ((int64_t)u * a.G + r) * kSmpRow + sq * kSmpW + lane, kNegInf);
+  const int64_t blk = (int64_t)blockIdx.x * a.ws.s_stride * kQB + wave;
+  const int64_t key = blk * kBlockTokens + lane;
+  const bool el = blk < nbu && key >= lo && key < hi;
+  float* dst = a.ws.samp + (int64_t)u * G * kSmpRow + (int64_t)blockIdx.x * kSmpW + 2 * wave;
+  if (__ballot(el) == 0ull) {  // no eligible key in the block
+    if (lane < 2 * G) gstore(dst + (int64_t)(lane >> 1) * kSmpRow + (lane & 1), kNegInf);
     return;
   }
-  wave_run<QF16, true, NSLM, kQB, 1, 0>(P, WL[wave], a, u, b0, b0 + kQB, nbu, lo, hi, sq);
+  // stage the block's words: cell c = 4 y + p (p < t_y) and the scales
+  const uint64_t* pu = a.planes + (int64_t)u * kD * kPlanes * a.nb_cap;
+  for (int c = lane; c < 4 * A; c += kWave) {
+    const uint32_t e = S.act[c >> 2];
+    if ((c & 3) < (int)(e >> 8)) {
+      const uint64_t v = gload(pu + ((int64_t)(e & 0xFFu) * kPlanes + (c & 3)) * a.nb_cap + blk);
+      S.w[wave][0][c] = (uint32_t)v;
+      S.w[wave][1][c] = (uint32_t)(v >> 32);
+    }
+  }
+  for (int y = lane; y < A4; y += kWave)
+    S.sc[wave][y] = y < A ? gload(a.scales + ((int64_t)u * kD + (S.act[y] & 0xFFu)) * a.nb_cap + blk) : (uint16_t)0;
+  wave_lds_sync();
+  // this lane's key: the documented chain, 4 channels a step (every read of a
+  // step first); a channel's four plane words (of this lane's half) are one
+  // 16-byte read, the planes past its depth masked off its digit
+  const int half = lane >> 5, bit = lane & 31;
+  const uint32_t* wl = &S.w[wave][half][0];
+  float sh[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+  for (int y0 = 0; y0 < A4; y0 += 4) {
+    const v4u ev = *reinterpret_cast<const v4u*>(&S.act[y0]);
+    const float4 zv = *reinterpret_cast<const float4*>(&S.zo[y0]);
+    const uint2 sv = *reinterpret_cast<const uint2*>(&S.sc[wave][y0]);
+    v4u wv[4];
+    float4 q4[4];
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      wv[c] = *reinterpret_cast<const v4u*>(&wl[4 * (y0 + c)]);
+      q4[c] = *reinterpret_cast<const float4*>(&S.q[y0 + c][0]);
+    }
+    const uint32_t es[4] = {ev.x, ev.y, ev.z, ev.w};
+    const float zs[4] = {zv.x, zv.y, zv.z, zv.w};
+    const uint32_t hs[4] = {sv.x & 0xFFFFu, sv.x >> 16, sv.y & 0xFFFFu, sv.y >> 16};
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const uint32_t d = ((wv[c].x >> bit) & 1u) << 3 | ((wv[c].y >> bit) & 1u) << 2 | ((wv[c].z >> bit) & 1u) << 1 |
+                         ((wv[c].w >> bit) & 1u);
+      const uint32_t dg = d & ((0xF0u >> (es[c] >> 8)) & 0xFu);  // planes p < t
+      const float x8 = __fmaf_rn((float)dg, 0.125f, zs[c]);
+      const float khat = __fmaf_rn(x8, half_bits_to_float((uint16_t)hs[c]), 0.0f);
+      sh[0] = __fmaf_rn(q4[c].x, khat, sh[0]);
+      sh[1] = __fmaf_rn(q4[c].y, khat, sh[1]);
+      sh[2] = __fmaf_rn(q4[c].z, khat, sh[2]);
+      sh[3] = __fmaf_rn(q4[c].w, khat, sh[3]);
+    }
+  }
+  // per head the two largest order-preserving keys (0: none)
+  uint32_t k1[4], k2[4];
+#pragma unroll
+  for (int h = 0; h < 4; ++h) k1[h] = el ? score_key(sh[h]) : 0u;
+  uint32_t m1[4] = {k1[0], k1[1], k1[2], k1[3]};
+  wave_max4_u(m1);
+#pragma unroll
+  for (int h = 0; h < 4; ++h) {
+    const uint64_t at = __ballot(k1[h] == m1[h]);
+    k2[h] = lane == (int)__builtin_ctzll(at) ? 0u : k1[h];  // the first lane holding the largest drops out
+  }
+  wave_max4_u(k2);
+  if (lane < 2 * G) {
+    const int h = lane >> 1;
+    const uint32_t k = (lane & 1) ? (h == 0 ? k2[0] : h == 1 ? k2[1] : h == 2 ? k2[2] : k2[3])
+                                  : (h == 0 ? m1[0] : h == 1 ? m1[1] : h == 2 ? m1[2] : m1[3]);
+    const float v = k == 0u ? kNegInf : __uint_as_float((k & 0x80000000u) ? (k & 0x7FFFFFFFu) : ~k);
+    gstore(dst + (int64_t)h * kSmpRow + (lane & 1), v);
+  }
 }
 
 // ---------------------------------------------------------------- pass 2
 // One workgroup of two waves per row (one thread per channel for the depth
-// count).  Zeroes the row's survivor count; tau = the m-th largest sampled
-// proxy, found by wave 0 with a bitwise search over order-preserving keys and
-// ballot counts.  Leaves the unit's slice count (0: no filter) in uovf[u] for
-// pass 3.
+// count), launched for the wide full pass or G > 4 (the cell filter finds tau
+// itself).  Sets the row's call state as unit_reset does; tau = the m-th
+// largest sample, found by wave 0 with a bitwise search over order-preserving
+// keys and ballot counts.  Leaves the unit's class in uovf[u] for pass 3.
 constexpr int kTauThreads = kD;
 constexpr int kTauPer = kSmpRow / kWave;  // sampled values per lane of wave 0
 __global__ __launch_bounds__(kTauThreads) void fused_tau_kernel(FusedArgs a) {
@@ -1052,7 +1153,7 @@ __global__ __launch_bounds__(kTauThreads) void fused_tau_kernel(FusedArgs a) {
   int nv = 0;
 #pragma unroll
   for (int x = 0; x < kTauPer; ++x) {
-    key[x] = sv[x] > kNegInf ? score_key(sv[x]) | 1u : 0u;  // proxies are never NaN; keep 0 free
+    key[x] = sv[x] > kNegInf ? score_key(sv[x]) | 1u : 0u;  // samples are never NaN; keep 0 free
     nv += __popcll(__ballot(key[x] != 0u));
   }
   int64_t m_s = 0;  // eligible keys in the sampled quads
@@ -1812,16 +1913,8 @@ fathom_status launch_scan_topk_fused(const uint64_t* planes, const uint16_t* sca
   // wide launches are skipped.  (A unit above the caller's bound is left to the
   // exact path of pass 4.)
   const bool wide = !(max_unit_bits > 0 && max_unit_bits <= 16 * kNarrow && nb_cap < kOneNbMax);
-  if (G <= 4) {
-    dim3 gs((unsigned)((fa.ws.s_quads + kFW - 1) / kFW), (unsigned)U);
-    if (f16) {
-      if (wide) hipLaunchKernelGGL((fused_sample_kernel<true, kMaxSl>), gs, dim3(kFT), 0, s, fa);
-      else hipLaunchKernelGGL((fused_sample_kernel<true, kNarrow>), gs, dim3(kFT), 0, s, fa);
-    } else {
-      if (wide) hipLaunchKernelGGL((fused_sample_kernel<false, kMaxSl>), gs, dim3(kFT), 0, s, fa);
-      else hipLaunchKernelGGL((fused_sample_kernel<false, kNarrow>), gs, dim3(kFT), 0, s, fa);
-    }
-  }
+  if (G <= 4)
+    hipLaunchKernelGGL(fused_sample_kernel, dim3((unsigned)fa.ws.s_quads, (unsigned)U), dim3(kFT), 0, s, fa);
   // narrow: the cell filter finds tau itself and the sample pass sets the
   // rows' state, so the tau pass runs only for the wide pass or G > 4
   if (wide || G > 4) hipLaunchKernelGGL(fused_tau_kernel, dim3(R), dim3(kTauThreads), 0, s, fa);

@@ -182,6 +182,39 @@ __device__ __forceinline__ void row_window(const FusedArgs& a, int u, int64_t* n
   if (*hi < *lo) *hi = *lo;
 }
 
+// Lane moves within rows of 16 (rotations and quad permutes: every lane has a
+// source, so the bound control only lets the move fuse into its user).
+template <int CTRL>
+__device__ __forceinline__ uint32_t dpp_u(uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, CTRL, 0xF, 0xF, true);
+}
+template <int CTRL>
+__device__ __forceinline__ int dpp_i(int v) {
+  return __builtin_amdgcn_update_dpp(0, v, CTRL, 0xF, 0xF, true);
+}
+// Largest of four unsigned values over the wave (non-negative floats may be
+// given as their bits, which order as the values), the four reductions
+// interleaved step by step; uniform results.
+__device__ __forceinline__ void wave_max4_u(uint32_t (&v)[4]) {
+#pragma unroll
+  for (int h = 0; h < 4; ++h) v[h] = max(v[h], dpp_u<0x128>(v[h]));  // row_ror 8
+#pragma unroll
+  for (int h = 0; h < 4; ++h) v[h] = max(v[h], dpp_u<0x124>(v[h]));  // row_ror 4
+#pragma unroll
+  for (int h = 0; h < 4; ++h) v[h] = max(v[h], dpp_u<0x122>(v[h]));  // row_ror 2
+#pragma unroll
+  for (int h = 0; h < 4; ++h) v[h] = max(v[h], dpp_u<0x121>(v[h]));  // row_ror 1: each lane holds its row's largest
+#pragma unroll
+  for (int h = 0; h < 4; ++h) {
+    const uint32_t a = (uint32_t)__builtin_amdgcn_readlane((int)v[h], 0);
+    const uint32_t b = (uint32_t)__builtin_amdgcn_readlane((int)v[h], 16);
+    const uint32_t c = (uint32_t)__builtin_amdgcn_readlane((int)v[h], 32);
+    const uint32_t d = (uint32_t)__builtin_amdgcn_readlane((int)v[h], 48);
+    const uint32_t m1 = a > b ? a : b, m2 = c > d ? c : d;
+    v[h] = m1 > m2 ? m1 : m2;
+  }
+}
+
 // The full pass over the units of class 1 (filter.hip).
 void launch_filter(const FusedArgs& fa, int U, hipStream_t s);
 
