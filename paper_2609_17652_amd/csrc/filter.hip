@@ -228,21 +228,22 @@ __device__ __forceinline__ void cell_plan(CellPlan& P, const FusedArgs& a, const
 // (nb_cap a multiple of 8) one 16-byte load per lane; blocks past nb_cap then
 // read the next row's scales, which only the (ineligible) keys of those
 // blocks and delta see.  Otherwise 8 two-byte loads, each past the range
-// beyond nb_cap.
+// beyond nb_cap.  An invalid load (no group of the wave there) reads past the
+// range: it is issued, so wait counts stay exact, but fetches nothing.
 struct CScl {
   uint32_t v[kCSB / 2];
 };
 typedef unsigned short u16x1;
 
 template <bool VEC>
-__device__ __forceinline__ void cscl_issue(CScl& r, const FusedArgs& a, int u, int A, int jrow, int sb0) {
+__device__ __forceinline__ void cscl_issue(CScl& r, const FusedArgs& a, int u, int A, int jrow, int sb0, bool valid) {
   const int lane = threadIdx.x & 63;
   const uint64_t base = reinterpret_cast<uint64_t>(a.scales + (int64_t)u * kD * a.nb_cap);
   const uint32_t alo = (uint32_t)cuni((int)(uint32_t)base), ahi = (uint32_t)cuni((int)(uint32_t)(base >> 32));
   const uint32_t bytes = (uint32_t)(kD * 2) * (uint32_t)a.nb_cap;
   const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
       reinterpret_cast<void*>(((uint64_t)ahi << 32) | alo), (short)0, (int)bytes, kRawBufferFlags);
-  const uint32_t off = lane < A ? ((uint32_t)jrow * (uint32_t)a.nb_cap + (uint32_t)sb0) * 2u : kPastRange;
+  const uint32_t off = lane < A && valid ? ((uint32_t)jrow * (uint32_t)a.nb_cap + (uint32_t)sb0) * 2u : kPastRange;
   if constexpr (VEC) {
     const v4u x0 = __builtin_amdgcn_raw_buffer_load_b128(rs, (int)off, 0, 0);
     r.v[0] = x0.x; r.v[1] = x0.y; r.v[2] = x0.z; r.v[3] = x0.w;
@@ -251,7 +252,7 @@ __device__ __forceinline__ void cscl_issue(CScl& r, const FusedArgs& a, int u, i
     uint32_t h[kCSB];
 #pragma unroll
     for (int b = 0; b < kCSB; ++b)
-      h[b] = __builtin_amdgcn_raw_buffer_load_b16(rs, (int)(b < left ? off + 2u * b : kPastRange), 0, 0);
+      h[b] = __builtin_amdgcn_raw_buffer_load_b16(rs, (int)(b < left && valid ? off + 2u * b : kPastRange), 0, 0);
 #pragma unroll
     for (int i = 0; i < kCSB / 2; ++i) r.v[i] = (h[2 * i] & 0xFFFFu) | (h[2 * i + 1] << 16);
   }
@@ -307,13 +308,15 @@ __device__ __forceinline__ CDel cscl_commit(const CScl& r, FilterLds& L, int slo
 struct CStage {
   __amdgpu_buffer_rsrc_t rs;  // the unit's planes (ub bytes)
   uint32_t boff[4];           // byte offset of cell k's word for block bq of a quad starting at block 0
+  uint32_t ub;                // an offset past the range
 };
 struct CRaw {
   uint64_t w[4];  // cell k's word of block bq
 };
 
-// Pad cells get the offset ub: with the quad's offset (at most 8 nb_cap bytes)
-// added it stays past the range without wrapping (ub + 8 nb_cap < 2^32).
+// Pad cells get the offset ub: with the quad's offset (at most 8 (nb_cap +
+// 40) bytes) added it stays past the range without wrapping (4104 nb_cap +
+// 320 < 2^32 for nb_cap < kOneNbMax).
 __device__ __forceinline__ void cstage_setup(CStage& S, const CellPlan& P, const FusedArgs& a, uint64_t ubase,
                                              uint32_t ub) {
   const int lane = threadIdx.x & 63, g = lane >> 2, bq = lane & 3;
@@ -326,16 +329,19 @@ __device__ __forceinline__ void cstage_setup(CStage& S, const CellPlan& P, const
 #pragma unroll
   for (int k = 0; k < 4; ++k)
     S.boff[k] = on && rows[k] != kCPad ? (rows[k] * (uint32_t)a.nb_cap + (uint32_t)bq) * 8u : ub;
+  S.ub = ub;
 }
 
-// Loads of the quad whose first block is qb0 (issued for every quad the loop
-// could reach, so that the compiler's wait counts stay exact; a quad past the
-// unit's blocks reads other rows' words or zeros and is never used).
-__device__ __forceinline__ void cstage_issue(CRaw& R, const CStage& S, int qb0) {
+// Loads of the quad whose first block is qb0, issued for every quad the loop
+// could reach so that the compiler's wait counts stay exact: an invalid quad
+// (no group of the wave there) reads past the range and fetches nothing; a
+// valid quad past the unit's blocks reads other rows' words or zeros, which
+// no eligible key uses.
+__device__ __forceinline__ void cstage_issue(CRaw& R, const CStage& S, int qb0, bool valid) {
   const int so = cuni((int)((uint32_t)qb0 * 8u));
 #pragma unroll
   for (int k = 0; k < 4; ++k) {
-    const v2u32 v = __builtin_amdgcn_raw_buffer_load_b64(S.rs, (int)S.boff[k], so, 0);
+    const v2u32 v = __builtin_amdgcn_raw_buffer_load_b64(S.rs, (int)(valid ? S.boff[k] : S.ub), so, 0);
     R.w[k] = ((uint64_t)v.y << 32) | v.x;
   }
 }
@@ -505,20 +511,23 @@ __device__ __forceinline__ void crescore(const CellPlan& P, FilterLds& L, const 
 }
 
 // ---------------------------------------------------------------- one wave
-// Blocks [b0, b1) of unit u (b0 a multiple of 4, b1 = b0 for a wave with no
-// blocks), quad by quad in groups of 8 blocks from b0 (one loop iteration
-// each).  `ready` runs once every first load is issued (every wave of the
-// workgroup calls it, so it may hold a barrier); the wave stops if it
-// returns false.  The plane words of a quad are
-// loaded two quads ahead (two register sets), the scales of a group one group
-// ahead, in the same order on every path into the loop so that the
-// compiler's load counters stay exact.  A wave's LDS accesses execute in
+// Groups of 8 blocks of unit u: the ng groups b0 / 8 + kCWaves i (i < ng;
+// the workgroup's waves take its groups in turn, so two waves read the two
+// halves of a 128-byte plane line at about the same time), quad by quad (one
+// loop iteration per group).  `ready` runs once every first load is issued
+// (every wave of the workgroup calls it, so it may hold a barrier); the wave
+// stops if it returns false.  The plane words of a quad are loaded two quads
+// ahead (two register sets), the scales of a group one group ahead, in the
+// same order on every path into the loop so that the compiler's load
+// counters stay exact.  A wave's LDS accesses execute in
 // program order, so staged data is read back without a wait.  Re-scoring
 // runs at one place: after a quad's candidates, when the queue holds kCFlush,
 // when a quad's candidates do not fit, before the ring slot of the oldest
 // queued key is reused, and at the end.
+constexpr int kCStride = kCWaves * kCSB;  // blocks from one group of a wave to its next
+
 template <bool VEC, class Ready>
-__device__ __forceinline__ void cwave_run(const CellPlan& P, FilterLds& L, const FusedArgs& a, int u, int b0, int b1,
+__device__ __forceinline__ void cwave_run(const CellPlan& P, FilterLds& L, const FusedArgs& a, int u, int b0, int ng,
                                           int nbu, int lo, int hi, Ready&& ready) {
   const int lane = threadIdx.x & 63;
   const int bq = lane >> 4, nib = (lane >> 3) & 1, oct = lane & 7;
@@ -558,21 +567,20 @@ __device__ __forceinline__ void cwave_run(const CellPlan& P, FilterLds& L, const
   // the issue order here (scales, quad 0, quad 1) is the loop's steady-state
   // order, so the compiler's load counters agree on every path into the loop
   CScl sr;
-  cscl_issue<VEC>(sr, a, u, A, srow, b0);
+  cscl_issue<VEC>(sr, a, u, A, srow, b0, ng > 0);
   sched_fence();
   CRaw R0, R1;
-  cstage_issue(R0, S, b0);
+  cstage_issue(R0, S, b0, ng > 0);
   sched_fence();
-  cstage_issue(R1, S, b0 + kQB);
+  cstage_issue(R1, S, b0 + kQB, ng > 0);
   sched_fence();
   if (!ready()) return;
   CHead H;
   int slot = 0;
-  auto quad = [&](CRaw& R, int qb0, int it) {
-    const int sbq = qb0 - b0 - kCSB * it;  // first block of the quad within its group
+  auto quad = [&](CRaw& R, int qb0, int it, int sbq) {  // sbq: first block of the quad within its group
     cstage_write(R, L);
     sched_fence();
-    cstage_issue(R, S, qb0 + 2 * kQB);
+    cstage_issue(R, S, qb0 + kCStride, it + 1 < ng);  // the same quad of the wave's next group
     sched_fence();
     cquad_weights(P, L, H, slot, sbq, wi);
     lds_order();
@@ -604,12 +612,11 @@ __device__ __forceinline__ void cwave_run(const CellPlan& P, FilterLds& L, const
     // at the unit's edges), and per key its candidate heads
     const int blk = qb0 + bq;
     const int kbase = blk * kBlockTokens + kb;
-    const bool live = qb0 < b1;
-    const bool inner = live && qb0 * kBlockTokens >= lo && (qb0 + 4) * kBlockTokens <= hi && qb0 + 4 <= nbu;
+    const bool inner = qb0 * kBlockTokens >= lo && (qb0 + 4) * kBlockTokens <= hi && qb0 + 4 <= nbu;
     uint32_t em = 0xFu;
     if (!inner) {
       const int e0 = min(max(lo - kbase, 0), 4), e1 = min(max(hi - kbase, 0), 4);
-      em = live && blk < nbu ? (0xFu << e0) & ~(0xFu << e1) & 0xFu : 0u;
+      em = blk < nbu ? (0xFu << e0) & ~(0xFu << e1) & 0xFu : 0u;
     }
     // byte h of D: bit mu set iff key mu is a candidate for head h (the sign
     // bytes of the four heads' accumulators side by side, flipped at pos 7)
@@ -622,7 +629,7 @@ __device__ __forceinline__ void cwave_run(const CellPlan& P, FilterLds& L, const
     }
     D &= em * 0x01010101u;
     uint32_t kmask = (D | D >> 8 | D >> 16 | D >> 24) & 0xFu;
-    const bool last = qb0 + kQB >= b1;  // the wave's last quad (or one past it)
+    const bool last = it == ng - 1 && sbq == kCSB - kQB;  // the wave's last quad
     const bool endg = sbq == kCSB - kQB;
     if (__ballot(kmask != 0u) != 0ull && pending == 0) oldest = it;
     const uint32_t meta = (uint32_t)slot << 3 | (uint32_t)(sbq + bq) << 8;
@@ -660,12 +667,12 @@ __device__ __forceinline__ void cwave_run(const CellPlan& P, FilterLds& L, const
   // one loop iteration = one group of 8 blocks (two quads): its scales and
   // delta, then the quads
   int it = 0;
-  for (int gb0 = b0; gb0 < b1; gb0 += kCSB, ++it) {
+  for (int gb0 = b0; it < ng; gb0 += kCStride, ++it) {
     slot = it & (kCSlots - 1);
     {
       const CDel dl = cscl_commit(sr, L, slot, hq, qv);
       sched_fence();
-      cscl_issue<VEC>(sr, a, u, A, srow, gb0 + kCSB);  // past the range: harmless, never used
+      cscl_issue<VEC>(sr, a, u, A, srow, gb0 + kCStride, it + 1 < ng);
       sched_fence();
       const float th = P.tau[hq];
       const float M0 = ldexpf(12582912.0f, dl.e);  // 1.5 * 2^(23 + e)
@@ -685,8 +692,8 @@ __device__ __forceinline__ void cwave_run(const CellPlan& P, FilterLds& L, const
       H.c0 = none ? kNoBound : -kNoBound;
       H.c1 = top ? -H.c0 : H.c0;
     }
-    quad(R0, gb0, it);
-    quad(R1, gb0 + kQB, it);  // past b1 (an odd quad count): staged but no candidates
+    quad(R0, gb0, it, 0);
+    quad(R1, gb0 + kQB, it, kQB);
   }
 #pragma unroll
   for (int h = 0; h < 4; ++h) cflush_head(L, a, u, h, svn[h]);
@@ -745,11 +752,12 @@ __device__ __forceinline__ float ctau(const FusedArgs& a, const float (&sv)[kCTa
 }
 
 // ---------------------------------------------------------------- kernel
-// Grid (workgroups per unit, U); wave w of workgroup x takes quads
-// [(x kCWaves + w) qpw, + qpw) of its unit.  Units that pass 2 left to another
-// full pass (uovf[u] >> 1 != 1) or to the exact path return at once.
+// Grid (workgroups per unit, U); workgroup x takes the 8-block groups
+// [x kCWaves gpw, (x + 1) kCWaves gpw) of its unit, wave w every kCWaves-th of
+// them from the w-th.  Units of another class (uovf[u] >> 1 != 1: the wide
+// pass, or no filter) and rows computed exactly return at once.
 template <bool VEC>
-__global__ __launch_bounds__(kCThreads, 3) void fused_filter_kernel(FusedArgs a, int qpw) {
+__global__ __launch_bounds__(kCThreads, 3) void fused_filter_kernel(FusedArgs a, int gpw) {
   __shared__ CellPlan P;
   __shared__ FilterLds WL[kCWaves];
   const int u = blockIdx.y, tid = threadIdx.x, wave = cuni(tid >> 6), lane = tid & 63, G = a.G;
@@ -768,16 +776,18 @@ __global__ __launch_bounds__(kCThreads, 3) void fused_filter_kernel(FusedArgs a,
   if ((uo >> 1) != 1u) return;
   if (hi - lo <= a.ws.cap) return;
   const int64_t nbu = (nu + kBlockTokens - 1) / kBlockTokens;
-  const int64_t gw = (int64_t)blockIdx.x * kCWaves;
-  const int64_t qlo = lo / (kQB * kBlockTokens);
-  const int64_t qhi = (hi + kQB * kBlockTokens - 1) / (kQB * kBlockTokens);
-  if (gw * qpw >= qhi || (gw + kCWaves) * qpw <= qlo) return;
+  // the workgroup's groups [g0, g1) and the window's [glo, ghi)
+  const int64_t g0 = (int64_t)blockIdx.x * kCWaves * gpw, g1 = g0 + kCWaves * gpw;
+  const int64_t glo = lo / (kCSB * kBlockTokens);
+  const int64_t ghi = (hi + kCSB * kBlockTokens - 1) / (kCSB * kBlockTokens);
+  if (g0 >= ghi || g1 <= glo) return;
   cell_plan(P, a, pre);
   if (!P.ok) return;
-  int64_t q0 = (gw + wave) * qpw, q1 = q0 + qpw;
-  if (q0 < qlo) q0 = qlo;
-  if (q1 > qhi) q1 = qhi;
-  const int64_t b1 = q0 >= q1 ? q0 * kQB : q1 * kQB < nbu ? q1 * kQB : nbu;
+  // this wave: groups g0 + wave + kCWaves i inside the window (ng = 0: none)
+  int64_t gf = g0 + wave;
+  if (gf < glo) gf += (glo - gf + kCWaves - 1) / kCWaves * kCWaves;
+  const int64_t gend = ghi < g1 ? ghi : g1;
+  const int ng = gf < gend ? (int)((gend - gf + kCWaves - 1) / kCWaves) : 0;
   // tau while the first loads are in flight: every workgroup finds the same
   // values; the one holding the window's first quad leaves them for the rank
   // pass
@@ -786,7 +796,7 @@ __global__ __launch_bounds__(kCThreads, 3) void fused_filter_kernel(FusedArgs a,
       const float tv = ctau(a, sv, lo, hi);
       if (lane == 0) {
         P.tau[wave] = tv;
-        if (gw * qpw <= qlo) gstore(a.ws.tau + u * G + wave, tv);
+        if (g0 <= glo) gstore(a.ws.tau + u * G + wave, tv);
       }
     }
     __syncthreads();
@@ -794,24 +804,22 @@ __global__ __launch_bounds__(kCThreads, 3) void fused_filter_kernel(FusedArgs a,
     for (int h = 0; h < G; ++h) any |= P.tau[h] != kNegInf;
     return any;
   };
-  cwave_run<VEC>(P, WL[wave], a, u, (int)(q0 * kQB), (int)b1, (int)nbu, (int)lo, (int)hi, ready);
+  cwave_run<VEC>(P, WL[wave], a, u, (int)(gf * kCSB), ng, (int)nbu, (int)lo, (int)hi, ready);
 }
 
-// Quads per wave: an even count (whole loop iterations), about kFResident
-// waves over all units (three per SIMD of the chip, one round).
+// Groups per wave: about kFResident waves over all units (three per SIMD of
+// the chip, one round); a workgroup takes kCWaves * gpw consecutive groups.
 constexpr int64_t kFResident = 3 * 4 * 256;
 void launch_filter(const FusedArgs& fa, int U, hipStream_t s) {
-  const int64_t nq = (fa.nb_cap + kQB - 1) / kQB;
-  int64_t qpw = ((int64_t)U * nq + kFResident - 1) / kFResident;
-  qpw = (qpw + 1) & ~(int64_t)1;  // whole groups of two quads
-  if (qpw < 2) qpw = 2;
-  const int64_t waves = (nq + qpw - 1) / qpw;
-  const unsigned wgs = (unsigned)((waves + kCWaves - 1) / kCWaves);
+  const int64_t ngr = (fa.nb_cap + kCSB - 1) / kCSB;
+  int64_t gpw = ((int64_t)U * ngr + kFResident - 1) / kFResident;
+  if (gpw < 1) gpw = 1;
+  const unsigned wgs = (unsigned)((ngr + kCWaves * gpw - 1) / (kCWaves * gpw));
   // 16-byte aligned scale rows: one 16-byte scale load per lane and group
   if ((fa.nb_cap & 7) == 0 && (reinterpret_cast<uintptr_t>(fa.scales) & 15) == 0)
-    hipLaunchKernelGGL(fused_filter_kernel<true>, dim3(wgs, (unsigned)U), dim3(kCThreads), 0, s, fa, (int)qpw);
+    hipLaunchKernelGGL(fused_filter_kernel<true>, dim3(wgs, (unsigned)U), dim3(kCThreads), 0, s, fa, (int)gpw);
   else
-    hipLaunchKernelGGL(fused_filter_kernel<false>, dim3(wgs, (unsigned)U), dim3(kCThreads), 0, s, fa, (int)qpw);
+    hipLaunchKernelGGL(fused_filter_kernel<false>, dim3(wgs, (unsigned)U), dim3(kCThreads), 0, s, fa, (int)gpw);
 }
 
 }  // namespace fathom
