@@ -88,7 +88,6 @@ struct alignas(16) Plan {
   int rgp[kMaxRg];             // row group g: plane p
   int rgslot[kMaxRg];          // row group g: staging slot 4 * (d mod 4) + p within its slice
   int slmask[kMaxSl];          // slice s: bit 4 dd + p set iff dword 4s + dd has plane p
-  int slshp[kMaxSl];           // slice s: bits 4p..4p+3 = c_p, the dwords with plane p (a prefix dd < c_p)
   float tau[4];
 };
 
@@ -228,13 +227,9 @@ __device__ void plan_setup(Plan& P, const FusedArgs& a, int u, const PlanPre& pr
     for (int sl = 0; sl < kMaxSl; ++sl) {
       P.slrg[sl] = g;
       srows[sl] = g;
-      int shp = 0, msk = 0;
-      for (int p = 0; p < kPlanes; ++p) {
-        shp |= scp[sl][p] << (4 * p);
-        g += scp[sl][p];
-      }
+      int msk = 0;
+      for (int p = 0; p < kPlanes; ++p) g += scp[sl][p];
       for (int dd = 0; dd < 4; ++dd) msk |= ((1 << snr[4 * sl + dd]) - 1) << (4 * dd);
-      P.slshp[sl] = shp;
       P.slmask[sl] = msk;
     }
     P.slrg[kMaxSl] = g;
@@ -267,22 +262,17 @@ __device__ void plan_setup(Plan& P, const FusedArgs& a, int u, const PlanPre& pr
 
 // ---------------------------------------------------------------- per-wave state
 // NSLM slices (16 NSLM proxy channels at most), superquads of SQB blocks, RQ
-// superquads of scales kept for re-scoring, QCAP queued candidates (0: the
-// sample pass, no queue).
-// Staged rows: one slice's 16 slots, or (narrow pass) every row group of the
-// unit plus 3 rows that plane segments may read past the last one.
-constexpr int st_rows(int nslm) { return nslm <= kNarrow ? kOneRows + 3 : 16; }
+// superquads of scales kept for re-scoring, QCAP queued candidates.
 template <int NSLM, int SQB, int RQ, int QCAP>
 struct alignas(16) WaveLdsT {
-  uint32_t st[st_rows(NSLM)][kStP];          // staged row groups (per-slice slot 4 (d mod 4) + p, or row group g)
+  uint32_t st[16][kStP];                     // one slice's staged row groups (slot 4 (d mod 4) + p)
   uint32_t W[SQB * 4 * 4 * NSLM];            // int8 weights [block][head][dword < 4 nsl] of the superquad
-  int32_t ci[SQB][4][4];                     // [block][mu][head] accumulator start; sample: [b][0][h] bias, [b][1][h] ok
+  int32_t ci[SQB][4][4];                     // [block][mu][head] accumulator start
   uint16_t scl[RQ * SQB * (16 * NSLM + 2)];  // fp16 scales [ring slot][block][proxy channel], rows of 4 ndw + 2
   float amx[16 * NSLM];                      // per proxy channel: largest scale of the superquad
-  uint32_t qd[QCAP > 0 ? QCAP * 4 * NSLM : 4];  // queued digit dwords, 4 nsl per entry
-  uint32_t qi[QCAP > 0 ? QCAP : 1];          // queued key index
-  uint32_t qf[QCAP > 0 ? QCAP : 1];          // queued mu | heads << 2 | ring slot << 8 | block << 12
-  float sdel[4];                             // sample pass: delta per head
+  uint32_t qd[QCAP * 4 * NSLM];              // queued digit dwords, 4 nsl per entry
+  uint32_t qi[QCAP];                         // queued key index
+  uint32_t qf[QCAP];                         // queued mu | heads << 2 | ring slot << 8 | block << 12
 };
 
 typedef __attribute__((ext_vector_type(4))) int v4i;
@@ -385,7 +375,7 @@ __device__ SqInfo scl_commit(const SclRegs<NCH, SQB>& r, const Plan& P, WL& W, i
 
 // Weights and accumulator starts of the superquad.  Lane (block beta = lane &
 // 15, head h = lane >> 4).
-template <bool QF16, bool SAMPLE, int SQB, class WL>
+template <bool QF16, int SQB, class WL>
 __device__ void superquad_weights(const Plan& P, WL& W, const FusedArgs& a, const SqInfo& si, int slot) {
   const int lane = threadIdx.x & 63, beta = lane & 15, h = lane >> 4;
   const int ndw = uni(P.ndw), aps = 4 * ndw + 2, ws = 4 * uni(P.nsl);
@@ -425,32 +415,26 @@ __device__ void superquad_weights(const Plan& P, WL& W, const FusedArgs& a, cons
     }
     for (int d = ndw; d < ws; ++d) wdst[d] = 0u;
     const bool hv = h < a.G && P.tau[h] != kNegInf;
-    if (SAMPLE) {
-      W.ci[beta][0][h] = bias;
-      W.ci[beta][1][h] = (h < a.G && si.valid) ? 1 : 0;
-      if (beta == 0) W.sdel[h] = ldexpf(1.0f, si.e);
+    int c0[4];
+    if (!hv) {
+#pragma unroll
+      for (int mu = 0; mu < 4; ++mu) c0[mu] = -kNoBound;
+    } else if (!si.valid) {
+#pragma unroll
+      for (int mu = 0; mu < 4; ++mu) c0[mu] = kNoBound;
     } else {
-      int c0[4];
-      if (!hv) {
+      const double del = ldexp(1.0, si.e);
+      const double E = del * P.Ku + P.Eabs;
+      double X = ((double)P.tau[h] - E) * 16.0 / del;
+      X = floor(X) - 1.0;
+      X = X < -2.0 * kThrMax ? -2.0 * kThrMax : X > 2.0 * kThrMax ? 2.0 * kThrMax : X;
+      int thr = ((int)X + bias) >> 1;
+      thr = thr < -kThrMax ? -kThrMax : thr > kThrMax ? kThrMax : thr;
 #pragma unroll
-        for (int mu = 0; mu < 4; ++mu) c0[mu] = -kNoBound;
-      } else if (!si.valid) {
-#pragma unroll
-        for (int mu = 0; mu < 4; ++mu) c0[mu] = kNoBound;
-      } else {
-        const double del = ldexp(1.0, si.e);
-        const double E = del * P.Ku + P.Eabs;
-        double X = ((double)P.tau[h] - E) * 16.0 / del;
-        X = floor(X) - 1.0;
-        X = X < -2.0 * kThrMax ? -2.0 * kThrMax : X > 2.0 * kThrMax ? 2.0 * kThrMax : X;
-        int thr = ((int)X + bias) >> 1;
-        thr = thr < -kThrMax ? -kThrMax : thr > kThrMax ? kThrMax : thr;
-#pragma unroll
-        for (int mu = 0; mu < 4; ++mu) c0[mu] = -(thr * (1 << mu));
-      }
-#pragma unroll
-      for (int mu = 0; mu < 4; ++mu) W.ci[beta][mu][h] = c0[mu];
+      for (int mu = 0; mu < 4; ++mu) c0[mu] = -(thr * (1 << mu));
     }
+#pragma unroll
+    for (int mu = 0; mu < 4; ++mu) W.ci[beta][mu][h] = c0[mu];
   }
   wave_lds_sync();
 }
@@ -506,119 +490,6 @@ __device__ __forceinline__ void task_stage(const uint64_t (&w)[4], const Plan& P
       }
     }
   }
-}
-
-// Narrow full pass: every row group of the unit is staged in one pass, lane =
-// (row group g = lane >> 2, block beta = lane & 3).  The per-lane constants
-// are fixed for the whole unit.
-struct StageLane {
-  uint32_t boff[4];   // byte offset of row K for block beta from the quad's first plane word (pad rows: row 0)
-  uint32_t sel[4];    // first transpose stage (rows 0-1 lo/hi, rows 2-3 lo/hi); pad rows select zero bytes
-  uint32_t shl, shr;  // nibble shifts 3 - p and 1 + p
-  uint32_t* dst;      // &W.st[g][16 beta]
-  bool on;            // the lane's row group exists
-};
-
-template <class WL>
-__device__ __forceinline__ void stage_lane_setup(StageLane& L, const Plan& P, WL& W, const FusedArgs& a) {
-  const int lane = threadIdx.x & 63, g = lane >> 2, beta = lane & 3;
-  L.on = g < uni(P.slrg[kMaxSl]);
-  const int gg = L.on ? g : 0;
-  const uint32_t rr0 = P.rgrow[gg][0], rr1 = P.rgrow[gg][1];
-  const uint32_t rows[4] = {rr0 & 0xFFFFu, rr0 >> 16, rr1 & 0xFFFFu, rr1 >> 16};
-  // row 0 of a row group always exists (the dword's first channel is its deepest)
-#pragma unroll
-  for (int K = 0; K < 4; ++K) {
-    const uint32_t rk = rows[K] == kPadRow ? rows[0] : rows[K];
-    L.boff[K] = (rk * (uint32_t)a.nb_cap + (uint32_t)beta) * 8u;
-  }
-  // v_perm bytes: 0-3 from the second operand (rows 0, 2), 4-7 from the first
-  // (rows 1, 3); selector 0x0c yields a zero byte
-  uint32_t s01l = 0x05010400u, s01h = 0x07030602u, s23l = 0x05010400u, s23h = 0x07030602u;
-  if (rows[1] == kPadRow) {
-    s01l = (s01l & 0x00FF00FFu) | 0x0C000C00u;
-    s01h = (s01h & 0x00FF00FFu) | 0x0C000C00u;
-  }
-  if (rows[2] == kPadRow) {
-    s23l = (s23l & 0xFF00FF00u) | 0x000C000Cu;
-    s23h = (s23h & 0xFF00FF00u) | 0x000C000Cu;
-  }
-  if (rows[3] == kPadRow) {
-    s23l = (s23l & 0x00FF00FFu) | 0x0C000C00u;
-    s23h = (s23h & 0x00FF00FFu) | 0x0C000C00u;
-  }
-  L.sel[0] = s01l;
-  L.sel[1] = s01h;
-  L.sel[2] = s23l;
-  L.sel[3] = s23h;
-  const int p = P.rgp[gg];
-  L.shl = (uint32_t)(3 - p);
-  L.shr = (uint32_t)(1 + p);
-  L.dst = &W.st[gg][16 * beta];
-}
-
-// Plane words of the lane's row group for the quad whose first plane word of
-// row 0 is at qaddr, through a buffer descriptor covering the rest of the
-// unit's planes (`bytes`): loads past it (blocks beyond the store in the last
-// row) return zero, and every other load stays inside the unit.  Lanes without
-// a row group load row group 0's words (staged nowhere).
-typedef unsigned int v2u32 __attribute__((ext_vector_type(2)));
-constexpr int kRawBufferFlags = 0x00020000;  // raw buffer, 32-bit data format
-__device__ __forceinline__ void stage_one_issue(uint64_t (&w)[4], const StageLane& L, uint64_t qaddr, uint32_t bytes) {
-  const uint32_t alo = (uint32_t)uni((int)(uint32_t)qaddr), ahi = (uint32_t)uni((int)(uint32_t)(qaddr >> 32));
-  const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
-      reinterpret_cast<void*>(((uint64_t)ahi << 32) | alo), (short)0, (int)(uint32_t)uni((int)bytes), kRawBufferFlags);
-#pragma unroll
-  for (int K = 0; K < 4; ++K) {
-    const v2u32 v = __builtin_amdgcn_raw_buffer_load_b64(rs, (int)L.boff[K], 0, 0);
-    w[K] = ((uint64_t)v.y << 32) | v.x;
-  }
-}
-
-// Byte transpose and nibble copies of the lane's row group (as task_stage).
-__device__ __forceinline__ void stage_one(const uint64_t (&w)[4], const StageLane& L) {
-  if (L.on) {
-    uint32_t* dst = L.dst;
-#pragma unroll
-    for (int hw = 0; hw < 2; ++hw) {
-      const uint32_t a0 = (uint32_t)(w[0] >> (32 * hw)), a1 = (uint32_t)(w[1] >> (32 * hw));
-      const uint32_t a2 = (uint32_t)(w[2] >> (32 * hw)), a3 = (uint32_t)(w[3] >> (32 * hw));
-      const uint32_t t01l = __builtin_amdgcn_perm(a1, a0, L.sel[0]);
-      const uint32_t t01h = __builtin_amdgcn_perm(a1, a0, L.sel[1]);
-      const uint32_t t23l = __builtin_amdgcn_perm(a3, a2, L.sel[2]);
-      const uint32_t t23h = __builtin_amdgcn_perm(a3, a2, L.sel[3]);
-      uint32_t T[4];
-      T[0] = __builtin_amdgcn_perm(t23l, t01l, 0x05040100u);
-      T[1] = __builtin_amdgcn_perm(t23l, t01l, 0x07060302u);
-      T[2] = __builtin_amdgcn_perm(t23h, t01h, 0x05040100u);
-      T[3] = __builtin_amdgcn_perm(t23h, t01h, 0x07060302u);
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int m = 4 * hw + j;
-        dst[2 * m] = T[j] << L.shl;
-        dst[2 * m + 1] = T[j] >> L.shr;
-      }
-    }
-  }
-}
-
-// Orders LDS accesses in the compiler only: a wave's LDS instructions are
-// executed in program order, so a wave reading rows it staged itself (or
-// restaging rows it has read) needs no wait.
-__device__ __forceinline__ void lds_program_order() { asm volatile("" ::: "memory"); }
-
-// A uniform value kept in a VGPR (opaque to the compiler) and read back per
-// use: loop-invariant uniforms otherwise stay live in SGPRs across the whole
-// loop, and this kernel has none to spare.
-__device__ __forceinline__ uint32_t to_vgpr(uint32_t x) {
-  uint32_t v;
-  asm volatile("v_mov_b32 %0, %1" : "=v"(v) : "v"(x));
-  return v;
-}
-__device__ __forceinline__ int from_vgpr(uint32_t v) {
-  int x;
-  asm volatile("v_readfirstlane_b32 %0, %1" : "=s"(x) : "v"(v));
-  return x;
 }
 
 // Exact documented scores of the queued keys (lane e < nq), from their queued
@@ -698,10 +569,9 @@ __device__ __forceinline__ void rescore_batch(const Plan& P, WL& W, const FusedA
 // Candidates of a quad are queued together; a batch is re-scored at the top
 // of the next quad once 48 are queued (or before the ring slot holding their
 // scales is reused), with a call only when one quad overflows the queue.
-// SAMPLE: one quad; the 8 largest proxies per head go to sample slot `sidx`.
-template <bool QF16, bool SAMPLE, int NSLM, int SQB, int RQ, int QCAP>
+template <bool QF16, int NSLM, int SQB, int RQ, int QCAP>
 __device__ void wave_run(const Plan& P, WaveLdsT<NSLM, SQB, RQ, QCAP>& W, const FusedArgs& a, int u, int64_t b0,
-                         int64_t b1, int64_t nbu, int64_t lo, int64_t hi, int64_t sidx) {
+                         int64_t b1, int64_t nbu, int64_t lo, int64_t hi) {
   constexpr int NCH = NSLM > 4 ? 2 : 1;
   constexpr int kFlushAt = QCAP * 3 / 4;
   const int lane = threadIdx.x & 63;
@@ -713,41 +583,24 @@ __device__ void wave_run(const Plan& P, WaveLdsT<NSLM, SQB, RQ, QCAP>& W, const 
   int pending = 0, oldest = 0;
   SclRegs<NCH, SQB> sr;
   scl_issue(sr, P, a, u, b0);
-  // kOne: all row groups staged in one pass (narrow full pass); otherwise one
-  // staging pass per slice
-  constexpr bool kOne = NSLM <= kNarrow;
-  uint64_t ring[kOne ? 1 : NSLM][4];
-  StageLane L;
-  uint32_t shpv[NSLM];          // kOne: slice shapes (c_p fields), kept in VGPRs
-  const uint32_t* rb0[NSLM];     // kOne: first staged row of each slice, this lane's column
-  const uint64_t ubase = reinterpret_cast<uint64_t>(a.planes + (int64_t)u * kD * kPlanes * a.nb_cap);
-  const uint32_t ubytes = (uint32_t)(kD * kPlanes * 8) * (uint32_t)a.nb_cap;  // kOne: nb_cap < kOneNbMax
-  if constexpr (kOne) {
-    stage_lane_setup(L, P, W, a);
+  // one staging pass per slice
+  uint64_t ring[NSLM][4];
 #pragma unroll
-    for (int sl = 0; sl < NSLM; ++sl) {
-      shpv[sl] = to_vgpr((uint32_t)P.slshp[sl]);
-      rb0[sl] = &W.st[uni(P.slrg[sl])][lane];
-    }
-    stage_one_issue(ring[0], L, ubase + (uint64_t)b0 * 8u, ubytes - (uint32_t)b0 * 8u);
-  } else {
-#pragma unroll
-    for (int sl = 0; sl < NSLM; ++sl)
-      if (sl < nsl) task_issue(ring[sl], P, a, u, b0, sl);
-  }
+  for (int sl = 0; sl < NSLM; ++sl)
+    if (sl < nsl) task_issue(ring[sl], P, a, u, b0, sl);
   int sqi = 0;
   for (int64_t sb0 = b0; sb0 < b1; sb0 += SQB, ++sqi) {
     const int rslot = sqi % RQ;
-    if (!SAMPLE && pending > 0 && oldest <= sqi - RQ) {  // its scales are about to be overwritten
+    if (pending > 0 && oldest <= sqi - RQ) {  // its scales are about to be overwritten
       rescore_batch<SQB>(P, W, a, u, pending);
       pending = 0;
     }
     const SqInfo si = scl_commit<QF16, NCH, SQB>(sr, P, W, rslot);
     if (sb0 + SQB < b1) scl_issue(sr, P, a, u, sb0 + SQB);
-    superquad_weights<QF16, SAMPLE, SQB>(P, W, a, si, rslot);
+    superquad_weights<QF16, SQB>(P, W, a, si, rslot);
     const int64_t sb1 = sb0 + SQB < b1 ? sb0 + SQB : b1;
     for (int64_t qb0 = sb0; qb0 < sb1; qb0 += kQB) {
-      if (!SAMPLE && pending >= kFlushAt) {
+      if (pending >= kFlushAt) {
         rescore_batch<SQB>(P, W, a, u, pending);
         pending = 0;
       }
@@ -756,66 +609,27 @@ __device__ void wave_run(const Plan& P, WaveLdsT<NSLM, SQB, RQ, QCAP>& W, const 
       v4i dig[4][NSLM];
       v4i acc[4];
 #pragma unroll
-      for (int mu = 0; mu < 4; ++mu) {
-        if (SAMPLE) acc[mu] = v4i{0, 0, 0, 0};
-        else acc[mu] = *reinterpret_cast<const v4i*>(&W.ci[qo + lb][mu][0]);
-      }
-      if constexpr (kOne) {
-        stage_one(ring[0], L);
-        if (more) stage_one_issue(ring[0], L, ubase + (uint64_t)(qb0 + kQB) * 8u, ubytes - (uint32_t)(qb0 + kQB) * 8u);
-        lds_program_order();
-      }
+      for (int mu = 0; mu < 4; ++mu) acc[mu] = *reinterpret_cast<const v4i*>(&W.ci[qo + lb][mu][0]);
 #pragma unroll
       for (int sl = 0; sl < NSLM; ++sl) {
         if (sl < nsl) {
-          if constexpr (!kOne) {
-            task_stage(ring[sl], P, W, sl);
-            if (more) task_issue(ring[sl], P, a, u, qb0 + kQB, sl);
-            wave_lds_sync();
-          }
+          task_stage(ring[sl], P, W, sl);
+          if (more) task_issue(ring[sl], P, a, u, qb0 + kQB, sl);
+          wave_lds_sync();
           uint32_t Z[4][4];
 #pragma unroll
           for (int dd = 0; dd < 4; ++dd)
 #pragma unroll
             for (int mu = 0; mu < 4; ++mu) Z[mu][dd] = 0u;
-          if constexpr (kOne) {
-            // plane segments: rows of plane p are the next c_p staged rows (dd < c_p);
-            // all 4 candidate rows of a segment are read together
-            const int cs = from_vgpr(shpv[sl]);
-            const uint32_t* rb = rb0[sl];
+          const int smask = uni(P.slmask[sl]);
+#pragma unroll
+          for (int dd = 0; dd < 4; ++dd) {
 #pragma unroll
             for (int p = 0; p < 4; ++p) {
-              const int c = (cs >> (4 * p)) & 15;
-              if (c == 0) break;
-              // only the c dwords that have plane p (a prefix, depths never increase
-              // along the proxy order) take this segment's rows
-              auto seg = [&](auto C) {
-                constexpr int cc = decltype(C)::value;
-                uint32_t x[cc];
+              if (smask & (1 << (4 * dd + p))) {
+                const uint32_t x = W.st[4 * dd + p][lane];
 #pragma unroll
-                for (int dd = 0; dd < cc; ++dd) x[dd] = rb[dd * kStP];
-#pragma unroll
-                for (int dd = 0; dd < cc; ++dd)
-#pragma unroll
-                  for (int mu = 0; mu < 4; ++mu) Z[mu][dd] |= x[dd] & (0x01010101u << (mu + 3 - p));
-              };
-              if (c >= 4) seg(std::integral_constant<int, 4>{});
-              else if (c == 3) seg(std::integral_constant<int, 3>{});
-              else if (c == 2) seg(std::integral_constant<int, 2>{});
-              else seg(std::integral_constant<int, 1>{});
-              rb += c * kStP;
-            }
-          } else {
-            const int smask = uni(P.slmask[sl]);
-#pragma unroll
-            for (int dd = 0; dd < 4; ++dd) {
-#pragma unroll
-              for (int p = 0; p < 4; ++p) {
-                if (smask & (1 << (4 * dd + p))) {
-                  const uint32_t x = W.st[4 * dd + p][lane];
-#pragma unroll
-                  for (int mu = 0; mu < 4; ++mu) Z[mu][dd] |= x & (0x01010101u << (mu + 3 - p));
-                }
+                for (int mu = 0; mu < 4; ++mu) Z[mu][dd] |= x & (0x01010101u << (mu + 3 - p));
               }
             }
           }
@@ -825,56 +639,12 @@ __device__ void wave_run(const Plan& P, WaveLdsT<NSLM, SQB, RQ, QCAP>& W, const 
           if (wl) wv = *reinterpret_cast<const v4i*>(&W.W[((qo + lb) * 4 + wh) * stride + 4 * sl]);
 #pragma unroll
           for (int mu = 0; mu < 4; ++mu) acc[mu] = __builtin_amdgcn_mfma_i32_16x16x64_i8(wv, dig[mu][sl], acc[mu], 0, 0, 0);
-          if constexpr (!kOne) wave_lds_sync();  // staged reads done before the next slice is staged
+          wave_lds_sync();  // staged reads done before the next slice is staged
         }
       }
-      if constexpr (kOne) lds_program_order();
       const int64_t kbase = (qb0 + lb) * kBlockTokens + kb;  // key of mu = 0
       const bool inner = qb0 * kBlockTokens >= lo && (qb0 + kQB) * kBlockTokens <= hi && qb0 + kQB <= nbu;
-      if (SAMPLE) {
-        float best[4];
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          best[r] = kNegInf;
-          const int bias = W.ci[qo + lb][0][r];
-          const bool okr = W.ci[qo + lb][1][r] != 0;
-          const float sc = W.sdel[r] * 0.0625f;
-#pragma unroll
-          for (int mu = 0; mu < 4; ++mu) {
-            const int64_t i = kbase + mu;
-            const bool el = inner || (i >= lo && i < hi && qb0 + lb < nbu);
-            const int S = acc[mu][r] >> mu;
-            const float v = __fmul_rn((float)(2 * S - bias), sc);
-            if (okr && el) best[r] = fmaxf(best[r], v);
-          }
-        }
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          if (r >= a.G) break;
-          // the kSmpW largest lane values: threshold = the kSmpW-th largest key
-          // (bitwise search with ballot counts), then the lanes above it
-          const uint32_t key = best[r] > kNegInf ? score_key(best[r]) | 1u : 0u;
-          uint32_t prefix = 0u;
-          for (int bit = 31; bit >= 0; --bit) {
-            const uint32_t cand = prefix | (1u << bit);
-            if (__popcll(__ballot(key >= cand)) >= kSmpW) prefix = cand;
-          }
-          const bool above = key > prefix && key != 0u;
-          const uint64_t ma = __ballot(above);
-          const int na = __popcll(ma);                       // < kSmpW
-          const uint64_t me = __ballot(key == prefix && key != 0u);
-          float* dst = a.ws.samp + ((int64_t)u * a.G + r) * kSmpRow + sidx * kSmpW;
-          int pos = -1;
-          if (above) pos = __popcll(ma & lanemask_lt(lane));
-          else if (key == prefix && key != 0u) {
-            const int e = __popcll(me & lanemask_lt(lane));
-            if (na + e < kSmpW) pos = na + e;
-          }
-          if (pos >= 0) gstore(dst + pos, best[r]);
-          const int nw = na + __popcll(me) < kSmpW ? na + __popcll(me) : kSmpW;
-          if (lane >= nw && lane < kSmpW) gstore(dst + lane, kNegInf);
-        }
-      } else {
+      {
         bool fl[4];
         uint64_t M[4];
         int tot = 0;
@@ -920,7 +690,7 @@ __device__ void wave_run(const Plan& P, WaveLdsT<NSLM, SQB, RQ, QCAP>& W, const 
       }
     }
   }
-  if (!SAMPLE && pending > 0) rescore_batch<SQB>(P, W, a, u, pending);
+  if (pending > 0) rescore_batch<SQB>(P, W, a, u, pending);
 }
 
 // ---------------------------------------------------------------- unit state
@@ -1192,8 +962,9 @@ __global__ __launch_bounds__(kTauThreads) void fused_tau_kernel(FusedArgs a) {
 // NSLM: the slices this instantiation keeps in registers; a unit is run by
 // the narrow (kNarrow) or the wide (8) instantiation according to its slice
 // count, which pass 2 leaves in uovf[u] (0: no filter for the unit).
-template <bool QF16, int NSLM, int SQB>
+template <bool QF16, int SQB>
 __global__ __launch_bounds__(kFT) void fused_main_kernel(FusedArgs a) {
+  constexpr int NSLM = kMaxSl;
   __shared__ Plan P;
   __shared__ WaveLdsT<NSLM, SQB, kRing, kQCap> WL[kFW];
   const int u = blockIdx.y, tid = threadIdx.x, wave = uni(tid >> 6);
@@ -1205,7 +976,7 @@ __global__ __launch_bounds__(kFT) void fused_main_kernel(FusedArgs a) {
   int64_t nu, lo, hi;
   row_window(a, u, &nu, &lo, &hi, blockIdx.x == 0 && tid == 0);
   const int ucls = (int)(uo >> 1);  // slices, or 0
-  if (ucls == 0 || ucls > NSLM || (NSLM > kNarrow && ucls <= kNarrow)) return;
+  if (ucls <= kNarrow || ucls > NSLM) return;  // no filter, or the cell filter's
   if (hi - lo <= a.ws.cap) return;
   const int64_t nbu = (nu + kBlockTokens - 1) / kBlockTokens;
   const int64_t gw = (int64_t)blockIdx.x * kFW;       // first wave of this workgroup
@@ -1214,7 +985,6 @@ __global__ __launch_bounds__(kFT) void fused_main_kernel(FusedArgs a) {
   if (gw * a.ws.qpw >= qhi || (gw + kFW) * a.ws.qpw <= qlo) return;
   plan_setup(P, a, u, pre);
   if (!P.ok || P.A == 0 || P.nsl > NSLM) return;
-  if (NSLM <= kNarrow && (P.slrg[kMaxSl] > kOneRows || a.nb_cap >= kOneNbMax)) return;  // the wide pass's units
   bool any = false;
   for (int h = 0; h < a.G; ++h) any |= P.tau[h] != kNegInf;
   if (!any) return;
@@ -1222,8 +992,8 @@ __global__ __launch_bounds__(kFT) void fused_main_kernel(FusedArgs a) {
   if (q0 < qlo) q0 = qlo;
   if (q1 > qhi) q1 = qhi;
   if (q0 >= q1) return;
-  wave_run<QF16, false, NSLM, SQB, kRing, kQCap>(P, WL[wave], a, u, q0 * kQB, q1 * kQB < nbu ? q1 * kQB : nbu, nbu,
-                                                  lo, hi, 0);
+  wave_run<QF16, NSLM, SQB, kRing, kQCap>(P, WL[wave], a, u, q0 * kQB, q1 * kQB < nbu ? q1 * kQB : nbu, nbu, lo,
+                                           hi);
 }
 
 // ---------------------------------------------------------------- pass 4
@@ -1922,8 +1692,8 @@ fathom_status launch_scan_topk_fused(const uint64_t* planes, const uint16_t* sca
     dim3 gm((unsigned)fa.ws.nwg, (unsigned)U);
     launch_filter(fa, U, s);
     if (wide) {
-      if (f16) hipLaunchKernelGGL((fused_main_kernel<true, kMaxSl, 8>), gm, dim3(kFT), 0, s, fa);
-      else hipLaunchKernelGGL((fused_main_kernel<false, kMaxSl, 8>), gm, dim3(kFT), 0, s, fa);
+      if (f16) hipLaunchKernelGGL((fused_main_kernel<true, 8>), gm, dim3(kFT), 0, s, fa);
+      else hipLaunchKernelGGL((fused_main_kernel<false, 8>), gm, dim3(kFT), 0, s, fa);
     }
   }
   const unsigned rank_wg = (unsigned)((R + kRankXcd - 1) / kRankXcd) * kRankXcd * kRankParts;

@@ -27,9 +27,9 @@ constexpr int kNoBound = 1 << 30;  // accumulator start: always (+) or never (-)
 constexpr int kMainWavesTarget = 2048;  // full-pass waves in flight over all units
 constexpr int kBackfillUnits = 64;      // from this many units per launch ...
 constexpr int kBackfillQpw = 16;        // ... at most this many quads per full-pass wave
-constexpr int kNarrow = 3;         // slices of the narrow full-pass instantiation (A <= 48)
-constexpr int kOneRows = 16;       // narrow: row groups at most (all staged in one 64-lane pass)
-constexpr int64_t kOneNbMax = ((int64_t)1 << 20) - 4096;  // narrow: byte offsets within a unit's planes (and past them) fit 32 bits
+constexpr int kNarrow = 3;         // a unit of at most this many 16-channel slices (A <= 48) may take the cell filter
+constexpr int kOneRows = 16;       // cell filter: row groups at most (all staged in one 64-lane pass)
+constexpr int64_t kOneNbMax = ((int64_t)1 << 20) - 4096;  // cell filter: byte offsets within a unit's planes (and past them) fit 32 bits
 constexpr float kNegInf = -__builtin_huge_valf();
 
 struct FusedWs {
