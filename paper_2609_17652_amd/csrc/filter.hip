@@ -43,25 +43,37 @@
 
 namespace fathom {
 
-constexpr int kCG = 16;          // row groups at most
+constexpr int kCG = 16;          // row groups at most (4 slices of 4)
+constexpr int kCC = 4 * kCG;     // cells at most
 constexpr int kCA = 48;          // active channels at most
 constexpr int kCSB = 8;          // blocks per group (one delta per head; one loop iteration)
-constexpr int kCSlots = 4;       // groups of scales kept for re-scoring
 constexpr int kCQ = 64;          // queued candidates per wave (one ballot fits)
 constexpr int kCFlush = 64;      // re-score at a quad boundary once the queue is full
-constexpr int kSclRow = kCA + 2; // halfs per scale row: an odd number of dwords
 constexpr int kSv = 16;          // survivors per head buffered in LDS before a list append
+
+// Geometry of an instantiation with NS slices of 4 row groups (16 cells):
+// NS = 3 serves units of at most 48 cells, NS = 4 of at most 64.  The scale
+// ring holds one row of C + 2 halfs per block (an odd number of dwords, so
+// the lanes of a re-scoring batch fall in different banks) for Slots groups;
+// three workgroups per CU fit the LDS with 4 slots at NS = 3 and 3 at NS = 4.
+template <int NS>
+struct CGeo {
+  static constexpr int G = 4 * NS;
+  static constexpr int C = 4 * G;
+  static constexpr int Slots = NS == 3 ? 4 : 3;
+  static constexpr int SclRow = C + 2;
+};
 constexpr int kCWaves = 4;       // waves per workgroup
 constexpr int kCThreads = kCWaves * kWave;
 
 struct alignas(16) CellPlan {
-  int A, rg, ns, ok;       // active channels, row groups, 16-cell slices, the unit fits this pass
-  int nd[4];               // row groups of plane p
-  int gp[5];               // first row group of plane p (gp[4] = rg)
+  int A, rg, C, ok;        // active channels, row groups, cells, the unit fits this pass
+  int np[4];               // cells of plane p: the channels of depth > p
+  int base[5];             // first cell of plane p (base[4] = C)
   double Ku, Eabs;         // E = delta Ku + Eabs
   uint32_t rrow[kCG][2];   // row group g: plane rows 4 j + p of its 4 cells (16-bit halves, kCPad: none)
-  uint32_t rgp[kCG];       // row group g: plane p | proxy dword i << 8
-  float qrg[kCG][4][4];    // row group g, head h, cell k: -q (0 for pad cells and heads >= G)
+  float qrg[kCG][4][4];    // row group g, head h, cell k: -q 2^-p of the cell (0 past the cells and for heads >= G)
+  int cx[kCC];             // cell -> proxy index of its channel (0 past the cells)
   float qx[kCA][4];        // q by proxy index and head (delta)
   int pj[kCA];             // proxy index -> channel
   int px[kCA];             // ascending position y -> proxy index x (padded to a multiple of 8: x = A)
@@ -71,13 +83,15 @@ struct alignas(16) CellPlan {
 };
 constexpr uint32_t kCPad = 0xFFFFu;
 
+template <int NS>
 struct alignas(16) FilterLds {
-  uint64_t raw[4 * kCG][4];               // the quad's plane words: padded cell, block
-  uint32_t zero[kCG];                     // zero dwords (the A operand of lanes that carry no weights)
-  uint32_t W[4][4][kCG];                  // int8 weights: block of the quad, head, row group
-  int32_t ini[4][2][4][4];                // accumulator starts: block, nibble, mu, head
-  uint16_t scl[kCSlots][kCSB][kSclRow];   // fp16 scales: ring slot, block, proxy channel
-  uint32_t qx[kCG][kCQ];                  // queued keys' staged dwords (digits while re-scored): dword, entry
+  using Geo = CGeo<NS>;
+  uint64_t raw[Geo::C][4];                        // the quad's plane words: cell, block
+  uint32_t zero[Geo::G];                          // zero dwords (the A operand of lanes that carry no weights)
+  uint32_t W[4][4][Geo::G];                       // int8 weights: block of the quad, head, row group
+  int32_t ini[4][2][4][4];                        // accumulator starts: block, nibble, mu, head
+  uint16_t scl[Geo::Slots][kCSB][Geo::SclRow];    // fp16 scales: ring slot, block, cell (its channel's scale)
+  uint32_t qx[Geo::G][kCQ];                       // queued keys' staged dwords (digits while re-scored): dword, entry
   uint32_t qi[kCQ];                       // queued key index
   uint32_t qf[kCQ];                       // pos | slot << 3 | block of the group << 8 | head h at bit 7 + 8 h
   uint64_t sv[4][kSv];                    // survivors per head not yet appended to the row's list
@@ -149,27 +163,24 @@ __device__ __forceinline__ void cell_plan(CellPlan& P, const FusedArgs& a, const
 #pragma unroll
     for (int v = p + 1; v <= kPlanes; ++v) np[p] += cnt[0][v] + cnt[1][v];
   }
-  int nd[kPlanes], gp[kPlanes + 1];
-  gp[0] = 0;
+  int base[kPlanes + 1];  // cells plane-major without padding: cell base[p] + x = (plane p, proxy channel x)
+  base[0] = 0;
 #pragma unroll
-  for (int p = 0; p < kPlanes; ++p) {
-    nd[p] = (np[p] + 3) >> 2;
-    gp[p + 1] = gp[p] + nd[p];
-  }
-  const int rg = gp[kPlanes];
-  const bool ok = G <= 4 && A > 0 && A <= kCA && rg <= kCG;
+  for (int p = 0; p < kPlanes; ++p) base[p + 1] = base[p] + np[p];
+  const int C = base[kPlanes], rg = (C + 3) >> 2;
+  const bool ok = G <= 4 && A > 0 && A <= kCA && C <= kCC;
   if (tid == 0) {
     P.A = A;
     P.rg = rg;
-    P.ns = (rg + 3) >> 2;
+    P.C = C;
     P.ok = ok;
 #pragma unroll
     for (int p = 0; p < kPlanes; ++p) {
-      P.nd[p] = nd[p];
-      P.gp[p] = gp[p];
+      P.np[p] = np[p];
+      P.base[p] = base[p];
     }
-    P.gp[kPlanes] = rg;
-    const double cells = (double)(np[0] + np[1] + np[2] + np[3]);
+    P.base[kPlanes] = C;
+    const double cells = (double)C;
     P.Ku = (cells / 4.0 + (double)A * (double)A * 127.0 * 0x1p-24) * (1.0 + 0x1p-20);
     P.Eabs = (double)A * 0x1p-120;
   }
@@ -200,31 +211,35 @@ __device__ __forceinline__ void cell_plan(CellPlan& P, const FusedArgs& a, const
     for (int h = 0; h < 4; ++h) P.qa[tid][h] = 0.0f;
   }
   __syncthreads();
-  // row groups: thread (g, k) fills cell k of row group g
-  if (tid < 4 * kCG) {
-    const int g = tid >> 2, k = tid & 3;
+  // cells: thread c fills cell c = 4 g + k (row group g, byte k).  Its weight
+  // uses -q 2^-p, so every cell shares one rounding constant per group and
+  // head (the scaling is exact unless q 2^-p is subnormal, and then the cell's
+  // weight is 0 either way: |q a16 2^-p| < 2^-110 is far below delta / 2)
+  if (tid < kCC) {
+    const int c = tid, g = c >> 2, k = c & 3;
     int p = 0;
 #pragma unroll
-    for (int pp = 1; pp < kPlanes; ++pp) p += g >= gp[pp];
-    const int i = g - gp[p], x = 4 * i + k;
-    const bool real = g < rg && x < np[p];
+    for (int pp = 1; pp < kPlanes; ++pp) p += c >= base[pp];
+    const bool real = c < C;
+    const int x = real ? c - base[p] : 0;
     const uint32_t row = real ? (uint32_t)(4 * (sact[x] & 0xFF) + p) : kCPad;
     // cells 0,1 -> rrow[g][0], cells 2,3 -> rrow[g][1] (16-bit halves)
     const uint32_t part = row << (16 * (k & 1));
     const uint32_t other = __shfl_xor(part, 1, kWave);
     if ((k & 1) == 0) P.rrow[g][k >> 1] = part | other;
 #pragma unroll
-    for (int h = 0; h < 4; ++h) P.qrg[g][h][k] = real && h < G ? -P.qx[x][h] : 0.0f;
-    if (k == 0) P.rgp[g] = (uint32_t)p | (uint32_t)i << 8;
+    for (int h = 0; h < 4; ++h) P.qrg[g][h][k] = real && h < G ? -ldexpf(P.qx[x][h], -p) : 0.0f;
+    P.cx[c] = x;
   }
   if (tid < 4) P.tau[tid] = kNegInf;
   __syncthreads();
 }
 
 // ---------------------------------------------------------------- scales
-// Lane x (< A) holds the 8 scales of proxy channel x for the group at block
-// sb0, two blocks a dword, read through a buffer descriptor over the unit's
-// scale rows (zero past them, and for lanes >= A).  With 16-byte aligned rows
+// Lane c (< C) holds the 8 scales of cell c's channel (scale row jrow) for the
+// group at block sb0, two blocks a dword, read through a buffer descriptor
+// over the unit's scale rows (zero past them, and for lanes >= C; the lanes of
+// one channel's cells read the same bytes).  With 16-byte aligned rows
 // (nb_cap a multiple of 8) one 16-byte load per lane; blocks past nb_cap then
 // read the next row's scales, which only the (ineligible) keys of those
 // blocks and delta see.  Otherwise 8 two-byte loads, each past the range
@@ -236,14 +251,14 @@ struct CScl {
 typedef unsigned short u16x1;
 
 template <bool VEC>
-__device__ __forceinline__ void cscl_issue(CScl& r, const FusedArgs& a, int u, int A, int jrow, int sb0, bool valid) {
+__device__ __forceinline__ void cscl_issue(CScl& r, const FusedArgs& a, int u, int nc, int jrow, int sb0, bool valid) {
   const int lane = threadIdx.x & 63;
   const uint64_t base = reinterpret_cast<uint64_t>(a.scales + (int64_t)u * kD * a.nb_cap);
   const uint32_t alo = (uint32_t)cuni((int)(uint32_t)base), ahi = (uint32_t)cuni((int)(uint32_t)(base >> 32));
   const uint32_t bytes = (uint32_t)(kD * 2) * (uint32_t)a.nb_cap;
   const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
       reinterpret_cast<void*>(((uint64_t)ahi << 32) | alo), (short)0, (int)bytes, kRawBufferFlags);
-  const uint32_t off = lane < A && valid ? ((uint32_t)jrow * (uint32_t)a.nb_cap + (uint32_t)sb0) * 2u : kPastRange;
+  const uint32_t off = lane < nc && valid ? ((uint32_t)jrow * (uint32_t)a.nb_cap + (uint32_t)sb0) * 2u : kPastRange;
   if constexpr (VEC) {
     const v4u x0 = __builtin_amdgcn_raw_buffer_load_b128(rs, (int)off, 0, 0);
     r.v[0] = x0.x; r.v[1] = x0.y; r.v[2] = x0.z; r.v[3] = x0.w;
@@ -264,13 +279,15 @@ struct CDel {
   bool valid;
 };
 
-// Writes the group's scales to ring slot `slot` and returns delta of head
-// `hq` (every lane: its own head for the weights).  qv: q of proxy channel
-// `lane` for the four heads (0 past A).
-__device__ __forceinline__ CDel cscl_commit(const CScl& r, FilterLds& L, int slot, int hq, const float (&qv)[4]) {
+// Writes the group's scales to ring slot `slot` (cell order: cell c holds
+// its channel's scale, so the plane-0 cell of proxy channel x is cell x) and
+// returns delta of head `hq` (every lane: its own head for the weights).  qv:
+// q of cell `lane`'s channel for the four heads (0 past the cells).
+template <int NS>
+__device__ __forceinline__ CDel cscl_commit(const CScl& r, FilterLds<NS>& L, int slot, int hq, const float (&qv)[4]) {
   const int lane = threadIdx.x & 63;
   uint32_t mx = 0u;
-  if (lane < kCA) {
+  if (lane < CGeo<NS>::C) {
 #pragma unroll
     for (int b = 0; b < kCSB; ++b) L.scl[slot][b][lane] = (uint16_t)((r.v[b >> 1] >> (16 * (b & 1))) & 0xFFFFu);
   }
@@ -346,17 +363,21 @@ __device__ __forceinline__ void cstage_issue(CRaw& R, const CStage& S, int qb0, 
   }
 }
 
-__device__ __forceinline__ void cstage_write(const CRaw& R, FilterLds& L) {
+template <int NS>
+__device__ __forceinline__ void cstage_write(const CRaw& R, FilterLds<NS>& L) {
   const int lane = threadIdx.x & 63, g = lane >> 2, bq = lane & 3;
+  if (g < CGeo<NS>::G) {
 #pragma unroll
-  for (int k = 0; k < 4; ++k) L.raw[4 * g + k][bq] = R.w[k];
+    for (int k = 0; k < 4; ++k) L.raw[4 * g + k][bq] = R.w[k];
+  }
 }
 
 // Row groups 2 P and 2 P + 1 of this lane's block and octet (v: its two dwords)
 // from the staged words; lane l (as a source) addresses cell 8 P + ((l & 15) >> 1)
 // of block l >> 4.
 typedef int v2i __attribute__((ext_vector_type(2)));
-__device__ __forceinline__ v2i ctr_read(const FilterLds& L, uint32_t src_off, int P) {
+template <int NS>
+__device__ __forceinline__ v2i ctr_read(const FilterLds<NS>& L, uint32_t src_off, int P) {
   const unsigned char* base = reinterpret_cast<const unsigned char*>(&L.raw[0][0]) + src_off + P * 8 * 4 * 8;
   return __builtin_amdgcn_ds_read_tr8_b64_v2i32((__attribute__((address_space(3))) v2i*)(base));
 }
@@ -365,37 +386,37 @@ __device__ __forceinline__ v2i ctr_read(const FilterLds& L, uint32_t src_off, in
 // Lanes (block b = lane >> 4 of the quad, head h = (lane >> 2) & 3, part =
 // lane & 3): the negated int8 weights -W of row groups g = part (mod 4) of
 // block b for head h, their sum, and the accumulator starts of (b, h).  With
-// Mp = 1.5 2^(23 + e + p) the low byte of fl(-q a16 + Mp) is rne(-q a16 2^-p
+// M0 = 1.5 2^(23 + e) the low byte of fl(-q 2^-p a16 + M0) is rne(-q a16 2^-p
 // / delta) as a two's complement byte.  Pad cells (q = 0) get weight 0; a
 // group without thresholds (a head past G, no tau, no valid delta) gets fixed
 // starts that no sum of products can cross (|S 2^pos| < 2^21), whatever its
 // weights.
 struct CHead {
-  float Mp[4];  // rounding constant of this lane's row groups g = part + 4 k
+  float M0;     // rounding constant, 1.5 2^(23 + e)
   int X;        // floor(2 (tau - E) / delta) - 1, clamped
   bool m0;      // thresholds apply
   int c0, c1;   // the starts of positions 2 part and 2 part + 1 when they do not
 };
 
-__device__ __forceinline__ void cquad_weights(const CellPlan& P, FilterLds& L, const CHead& H, int slot, int sbq,
-                                              uint32_t wi) {
+template <int NS>
+__device__ __forceinline__ void cquad_weights(const CellPlan& P, FilterLds<NS>& L, const CHead& H, int slot, int sbq) {
   const int lane = threadIdx.x & 63, b = lane >> 4, h = (lane >> 2) & 3, part = lane & 3;
   const uint16_t* srow = &L.scl[slot][sbq + b][0];
-  // every read first: row groups g = part + 4 k (wi byte k: dword i | plane p << 4 | real << 6)
-  float4 qv[4];
-  uint32_t s01[4], s23[4];
+  // every read first: row groups g = part + 4 k, cells 4 g .. 4 g + 3
+  float4 qv[NS];
+  uint32_t s01[NS], s23[NS];
 #pragma unroll
-  for (int k = 0; k < 4; ++k) {
-    const int i = (int)((wi >> (8 * k)) & 15u), g = part + 4 * k;
+  for (int k = 0; k < NS; ++k) {
+    const int g = part + 4 * k;
     qv[k] = *reinterpret_cast<const float4*>(&P.qrg[g][h][0]);
-    s01[k] = *reinterpret_cast<const uint32_t*>(&srow[4 * i]);
-    s23[k] = *reinterpret_cast<const uint32_t*>(&srow[4 * i + 2]);
+    s01[k] = *reinterpret_cast<const uint32_t*>(&srow[4 * g]);
+    s23[k] = *reinterpret_cast<const uint32_t*>(&srow[4 * g + 2]);
   }
   int wsum = 0;
+  const float Mp = H.M0;
 #pragma unroll
-  for (int k = 0; k < 4; ++k) {
+  for (int k = 0; k < NS; ++k) {
     const int g = part + 4 * k;
-    const float Mp = H.Mp[k];
     const float a0 = half_bits_to_float((uint16_t)(s01[k] & 0xFFFFu)), a1 = half_bits_to_float((uint16_t)(s01[k] >> 16));
     const float a2 = half_bits_to_float((uint16_t)(s23[k] & 0xFFFFu)), a3 = half_bits_to_float((uint16_t)(s23[k] >> 16));
     const uint32_t r0 = __float_as_uint(__fmaf_rn(qv[k].x, a0, Mp)), r1 = __float_as_uint(__fmaf_rn(qv[k].y, a1, Mp));
@@ -418,7 +439,8 @@ __device__ __forceinline__ void cquad_weights(const CellPlan& P, FilterLds& L, c
 
 // ---------------------------------------------------------------- survivors
 // Appends the n buffered survivors of head h to row u G + h (one atomic).
-__device__ __forceinline__ void cflush_head(FilterLds& L, const FusedArgs& a, int u, int h, int n) {
+template <int NS>
+__device__ __forceinline__ void cflush_head(FilterLds<NS>& L, const FusedArgs& a, int u, int h, int n) {
   const int lane = threadIdx.x & 63, G = a.G;
   if (n <= 0) return;
   uint32_t base = 0u;
@@ -435,7 +457,8 @@ __device__ __forceinline__ void cflush_head(FilterLds& L, const FusedArgs& a, in
 // place: the plane-p dwords of proxy dword i sit at or after dword i), then
 // the chain runs over the active channels ascending (padded to a multiple of
 // 4 with q = 0, which leaves every score unchanged).
-__device__ __forceinline__ void crescore(const CellPlan& P, FilterLds& L, const FusedArgs& a, int u, int nq, int (&svn)[4]) {
+template <int NS>
+__device__ __forceinline__ void crescore(const CellPlan& P, FilterLds<NS>& L, const FusedArgs& a, int u, int nq, int (&svn)[4]) {
   const int lane = threadIdx.x & 63, G = a.G;
   const bool on = lane < nq;
   const int e = on ? lane : 0;
@@ -443,15 +466,33 @@ __device__ __forceinline__ void crescore(const CellPlan& P, FilterLds& L, const 
   const uint32_t pos = f & 7u, hm = on ? f : 0u;
   const int slot = (int)((f >> 3) & 3u), blk = (int)((f >> 8) & 7u);
   uint32_t* ent = &L.qx[0][e];  // dword i of the entry at ent[i * kCQ] (entries side by side: no bank conflicts)
-  const int nd0 = cuni(P.nd[0]), nd1 = cuni(P.nd[1]), nd2 = cuni(P.nd[2]), nd3 = cuni(P.nd[3]);
-  const int g1 = cuni(P.gp[1]), g2 = cuni(P.gp[2]), g3 = cuni(P.gp[3]);
+  // digit dword i (proxy channels 4 i .. 4 i + 3): the plane-p bits of its
+  // channels are cells base_p + 4 i .., bytes (base_p & 3) .. of row group
+  // (base_p + 4 i) >> 2 and the next one (a byte funnel shift), the bytes of
+  // channels without plane p masked off; plane 0 is row group i itself, and
+  // every other dword read lies past i, so the digits overwrite in place
+  int npl[kPlanes], bpl[kPlanes];
+#pragma unroll
+  for (int p = 0; p < kPlanes; ++p) {
+    npl[p] = cuni(P.np[p]);
+    bpl[p] = cuni(P.base[p]);
+  }
+  const int nd0 = (npl[0] + 3) >> 2;
   for (int i = 0; i < nd0; ++i) {
-    const uint32_t w0 = ent[i * kCQ];
-    const uint32_t w1 = i < nd1 ? ent[(g1 + i) * kCQ] : 0u;
-    const uint32_t w2 = i < nd2 ? ent[(g2 + i) * kCQ] : 0u;
-    const uint32_t w3 = i < nd3 ? ent[(g3 + i) * kCQ] : 0u;
-    ent[i * kCQ] = ((w0 >> pos) & 0x01010101u) << 3 | ((w1 >> pos) & 0x01010101u) << 2 |
-                   ((w2 >> pos) & 0x01010101u) << 1 | ((w3 >> pos) & 0x01010101u);
+    uint32_t dw = 0u;
+#pragma unroll
+    for (int p = 0; p < kPlanes; ++p) {
+      const int v = npl[p] - 4 * i;  // channels of the dword with plane p
+      if (v > 0) {
+        const int c0 = bpl[p] + 4 * i, r = c0 >> 2, sh = c0 & 3;
+        const int r1 = r + 1 < CGeo<NS>::G ? r + 1 : r;
+        const uint32_t lo = ent[r * kCQ], hi = ent[r1 * kCQ];
+        const uint32_t w = sh ? __builtin_amdgcn_alignbyte(hi, lo, (uint32_t)sh) : lo;
+        const uint32_t m = v >= 4 ? 0x01010101u : 0x01010101u >> (8 * (4 - v));
+        dw |= ((w >> pos) & m) << (3 - p);
+      }
+    }
+    ent[i * kCQ] = dw;
   }
   // digit of proxy channel x: byte x & 3 of dword x >> 2
   const uint8_t* dg = reinterpret_cast<const uint8_t*>(ent);
@@ -526,9 +567,10 @@ __device__ __forceinline__ void crescore(const CellPlan& P, FilterLds& L, const 
 // queued key is reused, and at the end.
 constexpr int kCStride = kCWaves * kCSB;  // blocks from one group of a wave to its next
 
-template <bool VEC, class Ready>
-__device__ __forceinline__ void cwave_run(const CellPlan& P, FilterLds& L, const FusedArgs& a, int u, int b0, int ng,
+template <bool VEC, int NS, class Ready>
+__device__ __forceinline__ void cwave_run(const CellPlan& P, FilterLds<NS>& L, const FusedArgs& a, int u, int b0, int ng,
                                           int nbu, int lo, int hi, Ready&& ready) {
+  using Geo = CGeo<NS>;
   const int lane = threadIdx.x & 63;
   const int bq = lane >> 4, nib = (lane >> 3) & 1, oct = lane & 7;
   const int kb = 8 * oct + 4 * nib;                      // key of mu = 0 within its block
@@ -539,20 +581,12 @@ __device__ __forceinline__ void cwave_run(const CellPlan& P, FilterLds& L, const
 #pragma unroll
   for (int mu = 0; mu < 4; ++mu) mk[mu] = 0x01010101u << (4 * nib + mu);
   const bool top = (lane & 3) == 3;  // as a weight lane: its second start is position 7
-  const int A = cuni(P.A), rg = cuni(P.rg);
-  const int srow = lane < A ? P.pj[lane] : 0;  // the scale row of proxy channel `lane`
+  const int C = cuni(P.C);
+  const int cxl = P.cx[lane];                  // cell `lane`'s channel (proxy index)
+  const int srow = lane < C ? P.pj[cxl] : 0;   // its scale row
   float qv[4];
 #pragma unroll
-  for (int h = 0; h < 4; ++h) qv[h] = lane < A ? P.qx[lane][h] : 0.0f;
-  // this lane's weight row groups g = part + 4 k: dword i | plane p << 4 | real << 6
-  uint32_t wi = 0u;
-#pragma unroll
-  for (int k = 0; k < 4; ++k) {
-    const int g = (lane & 3) + 4 * k;
-    const uint32_t pi = P.rgp[g];
-    const uint32_t f = g < rg ? ((pi >> 8) & 15u) | (pi & 3u) << 4 | 0x40u : 0u;
-    wi |= f << (8 * k);
-  }
+  for (int h = 0; h < 4; ++h) qv[h] = lane < C ? P.qx[cxl][h] : 0.0f;
   // as a transpose source: cell (l & 15) >> 1 of pair 0, block l >> 4
   const uint32_t src_off = (uint32_t)((((lane & 15) >> 1) * 4 + bq) * 8);
   // the A operand: this lane's weights, or zeros
@@ -561,13 +595,13 @@ __device__ __forceinline__ void cwave_run(const CellPlan& P, FilterLds& L, const
   const uint32_t ubytes = (uint32_t)(kD * kPlanes * 8) * (uint32_t)a.nb_cap;
   CStage S;
   cstage_setup(S, P, a, ubase, ubytes);
-  if (lane < kCG) L.zero[lane] = 0u;
+  if (lane < Geo::G) L.zero[lane] = 0u;
   int pending = 0, oldest = 0;
   int svn[4] = {0, 0, 0, 0};  // buffered survivors per head
   // the issue order here (scales, quad 0, quad 1) is the loop's steady-state
   // order, so the compiler's load counters agree on every path into the loop
   CScl sr;
-  cscl_issue<VEC>(sr, a, u, A, srow, b0, ng > 0);
+  cscl_issue<VEC>(sr, a, u, C, srow, b0, ng > 0);
   sched_fence();
   CRaw R0, R1;
   cstage_issue(R0, S, b0, ng > 0);
@@ -582,24 +616,24 @@ __device__ __forceinline__ void cwave_run(const CellPlan& P, FilterLds& L, const
     sched_fence();
     cstage_issue(R, S, qb0 + kCStride, it + 1 < ng);  // the same quad of the wave's next group
     sched_fence();
-    cquad_weights(P, L, H, slot, sbq, wi);
+    cquad_weights(P, L, H, slot, sbq);
     lds_order();
     v4i acc[4];
 #pragma unroll
     for (int mu = 0; mu < 4; ++mu) acc[mu] = *reinterpret_cast<const v4i*>(&L.ini[bq][nib][mu][0]);
     // every row group of the quad (pads and groups past the unit's are zero)
-    uint32_t xr[kCG];
+    uint32_t xr[Geo::G];
 #pragma unroll
-    for (int pp = 0; pp < kCG / 2; ++pp) {
+    for (int pp = 0; pp < Geo::G / 2; ++pp) {
       const v2i v = ctr_read(L, src_off, pp);
       xr[2 * pp] = (uint32_t)v.x;
       xr[2 * pp + 1] = (uint32_t)v.y;
     }
-    v4i wv[kCG / 4];
+    v4i wv[NS];
 #pragma unroll
-    for (int s2 = 0; s2 < kCG / 4; ++s2) wv[s2] = *reinterpret_cast<const v4i*>(wsrc + 4 * s2);
+    for (int s2 = 0; s2 < NS; ++s2) wv[s2] = *reinterpret_cast<const v4i*>(wsrc + 4 * s2);
 #pragma unroll
-    for (int s2 = 0; s2 < kCG / 4; ++s2) {
+    for (int s2 = 0; s2 < NS; ++s2) {
       v4i bv[4];
 #pragma unroll
       for (int mu = 0; mu < 4; ++mu)
@@ -644,7 +678,7 @@ __device__ __forceinline__ void cwave_run(const CellPlan& P, FilterLds& L, const
           const int mu = __builtin_ctz(kmask);
           const int qp = pending + rank;
 #pragma unroll
-          for (int i = 0; i < kCG; ++i) L.qx[i][qp] = xr[i];
+          for (int i = 0; i < Geo::G; ++i) L.qx[i][qp] = xr[i];
           L.qi[qp] = (uint32_t)(kbase + mu);
           L.qf[qp] = (uint32_t)(4 * nib + mu) | meta | ((D >> mu) & 0x01010101u) << 7;
           kmask &= kmask - 1u;
@@ -652,9 +686,9 @@ __device__ __forceinline__ void cwave_run(const CellPlan& P, FilterLds& L, const
         pending += __popcll(__ballot(mine));
         continue;
       }
-      // entries of group it - 3 hold ring slot (it + 1) & 3, rewritten next
+      // entries of group it + 1 - Slots hold the ring slot rewritten next
       const bool flush = want != 0ull || pending >= kCFlush ||
-                         (pending > 0 && (last || (endg && oldest <= it + 1 - kCSlots)));
+                         (pending > 0 && (last || (endg && oldest <= it + 1 - Geo::Slots)));
       if (!flush) break;
       lds_order();
       crescore(P, L, a, u, pending, svn);
@@ -668,16 +702,14 @@ __device__ __forceinline__ void cwave_run(const CellPlan& P, FilterLds& L, const
   // delta, then the quads
   int it = 0;
   for (int gb0 = b0; it < ng; gb0 += kCStride, ++it) {
-    slot = it & (kCSlots - 1);
+    slot = it % Geo::Slots;
     {
       const CDel dl = cscl_commit(sr, L, slot, hq, qv);
       sched_fence();
-      cscl_issue<VEC>(sr, a, u, A, srow, gb0 + kCStride, it + 1 < ng);
+      cscl_issue<VEC>(sr, a, u, C, srow, gb0 + kCStride, it + 1 < ng);
       sched_fence();
       const float th = P.tau[hq];
-      const float M0 = ldexpf(12582912.0f, dl.e);  // 1.5 * 2^(23 + e)
-#pragma unroll
-      for (int k = 0; k < 4; ++k) H.Mp[k] = ldexpf(M0, (int)((wi >> (8 * k + 4)) & 3u));
+      H.M0 = ldexpf(12582912.0f, dl.e);  // 1.5 * 2^(23 + e)
       H.X = 0;
       const bool none = hq >= a.G || th == kNegInf;  // no key of this head is a candidate
       H.m0 = !none && dl.valid;
@@ -756,10 +788,10 @@ __device__ __forceinline__ float ctau(const FusedArgs& a, const float (&sv)[kCTa
 // [x kCWaves gpw, (x + 1) kCWaves gpw) of its unit, wave w every kCWaves-th of
 // them from the w-th.  Units of another class (uovf[u] >> 1 != 1: the wide
 // pass, or no filter) and rows computed exactly return at once.
-template <bool VEC>
+template <bool VEC, int NS>
 __global__ __launch_bounds__(kCThreads, 3) void fused_filter_kernel(FusedArgs a, int gpw) {
   __shared__ CellPlan P;
-  __shared__ FilterLds WL[kCWaves];
+  __shared__ FilterLds<NS> WL[kCWaves];
   const int u = blockIdx.y, tid = threadIdx.x, wave = cuni(tid >> 6), lane = tid & 63, G = a.G;
   const uint32_t uo = gload(a.ws.uovf + u);
   // this wave's row's samples first: tau waits on them
@@ -782,7 +814,7 @@ __global__ __launch_bounds__(kCThreads, 3) void fused_filter_kernel(FusedArgs a,
   const int64_t ghi = (hi + kCSB * kBlockTokens - 1) / (kCSB * kBlockTokens);
   if (g0 >= ghi || g1 <= glo) return;
   cell_plan(P, a, pre);
-  if (!P.ok) return;
+  if (!P.ok || P.C > CGeo<NS>::C) return;  // more cells than the caller's bound allowed: the exact path
   // this wave: groups g0 + wave + kCWaves i inside the window (ng = 0: none)
   int64_t gf = g0 + wave;
   if (gf < glo) gf += (glo - gf + kCWaves - 1) / kCWaves * kCWaves;
@@ -804,22 +836,28 @@ __global__ __launch_bounds__(kCThreads, 3) void fused_filter_kernel(FusedArgs a,
     for (int h = 0; h < G; ++h) any |= P.tau[h] != kNegInf;
     return any;
   };
-  cwave_run<VEC>(P, WL[wave], a, u, (int)(gf * kCSB), ng, (int)nbu, (int)lo, (int)hi, ready);
+  cwave_run<VEC, NS>(P, WL[wave], a, u, (int)(gf * kCSB), ng, (int)nbu, (int)lo, (int)hi, ready);
 }
 
 // Groups per wave: about kFResident waves over all units (three per SIMD of
 // the chip, one round); a workgroup takes kCWaves * gpw consecutive groups.
 constexpr int64_t kFResident = 3 * 4 * 256;
-void launch_filter(const FusedArgs& fa, int U, hipStream_t s) {
+void launch_filter(const FusedArgs& fa, int U, int max_cells, hipStream_t s) {
   const int64_t ngr = (fa.nb_cap + kCSB - 1) / kCSB;
   int64_t gpw = ((int64_t)U * ngr + kFResident - 1) / kFResident;
   if (gpw < 1) gpw = 1;
   const unsigned wgs = (unsigned)((ngr + kCWaves * gpw - 1) / (kCWaves * gpw));
+  const dim3 grid(wgs, (unsigned)U);
   // 16-byte aligned scale rows: one 16-byte scale load per lane and group
-  if ((fa.nb_cap & 7) == 0 && (reinterpret_cast<uintptr_t>(fa.scales) & 15) == 0)
-    hipLaunchKernelGGL(fused_filter_kernel<true>, dim3(wgs, (unsigned)U), dim3(kCThreads), 0, s, fa, (int)gpw);
-  else
-    hipLaunchKernelGGL(fused_filter_kernel<false>, dim3(wgs, (unsigned)U), dim3(kCThreads), 0, s, fa, (int)gpw);
+  const bool vec = (fa.nb_cap & 7) == 0 && (reinterpret_cast<uintptr_t>(fa.scales) & 15) == 0;
+  // three slices when no unit can have more than 48 cells
+  if (max_cells > 0 && max_cells <= CGeo<3>::C) {
+    if (vec) hipLaunchKernelGGL((fused_filter_kernel<true, 3>), grid, dim3(kCThreads), 0, s, fa, (int)gpw);
+    else hipLaunchKernelGGL((fused_filter_kernel<false, 3>), grid, dim3(kCThreads), 0, s, fa, (int)gpw);
+  } else {
+    if (vec) hipLaunchKernelGGL((fused_filter_kernel<true, 4>), grid, dim3(kCThreads), 0, s, fa, (int)gpw);
+    else hipLaunchKernelGGL((fused_filter_kernel<false, 4>), grid, dim3(kCThreads), 0, s, fa, (int)gpw);
+  }
 }
 
 }  // namespace fathom

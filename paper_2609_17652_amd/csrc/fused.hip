@@ -702,11 +702,10 @@ __device__ __forceinline__ uint32_t unit_class(const FusedArgs& a, const int (&s
   const int A = sc[1] + sc[2] + sc[3] + sc[4];
   if (!(a.G <= 4 && A > 0 && hi - lo > a.ws.cap)) return 0u;
   uint32_t cls = (uint32_t)((A + 15) >> 4);
-  // row groups: the depth of each dword's first channel in the proxy order
-  // (depth descending); the cell filter stages at most kOneRows of them
-  int rows = 0;
-  for (int x = 0; x < A; x += 4) rows += x < sc[4] ? 4 : x < sc[4] + sc[3] ? 3 : x < sc[4] + sc[3] + sc[2] ? 2 : 1;
-  if (cls <= (uint32_t)kNarrow) cls = (rows <= kOneRows && a.nb_cap < kOneNbMax) ? 1u : (uint32_t)(kNarrow + 1);
+  // the cell filter stages at most 4 kOneRows cells (one per active channel
+  // and plane)
+  const int cells = sc[1] + 2 * sc[2] + 3 * sc[3] + 4 * sc[4];
+  if (cls <= (uint32_t)kNarrow) cls = (cells <= 4 * kOneRows && a.nb_cap < kOneNbMax) ? 1u : (uint32_t)(kNarrow + 1);
   return cls;
 }
 
@@ -1690,7 +1689,7 @@ fathom_status launch_scan_topk_fused(const uint64_t* planes, const uint16_t* sca
   if (wide || G > 4) hipLaunchKernelGGL(fused_tau_kernel, dim3(R), dim3(kTauThreads), 0, s, fa);
   if (G <= 4) {
     dim3 gm((unsigned)fa.ws.nwg, (unsigned)U);
-    launch_filter(fa, U, s);
+    launch_filter(fa, U, max_unit_bits, s);
     if (wide) {
       if (f16) hipLaunchKernelGGL((fused_main_kernel<true, 8>), gm, dim3(kFT), 0, s, fa);
       else hipLaunchKernelGGL((fused_main_kernel<false, 8>), gm, dim3(kFT), 0, s, fa);

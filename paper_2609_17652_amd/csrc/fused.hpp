@@ -215,7 +215,8 @@ __device__ __forceinline__ void wave_max4_u(uint32_t (&v)[4]) {
   }
 }
 
-// The full pass over the units of class 1 (filter.hip).
-void launch_filter(const FusedArgs& fa, int U, hipStream_t s);
+// The full pass over the units of class 1 (filter.hip); max_cells: the
+// caller's bound on a unit's depth bits (0: none), which picks the geometry.
+void launch_filter(const FusedArgs& fa, int U, int max_cells, hipStream_t s);
 
 }  // namespace fathom
