@@ -55,14 +55,19 @@ constexpr int kSv = 16;          // survivors per head buffered in LDS before a 
 // NS = 3 serves units of at most 48 cells, NS = 4 of at most 64.  The scale
 // ring holds one row of C + 2 halfs per block (an odd number of dwords, so
 // the lanes of a re-scoring batch fall in different banks) for Slots groups;
-// three workgroups per CU fit the LDS with 4 slots at NS = 3 and 3 at NS = 4.
+// three workgroups per CU fit the LDS with 5 slots at NS = 3 and 3 at NS = 4.
 template <int NS>
 struct CGeo {
   static constexpr int G = 4 * NS;
   static constexpr int C = 4 * G;
-  static constexpr int Slots = NS == 3 ? 4 : 3;
+  static constexpr int Slots = NS == 3 ? 5 : 3;
   static constexpr int SclRow = C + 2;
+  static constexpr bool Fine = NS == 3;  // two-level weights (the registers fit them at three slices)
 };
+// Fine weights W' = 128 W + W_lo count in units of delta / 128; |S'| < 2^20
+// for 48 cells, so thresholds are clamped to +-2^21 and an accumulator stays
+// below 2^29.
+constexpr int kCThrMax = 1 << 21;
 constexpr int kCWaves = 4;       // waves per workgroup
 constexpr int kCThreads = kCWaves * kWave;
 
@@ -70,7 +75,7 @@ struct alignas(16) CellPlan {
   int A, rg, C, ok;        // active channels, row groups, cells, the unit fits this pass
   int np[4];               // cells of plane p: the channels of depth > p
   int base[5];             // first cell of plane p (base[4] = C)
-  double Ku, Eabs;         // E = delta Ku + Eabs
+  double Kc, Kch, Eabs;    // E = unit Kc + delta Kch + Eabs (unit: delta, or delta / 128 for fine weights)
   uint32_t rrow[kCG][2];   // row group g: plane rows 4 j + p of its 4 cells (16-bit halves, kCPad: none)
   float qrg[kCG][4][4];    // row group g, head h, cell k: -q 2^-p of the cell (0 past the cells and for heads >= G)
   int cx[kCC];             // cell -> proxy index of its channel (0 past the cells)
@@ -89,11 +94,12 @@ struct alignas(16) FilterLds {
   uint64_t raw[Geo::C][4];                        // the quad's plane words: cell, block
   uint32_t zero[Geo::G];                          // zero dwords (the A operand of lanes that carry no weights)
   uint32_t W[4][4][Geo::G];                       // int8 weights: block of the quad, head, row group
+  uint32_t Wlo[Geo::Fine ? 4 : 1][4][Geo::G];     // fine weights: the residual weights W_lo, likewise
   int32_t ini[4][2][4][4];                        // accumulator starts: block, nibble, mu, head
   uint16_t scl[Geo::Slots][kCSB][Geo::SclRow];    // fp16 scales: ring slot, block, cell (its channel's scale)
   uint32_t qx[Geo::G][kCQ];                       // queued keys' staged dwords (digits while re-scored): dword, entry
   uint32_t qi[kCQ];                       // queued key index
-  uint32_t qf[kCQ];                       // pos | slot << 3 | block of the group << 8 | head h at bit 7 + 8 h
+  uint32_t qf[kCQ];                       // pos | slot << 3 (3 bits) | block of the group << 8 | head h at bit 7 + 8 h
   uint64_t sv[4][kSv];                    // survivors per head not yet appended to the row's list
 };
 
@@ -181,7 +187,8 @@ __device__ __forceinline__ void cell_plan(CellPlan& P, const FusedArgs& a, const
     }
     P.base[kPlanes] = C;
     const double cells = (double)C;
-    P.Ku = (cells / 4.0 + (double)A * (double)A * 127.0 * 0x1p-24) * (1.0 + 0x1p-20);
+    P.Kc = cells / 4.0 * (1.0 + 0x1p-20);
+    P.Kch = (double)A * (double)A * 127.0 * 0x1p-24 * (1.0 + 0x1p-20);
     P.Eabs = (double)A * 0x1p-120;
   }
   if (!ok) {
@@ -386,13 +393,18 @@ __device__ __forceinline__ v2i ctr_read(const FilterLds<NS>& L, uint32_t src_off
 // Lanes (block b = lane >> 4 of the quad, head h = (lane >> 2) & 3, part =
 // lane & 3): the negated int8 weights -W of row groups g = part (mod 4) of
 // block b for head h, their sum, and the accumulator starts of (b, h).  With
-// M0 = 1.5 2^(23 + e) the low byte of fl(-q 2^-p a16 + M0) is rne(-q a16 2^-p
-// / delta) as a two's complement byte.  Pad cells (q = 0) get weight 0; a
-// group without thresholds (a head past G, no tau, no valid delta) gets fixed
-// starts that no sum of products can cross (|S 2^pos| < 2^21), whatever its
-// weights.
+// M0 = 1.5 2^(23 + e) the low byte of r = fl(-q 2^-p a16 + M0) is
+// W = rne(-q a16 2^-p / delta) as a two's complement byte.  Fine weights add
+// W_lo: with K1 = M0 (1 + 2^-7), K1 - r = M0 / 128 - W delta exactly, and the
+// low byte of fl(-q 2^-p a16 + (K1 - r)) is the residual rounded in units of
+// delta / 128 (|W_lo| <= 64), so W' = 128 W + W_lo is the cell's weight
+// rounded to delta / 128 with one rounding.  Pad cells (q = 0) get weight 0;
+// a group without thresholds (a head past G, no tau, no valid delta) gets
+// fixed starts that no sum of products can cross (|S' 2^pos| < 2^27),
+// whatever its weights.
 struct CHead {
   float M0;     // rounding constant, 1.5 2^(23 + e)
+  float K1;     // M0 (1 + 2^-7): fine weights
   int X;        // floor(2 (tau - E) / delta) - 1, clamped
   bool m0;      // thresholds apply
   int c0, c1;   // the starts of positions 2 part and 2 part + 1 when they do not
@@ -412,7 +424,7 @@ __device__ __forceinline__ void cquad_weights(const CellPlan& P, FilterLds<NS>& 
     s01[k] = *reinterpret_cast<const uint32_t*>(&srow[4 * g]);
     s23[k] = *reinterpret_cast<const uint32_t*>(&srow[4 * g + 2]);
   }
-  int wsum = 0;
+  int wsum = 0, wlo = 0;
   const float Mp = H.M0;
 #pragma unroll
   for (int k = 0; k < NS; ++k) {
@@ -424,13 +436,24 @@ __device__ __forceinline__ void cquad_weights(const CellPlan& P, FilterLds<NS>& 
     const uint32_t wd = __builtin_amdgcn_perm(r1, r0, 0x0c0c0400u) | __builtin_amdgcn_perm(r3, r2, 0x04000c0cu);
     L.W[b][h][g] = wd;
     wsum = __builtin_amdgcn_sdot4((int)wd, 0x01010101, wsum, false);
+    if constexpr (CGeo<NS>::Fine) {
+      const float c0 = H.K1 - __uint_as_float(r0), c1 = H.K1 - __uint_as_float(r1);
+      const float c2 = H.K1 - __uint_as_float(r2), c3 = H.K1 - __uint_as_float(r3);
+      const uint32_t l0 = __float_as_uint(__fmaf_rn(qv[k].x, a0, c0)), l1 = __float_as_uint(__fmaf_rn(qv[k].y, a1, c1));
+      const uint32_t l2 = __float_as_uint(__fmaf_rn(qv[k].z, a2, c2)), l3 = __float_as_uint(__fmaf_rn(qv[k].w, a3, c3));
+      const uint32_t wl = __builtin_amdgcn_perm(l1, l0, 0x0c0c0400u) | __builtin_amdgcn_perm(l3, l2, 0x04000c0cu);
+      L.Wlo[b][h][g] = wl;
+      wlo = __builtin_amdgcn_sdot4((int)wl, 0x01010101, wlo, false);
+    }
   }
+  if constexpr (CGeo<NS>::Fine) wsum = wsum * 128 + wlo;  // -sum W' of the lane's cells
   wsum += dpp_i<0xB1>(wsum);  // quad_perm [1,0,3,2]
   wsum += dpp_i<0x4E>(wsum);  // quad_perm [2,3,0,1]: -Wsum of (b, h)
   // part writes the starts of positions 2 part, 2 part + 1 (nibble hb = part >> 1);
   // position 7 is part 3's second
+  constexpr int tm = CGeo<NS>::Fine ? kCThrMax : kThrMax;
   int thr = (H.X - wsum) >> 1;
-  thr = thr < -kThrMax ? -kThrMax : thr > kThrMax ? kThrMax : thr;
+  thr = thr < -tm ? -tm : thr > tm ? tm : thr;
   const int hb = part >> 1, mu0 = 2 * (part & 1);
   const int t0 = thr * (1 << (4 * hb + mu0)), t1 = thr * (1 << (4 * hb + mu0 + 1));
   L.ini[b][hb][mu0][h] = H.m0 ? t0 - 1 : H.c0;
@@ -464,7 +487,7 @@ __device__ __forceinline__ void crescore(const CellPlan& P, FilterLds<NS>& L, co
   const int e = on ? lane : 0;
   const uint32_t ki = L.qi[e], f = L.qf[e];
   const uint32_t pos = f & 7u, hm = on ? f : 0u;
-  const int slot = (int)((f >> 3) & 3u), blk = (int)((f >> 8) & 7u);
+  const int slot = (int)((f >> 3) & 7u), blk = (int)((f >> 8) & 7u);
   uint32_t* ent = &L.qx[0][e];  // dword i of the entry at ent[i * kCQ] (entries side by side: no bank conflicts)
   // digit dword i (proxy channels 4 i .. 4 i + 3): the plane-p bits of its
   // channels are cells base_p + 4 i .., bytes (base_p & 3) .. of row group
@@ -591,6 +614,7 @@ __device__ __forceinline__ void cwave_run(const CellPlan& P, FilterLds<NS>& L, c
   const uint32_t src_off = (uint32_t)((((lane & 15) >> 1) * 4 + bq) * 8);
   // the A operand: this lane's weights, or zeros
   const uint32_t* wsrc = wl ? &L.W[bq][lane & 3][0] : &L.zero[0];
+  const uint32_t* wlsrc = wl && Geo::Fine ? &L.Wlo[Geo::Fine ? bq : 0][lane & 3][0] : &L.zero[0];
   const uint64_t ubase = reinterpret_cast<uint64_t>(a.planes + (int64_t)u * kD * kPlanes * a.nb_cap);
   const uint32_t ubytes = (uint32_t)(kD * kPlanes * 8) * (uint32_t)a.nb_cap;
   CStage S;
@@ -632,15 +656,35 @@ __device__ __forceinline__ void cwave_run(const CellPlan& P, FilterLds<NS>& L, c
     v4i wv[NS];
 #pragma unroll
     for (int s2 = 0; s2 < NS; ++s2) wv[s2] = *reinterpret_cast<const v4i*>(wsrc + 4 * s2);
+    if constexpr (Geo::Fine) {
+      // key position outer, slices inner: the W chain of one position at a
+      // time, scaled by 128 into the W_lo chain that started at the thresholds
+      v4i wlv[NS];
 #pragma unroll
-    for (int s2 = 0; s2 < NS; ++s2) {
-      v4i bv[4];
+      for (int s2 = 0; s2 < NS; ++s2) wlv[s2] = *reinterpret_cast<const v4i*>(wlsrc + 4 * s2);
 #pragma unroll
-      for (int mu = 0; mu < 4; ++mu)
-        bv[mu] = v4i{(int)(xr[4 * s2] & mk[mu]), (int)(xr[4 * s2 + 1] & mk[mu]), (int)(xr[4 * s2 + 2] & mk[mu]),
-                     (int)(xr[4 * s2 + 3] & mk[mu])};
+      for (int mu = 0; mu < 4; ++mu) {
+        v4i ah = v4i{0, 0, 0, 0};
 #pragma unroll
-      for (int mu = 0; mu < 4; ++mu) acc[mu] = __builtin_amdgcn_mfma_i32_16x16x64_i8(wv[s2], bv[mu], acc[mu], 0, 0, 0);
+        for (int s2 = 0; s2 < NS; ++s2) {
+          const v4i bv = v4i{(int)(xr[4 * s2] & mk[mu]), (int)(xr[4 * s2 + 1] & mk[mu]), (int)(xr[4 * s2 + 2] & mk[mu]),
+                             (int)(xr[4 * s2 + 3] & mk[mu])};
+          ah = __builtin_amdgcn_mfma_i32_16x16x64_i8(wv[s2], bv, ah, 0, 0, 0);
+          acc[mu] = __builtin_amdgcn_mfma_i32_16x16x64_i8(wlv[s2], bv, acc[mu], 0, 0, 0);
+        }
+        acc[mu] = acc[mu] + ah * 128;
+      }
+    } else {
+#pragma unroll
+      for (int s2 = 0; s2 < NS; ++s2) {
+        v4i bv[4];
+#pragma unroll
+        for (int mu = 0; mu < 4; ++mu)
+          bv[mu] = v4i{(int)(xr[4 * s2] & mk[mu]), (int)(xr[4 * s2 + 1] & mk[mu]), (int)(xr[4 * s2 + 2] & mk[mu]),
+                       (int)(xr[4 * s2 + 3] & mk[mu])};
+#pragma unroll
+        for (int mu = 0; mu < 4; ++mu) acc[mu] = __builtin_amdgcn_mfma_i32_16x16x64_i8(wv[s2], bv[mu], acc[mu], 0, 0, 0);
+      }
     }
     // candidates: this lane's eligible keys (all four inside the window but
     // at the unit's edges), and per key its candidate heads
@@ -710,14 +754,17 @@ __device__ __forceinline__ void cwave_run(const CellPlan& P, FilterLds<NS>& L, c
       sched_fence();
       const float th = P.tau[hq];
       H.M0 = ldexpf(12582912.0f, dl.e);  // 1.5 * 2^(23 + e)
+      H.K1 = ldexpf(12582912.0f * (1.0f + 0x1p-7f), dl.e);
       H.X = 0;
       const bool none = hq >= a.G || th == kNegInf;  // no key of this head is a candidate
       H.m0 = !none && dl.valid;
       if (H.m0) {
-        const double E = ldexp(P.Ku, dl.e) + P.Eabs;
-        double X = ldexp((double)th - E, 1 - dl.e);  // 2 (tau - E) / delta
+        const int eu = Geo::Fine ? dl.e - 7 : dl.e;  // the weights' unit: delta, or delta / 128
+        const double E = ldexp(P.Kc, eu) + ldexp(P.Kch, dl.e) + P.Eabs;
+        double X = ldexp((double)th - E, 1 - eu);  // 2 (tau - E) / unit
         X = floor(X) - 1.0;
-        X = X < -2.0 * kThrMax ? -2.0 * kThrMax : X > 2.0 * kThrMax ? 2.0 * kThrMax : X;
+        constexpr double xm = 2.0 * (Geo::Fine ? kCThrMax : kThrMax);
+        X = X < -xm ? -xm : X > xm ? xm : X;
         H.X = (int)X;
       }
       // no thresholds: every key a candidate (no valid delta) or none
