@@ -817,8 +817,19 @@ __device__ __forceinline__ float ctau(const FusedArgs& a, const float (&sv)[kCTa
   uint32_t m = m_s > 0u ? (5u * kk * m_s + 4u * m_e - 1u) / (4u * m_e) + 16u : 0u;
   if (m > (uint32_t)nv) m = 10ull * (uint64_t)nv * m_e >= 11ull * kk * m_s ? (uint32_t)nv : 0u;
   if (m == 0u) return kNegInf;
-  uint32_t prefix = 0u;
-  for (int bit = 31; bit >= 16; --bit) {
+  // the leading bits shared by the largest and the smallest sample are the
+  // answer's too (m <= nv): the search starts below them
+  uint32_t ext[4] = {0u, 0u, 0u, 0u};  // largest key, ~smallest (nonzero) key
+#pragma unroll
+  for (int x = 0; x < kCTauPer; ++x) {
+    ext[0] = max(ext[0], key[x]);
+    ext[1] = max(ext[1], key[x] != 0u ? ~key[x] : 0u);
+  }
+  wave_max4_u(ext);
+  const uint32_t kmax = ext[0], kmin = ~ext[1];
+  const int top = kmax == kmin ? -1 : 31 - __builtin_clz(kmax ^ kmin);  // highest differing bit
+  uint32_t prefix = top < 16 ? kmax & 0xFFFF0000u : kmax & ~((2u << top) - 1u);
+  for (int bit = top; bit >= 16; --bit) {
     const uint32_t cand = prefix | (1u << bit);
     uint32_t c = 0u;
 #pragma unroll
