@@ -49,18 +49,19 @@ constexpr int kCA = 48;          // active channels at most
 constexpr int kCSB = 8;          // blocks per group (one delta per head; one loop iteration)
 constexpr int kCQ = 64;          // queued candidates per wave (one ballot fits)
 constexpr int kCFlush = 64;      // re-score at a quad boundary once the queue is full
-constexpr int kSv = 16;          // survivors per head buffered in LDS before a list append
+constexpr int kSv = 8;           // survivors per head buffered in LDS before a list append
 
 // Geometry of an instantiation with NS slices of 4 row groups (16 cells):
 // NS = 3 serves units of at most 48 cells, NS = 4 of at most 64.  The scale
 // ring holds one row of C + 2 halfs per block (an odd number of dwords, so
 // the lanes of a re-scoring batch fall in different banks) for Slots groups;
-// three workgroups per CU fit the LDS with 5 slots at NS = 3 and 3 at NS = 4.
+// three workgroups per CU fit the LDS with 6 slots at NS = 3 (a wave's 6
+// groups of the 2^20-token layer: no flush before its end) and 3 at NS = 4.
 template <int NS>
 struct CGeo {
   static constexpr int G = 4 * NS;
   static constexpr int C = 4 * G;
-  static constexpr int Slots = NS == 3 ? 5 : 3;
+  static constexpr int Slots = NS == 3 ? 6 : 3;
   static constexpr int SclRow = C + 2;
   static constexpr bool Fine = NS == 3;  // two-level weights (the registers fit them at three slices)
 };
