@@ -748,17 +748,19 @@ __device__ __forceinline__ void unit_reset(const FusedArgs& a, int u, int t, int
 // scores of its keys (Sec. 3.2-3.3: prefix dequantisation, fma over the
 // active channels ascending from +0, as the re-scoring of the full pass);
 // per head, the two largest scores of each block are its samples (-inf where
-// the block has fewer eligible keys).  A wave stages its block's plane words
-// in LDS, one lane per (channel, plane) cell, and every lane then reads them
-// back as broadcasts and takes its own key's bit.  Workgroup 0 of each unit
-// also sets the rows' call state (unit_reset).
+// the block has fewer eligible keys).  The thread of each active channel
+// loads its plane words and scales for the workgroup's 4 blocks as soon as
+// it knows its depth and stores them in LDS by the channel's ascending
+// position; every lane then reads its block's words back as broadcasts and
+// takes its own key's bit.  Workgroup 0 of each unit also sets the rows'
+// call state (unit_reset).
 typedef unsigned int v4u __attribute__((ext_vector_type(4)));
 struct alignas(16) SampleLds {
   uint32_t act[kD];                  // ascending position -> channel | depth << 8 (0 on padding)
   float q[kD][4];                    // q by ascending position and head (0 past G and on padding)
   float zo[kD];                      // -(1 - 2^-t): khat = (u / 8 + zo) a16, exact (0 on padding)
-  uint32_t w[kFW][2][kD * kPlanes];  // the block's plane words, dword half h of cell 4 y + p
-  uint16_t sc[kFW][kD];              // the block's scales by ascending position (0 on padding)
+  uint32_t w[kFW][2][kD * kPlanes];  // block b's plane words, dword half h of cell 4 y + p
+  uint16_t sc[kFW][kD];              // block b's scales by ascending position (0 on padding)
   int cnt[2];                        // active channels of channels 0..63, 64..127
 };
 
@@ -773,6 +775,18 @@ __global__ __launch_bounds__(kFT) void fused_sample_kernel(FusedArgs a) {
 #pragma unroll
     for (int h = 0; h < 4; ++h)
       if (h < G) qv[h] = load_q(a.q, a.qdt, ((int64_t)u * G + h) * kD + tid);
+  }
+  // this channel's words and scales for the workgroup's blocks (0 past the store)
+  const int64_t blk0 = (int64_t)blockIdx.x * a.ws.s_stride * kQB;
+  uint64_t wd[kQB][kPlanes];
+  uint16_t scv[kQB];
+#pragma unroll
+  for (int b = 0; b < kQB; ++b) {
+    const bool inb = tid < kD && t > 0 && blk0 + b < a.nb_cap;
+    scv[b] = inb ? gload(a.scales + ((int64_t)u * kD + tid) * a.nb_cap + blk0 + b) : (uint16_t)0;
+#pragma unroll
+    for (int p = 0; p < kPlanes; ++p)
+      wd[b][p] = inb && p < t ? gload(a.planes + (((int64_t)u * kD + tid) * kPlanes + p) * a.nb_cap + blk0 + b) : 0ull;
   }
   int64_t nu, lo, hi;
   row_window(a, u, &nu, &lo, &hi, false);
@@ -789,6 +803,15 @@ __global__ __launch_bounds__(kFT) void fused_sample_kernel(FusedArgs a) {
 #pragma unroll
     for (int h = 0; h < 4; ++h) S.q[y][h] = qv[h];
     S.zo[y] = -(1.0f - ldexpf(1.0f, -t));
+#pragma unroll
+    for (int b = 0; b < kQB; ++b) {
+      S.sc[b][y] = scv[b];
+#pragma unroll
+      for (int p = 0; p < kPlanes; ++p) {
+        S.w[b][0][4 * y + p] = (uint32_t)wd[b][p];
+        S.w[b][1][4 * y + p] = (uint32_t)(wd[b][p] >> 32);
+      }
+    }
   }
   const int A4 = (A + 3) & ~3;  // the chain in steps of 4 channels; padding adds +0 to every score
   if (tid >= A && tid < A4) {
@@ -796,11 +819,13 @@ __global__ __launch_bounds__(kFT) void fused_sample_kernel(FusedArgs a) {
 #pragma unroll
     for (int h = 0; h < 4; ++h) S.q[tid][h] = 0.0f;
     S.zo[tid] = 0.0f;
+#pragma unroll
+    for (int b = 0; b < kQB; ++b) S.sc[b][tid] = 0;
   }
   __syncthreads();
   if (A == 0) return;  // no filter for the unit
   const int64_t nbu = (nu + kBlockTokens - 1) / kBlockTokens;
-  const int64_t blk = (int64_t)blockIdx.x * a.ws.s_stride * kQB + wave;
+  const int64_t blk = blk0 + wave;
   const int64_t key = blk * kBlockTokens + lane;
   const bool el = blk < nbu && key >= lo && key < hi;
   float* dst = a.ws.samp + (int64_t)u * G * kSmpRow + (int64_t)blockIdx.x * kSmpW + 2 * wave;
@@ -808,19 +833,6 @@ __global__ __launch_bounds__(kFT) void fused_sample_kernel(FusedArgs a) {
     if (lane < 2 * G) gstore(dst + (int64_t)(lane >> 1) * kSmpRow + (lane & 1), kNegInf);
     return;
   }
-  // stage the block's words: cell c = 4 y + p (p < t_y) and the scales
-  const uint64_t* pu = a.planes + (int64_t)u * kD * kPlanes * a.nb_cap;
-  for (int c = lane; c < 4 * A; c += kWave) {
-    const uint32_t e = S.act[c >> 2];
-    if ((c & 3) < (int)(e >> 8)) {
-      const uint64_t v = gload(pu + ((int64_t)(e & 0xFFu) * kPlanes + (c & 3)) * a.nb_cap + blk);
-      S.w[wave][0][c] = (uint32_t)v;
-      S.w[wave][1][c] = (uint32_t)(v >> 32);
-    }
-  }
-  for (int y = lane; y < A4; y += kWave)
-    S.sc[wave][y] = y < A ? gload(a.scales + ((int64_t)u * kD + (S.act[y] & 0xFFu)) * a.nb_cap + blk) : (uint16_t)0;
-  wave_lds_sync();
   // this lane's key: the documented chain, 4 channels a step (every read of a
   // step first); a channel's four plane words (of this lane's half) are one
   // 16-byte read, the planes past its depth masked off its digit
