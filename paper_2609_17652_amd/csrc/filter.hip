@@ -872,6 +872,9 @@ __global__ __launch_bounds__(kCThreads, 3) void fused_filter_kernel(FusedArgs a,
   const int64_t glo = lo / (kCSB * kBlockTokens);
   const int64_t ghi = (hi + kCSB * kBlockTokens - 1) / (kCSB * kBlockTokens);
   if (g0 >= ghi || g1 <= glo) return;
+  // tau of this wave's row first: it needs only the samples and the window,
+  // and runs while the plan's loads are in flight
+  const float tv = wave < G ? ctau(a, sv, lo, hi) : kNegInf;
   cell_plan(P, a, pre);
   if (!P.ok || P.C > CGeo<NS>::C) return;  // more cells than the caller's bound allowed: the exact path
   // this wave: groups g0 + wave + kCWaves i inside the window (ng = 0: none)
@@ -879,12 +882,10 @@ __global__ __launch_bounds__(kCThreads, 3) void fused_filter_kernel(FusedArgs a,
   if (gf < glo) gf += (glo - gf + kCWaves - 1) / kCWaves * kCWaves;
   const int64_t gend = ghi < g1 ? ghi : g1;
   const int ng = gf < gend ? (int)((gend - gf + kCWaves - 1) / kCWaves) : 0;
-  // tau while the first loads are in flight: every workgroup finds the same
-  // values; the one holding the window's first quad leaves them for the rank
-  // pass
+  // every workgroup finds the same tau; the one holding the window's first
+  // group leaves it for the rank pass
   auto ready = [&]() -> bool {
     if (wave < G) {
-      const float tv = ctau(a, sv, lo, hi);
       if (lane == 0) {
         P.tau[wave] = tv;
         if (g0 <= glo) gstore(a.ws.tau + u * G + wave, tv);
