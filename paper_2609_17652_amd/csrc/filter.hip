@@ -71,6 +71,7 @@ struct CGeo {
 constexpr int kCThrMax = 1 << 21;
 constexpr int kCWaves = 4;       // waves per workgroup
 constexpr int kCThreads = kCWaves * kWave;
+static_assert(kPools == kCWaves, "one pool counter per wave of a workgroup");
 
 struct alignas(16) CellPlan {
   int A, rg, C, ok;        // active channels, row groups, cells, the unit fits this pass
@@ -462,16 +463,28 @@ __device__ __forceinline__ void cquad_weights(const CellPlan& P, FilterLds<NS>& 
 }
 
 // ---------------------------------------------------------------- survivors
-// Appends the n buffered survivors of head h to row u G + h (one atomic).
+// Appends survivors to the rows' lists: the nb[h] buffered ones of head h and
+// this lane's new one of head h when bit h of `keep` is set (composite
+// comp[h], rank[h] among the wave's new ones, c[h] of them).  One atomic
+// instruction reserves every head's range (lane h for row u G + h), so a
+// flush costs one round trip whatever the number of heads.
 template <int NS>
-__device__ __forceinline__ void cflush_head(FilterLds<NS>& L, const FusedArgs& a, int u, int h, int n) {
+__device__ __forceinline__ void cappend(FilterLds<NS>& L, const FusedArgs& a, int u, const int (&nb)[4], const int (&c)[4],
+                                        uint32_t keep, const uint64_t (&comp)[4], const int (&rank)[4]) {
   const int lane = threadIdx.x & 63, G = a.G;
-  if (n <= 0) return;
+  const int tot = lane == 0 ? nb[0] + c[0] : lane == 1 ? nb[1] + c[1] : lane == 2 ? nb[2] + c[2] : nb[3] + c[3];
   uint32_t base = 0u;
-  if (lane == 0) base = gatomic_add(&a.ws.cnt[(u * G + h) * kCntStride], (uint32_t)n);
-  base = (uint32_t)__shfl((int)base, 0, kWave);
-  if (lane < n && base + lane < (uint32_t)a.ws.lcap)
-    gstore(&a.ws.cand[(int64_t)(u * G + h) * a.ws.lcap + base + lane], L.sv[h][lane]);
+  if (lane < G && tot > 0) base = gatomic_add(&a.ws.cnt[(u * G + lane) * kCntStride], (uint32_t)tot);
+  const uint32_t lcap = (uint32_t)a.ws.lcap;
+#pragma unroll
+  for (int h = 0; h < 4; ++h) {
+    if (nb[h] + c[h] == 0) continue;  // every head past G
+    const uint32_t b = (uint32_t)__builtin_amdgcn_readlane((int)base, h);
+    uint64_t* row = a.ws.cand + (int64_t)(u * G + h) * a.ws.lcap;
+    if (lane < nb[h] && b + (uint32_t)lane < lcap) gstore(&row[b + (uint32_t)lane], L.sv[h][lane]);
+    const uint32_t pos = b + (uint32_t)nb[h] + (uint32_t)rank[h];
+    if (((keep >> h) & 1u) && pos < lcap) gstore(&row[pos], comp[h]);
+  }
 }
 
 // ---------------------------------------------------------------- re-scoring
@@ -548,51 +561,64 @@ __device__ __forceinline__ void crescore(const CellPlan& P, FilterLds<NS>& L, co
       s[3] = __fmaf_rn(q4[c].w, khat, s[3]);
     }
   }
-  // survivors of each head go to the wave's LDS buffer; a full buffer (and
-  // the wave's end) appends it to the row's list with one atomic
+  // survivors of each head go to the wave's LDS buffer; when one head's
+  // would overflow, every head's buffer and new survivors go to the lists
+  // together (one atomic instruction), as at the wave's end
+  int c[4], rk[4];
+  uint64_t comp[4];
+  uint32_t keep = 0u;
+  bool over = false;
 #pragma unroll
   for (int h = 0; h < 4; ++h) {
-    const bool keep = h < G && ((hm >> (7 + 8 * h)) & 1u) && s[h] >= P.tau[h];
-    const uint64_t bm = __ballot(keep);
-    if (bm == 0ull) continue;
-    const int c = __popcll(bm);
-    if (svn[h] + c > kSv) {
-      cflush_head(L, a, u, h, svn[h]);
-      svn[h] = 0;
-    }
-    const uint64_t comp = ((uint64_t)score_key(s[h]) << 32) | (uint64_t)(~ki);
-    const int rank = __popcll(bm & lanes_below(lane));
-    if (c > kSv) {  // more than a buffer at once: straight to the list
-      uint32_t base = 0u;
-      if (lane == 0) base = gatomic_add(&a.ws.cnt[(u * G + h) * kCntStride], (uint32_t)c);
-      base = (uint32_t)__shfl((int)base, 0, kWave);
-      if (keep && base + rank < (uint32_t)a.ws.lcap) gstore(&a.ws.cand[(int64_t)(u * G + h) * a.ws.lcap + base + rank], comp);
-    } else {
-      if (keep) L.sv[h][svn[h] + rank] = comp;
-      svn[h] += c;
+    const bool k = h < G && ((hm >> (7 + 8 * h)) & 1u) && s[h] >= P.tau[h];
+    const uint64_t bm = __ballot(k);
+    c[h] = __popcll(bm);
+    rk[h] = __popcll(bm & lanes_below(lane));
+    comp[h] = ((uint64_t)score_key(s[h]) << 32) | (uint64_t)(~ki);
+    keep |= (uint32_t)k << h;
+    over |= svn[h] + c[h] > kSv;
+  }
+  if (over) {
+    cappend(L, a, u, svn, c, keep, comp, rk);
+#pragma unroll
+    for (int h = 0; h < 4; ++h) svn[h] = 0;
+  } else {
+#pragma unroll
+    for (int h = 0; h < 4; ++h) {
+      if ((keep >> h) & 1u) L.sv[h][svn[h] + rk[h]] = comp[h];
+      svn[h] += c[h];
     }
   }
   lds_order();
 }
 
 // ---------------------------------------------------------------- one wave
-// Groups of 8 blocks of unit u: the ng groups b0 / 8 + kCWaves i (i < ng;
-// the workgroup's waves take its groups in turn, so two waves read the two
-// halves of a 128-byte plane line at about the same time), quad by quad (one
-// loop iteration per group).  `ready` runs once every first load is issued
-// (every wave of the workgroup calls it, so it may hold a barrier); the wave
-// stops if it returns false.  The plane words of a quad are loaded two quads
-// ahead (two register sets), the scales of a group one group ahead, in the
-// same order on every path into the loop so that the compiler's load
-// counters stay exact.  A wave's LDS accesses execute in
-// program order, so staged data is read back without a wait.  Re-scoring
-// runs at one place: after a quad's candidates, when the queue holds kCFlush,
-// when a quad's candidates do not fit, before the ring slot of the oldest
-// queued key is reused, and at the end.
-constexpr int kCStride = kCWaves * kCSB;  // blocks from one group of a wave to its next
-
+// Groups of 8 blocks of unit u: first the wave's ns static groups s0 +
+// kCWaves i (the workgroup's waves take its static groups in turn, so two
+// waves read the two halves of a 128-byte plane line at about the same time),
+// then groups p0 + w + kPools j < pend taken one at a time through counter w
+// of the unit's pool (w: the wave's index in its workgroup; kPools counters,
+// so each sees a quarter of the atomics), quad by quad (one loop iteration
+// per group).  Waves of one SIMD
+// progress at unequal rates (older waves issue first), so the pool lets the
+// faster ones take more of the unit.  `ready` runs once every first load is
+// issued (every wave of the workgroup calls it, so it may hold a barrier); the
+// wave stops if it returns false.  The plane words of a quad are loaded one
+// group ahead (two register sets), the scales of a group one group ahead, in
+// the same order on every path into the loop so that the compiler's load
+// counters stay exact (a load with nothing to fetch reads past its range);
+// the pool's counter is read a group before the group it names is loaded.  A
+// wave's LDS accesses execute in program order, so staged data is read back
+// without a wait.  Re-scoring runs at one place: after a quad's candidates,
+// when the queue holds kCFlush, when a quad's candidates do not fit, before
+// the ring slot of the oldest queued key is reused, and at the end.
+struct CGroups {
+  int s0, ns;     // static groups s0 + kCWaves i, i < ns
+  int p0, pend;   // the unit's pool of groups
+  int ctr;        // the pool counter of this wave: word ctr of the pool counters (-1: no pool)
+};
 template <bool VEC, int NS, class Ready>
-__device__ __forceinline__ void cwave_run(const CellPlan& P, FilterLds<NS>& L, const FusedArgs& a, int u, int b0, int ng,
+__device__ __forceinline__ void cwave_run(const CellPlan& P, FilterLds<NS>& L, const FusedArgs& a, int u, const CGroups& gs,
                                           int nbu, int lo, int hi, Ready&& ready) {
   using Geo = CGeo<NS>;
   const int lane = threadIdx.x & 63;
@@ -600,7 +626,6 @@ __device__ __forceinline__ void cwave_run(const CellPlan& P, FilterLds<NS>& L, c
   const int kb = 8 * oct + 4 * nib;                      // key of mu = 0 within its block
   const bool wl = ((lane & 15) >> 2) == bq;              // carries weights in the A operand
   const int hq = (lane >> 2) & 3;                        // head of this lane's weights
-  const uint32_t flip = nib ? 0xFFFFFFFFu : 0u;          // mu = 3 sits at pos 7 in nibble 1
   uint32_t mk[4];
 #pragma unroll
   for (int mu = 0; mu < 4; ++mu) mk[mu] = 0x01010101u << (4 * nib + mu);
@@ -608,9 +633,6 @@ __device__ __forceinline__ void cwave_run(const CellPlan& P, FilterLds<NS>& L, c
   const int C = cuni(P.C);
   const int cxl = P.cx[lane];                  // cell `lane`'s channel (proxy index)
   const int srow = lane < C ? P.pj[cxl] : 0;   // its scale row
-  float qv[4];
-#pragma unroll
-  for (int h = 0; h < 4; ++h) qv[h] = lane < C ? P.qx[cxl][h] : 0.0f;
   // as a transpose source: cell (l & 15) >> 1 of pair 0, block l >> 4
   const uint32_t src_off = (uint32_t)((((lane & 15) >> 1) * 4 + bq) * 8);
   // the A operand: this lane's weights, or zeros
@@ -622,24 +644,31 @@ __device__ __forceinline__ void cwave_run(const CellPlan& P, FilterLds<NS>& L, c
   cstage_setup(S, P, a, ubase, ubytes);
   if (lane < Geo::G) L.zero[lane] = 0u;
   int pending = 0, oldest = 0;
+  const int b0 = gs.s0 * kCSB;
+  const bool any = gs.ns > 0;
   int svn[4] = {0, 0, 0, 0};  // buffered survivors per head
   // the issue order here (scales, quad 0, quad 1) is the loop's steady-state
   // order, so the compiler's load counters agree on every path into the loop
   CScl sr;
-  cscl_issue<VEC>(sr, a, u, C, srow, b0, ng > 0);
+  cscl_issue<VEC>(sr, a, u, C, srow, b0, any);
   sched_fence();
   CRaw R0, R1;
-  cstage_issue(R0, S, b0, ng > 0);
+  cstage_issue(R0, S, b0, any);
   sched_fence();
-  cstage_issue(R1, S, b0 + kQB, ng > 0);
+  cstage_issue(R1, S, b0 + kQB, any);
   sched_fence();
   if (!ready()) return;
   CHead H;
   int slot = 0;
+  // gnxt: the group after the current one (-1: none); grab: the pool's
+  // answer for the one after that, requested in the previous iteration
+  int gnxt = gs.ns > 1 ? gs.s0 + kCWaves : -1;
+  bool dry = gs.ctr < 0, asked = false;
+  uint32_t grab = 0u;
   auto quad = [&](CRaw& R, int qb0, int it, int sbq) {  // sbq: first block of the quad within its group
     cstage_write(R, L);
     sched_fence();
-    cstage_issue(R, S, qb0 + kCStride, it + 1 < ng);  // the same quad of the wave's next group
+    cstage_issue(R, S, gnxt * kCSB + sbq, gnxt >= 0);  // the same quad of the wave's next group
     sched_fence();
     cquad_weights(P, L, H, slot, sbq);
     lds_order();
@@ -704,11 +733,13 @@ __device__ __forceinline__ void cwave_run(const CellPlan& P, FilterLds<NS>& L, c
     for (int mu = 0; mu < 4; ++mu) {
       const uint32_t T = __builtin_amdgcn_perm((uint32_t)acc[mu][1], (uint32_t)acc[mu][0], 0x0c0c0703u) |
                          __builtin_amdgcn_perm((uint32_t)acc[mu][3], (uint32_t)acc[mu][2], 0x07030c0cu);
+      // mu = 3 sits at pos 7 in nibble 1: its sign bytes flip
+      const uint32_t flip = (uint32_t)(-(int)((threadIdx.x >> 3) & 1u));
       D |= ((mu == 3 ? T ^ flip : T) & 0x80808080u) >> (7 - mu);
     }
     D &= em * 0x01010101u;
     uint32_t kmask = (D | D >> 8 | D >> 16 | D >> 24) & 0xFu;
-    const bool last = it == ng - 1 && sbq == kCSB - kQB;  // the wave's last quad
+    const bool last = gnxt < 0 && sbq == kCSB - kQB;  // the wave's last quad
     const bool endg = sbq == kCSB - kQB;
     if (__ballot(kmask != 0u) != 0ull && pending == 0) oldest = it;
     const uint32_t meta = (uint32_t)slot << 3 | (uint32_t)(sbq + bq) << 8;
@@ -745,13 +776,33 @@ __device__ __forceinline__ void cwave_run(const CellPlan& P, FilterLds<NS>& L, c
   };
   // one loop iteration = one group of 8 blocks (two quads): its scales and
   // delta, then the quads
-  int it = 0;
-  for (int gb0 = b0; it < ng; gb0 += kCStride, ++it) {
+  int gcur = any ? gs.s0 : -1;
+  for (int it = 0; gcur >= 0; ++it) {
     slot = it % Geo::Slots;
+    const int gb0 = gcur * kCSB;
+    if (it > 0) {  // the group after this one: static, or the pool's answer
+      if (asked) {
+        const int g = gs.p0 + cuni((int)(threadIdx.x >> 6)) + kPools * cuni((int)grab);
+        gnxt = g < gs.pend ? g : -1;
+        dry = gnxt < 0;
+      } else {
+        gnxt = it + 1 < gs.ns ? gs.s0 + kCWaves * (it + 1) : -1;
+      }
+    }
+    // ask the pool for the group after gnxt once the static groups run out
+    asked = !dry && gnxt >= 0 && it + 2 >= gs.ns;
+    if (asked && lane == 0) grab = gatomic_add(a.ws.pool + gs.ctr, 1u);
+    sched_fence();
     {
+      float qv[4];  // q of cell `lane`'s channel (read here: fewer registers live across the loop)
+      {
+        const float4 q4 = *reinterpret_cast<const float4*>(&P.qx[cxl][0]);
+        const bool on = lane < C;
+        qv[0] = on ? q4.x : 0.0f; qv[1] = on ? q4.y : 0.0f; qv[2] = on ? q4.z : 0.0f; qv[3] = on ? q4.w : 0.0f;
+      }
       const CDel dl = cscl_commit(sr, L, slot, hq, qv);
       sched_fence();
-      cscl_issue<VEC>(sr, a, u, C, srow, gb0 + kCStride, it + 1 < ng);
+      cscl_issue<VEC>(sr, a, u, C, srow, gnxt * kCSB, gnxt >= 0);
       sched_fence();
       const float th = P.tau[hq];
       H.M0 = ldexpf(12582912.0f, dl.e);  // 1.5 * 2^(23 + e)
@@ -774,9 +825,11 @@ __device__ __forceinline__ void cwave_run(const CellPlan& P, FilterLds<NS>& L, c
     }
     quad(R0, gb0, it, 0);
     quad(R1, gb0 + kQB, it, kQB);
+    gcur = gnxt;
   }
-#pragma unroll
-  for (int h = 0; h < 4; ++h) cflush_head(L, a, u, h, svn[h]);
+  const int none[4] = {0, 0, 0, 0};
+  const uint64_t nocomp[4] = {0ull, 0ull, 0ull, 0ull};
+  cappend(L, a, u, svn, none, 0u, nocomp, none);
 }
 
 // ---------------------------------------------------------------- tau
@@ -843,52 +896,62 @@ __device__ __forceinline__ float ctau(const FusedArgs& a, const float (&sv)[kCTa
 }
 
 // ---------------------------------------------------------------- kernel
-// Grid (workgroups per unit, U); workgroup x takes the 8-block groups
-// [x kCWaves gpw, (x + 1) kCWaves gpw) of its unit, wave w every kCWaves-th of
-// them from the w-th.  Units of another class (uovf[u] >> 1 != 1: the wide
-// pass, or no filter) and rows computed exactly return at once.
+// Grid (W U): workgroup b takes unit u = b mod U (a unit's workgroups are
+// spread over the dispatch order, so over the workgroup slots of the CUs) as
+// its x = b / U -th.  The unit's window holds NG groups; each wave takes S of
+// them statically, 2/3 of an even share (the workgroup's 4 S groups are
+// consecutive, its waves take them in turn), and the rest form the unit's
+// pool.  With fewer than 2 static groups per wave every group is static.
+// Units of another class (uovf[u] >> 1 != 1: the wide pass, or no filter) and
+// rows computed exactly return at once.
 template <bool VEC, int NS>
-__global__ __launch_bounds__(kCThreads, 3) void fused_filter_kernel(FusedArgs a, int gpw) {
+__global__ __launch_bounds__(kCThreads, 3) void fused_filter_kernel(FusedArgs a, int U, int W) {
   __shared__ CellPlan P;
   __shared__ FilterLds<NS> WL[kCWaves];
-  const int u = blockIdx.y, tid = threadIdx.x, wave = cuni(tid >> 6), lane = tid & 63, G = a.G;
+  const int u = (int)(blockIdx.x % (unsigned)U), x = (int)(blockIdx.x / (unsigned)U);
+  const int tid = threadIdx.x, wave = cuni(tid >> 6), lane = tid & 63, G = a.G;
   const uint32_t uo = gload(a.ws.uovf + u);
   // this wave's row's samples first: tau waits on them
   const int nsm = wave < G ? a.ws.s_quads * kSmpW : 0;
   float sv[kCTauPer];
 #pragma unroll
-  for (int x = 0; x < kCTauPer; ++x) {
-    const int i = lane + kWave * x;
-    sv[x] = i < nsm ? gload(a.ws.samp + (int64_t)(u * G + wave) * kSmpRow + i) : kNegInf;
+  for (int i0 = 0; i0 < kCTauPer; ++i0) {
+    const int i = lane + kWave * i0;
+    sv[i0] = i < nsm ? gload(a.ws.samp + (int64_t)(u * G + wave) * kSmpRow + i) : kNegInf;
   }
   const CellPre pre = cell_load(a, u);
   int64_t nu, lo, hi;
-  row_window(a, u, &nu, &lo, &hi, blockIdx.x == 0 && tid == 0);
+  row_window(a, u, &nu, &lo, &hi, x == 0 && tid == 0);
   if ((uo >> 1) != 1u) return;
   if (hi - lo <= a.ws.cap) return;
   const int64_t nbu = (nu + kBlockTokens - 1) / kBlockTokens;
-  // the workgroup's groups [g0, g1) and the window's [glo, ghi)
-  const int64_t g0 = (int64_t)blockIdx.x * kCWaves * gpw, g1 = g0 + kCWaves * gpw;
-  const int64_t glo = lo / (kCSB * kBlockTokens);
-  const int64_t ghi = (hi + kCSB * kBlockTokens - 1) / (kCSB * kBlockTokens);
-  if (g0 >= ghi || g1 <= glo) return;
+  const int glo = (int)(lo / (kCSB * kBlockTokens));
+  const int NG = (int)((hi + kCSB * kBlockTokens - 1) / (kCSB * kBlockTokens)) - glo;
+  const int per = kCWaves * W;  // waves of the unit
+  int S = (int)((int64_t)NG * 2 / (3 * per)), p0 = NG;
+  if (S >= 2) p0 = S * per;
+  else S = (NG + per - 1) / per;
+  const int sb = x * kCWaves * S;  // the workgroup's first static group
+  if (sb >= NG) return;
   // tau of this wave's row first: it needs only the samples and the window,
   // and runs while the plan's loads are in flight
   const float tv = wave < G ? ctau(a, sv, lo, hi) : kNegInf;
   cell_plan(P, a, pre);
   if (!P.ok || P.C > CGeo<NS>::C) return;  // more cells than the caller's bound allowed: the exact path
-  // this wave: groups g0 + wave + kCWaves i inside the window (ng = 0: none)
-  int64_t gf = g0 + wave;
-  if (gf < glo) gf += (glo - gf + kCWaves - 1) / kCWaves * kCWaves;
-  const int64_t gend = ghi < g1 ? ghi : g1;
-  const int ng = gf < gend ? (int)((gend - gf + kCWaves - 1) / kCWaves) : 0;
-  // every workgroup finds the same tau; the one holding the window's first
-  // group leaves it for the rank pass
+  CGroups gs;  // wave-uniform (read from memory, so held in scalar registers only through readfirstlane)
+  const int rem = NG - sb - wave;
+  gs.s0 = cuni(glo + sb + wave);
+  gs.ns = cuni(rem > 0 ? min(S, (rem + kCWaves - 1) / kCWaves) : 0);
+  gs.p0 = cuni(glo + p0);
+  gs.pend = cuni(glo + NG);
+  gs.ctr = cuni(p0 < NG ? (u * kPools + wave) * kPoolStride : -1);
+  // every workgroup finds the same tau; the first of the unit leaves it for
+  // the rank pass
   auto ready = [&]() -> bool {
     if (wave < G) {
       if (lane == 0) {
         P.tau[wave] = tv;
-        if (g0 <= glo) gstore(a.ws.tau + u * G + wave, tv);
+        if (x == 0) gstore(a.ws.tau + u * G + wave, tv);
       }
     }
     __syncthreads();
@@ -896,27 +959,28 @@ __global__ __launch_bounds__(kCThreads, 3) void fused_filter_kernel(FusedArgs a,
     for (int h = 0; h < G; ++h) any |= P.tau[h] != kNegInf;
     return any;
   };
-  cwave_run<VEC, NS>(P, WL[wave], a, u, (int)(gf * kCSB), ng, (int)nbu, (int)lo, (int)hi, ready);
+  cwave_run<VEC, NS>(P, WL[wave], a, u, gs, (int)nbu, (int)lo, (int)hi, ready);
 }
 
-// Groups per wave: about kFResident waves over all units (three per SIMD of
-// the chip, one round); a workgroup takes kCWaves * gpw consecutive groups.
-constexpr int64_t kFResident = 3 * 4 * 256;
+// Workgroups per unit: about kFResident of them over all units (three per
+// CU, one round), and no more than one group per wave.
+constexpr int64_t kFResident = 3 * 256;
 void launch_filter(const FusedArgs& fa, int U, int max_cells, hipStream_t s) {
   const int64_t ngr = (fa.nb_cap + kCSB - 1) / kCSB;
-  int64_t gpw = ((int64_t)U * ngr + kFResident - 1) / kFResident;
-  if (gpw < 1) gpw = 1;
-  const unsigned wgs = (unsigned)((ngr + kCWaves * gpw - 1) / (kCWaves * gpw));
-  const dim3 grid(wgs, (unsigned)U);
+  int64_t W = kFResident / U;
+  const int64_t wmax = (ngr + kCWaves - 1) / kCWaves;
+  if (W > wmax) W = wmax;
+  if (W < 1) W = 1;
+  const dim3 grid((unsigned)(W * U));
   // 16-byte aligned scale rows: one 16-byte scale load per lane and group
   const bool vec = (fa.nb_cap & 7) == 0 && (reinterpret_cast<uintptr_t>(fa.scales) & 15) == 0;
   // three slices when no unit can have more than 48 cells
   if (max_cells > 0 && max_cells <= CGeo<3>::C) {
-    if (vec) hipLaunchKernelGGL((fused_filter_kernel<true, 3>), grid, dim3(kCThreads), 0, s, fa, (int)gpw);
-    else hipLaunchKernelGGL((fused_filter_kernel<false, 3>), grid, dim3(kCThreads), 0, s, fa, (int)gpw);
+    if (vec) hipLaunchKernelGGL((fused_filter_kernel<true, 3>), grid, dim3(kCThreads), 0, s, fa, U, (int)W);
+    else hipLaunchKernelGGL((fused_filter_kernel<false, 3>), grid, dim3(kCThreads), 0, s, fa, U, (int)W);
   } else {
-    if (vec) hipLaunchKernelGGL((fused_filter_kernel<true, 4>), grid, dim3(kCThreads), 0, s, fa, (int)gpw);
-    else hipLaunchKernelGGL((fused_filter_kernel<false, 4>), grid, dim3(kCThreads), 0, s, fa, (int)gpw);
+    if (vec) hipLaunchKernelGGL((fused_filter_kernel<true, 4>), grid, dim3(kCThreads), 0, s, fa, U, (int)W);
+    else hipLaunchKernelGGL((fused_filter_kernel<false, 4>), grid, dim3(kCThreads), 0, s, fa, U, (int)W);
   }
 }
 

@@ -58,7 +58,8 @@ namespace fathom {
 size_t fused_ws_bytes(int R, int U, int64_t nb_cap, int k) {
   if (nb_cap < 1) nb_cap = 1;
   const size_t xch = (size_t)exact_chunks(nb_cap), pk = (size_t)exact_pk(k);
-  return a256((size_t)R * 4) + a256((size_t)R * kCntStride * 4) + a256((size_t)R * fused_lcap(k) * 8) +
+  return a256((size_t)R * 4) + a256((size_t)R * kCntStride * 4) + a256((size_t)U * kPools * kPoolStride * 4) +
+         a256((size_t)R * fused_lcap(k) * 8) +
          a256((size_t)U * 4) +
          a256((size_t)R * kSmpRow * 4) +
          a256((size_t)(1 + R) * 4) + a256((size_t)R * 4) + a256((size_t)R * xch * pk * 8) + a256((size_t)R * xch * 4) +
@@ -731,6 +732,7 @@ __device__ __forceinline__ void unit_reset(const FusedArgs& a, int u, int t, int
     gstore(a.ws.xctl + 1 + r, 0u);
     gstore(a.ws.tau + r, kNegInf);
   }
+  if (tid < kPools) gstore(a.ws.pool + (u * kPools + tid) * kPoolStride, 0u);
   if (u == 0 && tid == 0) gstore(a.ws.xctl, 0u);
   __syncthreads();
   if (tid == 0) {
