@@ -1082,7 +1082,7 @@ constexpr int kRankXcd = 8;
 __global__ __launch_bounds__(kRankThreads) void fused_rank_kernel(FusedArgs a, int R, int32_t* __restrict__ idx,
                                                                  float* __restrict__ val) {
   __shared__ uint64_t grp[kRankCap];
-  __shared__ uint32_t hist[kRankSub + 1];
+  __shared__ __align__(16) uint32_t hist[kRankSub + 1];
   __shared__ uint32_t s_red[2][kRankThreads / kWave], s_part[kRankThreads / kWave];
   __shared__ uint32_t s_first[kRankParts + 1];  // part z: sub-buckets [s_first[z], s_first[z + 1])
   __shared__ uint32_t s_c, s_ovf;
@@ -1139,11 +1139,11 @@ __global__ __launch_bounds__(kRankThreads) void fused_rank_kernel(FusedArgs a, i
     kmin = key < kmin ? key : kmin;
     kmax = key > kmax ? key : kmax;
   });
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) {
-    const uint32_t m0 = __shfl_xor(kmin, o, kWave), m1 = __shfl_xor(kmax, o, kWave);
-    kmin = m0 < kmin ? m0 : kmin;
-    kmax = m1 > kmax ? m1 : kmax;
+  {
+    uint32_t mm[4] = {kmax, ~kmin, 0u, 0u};  // the smallest key as the largest complement
+    wave_max4_u(mm);
+    kmax = mm[0];
+    kmin = ~mm[1];
   }
   if (lane == 0) {
     s_red[0][wave] = kmin;
@@ -1171,32 +1171,52 @@ __global__ __launch_bounds__(kRankThreads) void fused_rank_kernel(FusedArgs a, i
   // the sub-bucket whose positions cross b_z.
   const uint32_t K = c < k ? c : k;
   {
+    constexpr int kPerMax = kRankSub / kRankThreads;
+    static_assert(kPerMax == 8, "two 16-byte runs per thread");
     const int per = ns / kRankThreads > 0 ? ns / kRankThreads : 1;
     const int x0 = tid * per;
-    uint32_t run = 0;
-    for (int x = 0; x < per; ++x)
-      if (x0 + x < ns) run += hist[x0 + x];
-    uint32_t inc = run;
+    uint32_t hv[kPerMax];  // this thread's run of sub-buckets (0 past it)
+    if (per == 8) {
+      const uint4 h0 = *reinterpret_cast<const uint4*>(&hist[x0]), h1 = *reinterpret_cast<const uint4*>(&hist[x0 + 4]);
+      hv[0] = h0.x; hv[1] = h0.y; hv[2] = h0.z; hv[3] = h0.w;
+      hv[4] = h1.x; hv[5] = h1.y; hv[6] = h1.z; hv[7] = h1.w;
+    } else {
 #pragma unroll
-    for (int o = 1; o < kWave; o <<= 1) {
-      const uint32_t t = __shfl_up(inc, o, kWave);
-      if (lane >= o) inc += t;
+      for (int x = 0; x < kPerMax; ++x) hv[x] = x < per && x0 + x < ns ? hist[x0 + x] : 0u;
     }
+    uint32_t run = 0;
+#pragma unroll
+    for (int x = 0; x < kPerMax; ++x) run += hv[x];
+    const uint32_t inc = wave_incl_scan_u(run);
     if (lane == kWave - 1) s_part[wave] = inc;
     __syncthreads();
     uint32_t acc = inc - run;
     for (int x = 0; x < wave; ++x) acc += s_part[x];
-    for (int x = 0; x < per; ++x)
-      if (x0 + x < ns) {
-        const uint32_t h0 = hist[x0 + x];
-        hist[x0 + x] = acc;
+    const uint32_t a0 = acc;
+    uint32_t ov[kPerMax];  // exclusive prefix of each sub-bucket
 #pragma unroll
-        for (int zz = 1; zz <= kRankParts; ++zz) {
-          const uint32_t b = (uint32_t)(((uint64_t)zz * K) / kRankParts);
-          if (acc < b && acc + h0 >= b) s_first[zz] = (uint32_t)(x0 + x + 1);
-        }
-        acc += h0;
+    for (int x = 0; x < kPerMax; ++x) {
+      ov[x] = acc;
+      acc += hv[x];
+    }
+    if (per == 8) {
+      *reinterpret_cast<uint4*>(&hist[x0]) = make_uint4(ov[0], ov[1], ov[2], ov[3]);
+      *reinterpret_cast<uint4*>(&hist[x0 + 4]) = make_uint4(ov[4], ov[5], ov[6], ov[7]);
+    } else {
+#pragma unroll
+      for (int x = 0; x < kPerMax; ++x)
+        if (x < per && x0 + x < ns) hist[x0 + x] = ov[x];
+    }
+    // part bounds b = zz K / parts inside this thread's positions [a0, acc]
+#pragma unroll
+    for (int zz = 1; zz <= kRankParts; ++zz) {
+      const uint32_t b = (uint32_t)(((uint64_t)zz * K) / kRankParts);
+      if (a0 < b && acc >= b) {
+#pragma unroll
+        for (int x = 0; x < kPerMax; ++x)
+          if (ov[x] < b && ov[x] + hv[x] >= b) s_first[zz] = (uint32_t)(x0 + x + 1);
       }
+    }
     if (tid == 0) {
       hist[ns] = c;
 #pragma unroll

@@ -219,6 +219,19 @@ __device__ __forceinline__ void wave_max4_u(uint32_t (&v)[4]) {
   }
 }
 
+// Inclusive prefix sum over the wave: within rows of 16 lanes by shifted
+// adds, then rows 1 and 3 add the last lane of the row before, and rows 2 and
+// 3 the last lane of row 1.
+__device__ __forceinline__ uint32_t wave_incl_scan_u(uint32_t v) {
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x111, 0xF, 0xF, false);  // row_shr 1
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x112, 0xF, 0xF, false);  // row_shr 2
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x114, 0xF, 0xF, false);  // row_shr 4
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x118, 0xF, 0xF, false);  // row_shr 8
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x142, 0xA, 0xF, false);  // row_bcast 15
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x143, 0xC, 0xF, false);  // row_bcast 31
+  return v;
+}
+
 // The full pass over the units of class 1 (filter.hip); max_cells: the
 // caller's bound on a unit's depth bits (0: none), which picks the geometry.
 void launch_filter(const FusedArgs& fa, int U, int max_cells, hipStream_t s);
