@@ -51,7 +51,7 @@
 #include <type_traits>
 #include <mutex>
 
-#include "fused.hpp"
+#include "cellplan.hpp"
 
 namespace fathom {
 
@@ -59,6 +59,7 @@ size_t fused_ws_bytes(int R, int U, int64_t nb_cap, int k) {
   if (nb_cap < 1) nb_cap = 1;
   const size_t xch = (size_t)exact_chunks(nb_cap), pk = (size_t)exact_pk(k);
   return a256((size_t)R * 4) + a256((size_t)R * kCntStride * 4) + a256((size_t)U * kPools * kPoolStride * 4) +
+         (size_t)U * kPlanBytes +
          a256((size_t)R * fused_lcap(k) * 8) +
          a256((size_t)U * 4) +
          a256((size_t)R * kSmpRow * 4) +
@@ -755,7 +756,8 @@ __device__ __forceinline__ void unit_reset(const FusedArgs& a, int u, int t, int
 // it knows its depth and stores them in LDS by the channel's ascending
 // position; every lane then reads its block's words back as broadcasts and
 // takes its own key's bit.  Workgroup 0 of each unit also sets the rows'
-// call state (unit_reset).
+// call state (unit_reset) and builds the unit's cell plan for the filter in
+// the workspace while its plane words load.
 typedef unsigned int v4u __attribute__((ext_vector_type(4)));
 struct alignas(16) SampleLds {
   uint32_t act[kD];                  // ascending position -> channel | depth << 8 (0 on padding)
@@ -792,7 +794,17 @@ __global__ __launch_bounds__(kFT) void fused_sample_kernel(FusedArgs a) {
   }
   int64_t nu, lo, hi;
   row_window(a, u, &nu, &lo, &hi, false);
-  if (blockIdx.x == 0) unit_reset(a, u, t, lo, hi);
+  if (blockIdx.x == 0) {  // the unit's call state and its cell plan for the filter, while the words load
+    unit_reset(a, u, t, lo, hi);
+    __shared__ CellPlan P;
+    CellPre pre;
+    pre.t = t;
+#pragma unroll
+    for (int h = 0; h < 4; ++h) pre.q[h] = qv[h];
+    cell_plan(P, a, pre);
+    if (tid * 16 < (int)sizeof(CellPlan))
+      gstore(reinterpret_cast<PlanWord*>(a.ws.plan + (size_t)u * kPlanBytes) + tid, reinterpret_cast<const PlanWord*>(&P)[tid]);
+  }
   if (hi - lo <= a.ws.cap) return;  // computed directly by the exact pass
   // the active channels in ascending order
   const uint64_t on = __ballot(tid < kD && t > 0);

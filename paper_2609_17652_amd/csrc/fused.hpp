@@ -21,6 +21,7 @@ constexpr int kSmpW = 8;           // sample proxies kept per (sampled wave, hea
 constexpr int kSampleQuads = 64;   // at most this many sampled quads per unit
 constexpr int kSmpRow = kSampleQuads * kSmpW;
 constexpr int kCntStride = 64;     // survivor counters one 256-byte line apart (device-scope atomics)
+constexpr size_t kPlanBytes = 4096;  // workspace slot of a unit's cell plan
 constexpr int kPools = 4;          // cell filter: group pools per unit (one per wave of a workgroup)
 constexpr int kPoolStride = 32;    // pool counters one 128-byte line apart
 constexpr int kSelCap = 16384;     // rows with at most this many eligible keys are computed exactly
@@ -38,6 +39,7 @@ struct FusedWs {
   float* tau;       // [R] threshold on exact scores (-inf: the row is computed exactly by pass 5)
   uint32_t* cnt;    // [R][kCntStride] word 0: survivors appended to the row's list (counted past its capacity too)
   uint32_t* pool;   // [U][kPools][kPoolStride] word 0: groups taken from the cell filter's pool
+  unsigned char* plan;  // [U][kPlanBytes] the cell filter's plan of each unit (built by the sample pass)
   uint64_t* cand;   // [R][lcap] survivors in append order: score_key << 32 | ~index
   uint32_t* uovf;   // [U] from pass 2: (slices of the unit's filter, at least kNarrow + 1 for the wide pass) << 1, 0 = no filter
   float* samp;      // [R][kSmpRow] sampled proxies
@@ -123,6 +125,7 @@ static FusedWs fused_carve(void* ws, int R, int U, int64_t nb_cap, int k) {
   w.tau = reinterpret_cast<float*>(p); p += a256((size_t)R * 4);
   w.cnt = reinterpret_cast<uint32_t*>(p); p += a256((size_t)R * kCntStride * 4);
   w.pool = reinterpret_cast<uint32_t*>(p); p += a256((size_t)U * kPools * kPoolStride * 4);
+  w.plan = reinterpret_cast<unsigned char*>(p); p += (size_t)U * kPlanBytes;
   w.cand = reinterpret_cast<uint64_t*>(p); p += a256((size_t)R * w.lcap * 8);
   w.uovf = reinterpret_cast<uint32_t*>(p); p += a256((size_t)U * 4);
   w.samp = reinterpret_cast<float*>(p); p += a256((size_t)R * kSmpRow * 4);
