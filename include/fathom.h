@@ -201,7 +201,11 @@ size_t fathom_topk_workspace_size(int U, int G, int64_t max_n, int k);
  * the same outputs bit for bit (same scores, same order rules), without the
  * score array as an output.  This is the decode-step scan.
  *   ws       device workspace of at least
- *            fathom_scan_topk_workspace_size(U, G, max_n, k) bytes.
+ *            fathom_scan_topk_workspace_size(U, G, max_n, k) bytes (any
+ *            contents: every call sets the state it reads).
+ * The filter that spares most keys their exact score serves units of at most
+ * 4 query heads per KV head; with G > 4 every row takes the exact path (the
+ * same outputs; TOPK_FALLBACK is raised).
  * Device status: NONFINITE, TOPK_SHORT, TOPK_FALLBACK, BAD_N.
  */
 fathom_status fathom_scan_topk(const uint64_t* planes, const uint16_t* scales, const int64_t* n,

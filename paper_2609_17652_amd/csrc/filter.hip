@@ -720,9 +720,7 @@ __device__ __forceinline__ float ctau(const FusedArgs& a, const float (&sv)[kCTa
     const int64_t x0 = k0 > lo ? k0 : lo, x1 = k1 < hi ? k1 : hi;
     m_s += x1 > x0 ? (uint32_t)(x1 - x0) : 0u;
   }
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) m_s += (uint32_t)__shfl_xor((int)m_s, o, kWave);
-  m_s = (uint32_t)cuni((int)m_s);
+  m_s = (uint32_t)__builtin_amdgcn_readlane((int)wave_incl_scan_u(m_s), kWave - 1);
   const uint32_t m_e = (uint32_t)(hi - lo), kk = (uint32_t)a.k;
   uint32_t m = m_s > 0u ? (5u * kk * m_s + 4u * m_e - 1u) / (4u * m_e) + 16u : 0u;
   if (m > (uint32_t)nv) m = 10ull * (uint64_t)nv * m_e >= 11ull * kk * m_s ? (uint32_t)nv : 0u;
