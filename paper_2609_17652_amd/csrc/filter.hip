@@ -804,7 +804,7 @@ __global__ __launch_bounds__(kCThreads, 3) void fused_filter_kernel(FusedArgs a,
   gs.pend = cuni(glo + NG);
   gs.ctr = cuni(p0 < NG ? (u * kPools + wave) * kPoolStride : -1);
   // every workgroup finds the same tau; the first of the unit leaves it for
-  // the rank pass
+  // the select pass
   auto ready = [&]() -> bool {
     if (wave < G) {
       if (lane == 0) {

@@ -20,6 +20,10 @@
 // A key is a candidate for head h iff proxy + E >= tau_h, i.e.
 //   S >= thr = floor((floor((tau - E) 16 / delta) - 1 + b) / 2).
 //
+// That proxy is the wide full pass below (units of more than 48 active
+// channels or 16 row groups); the cell filter (filter.hip) serves the others
+// with a per-cell proxy.
+//
 // Mapping to CDNA4.  A wave handles 4 blocks ("quad", 256 keys) at a time.
 // Lane l owns octet m = (l >> 1) & 7, half hb = l & 1 of block l >> 4, i.e.
 // keys 8m + 4hb + mu, mu = 0..3.  Row groups (one plane p of the 4 proxy
@@ -37,16 +41,19 @@
 // scored exactly (channels ascending, scales kept in an LDS ring) and the keys
 // with score >= tau are appended to their row's survivor list.
 //
-// Passes: (1) sample: exact scores of every s-th quad, the 2 largest per
-// (block, head); (2) per row, tau = the m-th largest sample, m ~ 1.25 k *
-// sampled / eligible + 16; (3) the full pass above; (4) 8 workgroups per row share out
-// its top k positions by a histogram of the survivors' scores and order their
-// share in LDS; (5) rows with at most 2k + 2048 eligible keys, and rows whose
+// Passes (launches): (1) sample: exact scores of every s-th quad, the 2
+// largest per (block, head), and per unit the rows' call state and the cell
+// plan; (2) tau, only for the wide pass or G > 4: per row the m-th largest
+// sample, m ~ 1.25 k sampled / eligible + 16 (the cell filter finds the same
+// tau itself); (3) the full pass: the cell filter, and the wide pass above
+// when launched; (4) select: 8 workgroups per row share out its top k
+// positions by a histogram of the survivors' scores and order their share in
+// LDS, and rows with at most 2k + 2048 eligible keys, and rows whose
 // survivors cannot give the top k (fewer than k reached tau, the list
 // overflowed, or too many equal scores for one workgroup's share;
 // FATHOM_DEV_TOPK_FALLBACK), are computed from exact scores by a chunked
-// selection.  The result never depends on tau; it only decides how much work
-// is saved.
+// selection in the same launch.  The result never depends on tau; it only
+// decides how much work is saved.
 #include <atomic>
 #include <type_traits>
 #include <mutex>
@@ -63,7 +70,7 @@ size_t fused_ws_bytes(int R, int U, int64_t nb_cap, int k) {
          a256((size_t)R * fused_lcap(k) * 8) +
          a256((size_t)U * 4) +
          a256((size_t)R * kSmpRow * 4) +
-         a256((size_t)(1 + R) * 4) + a256((size_t)R * 4) + a256((size_t)R * xch * pk * 8) + a256((size_t)R * xch * 4) +
+         a256((size_t)(1 + R) * 4) + a256((size_t)R * xch * pk * 8) + a256((size_t)R * xch * 4) +
          a256((size_t)R * xch * 8);
 }
 
@@ -577,7 +584,7 @@ __device__ void wave_run(const Plan& P, WaveLdsT<NSLM, SQB, RQ, QCAP>& W, const 
   constexpr int NCH = NSLM > 4 ? 2 : 1;
   constexpr int kFlushAt = QCAP * 3 / 4;
   const int lane = threadIdx.x & 63;
-  const int nsl = uni(P.nsl), ndw = uni(P.ndw), stride = 4 * nsl;
+  const int nsl = uni(P.nsl), stride = 4 * nsl;
   const int kb = 8 * ((lane >> 1) & 7) + 4 * (lane & 1);  // key of mu = 0 within the block
   const int lb = lane >> 4;                              // block of the quad
   const bool wl = ((lane & 15) >> 2) == lb;              // carries weights in the A operand
@@ -734,7 +741,6 @@ __device__ __forceinline__ void unit_reset(const FusedArgs& a, int u, int t, int
     gstore(a.ws.tau + r, kNegInf);
   }
   if (tid < kPools) gstore(a.ws.pool + (u * kPools + tid) * kPoolStride, 0u);
-  if (u == 0 && tid == 0) gstore(a.ws.xctl, 0u);
   __syncthreads();
   if (tid == 0) {
     int sc[kPlanes + 1];
@@ -924,7 +930,6 @@ __global__ __launch_bounds__(kTauThreads) void fused_tau_kernel(FusedArgs a) {
   if (tid == 0) {
     a.ws.cnt[r * kCntStride] = 0u;
     a.ws.xctl[1 + r] = 0u;
-    if (r == 0) a.ws.xctl[0] = 0u;
   }
   int64_t nu, lo, hi;
   row_window(a, u, &nu, &lo, &hi, false);
@@ -1021,7 +1026,7 @@ __global__ __launch_bounds__(kFT) void fused_main_kernel(FusedArgs a) {
                                            hi);
 }
 
-// ---------------------------------------------------------------- pass 4
+// ---------------------------------------------------------------- select: ranks
 // Bitonic sort of buf[0..P) (P a power of two) into descending order; every
 // thread owns whole compare-exchange pairs, all loads of a stage issued first.
 __device__ void bitonic_desc(uint64_t* buf, int P) {
@@ -1069,7 +1074,7 @@ __device__ __forceinline__ float key_to_score(uint32_t key) {
   return __uint_as_float((key & 0x80000000u) ? (key & 0x7FFFFFFFu) : ~key);
 }
 
-// Pass 4 (filtered rows).  The row's survivor list holds its top k exactly
+// Ranks of filtered rows.  The row's survivor list holds its top k exactly
 // when at least k keys survived, the list kept them all (the count goes on
 // past the capacity) and the filter ran for the row.  Its top K = min(c, k)
 // output positions are shared by kRankParts workgroups: each reads the c
@@ -1081,29 +1086,38 @@ __device__ __forceinline__ float key_to_score(uint32_t key) {
 // in [z K / parts, (z + 1) K / parts) and orders their survivors in LDS; only
 // survivors sharing a sub-bucket are compared.  Composites are distinct (they
 // carry the index), so the positions are a permutation.  A row whose share
-// for some part exceeds kRankCap (many equal scores) goes to pass 5 with the
-// rows that the list cannot serve; every part reaches the same decision from
-// the same histogram.  The parts of a row run on one XCD (workgroups are
-// dealt to the 8 XCDs in turn), so the list is read once into that XCD's L2.
+// for some part exceeds kRankCap (many equal scores) is computed exactly by
+// its own parts instead; every part reaches the same decision from the same
+// histogram.  The parts of a row run on one XCD (workgroups are dealt to the
+// 8 XCDs in turn), so the list is read once into that XCD's L2.
 constexpr int kRankParts = 8;
-constexpr int kRankThreads = 512;
+constexpr int kRankThreads = 1024;  // the select pass's workgroup
 constexpr int kRankPer = 8;      // survivors per thread read with the count (the rest re-read)
 constexpr int kRankCap = 4096;   // survivors one part orders at most
 constexpr int kRankSub = 4096;   // sub-buckets at most
 constexpr int kRankXcd = 8;
-__global__ __launch_bounds__(kRankThreads) void fused_rank_kernel(FusedArgs a, int R, int32_t* __restrict__ idx,
-                                                                 float* __restrict__ val) {
-  __shared__ uint64_t grp[kRankCap];
-  __shared__ __align__(16) uint32_t hist[kRankSub + 1];
-  __shared__ uint32_t s_red[2][kRankThreads / kWave], s_part[kRankThreads / kWave];
-  __shared__ uint32_t s_first[kRankParts + 1];  // part z: sub-buckets [s_first[z], s_first[z + 1])
-  __shared__ uint32_t s_c, s_ovf;
-  __shared__ float s_tau;
-  __shared__ int64_t s_n;
+struct RankShared {
+  uint32_t s_red[2][kRankThreads / kWave], s_part[kRankThreads / kWave];
+  uint32_t s_first[kRankParts + 1];  // part z: sub-buckets [s_first[z], s_first[z + 1])
+  uint32_t s_c, s_ovf;
+  float s_tau;
+  int64_t s_n;
+};
+// Part z of row r (every thread of the workgroup calls it, for a row whose
+// list holds its top k); grp and hist are LDS areas of kRankCap composites
+// and kRankSub + 1 counts, 16-byte aligned.  Returns true when a part's share
+// exceeds kRankCap after all (many equal scores): the row is then computed
+// exactly.
+__device__ bool rank_part(const FusedArgs& a, int r, int z, int32_t* __restrict__ idx, float* __restrict__ val,
+                          uint64_t* grp, uint32_t* hist, RankShared& RS) {
+  auto& s_red = RS.s_red;
+  auto& s_part = RS.s_part;
+  auto& s_first = RS.s_first;
+  auto& s_c = RS.s_c;
+  auto& s_ovf = RS.s_ovf;
+  auto& s_tau = RS.s_tau;
+  auto& s_n = RS.s_n;
   const int G = a.G;
-  const int w = blockIdx.x, j = w / kRankXcd;
-  const int z = j % kRankParts, r = (j / kRankParts) * kRankXcd + w % kRankXcd;
-  if (r >= R) return;
   const int u = r / G, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int lcap = a.ws.lcap;
   const uint64_t* src = a.ws.cand + (int64_t)r * lcap;
@@ -1125,16 +1139,7 @@ __global__ __launch_bounds__(kRankThreads) void fused_rank_kernel(FusedArgs a, i
   const uint32_t c = s_c, k = (uint32_t)a.k;
   const bool direct = hi - lo <= a.ws.cap;
   const bool complete = c >= k && c <= (uint32_t)lcap && (s_ovf & 1u) == 0u && s_tau != kNegInf;
-  auto list_exact = [&]() {
-    if (z == 0 && tid == 0) {
-      const uint32_t jx = gatomic_add(a.ws.xctl, 1u);
-      gstore(a.ws.xrows + jx, (uint32_t)r | (direct ? kXDirect : 0u));
-    }
-  };
-  if (direct || !complete) {
-    list_exact();
-    return;
-  }
+  if (direct || !complete) return false;  // the caller's row test rules this out
   // visits every survivor: the first kRankPer per thread from registers
   auto each = [&](auto fn) {
 #pragma unroll
@@ -1184,14 +1189,16 @@ __global__ __launch_bounds__(kRankThreads) void fused_rank_kernel(FusedArgs a, i
   const uint32_t K = c < k ? c : k;
   {
     constexpr int kPerMax = kRankSub / kRankThreads;
-    static_assert(kPerMax == 8, "two 16-byte runs per thread");
+    static_assert(kPerMax % 4 == 0, "16-byte runs per thread");
     const int per = ns / kRankThreads > 0 ? ns / kRankThreads : 1;
     const int x0 = tid * per;
     uint32_t hv[kPerMax];  // this thread's run of sub-buckets (0 past it)
-    if (per == 8) {
-      const uint4 h0 = *reinterpret_cast<const uint4*>(&hist[x0]), h1 = *reinterpret_cast<const uint4*>(&hist[x0 + 4]);
-      hv[0] = h0.x; hv[1] = h0.y; hv[2] = h0.z; hv[3] = h0.w;
-      hv[4] = h1.x; hv[5] = h1.y; hv[6] = h1.z; hv[7] = h1.w;
+    if (per == kPerMax) {
+#pragma unroll
+      for (int v = 0; v < kPerMax / 4; ++v) {
+        const uint4 h = *reinterpret_cast<const uint4*>(&hist[x0 + 4 * v]);
+        hv[4 * v] = h.x; hv[4 * v + 1] = h.y; hv[4 * v + 2] = h.z; hv[4 * v + 3] = h.w;
+      }
     } else {
 #pragma unroll
       for (int x = 0; x < kPerMax; ++x) hv[x] = x < per && x0 + x < ns ? hist[x0 + x] : 0u;
@@ -1211,9 +1218,10 @@ __global__ __launch_bounds__(kRankThreads) void fused_rank_kernel(FusedArgs a, i
       ov[x] = acc;
       acc += hv[x];
     }
-    if (per == 8) {
-      *reinterpret_cast<uint4*>(&hist[x0]) = make_uint4(ov[0], ov[1], ov[2], ov[3]);
-      *reinterpret_cast<uint4*>(&hist[x0 + 4]) = make_uint4(ov[4], ov[5], ov[6], ov[7]);
+    if (per == kPerMax) {
+#pragma unroll
+      for (int v = 0; v < kPerMax / 4; ++v)
+        *reinterpret_cast<uint4*>(&hist[x0 + 4 * v]) = make_uint4(ov[4 * v], ov[4 * v + 1], ov[4 * v + 2], ov[4 * v + 3]);
     } else {
 #pragma unroll
       for (int x = 0; x < kPerMax; ++x)
@@ -1240,12 +1248,9 @@ __global__ __launch_bounds__(kRankThreads) void fused_rank_kernel(FusedArgs a, i
   bool over = false;
 #pragma unroll
   for (int x = 0; x < kRankParts; ++x) over |= hist[s_first[x + 1]] - hist[s_first[x]] > (uint32_t)kRankCap;
-  if (over) {
-    list_exact();
-    return;
-  }
+  if (over) return true;
   const int s0 = (int)s_first[z], s1 = (int)s_first[z + 1];
-  if (s0 == s1) return;
+  if (s0 == s1) return false;
   const uint32_t start = hist[s0], share = hist[s1] - start;
   __syncthreads();  // every part bound read before hist[s0 .. s1) serve as cursors
   each([&](uint64_t v) {  // group by sub-bucket; hist[s] ends at the group's end
@@ -1264,12 +1269,13 @@ __global__ __launch_bounds__(kRankThreads) void fused_rank_kernel(FusedArgs a, i
       if (val) val[(int64_t)r * k + rank] = key_to_score((uint32_t)(v >> 32));
     }
   }
+  return false;
 }
 
-// ---------------------------------------------------------------- pass 5
-// The exact pass: the rows pass 4 listed (direct rows, and rows whose survivor
-// lists do not determine the top k) are computed from exact documented scores.
-// Workgroup (z, s) takes chunk z of the listed rows s, s + kXSlots, ...: the
+// ---------------------------------------------------------------- exact rows
+// Rows whose survivor lists do not determine the top k (direct rows too) are
+// computed from exact documented scores, chunk by chunk (the select pass
+// below hands out the chunks): the
 // exact scores of the chunk's keys go to LDS (kXKeys at a time), and the
 // chunk's top min(k, keys) composites (score key << 32 | ~index) to its
 // partial list; the workgroup that completes a row's last chunk selects the
@@ -1278,7 +1284,7 @@ __global__ __launch_bounds__(kRankThreads) void fused_rank_kernel(FusedArgs a, i
 // so the result is the documented top k whatever the chunking.
 constexpr int kXThreads = 1024;
 constexpr int kXWaves = kXThreads / kWave;  // blocks scored per stage, one per wave
-constexpr int kXSlots = 4;                  // listed rows in flight (grid y)
+constexpr int kXSlots = 4;                  // exact rows in flight (workgroups per chunk index)
 constexpr int kXMaxCells = kD * kPlanes;    // (channel, plane) cells of a unit at most
 constexpr int kXPre = kXMaxCells * kXWaves / kXThreads;  // plane words staged per thread at most
 constexpr int kXPreS = kD * kXWaves / kXThreads;         // scales staged per thread at most
@@ -1341,9 +1347,12 @@ __device__ __forceinline__ uint64_t key_composite(uint32_t key, int64_t i) {
   return ((uint64_t)key << 32) | (uint64_t)(~(uint32_t)i);
 }
 
-__global__ __launch_bounds__(kXThreads) void fused_exact_kernel(FusedArgs a, int32_t* __restrict__ idx,
-                                                                float* __restrict__ val) {
-  extern __shared__ __align__(16) unsigned char xl[];
+// Chunk z of row r computed exactly (every thread of the workgroup calls
+// it): the chunk's top composites go to the row's partial list z, and the
+// workgroup that completes the row's last chunk merges them and writes the
+// row.  xl: the dynamic LDS (kXLdsBytes).
+__device__ void exact_chunk(const FusedArgs& a, int r, int z, int32_t* __restrict__ idx, float* __restrict__ val,
+                            unsigned char* xl, XShared& S) {
   uint32_t* keys = reinterpret_cast<uint32_t*>(xl);
   uint32_t* stw = reinterpret_cast<uint32_t*>(xl + kXLdsKeys);
   uint64_t* sel = reinterpret_cast<uint64_t*>(xl + kXLdsKeys);  // a pass's selection (stw is free then)
@@ -1353,22 +1362,19 @@ __global__ __launch_bounds__(kXThreads) void fused_exact_kernel(FusedArgs a, int
   uint32_t* crow = reinterpret_cast<uint32_t*>(qa + kD);  // cell c: plane row 4 j + p | slot 4 a + p << 9
   uint32_t* hist = reinterpret_cast<uint32_t*>(xl + kXLdsKeys + kXLdsStw + kXLdsSts + kXLdsTab);
   uint64_t* mbuf = reinterpret_cast<uint64_t*>(xl);  // merge: candidates [0, 2 FATHOM_MAX_K - k), then the top k
-  __shared__ XShared S;
-  const int z = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int G = a.G, k = a.k, pk = a.ws.pk;
-  const uint32_t nx = gload(a.ws.xctl);
-  for (uint32_t j = blockIdx.y; j < nx; j += gridDim.y) {
-    const uint32_t code = gload(a.ws.xrows + j);
-    const int r = (int)(code & ~kXDirect), u = r / G, h = r % G;
-    const bool direct = (code & kXDirect) != 0u;
+  {
+    const int u = r / G, h = r % G;
     int64_t nu, lo, hi;
     row_window(a, u, &nu, &lo, &hi, false);
+    const bool direct = hi - lo <= a.ws.cap;
     const int64_t bfirst = lo / kBlockTokens, bend = hi > lo ? (hi + kBlockTokens - 1) / kBlockTokens : bfirst;
     const int64_t rb = bend - bfirst;  // blocks holding eligible keys
     int nz = (int)((rb + kXBlocks - 1) / kXBlocks);
     if (nz > a.ws.xch) nz = a.ws.xch;
     if (nz < 1) nz = 1;
-    if (z >= nz) continue;
+    if (z >= nz) return;
     const int64_t cbk = (rb + nz - 1) / nz;  // blocks per chunk
     const int64_t cb0 = bfirst + z * cbk, cb1 = cb0 + cbk < bend ? cb0 + cbk : bend;
     // ---- the row's active channels ascending, their q, and their cells: cell
@@ -1413,7 +1419,7 @@ __global__ __launch_bounds__(kXThreads) void fused_exact_kernel(FusedArgs a, int
     const uint16_t* Su = a.scales + (int64_t)u * kD * a.nb_cap;
     uint32_t lcnt = 0;      // composites in this chunk's partial list so far
     uint64_t lsplit = 0ull; // its top min(lcnt, xs) composites are those >= lsplit
-    uint64_t* plist = a.ws.part + ((int64_t)j * a.ws.xch + z) * pk;
+    uint64_t* plist = a.ws.part + ((int64_t)r * a.ws.xch + z) * pk;
     for (int64_t pb0 = cb0; pb0 < cb1; pb0 += kXBlocks) {  // passes of at most kXKeys keys
       const int64_t pb1 = pb0 + kXBlocks < cb1 ? pb0 + kXBlocks : cb1;
       // ---- exact scores of blocks [pb0, pb1) into keys[]: 16 blocks per stage
@@ -1535,14 +1541,14 @@ __global__ __launch_bounds__(kXThreads) void fused_exact_kernel(FusedArgs a, int
       __syncthreads();
     }
     if (tid == 0) {
-      gstore(a.ws.pcnt + (int64_t)j * a.ws.xch + z, lcnt);
-      gstore(a.ws.pmin + (int64_t)j * a.ws.xch + z, lsplit);
+      gstore(a.ws.pcnt + (int64_t)r * a.ws.xch + z, lcnt);
+      gstore(a.ws.pmin + (int64_t)r * a.ws.xch + z, lsplit);
     }
     // ---- arrive; the last chunk of the row merges
     __threadfence();
     __syncthreads();
     if (tid == 0) {
-      const uint32_t prev = __hip_atomic_fetch_add((__attribute__((address_space(1))) uint32_t*)(a.ws.xctl + 1 + j),
+      const uint32_t prev = __hip_atomic_fetch_add((__attribute__((address_space(1))) uint32_t*)(a.ws.xctl + 1 + r),
                                                    1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
       S.last = prev == (uint32_t)(nz - 1) ? 1u : 0u;
     }
@@ -1550,7 +1556,7 @@ __global__ __launch_bounds__(kXThreads) void fused_exact_kernel(FusedArgs a, int
     if (S.last) {
       __threadfence();
       if (tid < nz) {
-        const int64_t o = (int64_t)j * a.ws.xch + tid;
+        const int64_t o = (int64_t)r * a.ws.xch + tid;
         S.pc[tid] = __hip_atomic_load((__attribute__((address_space(1))) uint32_t*)(a.ws.pcnt + o), __ATOMIC_RELAXED,
                                       __HIP_MEMORY_SCOPE_AGENT);
         S.ps[tid] = __hip_atomic_load((__attribute__((address_space(1))) uint64_t*)(a.ws.pmin + o), __ATOMIC_RELAXED,
@@ -1561,7 +1567,7 @@ __global__ __launch_bounds__(kXThreads) void fused_exact_kernel(FusedArgs a, int
         S.above = 0u;
       }
       __syncthreads();
-      const uint64_t* rl = a.ws.part + (int64_t)j * a.ws.xch * pk;
+      const uint64_t* rl = a.ws.part + (int64_t)r * a.ws.xch * pk;
       const uint32_t xs = (uint32_t)exact_split(k, nz);
       const uint32_t capm = (uint32_t)(2 * FATHOM_MAX_K - exact_pow2(k));  // candidates in LDS at most
       uint64_t* top = mbuf + capm;                              // the row's top k, then ordered
@@ -1665,7 +1671,87 @@ __global__ __launch_bounds__(kXThreads) void fused_exact_kernel(FusedArgs a, int
       if (__syncthreads_or(shortfall) && tid == 0) set_status(a.st, FATHOM_DEV_TOPK_SHORT);
       if (tid == 0 && !direct) set_status(a.st, FATHOM_DEV_TOPK_FALLBACK);
     }
-    __syncthreads();  // LDS reused by the next listed row
+    __syncthreads();  // LDS reused by the caller's next chunk
+  }
+}
+
+// Whether row r is computed exactly: a direct row (at most cap eligible keys),
+// or a row whose survivor list does not hold its top k (fewer than k
+// survivors, more than the list holds, the unit's overflow flag, no tau).
+// The rank part decides the same from the same values.
+__device__ __forceinline__ bool row_exact(const FusedArgs& a, int r) {
+  const int u = r / a.G;
+  int64_t nu = gload(a.n + u);
+  if (nu < 0 || nu > a.nb_cap * kBlockTokens) nu = 0;
+  int64_t lo = a.lo, hi = nu - a.tail;
+  if (hi < lo) hi = lo;
+  if (hi - lo <= a.ws.cap) return true;
+  const uint32_t c = gload(a.ws.cnt + r * kCntStride), ovf = gload(a.ws.uovf + u);
+  const float tau = gload(a.ws.tau + r);
+  return !(c >= (uint32_t)a.k && c <= (uint32_t)a.ws.lcap && (ovf & 1u) == 0u && tau != kNegInf);
+}
+
+// The select pass: ranks and exact rows in one launch.  Workgroup b < rank_wg
+// is part z of row r of the ranks above unless the row is computed exactly;
+// a part that finds its share too large computes the row's chunks z,
+// z + kRankParts, ... itself.  Workgroup b < xch kXSlots then takes chunk b mod xch of the rows computed
+// exactly with list index s, s + kXSlots, ... (s = b / xch): it marks the
+// rows 1024 at a time (the same marks in every workgroup: they follow from
+// the filter's counts, tau and flags) and counts them in row order.
+static_assert(kRankThreads == kXThreads, "one workgroup shape for both parts");
+static_assert((size_t)kRankCap * 8 + ((size_t)kRankSub + 4) * 4 <= kXLdsBytes, "the rank part's LDS inside the exact part's");
+__global__ __launch_bounds__(kXThreads) void fused_select_kernel(FusedArgs a, int R, int rank_wg,
+                                                                 int32_t* __restrict__ idx, float* __restrict__ val) {
+  extern __shared__ __align__(16) unsigned char xl[];
+  __shared__ XShared S;
+  __shared__ RankShared RS;
+  __shared__ uint32_t cflg[kXThreads / 32];  // bit i: row r0 + i is computed exactly
+  __shared__ int s_ex;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, b = (int)blockIdx.x;
+  // marks of rows [r0, r0 + 1024) into cflg (every thread)
+  auto mark = [&](int r0) {
+    const uint64_t bm = __ballot(r0 + tid < R && row_exact(a, r0 + tid));
+    if (lane == 0) {
+      cflg[2 * wave] = (uint32_t)bm;
+      cflg[2 * wave + 1] = (uint32_t)(bm >> 32);
+    }
+  };
+  mark(0);  // the first rows' marks now: their loads overlap the rank part's
+  if (b < rank_wg) {
+    const int j = b / kRankXcd, z = j % kRankParts, r = (j / kRankParts) * kRankXcd + b % kRankXcd;
+    if (r < R) {
+      if (r >= kXThreads && tid == 0) s_ex = row_exact(a, r) ? 1 : 0;
+      __syncthreads();
+      const bool ex = r < kXThreads ? ((cflg[r >> 5] >> (r & 31)) & 1u) != 0u : s_ex != 0;
+      if (!ex) {
+        const bool over = rank_part(a, r, z, idx, val, reinterpret_cast<uint64_t*>(xl),
+                                    reinterpret_cast<uint32_t*>(xl + (size_t)kRankCap * 8), RS);
+        __syncthreads();
+        if (over)
+          for (int zz = z; zz < a.ws.xch; zz += kRankParts) exact_chunk(a, r, zz, idx, val, xl, S);
+      }
+    }
+  }
+  const int xch = a.ws.xch, zz = b % xch, s = b / xch;
+  if (s >= kXSlots) return;
+  int before = 0;  // rows computed exactly below r0
+  for (int r0 = 0; r0 < R; r0 += kXThreads) {
+    if (r0 > 0) {
+      __syncthreads();  // the marks of the previous rows are read
+      mark(r0);
+    }
+    __syncthreads();
+    int cnt = 0;
+    for (int x = 0; x < kXThreads / 32; ++x) cnt += __popc(cflg[x]);
+    // list indexes jl = s (mod kXSlots) among this run's rows
+    for (int jl = before + (s - before % kXSlots + kXSlots) % kXSlots; jl < before + cnt; jl += kXSlots) {
+      int x = 0, left = jl - before;
+      while (left >= __popc(cflg[x])) left -= __popc(cflg[x++]);
+      uint32_t w = cflg[x];
+      for (; left > 0; --left) w &= w - 1u;
+      exact_chunk(a, r0 + 32 * x + __builtin_ctz(w), zz, idx, val, xl, S);
+    }
+    before += cnt;
   }
 }
 
@@ -1700,7 +1786,7 @@ fathom_status launch_scan_topk_fused(const uint64_t* planes, const uint16_t* sca
   }
   const uint64_t bit = dev < 64 ? 1ull << dev : 0ull;
   if (!bit || !(attr_set.load(std::memory_order_acquire) & bit)) {
-    if (hipFuncSetAttribute(reinterpret_cast<const void*>(&fused_exact_kernel),
+    if (hipFuncSetAttribute(reinterpret_cast<const void*>(&fused_select_kernel),
                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)kXLdsBytes) != hipSuccess) {
       (void)hipGetLastError();
       return FATHOM_ERR_HIP;
@@ -1726,7 +1812,7 @@ fathom_status launch_scan_topk_fused(const uint64_t* planes, const uint16_t* sca
   // a unit with at most 48 depth bits has A <= 48 channels and at most
   // 4 + 48 / 4 = 16 row groups: the narrow pass takes every unit, and the
   // wide launches are skipped.  (A unit above the caller's bound is left to the
-  // exact path of pass 4.)
+  // exact rows of the select pass.)
   const bool wide = !(max_unit_bits > 0 && max_unit_bits <= 16 * kNarrow && nb_cap < kOneNbMax);
   if (G <= 4)
     hipLaunchKernelGGL(fused_sample_kernel, dim3((unsigned)fa.ws.s_quads, (unsigned)U), dim3(kFT), 0, s, fa);
@@ -1742,9 +1828,9 @@ fathom_status launch_scan_topk_fused(const uint64_t* planes, const uint16_t* sca
     }
   }
   const unsigned rank_wg = (unsigned)((R + kRankXcd - 1) / kRankXcd) * kRankXcd * kRankParts;
-  hipLaunchKernelGGL(fused_rank_kernel, dim3(rank_wg), dim3(kRankThreads), 0, s, fa, R, idx, val);
-  hipLaunchKernelGGL(fused_exact_kernel, dim3((unsigned)fa.ws.xch, (unsigned)kXSlots), dim3(kXThreads), kXLdsBytes,
-                     s, fa, idx, val);
+  const unsigned xg = (unsigned)fa.ws.xch * (unsigned)kXSlots;
+  hipLaunchKernelGGL(fused_select_kernel, dim3(rank_wg > xg ? rank_wg : xg), dim3(kXThreads), kXLdsBytes, s, fa, R,
+                     (int)rank_wg, idx, val);
   FATHOM_LAUNCH_CHECK();
   return FATHOM_OK;
 }

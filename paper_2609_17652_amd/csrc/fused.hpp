@@ -36,15 +36,14 @@ constexpr int64_t kOneNbMax = ((int64_t)1 << 20) - 4096;  // cell filter: byte o
 constexpr float kNegInf = -__builtin_huge_valf();
 
 struct FusedWs {
-  float* tau;       // [R] threshold on exact scores (-inf: the row is computed exactly by pass 5)
+  float* tau;       // [R] threshold on exact scores (-inf: the row is computed exactly)
   uint32_t* cnt;    // [R][kCntStride] word 0: survivors appended to the row's list (counted past its capacity too)
   uint32_t* pool;   // [U][kPools][kPoolStride] word 0: groups taken from the cell filter's pool
   unsigned char* plan;  // [U][kPlanBytes] the cell filter's plan of each unit (built by the sample pass)
   uint64_t* cand;   // [R][lcap] survivors in append order: score_key << 32 | ~index
   uint32_t* uovf;   // [U] from pass 2: (slices of the unit's filter, at least kNarrow + 1 for the wide pass) << 1, 0 = no filter
   float* samp;      // [R][kSmpRow] sampled proxies
-  uint32_t* xctl;   // [1 + R]: exact rows listed by pass 4, then per listed row the chunks merged so far
-  uint32_t* xrows;  // [R] rows the exact pass computes: row | kXDirect (direct rows) in list order
+  uint32_t* xctl;   // [1 + R] word 1 + r: chunks of row r merged so far (exact rows; word 0 unused)
   uint64_t* part;   // [R][xch][pk] per listed row and chunk: the chunk's top pk composites
   uint32_t* pcnt;   // [R][xch] composites in each partial list
   uint64_t* pmin;   // [R][xch] a lower bound on each full partial list's smallest composite (0: list not full)
@@ -90,7 +89,6 @@ static inline void fused_geometry(int U, int64_t nb_cap, int64_t* stride, int* s
 constexpr int kXBlocks = 256;
 constexpr int kXKeys = kXBlocks * kBlockTokens;  // 16384 keys per chunk
 constexpr int kXChunks = 64;
-constexpr uint32_t kXDirect = 0x80000000u;
 static inline int exact_chunks(int64_t nb_cap) {
   const int64_t c = (nb_cap + kXBlocks - 1) / kXBlocks;
   return (int)(c < 1 ? 1 : c > kXChunks ? kXChunks : c);
@@ -132,7 +130,6 @@ static FusedWs fused_carve(void* ws, int R, int U, int64_t nb_cap, int k) {
   w.xch = exact_chunks(nb_cap);
   w.pk = exact_pk(k);
   w.xctl = reinterpret_cast<uint32_t*>(p); p += a256((size_t)(1 + R) * 4);
-  w.xrows = reinterpret_cast<uint32_t*>(p); p += a256((size_t)R * 4);
   w.part = reinterpret_cast<uint64_t*>(p); p += a256((size_t)R * w.xch * w.pk * 8);
   w.pcnt = reinterpret_cast<uint32_t*>(p); p += a256((size_t)R * w.xch * 4);
   w.pmin = reinterpret_cast<uint64_t*>(p);
