@@ -836,6 +836,36 @@ def test_scan_topk_empty_and_short_rows():
         assert torch.equal(idx, i2)
 
 
+def test_scan_topk_rows_past_one_marking_run():
+    """The select pass marks the rows computed exactly 1024 at a time: 260 units
+    x 4 heads (1040 rows) mixing filtered rows (n above cap = 2k + 2048),
+    direct rows (n at most cap) and rows recomputed exactly (depths above the
+    caller's bit bound), with each kind below and past row 1024.  Every row
+    equals the oracle, and the call reports TOPK_FALLBACK for the recomputed
+    rows only."""
+    k = 16
+    cap = 2 * k + 2048
+    rng = np.random.default_rng(91)
+    U = 260
+    ns = [int(n) for n in rng.integers(cap + 1, 2300, U)]
+    direct = [5, 77, 200, 257, 258]
+    for u in direct:
+        ns[u] = int(rng.integers(k, cap + 1))
+    K, nt, planes, scales = _store(ns, 92)
+    q = rng.standard_normal((U, 4, 128)).astype(np.float16)
+    qt = torch.from_numpy(q).to(DEV)
+    var = torch.from_numpy(np.exp(rng.standard_normal((U, 128))).astype(np.float32)).to(DEV)
+    d, _ = F.fathom_alloc_depths(qt, var, F.FATHOM_WATERFILL, 48)
+    for u in [3, 130, 256, 259]:  # far above 48 bits: every row of the unit computed exactly
+        d[u] = torch.from_numpy(rng.integers(1, 5, 128).astype(np.uint8)).to(DEV)
+    st = F.new_status()
+    idx, val = F.fathom_scan_topk(planes, scales, nt, qt, d, k, dev_status=st, max_unit_bits=48)
+    assert status(st) == F.FATHOM_DEV_TOPK_FALLBACK, hex(status(st))
+    _assert_rows_match(idx, val, planes, scales, ns, q, d, k, 0, 0)
+    del K, planes, scales
+    torch.cuda.empty_cache()
+
+
 def test_gather_host_store_leaves_scan_topk_unchanged():
     """Sec. 3.6: the store in pinned host memory; gathering the rows the depths
     read into a zeroed device store copies exactly the active runs (first t
