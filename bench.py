@@ -123,7 +123,8 @@ def cpu_baseline(planes, scales, q, var, n, mode, B, k, units):
 TRAFFIC_JSON = os.path.join(ROOT, "profiles", "scan_topk_layer1m_b48_traffic.json")
 SQ_JSON = os.path.join(ROOT, "profiles", "scan_topk_layer1m_b48_sq.json")
 KERNEL_SOURCES = ("paper_2609_17652_amd/csrc/fused.hip", "paper_2609_17652_amd/csrc/filter.hip",
-                  "paper_2609_17652_amd/csrc/fused.hpp", "paper_2609_17652_amd/csrc/common.hpp")
+                  "paper_2609_17652_amd/csrc/fused.hpp", "paper_2609_17652_amd/csrc/common.hpp",
+                  "paper_2609_17652_amd/csrc/cellplan.hpp")
 # the three counter passes behind SQ_JSON (at most 8 SQ counters per pass)
 SQ_PASSES = (
     ("SQ_WAVES", "SQ_WAVE_CYCLES", "SQ_BUSY_CYCLES", "SQ_WAIT_ANY", "SQ_INSTS_VALU", "SQ_INSTS_SALU",
