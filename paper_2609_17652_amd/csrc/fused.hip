@@ -1717,6 +1717,9 @@ __global__ __launch_bounds__(kXThreads) void fused_select_kernel(FusedArgs a, in
     }
   };
   mark(0);  // the first rows' marks now: their loads overlap the rank part's
+  __syncthreads();
+  int cnt0 = 0;  // rows computed exactly among the first 1024
+  for (int x = 0; x < kXThreads / 32; ++x) cnt0 += __popc(cflg[x]);
   if (b < rank_wg) {
     const int j = b / kRankXcd, z = j % kRankParts, r = (j / kRankParts) * kRankXcd + b % kRankXcd;
     if (r < R) {
@@ -1734,6 +1737,7 @@ __global__ __launch_bounds__(kXThreads) void fused_select_kernel(FusedArgs a, in
   }
   const int xch = a.ws.xch, zz = b % xch, s = b / xch;
   if (s >= kXSlots) return;
+  if (R <= kXThreads && cnt0 <= s) return;  // no exact row for this workgroup (the usual case)
   int before = 0;  // rows computed exactly below r0
   for (int r0 = 0; r0 < R; r0 += kXThreads) {
     if (r0 > 0) {
