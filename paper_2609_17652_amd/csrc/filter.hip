@@ -647,7 +647,12 @@ __device__ __forceinline__ void cwave_run(const CellPlan& P, FilterLds<NS>& L, c
     }
     // ask the pool for the group after gnxt once the static groups run out
     asked = !dry && gnxt >= 0 && it + 2 >= gs.ns;
-    if (asked && lane == 0) grab = gatomic_add(a.ws.pool + gs.ctr, 1u);
+    // an increment, not an add: the compiler's atomic optimizer would turn a
+    // single-lane add into a wave-aggregated one whose result is read at once
+    // (a wait on every load in flight); the result is first read one group later
+    if (asked && lane == 0)
+      grab = __builtin_amdgcn_atomic_inc32((__attribute__((address_space(1))) uint32_t*)(a.ws.pool + gs.ctr), 0xFFFFFFFFu,
+                                           __ATOMIC_RELAXED, "agent");
     sched_fence();
     {
       float qv[4];  // q of cell `lane`'s channel (read here: fewer registers live across the loop)
