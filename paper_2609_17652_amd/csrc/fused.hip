@@ -1091,13 +1091,14 @@ __device__ __forceinline__ float key_to_score(uint32_t key) {
 // histogram.  The parts of a row run on one XCD (workgroups are dealt to the
 // 8 XCDs in turn), so the list is read once into that XCD's L2.
 constexpr int kRankParts = 8;
-constexpr int kRankThreads = 1024;  // the select pass's workgroup
+constexpr int kRankThreads = 512;   // the rank pass's workgroup (the select pass's is kXThreads)
 constexpr int kRankPer = 8;      // survivors per thread read with the count (the rest re-read)
 constexpr int kRankCap = 4096;   // survivors one part orders at most
 constexpr int kRankSub = 4096;   // sub-buckets at most
 constexpr int kRankXcd = 8;
+template <int T>
 struct RankShared {
-  uint32_t s_red[2][kRankThreads / kWave], s_part[kRankThreads / kWave];
+  uint32_t s_red[2][T / kWave], s_part[T / kWave];
   uint32_t s_first[kRankParts + 1];  // part z: sub-buckets [s_first[z], s_first[z + 1])
   uint32_t s_c, s_ovf;
   float s_tau;
@@ -1108,8 +1109,10 @@ struct RankShared {
 // and kRankSub + 1 counts, 16-byte aligned.  Returns true when a part's share
 // exceeds kRankCap after all (many equal scores): the row is then computed
 // exactly.
+template <int T>
 __device__ bool rank_part(const FusedArgs& a, int r, int z, int32_t* __restrict__ idx, float* __restrict__ val,
-                          uint64_t* grp, uint32_t* hist, RankShared& RS) {
+                          uint64_t* grp, uint32_t* hist, RankShared<T>& RS) {
+  constexpr int kRankThreads = T;  // threads of the calling workgroup
   auto& s_red = RS.s_red;
   auto& s_part = RS.s_part;
   auto& s_first = RS.s_first;
@@ -1691,20 +1694,40 @@ __device__ __forceinline__ bool row_exact(const FusedArgs& a, int r) {
   return !(c >= (uint32_t)a.k && c <= (uint32_t)a.ws.lcap && (ovf & 1u) == 0u && tau != kNegInf);
 }
 
-// The select pass: ranks and exact rows in one launch.  Workgroup b < rank_wg
-// is part z of row r of the ranks above unless the row is computed exactly;
-// a part that finds its share too large computes the row's chunks z,
-// z + kRankParts, ... itself.  Workgroup b < xch kXSlots then takes chunk b mod xch of the rows computed
+// The rank pass, when the rank parts do not fit one round in the select
+// pass's workgroups (1024 threads, one a CU): part z of row r as above; a part
+// whose share is too large marks the row for the exact rows of the select
+// pass that follows (tau = -inf, which every part of the row writes alike,
+// before any of them writes a position).
+__global__ __launch_bounds__(kRankThreads) void fused_rank_kernel(FusedArgs a, int R, int32_t* __restrict__ idx,
+                                                                 float* __restrict__ val) {
+  __shared__ uint64_t grp[kRankCap];
+  __shared__ __align__(16) uint32_t hist[kRankSub + 4];
+  __shared__ RankShared<kRankThreads> RS;
+  __shared__ int s_ex;
+  const int b = (int)blockIdx.x, j = b / kRankXcd, z = j % kRankParts, r = (j / kRankParts) * kRankXcd + b % kRankXcd;
+  if (r >= R) return;
+  if (threadIdx.x == 0) s_ex = row_exact(a, r) ? 1 : 0;
+  __syncthreads();
+  if (s_ex) return;
+  if (rank_part<kRankThreads>(a, r, z, idx, val, grp, hist, RS) && threadIdx.x == 0) gstore(a.ws.tau + r, kNegInf);
+}
+
+// The select pass: ranks and exact rows in one launch when the rank parts fit
+// one round of the chip (ranks set: rank_wg > 0), else the exact rows only
+// after the rank pass below.  Workgroup b < rank_wg is part z of row r of the
+// ranks above unless the row is computed exactly; a part that finds its
+// share too large computes the row's chunks z, z + kRankParts, ... itself.
+// Workgroup b < xch kXSlots then takes chunk b mod xch of the rows computed
 // exactly with list index s, s + kXSlots, ... (s = b / xch): it marks the
 // rows 1024 at a time (the same marks in every workgroup: they follow from
 // the filter's counts, tau and flags) and counts them in row order.
-static_assert(kRankThreads == kXThreads, "one workgroup shape for both parts");
 static_assert((size_t)kRankCap * 8 + ((size_t)kRankSub + 4) * 4 <= kXLdsBytes, "the rank part's LDS inside the exact part's");
 __global__ __launch_bounds__(kXThreads) void fused_select_kernel(FusedArgs a, int R, int rank_wg,
                                                                  int32_t* __restrict__ idx, float* __restrict__ val) {
   extern __shared__ __align__(16) unsigned char xl[];
   __shared__ XShared S;
-  __shared__ RankShared RS;
+  __shared__ RankShared<kXThreads> RS;
   __shared__ uint32_t cflg[kXThreads / 32];  // bit i: row r0 + i is computed exactly
   __shared__ int s_ex;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, b = (int)blockIdx.x;
@@ -1727,7 +1750,7 @@ __global__ __launch_bounds__(kXThreads) void fused_select_kernel(FusedArgs a, in
       __syncthreads();
       const bool ex = r < kXThreads ? ((cflg[r >> 5] >> (r & 31)) & 1u) != 0u : s_ex != 0;
       if (!ex) {
-        const bool over = rank_part(a, r, z, idx, val, reinterpret_cast<uint64_t*>(xl),
+        const bool over = rank_part<kXThreads>(a, r, z, idx, val, reinterpret_cast<uint64_t*>(xl),
                                     reinterpret_cast<uint32_t*>(xl + (size_t)kRankCap * 8), RS);
         __syncthreads();
         if (over)
@@ -1768,6 +1791,21 @@ __global__ void fused_empty_kernel(const int64_t* __restrict__ n, int G, int k, 
     if (val) val[(int64_t)r * k + x] = __uint_as_float(0x7FC00000u);
   }
   if (threadIdx.x == 0) set_status(st, FATHOM_DEV_TOPK_SHORT | (n[r / G] != 0 ? FATHOM_DEV_BAD_N : 0u));
+}
+
+// Compute units of device dev (looked up once per device).
+static int device_cus(int dev) {
+  static std::atomic<int> cus[64];
+  if (dev < 0 || dev >= 64) return 0;
+  int c = cus[dev].load(std::memory_order_relaxed);
+  if (c == 0) {
+    if (hipDeviceGetAttribute(&c, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) {
+      (void)hipGetLastError();
+      c = -1;  // unknown: no one-launch select pass
+    }
+    cus[dev].store(c, std::memory_order_relaxed);
+  }
+  return c > 0 ? c : 0;
 }
 
 fathom_status launch_scan_topk_fused(const uint64_t* planes, const uint16_t* scales, const int64_t* n, int U,
@@ -1833,8 +1871,13 @@ fathom_status launch_scan_topk_fused(const uint64_t* planes, const uint16_t* sca
   }
   const unsigned rank_wg = (unsigned)((R + kRankXcd - 1) / kRankXcd) * kRankXcd * kRankParts;
   const unsigned xg = (unsigned)fa.ws.xch * (unsigned)kXSlots;
-  hipLaunchKernelGGL(fused_select_kernel, dim3(rank_wg > xg ? rank_wg : xg), dim3(kXThreads), kXLdsBytes, s, fa, R,
-                     (int)rank_wg, idx, val);
+  if (rank_wg <= (unsigned)device_cus(dev)) {  // the rank parts fit one round: ranks and exact rows in one launch
+    hipLaunchKernelGGL(fused_select_kernel, dim3(rank_wg > xg ? rank_wg : xg), dim3(kXThreads), kXLdsBytes, s, fa, R,
+                       (int)rank_wg, idx, val);
+  } else {
+    hipLaunchKernelGGL(fused_rank_kernel, dim3(rank_wg), dim3(kRankThreads), 0, s, fa, R, idx, val);
+    hipLaunchKernelGGL(fused_select_kernel, dim3(xg), dim3(kXThreads), kXLdsBytes, s, fa, R, 0, idx, val);
+  }
   FATHOM_LAUNCH_CHECK();
   return FATHOM_OK;
 }

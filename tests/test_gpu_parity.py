@@ -641,6 +641,32 @@ def test_equal_scores_top_k(tied_blocks):
     assert np.array_equal(val[0, 0].cpu().numpy().view(np.uint32), ov.view(np.uint32))
 
 
+def test_equal_scores_rows_past_one_round_of_rank_parts():
+    """As test_equal_scores_top_k with 80 tied blocks, over 10 units x 4 heads
+    (40 rows): the rank parts then outnumber one round of the chip, so the
+    ranks run in their own pass and a row with a too-large share is deferred
+    to the exact rows that follow (TOPK_FALLBACK).  Every row equals the
+    oracle."""
+    rng = np.random.default_rng(96)
+    U, G, n, k, tied = 10, 4, 20000, 2048, 80
+    q = np.repeat(rng.standard_normal((U, 1, 128)).astype(np.float32), G, axis=1)
+    K = rng.standard_normal((U, n, 128)).astype(np.float32)
+    t0 = 100 * 64
+    for u in range(U):
+        K[u, t0:t0 + 64 * tied] = 30.0 * q[u, 0] / np.linalg.norm(q[u, 0])
+    nt = torch.full((U,), n, dtype=torch.int64, device=DEV)
+    planes, scales = F.fathom_pack(torch.from_numpy(K).to(DEV), nt)
+    qt = torch.from_numpy(q).to(DEV)
+    var = torch.ones((U, 128), dtype=torch.float32, device=DEV)
+    d, _ = F.fathom_alloc_depths(qt, var, F.FATHOM_WATERFILL, 48)
+    st = F.new_status()
+    idx, val = F.fathom_scan_topk(planes, scales, nt, qt, d, k, dev_status=st, max_unit_bits=48)
+    assert status(st) == F.FATHOM_DEV_TOPK_FALLBACK, hex(status(st))
+    _assert_rows_match(idx, val, planes, scales, [n] * U, q, d, k, 0, 0)
+    del K, planes, scales
+    torch.cuda.empty_cache()
+
+
 def test_scan_topk_no_fallback_on_workload_data():
     """On the synthetic workloads the sampled threshold never needs the fallback."""
     cfg = synth.WORKLOADS["layer128k"]
