@@ -1,6 +1,6 @@
 // Full pass of fathom_scan_topk for units of at most 48 active channels and
-// 16 row groups (every unit under water-filling at up to 48 code bits, and
-// uniform depth at r <= 16): an int8 MFMA proxy of every key's four head
+// 64 cells (every unit under water-filling at up to 48 code bits, and uniform
+// depth at r <= 16): an int8 MFMA proxy of every key's four head
 // scores over its plane bits, exact re-scoring of the keys the proxy's bound
 // cannot exclude, and the appends of keys with exact score >= tau to their
 // row's survivor list (Sec. 3.2-3.3 scores, Sec. 2 top-k).
@@ -16,14 +16,17 @@
 //   |s - delta (S - Wsum / 2)| <= delta cells / 4 + (A^2 127 2^-24) delta
 // (weight rounding, then the A roundings of the fp32 chain), plus A 2^-120
 // for subnormal results.  A key is a candidate for head h iff
-// S >= thr = floor((floor(2 (tau - E) / delta) - 1 + Wsum) / 2).
+// S >= thr = floor((floor(2 (tau - E) / delta) - 1 + Wsum) / 2).  At three
+// slices the weights have two levels, W' = 128 W + W_lo in units of
+// delta / 128 (the bound's cell term shrinks by 128).
 //
-// Layout.  Cells are ordered plane-major, each plane's channels (a prefix of
-// the proxy order: depth descending, channel ascending) padded to a multiple
-// of 4: row group g = plane p_g, proxy channels 4 i_g .. 4 i_g + 3.  The plane
-// words of a quad (4 blocks) are staged in LDS as loaded, cell by cell (pad
-// cells read as zero), and ds_read_b64_tr_b8 hands lane l the bytes of 8
-// cells (two row groups) at octet l & 7 of block l >> 4: within a 16-lane
+// Layout.  Cells are ordered plane-major without padding (plane p's cells are
+// its channels, a prefix of the proxy order: depth descending, channel
+// ascending); row group g = cells 4 g .. 4 g + 3, which may span two planes.
+// The plane words of a quad (4 blocks) are staged in LDS as loaded, cell by
+// cell (cells past the unit's read as zero), and ds_read_b64_tr_b8 hands
+// lane l the bytes of 8 cells (two row groups) at octet l & 7 of block
+// l >> 4: within a 16-lane
 // group, output lane 8h + r takes byte r of the words addressed by lanes h,
 // h + 2, ..., h + 14.  So lane l owns the 4 keys 8 o + 4 nib + mu (o = l & 7,
 // nib = (l >> 3) & 1) of block l >> 4, and with pos = 4 nib + mu,
@@ -36,8 +39,9 @@
 // bits of a lane's 16 accumulators, gathered a byte per head, are its keys'
 // candidate heads.
 //
-// Candidate keys are queued per wave in LDS with their lane's staged dwords; a batch is scored exactly in the documented order (channels
-// ascending, fmaf from +0) with the scales of the last four groups kept in
+// Candidate keys are queued per wave in LDS with their lane's staged
+// dwords; a batch is scored exactly in the documented order (channels
+// ascending, fmaf from +0) with the scales of the last Slots groups kept in
 // an LDS ring, and keys with score >= tau are appended to their row's list.
 #include "cellplan.hpp"
 
