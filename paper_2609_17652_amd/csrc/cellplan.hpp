@@ -11,9 +11,9 @@
 
 namespace fathom {
 
-constexpr int kCG = 16;          // row groups at most (4 slices of 4)
+constexpr int kCG = 20;          // row groups at most (5 slices of 4)
 constexpr int kCC = 4 * kCG;     // cells at most
-constexpr int kCA = 48;          // active channels at most
+constexpr int kCA = 64;          // active channels at most (one lane each for the scales)
 
 struct alignas(16) CellPlan {
   int A, rg, C, ok;        // active channels, row groups, cells, the unit fits this pass
@@ -32,9 +32,11 @@ struct alignas(16) CellPlan {
 };
 constexpr uint32_t kCPad = 0xFFFFu;
 
-typedef unsigned int PlanWord __attribute__((ext_vector_type(4)));  // plans move 16 bytes a thread
-static_assert(sizeof(CellPlan) <= kPlanBytes, "a unit's plan fits its workspace slot");
-static_assert(sizeof(CellPlan) <= 16 * kFT, "one 16-byte word per thread copies a plan");
+typedef unsigned int PlanWord __attribute__((ext_vector_type(4)));  // plans move 16 bytes a thread and step
+constexpr int kPlanWords = (int)((sizeof(CellPlan) + 15) / 16);
+constexpr int kPlanSteps = 2;  // copy steps of 256 threads
+static_assert(sizeof(CellPlan) % 16 == 0 && sizeof(CellPlan) <= kPlanBytes, "a unit's plan fits its workspace slot");
+static_assert(kPlanWords <= kPlanSteps * kFT, "two 16-byte words per thread copy a plan");
 
 // ---------------------------------------------------------------- plan
 // Depth and q of channel tid (< 128), read by the kernel before its other

@@ -1,6 +1,7 @@
-// Full pass of fathom_scan_topk for units of at most 48 active channels and
-// 64 cells (every unit under water-filling at up to 48 code bits, and uniform
-// depth at r <= 16): an int8 MFMA proxy of every key's four head
+// Full pass of fathom_scan_topk for units of at most 64 active channels and
+// 80 cells (every unit under water-filling at up to 48 code bits, units of
+// up to 64 channels at up to 80 bits, and uniform depth at r <= 16): an int8
+// MFMA proxy of every key's four head
 // scores over its plane bits, exact re-scoring of the keys the proxy's bound
 // cannot exclude, and the appends of keys with exact score >= tau to their
 // row's survivor list (Sec. 3.2-3.3 scores, Sec. 2 top-k).
@@ -48,23 +49,27 @@
 namespace fathom {
 
 constexpr int kCSB = 8;          // blocks per group (one delta per head; one loop iteration)
-constexpr int kCQ = 64;          // queued candidates per wave (one ballot fits)
-constexpr int kCFlush = 64;      // re-score at a quad boundary once the queue is full
 constexpr int kSv = 8;           // survivors per head buffered in LDS before a list append
 
 // Geometry of an instantiation with NS slices of 4 row groups (16 cells):
-// NS = 3 serves units of at most 48 cells, NS = 4 of at most 64.  The scale
-// ring holds one row of C + 2 halfs per block (an odd number of dwords, so
-// the lanes of a re-scoring batch fall in different banks) for Slots groups;
-// three workgroups per CU fit the LDS with 6 slots at NS = 3 (a wave's 6
-// groups of the 2^20-token layer: no flush before its end) and 3 at NS = 4.
+// NS = 3 serves units of at most 48 cells, NS = 4 of at most 64, NS = 5 of
+// at most 80.  The scale ring holds one row of C + 2 halfs per block (an odd
+// number of dwords, so the lanes of a re-scoring batch fall in different
+// banks) for Slots groups; three workgroups per CU fit the LDS with 6 slots
+// at NS = 3 (a wave's 6 groups of the 2^20-token layer: no flush before its
+// end) and 3 at NS = 4 and 5, the last with a queue of 32 candidates.  A
+// lane stages K plane words per quad: 4 cells of its row group up to NS = 4,
+// at NS = 5 the cells lane / 4 + 16 k, k < 5.
 template <int NS>
 struct CGeo {
+  static_assert(NS >= 3 && NS <= 5, "three to five slices");
   static constexpr int G = 4 * NS;
   static constexpr int C = 4 * G;
   static constexpr int Slots = NS == 3 ? 6 : 3;
   static constexpr int SclRow = C + 2;
   static constexpr bool Fine = NS == 3;  // two-level weights (the registers fit them at three slices)
+  static constexpr int Q = NS == 5 ? 32 : 64;  // queued candidates per wave; re-scored at a quad boundary once full
+  static constexpr int K = NS == 5 ? 5 : 4;    // plane words a lane stages per quad
 };
 // Fine weights W' = 128 W + W_lo count in units of delta / 128; |S'| < 2^20
 // for 48 cells, so thresholds are clamped to +-2^21 and an accumulator stays
@@ -83,9 +88,9 @@ struct alignas(16) FilterLds {
   uint32_t Wlo[Geo::Fine ? 4 : 1][4][Geo::G];     // fine weights: the residual weights W_lo, likewise
   int32_t ini[4][2][4][4];                        // accumulator starts: block, nibble, mu, head
   uint16_t scl[Geo::Slots][kCSB][Geo::SclRow];    // fp16 scales: ring slot, block, cell (its channel's scale)
-  uint32_t qx[Geo::G][kCQ];                       // queued keys' staged dwords (digits while re-scored): dword, entry
-  uint32_t qi[kCQ];                       // queued key index
-  uint32_t qf[kCQ];                       // pos | slot << 3 (3 bits) | block of the group << 8 | head h at bit 7 + 8 h
+  uint32_t qx[Geo::G][Geo::Q];                    // queued keys' staged dwords (digits while re-scored): dword, entry
+  uint32_t qi[Geo::Q];                    // queued key index
+  uint32_t qf[Geo::Q];                    // pos | slot << 3 (3 bits) | block of the group << 8 | head h at bit 7 + 8 h
   uint64_t sv[4][kSv];                    // survivors per head not yet appended to the row's list
 };
 
@@ -151,14 +156,24 @@ struct CDel {
 // Writes the group's scales to ring slot `slot` (cell order: cell c holds
 // its channel's scale, so the plane-0 cell of proxy channel x is cell x) and
 // returns delta of head `hq` (every lane: its own head for the weights).  qv:
-// q of cell `lane`'s channel for the four heads (0 past the cells).
+// q of cell `lane`'s channel for the four heads (0 past the cells).  Cells
+// past 64 (NS = 5) copy the scale of their channel's plane-0 cell x2 (lane
+// l < 16 for cell 64 + l; every active channel lies below kCA = 64).
 template <int NS>
-__device__ __forceinline__ CDel cscl_commit(const CScl& r, FilterLds<NS>& L, int slot, int hq, const float (&qv)[4]) {
+__device__ __forceinline__ CDel cscl_commit(const CScl& r, FilterLds<NS>& L, int slot, int hq, const float (&qv)[4],
+                                            int x2) {
   const int lane = threadIdx.x & 63;
   uint32_t mx = 0u;
   if (lane < CGeo<NS>::C) {
 #pragma unroll
     for (int b = 0; b < kCSB; ++b) L.scl[slot][b][lane] = (uint16_t)((r.v[b >> 1] >> (16 * (b & 1))) & 0xFFFFu);
+  }
+  if constexpr (CGeo<NS>::C > kWave) {
+    lds_order();  // the wave's LDS accesses run in order: the reads see the writes above
+    if (lane < CGeo<NS>::C - kWave) {
+#pragma unroll
+      for (int b = 0; b < kCSB; ++b) L.scl[slot][b][kWave + lane] = L.scl[slot][b][x2];
+    }
   }
 #pragma unroll
   for (int i = 0; i < kCSB / 2; ++i) {
@@ -186,35 +201,54 @@ __device__ __forceinline__ CDel cscl_commit(const CScl& r, FilterLds<NS>& L, int
 }
 
 // ---------------------------------------------------------------- staging
-// Lane (row group g = lane >> 2, block bq = lane & 3 of the quad) loads the
-// plane words of g's 4 cells for its block through a buffer descriptor over
-// the unit's planes, and stores them as raw[4 g + k][bq].  Pad cells (and row
-// groups past the unit's) read past the descriptor's range, which returns
-// zero; every other load stays inside the unit.
+// Lane (block bq = lane & 3 of the quad) loads the plane words of K cells for
+// its block through a buffer descriptor over the unit's planes, and stores
+// them as raw[cell][bq]: up to NS = 4 the 4 cells of row group g = lane >> 2,
+// at NS = 5 the cells lane / 4 + 16 k.  Pad cells (and row groups past the
+// unit's) read past the descriptor's range, which returns zero; every other
+// load stays inside the unit.
+template <int NS>
+__device__ __forceinline__ int cstage_cell(int lane, int k) {
+  return CGeo<NS>::K == 5 ? (lane >> 2) + 16 * k : 4 * (lane >> 2) + k;
+}
+template <int NS>
 struct CStage {
-  __amdgpu_buffer_rsrc_t rs;  // the unit's planes (ub bytes)
-  uint32_t boff[4];           // byte offset of cell k's word for block bq of a quad starting at block 0
-  uint32_t ub;                // an offset past the range
+  __amdgpu_buffer_rsrc_t rs;     // the unit's planes (ub bytes)
+  uint32_t boff[CGeo<NS>::K];    // byte offset of word k for block bq of a quad starting at block 0
+  uint32_t ub;                   // an offset past the range
 };
+template <int NS>
 struct CRaw {
-  uint64_t w[4];  // cell k's word of block bq
+  uint64_t w[CGeo<NS>::K];  // word k (cell cstage_cell(lane, k)) of block bq
 };
 
 // Pad cells get the offset ub: with the quad's offset (at most 8 (nb_cap +
 // 40) bytes) added it stays past the range without wrapping (4104 nb_cap +
 // 320 < 2^32 for nb_cap < kOneNbMax).
-__device__ __forceinline__ void cstage_setup(CStage& S, const CellPlan& P, const FusedArgs& a, uint64_t ubase,
+template <int NS>
+__device__ __forceinline__ void cstage_setup(CStage<NS>& S, const CellPlan& P, const FusedArgs& a, uint64_t ubase,
                                              uint32_t ub) {
   const int lane = threadIdx.x & 63, g = lane >> 2, bq = lane & 3;
   const uint32_t alo = (uint32_t)cuni((int)(uint32_t)ubase), ahi = (uint32_t)cuni((int)(uint32_t)(ubase >> 32));
   S.rs = __builtin_amdgcn_make_buffer_rsrc(reinterpret_cast<void*>(((uint64_t)ahi << 32) | alo), (short)0,
                                           (int)(uint32_t)cuni((int)ub), kRawBufferFlags);
-  const bool on = g < cuni(P.rg);
-  const uint32_t r0 = P.rrow[on ? g : 0][0], r1 = P.rrow[on ? g : 0][1];
-  const uint32_t rows[4] = {r0 & 0xFFFFu, r0 >> 16, r1 & 0xFFFFu, r1 >> 16};
+  if constexpr (CGeo<NS>::K == 5) {
+    // cell c's row: half c & 1 of word (c >> 1) & 1 of row group c >> 2
+    // (kCPad for every cell past the unit's)
 #pragma unroll
-  for (int k = 0; k < 4; ++k)
-    S.boff[k] = on && rows[k] != kCPad ? (rows[k] * (uint32_t)a.nb_cap + (uint32_t)bq) * 8u : ub;
+    for (int k = 0; k < 5; ++k) {
+      const int c = cstage_cell<NS>(lane, k);
+      const uint32_t row = (P.rrow[c >> 2][(c >> 1) & 1] >> (16 * (c & 1))) & 0xFFFFu;
+      S.boff[k] = row != kCPad ? (row * (uint32_t)a.nb_cap + (uint32_t)bq) * 8u : ub;
+    }
+  } else {
+    const bool on = g < cuni(P.rg);
+    const uint32_t r0 = P.rrow[on ? g : 0][0], r1 = P.rrow[on ? g : 0][1];
+    const uint32_t rows[4] = {r0 & 0xFFFFu, r0 >> 16, r1 & 0xFFFFu, r1 >> 16};
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+      S.boff[k] = on && rows[k] != kCPad ? (rows[k] * (uint32_t)a.nb_cap + (uint32_t)bq) * 8u : ub;
+  }
   S.ub = ub;
 }
 
@@ -223,19 +257,23 @@ __device__ __forceinline__ void cstage_setup(CStage& S, const CellPlan& P, const
 // (no group of the wave there) reads past the range and fetches nothing; a
 // valid quad past the unit's blocks reads other rows' words or zeros, which
 // no eligible key uses.
-__device__ __forceinline__ void cstage_issue(CRaw& R, const CStage& S, int qb0, bool valid) {
+template <int NS>
+__device__ __forceinline__ void cstage_issue(CRaw<NS>& R, const CStage<NS>& S, int qb0, bool valid) {
   const int so = cuni((int)((uint32_t)qb0 * 8u));
 #pragma unroll
-  for (int k = 0; k < 4; ++k) {
+  for (int k = 0; k < CGeo<NS>::K; ++k) {
     const v2u32 v = __builtin_amdgcn_raw_buffer_load_b64(S.rs, (int)(valid ? S.boff[k] : S.ub), so, 0);
     R.w[k] = ((uint64_t)v.y << 32) | v.x;
   }
 }
 
 template <int NS>
-__device__ __forceinline__ void cstage_write(const CRaw& R, FilterLds<NS>& L) {
+__device__ __forceinline__ void cstage_write(const CRaw<NS>& R, FilterLds<NS>& L) {
   const int lane = threadIdx.x & 63, g = lane >> 2, bq = lane & 3;
-  if (g < CGeo<NS>::G) {
+  if constexpr (CGeo<NS>::K == 5) {
+#pragma unroll
+    for (int k = 0; k < 5; ++k) L.raw[cstage_cell<NS>(lane, k)][bq] = R.w[k];
+  } else if (g < CGeo<NS>::G) {
 #pragma unroll
     for (int k = 0; k < 4; ++k) L.raw[4 * g + k][bq] = R.w[k];
   }
@@ -362,7 +400,8 @@ __device__ __forceinline__ void crescore(const CellPlan& P, FilterLds<NS>& L, co
   const uint32_t ki = L.qi[e], f = L.qf[e];
   const uint32_t pos = f & 7u, hm = on ? f : 0u;
   const int slot = (int)((f >> 3) & 7u), blk = (int)((f >> 8) & 7u);
-  uint32_t* ent = &L.qx[0][e];  // dword i of the entry at ent[i * kCQ] (entries side by side: no bank conflicts)
+  constexpr int Q = CGeo<NS>::Q;
+  uint32_t* ent = &L.qx[0][e];  // dword i of the entry at ent[i * Q] (entries side by side: no bank conflicts)
   // digit dword i (proxy channels 4 i .. 4 i + 3): the plane-p bits of its
   // channels are cells base_p + 4 i .., bytes (base_p & 3) .. of row group
   // (base_p + 4 i) >> 2 and the next one (a byte funnel shift), the bytes of
@@ -383,13 +422,13 @@ __device__ __forceinline__ void crescore(const CellPlan& P, FilterLds<NS>& L, co
       if (v > 0) {
         const int c0 = bpl[p] + 4 * i, r = c0 >> 2, sh = c0 & 3;
         const int r1 = r + 1 < CGeo<NS>::G ? r + 1 : r;
-        const uint32_t lo = ent[r * kCQ], hi = ent[r1 * kCQ];
+        const uint32_t lo = ent[r * Q], hi = ent[r1 * Q];
         const uint32_t w = sh ? __builtin_amdgcn_alignbyte(hi, lo, (uint32_t)sh) : lo;
         const uint32_t m = v >= 4 ? 0x01010101u : 0x01010101u >> (8 * (4 - v));
         dw |= ((w >> pos) & m) << (3 - p);
       }
     }
-    ent[i * kCQ] = dw;
+    ent[i * Q] = dw;
   }
   // digit of proxy channel x: byte x & 3 of dword x >> 2
   const uint8_t* dg = reinterpret_cast<const uint8_t*>(ent);
@@ -405,7 +444,7 @@ __device__ __forceinline__ void crescore(const CellPlan& P, FilterLds<NS>& L, co
     float4 q4[4];
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
-      dv[c] = dg[(xs[c] >> 2) * (kCQ * 4) + (xs[c] & 3)];
+      dv[c] = dg[(xs[c] >> 2) * (Q * 4) + (xs[c] & 3)];
       hv[c] = sv[xs[c]];
       q4[c] = *reinterpret_cast<const float4*>(&P.qa[y0 + c][0]);
     }
@@ -470,7 +509,7 @@ __device__ __forceinline__ void crescore(const CellPlan& P, FilterLds<NS>& L, co
 // the pool's counter is read a group before the group it names is loaded.  A
 // wave's LDS accesses execute in program order, so staged data is read back
 // without a wait.  Re-scoring runs at one place: after a quad's candidates,
-// when the queue holds kCFlush, when a quad's candidates do not fit, before
+// when the queue is full, when a quad's candidates do not fit, before
 // the ring slot of the oldest queued key is reused, and at the end.
 struct CGroups {
   int s0, ns;     // static groups s0 + kCWaves i, i < ns
@@ -492,6 +531,7 @@ __device__ __forceinline__ void cwave_run(const CellPlan& P, FilterLds<NS>& L, c
   const bool top = (lane & 3) == 3;  // as a weight lane: its second start is position 7
   const int C = cuni(P.C);
   const int cxl = P.cx[lane];                  // cell `lane`'s channel (proxy index)
+  const int cx2 = Geo::C > kWave ? P.cx[kWave + (lane & 15)] : 0;  // cell 64 + (lane & 15)'s (NS = 5)
   const int srow = lane < C ? P.pj[cxl] : 0;   // its scale row
   // as a transpose source: cell (l & 15) >> 1 of pair 0, block l >> 4
   const uint32_t src_off = (uint32_t)((((lane & 15) >> 1) * 4 + bq) * 8);
@@ -500,8 +540,8 @@ __device__ __forceinline__ void cwave_run(const CellPlan& P, FilterLds<NS>& L, c
   const uint32_t* wlsrc = wl && Geo::Fine ? &L.Wlo[Geo::Fine ? bq : 0][lane & 3][0] : &L.zero[0];
   const uint64_t ubase = reinterpret_cast<uint64_t>(a.planes + (int64_t)u * kD * kPlanes * a.nb_cap);
   const uint32_t ubytes = (uint32_t)(kD * kPlanes * 8) * (uint32_t)a.nb_cap;
-  CStage S;
-  cstage_setup(S, P, a, ubase, ubytes);
+  CStage<NS> S;
+  cstage_setup<NS>(S, P, a, ubase, ubytes);
   if (lane < Geo::G) L.zero[lane] = 0u;
   int pending = 0, oldest = 0;
   const int b0 = gs.s0 * kCSB;
@@ -512,7 +552,7 @@ __device__ __forceinline__ void cwave_run(const CellPlan& P, FilterLds<NS>& L, c
   CScl sr;
   cscl_issue<VEC>(sr, a, u, C, srow, b0, any);
   sched_fence();
-  CRaw R0, R1;
+  CRaw<NS> R0, R1;
   cstage_issue(R0, S, b0, any);
   sched_fence();
   cstage_issue(R1, S, b0 + kQB, any);
@@ -525,7 +565,7 @@ __device__ __forceinline__ void cwave_run(const CellPlan& P, FilterLds<NS>& L, c
   int gnxt = gs.ns > 1 ? gs.s0 + kCWaves : -1;
   bool dry = gs.ctr < 0, asked = false;
   uint32_t grab = 0u;
-  auto quad = [&](CRaw& R, int qb0, int it, int sbq) {  // sbq: first block of the quad within its group
+  auto quad = [&](CRaw<NS>& R, int qb0, int it, int sbq) {  // sbq: first block of the quad within its group
     cstage_write(R, L);
     sched_fence();
     cstage_issue(R, S, gnxt * kCSB + sbq, gnxt >= 0);  // the same quad of the wave's next group
@@ -607,9 +647,9 @@ __device__ __forceinline__ void cwave_run(const CellPlan& P, FilterLds<NS>& L, c
       // every lane's lowest remaining key, as many as fit; re-score when the
       // queue is full and keys remain, or at the flush points
       const uint64_t want = __ballot(kmask != 0u);
-      if (want != 0ull && pending < kCQ) {
+      if (want != 0ull && pending < Geo::Q) {
         const int rank = (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(want >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)want, 0u));
-        const bool mine = kmask != 0u && rank < kCQ - pending;
+        const bool mine = kmask != 0u && rank < Geo::Q - pending;
         if (mine) {
           const int mu = __builtin_ctz(kmask);
           const int qp = pending + rank;
@@ -623,7 +663,7 @@ __device__ __forceinline__ void cwave_run(const CellPlan& P, FilterLds<NS>& L, c
         continue;
       }
       // entries of group it + 1 - Slots hold the ring slot rewritten next
-      const bool flush = want != 0ull || pending >= kCFlush ||
+      const bool flush = want != 0ull || pending >= Geo::Q ||
                          (pending > 0 && (last || (endg && oldest <= it + 1 - Geo::Slots)));
       if (!flush) break;
       lds_order();
@@ -665,7 +705,7 @@ __device__ __forceinline__ void cwave_run(const CellPlan& P, FilterLds<NS>& L, c
         const bool on = lane < C;
         qv[0] = on ? q4.x : 0.0f; qv[1] = on ? q4.y : 0.0f; qv[2] = on ? q4.z : 0.0f; qv[3] = on ? q4.w : 0.0f;
       }
-      const CDel dl = cscl_commit(sr, L, slot, hq, qv);
+      const CDel dl = cscl_commit(sr, L, slot, hq, qv, cx2);
       sched_fence();
       cscl_issue<VEC>(sr, a, u, C, srow, gnxt * kCSB, gnxt >= 0);
       sched_fence();
@@ -782,10 +822,15 @@ __global__ __launch_bounds__(kCThreads, 3) void fused_filter_kernel(FusedArgs a,
     const int i = lane + kWave * i0;
     sv[i0] = i < nsm ? gload(a.ws.samp + (int64_t)(u * G + wave) * kSmpRow + i) : kNegInf;
   }
-  // the unit's plan (built by the sample pass), one 16-byte word per thread
-  PlanWord pw = PlanWord{0u, 0u, 0u, 0u};
-  if (tid * 16 < (int)sizeof(CellPlan))
-    pw = gload(reinterpret_cast<const PlanWord*>(a.ws.plan + (size_t)u * kPlanBytes) + tid);
+  // the unit's plan (built by the sample pass), up to two 16-byte words per thread
+  static_assert(kCThreads == kFT, "the plan's copy steps");
+  PlanWord pw[kPlanSteps];
+#pragma unroll
+  for (int i = 0; i < kPlanSteps; ++i) {
+    const int w = tid + kCThreads * i;
+    pw[i] = w < kPlanWords ? gload(reinterpret_cast<const PlanWord*>(a.ws.plan + (size_t)u * kPlanBytes) + w)
+                           : PlanWord{0u, 0u, 0u, 0u};
+  }
   int64_t nu, lo, hi;
   row_window(a, u, &nu, &lo, &hi, x == 0 && tid == 0);
   if ((uo >> 1) != 1u) return;
@@ -802,7 +847,9 @@ __global__ __launch_bounds__(kCThreads, 3) void fused_filter_kernel(FusedArgs a,
   // tau of this wave's row first: it needs only the samples and the window,
   // and runs while the plan's loads are in flight
   const float tv = wave < G ? ctau(a, sv, lo, hi) : kNegInf;
-  if (tid * 16 < (int)sizeof(CellPlan)) reinterpret_cast<PlanWord*>(&P)[tid] = pw;
+#pragma unroll
+  for (int i = 0; i < kPlanSteps; ++i)
+    if (tid + kCThreads * i < kPlanWords) reinterpret_cast<PlanWord*>(&P)[tid + kCThreads * i] = pw[i];
   __syncthreads();
   if (!P.ok || P.C > CGeo<NS>::C) return;  // more cells than the caller's bound allowed: the exact path
   CGroups gs;  // wave-uniform (read from memory, so held in scalar registers only through readfirstlane)
@@ -841,10 +888,14 @@ void launch_filter(const FusedArgs& fa, int U, int max_cells, hipStream_t s) {
   const dim3 grid((unsigned)(W * U));
   // 16-byte aligned scale rows: one 16-byte scale load per lane and group
   const bool vec = (fa.nb_cap & 7) == 0 && (reinterpret_cast<uintptr_t>(fa.scales) & 15) == 0;
-  // three slices when no unit can have more than 48 cells
+  // three slices when no unit can have more than 48 cells, five when units
+  // of up to 80 cells take the filter (fa.ccap), else four
   if (max_cells > 0 && max_cells <= CGeo<3>::C) {
     if (vec) hipLaunchKernelGGL((fused_filter_kernel<true, 3>), grid, dim3(kCThreads), 0, s, fa, U, (int)W);
     else hipLaunchKernelGGL((fused_filter_kernel<false, 3>), grid, dim3(kCThreads), 0, s, fa, U, (int)W);
+  } else if (fa.ccap > CGeo<4>::C) {
+    if (vec) hipLaunchKernelGGL((fused_filter_kernel<true, 5>), grid, dim3(kCThreads), 0, s, fa, U, (int)W);
+    else hipLaunchKernelGGL((fused_filter_kernel<false, 5>), grid, dim3(kCThreads), 0, s, fa, U, (int)W);
   } else {
     if (vec) hipLaunchKernelGGL((fused_filter_kernel<true, 4>), grid, dim3(kCThreads), 0, s, fa, U, (int)W);
     else hipLaunchKernelGGL((fused_filter_kernel<false, 4>), grid, dim3(kCThreads), 0, s, fa, U, (int)W);

@@ -20,9 +20,9 @@
 // A key is a candidate for head h iff proxy + E >= tau_h, i.e.
 //   S >= thr = floor((floor((tau - E) 16 / delta) - 1 + b) / 2).
 //
-// That proxy is the wide full pass below (units of more than 48 active
-// channels or 16 row groups); the cell filter (filter.hip) serves the others
-// with a per-cell proxy.
+// That proxy is the wide full pass below (units of more than 64 active
+// channels or more cells than the launched cell filter stages); the cell
+// filter (filter.hip) serves the others with a per-cell proxy.
 //
 // Mapping to CDNA4.  A wave handles 4 blocks ("quad", 256 keys) at a time.
 // Lane l owns octet m = (l >> 1) & 7, half hb = l & 1 of block l >> 4, i.e.
@@ -710,12 +710,12 @@ __device__ __forceinline__ uint32_t unit_class(const FusedArgs& a, const int (&s
                                                int64_t hi) {
   const int A = sc[1] + sc[2] + sc[3] + sc[4];
   if (!(a.G <= 4 && A > 0 && hi - lo > a.ws.cap)) return 0u;
-  uint32_t cls = (uint32_t)((A + 15) >> 4);
-  // the cell filter stages at most 4 kOneRows cells (one per active channel
-  // and plane)
+  // the launched cell filter takes at most kCA channels and a.ccap cells (one
+  // per active channel and plane)
   const int cells = sc[1] + 2 * sc[2] + 3 * sc[3] + 4 * sc[4];
-  if (cls <= (uint32_t)kNarrow) cls = (cells <= 4 * kOneRows && a.nb_cap < kOneNbMax) ? 1u : (uint32_t)(kNarrow + 1);
-  return cls;
+  if (A <= kCA && cells <= a.ccap && a.nb_cap < kOneNbMax) return 1u;
+  const uint32_t cls = (uint32_t)((A + 15) >> 4);
+  return cls <= (uint32_t)kNarrow ? (uint32_t)(kNarrow + 1) : cls;
 }
 
 // The per-call state of unit u's rows, set by the sample pass's workgroup 0
@@ -808,8 +808,12 @@ __global__ __launch_bounds__(kFT) void fused_sample_kernel(FusedArgs a) {
 #pragma unroll
     for (int h = 0; h < 4; ++h) pre.q[h] = qv[h];
     cell_plan(P, a, pre);
-    if (tid * 16 < (int)sizeof(CellPlan))
-      gstore(reinterpret_cast<PlanWord*>(a.ws.plan + (size_t)u * kPlanBytes) + tid, reinterpret_cast<const PlanWord*>(&P)[tid]);
+#pragma unroll
+    for (int i = 0; i < kPlanSteps; ++i) {
+      const int w = tid + kFT * i;
+      if (w < kPlanWords)
+        gstore(reinterpret_cast<PlanWord*>(a.ws.plan + (size_t)u * kPlanBytes) + w, reinterpret_cast<const PlanWord*>(&P)[w]);
+    }
   }
   if (hi - lo <= a.ws.cap) return;  // computed directly by the exact pass
   // the active channels in ascending order
@@ -1849,6 +1853,7 @@ fathom_status launch_scan_topk_fused(const uint64_t* planes, const uint16_t* sca
   fa.k = k;
   fa.ws = fused_carve(ws, U * G, U, nb_cap, k);
   fa.st = st;
+  fa.ccap = max_unit_bits > 64 && max_unit_bits <= 80 ? 80 : 64;
   const int R = U * G;
   const bool f16 = qdt == FATHOM_F16;
   // a unit with at most 48 depth bits has A <= 48 channels and at most

@@ -21,7 +21,7 @@ constexpr int kSmpW = 8;           // sample proxies kept per (sampled wave, hea
 constexpr int kSampleQuads = 64;   // at most this many sampled quads per unit
 constexpr int kSmpRow = kSampleQuads * kSmpW;
 constexpr int kCntStride = 64;     // survivor counters one 256-byte line apart (device-scope atomics)
-constexpr size_t kPlanBytes = 4096;  // workspace slot of a unit's cell plan
+constexpr size_t kPlanBytes = 8192;  // workspace slot of a unit's cell plan
 constexpr int kPools = 4;          // cell filter: group pools per unit (one per wave of a workgroup)
 constexpr int kPoolStride = 32;    // pool counters one 128-byte line apart
 constexpr int kSelCap = 16384;     // rows with at most this many eligible keys are computed exactly
@@ -30,8 +30,7 @@ constexpr int kNoBound = 1 << 30;  // accumulator start: always (+) or never (-)
 constexpr int kMainWavesTarget = 2048;  // full-pass waves in flight over all units
 constexpr int kBackfillUnits = 64;      // from this many units per launch ...
 constexpr int kBackfillQpw = 16;        // ... at most this many quads per full-pass wave
-constexpr int kNarrow = 3;         // a unit of at most this many 16-channel slices (A <= 48) may take the cell filter
-constexpr int kOneRows = 16;       // cell filter: row groups at most (all staged in one 64-lane pass)
+constexpr int kNarrow = 3;         // wide-pass classes lie above this; a unit of at most 16 kNarrow = 48 depth bits always takes the cell filter
 constexpr int64_t kOneNbMax = ((int64_t)1 << 20) - 4096;  // cell filter: byte offsets within a unit's planes (and past them) fit 32 bits
 constexpr float kNegInf = -__builtin_huge_valf();
 
@@ -149,6 +148,7 @@ struct FusedArgs {
   int k;
   FusedWs ws;
   uint32_t* st;
+  int ccap;  // cells at most of a unit the cell filter takes (64, or 80 when the call's units have 65 to 80 bits)
 };
 
 __device__ __forceinline__ uint64_t lanemask_lt(int lane) { return lane == 0 ? 0ull : (~0ull >> (64 - lane)); }

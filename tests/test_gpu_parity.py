@@ -806,6 +806,53 @@ def test_scan_topk_heads_and_query_dtypes(G, qdt):
         _assert_rows_match(idx, val, planes, scales, ns, q, d, k, lo, tail)
 
 
+def _depth_row(spec, rng):
+    """A depth row with spec = {depth: channel count} on channels spread over
+    the 128 at random."""
+    d = np.zeros(128, np.uint8)
+    ch = rng.permutation(128)
+    i = 0
+    for t, c in spec.items():
+        d[ch[i:i + c]] = t
+        i += c
+    return d
+
+
+@pytest.mark.parametrize("G,qdt", [(4, np.float16), (3, np.float32), (1, np.float32)])
+def test_scan_topk_65_to_80_cells(G, qdt):
+    """Units of 65 to 80 depth bits and at most 48 channels take the cell
+    filter at five slices when the caller bounds the bits by 80: 20 channels at
+    4 planes (80 cells), 48 channels (32 at one plane, 16 at three), 65 cells
+    (17 row groups, a ragged last one), 64 channels (48 at one plane, 16 at
+    two), 70 one-plane channels beside them (more than 64 channels: the wide
+    pass in the same call), water-filling at 80 bits and a one-token unit;
+    ragged lengths, a window with lo and tail, k = 1 and 300.  The same call without a bound (units above 64 cells in the wide pass)
+    must give the same outputs; both against the oracle."""
+    ns = [70000, 23456, 40001, 30000, 50000, 1, 20000]
+    K, nt, planes, scales = _store(ns, 171 + G)
+    rng = np.random.default_rng(172 + G)
+    U = len(ns)
+    q = rng.standard_normal((U, G, 128)).astype(qdt)
+    qt = torch.from_numpy(q).to(DEV)
+    var = torch.from_numpy(np.exp(2 * rng.standard_normal((U, 128))).astype(np.float32)).to(DEV)
+    d, _ = F.fathom_alloc_depths(qt, var, F.FATHOM_WATERFILL, 80)
+    dn = d.cpu().numpy()
+    specs = {0: {4: 20}, 1: {1: 32, 3: 16}, 2: {4: 13, 1: 13}, 3: {1: 70}, 4: {1: 48, 2: 16}, 5: {4: 16, 2: 8}}
+    for u, spec in specs.items():
+        dn[u] = _depth_row(spec, rng)
+    assert [int(np.minimum(dn[u], 4).sum()) for u in specs] == [80, 80, 65, 70, 80, 80]
+    assert np.minimum(dn, 4).astype(int).sum(axis=1).max() <= 80
+    d = torch.from_numpy(dn).to(DEV)
+    for k, lo, tail in [(300, 0, 0), (300, 4, 32), (1, 0, 0)]:
+        for bound in [80, 0]:
+            st = F.new_status()
+            idx, val = F.fathom_scan_topk(planes, scales, nt, qt, d, k, lo, tail, dev_status=st,
+                                          max_unit_bits=bound)
+            s = status(st)  # the one-token unit's rows are short for k > 1
+            assert s & ~(F.FATHOM_DEV_TOPK_SHORT | F.FATHOM_DEV_TOPK_FALLBACK) == 0, (bound, hex(s))
+            _assert_rows_match(idx, val, planes, scales, ns, q, d, k, lo, tail)
+
+
 @pytest.mark.parametrize("G,qdt", [(1, np.float32), (4, np.float16)])
 def test_scan_topk_uniform_depth_mode(G, qdt):
     """Sec. 2 (SparQ grouped rule) through the fused scan + top-k: r channels at
