@@ -219,11 +219,11 @@ size_t fathom_scan_topk_workspace_size(int U, int G, int64_t max_n, int k);
  * fathom_scan_topk_ex -- fathom_scan_topk with a caller's bound on the depth
  * bits of every unit, max_unit_bits >= sum_j min(depths[u][j], 4) for all u
  * (0: no bound).  The outputs are those of fathom_scan_topk for any bound;
- * the bound only selects work: with max_unit_bits <= 48 the filter pass for
- * units of more channels or row groups is not launched, so a unit that
- * exceeds a wrong bound is recomputed by the exact path (TOPK_FALLBACK);
- * with 64 < max_unit_bits <= 80 the cell filter also takes units of 65 to 80
- * bits (at most 64 channels), which otherwise take the wider filter pass.
+ * the bound only selects work: with max_unit_bits <= 80 the filter pass for
+ * units of more bits is not launched, so a unit that exceeds a wrong bound is
+ * recomputed by the exact path (TOPK_FALLBACK); with 64 < max_unit_bits <= 80
+ * the filter is instantiated for units of up to 80 bits, which otherwise take
+ * the wider filter pass.
  * Water-filling at budget B (Sec. 3.3) gives every unit at most B bits.
  * Errors: as fathom_scan_topk; max_unit_bits < 0 is FATHOM_ERR_INVALID.
  */

@@ -13,7 +13,7 @@ namespace fathom {
 
 constexpr int kCG = 20;          // row groups at most (5 slices of 4)
 constexpr int kCC = 4 * kCG;     // cells at most
-constexpr int kCA = 64;          // active channels at most (one lane each for the scales)
+constexpr int kCA = 80;          // active channels at most
 
 struct alignas(16) CellPlan {
   int A, rg, C, ok;        // active channels, row groups, cells, the unit fits this pass
@@ -21,14 +21,14 @@ struct alignas(16) CellPlan {
   int base[5];             // first cell of plane p (base[4] = C)
   double Kc, Kch, Eabs;    // E = unit Kc + delta Kch + Eabs (unit: delta, or delta / 128 for fine weights)
   uint32_t rrow[kCG][2];   // row group g: plane rows 4 j + p of its 4 cells (16-bit halves, kCPad: none)
-  float qrg[kCG][4][4];    // row group g, head h, cell k: -q 2^-p of the cell (0 past the cells and for heads >= G)
-  int cx[kCC];             // cell -> proxy index of its channel (0 past the cells)
-  float qx[kCA][4];        // q by proxy index and head (delta)
-  int pj[kCA];             // proxy index -> channel
-  int px[kCA];             // ascending position y -> proxy index x (padded to a multiple of 8: x = A)
-  float qa[kCA][4];        // q by ascending position and head (re-scoring; 0 on padding)
-  float zo[kCA];           // -(1 - 2^-t) by ascending position: khat = (u / 8 + zo) a16, exact (0 on padding)
+  alignas(16) float qrg[kCG][4][4];  // row group g, head h, cell k: -q 2^-p of the cell (0 past the cells and for heads >= G)
+  alignas(16) int px[kCA];           // ascending position y -> proxy index x (padded to a multiple of 8: x = A)
+  alignas(16) float qa[kCA][4];      // q by ascending position and head (re-scoring; 0 on padding)
+  alignas(16) float zo[kCA];         // -(1 - 2^-t) by ascending position: khat = (u / 8 + zo) a16, exact (0 on padding)
   float tau[4];
+  uint8_t cx[kCC];         // cell -> proxy index of its channel (0 past the cells)
+  uint8_t pj[kCA];         // proxy index -> channel
+  uint8_t py[kCA];         // proxy index -> ascending position (q of proxy x: qa[py[x]])
 };
 constexpr uint32_t kCPad = 0xFFFFu;
 
@@ -119,14 +119,13 @@ __device__ __forceinline__ void cell_plan(CellPlan& P, const FusedArgs& a, const
   if (tid < kD && t > 0) {
     xp = first[t] + (wave == 1 ? cnt[0][t] : 0) + __popcll(bal[t] & lanemask_lt(lane));
     sact[xp] = tid | (t << 8);
-#pragma unroll
-    for (int h = 0; h < 4; ++h) P.qx[xp][h] = pre.q[h];
-    P.pj[xp] = tid;
+    P.pj[xp] = (uint8_t)tid;
     // ascending position: active channels below this one
     const uint64_t on = bal[1] | bal[2] | bal[3] | bal[4];
     int y = __popcll(on & lanemask_lt(lane));
     if (wave == 1) y += cnt[0][1] + cnt[0][2] + cnt[0][3] + cnt[0][4];
     P.px[y] = xp;
+    P.py[xp] = (uint8_t)y;
     P.zo[y] = -(1.0f - ldexpf(1.0f, -t));
 #pragma unroll
     for (int h = 0; h < 4; ++h) P.qa[y][h] = pre.q[h];
@@ -155,8 +154,8 @@ __device__ __forceinline__ void cell_plan(CellPlan& P, const FusedArgs& a, const
     const uint32_t other = __shfl_xor(part, 1, kWave);
     if ((k & 1) == 0) P.rrow[g][k >> 1] = part | other;
 #pragma unroll
-    for (int h = 0; h < 4; ++h) P.qrg[g][h][k] = real && h < G ? -ldexpf(P.qx[x][h], -p) : 0.0f;
-    P.cx[c] = x;
+    for (int h = 0; h < 4; ++h) P.qrg[g][h][k] = real && h < G ? -ldexpf(P.qa[P.py[x]][h], -p) : 0.0f;
+    P.cx[c] = (uint8_t)x;
   }
   if (tid < 4) P.tau[tid] = kNegInf;
   __syncthreads();

@@ -1,6 +1,6 @@
-// Full pass of fathom_scan_topk for units of at most 64 active channels and
-// 80 cells (every unit under water-filling at up to 48 code bits, units of
-// up to 64 channels at up to 80 bits, and uniform depth at r <= 16): an int8
+// Full pass of fathom_scan_topk for units of at most 80 cells (one per
+// active channel and plane: every unit of at most 80 depth bits, so every
+// unit under water-filling at B <= 80 and uniform depth at r <= 16): an int8
 // MFMA proxy of every key's four head
 // scores over its plane bits, exact re-scoring of the keys the proxy's bound
 // cannot exclude, and the appends of keys with exact score >= tau to their
@@ -111,21 +111,26 @@ __device__ __forceinline__ uint64_t lanes_below(int lane) { return lane == 0 ? 0
 
 // ---------------------------------------------------------------- scales
 // Lane c (< C) holds the 8 scales of cell c's channel (scale row jrow) for the
-// group at block sb0, two blocks a dword, read through a buffer descriptor
-// over the unit's scale rows (zero past them, and for lanes >= C; the lanes of
-// one channel's cells read the same bytes).  With 16-byte aligned rows
+// group at block sb0, two blocks a dword, and at NS = 5 lane l also those of
+// cell 64 + l (row jrow2), read through a buffer descriptor over the unit's
+// scale rows (zero past them, and for cells >= C; the lanes of one channel's
+// cells read the same bytes).  With 16-byte aligned rows
 // (nb_cap a multiple of 8) one 16-byte load per lane; blocks past nb_cap then
 // read the next row's scales, which only the (ineligible) keys of those
 // blocks and delta see.  Otherwise 8 two-byte loads, each past the range
 // beyond nb_cap.  An invalid load (no group of the wave there) reads past the
 // range: it is issued, so wait counts stay exact, but fetches nothing.
+template <int NS>
 struct CScl {
+  static constexpr bool Two = CGeo<NS>::C > kWave;  // a second cell per lane
   uint32_t v[kCSB / 2];
+  uint32_t v2[Two ? kCSB / 2 : 1];
 };
 typedef unsigned short u16x1;
 
-template <bool VEC>
-__device__ __forceinline__ void cscl_issue(CScl& r, const FusedArgs& a, int u, int nc, int jrow, int sb0, bool valid) {
+template <bool VEC, int NS>
+__device__ __forceinline__ void cscl_issue(CScl<NS>& r, const FusedArgs& a, int u, int nc, int jrow, int jrow2, int sb0,
+                                           bool valid) {
   const int lane = threadIdx.x & 63;
   const uint64_t base = reinterpret_cast<uint64_t>(a.scales + (int64_t)u * kD * a.nb_cap);
   const uint32_t alo = (uint32_t)cuni((int)(uint32_t)base), ahi = (uint32_t)cuni((int)(uint32_t)(base >> 32));
@@ -133,9 +138,15 @@ __device__ __forceinline__ void cscl_issue(CScl& r, const FusedArgs& a, int u, i
   const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
       reinterpret_cast<void*>(((uint64_t)ahi << 32) | alo), (short)0, (int)bytes, kRawBufferFlags);
   const uint32_t off = lane < nc && valid ? ((uint32_t)jrow * (uint32_t)a.nb_cap + (uint32_t)sb0) * 2u : kPastRange;
+  const uint32_t off2 =
+      lane + kWave < nc && valid ? ((uint32_t)jrow2 * (uint32_t)a.nb_cap + (uint32_t)sb0) * 2u : kPastRange;
   if constexpr (VEC) {
     const v4u x0 = __builtin_amdgcn_raw_buffer_load_b128(rs, (int)off, 0, 0);
     r.v[0] = x0.x; r.v[1] = x0.y; r.v[2] = x0.z; r.v[3] = x0.w;
+    if constexpr (CScl<NS>::Two) {
+      const v4u x1 = __builtin_amdgcn_raw_buffer_load_b128(rs, (int)off2, 0, 0);
+      r.v2[0] = x1.x; r.v2[1] = x1.y; r.v2[2] = x1.z; r.v2[3] = x1.w;
+    }
   } else {
     const int64_t left = a.nb_cap - (int64_t)sb0;  // blocks of the group inside the row
     uint32_t h[kCSB];
@@ -144,6 +155,13 @@ __device__ __forceinline__ void cscl_issue(CScl& r, const FusedArgs& a, int u, i
       h[b] = __builtin_amdgcn_raw_buffer_load_b16(rs, (int)(b < left && valid ? off + 2u * b : kPastRange), 0, 0);
 #pragma unroll
     for (int i = 0; i < kCSB / 2; ++i) r.v[i] = (h[2 * i] & 0xFFFFu) | (h[2 * i + 1] << 16);
+    if constexpr (CScl<NS>::Two) {
+#pragma unroll
+      for (int b = 0; b < kCSB; ++b)
+        h[b] = __builtin_amdgcn_raw_buffer_load_b16(rs, (int)(b < left && valid ? off2 + 2u * b : kPastRange), 0, 0);
+#pragma unroll
+      for (int i = 0; i < kCSB / 2; ++i) r.v2[i] = (h[2 * i] & 0xFFFFu) | (h[2 * i + 1] << 16);
+    }
   }
 }
 
@@ -156,36 +174,49 @@ struct CDel {
 // Writes the group's scales to ring slot `slot` (cell order: cell c holds
 // its channel's scale, so the plane-0 cell of proxy channel x is cell x) and
 // returns delta of head `hq` (every lane: its own head for the weights).  qv:
-// q of cell `lane`'s channel for the four heads (0 past the cells).  Cells
-// past 64 (NS = 5) copy the scale of their channel's plane-0 cell x2 (lane
-// l < 16 for cell 64 + l; every active channel lies below kCA = 64).
-template <int NS>
-__device__ __forceinline__ CDel cscl_commit(const CScl& r, FilterLds<NS>& L, int slot, int hq, const float (&qv)[4],
-                                            int x2) {
-  const int lane = threadIdx.x & 63;
+// q of cell `lane`'s channel for the four heads (0 past the cells), qv2 that
+// of cell 64 + lane (NS = 5).
+__device__ __forceinline__ uint32_t cscl_absmax(const uint32_t (&v)[kCSB / 2]) {
   uint32_t mx = 0u;
+#pragma unroll
+  for (int i = 0; i < kCSB / 2; ++i) {
+    const uint32_t w = v[i] & 0x7FFF7FFFu;
+    const uint32_t m = (w & 0xFFFFu) > (w >> 16) ? (w & 0xFFFFu) : (w >> 16);
+    mx = m > mx ? m : mx;
+  }
+  return mx;
+}
+template <int NS>
+__device__ __forceinline__ CDel cscl_commit(const CScl<NS>& r, FilterLds<NS>& L, int slot, int hq, const float (&qv)[4],
+                                            const float (&qv2)[4]) {
+  const int lane = threadIdx.x & 63;
   if (lane < CGeo<NS>::C) {
 #pragma unroll
     for (int b = 0; b < kCSB; ++b) L.scl[slot][b][lane] = (uint16_t)((r.v[b >> 1] >> (16 * (b & 1))) & 0xFFFFu);
   }
-  if constexpr (CGeo<NS>::C > kWave) {
-    lds_order();  // the wave's LDS accesses run in order: the reads see the writes above
+  const uint32_t mx = cscl_absmax(r.v);
+  uint32_t mx2 = 0u;
+  if constexpr (CScl<NS>::Two) {
     if (lane < CGeo<NS>::C - kWave) {
 #pragma unroll
-      for (int b = 0; b < kCSB; ++b) L.scl[slot][b][kWave + lane] = L.scl[slot][b][x2];
+      for (int b = 0; b < kCSB; ++b)
+        L.scl[slot][b][kWave + lane] = (uint16_t)((r.v2[b >> 1] >> (16 * (b & 1))) & 0xFFFFu);
     }
+    mx2 = cscl_absmax(r.v2);
   }
-#pragma unroll
-  for (int i = 0; i < kCSB / 2; ++i) {
-    const uint32_t v = r.v[i] & 0x7FFF7FFFu;
-    const uint32_t m = (v & 0xFFFFu) > (v >> 16) ? (v & 0xFFFFu) : (v >> 16);
-    mx = m > mx ? m : mx;
-  }
-  const bool nf = __ballot(mx >= 0x7C00u) != 0ull;
+  const bool nf = __ballot(mx >= 0x7C00u || mx2 >= 0x7C00u) != 0ull;
   const float am = half_bits_to_float((uint16_t)(mx >= 0x7C00u ? 0u : mx));
   uint32_t M[4];
 #pragma unroll
   for (int h = 0; h < 4; ++h) M[h] = __float_as_uint(__fmul_rn(fabsf(qv[h]), am));
+  if constexpr (CScl<NS>::Two) {
+    const float am2 = half_bits_to_float((uint16_t)(mx2 >= 0x7C00u ? 0u : mx2));
+#pragma unroll
+    for (int h = 0; h < 4; ++h) {
+      const uint32_t m2 = __float_as_uint(__fmul_rn(fabsf(qv2[h]), am2));
+      M[h] = m2 > M[h] ? m2 : M[h];
+    }
+  }
   wave_max4_u(M);
   const float Mh = __uint_as_float(hq == 0 ? M[0] : hq == 1 ? M[1] : hq == 2 ? M[2] : M[3]);
   CDel d;
@@ -531,8 +562,12 @@ __device__ __forceinline__ void cwave_run(const CellPlan& P, FilterLds<NS>& L, c
   const bool top = (lane & 3) == 3;  // as a weight lane: its second start is position 7
   const int C = cuni(P.C);
   const int cxl = P.cx[lane];                  // cell `lane`'s channel (proxy index)
-  const int cx2 = Geo::C > kWave ? P.cx[kWave + (lane & 15)] : 0;  // cell 64 + (lane & 15)'s (NS = 5)
   const int srow = lane < C ? P.pj[cxl] : 0;   // its scale row
+  const int yl = P.py[cxl];                    // its ascending position (q: qa[yl])
+  // cell 64 + lane's channel: scale row and ascending position (NS = 5)
+  const int cx2 = Geo::C > kWave && lane + kWave < C ? P.cx[kWave + lane] : 0;
+  const int srow2 = Geo::C > kWave && lane + kWave < C ? P.pj[cx2] : 0;
+  const int y2 = P.py[cx2];
   // as a transpose source: cell (l & 15) >> 1 of pair 0, block l >> 4
   const uint32_t src_off = (uint32_t)((((lane & 15) >> 1) * 4 + bq) * 8);
   // the A operand: this lane's weights, or zeros
@@ -549,8 +584,8 @@ __device__ __forceinline__ void cwave_run(const CellPlan& P, FilterLds<NS>& L, c
   int svn[4] = {0, 0, 0, 0};  // buffered survivors per head
   // the issue order here (scales, quad 0, quad 1) is the loop's steady-state
   // order, so the compiler's load counters agree on every path into the loop
-  CScl sr;
-  cscl_issue<VEC>(sr, a, u, C, srow, b0, any);
+  CScl<NS> sr;
+  cscl_issue<VEC, NS>(sr, a, u, C, srow, srow2, b0, any);
   sched_fence();
   CRaw<NS> R0, R1;
   cstage_issue(R0, S, b0, any);
@@ -701,13 +736,19 @@ __device__ __forceinline__ void cwave_run(const CellPlan& P, FilterLds<NS>& L, c
     {
       float qv[4];  // q of cell `lane`'s channel (read here: fewer registers live across the loop)
       {
-        const float4 q4 = *reinterpret_cast<const float4*>(&P.qx[cxl][0]);
+        const float4 q4 = *reinterpret_cast<const float4*>(&P.qa[yl][0]);
         const bool on = lane < C;
         qv[0] = on ? q4.x : 0.0f; qv[1] = on ? q4.y : 0.0f; qv[2] = on ? q4.z : 0.0f; qv[3] = on ? q4.w : 0.0f;
       }
-      const CDel dl = cscl_commit(sr, L, slot, hq, qv, cx2);
+      float qv2[4] = {0.0f, 0.0f, 0.0f, 0.0f};  // cell 64 + lane's (NS = 5)
+      if constexpr (Geo::C > kWave) {
+        const float4 q4 = *reinterpret_cast<const float4*>(&P.qa[y2][0]);
+        const bool on = lane + kWave < C;
+        qv2[0] = on ? q4.x : 0.0f; qv2[1] = on ? q4.y : 0.0f; qv2[2] = on ? q4.z : 0.0f; qv2[3] = on ? q4.w : 0.0f;
+      }
+      const CDel dl = cscl_commit(sr, L, slot, hq, qv, qv2);
       sched_fence();
-      cscl_issue<VEC>(sr, a, u, C, srow, gnxt * kCSB, gnxt >= 0);
+      cscl_issue<VEC, NS>(sr, a, u, C, srow, srow2, gnxt * kCSB, gnxt >= 0);
       sched_fence();
       const float th = P.tau[hq];
       H.M0 = ldexpf(12582912.0f, dl.e);  // 1.5 * 2^(23 + e)
@@ -807,8 +848,12 @@ __device__ __forceinline__ float ctau(const FusedArgs& a, const float (&sv)[kCTa
 // pool.  With fewer than 2 static groups per wave every group is static.
 // Units of another class (uovf[u] >> 1 != 1: the wide pass, or no filter) and
 // rows computed exactly return at once.
+// Three workgroups per CU: LDS is handed out in 1280-byte units, so a
+// workgroup may hold at most 42 of them (a 53,984-byte build ran two per CU).
+constexpr size_t kCLdsMax = 42 * 1280;
 template <bool VEC, int NS>
 __global__ __launch_bounds__(kCThreads, 3) void fused_filter_kernel(FusedArgs a, int U, int W) {
+  static_assert(sizeof(CellPlan) + kCWaves * sizeof(FilterLds<NS>) <= kCLdsMax, "three workgroups per CU");
   __shared__ CellPlan P;
   __shared__ FilterLds<NS> WL[kCWaves];
   const int u = (int)(blockIdx.x % (unsigned)U), x = (int)(blockIdx.x / (unsigned)U);

@@ -20,9 +20,9 @@
 // A key is a candidate for head h iff proxy + E >= tau_h, i.e.
 //   S >= thr = floor((floor((tau - E) 16 / delta) - 1 + b) / 2).
 //
-// That proxy is the wide full pass below (units of more than 64 active
-// channels or more cells than the launched cell filter stages); the cell
-// filter (filter.hip) serves the others with a per-cell proxy.
+// That proxy is the wide full pass below (units of more cells than the
+// launched cell filter stages); the cell filter (filter.hip) serves the
+// others with a per-cell proxy.
 //
 // Mapping to CDNA4.  A wave handles 4 blocks ("quad", 256 keys) at a time.
 // Lane l owns octet m = (l >> 1) & 7, half hb = l & 1 of block l >> 4, i.e.
@@ -1856,11 +1856,11 @@ fathom_status launch_scan_topk_fused(const uint64_t* planes, const uint16_t* sca
   fa.ccap = max_unit_bits > 64 && max_unit_bits <= 80 ? 80 : 64;
   const int R = U * G;
   const bool f16 = qdt == FATHOM_F16;
-  // a unit with at most 48 depth bits has A <= 48 channels and at most
-  // 4 + 48 / 4 = 16 row groups: the narrow pass takes every unit, and the
-  // wide launches are skipped.  (A unit above the caller's bound is left to the
+  // a unit with at most 80 depth bits has at most 80 cells and channels:
+  // with such a bound the cell filter takes every unit, and the wide
+  // launches are skipped.  (A unit above the caller's bound is left to the
   // exact rows of the select pass.)
-  const bool wide = !(max_unit_bits > 0 && max_unit_bits <= 16 * kNarrow && nb_cap < kOneNbMax);
+  const bool wide = !(max_unit_bits > 0 && max_unit_bits <= kCC && nb_cap < kOneNbMax);
   if (G <= 4)
     hipLaunchKernelGGL(fused_sample_kernel, dim3((unsigned)fa.ws.s_quads, (unsigned)U), dim3(kFT), 0, s, fa);
   // narrow: the cell filter finds tau itself and the sample pass sets the

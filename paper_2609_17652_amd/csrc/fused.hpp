@@ -30,7 +30,7 @@ constexpr int kNoBound = 1 << 30;  // accumulator start: always (+) or never (-)
 constexpr int kMainWavesTarget = 2048;  // full-pass waves in flight over all units
 constexpr int kBackfillUnits = 64;      // from this many units per launch ...
 constexpr int kBackfillQpw = 16;        // ... at most this many quads per full-pass wave
-constexpr int kNarrow = 3;         // wide-pass classes lie above this; a unit of at most 16 kNarrow = 48 depth bits always takes the cell filter
+constexpr int kNarrow = 3;         // wide-pass classes lie above this
 constexpr int64_t kOneNbMax = ((int64_t)1 << 20) - 4096;  // cell filter: byte offsets within a unit's planes (and past them) fit 32 bits
 constexpr float kNegInf = -__builtin_huge_valf();
 

@@ -820,15 +820,16 @@ def _depth_row(spec, rng):
 
 @pytest.mark.parametrize("G,qdt", [(4, np.float16), (3, np.float32), (1, np.float32)])
 def test_scan_topk_65_to_80_cells(G, qdt):
-    """Units of 65 to 80 depth bits and at most 48 channels take the cell
-    filter at five slices when the caller bounds the bits by 80: 20 channels at
-    4 planes (80 cells), 48 channels (32 at one plane, 16 at three), 65 cells
-    (17 row groups, a ragged last one), 64 channels (48 at one plane, 16 at
-    two), 70 one-plane channels beside them (more than 64 channels: the wide
-    pass in the same call), water-filling at 80 bits and a one-token unit;
-    ragged lengths, a window with lo and tail, k = 1 and 300.  The same call without a bound (units above 64 cells in the wide pass)
-    must give the same outputs; both against the oracle."""
-    ns = [70000, 23456, 40001, 30000, 50000, 1, 20000]
+    """Units of 65 to 80 depth bits take the cell filter at five slices when
+    the caller bounds the bits by 80: 20 channels at 4 planes (80 cells), 48
+    channels (32 at one plane, 16 at three), 65 cells (17 row groups, a ragged
+    last one), 64 channels (48 at one plane, 16 at two), 70 and 80 one-plane
+    channels (scales of channels past 64 on a second set of lanes),
+    water-filling at 80 bits and a one-token unit; ragged lengths, a window
+    with lo and tail, k = 1 and 300.  The same call without a bound (units of
+    more than 64 cells in the wide pass) must give the same outputs; both
+    against the oracle."""
+    ns = [70000, 23456, 40001, 30000, 50000, 1, 20000, 30001]
     K, nt, planes, scales = _store(ns, 171 + G)
     rng = np.random.default_rng(172 + G)
     U = len(ns)
@@ -837,10 +838,11 @@ def test_scan_topk_65_to_80_cells(G, qdt):
     var = torch.from_numpy(np.exp(2 * rng.standard_normal((U, 128))).astype(np.float32)).to(DEV)
     d, _ = F.fathom_alloc_depths(qt, var, F.FATHOM_WATERFILL, 80)
     dn = d.cpu().numpy()
-    specs = {0: {4: 20}, 1: {1: 32, 3: 16}, 2: {4: 13, 1: 13}, 3: {1: 70}, 4: {1: 48, 2: 16}, 5: {4: 16, 2: 8}}
+    specs = {0: {4: 20}, 1: {1: 32, 3: 16}, 2: {4: 13, 1: 13}, 3: {1: 70}, 4: {1: 48, 2: 16}, 5: {4: 16, 2: 8},
+             7: {1: 80}}
     for u, spec in specs.items():
         dn[u] = _depth_row(spec, rng)
-    assert [int(np.minimum(dn[u], 4).sum()) for u in specs] == [80, 80, 65, 70, 80, 80]
+    assert [int(np.minimum(dn[u], 4).sum()) for u in specs] == [80, 80, 65, 70, 80, 80, 80]
     assert np.minimum(dn, 4).astype(int).sum(axis=1).max() <= 80
     d = torch.from_numpy(dn).to(DEV)
     for k, lo, tail in [(300, 0, 0), (300, 4, 32), (1, 0, 0)]:
