@@ -57,18 +57,20 @@ constexpr int kSv = 8;           // survivors per head buffered in LDS before a 
 // number of dwords, so the lanes of a re-scoring batch fall in different
 // banks) for Slots groups; three workgroups per CU fit the LDS with 6 slots
 // at NS = 3 (a wave's 6 groups of the 2^20-token layer: no flush before its
-// end) and 3 at NS = 4 and 5, the last with a queue of 32 candidates.  A
-// lane stages K plane words per quad: 4 cells of its row group up to NS = 4,
-// at NS = 5 the cells lane / 4 + 16 k, k < 5.
+// end), 3 at NS = 4 and 2 at NS = 5, whose single-level weights over 80
+// cells leave more keys to re-score: its queue of 48 candidates (with 2
+// slots) ran 21 % faster than 32 (with 3) and 3 % faster than 64 (with 1).
+// A lane stages K plane words per quad: 4 cells of its row group up to
+// NS = 4, at NS = 5 the cells lane / 4 + 16 k, k < 5.
 template <int NS>
 struct CGeo {
   static_assert(NS >= 3 && NS <= 5, "three to five slices");
   static constexpr int G = 4 * NS;
   static constexpr int C = 4 * G;
-  static constexpr int Slots = NS == 3 ? 6 : 3;
+  static constexpr int Slots = NS == 3 ? 6 : NS == 4 ? 3 : 2;
   static constexpr int SclRow = C + 2;
   static constexpr bool Fine = NS == 3;  // two-level weights (the registers fit them at three slices)
-  static constexpr int Q = NS == 5 ? 32 : 64;  // queued candidates per wave; re-scored at a quad boundary once full
+  static constexpr int Q = NS == 5 ? 48 : 64;  // queued candidates per wave; re-scored at a quad boundary once full
   static constexpr int K = NS == 5 ? 5 : 4;    // plane words a lane stages per quad
 };
 // Fine weights W' = 128 W + W_lo count in units of delta / 128; |S'| < 2^20
