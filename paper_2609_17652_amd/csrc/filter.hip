@@ -18,8 +18,8 @@
 // (weight rounding, then the A roundings of the fp32 chain), plus A 2^-120
 // for subnormal results.  A key is a candidate for head h iff
 // S >= thr = floor((floor(2 (tau - E) / delta) - 1 + Wsum) / 2).  At three
-// slices the weights have two levels, W' = 128 W + W_lo in units of
-// delta / 128 (the bound's cell term shrinks by 128).
+// and five slices the weights have two levels, W' = 128 W + W_lo in units
+// of delta / 128 (the bound's cell term shrinks by 128).
 //
 // Layout.  Cells are ordered plane-major without padding (plane p's cells are
 // its channels, a prefix of the proxy order: depth descending, channel
@@ -57,10 +57,11 @@ constexpr int kSv = 8;           // survivors per head buffered in LDS before a 
 // number of dwords, so the lanes of a re-scoring batch fall in different
 // banks) for Slots groups; three workgroups per CU fit the LDS with 6 slots
 // at NS = 3 (a wave's 6 groups of the 2^20-token layer: no flush before its
-// end), 3 at NS = 4 and 2 at NS = 5, whose single-level weights over 80
-// cells leave more keys to re-score: its queue of 48 candidates (with 2
-// slots) ran 21 % faster than 32 (with 3) and 3 % faster than 64 (with 1).
-// A lane stages K plane words per quad: 4 cells of its row group up to
+// end), 3 at NS = 4 and 2 at NS = 5 with a queue of 32 candidates (the
+// space of the second-level weights; 24 candidates with 3 slots ran as
+// fast, 48 with 1 slot 19 % slower).  NS = 3 and 5 have two-level weights
+// (at NS = 5 the MFMA loop runs slice by slice so that one slice's two
+// weight sets are live at a time); NS = 4 keeps one level.  A lane stages K plane words per quad: 4 cells of its row group up to
 // NS = 4, at NS = 5 the cells lane / 4 + 16 k, k < 5.
 template <int NS>
 struct CGeo {
@@ -69,13 +70,13 @@ struct CGeo {
   static constexpr int C = 4 * G;
   static constexpr int Slots = NS == 3 ? 6 : NS == 4 ? 3 : 2;
   static constexpr int SclRow = C + 2;
-  static constexpr bool Fine = NS == 3;  // two-level weights (the registers fit them at three slices)
-  static constexpr int Q = NS == 5 ? 48 : 64;  // queued candidates per wave; re-scored at a quad boundary once full
+  static constexpr bool Fine = NS != 4;  // two-level weights (slice-outer at five slices, so the registers fit them)
+  static constexpr int Q = NS == 5 ? 32 : 64;  // queued candidates per wave; re-scored at a quad boundary once full
   static constexpr int K = NS == 5 ? 5 : 4;    // plane words a lane stages per quad
 };
-// Fine weights W' = 128 W + W_lo count in units of delta / 128; |S'| < 2^20
-// for 48 cells, so thresholds are clamped to +-2^21 and an accumulator stays
-// below 2^29.
+// Fine weights W' = 128 W + W_lo count in units of delta / 128; |W'| <=
+// 127 * 128 + 64, so |S'| < 2^21 for up to 80 cells: thresholds are clamped
+// to +-2^21 and an accumulator stays below 2^29.
 constexpr int kCThrMax = 1 << 21;
 constexpr int kCWaves = 4;       // waves per workgroup
 constexpr int kCThreads = kCWaves * kWave;
@@ -566,10 +567,9 @@ __device__ __forceinline__ void cwave_run(const CellPlan& P, FilterLds<NS>& L, c
   const int cxl = P.cx[lane];                  // cell `lane`'s channel (proxy index)
   const int srow = lane < C ? P.pj[cxl] : 0;   // its scale row
   const int yl = P.py[cxl];                    // its ascending position (q: qa[yl])
-  // cell 64 + lane's channel: scale row and ascending position (NS = 5)
-  const int cx2 = Geo::C > kWave && lane + kWave < C ? P.cx[kWave + lane] : 0;
-  const int srow2 = Geo::C > kWave && lane + kWave < C ? P.pj[cx2] : 0;
-  const int y2 = P.py[cx2];
+  // cell 64 + lane's channel (NS = 5; read from the plan where needed, so
+  // that no register holds it across the loop)
+  auto cell2 = [&]() -> int { return Geo::C > kWave && lane + kWave < C ? P.cx[kWave + lane] : 0; };
   // as a transpose source: cell (l & 15) >> 1 of pair 0, block l >> 4
   const uint32_t src_off = (uint32_t)((((lane & 15) >> 1) * 4 + bq) * 8);
   // the A operand: this lane's weights, or zeros
@@ -587,7 +587,7 @@ __device__ __forceinline__ void cwave_run(const CellPlan& P, FilterLds<NS>& L, c
   // the issue order here (scales, quad 0, quad 1) is the loop's steady-state
   // order, so the compiler's load counters agree on every path into the loop
   CScl<NS> sr;
-  cscl_issue<VEC, NS>(sr, a, u, C, srow, srow2, b0, any);
+  cscl_issue<VEC, NS>(sr, a, u, C, srow, Geo::C > kWave ? P.pj[cell2()] : 0, b0, any);
   sched_fence();
   CRaw<NS> R0, R1;
   cstage_issue(R0, S, b0, any);
@@ -620,6 +620,27 @@ __device__ __forceinline__ void cwave_run(const CellPlan& P, FilterLds<NS>& L, c
       xr[2 * pp] = (uint32_t)v.x;
       xr[2 * pp + 1] = (uint32_t)v.y;
     }
+    if constexpr (Geo::Fine && NS == 5) {
+      // slices outer: one slice's W and W_lo live at a time, the W chain of
+      // each position kept apart and scaled by 128 into the W_lo chain
+      v4i ah[4];
+#pragma unroll
+      for (int mu = 0; mu < 4; ++mu) ah[mu] = v4i{0, 0, 0, 0};
+#pragma unroll
+      for (int s2 = 0; s2 < NS; ++s2) {
+        const v4i w = *reinterpret_cast<const v4i*>(wsrc + 4 * s2);
+        const v4i wlo = *reinterpret_cast<const v4i*>(wlsrc + 4 * s2);
+#pragma unroll
+        for (int mu = 0; mu < 4; ++mu) {
+          const v4i bv = v4i{(int)(xr[4 * s2] & mk[mu]), (int)(xr[4 * s2 + 1] & mk[mu]), (int)(xr[4 * s2 + 2] & mk[mu]),
+                             (int)(xr[4 * s2 + 3] & mk[mu])};
+          ah[mu] = __builtin_amdgcn_mfma_i32_16x16x64_i8(w, bv, ah[mu], 0, 0, 0);
+          acc[mu] = __builtin_amdgcn_mfma_i32_16x16x64_i8(wlo, bv, acc[mu], 0, 0, 0);
+        }
+      }
+#pragma unroll
+      for (int mu = 0; mu < 4; ++mu) acc[mu] = acc[mu] + ah[mu] * 128;
+    } else {
     v4i wv[NS];
 #pragma unroll
     for (int s2 = 0; s2 < NS; ++s2) wv[s2] = *reinterpret_cast<const v4i*>(wsrc + 4 * s2);
@@ -652,6 +673,7 @@ __device__ __forceinline__ void cwave_run(const CellPlan& P, FilterLds<NS>& L, c
 #pragma unroll
         for (int mu = 0; mu < 4; ++mu) acc[mu] = __builtin_amdgcn_mfma_i32_16x16x64_i8(wv[s2], bv[mu], acc[mu], 0, 0, 0);
       }
+    }
     }
     // candidates: this lane's eligible keys (all four inside the window but
     // at the unit's edges), and per key its candidate heads
@@ -743,8 +765,11 @@ __device__ __forceinline__ void cwave_run(const CellPlan& P, FilterLds<NS>& L, c
         qv[0] = on ? q4.x : 0.0f; qv[1] = on ? q4.y : 0.0f; qv[2] = on ? q4.z : 0.0f; qv[3] = on ? q4.w : 0.0f;
       }
       float qv2[4] = {0.0f, 0.0f, 0.0f, 0.0f};  // cell 64 + lane's (NS = 5)
+      int srow2 = 0;
       if constexpr (Geo::C > kWave) {
-        const float4 q4 = *reinterpret_cast<const float4*>(&P.qa[y2][0]);
+        const int x2 = cell2();
+        srow2 = P.pj[x2];
+        const float4 q4 = *reinterpret_cast<const float4*>(&P.qa[P.py[x2]][0]);
         const bool on = lane + kWave < C;
         qv2[0] = on ? q4.x : 0.0f; qv2[1] = on ? q4.y : 0.0f; qv2[2] = on ? q4.z : 0.0f; qv2[3] = on ? q4.w : 0.0f;
       }
